@@ -1,0 +1,474 @@
+"""Pins of the fp64 oracle against things other than itself: brute force on tiny
+inputs, closed forms, invariants, library routines and the paper's Figure 10
+visibility pattern.  Each group names the mistake it is there to catch."""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import attention, rope_split, rope_angles, apply_rope, chunk_positions
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def rnd(*shape, seed=0):
+    return np.random.default_rng(seed).standard_normal(shape)
+
+
+# ----------------------------------------------------------------------------- P1
+def brute_attention(q, k, v, visible, scale):
+    """Triple loop, explicit boolean mask, no vectorisation."""
+    Lq, H, Dh = q.shape
+    Lk = k.shape[0]
+    o = np.zeros((Lq, H, v.shape[2]))
+    for h in range(H):
+        for i in range(Lq):
+            scores = []
+            for j in range(Lk):
+                if visible[i][j]:
+                    s = 0.0
+                    for c in range(Dh):
+                        s += q[i, h, c] * k[j, h, c]
+                    scores.append((j, s * scale))
+            mx = max(s for _, s in scores)
+            den = sum(math.exp(s - mx) for _, s in scores)
+            for j, s in scores:
+                w = math.exp(s - mx) / den
+                for c in range(v.shape[2]):
+                    o[i, h, c] += w * v[j, h, c]
+    return o
+
+
+def test_attention_matches_brute_force_with_explicit_mask():
+    # B=1, H=2, Dh=8, three chunks of five tokens; queries from chunks 0..2
+    k_chunk = np.repeat([0, 1, 2], 5)
+    q_chunk = np.array([0, 0, 1, 1, 1, 2, 2, 0, 2])
+    q, k, v = rnd(9, 2, 8, seed=1), rnd(15, 2, 8, seed=2), rnd(15, 2, 8, seed=3)
+    visible = [[k_chunk[j] <= q_chunk[i] for j in range(15)] for i in range(9)]
+    ref = brute_attention(q, k, v, visible, 1 / math.sqrt(8))
+    got = attention(q, k, v, q_chunk, k_chunk)
+    assert np.max(np.abs(got - ref)) <= 1e-12
+
+
+def test_attention_explicit_scale_and_empty_rows():
+    q, k, v = rnd(4, 1, 8, seed=4), rnd(6, 1, 8, seed=5), rnd(6, 1, 8, seed=6)
+    vis = [[True] * 6] * 4
+    ref = brute_attention(q, k, v, vis, 0.37)
+    assert np.max(np.abs(attention(q, k, v, np.zeros(4), np.zeros(6), 0.37) - ref)) <= 1e-12
+    with pytest.raises(ValueError):
+        attention(q, k, v, np.zeros(4), np.ones(6))
+
+
+# ----------------------------------------------------------------------------- Figure 10
+def read_visibility():
+    cases = {}
+    with open(os.path.join(GOLDEN, "fig10b_chunk_visibility.txt")) as f:
+        for line in f:
+            line = line.split("#")[0].strip()
+            if not line:
+                continue
+            head, vis = line.split(":")
+            case, qc = head.split()
+            cases.setdefault(case, {})[int(qc)] = set(int(x) for x in vis.split())
+    return cases
+
+
+def test_attention_visibility_matches_figure_10():
+    cases = read_visibility()
+    n = 4
+    k_chunk = np.repeat(np.arange(n), 3)
+    k, v = rnd(12, 2, 8, seed=7), rnd(12, 2, 8, seed=8)
+    for case, table in cases.items():
+        for qc, vis in table.items():
+            q = rnd(2, 2, 8, seed=9 + qc)
+            qch = np.full(2, qc)
+            base = attention(q, k, v, qch, k_chunk)
+            for kc in range(n):
+                v2 = v.copy()
+                v2[k_chunk == kc] += 1.0
+                changed = np.max(np.abs(attention(q, k, v2, qch, k_chunk) - base)) > 1e-9
+                assert changed == (kc in vis), (case, qc, kc)
+
+
+# ----------------------------------------------------------------------------- P5, P6, P7
+def test_softmax_invariants():
+    k_chunk = np.repeat([0, 1, 2], 4)
+    q_chunk = np.array([0, 1, 2, 2])
+    q, k = rnd(4, 2, 8, seed=10), rnd(12, 2, 8, seed=11)
+    row = rnd(1, 2, 8, seed=12)
+    v_const = np.repeat(row, 12, axis=0)
+    # constant V rows -> that row
+    assert np.allclose(attention(q, k, v_const, q_chunk, k_chunk), np.repeat(row, 4, 0), atol=1e-13)
+    # q = 0 -> mean of the visible V
+    v = rnd(12, 2, 8, seed=13)
+    o = attention(np.zeros_like(q), k, v, q_chunk, k_chunk)
+    for i, c in enumerate(q_chunk):
+        assert np.allclose(o[i], v[k_chunk <= c].mean(axis=0), atol=1e-13)
+    # adding the same amount to every score of a query changes nothing: shift every
+    # key along that query's direction
+    q1 = q[:1]
+    alpha = 3.7
+    shift = alpha * q1[0] / np.sum(q1[0] ** 2, axis=-1, keepdims=True) * math.sqrt(8)
+    a = attention(q1, k, v, q_chunk[:1], k_chunk)
+    b = attention(q1, k + shift[None], v, q_chunk[:1], k_chunk)
+    assert np.allclose(a, b, atol=1e-12)
+    # one visible key -> its value
+    o1 = attention(q[:1], k[:1], v[:1], np.zeros(1), np.zeros(1))
+    assert np.allclose(o1, v[:1], atol=1e-15)
+
+
+def test_future_independence_and_permutation():
+    k_chunk = np.repeat([0, 1, 2], 5)
+    q_chunk = np.repeat([0, 1, 2], 5)
+    q, k, v = rnd(15, 2, 8, seed=14), rnd(15, 2, 8, seed=15), rnd(15, 2, 8, seed=16)
+    base = attention(q, k, v, q_chunk, k_chunk)
+    k2, v2 = k.copy(), v.copy()
+    k2[10:] = rnd(5, 2, 8, seed=17)
+    v2[10:] = rnd(5, 2, 8, seed=18)
+    o2 = attention(q, k2, v2, q_chunk, k_chunk)
+    assert np.array_equal(o2[:10], base[:10])
+    # permuting tokens inside chunk 1 (queries and keys alike) permutes the outputs
+    perm = np.arange(15)
+    perm[5:10] = [8, 5, 9, 7, 6]
+    o3 = attention(q[perm], k[perm], v[perm], q_chunk, k_chunk)
+    assert np.allclose(o3, base[perm], atol=1e-13)
+
+
+# ----------------------------------------------------------------------------- KV-cache equivalence (P4)
+def test_attention_kv_cache_equivalence():
+    sizes = [4, 6, 5]
+    k_chunk = np.repeat(np.arange(3), sizes)
+    q, k, v = rnd(15, 3, 16, seed=20), rnd(15, 3, 16, seed=21), rnd(15, 3, 16, seed=22)
+    full = attention(q, k, v, k_chunk, k_chunk)
+    off = np.concatenate([[0], np.cumsum(sizes)])
+    for c in range(3):
+        rows = slice(off[c], off[c + 1])
+        cached = attention(q[rows], k[:off[c + 1]], v[:off[c + 1]],
+                           np.full(sizes[c], c), k_chunk[:off[c + 1]])
+        assert np.allclose(cached, full[rows], atol=1e-13)
+
+
+# ----------------------------------------------------------------------------- RoPE (P2)
+def test_rope_split_matches_44_42_42():
+    assert rope_split(128) == (44, 42, 42)
+    assert sum(rope_split(64)) == 64 and all(s % 2 == 0 for s in rope_split(64))
+
+
+def test_rope_rotation_properties():
+    Dh = 128
+    x = rnd(7, 3, Dh, seed=30)
+    pos = np.array([[0, 0, 0], [1, 2, 3], [5, 29, 51], [9, 0, 0], [3, 7, 155], [2, 2, 2], [33, 1, 0]])
+    y = apply_rope(x, pos)
+    # norm preserved per head vector, and per rotated pair
+    assert np.allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(x, axis=-1), atol=1e-12)
+    assert np.allclose(y[..., 0::2] ** 2 + y[..., 1::2] ** 2, x[..., 0::2] ** 2 + x[..., 1::2] ** 2)
+    # R(0) = I
+    assert np.array_equal(y[0], x[0])
+    # each axis only moves its own segment: 44 dims for t, 42 for h, 42 for w
+    seg = np.cumsum([0] + list(rope_split(Dh)))
+    for axis in range(3):
+        p = np.zeros((1, 3), int)
+        p[0, axis] = 5
+        z = apply_rope(x[:1], p)
+        moved = np.any(np.abs(z - x[:1]) > 0, axis=(0, 1))
+        assert moved[seg[axis]:seg[axis + 1]].all()
+        assert not moved[:seg[axis]].any() and not moved[seg[axis + 1]:].any()
+
+
+def test_rope_angles_first_pair_and_geometric_spectrum():
+    Dh = 128
+    seg = rope_split(Dh)
+    # measure the rotation of unit pairs: rotate e0 = (1, 0) in every pair
+    e = np.zeros((1, 1, Dh))
+    e[..., 0::2] = 1.0
+    for axis in range(3):
+        p = np.zeros((1, 3), int)
+        p[0, axis] = 1
+        r = apply_rope(e, p)[0, 0]
+        ang = np.arctan2(r[1::2], r[0::2])
+        start = sum(seg[:axis]) // 2
+        a = ang[start:start + seg[axis] // 2]
+        assert abs(a[0] - 1.0) < 1e-15  # first pair turns by exactly p radians
+        ratio = a[1:] / a[:-1]  # geometric with ratio 10000^(-2/D_a)
+        assert np.allclose(ratio, 10000.0 ** (-2.0 / seg[axis]), rtol=1e-12)
+        assert a[-1] > 1e-4 and a[-1] < 1.0
+
+
+def test_rope_relative_position_invariance():
+    Dh = 64
+    qv, kv = rnd(1, 2, Dh, seed=31), rnd(1, 2, Dh, seed=32)
+    p, pp = np.array([[3, 4, 5]]), np.array([[1, 9, 2]])
+    base = np.sum(apply_rope(qv, p) * apply_rope(kv, pp), axis=-1)
+    for s in ([7, 0, 0], [0, 11, 0], [0, 0, 13], [2, 3, 4]):
+        s = np.array([s])
+        sh = np.sum(apply_rope(qv, p + s) * apply_rope(kv, pp + s), axis=-1)
+        assert np.allclose(sh, base, atol=1e-12)
+
+
+def test_chunk_positions():
+    pos = chunk_positions(2, 2, 3, 4, 5)
+    assert pos.shape == (2 * 3 * 4 + 5, 3)
+    # video tokens run frame-major, then row, then column, frames 2c .. 2c+1
+    assert pos[0].tolist() == [4, 0, 0] and pos[1].tolist() == [4, 0, 1]
+    assert pos[4].tolist() == [4, 1, 0] and pos[12].tolist() == [5, 0, 0]
+    assert pos[23].tolist() == [5, 2, 3]
+    # action tokens come after the chunk's last frame
+    assert pos[24:].tolist() == [[6 + j, 0, 0] for j in range(5)]
+
+
+# ----------------------------------------------------------------------------- LN, AdaLN, GELU, Linear
+def test_layernorm_moments_and_closed_form():
+    eps = 1e-6
+    x = rnd(5, 64, seed=40) * 3 + 2
+    y = oracle.layernorm(x, eps)
+    var = x.var(axis=-1)
+    assert np.allclose(y.mean(axis=-1), 0, atol=1e-13)
+    assert np.allclose(y.var(axis=-1), var / (var + eps), rtol=1e-12)
+    a = 0.3
+    assert np.allclose(oracle.layernorm(np.array([a, -a]), eps), np.array([a, -a]) / math.sqrt(a * a + eps))
+    g, b = rnd(64, seed=41), rnd(64, seed=42)
+    assert np.allclose(oracle.layernorm(x, eps, g, b), y * g + b)
+    # invariance under per-row affine change of the input (up to eps)
+    assert np.allclose(oracle.layernorm(5 * x + 7, 0.0), oracle.layernorm(x, 0.0), atol=1e-12)
+
+
+def test_adaln_zero_modulation_is_layernorm():
+    x = rnd(3, 32, seed=43)
+    z = np.zeros(32)
+    assert np.array_equal(oracle.modulate(x, z, z, 1e-6), oracle.layernorm(x, 1e-6))
+    sc, sh = rnd(32, seed=44), rnd(32, seed=45)
+    m = oracle.modulate(x, sh, sc, 1e-6)
+    assert np.allclose(oracle.layernorm(m - sh, 0.0), oracle.layernorm(oracle.layernorm(x, 1e-6) * (1 + sc), 0.0))
+
+
+def test_gelu_tanh():
+    u = np.linspace(-8, 8, 2001)
+    g = oracle.gelu_tanh(u)
+    assert oracle.gelu_tanh(np.array(0.0)) == 0.0
+    assert np.allclose(g - oracle.gelu_tanh(-u), u, atol=1e-14)
+    erf_gelu = np.array([0.5 * x * (1 + math.erf(x / math.sqrt(2))) for x in u])
+    err = np.max(np.abs(g - erf_gelu))
+    assert 1e-5 < err < 1e-3  # a close approximation of GELU, but not GELU itself
+    assert abs(oracle.gelu_tanh(np.array(30.0)) - 30.0) < 1e-12
+    assert abs(oracle.gelu_tanh(np.array(-30.0))) < 1e-12
+
+
+def test_silu():
+    u = np.linspace(-20, 20, 101)
+    ref = np.array([x / (1 + math.exp(-x)) for x in u])
+    assert np.allclose(oracle.silu(u), ref, rtol=1e-14, atol=1e-300)
+
+
+def test_linear_brute_force():
+    x, w, b = rnd(2, 3, 5, seed=46), rnd(4, 5, seed=47), rnd(4, seed=48)
+    y = oracle.linear(x, w, b)
+    for i in range(2):
+        for j in range(3):
+            for o in range(4):
+                assert abs(y[i, j, o] - (sum(x[i, j, c] * w[o, c] for c in range(5)) + b[o])) < 1e-13
+
+
+def test_timestep_sinusoid():
+    s = oracle.timestep_sinusoid(np.array([0.0, 0.3, 1.0]))
+    assert s.shape == (3, 256)
+    assert np.array_equal(s[0], np.concatenate([np.ones(128), np.zeros(128)]))
+    # cos and sin of the same frequency are paired
+    assert np.allclose(s[:, :128] ** 2 + s[:, 128:] ** 2, 1.0)
+    # measured angular frequencies are geometric from 1000 rad per unit t down by 10^4
+    t = 1e-5
+    a = np.arctan2(oracle.timestep_sinusoid(np.array([t]))[0, 128:], oracle.timestep_sinusoid(np.array([t]))[0, :128]) / t
+    assert abs(a[0] - 1000.0) < 1e-6
+    assert np.allclose(a[1:] / a[:-1], 10000.0 ** (-1 / 128), rtol=1e-9)
+
+
+# ----------------------------------------------------------------------------- patchify (P8)
+def test_patchify_roundtrip_and_layout():
+    B, C, F, Hl, Wl = 2, 3, 2, 4, 6
+    z = rnd(B, C, F, Hl, Wl, seed=50)
+    tok = oracle.patchify(z)
+    assert tok.shape == (B, F * 2 * 3, C * 4)
+    assert np.array_equal(oracle.unpatchify(tok, C, F, Hl, Wl), z)
+    # coordinate-encoded latent: decode every token feature back to its coordinates
+    c, f, y, x = np.meshgrid(np.arange(C), np.arange(F), np.arange(Hl), np.arange(Wl), indexing="ij")
+    code = (c * 1000 + f * 100 + y * 10 + x).astype(float)[None]
+    t = oracle.patchify(code)[0]
+    for ti in range(t.shape[0]):
+        fi, rem = divmod(ti, 2 * 3)
+        r, s = divmod(rem, 3)
+        for fe in range(C * 4):
+            cc, rest = divmod(fe, 4)
+            ph, pw = divmod(rest, 2)
+            assert t[ti, fe] == cc * 1000 + fi * 100 + (2 * r + ph) * 10 + (2 * s + pw)
+
+
+# ----------------------------------------------------------------------------- block-level pins
+def small_block_weights(d, F, seed, zero_gates=False):
+    g = np.random.default_rng(seed)
+    W = {
+        "w_qkv": g.standard_normal((3 * d, d)) * 0.1, "b_qkv": g.standard_normal(3 * d) * 0.1,
+        "w_o": g.standard_normal((d, d)) * 0.1, "b_o": g.standard_normal(d) * 0.1,
+        "w_cq": g.standard_normal((d, d)) * 0.1, "b_cq": g.standard_normal(d) * 0.1,
+        "w_ckv": g.standard_normal((2 * d, d)) * 0.1, "b_ckv": g.standard_normal(2 * d) * 0.1,
+        "w_co": g.standard_normal((d, d)) * 0.1, "b_co": g.standard_normal(d) * 0.1,
+        "w_f1": g.standard_normal((F, d)) * 0.1, "b_f1": g.standard_normal(F) * 0.1,
+        "w_f2": g.standard_normal((d, F)) * 0.1, "b_f2": g.standard_normal(d) * 0.1,
+        "mod6": g.standard_normal((6, d)) * 0.3,
+        "lnc_gamma": 1 + 0.1 * g.standard_normal(d), "lnc_beta": 0.1 * g.standard_normal(d),
+    }
+    return W
+
+
+def test_block_kv_cache_equivalence():
+    """Three chunks in one masked call equal three sequential cached calls, each
+    appending its post-RoPE K and V to the cache (Figure 10b, section 3.1)."""
+    d, H, Fh, B = 24, 2, 40, 2
+    Fg, Hg, Wg, A = 2, 2, 3, 2
+    W = small_block_weights(d, Fh, 60)
+    Lc = 5
+    ctx = rnd(B, Lc, d, seed=61)
+    e0 = rnd(B, 6, d, seed=62) * 0.5
+    Lch = Fg * Hg * Wg + A
+    pos = np.concatenate([chunk_positions(c, Fg, Hg, Wg, A) for c in range(3)])
+    chunk = np.repeat(np.arange(3), Lch)
+    x = rnd(B, 3 * Lch, d, seed=63)
+    full, k_full, v_full = oracle.dit_block(x, e0, W, H, 1e-6, pos, chunk, ctx=ctx)
+    kc = vc = pc = None
+    for c in range(3):
+        rows = slice(c * Lch, (c + 1) * Lch)
+        out, k, v = oracle.dit_block(x[:, rows], e0, W, H, 1e-6, pos[rows], chunk[rows], kc, vc, pc, ctx=ctx)
+        assert np.allclose(out, full[:, rows], atol=1e-12)
+        kc = k if kc is None else np.concatenate([kc, k], 1)
+        vc = v if vc is None else np.concatenate([vc, v], 1)
+        pc = chunk[rows] if pc is None else np.concatenate([pc, chunk[rows]])
+    assert np.allclose(kc, k_full, atol=1e-13) and np.allclose(vc, v_full, atol=1e-13)
+
+
+def test_block_zero_gates():
+    d, H, Fh, B, L = 16, 2, 32, 1, 7
+    W = small_block_weights(d, Fh, 70)
+    W["mod6"][2] = 0.0  # gate1
+    W["mod6"][5] = 0.0  # gate2
+    e0 = rnd(B, 6, d, seed=71)
+    e0[:, 2] = 0.0
+    e0[:, 5] = 0.0
+    x = rnd(B, L, d, seed=72)
+    ctx = rnd(B, 4, d, seed=73)
+    pos = chunk_positions(0, 1, 1, 5, 2)
+    ch = np.zeros(L, int)
+    out, _, _ = oracle.dit_block(x, e0, W, H, 1e-6, pos, ch, ctx=ctx)
+    # with both gates zero the self-attention and FFN weights do not matter
+    W2 = dict(W)
+    for n in ("w_qkv", "w_o", "w_f1", "w_f2", "b_qkv", "b_o", "b_f1", "b_f2"):
+        W2[n] = W[n] * -3.0 + 1.0
+    out2, _, _ = oracle.dit_block(x, e0, W2, H, 1e-6, pos, ch, ctx=ctx)
+    assert np.allclose(out, out2, atol=1e-13)
+    # ... and with the cross-attention output projection zeroed the block is the identity
+    W2["w_co"] = np.zeros_like(W["w_co"])
+    W2["b_co"] = np.zeros_like(W["b_co"])
+    out3, _, _ = oracle.dit_block(x, e0, W2, H, 1e-6, pos, ch, ctx=ctx)
+    assert np.array_equal(out3, x)
+
+
+def test_block_token_permutation_equivariance():
+    d, H, Fh, B, L = 16, 2, 32, 1, 8
+    W = small_block_weights(d, Fh, 80)
+    e0 = rnd(B, 6, d, seed=81)
+    x = rnd(B, L, d, seed=82)
+    ctx = rnd(B, 3, d, seed=83)
+    pos = chunk_positions(1, 1, 2, 3, 2)
+    ch = np.full(L, 1)
+    kp, vp = rnd(B, 4, H, d // H, seed=84), rnd(B, 4, H, d // H, seed=85)
+    pc = np.zeros(4, int)
+    out, k, v = oracle.dit_block(x, e0, W, H, 1e-6, pos, ch, kp, vp, pc, ctx=ctx)
+    perm = np.array([3, 0, 7, 1, 2, 6, 4, 5])
+    out_p, k_p, _ = oracle.dit_block(x[:, perm], e0, W, H, 1e-6, pos[perm], ch, kp, vp, pc, ctx=ctx)
+    assert np.allclose(out_p, out[:, perm], atol=1e-12)
+    assert np.allclose(k_p, k[:, perm], atol=1e-13)
+
+
+def test_block_precomputed_cross_kv():
+    d, H, Fh, B, L = 16, 2, 32, 2, 5
+    W = small_block_weights(d, Fh, 90)
+    x, e0, ctx = rnd(B, L, d, seed=91), rnd(B, 6, d, seed=92), rnd(B, 3, d, seed=93)
+    pos = chunk_positions(0, 1, 1, 3, 2)
+    ch = np.zeros(L, int)
+    a, _, _ = oracle.dit_block(x, e0, W, H, 1e-6, pos, ch, ctx=ctx)
+    kv = oracle.linear(ctx, W["w_ckv"], W["b_ckv"])
+    b, _, _ = oracle.dit_block(x, e0, W, H, 1e-6, pos, ch, ctx_kv=kv)
+    assert np.array_equal(a, b)
+
+
+# ----------------------------------------------------------------------------- step (P12)
+def test_step_identity_blocks_reduce_to_embed_and_head():
+    """All gates zero and W_co = b_co = 0 in every block => every block is the identity,
+    so the velocity is head(embed(z, a)); this checks the step's wiring of time
+    embedding, patchify, embeddings, head and unpatchify."""
+    g = np.random.default_rng(100)
+    B, C, F, Hl, Wl, A, ad, d, H = 2, 4, 2, 4, 6, 3, 5, 16, 2
+    tdim, Lc = 12, 4
+    P = {"w_t1": g.standard_normal((d, 256)) * 0.1, "b_t1": g.standard_normal(d) * 0.1,
+         "w_t2": g.standard_normal((d, d)) * 0.1, "b_t2": g.standard_normal(d) * 0.1,
+         "w_t6": g.standard_normal((6 * d, d)) * 0.1, "b_t6": g.standard_normal(6 * d) * 0.1,
+         "w_x1": g.standard_normal((d, tdim)) * 0.1, "b_x1": np.zeros(d),
+         "w_x2": g.standard_normal((d, d)) * 0.1, "b_x2": np.zeros(d),
+         "w_patch": g.standard_normal((d, C * 4)), "b_patch": g.standard_normal(d),
+         "w_ain": g.standard_normal((d, ad)), "b_ain": g.standard_normal(d),
+         "w_hv": g.standard_normal((C * 4, d)), "b_hv": g.standard_normal(C * 4),
+         "w_ha": g.standard_normal((ad, d)), "b_ha": g.standard_normal(ad),
+         "head_mod2": g.standard_normal((2, d)) * 0.1}
+    # zero the gate rows of the time projection so e0's gates are exactly zero
+    for gate in (2, 5):
+        P["w_t6"][gate * d:(gate + 1) * d] = 0.0
+        P["b_t6"][gate * d:(gate + 1) * d] = 0.0
+    W = small_block_weights(d, 32, 101)
+    W["mod6"][2] = W["mod6"][5] = 0.0
+    W["w_co"] = np.zeros((d, d))
+    W["b_co"] = np.zeros(d)
+    z, a = g.standard_normal((B, C, F, Hl, Wl)), g.standard_normal((B, A, ad))
+    t = np.array([0.25, 0.8])
+    text = g.standard_normal((B, Lc, tdim))
+    Lv = F * (Hl // 2) * (Wl // 2)
+    pos = chunk_positions(1, F, Hl // 2, Wl // 2, A)
+    kp = g.standard_normal((B, 6, H, d // H))
+    vv, va = oracle.dit_step(z, a, t, text, P, lambda l: (W, kp, kp), 3, H, 1e-6, 1, pos,
+                             prev_chunk=np.zeros(6, int))
+    # independent composition: tokens -> head, per token, written out by hand
+    e = np.zeros((B, d))
+    for b in range(B):
+        s = np.array([math.cos(1000 * t[b] * 10000 ** (-k / 128)) for k in range(128)]
+                     + [math.sin(1000 * t[b] * 10000 ** (-k / 128)) for k in range(128)])
+        h1 = P["w_t1"] @ s + P["b_t1"]
+        h1 = h1 / (1 + np.exp(-h1))
+        e[b] = P["w_t2"] @ h1 + P["b_t2"]
+    for b in range(B):
+        sh, sc = P["head_mod2"][0] + e[b], P["head_mod2"][1] + e[b]
+        for tok in range(Lv + A):
+            if tok < Lv:
+                f, rem = divmod(tok, (Hl // 2) * (Wl // 2))
+                r, s_ = divmod(rem, Wl // 2)
+                feat = np.array([z[b, c, f, 2 * r + ph, 2 * s_ + pw]
+                                 for c in range(C) for ph in range(2) for pw in range(2)])
+                xt = P["w_patch"] @ feat + P["b_patch"]
+            else:
+                xt = P["w_ain"] @ a[b, tok - Lv] + P["b_ain"]
+            ht = (xt - xt.mean()) / math.sqrt(xt.var() + 1e-6) * (1 + sc) + sh
+            if tok < Lv:
+                out = P["w_hv"] @ ht + P["b_hv"]
+                for c in range(C):
+                    for ph in range(2):
+                        for pw in range(2):
+                            assert abs(vv[b, c, f, 2 * r + ph, 2 * s_ + pw] - out[c * 4 + ph * 2 + pw]) < 1e-10
+            else:
+                assert np.allclose(va[b, tok - Lv], P["w_ha"] @ ht + P["b_ha"], atol=1e-10)
+
+
+# ----------------------------------------------------------------------------- shared input generator
+def test_bf16_rounding_matches_torch():
+    torch = pytest.importorskip("torch")
+    from synth import bf16_bits
+    x = np.concatenate([rnd(10000, seed=110) * 10.0 ** np.arange(-3, 7).repeat(1000),
+                        [0.0, -0.0, 1.0, 65504.0, 3.0e38, 1e-40]]).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(bf16_bits(x), ref)
