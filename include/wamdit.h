@@ -1,0 +1,338 @@
+/*
+ * libwamdit — one denoising step of a block-causal video/action diffusion
+ * transformer (DiT) on AMD Instinct MI355X (gfx950).
+ *
+ * The step is the velocity call u_theta([z_t, a_t]; KV, c, t) of the paper's
+ * closed-loop inference (Appendix C, Algorithm 2, the denoising forward with
+ * update=False): a chunk of K=2 latent video frames plus its action tokens
+ * attends to a KV cache of earlier, clean chunks and to itself (section 3.1,
+ * Model Inference; Appendix C, Figure 10b).  The KV cache is passed in and out
+ * explicitly, never held by the library (Appendix D.2, the functional KV cache
+ * used for graph capture).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Ownership  The caller owns every buffer, stream and event.  Tensor pointers are
+ *            DEVICE pointers unless a comment says HOST.  The library allocates no
+ *            memory, creates no stream and never synchronises; every call only
+ *            validates its arguments on the host and enqueues kernels on `stream`.
+ *            It keeps no state between calls, so calls on different streams with
+ *            different workspaces may run concurrently.
+ * Errors     Every entry point returns a wam_status.  All argument checks happen on
+ *            the host before the first launch; on failure nothing is enqueued and
+ *            wam_last_error() (thread-local) describes the problem.  WAM_EHIP means
+ *            a launch was rejected by the HIP runtime (work enqueued before it in
+ *            the same call may have run).  Kernel faults surface asynchronously at
+ *            the caller's next synchronisation, as with any HIP kernel.
+ * Dtypes     "bf16" = bfloat16 storage, round-to-nearest-even; every product is
+ *            accumulated in fp32.  Weight matrices, activations, q/k/v/o, the KV
+ *            cache and the text context are bf16.  The residual stream x, biases,
+ *            modulation tables, LayerNorm affine, RoPE tables, timesteps and the
+ *            output velocities are fp32.
+ * Layouts    Row-major, token-major.  A [B][L][H][Dh] tensor is the same memory as
+ *            [B][L][d] with d = H*Dh, head h at columns [h*Dh, (h+1)*Dh).  Weight
+ *            matrices are PyTorch Linear layout [out][in].  Strides are in ELEMENTS.
+ * Alignment  Device pointers must be 16-byte aligned; bf16 row strides must be
+ *            multiples of 8 elements.
+ */
+#ifndef WAMDIT_H
+#define WAMDIT_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define WAM_ABI_VERSION 1
+#define WAM_MAX_CHUNKS 16
+
+typedef enum {
+  WAM_OK = 0,
+  WAM_EINVAL = 1,        /* bad argument: null/misaligned pointer, inconsistent sizes */
+  WAM_EUNSUPPORTED = 2,  /* well-formed but outside what the kernels implement      */
+  WAM_EWORKSPACE = 3,    /* workspace missing or smaller than the query function says */
+  WAM_EHIP = 4           /* the HIP runtime rejected a launch                          */
+} wam_status;
+
+/* Thread-local, human-readable detail of the last non-OK status of this thread. */
+const char* wam_last_error(void);
+int32_t wam_abi_version(void);
+
+/* ------------------------------------------------------------------------------
+ * Chunk layout of one attention call (Appendix C, Figure 10b; section 3.1).
+ *
+ * Key rows are grouped into chunks in order: key chunk j holds key rows
+ * [k_off[j], k_off[j+1]).  Query rows are grouped likewise into query chunks; query
+ * chunk i holds query rows [q_off[i], q_off[i+1]) and carries the global chunk id
+ * q_chunk_id[i].  A query of chunk id c sees exactly the keys of key chunks j <= c:
+ * the clean cached chunks before it and its own chunk; attention inside a chunk is
+ * bidirectional.  So the visible keys of a query form the prefix [0, k_off[c+1]).
+ *
+ * Requirements (else WAM_EINVAL): 1 <= n_k_chunks, n_q_chunks <= WAM_MAX_CHUNKS;
+ * k_off[0] = 0, non-decreasing, k_off[n_k_chunks] = Lk; q_off[0] = 0,
+ * non-decreasing, q_off[n_q_chunks] = Lq; 0 <= q_chunk_id[i] < n_k_chunks,
+ * non-decreasing in i; every non-empty query chunk sees at least one key.
+ *
+ * Cached denoising (one query chunk that is the last key chunk) masks nothing.
+ * ------------------------------------------------------------------------------ */
+typedef struct {
+  int32_t n_k_chunks;
+  int32_t k_off[WAM_MAX_CHUNKS + 1];
+  int32_t n_q_chunks;
+  int32_t q_off[WAM_MAX_CHUNKS + 1];
+  int32_t q_chunk_id[WAM_MAX_CHUNKS];
+} wam_chunks;
+
+/* ------------------------------------------------------------------------------
+ * wam_attn_blockcausal — block-causal softmax attention (the rule above).
+ *
+ *   o[b, i, h, :] = sum_j softmax_j(scale * q[b,i,h,:] . k[b,j,h,:]) v[b,j,h,:]
+ *                   over the keys j visible to query i.
+ *
+ * q: [B] x [Lq] tokens x [H][Dh] bf16, token stride q_tok_stride, batch stride
+ * q_batch_stride; k, v: [B] x [Lk] x [H][Dh] bf16 sharing kv_tok_stride and
+ * kv_batch_stride (k and v may be two halves of one [.., 2*d] buffer); o: written,
+ * [B] x [Lq] x [H][Dh] bf16.  scale <= 0 selects 1/sqrt(Dh).  Dh must be 64 or 128.
+ * Lq = 0 or B = 0 is a no-op.  o must not overlap q, k or v.  Deterministic: the
+ * same inputs give bitwise the same output (no atomics, no split-K).
+ * ------------------------------------------------------------------------------ */
+typedef struct {
+  int32_t B, H, Dh, Lq, Lk;
+  int64_t q_tok_stride, q_batch_stride;
+  int64_t kv_tok_stride, kv_batch_stride;
+  int64_t o_tok_stride, o_batch_stride;
+  float scale;
+  wam_chunks ch;
+} wam_attn_desc;
+
+wam_status wam_attn_blockcausal(const wam_attn_desc* desc, const void* q, const void* k,
+                                const void* v, void* o, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * Model dimensions.  d = H*Dh, d % 256 == 0, Dh in {64, 128}; latent_ch*4 patch
+ * features per token (1x2x2 patches); act_dim action features; text_dim text
+ * feature width; freq_dim sinusoid width (even); eps the LayerNorm epsilon.
+ * ------------------------------------------------------------------------------ */
+typedef struct {
+  int32_t d, H, Dh, ffn, n_layers, latent_ch, act_dim, text_dim, freq_dim;
+  float eps;
+} wam_dims;
+
+/* Per-block weights.  Matrices bf16 [out][in]:
+ *   w_qkv [3d][d] (rows: q | k | v), w_o [d][d], w_cq [d][d], w_ckv [2d][d] (k | v),
+ *   w_co [d][d], w_f1 [ffn][d], w_f2 [d][ffn].
+ * Vectors fp32: every b_* of its matrix's out size (NULL = zero bias); mod6 [6][d]
+ * the block's modulation table added to the per-sample time modulation e0, rows
+ * (shift1, scale1, gate1, shift2, scale2, gate2); lnc_gamma, lnc_beta [d] the affine
+ * of the cross-attention LayerNorm (NULL = 1 and 0). */
+typedef struct {
+  const void *w_qkv, *w_o, *w_cq, *w_ckv, *w_co, *w_f1, *w_f2;
+  const float *b_qkv, *b_o, *b_cq, *b_ckv, *b_co, *b_f1, *b_f2;
+  const float* mod6;
+  const float *lnc_gamma, *lnc_beta;
+} wam_block_weights;
+
+/* ------------------------------------------------------------------------------
+ * wam_dit_block_fwd — one DiT block over the current rows (in place on x).
+ *
+ *   m = mod6 + e0[b];  (sh1, sc1, g1, sh2, sc2, g2) = rows of m
+ *   qkv = (LN(x)(1+sc1)+sh1) W_qkv^T + b_qkv;  q, k <- 3D RoPE (tables rope_cos/sin)
+ *   k, v of the current rows -> cache rows [cache_len, cache_len + L)
+ *   x += g1 * (Attn(q, cache rows [0, cache_len+L), chunks ch) W_o^T + b_o)
+ *   x += Attn((LN(x)*gamma+beta) W_cq^T + b_cq, ctx W_ckv^T + b_ckv) W_co^T + b_co
+ *   x += g2 * (gelu_tanh((LN(x)(1+sc2)+sh2) W_f1^T + b_f1) W_f2^T + b_f2)
+ *
+ * x      [B][L][d] fp32 residual, read and updated in place.
+ * e0     [B][6][d] fp32 per-sample time modulation.
+ * rope_cos, rope_sin  [L][Dh/2] fp32, built with wam_rope_tables for the rows'
+ *        positions (all samples share positions).
+ * k_cache, v_cache  [B][Lcap][H][Dh] bf16, K stored after RoPE.  Rows
+ *        [0, cache_len) are read; rows [cache_len, cache_len+L) are overwritten with
+ *        the current rows' K and V.  The caller advances cache_len by L only for a
+ *        cache-update pass; a denoising step leaves it, so the next step overwrites
+ *        the same rows.  cache_len + L <= Lcap.
+ * ch     key/query chunks of the self-attention: Lk = cache_len + L, Lq = L.
+ * ctx    [B][Lc][d] bf16 projected text; or ctx_kv [B][Lc][2d] bf16 its cross K|V
+ *        already projected with this block's w_ckv (then ctx may be NULL and w_ckv
+ *        is not read).
+ * ws     device workspace of at least wam_block_workspace_bytes(...) bytes,
+ *        256-byte aligned; its contents on entry do not matter.
+ * ------------------------------------------------------------------------------ */
+typedef struct {
+  float* x;
+  const float* e0;
+  const float *rope_cos, *rope_sin;
+  void *k_cache, *v_cache;
+  int32_t Lcap, cache_len;
+  wam_chunks ch;
+  const void* ctx;
+  const void* ctx_kv;
+  int32_t B, L, Lc;
+} wam_block_io;
+
+size_t wam_block_workspace_bytes(const wam_dims* dims, int32_t B, int32_t L, int32_t Lc);
+wam_status wam_dit_block_fwd(const wam_dims* dims, const wam_block_weights* w,
+                             const wam_block_io* io, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * Model-level weights (bf16 [out][in] matrices, fp32 vectors, NULL bias = 0):
+ *   time MLP   w_t1 [d][freq_dim], w_t2 [d][d], w_t6 [6d][d]
+ *              e = W_t2 silu(W_t1 sinusoid(t) + b_t1) + b_t2;  e0 = W_t6 silu(e) + b_t6
+ *   text proj  w_x1 [d][text_dim], w_x2 [d][d]:  ctx = W_x2 gelu_tanh(W_x1 text + b_x1) + b_x2
+ *   embed      w_patch [d][latent_ch*4] on patchified latents, w_ain [d][act_dim]
+ *   head       head_mod2 [2][d] (shift, scale) added to e;
+ *              w_hv [latent_ch*4][d] (unpatchified), w_ha [act_dim][d]
+ * blocks is a HOST array of n_layers block weight sets.
+ * ------------------------------------------------------------------------------ */
+typedef struct {
+  wam_dims dims;
+  const wam_block_weights* blocks;
+  const void *w_t1, *w_t2, *w_t6, *w_x1, *w_x2, *w_patch, *w_ain, *w_hv, *w_ha;
+  const float *b_t1, *b_t2, *b_t6, *b_x1, *b_x2, *b_patch, *b_ain, *b_hv, *b_ha;
+  const float* head_mod2;
+} wam_model;
+
+/* ------------------------------------------------------------------------------
+ * wam_dit_step_fwd — one denoising step u_theta([z_t, a_t]; KV, c, t) of one chunk
+ * (Algorithm 2, the forward inside the denoising loop).
+ *
+ * z_t      [B][latent_ch][F][Hl][Wl] bf16 noisy latents (Hl, Wl even); the chunk's
+ *          video tokens are its 1x2x2 patches, frame-major, then row, then column
+ *          (Lv = F*Hl/2*Wl/2), followed by its A action tokens: L = Lv + A.
+ * a_t      [B][A][act_dim] bf16 noisy actions.
+ * t        [B] fp32 timestep per sample (one per chunk, section 3.1).
+ * text     [B][Lc][text_dim] bf16 text features.
+ * k_cache, v_cache  HOST arrays of n_layers device pointers, each [B][Lcap][H][Dh]
+ *          bf16, semantics as in wam_dit_block_fwd.
+ * ctx_kv   optional HOST array of n_layers device pointers [B][Lc][2d] bf16 holding
+ *          each block's precomputed cross K|V of this text (NULL: computed here).
+ * rope_cos, rope_sin  [L][Dh/2] fp32 tables of the rows' positions.
+ * ch       self-attention chunks (Lk = cache_len + L, Lq = L).
+ * v_video  written, [B][latent_ch][F][Hl][Wl] fp32;  v_action  written, [B][A][act_dim] fp32.
+ * attn_events  optional HOST array of 2*n_layers hipEvent_t: when non-NULL,
+ *          events[2l] and events[2l+1] are recorded on `stream` just before and just
+ *          after block l's self-attention kernel (for per-kernel timing).
+ * ------------------------------------------------------------------------------ */
+typedef struct {
+  const void* z_t;
+  const void* a_t;
+  const float* t;
+  const void* text;
+  void* const* k_cache;
+  void* const* v_cache;
+  const void* const* ctx_kv;
+  const float *rope_cos, *rope_sin;
+  int32_t B, F, Hl, Wl, A, Lc, Lcap, cache_len;
+  wam_chunks ch;
+  float* v_video;
+  float* v_action;
+  hipEvent_t* attn_events;
+} wam_step_io;
+
+size_t wam_step_workspace_bytes(const wam_model* m, const wam_step_io* io);
+wam_status wam_dit_step_fwd(const wam_model* m, const wam_step_io* io, void* ws,
+                            size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * Pieces of the step, exported for testing each kernel on its own.
+ * ------------------------------------------------------------------------------ */
+
+/* Time embedding: e [B][d] and e0 [B][6][d] (fp32) from t [B].  ws >= B*(freq_dim+d)*4 bytes. */
+size_t wam_time_embed_workspace_bytes(const wam_dims* dims, int32_t B);
+wam_status wam_time_embed_fwd(const wam_model* m, int32_t B, const float* t, float* e,
+                              float* e0, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Text projection: ctx [B*Lc][d] bf16 from text [B*Lc][text_dim] bf16.
+ * ws >= B*Lc*d*2 bytes (the GELU hidden). */
+size_t wam_text_proj_workspace_bytes(const wam_dims* dims, int32_t B, int32_t Lc);
+wam_status wam_text_proj_fwd(const wam_model* m, int32_t B, int32_t Lc, const void* text,
+                             void* ctx, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* LayerNorm over rows of d fp32 values, then optional affine and modulation, to bf16:
+ *   h[b,r,:] = ((x - mean)/sqrt(var + eps) * gamma + beta) * (1 + scale_b) + shift_b
+ * with shift_b = shift_a + shift_v[b*mod_stride .. ] (likewise scale).  Rows are
+ * [B][rows_per_batch] with row stride d (x) and d (h).  gamma/beta NULL = 1/0; a
+ * NULL shift_a/shift_v (scale_a/scale_v) contributes 0. */
+wam_status wam_adaln_ln_mod(int32_t B, int32_t rows_per_batch, int32_t d, float eps,
+                            const float* x, const float* gamma, const float* beta,
+                            const float* shift_a, const float* shift_v,
+                            const float* scale_a, const float* scale_v, int64_t mod_stride,
+                            void* h, hipStream_t stream);
+
+/* 3D RoPE on a fused QKV projection and KV-cache append.
+ * qkv [B][L][3][H][Dh] bf16 (q | k | v per token); rope_cos/sin [L][Dh/2] fp32.
+ * Writes q_out [B][L][H][Dh] (rotated q), rotated k into k_cache rows
+ * [row0, row0+L) and v into v_cache rows [row0, row0+L) of [B][Lcap][H][Dh]. */
+wam_status wam_rope_qkv(int32_t B, int32_t L, int32_t H, int32_t Dh, const void* qkv,
+                        const float* rope_cos, const float* rope_sin, void* q_out,
+                        void* k_cache, void* v_cache, int32_t Lcap, int32_t row0,
+                        hipStream_t stream);
+
+/* GEMM with fused epilogue: acc[m][n] = sum_k A[m][k] W[n][k] (bf16 in, fp32 acc),
+ * v = acc + bias[n] (bias NULL = 0), then by epilogue:
+ *   WAM_EPI_BF16         out_bf16[m][n] = v
+ *   WAM_EPI_GELU_BF16    out_bf16[m][n] = gelu_tanh(v)
+ *   WAM_EPI_RESID_F32    out_f32[m][n] += g * v, g = gate_a[n] + gate_v[(m / gate_rows)*gate_stride + n]
+ *                        (both gate pointers NULL: g = 1)
+ *   WAM_EPI_F32          out_f32[m][n] = v
+ * Row m of A is at A + (m / a_rows)*a_batch_stride + (m % a_rows)*lda and row m of
+ * out at out + (m / out_rows)*out_batch_stride + (m % out_rows)*ldo (a_rows or
+ * out_rows = 0: plain, i.e. row m at m*lda / m*ldo).  K % 8 == 0. */
+enum { WAM_EPI_BF16 = 0, WAM_EPI_GELU_BF16 = 1, WAM_EPI_RESID_F32 = 2, WAM_EPI_F32 = 3 };
+typedef struct {
+  int32_t M, N, K, epilogue;
+  const void* A;
+  int64_t lda, a_batch_stride;
+  int32_t a_rows;
+  const void* W;
+  int64_t ldw;
+  const float* bias;
+  void* out;
+  int64_t ldo, out_batch_stride;
+  int32_t out_rows;
+  const float *gate_a, *gate_v;
+  int64_t gate_stride;
+  int32_t gate_rows;
+} wam_gemm_desc;
+
+wam_status wam_gemm_bf16(const wam_gemm_desc* g, hipStream_t stream);
+
+/* Patch and action embedding into the fp32 residual x [B][Lv+A][d]. */
+size_t wam_embed_workspace_bytes(const wam_dims* dims, int32_t B, int32_t F, int32_t Hl, int32_t Wl);
+wam_status wam_embed_fwd(const wam_model* m, int32_t B, int32_t F, int32_t Hl, int32_t Wl,
+                         int32_t A, const void* z_t, const void* a_t, float* x, void* ws,
+                         size_t ws_bytes, hipStream_t stream);
+
+/* Output head from x [B][Lv+A][d] and e [B][d]: v_video [B][latent_ch][F][Hl][Wl] and
+ * v_action [B][A][act_dim], both fp32. */
+size_t wam_head_workspace_bytes(const wam_dims* dims, int32_t B, int32_t F, int32_t Hl, int32_t Wl, int32_t A);
+wam_status wam_head_fwd(const wam_model* m, int32_t B, int32_t F, int32_t Hl, int32_t Wl,
+                        int32_t A, const float* x, const float* e, float* v_video,
+                        float* v_action, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * Host helpers (HOST memory, no GPU work).
+ * ------------------------------------------------------------------------------ */
+
+/* RoPE positions of chunk c: video token (f, r, s) of its F frames at (F*c + f, r, s),
+ * frame-major then row then column over an Hg x Wg grid; action token j after the
+ * last frame at (F*c + F + j, 0, 0).  pos: HOST [(F*Hg*Wg + A)][3]. */
+wam_status wam_chunk_positions(int32_t c, int32_t F, int32_t Hg, int32_t Wg, int32_t A,
+                               int32_t* pos);
+
+/* RoPE tables for L positions pos [L][3] (HOST): the head vector splits into
+ * contiguous (t, h, w) segments of (Dh - 4*floor(Dh/6), 2*floor(Dh/6), 2*floor(Dh/6))
+ * dims; pair i of a segment with D_a dims at position p rotates by
+ * p * theta^(-2i/D_a).  Computed in double, rounded to fp32:
+ * cos_out, sin_out HOST [L][Dh/2]. */
+wam_status wam_rope_tables(const int32_t* pos, int32_t L, int32_t Dh, double theta,
+                           float* cos_out, float* sin_out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WAMDIT_H */

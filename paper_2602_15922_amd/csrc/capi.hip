@@ -1,0 +1,676 @@
+// C ABI of libwamdit: host-side validation, workspace planning and the launch
+// sequences of the DiT block and denoising step.  No memory is allocated and no
+// stream is synchronised here; every entry point validates all arguments before its
+// first launch.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "kernels.h"
+
+using namespace wam;
+
+namespace {
+
+thread_local std::string g_err;
+
+wam_status fail(wam_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define CHECK(cond, st, ...) \
+  do {                       \
+    if (!(cond)) return fail(st, __VA_ARGS__); \
+  } while (0)
+
+#define HIPCHECK(expr)                                                              \
+  do {                                                                              \
+    hipError_t e_ = (expr);                                                         \
+    if (e_ != hipSuccess) return fail(WAM_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+#define TRY(expr)                      \
+  do {                                 \
+    wam_status s_ = (expr);            \
+    if (s_ != WAM_OK) return s_;       \
+  } while (0)
+
+bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+wam_status need_ptr(const void* p, const char* name) {
+  if (!p) return fail(WAM_EINVAL, "%s is NULL", name);
+  if (!al16(p)) return fail(WAM_EINVAL, "%s is not 16-byte aligned", name);
+  return WAM_OK;
+}
+wam_status opt_ptr(const void* p, const char* name) {
+  if (p && !al16(p)) return fail(WAM_EINVAL, "%s is not 16-byte aligned", name);
+  return WAM_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Validate a chunk layout for Lq query rows and Lk key rows; on success fill the
+// per-query-chunk visible key prefix.
+wam_status check_chunks(const wam_chunks& c, int32_t Lq, int32_t Lk, int32_t* kend) {
+  CHECK(c.n_k_chunks >= 1 && c.n_k_chunks <= WAM_MAX_CHUNKS, WAM_EINVAL,
+        "n_k_chunks=%d outside [1,%d]", c.n_k_chunks, WAM_MAX_CHUNKS);
+  CHECK(c.n_q_chunks >= 1 && c.n_q_chunks <= WAM_MAX_CHUNKS, WAM_EINVAL,
+        "n_q_chunks=%d outside [1,%d]", c.n_q_chunks, WAM_MAX_CHUNKS);
+  CHECK(c.k_off[0] == 0 && c.k_off[c.n_k_chunks] == Lk, WAM_EINVAL,
+        "k_off must run from 0 to Lk=%d (got %d..%d)", Lk, c.k_off[0], c.k_off[c.n_k_chunks]);
+  for (int j = 0; j < c.n_k_chunks; ++j)
+    CHECK(c.k_off[j] <= c.k_off[j + 1], WAM_EINVAL, "k_off not non-decreasing at %d", j);
+  CHECK(c.q_off[0] == 0 && c.q_off[c.n_q_chunks] == Lq, WAM_EINVAL,
+        "q_off must run from 0 to Lq=%d (got %d..%d)", Lq, c.q_off[0], c.q_off[c.n_q_chunks]);
+  for (int i = 0; i < c.n_q_chunks; ++i) {
+    CHECK(c.q_off[i] <= c.q_off[i + 1], WAM_EINVAL, "q_off not non-decreasing at %d", i);
+    CHECK(c.q_chunk_id[i] >= 0 && c.q_chunk_id[i] < c.n_k_chunks, WAM_EINVAL,
+          "q_chunk_id[%d]=%d outside [0,%d)", i, c.q_chunk_id[i], c.n_k_chunks);
+    CHECK(i == 0 || c.q_chunk_id[i] >= c.q_chunk_id[i - 1], WAM_EINVAL,
+          "q_chunk_id not non-decreasing at %d", i);
+    kend[i] = c.k_off[c.q_chunk_id[i] + 1];
+    CHECK(c.q_off[i] == c.q_off[i + 1] || kend[i] > 0, WAM_EINVAL,
+          "query chunk %d sees no key", i);
+  }
+  return WAM_OK;
+}
+
+wam_status check_dims(const wam_dims& D) {
+  CHECK(D.Dh == 64 || D.Dh == 128, WAM_EUNSUPPORTED, "Dh=%d (supported: 64, 128)", D.Dh);
+  CHECK(D.H >= 1 && D.H * D.Dh == D.d, WAM_EINVAL, "H*Dh=%d != d=%d", D.H * D.Dh, D.d);
+  CHECK(D.d % 256 == 0 && D.d <= 8192, WAM_EUNSUPPORTED, "d=%d must be a multiple of 256, <= 8192", D.d);
+  CHECK(D.ffn >= 8 && D.ffn % 8 == 0, WAM_EUNSUPPORTED, "ffn=%d must be a positive multiple of 8", D.ffn);
+  CHECK(D.eps > 0.f, WAM_EINVAL, "eps must be > 0");
+  return WAM_OK;
+}
+
+// ---------------------------------------------------------------------------------
+// attention
+// ---------------------------------------------------------------------------------
+wam_status attn_checked(const wam_attn_desc& d, const void* q, const void* k, const void* v, void* o,
+                        hipStream_t s) {
+  CHECK(d.Dh == 64 || d.Dh == 128, WAM_EUNSUPPORTED, "Dh=%d (supported: 64, 128)", d.Dh);
+  CHECK(d.B >= 0 && d.H >= 1 && d.Lq >= 0 && d.Lk >= 0, WAM_EINVAL, "negative size (B=%d H=%d Lq=%d Lk=%d)",
+        d.B, d.H, d.Lq, d.Lk);
+  AttnArgs a{};
+  TRY(check_chunks(d.ch, d.Lq, d.Lk, a.kend));
+  if (d.B == 0 || d.Lq == 0) return WAM_OK;
+  TRY(need_ptr(q, "q"));
+  TRY(need_ptr(k, "k"));
+  TRY(need_ptr(v, "v"));
+  TRY(need_ptr(o, "o"));
+  const int64_t hd = (int64_t)d.H * d.Dh;
+  CHECK(d.q_tok_stride >= hd && d.kv_tok_stride >= hd && d.o_tok_stride >= hd, WAM_EINVAL,
+        "token strides must be >= H*Dh=%lld", (long long)hd);
+  CHECK(d.q_tok_stride % 8 == 0 && d.kv_tok_stride % 8 == 0 && d.o_tok_stride % 8 == 0 &&
+            d.q_batch_stride % 8 == 0 && d.kv_batch_stride % 8 == 0 && d.o_batch_stride % 8 == 0,
+        WAM_EINVAL, "strides must be multiples of 8 elements");
+  CHECK(d.B == 1 || (d.q_batch_stride >= (int64_t)d.Lq * d.q_tok_stride &&
+                     d.o_batch_stride >= (int64_t)d.Lq * d.o_tok_stride &&
+                     d.kv_batch_stride >= (int64_t)d.Lk * d.kv_tok_stride),
+        WAM_EINVAL, "batch strides smaller than one sample");
+  a.q = q; a.k = k; a.v = v; a.o = o;
+  a.q_ts = d.q_tok_stride; a.q_bs = d.q_batch_stride;
+  a.kv_ts = d.kv_tok_stride; a.kv_bs = d.kv_batch_stride;
+  a.o_ts = d.o_tok_stride; a.o_bs = d.o_batch_stride;
+  a.B = d.B; a.H = d.H; a.Dh = d.Dh; a.Lq = d.Lq; a.Lk = d.Lk;
+  const float scale = d.scale > 0.f ? d.scale : 1.0f / std::sqrt((float)d.Dh);
+  a.c = scale * 1.4426950408889634f;
+  a.n_q_chunks = d.ch.n_q_chunks;
+  for (int i = 0; i <= d.ch.n_q_chunks; ++i) a.q_off[i] = d.ch.q_off[i];
+  HIPCHECK(launch_attn(a, s));
+  return WAM_OK;
+}
+
+wam_chunks single_chunk(int32_t Lq, int32_t Lk) {
+  wam_chunks c{};
+  c.n_k_chunks = 1; c.k_off[0] = 0; c.k_off[1] = Lk;
+  c.n_q_chunks = 1; c.q_off[0] = 0; c.q_off[1] = Lq; c.q_chunk_id[0] = 0;
+  return c;
+}
+
+// ---------------------------------------------------------------------------------
+// GEMM
+// ---------------------------------------------------------------------------------
+wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s) {
+  CHECK(g.M >= 0 && g.N >= 1 && g.K >= 8 && g.K % 8 == 0, WAM_EINVAL,
+        "GEMM sizes M=%d N=%d K=%d (need N>=1, K>=8, K%%8==0)", g.M, g.N, g.K);
+  CHECK(g.epilogue >= WAM_EPI_BF16 && g.epilogue <= WAM_EPI_F32, WAM_EINVAL, "unknown epilogue %d", g.epilogue);
+  if (g.M == 0) return WAM_OK;
+  TRY(need_ptr(g.A, "A"));
+  TRY(need_ptr(g.W, "W"));
+  TRY(need_ptr(g.out, "out"));
+  CHECK(g.lda >= g.K && g.lda % 8 == 0 && g.ldw >= g.K && g.ldw % 8 == 0, WAM_EINVAL,
+        "lda/ldw must be >= K and multiples of 8");
+  CHECK(g.ldo >= g.N, WAM_EINVAL, "ldo < N");
+  CHECK(g.a_rows >= 0 && g.out_rows >= 0 && g.gate_rows >= 0, WAM_EINVAL, "negative row groups");
+  CHECK(g.a_batch_stride % 8 == 0, WAM_EINVAL, "a_batch_stride must be a multiple of 8");
+  GemmArgs a{};
+  a.M = g.M; a.N = g.N; a.K = g.K; a.epi = g.epilogue;
+  a.A = g.A; a.lda = g.lda; a.a_bs = g.a_batch_stride; a.a_rows = g.a_rows;
+  a.W = g.W; a.ldw = g.ldw; a.bias = g.bias;
+  a.out = g.out; a.ldo = g.ldo; a.o_bs = g.out_batch_stride; a.o_rows = g.out_rows;
+  a.gate_a = g.gate_a; a.gate_v = g.gate_v; a.gate_stride = g.gate_stride; a.gate_rows = g.gate_rows;
+  HIPCHECK(launch_gemm(a, s));
+  return WAM_OK;
+}
+
+wam_gemm_desc gemm(int M, int N, int K, int epi, const void* A, int64_t lda, const void* W,
+                   const float* bias, void* out, int64_t ldo) {
+  wam_gemm_desc g{};
+  g.M = M; g.N = N; g.K = K; g.epilogue = epi;
+  g.A = A; g.lda = lda; g.W = W; g.ldw = K; g.bias = bias; g.out = out; g.ldo = ldo;
+  return g;
+}
+
+// ---------------------------------------------------------------------------------
+// block
+// ---------------------------------------------------------------------------------
+struct BlockWs {
+  size_t h, big, q, o, ckv, total;
+};
+BlockWs block_ws(const wam_dims& D, int32_t B, int32_t L, int32_t Lc) {
+  const size_t M = (size_t)B * L, d = D.d;
+  const size_t wide = (size_t)(3 * D.d > D.ffn ? 3 * D.d : D.ffn);
+  BlockWs w{};
+  size_t off = 0;
+  w.h = off; off += align256(M * d * 2);
+  w.big = off; off += align256(M * wide * 2);
+  w.q = off; off += align256(M * d * 2);
+  w.o = off; off += align256(M * d * 2);
+  w.ckv = off; off += align256((size_t)B * Lc * 2 * d * 2);
+  w.total = off;
+  return w;
+}
+
+wam_status check_block_weights(const wam_block_weights& w) {
+  TRY(need_ptr(w.w_qkv, "w_qkv")); TRY(need_ptr(w.w_o, "w_o")); TRY(need_ptr(w.w_cq, "w_cq"));
+  TRY(need_ptr(w.w_co, "w_co")); TRY(need_ptr(w.w_f1, "w_f1")); TRY(need_ptr(w.w_f2, "w_f2"));
+  TRY(need_ptr(w.mod6, "mod6"));
+  TRY(opt_ptr(w.w_ckv, "w_ckv"));
+  TRY(opt_ptr(w.b_qkv, "b_qkv")); TRY(opt_ptr(w.b_o, "b_o")); TRY(opt_ptr(w.b_cq, "b_cq"));
+  TRY(opt_ptr(w.b_ckv, "b_ckv")); TRY(opt_ptr(w.b_co, "b_co")); TRY(opt_ptr(w.b_f1, "b_f1"));
+  TRY(opt_ptr(w.b_f2, "b_f2")); TRY(opt_ptr(w.lnc_gamma, "lnc_gamma")); TRY(opt_ptr(w.lnc_beta, "lnc_beta"));
+  return WAM_OK;
+}
+
+wam_status check_block_io(const wam_dims& D, const wam_block_weights& w, const wam_block_io& io) {
+  CHECK(io.B >= 1 && io.L >= 1 && io.Lc >= 1, WAM_EINVAL, "B=%d L=%d Lc=%d must be >= 1", io.B, io.L, io.Lc);
+  CHECK(io.B <= 8, WAM_EUNSUPPORTED, "B=%d > 8", io.B);
+  CHECK(io.cache_len >= 0 && (int64_t)io.cache_len + io.L <= io.Lcap, WAM_EINVAL,
+        "cache_len=%d + L=%d exceeds Lcap=%d", io.cache_len, io.L, io.Lcap);
+  int32_t kend[WAM_MAX_CHUNKS];
+  TRY(check_chunks(io.ch, io.L, io.cache_len + io.L, kend));
+  TRY(need_ptr(io.x, "x")); TRY(need_ptr(io.e0, "e0"));
+  TRY(need_ptr(io.rope_cos, "rope_cos")); TRY(need_ptr(io.rope_sin, "rope_sin"));
+  TRY(need_ptr(io.k_cache, "k_cache")); TRY(need_ptr(io.v_cache, "v_cache"));
+  if (io.ctx_kv) {
+    TRY(need_ptr(io.ctx_kv, "ctx_kv"));
+  } else {
+    TRY(need_ptr(io.ctx, "ctx"));
+    TRY(need_ptr(w.w_ckv, "w_ckv"));
+  }
+  return WAM_OK;
+}
+
+// The launch sequence of one block; arguments already validated.
+wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_block_io& io, char* ws,
+                     hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  const int d = D.d, B = io.B, L = io.L, M = B * L;
+  const BlockWs lay = block_ws(D, B, L, io.Lc);
+  void* h = ws + lay.h;
+  void* big = ws + lay.big;
+  void* q = ws + lay.q;
+  void* o = ws + lay.o;
+  void* ckv = ws + lay.ckv;
+  const float* m6 = W.mod6;
+  const float* e0 = io.e0;
+  const int64_t ms = 6 * (int64_t)d;
+
+  // 1. AdaLN: h = LN(x)(1 + scale1) + shift1
+  LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h};
+  HIPCHECK(launch_ln_mod(ln, s));
+  // 2. fused QKV projection
+  TRY(gemm_checked(gemm(M, 3 * d, d, WAM_EPI_BF16, h, d, W.w_qkv, W.b_qkv, big, 3 * d), s));
+  // 3. RoPE on q, k; k, v appended to the cache rows of this chunk
+  RopeArgs ra{B, L, D.H, D.Dh, io.Lcap, io.cache_len, big, io.rope_cos, io.rope_sin, q, io.k_cache, io.v_cache};
+  HIPCHECK(launch_rope_qkv(ra, s));
+  // 4. block-causal self-attention over cache rows [0, cache_len + L)
+  wam_attn_desc ad{};
+  ad.B = B; ad.H = D.H; ad.Dh = D.Dh; ad.Lq = L; ad.Lk = io.cache_len + L;
+  ad.q_tok_stride = d; ad.q_batch_stride = (int64_t)L * d;
+  ad.kv_tok_stride = d; ad.kv_batch_stride = (int64_t)io.Lcap * d;
+  ad.o_tok_stride = d; ad.o_batch_stride = (int64_t)L * d;
+  ad.ch = io.ch;
+  if (ev0) HIPCHECK(hipEventRecord(ev0, s));
+  TRY(attn_checked(ad, q, io.k_cache, io.v_cache, o, s));
+  if (ev1) HIPCHECK(hipEventRecord(ev1, s));
+  // 5. x += gate1 * (o W_o^T + b_o)
+  {
+    wam_gemm_desc g = gemm(M, d, d, WAM_EPI_RESID_F32, o, d, W.w_o, W.b_o, io.x, d);
+    g.gate_a = m6 + 2 * d; g.gate_v = e0 + 2 * d; g.gate_stride = ms; g.gate_rows = L;
+    TRY(gemm_checked(g, s));
+  }
+  // 6. cross-attention LayerNorm (affine, no modulation)
+  LnArgs lc{M, L, d, D.eps, io.x, W.lnc_gamma, W.lnc_beta, nullptr, nullptr, nullptr, nullptr, 0, h};
+  HIPCHECK(launch_ln_mod(lc, s));
+  // 7. cross query
+  TRY(gemm_checked(gemm(M, d, d, WAM_EPI_BF16, h, d, W.w_cq, W.b_cq, q, d), s));
+  // 8. cross K|V of the text (unless precomputed for this block)
+  const void* kv = io.ctx_kv;
+  if (!kv) {
+    TRY(gemm_checked(gemm(B * io.Lc, 2 * d, d, WAM_EPI_BF16, io.ctx, d, W.w_ckv, W.b_ckv, ckv, 2 * d), s));
+    kv = ckv;
+  }
+  // 9. cross-attention: every text token visible
+  wam_attn_desc cd{};
+  cd.B = B; cd.H = D.H; cd.Dh = D.Dh; cd.Lq = L; cd.Lk = io.Lc;
+  cd.q_tok_stride = d; cd.q_batch_stride = (int64_t)L * d;
+  cd.kv_tok_stride = 2 * d; cd.kv_batch_stride = (int64_t)io.Lc * 2 * d;
+  cd.o_tok_stride = d; cd.o_batch_stride = (int64_t)L * d;
+  cd.ch = single_chunk(L, io.Lc);
+  TRY(attn_checked(cd, q, kv, static_cast<const char*>(kv) + (size_t)d * 2, o, s));
+  // 10. x += o W_co^T + b_co (no gate)
+  TRY(gemm_checked(gemm(M, d, d, WAM_EPI_RESID_F32, o, d, W.w_co, W.b_co, io.x, d), s));
+  // 11. AdaLN #2
+  LnArgs l2{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 3 * d, e0 + 3 * d, m6 + 4 * d, e0 + 4 * d, ms, h};
+  HIPCHECK(launch_ln_mod(l2, s));
+  // 12. FFN up-projection with tanh-GELU
+  TRY(gemm_checked(gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, big, D.ffn), s));
+  // 13. x += gate2 * (u W_f2^T + b_f2)
+  {
+    wam_gemm_desc g = gemm(M, d, D.ffn, WAM_EPI_RESID_F32, big, D.ffn, W.w_f2, W.b_f2, io.x, d);
+    g.gate_a = m6 + 5 * d; g.gate_v = e0 + 5 * d; g.gate_stride = ms; g.gate_rows = L;
+    TRY(gemm_checked(g, s));
+  }
+  return WAM_OK;
+}
+
+// ---------------------------------------------------------------------------------
+// model-level pieces
+// ---------------------------------------------------------------------------------
+wam_status check_model_common(const wam_model& m) {
+  TRY(check_dims(m.dims));
+  CHECK(m.dims.freq_dim >= 2 && m.dims.freq_dim % 8 == 0, WAM_EUNSUPPORTED, "freq_dim=%d must be a multiple of 8",
+        m.dims.freq_dim);
+  CHECK(m.dims.text_dim >= 8 && m.dims.text_dim % 8 == 0, WAM_EUNSUPPORTED, "text_dim=%d must be a multiple of 8",
+        m.dims.text_dim);
+  CHECK(m.dims.act_dim >= 8 && m.dims.act_dim % 8 == 0, WAM_EUNSUPPORTED, "act_dim=%d must be a multiple of 8",
+        m.dims.act_dim);
+  CHECK(m.dims.latent_ch >= 2 && m.dims.latent_ch % 2 == 0, WAM_EUNSUPPORTED,
+        "latent_ch=%d must be even (patch features a multiple of 8)", m.dims.latent_ch);
+  return WAM_OK;
+}
+
+size_t time_ws(const wam_dims& D, int32_t B) { return align256((size_t)B * (D.freq_dim + D.d) * 4); }
+
+wam_status time_run(const wam_model& m, int32_t B, const float* t, float* e, float* e0, char* ws, hipStream_t s) {
+  const wam_dims& D = m.dims;
+  float* sinus = reinterpret_cast<float*>(ws);
+  float* hid = sinus + (size_t)B * D.freq_dim;
+  HIPCHECK(launch_sinusoid(B, D.freq_dim, t, sinus, s));
+  HIPCHECK(launch_gemv(B, D.d, D.freq_dim, sinus, GEMV_ACT_NONE, m.w_t1, m.b_t1, hid, s));
+  HIPCHECK(launch_gemv(B, D.d, D.d, hid, GEMV_ACT_SILU, m.w_t2, m.b_t2, e, s));
+  HIPCHECK(launch_gemv(B, 6 * D.d, D.d, e, GEMV_ACT_SILU, m.w_t6, m.b_t6, e0, s));
+  return WAM_OK;
+}
+
+size_t text_ws(const wam_dims& D, int32_t B, int32_t Lc) { return align256((size_t)B * Lc * D.d * 2); }
+
+wam_status text_run(const wam_model& m, int32_t B, int32_t Lc, const void* text, void* ctx, char* ws,
+                    hipStream_t s) {
+  const wam_dims& D = m.dims;
+  TRY(gemm_checked(gemm(B * Lc, D.d, D.text_dim, WAM_EPI_GELU_BF16, text, D.text_dim, m.w_x1, m.b_x1, ws, D.d), s));
+  TRY(gemm_checked(gemm(B * Lc, D.d, D.d, WAM_EPI_BF16, ws, D.d, m.w_x2, m.b_x2, ctx, D.d), s));
+  return WAM_OK;
+}
+
+size_t embed_ws(const wam_dims& D, int32_t B, int32_t F, int32_t Hl, int32_t Wl) {
+  return align256((size_t)B * F * (Hl / 2) * (Wl / 2) * D.latent_ch * 4 * 2);
+}
+
+wam_status embed_run(const wam_model& m, int32_t B, int32_t F, int32_t Hl, int32_t Wl, int32_t A, const void* z,
+                     const void* a, float* x, char* ws, hipStream_t s) {
+  const wam_dims& D = m.dims;
+  const int P = D.latent_ch * 4, Lv = F * (Hl / 2) * (Wl / 2), L = Lv + A;
+  HIPCHECK(launch_patchify(B, D.latent_ch, F, Hl, Wl, z, ws, s));
+  wam_gemm_desc g = gemm(B * Lv, D.d, P, WAM_EPI_F32, ws, P, m.w_patch, m.b_patch, x, D.d);
+  g.out_rows = Lv; g.out_batch_stride = (int64_t)L * D.d;
+  TRY(gemm_checked(g, s));
+  if (A > 0) {
+    wam_gemm_desc ga = gemm(B * A, D.d, D.act_dim, WAM_EPI_F32, a, D.act_dim, m.w_ain, m.b_ain,
+                            x + (size_t)Lv * D.d, D.d);
+    ga.out_rows = A; ga.out_batch_stride = (int64_t)L * D.d;
+    TRY(gemm_checked(ga, s));
+  }
+  return WAM_OK;
+}
+
+struct HeadWs {
+  size_t h, tok, total;
+};
+HeadWs head_ws(const wam_dims& D, int32_t B, int32_t F, int32_t Hl, int32_t Wl, int32_t A) {
+  const size_t Lv = (size_t)F * (Hl / 2) * (Wl / 2), M = (size_t)B * (Lv + A);
+  HeadWs w{};
+  w.h = 0;
+  w.tok = align256(M * D.d * 2);
+  w.total = w.tok + align256((size_t)B * Lv * D.latent_ch * 4 * 4);
+  return w;
+}
+
+wam_status head_run(const wam_model& m, int32_t B, int32_t F, int32_t Hl, int32_t Wl, int32_t A, const float* x,
+                    const float* e, float* v_video, float* v_action, char* ws, hipStream_t s) {
+  const wam_dims& D = m.dims;
+  const int d = D.d, P = D.latent_ch * 4, Lv = F * (Hl / 2) * (Wl / 2), L = Lv + A;
+  const HeadWs lay = head_ws(D, B, F, Hl, Wl, A);
+  char* h = ws + lay.h;
+  float* tok = reinterpret_cast<float*>(ws + lay.tok);
+  LnArgs ln{B * L, L, d, D.eps, x, nullptr, nullptr, m.head_mod2, e, m.head_mod2 + d, e, d, h};
+  HIPCHECK(launch_ln_mod(ln, s));
+  wam_gemm_desc gv = gemm(B * Lv, P, d, WAM_EPI_F32, h, d, m.w_hv, m.b_hv, tok, P);
+  gv.a_rows = Lv; gv.a_batch_stride = (int64_t)L * d;
+  TRY(gemm_checked(gv, s));
+  HIPCHECK(launch_unpatchify(B, D.latent_ch, F, Hl, Wl, tok, v_video, s));
+  if (A > 0) {
+    wam_gemm_desc ga = gemm(B * A, D.act_dim, d, WAM_EPI_F32, h + (size_t)Lv * d * 2, d, m.w_ha, m.b_ha,
+                            v_action, D.act_dim);
+    ga.a_rows = A; ga.a_batch_stride = (int64_t)L * d;
+    TRY(gemm_checked(ga, s));
+  }
+  return WAM_OK;
+}
+
+struct StepWs {
+  size_t x, e, e0, ctx, piece, block, total;
+};
+StepWs step_ws(const wam_model& m, const wam_step_io& io) {
+  const wam_dims& D = m.dims;
+  const size_t Lv = (size_t)io.F * (io.Hl / 2) * (io.Wl / 2), L = Lv + io.A, M = (size_t)io.B * L;
+  StepWs w{};
+  size_t off = 0;
+  w.x = off; off += align256(M * D.d * 4);
+  w.e = off; off += align256((size_t)io.B * D.d * 4);
+  w.e0 = off; off += align256((size_t)io.B * 6 * D.d * 4);
+  w.ctx = off; off += align256((size_t)io.B * io.Lc * D.d * 2);
+  // scratch for the time MLP, text projection, embedding and head (used one at a time)
+  size_t piece = time_ws(D, io.B);
+  piece = std::max(piece, text_ws(D, io.B, io.Lc));
+  piece = std::max(piece, embed_ws(D, io.B, io.F, io.Hl, io.Wl));
+  piece = std::max(piece, head_ws(D, io.B, io.F, io.Hl, io.Wl, io.A).total);
+  w.piece = off; off += align256(piece);
+  w.block = off; off += block_ws(D, io.B, (int32_t)L, io.Lc).total;
+  w.total = off;
+  return w;
+}
+
+wam_status check_ws(const void* ws, size_t have, size_t need) {
+  CHECK(ws != nullptr, WAM_EWORKSPACE, "workspace is NULL (need %zu bytes)", need);
+  CHECK((reinterpret_cast<uintptr_t>(ws) & 255) == 0, WAM_EWORKSPACE, "workspace must be 256-byte aligned");
+  CHECK(have >= need, WAM_EWORKSPACE, "workspace %zu bytes < %zu needed", have, need);
+  return WAM_OK;
+}
+
+wam_status check_step(const wam_model& m, const wam_step_io& io) {
+  TRY(check_model_common(m));
+  const wam_dims& D = m.dims;
+  CHECK(D.n_layers >= 0, WAM_EINVAL, "n_layers < 0");
+  CHECK(io.B >= 1 && io.B <= 8, WAM_EUNSUPPORTED, "B=%d outside [1,8]", io.B);
+  CHECK(io.F >= 1 && io.Hl >= 2 && io.Wl >= 2 && io.Hl % 2 == 0 && io.Wl % 2 == 0, WAM_EINVAL,
+        "latent F=%d Hl=%d Wl=%d (Hl, Wl even)", io.F, io.Hl, io.Wl);
+  CHECK(io.A >= 0 && io.Lc >= 1, WAM_EINVAL, "A=%d Lc=%d", io.A, io.Lc);
+  const int64_t L = (int64_t)io.F * (io.Hl / 2) * (io.Wl / 2) + io.A;
+  CHECK(L < (1 << 30), WAM_EINVAL, "chunk too long");
+  CHECK(io.cache_len >= 0 && io.cache_len + L <= io.Lcap, WAM_EINVAL, "cache_len=%d + L=%lld exceeds Lcap=%d",
+        io.cache_len, (long long)L, io.Lcap);
+  int32_t kend[WAM_MAX_CHUNKS];
+  TRY(check_chunks(io.ch, (int32_t)L, (int32_t)(io.cache_len + L), kend));
+  TRY(need_ptr(io.z_t, "z_t")); TRY(need_ptr(io.t, "t")); TRY(need_ptr(io.text, "text"));
+  if (io.A > 0) { TRY(need_ptr(io.a_t, "a_t")); TRY(need_ptr(io.v_action, "v_action")); }
+  TRY(need_ptr(io.rope_cos, "rope_cos")); TRY(need_ptr(io.rope_sin, "rope_sin"));
+  TRY(need_ptr(io.v_video, "v_video"));
+  TRY(need_ptr(m.w_t1, "w_t1")); TRY(need_ptr(m.w_t2, "w_t2")); TRY(need_ptr(m.w_t6, "w_t6"));
+  TRY(need_ptr(m.w_x1, "w_x1")); TRY(need_ptr(m.w_x2, "w_x2")); TRY(need_ptr(m.w_patch, "w_patch"));
+  TRY(need_ptr(m.w_hv, "w_hv")); TRY(need_ptr(m.head_mod2, "head_mod2"));
+  if (io.A > 0) { TRY(need_ptr(m.w_ain, "w_ain")); TRY(need_ptr(m.w_ha, "w_ha")); }
+  if (D.n_layers > 0) {
+    CHECK(m.blocks != nullptr, WAM_EINVAL, "blocks is NULL");
+    CHECK(io.k_cache != nullptr && io.v_cache != nullptr, WAM_EINVAL, "k_cache/v_cache arrays are NULL");
+  }
+  for (int l = 0; l < D.n_layers; ++l) {
+    wam_status st = check_block_weights(m.blocks[l]);
+    if (st != WAM_OK) return fail(st, "block %d: %s", l, g_err.c_str());
+    CHECK(io.k_cache[l] && io.v_cache[l] && al16(io.k_cache[l]) && al16(io.v_cache[l]), WAM_EINVAL,
+          "k_cache/v_cache[%d] NULL or misaligned", l);
+    if (io.ctx_kv) {
+      CHECK(io.ctx_kv[l] && al16(io.ctx_kv[l]), WAM_EINVAL, "ctx_kv[%d] NULL or misaligned", l);
+    } else {
+      TRY(need_ptr(m.blocks[l].w_ckv, "w_ckv"));
+    }
+  }
+  return WAM_OK;
+}
+
+}  // namespace
+
+// =================================================================================
+// exported entry points
+// =================================================================================
+extern "C" {
+
+const char* wam_last_error(void) { return g_err.c_str(); }
+int32_t wam_abi_version(void) { return WAM_ABI_VERSION; }
+
+wam_status wam_attn_blockcausal(const wam_attn_desc* desc, const void* q, const void* k, const void* v, void* o,
+                                hipStream_t stream) {
+  CHECK(desc != nullptr, WAM_EINVAL, "desc is NULL");
+  return attn_checked(*desc, q, k, v, o, stream);
+}
+
+wam_status wam_gemm_bf16(const wam_gemm_desc* g, hipStream_t stream) {
+  CHECK(g != nullptr, WAM_EINVAL, "desc is NULL");
+  return gemm_checked(*g, stream);
+}
+
+wam_status wam_adaln_ln_mod(int32_t B, int32_t rows_per_batch, int32_t d, float eps, const float* x,
+                            const float* gamma, const float* beta, const float* shift_a, const float* shift_v,
+                            const float* scale_a, const float* scale_v, int64_t mod_stride, void* h,
+                            hipStream_t stream) {
+  CHECK(B >= 0 && rows_per_batch >= 0, WAM_EINVAL, "negative sizes");
+  CHECK(d % 256 == 0 && d >= 256 && d <= 8192, WAM_EUNSUPPORTED, "d=%d must be a multiple of 256 in [256, 8192]", d);
+  CHECK(eps > 0.f, WAM_EINVAL, "eps must be > 0");
+  if ((int64_t)B * rows_per_batch == 0) return WAM_OK;
+  CHECK((int64_t)B * rows_per_batch < (1ll << 31), WAM_EINVAL, "too many rows");
+  TRY(need_ptr(x, "x")); TRY(need_ptr(h, "h"));
+  TRY(opt_ptr(gamma, "gamma")); TRY(opt_ptr(beta, "beta"));
+  TRY(opt_ptr(shift_a, "shift_a")); TRY(opt_ptr(shift_v, "shift_v"));
+  TRY(opt_ptr(scale_a, "scale_a")); TRY(opt_ptr(scale_v, "scale_v"));
+  CHECK(mod_stride % 4 == 0, WAM_EINVAL, "mod_stride must be a multiple of 4");
+  LnArgs a{B * rows_per_batch, rows_per_batch, d, eps, x, gamma, beta, shift_a, shift_v, scale_a, scale_v,
+           mod_stride, h};
+  HIPCHECK(launch_ln_mod(a, stream));
+  return WAM_OK;
+}
+
+wam_status wam_rope_qkv(int32_t B, int32_t L, int32_t H, int32_t Dh, const void* qkv, const float* rope_cos,
+                        const float* rope_sin, void* q_out, void* k_cache, void* v_cache, int32_t Lcap,
+                        int32_t row0, hipStream_t stream) {
+  CHECK(Dh == 64 || Dh == 128, WAM_EUNSUPPORTED, "Dh=%d (supported: 64, 128)", Dh);
+  CHECK(B >= 0 && L >= 0 && H >= 1, WAM_EINVAL, "bad sizes B=%d L=%d H=%d", B, L, H);
+  CHECK(row0 >= 0 && (int64_t)row0 + L <= Lcap, WAM_EINVAL, "row0=%d + L=%d exceeds Lcap=%d", row0, L, Lcap);
+  if ((int64_t)B * L == 0) return WAM_OK;
+  TRY(need_ptr(qkv, "qkv")); TRY(need_ptr(rope_cos, "rope_cos")); TRY(need_ptr(rope_sin, "rope_sin"));
+  TRY(need_ptr(q_out, "q_out")); TRY(need_ptr(k_cache, "k_cache")); TRY(need_ptr(v_cache, "v_cache"));
+  RopeArgs a{B, L, H, Dh, Lcap, row0, qkv, rope_cos, rope_sin, q_out, k_cache, v_cache};
+  HIPCHECK(launch_rope_qkv(a, stream));
+  return WAM_OK;
+}
+
+size_t wam_block_workspace_bytes(const wam_dims* dims, int32_t B, int32_t L, int32_t Lc) {
+  if (!dims || B < 0 || L < 0 || Lc < 0) return 0;
+  return block_ws(*dims, B, L, Lc).total;
+}
+
+wam_status wam_dit_block_fwd(const wam_dims* dims, const wam_block_weights* w, const wam_block_io* io, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
+  CHECK(dims && w && io, WAM_EINVAL, "NULL dims/weights/io");
+  TRY(check_dims(*dims));
+  TRY(check_block_weights(*w));
+  TRY(check_block_io(*dims, *w, *io));
+  TRY(check_ws(ws, ws_bytes, block_ws(*dims, io->B, io->L, io->Lc).total));
+  return block_run(*dims, *w, *io, static_cast<char*>(ws), stream, nullptr, nullptr);
+}
+
+size_t wam_time_embed_workspace_bytes(const wam_dims* dims, int32_t B) {
+  if (!dims || B < 0) return 0;
+  return time_ws(*dims, B);
+}
+
+wam_status wam_time_embed_fwd(const wam_model* m, int32_t B, const float* t, float* e, float* e0, void* ws,
+                              size_t ws_bytes, hipStream_t stream) {
+  CHECK(m != nullptr, WAM_EINVAL, "model is NULL");
+  TRY(check_model_common(*m));
+  CHECK(B >= 1 && B <= 8, WAM_EUNSUPPORTED, "B=%d outside [1,8]", B);
+  TRY(need_ptr(t, "t")); TRY(need_ptr(e, "e")); TRY(need_ptr(e0, "e0"));
+  TRY(need_ptr(m->w_t1, "w_t1")); TRY(need_ptr(m->w_t2, "w_t2")); TRY(need_ptr(m->w_t6, "w_t6"));
+  TRY(check_ws(ws, ws_bytes, time_ws(m->dims, B)));
+  return time_run(*m, B, t, e, e0, static_cast<char*>(ws), stream);
+}
+
+size_t wam_text_proj_workspace_bytes(const wam_dims* dims, int32_t B, int32_t Lc) {
+  if (!dims || B < 0 || Lc < 0) return 0;
+  return text_ws(*dims, B, Lc);
+}
+
+wam_status wam_text_proj_fwd(const wam_model* m, int32_t B, int32_t Lc, const void* text, void* ctx, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
+  CHECK(m != nullptr, WAM_EINVAL, "model is NULL");
+  TRY(check_model_common(*m));
+  CHECK(B >= 1 && Lc >= 1, WAM_EINVAL, "B=%d Lc=%d", B, Lc);
+  TRY(need_ptr(text, "text")); TRY(need_ptr(ctx, "ctx"));
+  TRY(need_ptr(m->w_x1, "w_x1")); TRY(need_ptr(m->w_x2, "w_x2"));
+  TRY(check_ws(ws, ws_bytes, text_ws(m->dims, B, Lc)));
+  return text_run(*m, B, Lc, text, ctx, static_cast<char*>(ws), stream);
+}
+
+size_t wam_embed_workspace_bytes(const wam_dims* dims, int32_t B, int32_t F, int32_t Hl, int32_t Wl) {
+  if (!dims || B < 0 || F < 0 || Hl < 0 || Wl < 0) return 0;
+  return embed_ws(*dims, B, F, Hl, Wl);
+}
+
+wam_status wam_embed_fwd(const wam_model* m, int32_t B, int32_t F, int32_t Hl, int32_t Wl, int32_t A,
+                         const void* z_t, const void* a_t, float* x, void* ws, size_t ws_bytes,
+                         hipStream_t stream) {
+  CHECK(m != nullptr, WAM_EINVAL, "model is NULL");
+  TRY(check_model_common(*m));
+  CHECK(B >= 1 && F >= 1 && Hl >= 2 && Wl >= 2 && Hl % 2 == 0 && Wl % 2 == 0 && A >= 0, WAM_EINVAL,
+        "bad latent/action sizes");
+  TRY(need_ptr(z_t, "z_t")); TRY(need_ptr(x, "x")); TRY(need_ptr(m->w_patch, "w_patch"));
+  if (A > 0) { TRY(need_ptr(a_t, "a_t")); TRY(need_ptr(m->w_ain, "w_ain")); }
+  TRY(check_ws(ws, ws_bytes, embed_ws(m->dims, B, F, Hl, Wl)));
+  return embed_run(*m, B, F, Hl, Wl, A, z_t, a_t, x, static_cast<char*>(ws), stream);
+}
+
+size_t wam_head_workspace_bytes(const wam_dims* dims, int32_t B, int32_t F, int32_t Hl, int32_t Wl, int32_t A) {
+  if (!dims || B < 0 || F < 0 || Hl < 0 || Wl < 0 || A < 0) return 0;
+  return head_ws(*dims, B, F, Hl, Wl, A).total;
+}
+
+wam_status wam_head_fwd(const wam_model* m, int32_t B, int32_t F, int32_t Hl, int32_t Wl, int32_t A,
+                        const float* x, const float* e, float* v_video, float* v_action, void* ws,
+                        size_t ws_bytes, hipStream_t stream) {
+  CHECK(m != nullptr, WAM_EINVAL, "model is NULL");
+  TRY(check_model_common(*m));
+  CHECK(B >= 1 && B <= 8 && F >= 1 && Hl >= 2 && Wl >= 2 && Hl % 2 == 0 && Wl % 2 == 0 && A >= 0, WAM_EINVAL,
+        "bad latent/action sizes");
+  TRY(need_ptr(x, "x")); TRY(need_ptr(e, "e")); TRY(need_ptr(v_video, "v_video"));
+  TRY(need_ptr(m->w_hv, "w_hv")); TRY(need_ptr(m->head_mod2, "head_mod2"));
+  if (A > 0) { TRY(need_ptr(v_action, "v_action")); TRY(need_ptr(m->w_ha, "w_ha")); }
+  TRY(check_ws(ws, ws_bytes, head_ws(m->dims, B, F, Hl, Wl, A).total));
+  return head_run(*m, B, F, Hl, Wl, A, x, e, v_video, v_action, static_cast<char*>(ws), stream);
+}
+
+size_t wam_step_workspace_bytes(const wam_model* m, const wam_step_io* io) {
+  if (!m || !io || io->B < 0 || io->F < 0 || io->Hl < 0 || io->Wl < 0 || io->A < 0 || io->Lc < 0) return 0;
+  return step_ws(*m, *io).total;
+}
+
+wam_status wam_dit_step_fwd(const wam_model* m, const wam_step_io* io, void* ws, size_t ws_bytes,
+                            hipStream_t stream) {
+  CHECK(m && io, WAM_EINVAL, "NULL model/io");
+  TRY(check_step(*m, *io));
+  const StepWs lay = step_ws(*m, *io);
+  TRY(check_ws(ws, ws_bytes, lay.total));
+  const wam_dims& D = m->dims;
+  char* w = static_cast<char*>(ws);
+  float* x = reinterpret_cast<float*>(w + lay.x);
+  float* e = reinterpret_cast<float*>(w + lay.e);
+  float* e0 = reinterpret_cast<float*>(w + lay.e0);
+  void* ctx = w + lay.ctx;
+  char* piece = w + lay.piece;
+  const int32_t Lv = io->F * (io->Hl / 2) * (io->Wl / 2), L = Lv + io->A;
+
+  TRY(time_run(*m, io->B, io->t, e, e0, piece, stream));
+  if (!io->ctx_kv) TRY(text_run(*m, io->B, io->Lc, io->text, ctx, piece, stream));
+  TRY(embed_run(*m, io->B, io->F, io->Hl, io->Wl, io->A, io->z_t, io->a_t, x, piece, stream));
+  for (int l = 0; l < D.n_layers; ++l) {
+    wam_block_io b{};
+    b.x = x; b.e0 = e0; b.rope_cos = io->rope_cos; b.rope_sin = io->rope_sin;
+    b.k_cache = io->k_cache[l]; b.v_cache = io->v_cache[l]; b.Lcap = io->Lcap; b.cache_len = io->cache_len;
+    b.ch = io->ch; b.ctx = ctx; b.ctx_kv = io->ctx_kv ? io->ctx_kv[l] : nullptr;
+    b.B = io->B; b.L = L; b.Lc = io->Lc;
+    hipEvent_t ev0 = io->attn_events ? io->attn_events[2 * l] : nullptr;
+    hipEvent_t ev1 = io->attn_events ? io->attn_events[2 * l + 1] : nullptr;
+    TRY(block_run(D, m->blocks[l], b, w + lay.block, stream, ev0, ev1));
+  }
+  TRY(head_run(*m, io->B, io->F, io->Hl, io->Wl, io->A, x, e, io->v_video, io->v_action, piece, stream));
+  return WAM_OK;
+}
+
+wam_status wam_chunk_positions(int32_t c, int32_t F, int32_t Hg, int32_t Wg, int32_t A, int32_t* pos) {
+  CHECK(pos != nullptr, WAM_EINVAL, "pos is NULL");
+  CHECK(c >= 0 && F >= 1 && Hg >= 1 && Wg >= 1 && A >= 0, WAM_EINVAL, "bad chunk geometry");
+  int64_t i = 0;
+  for (int f = 0; f < F; ++f)
+    for (int r = 0; r < Hg; ++r)
+      for (int s = 0; s < Wg; ++s, ++i) {
+        pos[3 * i + 0] = F * c + f;
+        pos[3 * i + 1] = r;
+        pos[3 * i + 2] = s;
+      }
+  for (int j = 0; j < A; ++j, ++i) {
+    pos[3 * i + 0] = F * c + F + j;
+    pos[3 * i + 1] = 0;
+    pos[3 * i + 2] = 0;
+  }
+  return WAM_OK;
+}
+
+wam_status wam_rope_tables(const int32_t* pos, int32_t L, int32_t Dh, double theta, float* cos_out,
+                           float* sin_out) {
+  CHECK(pos && cos_out && sin_out, WAM_EINVAL, "NULL pointer");
+  CHECK(L >= 0 && Dh >= 6 && Dh % 2 == 0, WAM_EINVAL, "bad L=%d or Dh=%d", L, Dh);
+  CHECK(theta > 0.0, WAM_EINVAL, "theta must be > 0");
+  const int a = Dh / 6;
+  const int seg[3] = {Dh - 4 * a, 2 * a, 2 * a};
+  for (int64_t l = 0; l < L; ++l) {
+    int p = 0;
+    for (int ax = 0; ax < 3; ++ax)
+      for (int i = 0; i < seg[ax] / 2; ++i, ++p) {
+        const double ang = (double)pos[3 * l + ax] * std::pow(theta, -2.0 * i / seg[ax]);
+        cos_out[l * (Dh / 2) + p] = (float)std::cos(ang);
+        sin_out[l * (Dh / 2) + p] = (float)std::sin(ang);
+      }
+  }
+  return WAM_OK;
+}
+
+}  // extern "C"

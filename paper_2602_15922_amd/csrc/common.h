@@ -1,0 +1,44 @@
+// Shared device-side definitions for the gfx950 kernels of libwamdit.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+#define WAM_DEV __device__ __forceinline__
+
+// 32x32x16 bf16 MFMA (gfx950).  Lane l, half h = l/32:
+//   A operand: A[m = l%32][k = 8h .. 8h+7]      (8 consecutive k of one row)
+//   B operand: B[k = 8h .. 8h+7][n = l%32]      (8 consecutive k of one column)
+//   C/D:       register r holds D[m = 8*(r/4) + 4h + r%4][n = l%32]
+WAM_DEV f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+WAM_DEV float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+WAM_DEV bf16x8 load_bf16x8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
+
+WAM_DEV float gelu_tanh_f(float u) {
+  // 0.5 u (1 + tanh(sqrt(2/pi) (u + 0.044715 u^3))), tanh(y) = 1 - 2/(exp(2y)+1)
+  const float k0 = 0.7978845608028654f, k1 = 0.044715f;
+  float y = k0 * (u + k1 * u * u * u);
+  float t = 1.0f - 2.0f / (__expf(2.0f * y) + 1.0f);
+  return 0.5f * u * (1.0f + t);
+}
+
+WAM_DEV float silu_f(float u) { return u / (1.0f + __expf(-u)); }
+
+// 64-lane wavefront reductions
+WAM_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}

@@ -1,0 +1,226 @@
+// HBM-bound and small kernels of the DiT step for gfx950: AdaLN LayerNorm+modulate,
+// 3D RoPE with KV-cache append, time-embedding GEMV and sinusoid, patchify and
+// unpatchify.  All loads and stores are 16-byte vectors over contiguous rows.
+#include "common.h"
+#include "kernels.h"
+
+namespace wam {
+namespace {
+
+// ---------------------------------------------------------------------------------
+// LayerNorm (biased variance, eps) of fp32 rows -> optional affine -> AdaLN
+// modulation -> bf16.  One wavefront per row; the row stays in registers between the
+// mean pass, the variance pass and the output pass, so x is read from HBM once.
+// ---------------------------------------------------------------------------------
+constexpr int LN_MAXV = 32;  // d <= 32 * 256
+
+__global__ __launch_bounds__(256) void ln_mod_kernel(const LnArgs a) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + w;
+  if (row >= a.rows) return;
+  const int b = row / a.rows_per_batch;
+  const int nv = a.d >> 8;
+  const float* xr = a.x + (int64_t)row * a.d;
+  f32x4 v[LN_MAXV];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < LN_MAXV; ++i)
+    if (i < nv) {
+      v[i] = *reinterpret_cast<const f32x4*>(xr + (i * 64 + lane) * 4);
+      s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
+    }
+  const float mean = wave_sum(s) / (float)a.d;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < LN_MAXV; ++i)
+    if (i < nv) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float t = v[i][j] - mean;
+        q += t * t;
+      }
+    }
+  const float var = wave_sum(q) / (float)a.d;
+  const float rstd = rsqrtf(var + a.eps);
+  const int64_t mb = (int64_t)b * a.mod_stride;
+  bf16* hr = static_cast<bf16*>(a.h) + (int64_t)row * a.d;
+#pragma unroll
+  for (int i = 0; i < LN_MAXV; ++i)
+    if (i < nv) {
+      const int col = (i * 64 + lane) * 4;
+      f32x4 y;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) y[j] = (v[i][j] - mean) * rstd;
+      if (a.gamma) y *= *reinterpret_cast<const f32x4*>(a.gamma + col);
+      if (a.beta) y += *reinterpret_cast<const f32x4*>(a.beta + col);
+      f32x4 sc = {0.f, 0.f, 0.f, 0.f}, sh = {0.f, 0.f, 0.f, 0.f};
+      if (a.scale_a) sc += *reinterpret_cast<const f32x4*>(a.scale_a + col);
+      if (a.scale_v) sc += *reinterpret_cast<const f32x4*>(a.scale_v + mb + col);
+      if (a.shift_a) sh += *reinterpret_cast<const f32x4*>(a.shift_a + col);
+      if (a.shift_v) sh += *reinterpret_cast<const f32x4*>(a.shift_v + mb + col);
+      bf16x4 o;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[j] = (bf16)(y[j] * (1.f + sc[j]) + sh[j]);
+      *reinterpret_cast<bf16x4*>(hr + col) = o;
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// 3D RoPE + KV append.  A thread owns 8 consecutive dims (4 rotation pairs) of one
+// head of one token and moves the q, k and v slices of the fused QKV row: q rotated
+// to q_out, k rotated and v copied into the cache rows [row0, row0 + L).
+// ---------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void rope_qkv_kernel(const RopeArgs a) {
+  const int d = a.H * a.Dh, d8 = d >> 3;
+  const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (id >= (int64_t)a.B * a.L * d8) return;
+  const int c = (int)(id % d8);
+  const int64_t bl = id / d8;
+  const int l = (int)(bl % a.L), b = (int)(bl / a.L);
+  const int col = c * 8;            // column inside the d-wide q/k/v slice
+  const int pair0 = (col % a.Dh) >> 1;  // first rotation pair inside the head
+  const bf16* src = static_cast<const bf16*>(a.qkv) + bl * 3 * d + col;
+  const bf16x8 qv = load_bf16x8(src), kv = load_bf16x8(src + d), vv = load_bf16x8(src + 2 * d);
+  const f32x4 cs = *reinterpret_cast<const f32x4*>(a.cos_t + (int64_t)l * (a.Dh >> 1) + pair0);
+  const f32x4 sn = *reinterpret_cast<const f32x4*>(a.sin_t + (int64_t)l * (a.Dh >> 1) + pair0);
+  bf16x8 qo, ko;
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const float q0 = (float)qv[2 * p], q1 = (float)qv[2 * p + 1];
+    const float k0 = (float)kv[2 * p], k1 = (float)kv[2 * p + 1];
+    qo[2 * p] = (bf16)(q0 * cs[p] - q1 * sn[p]);
+    qo[2 * p + 1] = (bf16)(q0 * sn[p] + q1 * cs[p]);
+    ko[2 * p] = (bf16)(k0 * cs[p] - k1 * sn[p]);
+    ko[2 * p + 1] = (bf16)(k0 * sn[p] + k1 * cs[p]);
+  }
+  *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.q_out) + bl * d + col) = qo;
+  const int64_t crow = ((int64_t)b * a.Lcap + a.row0 + l) * d + col;
+  *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.k_cache) + crow) = ko;
+  *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.v_cache) + crow) = vv;
+}
+
+// ---------------------------------------------------------------------------------
+// Small-batch GEMV for the time MLP: one wavefront per output feature n computes it
+// for every sample b (B <= 8); W row read once with 16-byte loads.
+// ---------------------------------------------------------------------------------
+constexpr int GEMV_MAXB = 8;
+
+__global__ __launch_bounds__(256) void gemv_kernel(int B, int N, int K, const float* __restrict__ x,
+                                                   int act, const bf16* __restrict__ W,
+                                                   const float* __restrict__ bias, float* __restrict__ out) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int n = blockIdx.x * 4 + w;
+  if (n >= N) return;
+  float acc[GEMV_MAXB];
+#pragma unroll
+  for (int b = 0; b < GEMV_MAXB; ++b) acc[b] = 0.f;
+  const bf16* wr = W + (int64_t)n * K;
+  for (int k0 = lane * 8; k0 < K; k0 += 512) {
+    const bf16x8 wv = load_bf16x8(wr + k0);
+#pragma unroll
+    for (int b = 0; b < GEMV_MAXB; ++b)
+      if (b < B) {
+        const float* xb = x + (int64_t)b * K + k0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          float xv = xb[j];
+          if (act == GEMV_ACT_SILU) xv = silu_f(xv);
+          acc[b] += xv * (float)wv[j];
+        }
+      }
+  }
+#pragma unroll
+  for (int b = 0; b < GEMV_MAXB; ++b)
+    if (b < B) {
+      const float s = wave_sum(acc[b]);
+      if (lane == 0) out[(int64_t)b * N + n] = s + (bias ? bias[n] : 0.f);
+    }
+}
+
+// [cos(1000 t w_k), sin(1000 t w_k)], w_k = 10000^(-k/half); evaluated in double so the
+// large arguments (up to 1000 rad) keep full fp32 accuracy.
+__global__ void sinusoid_kernel(int B, int fd, const float* t, float* out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= B * fd) return;
+  const int b = i / fd, k = i % fd, half = fd / 2;
+  const int kk = k < half ? k : k - half;
+  const double omega = pow(10000.0, -(double)kk / (double)half);
+  const double arg = 1000.0 * (double)t[b] * omega;
+  out[i] = (float)(k < half ? cos(arg) : sin(arg));
+}
+
+// token (f, r, s) feature (c, ph, pw) <- z[b][c][f][2r+ph][2s+pw]
+__global__ void patchify_kernel(int B, int C, int F, int Hl, int Wl, const bf16* z, bf16* tok) {
+  const int Hg = Hl / 2, Wg = Wl / 2, P = C * 4;
+  const int64_t n = (int64_t)B * F * Hg * Wg * P;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int fe = (int)(i % P);
+  int64_t t = i / P;
+  const int s = (int)(t % Wg); t /= Wg;
+  const int r = (int)(t % Hg); t /= Hg;
+  const int f = (int)(t % F);
+  const int b = (int)(t / F);
+  const int c = fe / 4, ph = (fe / 2) & 1, pw = fe & 1;
+  tok[i] = z[((((int64_t)b * C + c) * F + f) * Hl + 2 * r + ph) * Wl + 2 * s + pw];
+}
+
+__global__ void unpatchify_kernel(int B, int C, int F, int Hl, int Wl, const float* tok, float* out) {
+  const int Hg = Hl / 2, Wg = Wl / 2;
+  const int64_t n = (int64_t)B * C * F * Hl * Wl;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  int64_t t = i;
+  const int xw = (int)(t % Wl); t /= Wl;
+  const int y = (int)(t % Hl); t /= Hl;
+  const int f = (int)(t % F); t /= F;
+  const int c = (int)(t % C);
+  const int b = (int)(t / C);
+  const int64_t token = ((int64_t)b * F + f) * Hg * Wg + (y / 2) * Wg + xw / 2;
+  out[i] = tok[token * (C * 4) + c * 4 + (y & 1) * 2 + (xw & 1)];
+}
+
+}  // namespace
+
+hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s) {
+  if (a.rows == 0) return hipSuccess;
+  hipLaunchKernelGGL(ln_mod_kernel, dim3((a.rows + 3) / 4), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_qkv(const RopeArgs& a, hipStream_t s) {
+  const int64_t n = (int64_t)a.B * a.L * (a.H * a.Dh / 8);
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_qkv_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv(int32_t B, int32_t N, int32_t K, const float* x, int32_t act, const void* W,
+                       const float* bias, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(gemv_kernel, dim3((N + 3) / 4), dim3(256), 0, s, B, N, K, x, act,
+                     static_cast<const bf16*>(W), bias, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_sinusoid(int32_t B, int32_t fd, const float* t, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(sinusoid_kernel, dim3((B * fd + 255) / 256), dim3(256), 0, s, B, fd, t, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_patchify(int32_t B, int32_t C, int32_t F, int32_t Hl, int32_t Wl, const void* z,
+                           void* tok, hipStream_t s) {
+  const int64_t n = (int64_t)B * F * (Hl / 2) * (Wl / 2) * C * 4;
+  hipLaunchKernelGGL(patchify_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, B, C, F,
+                     Hl, Wl, static_cast<const bf16*>(z), static_cast<bf16*>(tok));
+  return hipGetLastError();
+}
+
+hipError_t launch_unpatchify(int32_t B, int32_t C, int32_t F, int32_t Hl, int32_t Wl, const float* tok,
+                             float* out, hipStream_t s) {
+  const int64_t n = (int64_t)B * C * F * Hl * Wl;
+  hipLaunchKernelGGL(unpatchify_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, B, C, F,
+                     Hl, Wl, tok, out);
+  return hipGetLastError();
+}
+
+}  // namespace wam

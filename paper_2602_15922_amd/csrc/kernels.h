@@ -1,0 +1,74 @@
+// Internal launchers of the gfx950 kernels.  Arguments are validated by the C-ABI
+// layer (capi.hip) before any of these is called; the launchers assume valid input.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/wamdit.h"
+
+namespace wam {
+
+struct AttnArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  int64_t q_ts, q_bs, kv_ts, kv_bs, o_ts, o_bs;
+  int32_t B, H, Dh, Lq, Lk;
+  float c;  // softmax scale * log2(e)
+  int32_t n_q_chunks;
+  int32_t q_off[WAM_MAX_CHUNKS + 1];
+  int32_t kend[WAM_MAX_CHUNKS];  // visible key prefix [0, kend) of each query chunk
+};
+hipError_t launch_attn(const AttnArgs& a, hipStream_t s);
+
+struct GemmArgs {
+  int32_t M, N, K, epi;
+  const void* A;
+  int64_t lda, a_bs;
+  int32_t a_rows;
+  const void* W;
+  int64_t ldw;
+  const float* bias;
+  void* out;
+  int64_t ldo, o_bs;
+  int32_t o_rows;
+  const float* gate_a;
+  const float* gate_v;
+  int64_t gate_stride;
+  int32_t gate_rows;
+};
+hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
+
+struct LnArgs {
+  int32_t rows, rows_per_batch, d;
+  float eps;
+  const float* x;
+  const float *gamma, *beta, *shift_a, *shift_v, *scale_a, *scale_v;
+  int64_t mod_stride;
+  void* h;
+};
+hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s);
+
+struct RopeArgs {
+  int32_t B, L, H, Dh, Lcap, row0;
+  const void* qkv;
+  const float *cos_t, *sin_t;
+  void *q_out, *k_cache, *v_cache;
+};
+hipError_t launch_rope_qkv(const RopeArgs& a, hipStream_t s);
+
+// out[b][n] = act(x[b][:]) . W[n][:] + bias[n]  (fp32 in/out, bf16 W [N][K])
+enum { GEMV_ACT_NONE = 0, GEMV_ACT_SILU = 1 };
+hipError_t launch_gemv(int32_t B, int32_t N, int32_t K, const float* x, int32_t act,
+                       const void* W, const float* bias, float* out, hipStream_t s);
+// [B][freq_dim] sinusoid of 1000*t
+hipError_t launch_sinusoid(int32_t B, int32_t freq_dim, const float* t, float* out, hipStream_t s);
+// latent [B][C][F][Hl][Wl] bf16 -> tokens [B][F*Hg*Wg][C*4] bf16
+hipError_t launch_patchify(int32_t B, int32_t C, int32_t F, int32_t Hl, int32_t Wl,
+                           const void* z, void* tok, hipStream_t s);
+// tokens [B][Lv][C*4] fp32 -> video [B][C][F][Hl][Wl] fp32
+hipError_t launch_unpatchify(int32_t B, int32_t C, int32_t F, int32_t Hl, int32_t Wl,
+                             const float* tok, float* out, hipStream_t s);
+
+}  // namespace wam

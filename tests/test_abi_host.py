@@ -1,0 +1,117 @@
+"""Host-only checks of the C ABI (no GPU needed): the library loads, exports every
+symbol the header declares, and rejects bad arguments with a status and a message
+before touching the GPU."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def lib():
+    import paper_2602_15922_amd as w
+    return w
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "wamdit.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(wam_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    w = lib()
+    declared = header_functions()
+    assert len(declared) >= 20
+    L = w.lib()
+    for name in declared:
+        assert hasattr(L, name), name
+    assert sorted(w.binding.EXPORTED) == declared
+    assert w.wam_abi_version() == 1
+
+
+def test_struct_sizes_match_the_header_layout():
+    w = lib()
+    b = w.binding
+    assert C.sizeof(b.wam_chunks) == 4 * (1 + 17 + 1 + 17 + 16)
+    assert C.sizeof(b.wam_dims) == 10 * 4
+    assert C.sizeof(b.wam_block_weights) == 17 * 8
+
+
+def _status(fn, *args):
+    return fn(*args)
+
+
+def test_attention_rejects_bad_arguments_without_a_gpu():
+    w = lib()
+    b = w.binding
+    L = w.lib()
+
+    def call(**kw):
+        d = b.wam_attn_desc(B=1, H=2, Dh=128, Lq=10, Lk=20, q_tok_stride=256, q_batch_stride=2560,
+                            kv_tok_stride=256, kv_batch_stride=5120, o_tok_stride=256, o_batch_stride=2560,
+                            scale=0.0, ch=w.make_chunks([10, 10], [10], [1]))
+        ptrs = dict(q=4096, k=8192, v=12288, o=16384)
+        for k_, v_ in kw.items():
+            if k_ in ptrs:
+                ptrs[k_] = v_
+            elif k_ == "ch":
+                d.ch = v_
+            else:
+                setattr(d, k_, v_)
+        return L.wam_attn_blockcausal(C.byref(d), ptrs["q"], ptrs["k"], ptrs["v"], ptrs["o"], None)
+
+    assert call(Dh=96) == b.WAM_EUNSUPPORTED
+    assert call(q=0) == b.WAM_EINVAL and b"q is NULL" in L.wam_last_error()
+    assert call(k=8200) == b.WAM_EINVAL and b"aligned" in L.wam_last_error()
+    assert call(q_tok_stride=100) == b.WAM_EINVAL
+    assert call(Lk=21) == b.WAM_EINVAL  # chunks do not cover Lk
+    assert call(ch=w.make_chunks([10, 10], [10], [2])) == b.WAM_EINVAL  # chunk id out of range
+    assert call(ch=w.make_chunks([0, 20], [10], [0])) == b.WAM_EINVAL  # sees no key
+    assert call(ch=w.make_chunks([10, 10], [5, 5], [1, 0])) == b.WAM_EINVAL  # ids decreasing
+    assert call(B=-1) == b.WAM_EINVAL
+    # nothing to do is not an error, and needs no valid pointers
+    assert call(Lq=0, ch=w.make_chunks([10, 10], [0], [1]), q=0, o=0) == b.WAM_OK
+
+
+def test_gemm_and_block_reject_bad_arguments():
+    w = lib()
+    b = w.binding
+    L = w.lib()
+    g = b.wam_gemm_desc(M=10, N=10, K=12, epilogue=0, A=4096, lda=16, W=8192, ldw=16, out=16384, ldo=10)
+    assert L.wam_gemm_bf16(C.byref(g), None) == b.WAM_EINVAL  # K % 8
+    g.K = 16
+    g.epilogue = 9
+    assert L.wam_gemm_bf16(C.byref(g), None) == b.WAM_EINVAL
+    dims = w.make_dims(d=512, H=8, Dh=64, ffn=2048, n_layers=1)
+    wts = b.wam_block_weights()
+    io = b.wam_block_io(B=1, L=10, Lc=4, Lcap=8, cache_len=0, ch=w.cached_chunks(0, 10))
+    assert L.wam_dit_block_fwd(C.byref(dims), C.byref(wts), C.byref(io), None, 0, None) == b.WAM_EINVAL
+    bad = w.make_dims(d=500, H=5, Dh=100, ffn=2048, n_layers=1)
+    assert L.wam_dit_block_fwd(C.byref(bad), C.byref(wts), C.byref(io), None, 0, None) == b.WAM_EUNSUPPORTED
+    assert L.wam_block_workspace_bytes(C.byref(dims), 1, 144, 32) > 0
+
+
+def test_rope_tables_and_positions_agree_with_the_oracle():
+    w = lib()
+    for Dh, (c, F, Hg, Wg, A) in [(128, (3, 2, 30, 52, 32)), (64, (0, 2, 8, 8, 16))]:
+        pos = w.wam_chunk_positions(c, F, Hg, Wg, A)
+        assert np.array_equal(pos, oracle.chunk_positions(c, F, Hg, Wg, A))
+        cos, sin = w.wam_rope_tables(pos, Dh)
+        phi = oracle.rope_angles(pos, Dh)
+        # double-precision tables rounded to fp32: within one fp32 ulp of 1
+        assert np.max(np.abs(cos - np.cos(phi))) <= 1.2e-7
+        assert np.max(np.abs(sin - np.sin(phi))) <= 1.2e-7
+
+
+def test_loader_fails_loudly_without_the_library(monkeypatch, tmp_path):
+    w = lib()
+    monkeypatch.setattr(w.binding, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(w.binding, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        w.binding.lib()
