@@ -1,0 +1,191 @@
+"""Throughput of one DiT denoising step on one MI355X, through libwamdit's C ABI.
+
+Workload (the 14B-class step): 40 blocks, d=5120, 40 heads of 128, FFN 13824; one chunk of
+2 latent frames x 30x52 patches (3120 video tokens) + 32 action tokens; 4 cached chunks per
+layer (12608 rows; 15760 keys per query); 512 text tokens of width 4096.  Weights are
+random bf16 N(0, 0.02^2), ~28 GB resident; inputs are synthetic Gaussians of the paper's
+shapes (no trained weights or datasets exist here).  A step is the whole velocity call:
+time embedding, text projection, patch/action embedding, 40 blocks (each recomputing its
+cross-attention K/V of the text) and the output head.
+
+Prints one JSON line: steps/s, plus the self-attention kernel's achieved bf16 TFLOP/s
+against the MFMA peak (per-launch durations from HIP events recorded around every
+self-attention launch inside the timed steps), and the fp64 oracle timed on the host
+cores on a bounded sample (one full-shape block), scaled to steps/s.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MI355X_BF16_DENSE_TFLOPS = 2500.0  # published dense bf16 MFMA peak
+WORKLOAD = "step_14b"
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--workload", default=WORKLOAD)
+    return p.parse_args()
+
+
+def build_model(wl, torch):
+    import paper_2602_15922_amd as w
+    d, dev = wl.d, "cuda"
+    g = torch.Generator(device=dev).manual_seed(1234)
+
+    def rn(*shape, std=0.02):
+        t = torch.randn(*shape, generator=g, device=dev, dtype=torch.bfloat16)
+        return t.mul_(std) if std != 1.0 else t
+
+    def zf(n):
+        return torch.zeros(n, dtype=torch.float32, device=dev)
+
+    top = {"w_t1": rn(d, wl.freq_dim), "w_t2": rn(d, d), "w_t6": rn(6 * d, d), "w_x1": rn(d, wl.text_dim),
+           "w_x2": rn(d, d), "w_patch": rn(d, wl.patch_dim), "w_ain": rn(d, wl.act_dim),
+           "w_hv": rn(wl.patch_dim, d), "w_ha": rn(wl.act_dim, d),
+           "head_mod2": torch.randn(2, d, generator=g, device=dev) * 0.02}
+    for n, k in (("b_t1", d), ("b_t2", d), ("b_t6", 6 * d), ("b_x1", d), ("b_x2", d), ("b_patch", d),
+                 ("b_ain", d), ("b_hv", wl.patch_dim), ("b_ha", wl.act_dim)):
+        top[n] = zf(k)
+    blocks, kcs, vcs = [], [], []
+    for _ in range(wl.n_layers):
+        b = {"w_qkv": rn(3 * d, d), "w_o": rn(d, d), "w_cq": rn(d, d), "w_ckv": rn(2 * d, d), "w_co": rn(d, d),
+             "w_f1": rn(wl.ffn, d), "w_f2": rn(d, wl.ffn),
+             "mod6": torch.randn(6, d, generator=g, device=dev) * 0.02,
+             "lnc_gamma": torch.ones(d, device=dev), "lnc_beta": zf(d)}
+        for n, k in (("b_qkv", 3 * d), ("b_o", d), ("b_cq", d), ("b_ckv", 2 * d), ("b_co", d),
+                     ("b_f1", wl.ffn), ("b_f2", d)):
+            b[n] = zf(k)
+        blocks.append(b)
+        kcs.append(rn(wl.B, wl.Lcap, wl.H, wl.Dh, std=1.0))
+        vcs.append(rn(wl.B, wl.Lcap, wl.H, wl.Dh, std=1.0))
+    dims = w.make_dims(d, wl.H, wl.Dh, wl.ffn, wl.n_layers, wl.latent_ch, wl.act_dim, wl.text_dim,
+                       wl.freq_dim, wl.eps)
+    model = w.make_model(dims, top, blocks)
+    inputs = {
+        "z": rn(wl.B, wl.latent_ch, wl.F, wl.Hl, wl.Wl, std=1.0),
+        "a": rn(wl.B, wl.A, wl.act_dim, std=1.0),
+        "t": torch.rand(wl.B, generator=g, device=dev),
+        "text": rn(wl.B, wl.Lc, wl.text_dim, std=1.0),
+    }
+    pos = w.wam_chunk_positions(wl.n_cached, wl.F, wl.Hg, wl.Wg, wl.A)
+    cos, sin = w.wam_rope_tables(pos, wl.Dh)
+    inputs["cos"] = torch.from_numpy(cos).to(dev)
+    inputs["sin"] = torch.from_numpy(sin).to(dev)
+    return model, (top, blocks), kcs, vcs, inputs
+
+
+def cpu_baseline(wl):
+    """The fp64 oracle on one full-shape block of the workload (a 1/40 sample of the
+    step's blocks), scaled to steps/s; inputs come from the seeded generators."""
+    import numpy as np
+    import oracle
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    W = {k: v.f64 for k, v in synth.block_params(wl, 0).items()}
+    kc, vc = synth.kv_cache(wl, 0)
+    x = synth.normal(wl.seed, "x", (wl.B, wl.L, wl.d), 1.0, dtype="f32").f64
+    e0 = synth.normal(wl.seed, "e0", (wl.B, 6, wl.d), 0.02, dtype="f32").f64
+    ctx = synth.normal(wl.seed, "ctx", (wl.B, wl.Lc, wl.d), 1.0).f64
+    pos = oracle.chunk_positions(wl.n_cached, wl.F, wl.Hg, wl.Wg, wl.A)
+    t0 = time.perf_counter()
+    oracle.dit_block(x, e0, W, wl.H, wl.eps, pos, np.full(wl.L, wl.n_cached), kc.f64, vc.f64,
+                     np.repeat(np.arange(wl.n_cached), wl.L), ctx=ctx)
+    dt = time.perf_counter() - t0
+    step_s = dt * wl.n_layers
+    return {"value": 1.0 / step_s, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"one full-shape block ({dt:.1f} s fp64 numpy, {threads} BLAS threads), "
+                      f"x{wl.n_layers} blocks; embeddings and head not timed"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build runs on one GPU only (no sharding or collectives); "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import synth
+    import paper_2602_15922_amd as w
+
+    wl = synth.WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    model, keep, kcs, vcs, inp = build_model(wl, torch)
+    B, d = wl.B, wl.d
+    vv = torch.empty((B, wl.latent_ch, wl.F, wl.Hl, wl.Wl), dtype=torch.float32, device="cuda")
+    va = torch.empty((B, wl.A, wl.act_dim), dtype=torch.float32, device="cuda")
+    chunks = w.cached_chunks(wl.cache_rows, wl.L)
+    n_ev = 2 * wl.n_layers
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(args.steps)]
+    ios = [w.make_step_io(inp["z"], inp["a"], inp["t"], inp["text"], kcs, vcs, inp["cos"], inp["sin"],
+                          wl.cache_rows, chunks, vv, va, events=events[i]) for i in range(args.steps)]
+    io_plain = w.make_step_io(inp["z"], inp["a"], inp["t"], inp["text"], kcs, vcs, inp["cos"], inp["sin"],
+                              wl.cache_rows, chunks, vv, va)
+    ws = torch.empty(w.wam_step_workspace_bytes(model, io_plain), dtype=torch.uint8, device="cuda")
+
+    for _ in range(args.warmup):
+        w.wam_dit_step_fwd(model, io_plain, ws)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for i in range(args.steps):
+        w.wam_dit_step_fwd(model, ios[i], ws)
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = start.elapsed_time(stop) / args.steps
+    assert torch.isfinite(vv).all() and torch.isfinite(va).all()
+
+    attn_ms = [events[i][2 * l].elapsed_time(events[i][2 * l + 1])
+               for i in range(args.steps) for l in range(wl.n_layers)]
+    attn_avg = sum(attn_ms) / len(attn_ms)
+    attn_flop = 4.0 * wl.H * wl.Dh * wl.B * wl.L * wl.Lk  # visible (q, k) pairs x 4 Dh
+    attn_tflops = attn_flop / (attn_avg * 1e-3) / 1e12
+    step_flop = wl.step_flops()
+
+    rec = {
+        "metric": "DiT denoising steps/sec (14B-class chunk); attention TFLOP/s as % bf16 MFMA peak",
+        "value": round(1000.0 / ms, 4),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic Gaussians of the workload's shapes; random-init bf16 weights",
+        "config": {"workload": f"{wl.name}: {wl.n_layers} blocks, d={d}, {wl.H}x{wl.Dh} heads, FFN {wl.ffn}, "
+                               f"chunk {wl.Lv}+{wl.A} tokens, {wl.n_cached} cached chunks (Lk {wl.Lk}), "
+                               f"text {wl.Lc}x{wl.text_dim}, batch {B}",
+                   "global_batch": B, "seq_len": wl.L, "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "mfma", "kernel": "attn_fwd (block-causal self-attention)",
+                     "achieved": round(attn_tflops, 1), "peak": MI355X_BF16_DENSE_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(attn_tflops / MI355X_BF16_DENSE_TFLOPS, 4), "traffic": None,
+                     "avg_launch_ms": round(attn_avg, 4), "flop_per_launch": attn_flop},
+        "step_tflops": round(step_flop / (ms * 1e-3) / 1e12, 1),
+        "step_mfma_frac": round(step_flop / (ms * 1e-3) / 1e12 / MI355X_BF16_DENSE_TFLOPS, 4),
+        "wall_s_timed": round(wall, 3),
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -341,6 +341,10 @@ def make_step_io(z_t, a_t, t, text, k_caches, v_caches, rope_cos, rope_sin, cach
         io.ctx_kv = C.cast(ck, C.POINTER(_vp))
         keep.append(ck)
     if events is not None:
+        # torch's Event.elapsed_time() only reads events torch has seen recorded; record
+        # each once here so the library's later hipEventRecord on them can be read back.
+        for e in events:
+            e.record()
         ev = (_vp * len(events))(*[e.cuda_event for e in events])
         io.attn_events = C.cast(ev, C.POINTER(_vp))
         keep.append(ev)

@@ -154,6 +154,11 @@ wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s) {
   CHECK(g.ldo >= g.N, WAM_EINVAL, "ldo < N");
   CHECK(g.a_rows >= 0 && g.out_rows >= 0 && g.gate_rows >= 0, WAM_EINVAL, "negative row groups");
   CHECK(g.a_batch_stride % 8 == 0, WAM_EINVAL, "a_batch_stride must be a multiple of 8");
+  CHECK(g.ldo % 4 == 0 && g.out_batch_stride % 4 == 0 && g.gate_stride % 4 == 0, WAM_EINVAL,
+        "ldo, out_batch_stride and gate_stride must be multiples of 4");
+  TRY(opt_ptr(g.bias, "bias"));
+  TRY(opt_ptr(g.gate_a, "gate_a"));
+  TRY(opt_ptr(g.gate_v, "gate_v"));
   GemmArgs a{};
   a.M = g.M; a.N = g.N; a.K = g.K; a.epi = g.epilogue;
   a.A = g.A; a.lda = g.lda; a.a_bs = g.a_batch_stride; a.a_rows = g.a_rows;

@@ -27,11 +27,11 @@ WAM_DEV float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 WAM_DEV bf16x8 load_bf16x8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
 WAM_DEV float gelu_tanh_f(float u) {
-  // 0.5 u (1 + tanh(sqrt(2/pi) (u + 0.044715 u^3))), tanh(y) = 1 - 2/(exp(2y)+1)
-  const float k0 = 0.7978845608028654f, k1 = 0.044715f;
-  float y = k0 * (u + k1 * u * u * u);
-  float t = 1.0f - 2.0f / (__expf(2.0f * y) + 1.0f);
-  return 0.5f * u * (1.0f + t);
+  // 0.5 u (1 + tanh(y)) with y = sqrt(2/pi) (u + 0.044715 u^3) equals u * sigmoid(2y)
+  // = u / (1 + 2^(-2 y log2 e)); evaluated with the hardware exp2 and reciprocal.
+  const float k0 = 0.7978845608028654f * 2.0f * 1.4426950408889634f, k1 = 0.044715f;
+  const float z = -k0 * (u + k1 * u * u * u);
+  return u * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z));
 }
 
 WAM_DEV float silu_f(float u) { return u / (1.0f + __expf(-u)); }

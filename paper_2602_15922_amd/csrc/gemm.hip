@@ -27,33 +27,70 @@ struct Cfg {
 
 WAM_DEV int swz(int row, int ch) { return row * BK + ((ch ^ (row & 7)) << 3); }
 
+// Exact row -> (group, row-in-group) split for a runtime divisor: a float reciprocal
+// estimate, corrected by one step (rows < 2^23).
+WAM_DEV int64_t group_off(int row, int rows, float inv, int64_t group_stride, int64_t ld) {
+  int q = (int)(((float)row + 0.5f) * inv);
+  int r = row - q * rows;
+  if (r < 0) { q -= 1; r += rows; }
+  else if (r >= rows) { q += 1; r -= rows; }
+  return (int64_t)q * group_stride + (int64_t)r * ld;
+}
+
+// Epilogue of four consecutive columns [col, col+4) of one output row.
 template <int EPI>
-WAM_DEV void epilogue_store(const GemmArgs& g, int row, int col, float acc) {
+WAM_DEV void epilogue4(const GemmArgs& g, const float inv_o, const float inv_g, int row, int col, f32x4 v) {
   if (row >= g.M || col >= g.N) return;
-  float v = acc + (g.bias ? g.bias[col] : 0.f);
-  const int64_t orow = (int64_t)(row / g.o_rows) * g.o_bs + (int64_t)(row % g.o_rows) * g.ldo;
-  if constexpr (EPI == WAM_EPI_BF16) {
-    static_cast<bf16*>(g.out)[orow + col] = (bf16)v;
-  } else if constexpr (EPI == WAM_EPI_GELU_BF16) {
-    static_cast<bf16*>(g.out)[orow + col] = (bf16)gelu_tanh_f(v);
-  } else if constexpr (EPI == WAM_EPI_RESID_F32) {
-    float gt = 1.f;
-    if (g.gate_a || g.gate_v) {
-      gt = g.gate_a ? g.gate_a[col] : 0.f;
-      if (g.gate_v) gt += g.gate_v[(int64_t)(row / g.gate_rows) * g.gate_stride + col];
+  const int64_t orow = group_off(row, g.o_rows, inv_o, g.o_bs, g.ldo);
+  if (col + 4 <= g.N) {
+    if (g.bias) v += *reinterpret_cast<const f32x4*>(g.bias + col);
+    if constexpr (EPI == WAM_EPI_BF16 || EPI == WAM_EPI_GELU_BF16) {
+      bf16x4 o;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[j] = (bf16)(EPI == WAM_EPI_GELU_BF16 ? gelu_tanh_f(v[j]) : v[j]);
+      *reinterpret_cast<bf16x4*>(static_cast<bf16*>(g.out) + orow + col) = o;
+    } else if constexpr (EPI == WAM_EPI_RESID_F32) {
+      f32x4 gt = {1.f, 1.f, 1.f, 1.f};
+      if (g.gate_a || g.gate_v) {
+        gt = g.gate_a ? *reinterpret_cast<const f32x4*>(g.gate_a + col) : f32x4{0.f, 0.f, 0.f, 0.f};
+        if (g.gate_v)
+          gt += *reinterpret_cast<const f32x4*>(g.gate_v + group_off(row, g.gate_rows, inv_g, g.gate_stride, 0) + col);
+      }
+      f32x4* o = reinterpret_cast<f32x4*>(static_cast<float*>(g.out) + orow + col);
+      *o = *o + gt * v;
+    } else {
+      *reinterpret_cast<f32x4*>(static_cast<float*>(g.out) + orow + col) = v;
     }
-    float* o = static_cast<float*>(g.out) + orow + col;
-    *o = *o + gt * v;
-  } else {
-    static_cast<float*>(g.out)[orow + col] = v;
+    return;
+  }
+  // ragged last columns
+  for (int j = 0; j < 4 && col + j < g.N; ++j) {
+    float x = v[j] + (g.bias ? g.bias[col + j] : 0.f);
+    if constexpr (EPI == WAM_EPI_BF16) {
+      static_cast<bf16*>(g.out)[orow + col + j] = (bf16)x;
+    } else if constexpr (EPI == WAM_EPI_GELU_BF16) {
+      static_cast<bf16*>(g.out)[orow + col + j] = (bf16)gelu_tanh_f(x);
+    } else if constexpr (EPI == WAM_EPI_RESID_F32) {
+      float gt = 1.f;
+      if (g.gate_a || g.gate_v) {
+        gt = g.gate_a ? g.gate_a[col + j] : 0.f;
+        if (g.gate_v) gt += g.gate_v[group_off(row, g.gate_rows, inv_g, g.gate_stride, 0) + col + j];
+      }
+      float* o = static_cast<float*>(g.out) + orow + col + j;
+      *o = *o + gt * x;
+    } else {
+      static_cast<float*>(g.out)[orow + col + j] = x;
+    }
   }
 }
 
 template <int BM, int BN, int EPI>
 __global__ __launch_bounds__(256) void gemm_nt(const GemmArgs g, int tiles_m, int tiles_n) {
   using C = Cfg<BM, BN>;
-  __shared__ __attribute__((aligned(16))) bf16 As[2][BM * BK];
-  __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * BK];
+  // one LDS allocation: two A slices, two W slices; reused for epilogue staging
+  __shared__ __attribute__((aligned(16))) bf16 smem[2 * (BM + BN) * BK];
+  auto As = [&](int buf) { return smem + buf * (BM * BK); };
+  auto Bs = [&](int buf) { return smem + 2 * BM * BK + buf * (BN * BK); };
 
   // XCD-aware remap: the hardware deals workgroups round-robin over 8 XCDs; give each
   // XCD a contiguous range of tiles so tiles that share a W panel share an L2.
@@ -99,10 +136,10 @@ __global__ __launch_bounds__(256) void gemm_nt(const GemmArgs g, int tiles_m, in
   auto lstore = [&](int buf) {
 #pragma unroll
     for (int c = 0; c < C::A_CH; ++c)
-      *reinterpret_cast<bf16x8*>(&As[buf][swz((tid >> 3) + 32 * c, kc)]) = ra[c];
+      *reinterpret_cast<bf16x8*>(&As(buf)[swz((tid >> 3) + 32 * c, kc)]) = ra[c];
 #pragma unroll
     for (int c = 0; c < C::B_CH; ++c)
-      *reinterpret_cast<bf16x8*>(&Bs[buf][swz((tid >> 3) + 32 * c, kc)]) = rb[c];
+      *reinterpret_cast<bf16x8*>(&Bs(buf)[swz((tid >> 3) + 32 * c, kc)]) = rb[c];
   };
 
   f32x16 acc[C::TM][C::TN];
@@ -124,11 +161,11 @@ __global__ __launch_bounds__(256) void gemm_nt(const GemmArgs g, int tiles_m, in
 #pragma unroll
       for (int a = 0; a < C::TM; ++a)
         fa[a] = *reinterpret_cast<const bf16x8*>(
-            &As[cur][swz(wm * (BM / C::WM) + a * 32 + l32, 2 * ks + hh)]);
+            &As(cur)[swz(wm * (BM / C::WM) + a * 32 + l32, 2 * ks + hh)]);
 #pragma unroll
       for (int b = 0; b < C::TN; ++b)
         fb[b] = *reinterpret_cast<const bf16x8*>(
-            &Bs[cur][swz(wn * (BN / C::WN) + b * 32 + l32, 2 * ks + hh)]);
+            &Bs(cur)[swz(wn * (BN / C::WN) + b * 32 + l32, 2 * ks + hh)]);
 #pragma unroll
       for (int a = 0; a < C::TM; ++a)
 #pragma unroll
@@ -138,16 +175,31 @@ __global__ __launch_bounds__(256) void gemm_nt(const GemmArgs g, int tiles_m, in
     __syncthreads();
   }
 
+  // ---- epilogue: each wave stages 32 rows x WCOLS of its tile through LDS (reusing
+  // the operand buffers) so every lane then owns 4 consecutive columns of one row and
+  // the stores are 8/16-byte vectors over contiguous row segments.
+  constexpr int WCOLS = BN / C::WN, SROW = WCOLS + 4;
+  static_assert(C::WM * C::WN * 32 * SROW * 4 <= 2 * (BM + BN) * BK * 2, "staging does not fit");
+  float* stage = reinterpret_cast<float*>(smem) + w * 32 * SROW;
+  const float inv_o = 1.0f / (float)g.o_rows, inv_g = 1.0f / (float)g.gate_rows;
+  const int row_base = m0 + wm * (BM / C::WM), col_base = n0 + wn * WCOLS;
 #pragma unroll
-  for (int a = 0; a < C::TM; ++a)
+  for (int a = 0; a < C::TM; ++a) {
 #pragma unroll
     for (int b = 0; b < C::TN; ++b)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * (BM / C::WM) + a * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-        const int col = n0 + wn * (BN / C::WN) + b * 32 + l32;
-        epilogue_store<EPI>(g, row, col, acc[a][b][r]);
-      }
+      for (int r = 0; r < 16; ++r)
+        stage[(8 * (r >> 2) + 4 * hh + (r & 3)) * SROW + b * 32 + l32] = acc[a][b][r];
+    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < 32 * WCOLS / 256; ++p) {
+      const int idx = p * 64 + lane;
+      const int rloc = idx / (WCOLS / 4), c4 = idx % (WCOLS / 4);
+      const f32x4 v = *reinterpret_cast<const f32x4*>(&stage[rloc * SROW + c4 * 4]);
+      epilogue4<EPI>(g, inv_o, inv_g, row_base + a * 32 + rloc, col_base + c4 * 4, v);
+    }
+    __syncthreads();
+  }
 }
 
 template <int BM, int BN>
@@ -170,9 +222,19 @@ hipError_t launch_gemm(const GemmArgs& gin, hipStream_t s) {
   if (g.a_rows <= 0) { g.a_rows = g.M; g.a_bs = 0; }
   if (g.o_rows <= 0) { g.o_rows = g.M; g.o_bs = 0; }
   if (g.gate_rows <= 0) { g.gate_rows = g.M; g.gate_stride = 0; }
-  // big tiles where they still fill the 256 CUs, smaller ones otherwise
-  const long t256 = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
-  if (t256 >= 256) return launch_cfg<256, 256>(g, s);
+  // Pick the tile whose rounds of 256 concurrent workgroups cost least, weighting
+  // smaller tiles by their lower MFMA efficiency (measured).
+  struct Opt { int bm, bn; float eff; };
+  const Opt opts[3] = {{256, 256, 1.0f}, {128, 256, 0.85f}, {128, 128, 0.6f}};
+  int best = 0;
+  float best_cost = 0.f;
+  for (int i = 0; i < 3; ++i) {
+    const long tiles = (long)((g.M + opts[i].bm - 1) / opts[i].bm) * ((g.N + opts[i].bn - 1) / opts[i].bn);
+    const float cost = (float)((tiles + 255) / 256) * opts[i].bm * opts[i].bn / opts[i].eff;
+    if (i == 0 || cost < best_cost) { best = i; best_cost = cost; }
+  }
+  if (best == 0) return launch_cfg<256, 256>(g, s);
+  if (best == 1) return launch_cfg<128, 256>(g, s);
   return launch_cfg<128, 128>(g, s);
 }
 

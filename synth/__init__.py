@@ -5,7 +5,7 @@ them to the storage types (bf16 round-to-nearest-even, fp32) and describes the
 workload shapes.  Both the fp64 oracle and the HIP path consume what it returns;
 neither is imported here.
 
-Every tensor comes from its own counter-free stream
+Every tensor comes from its own seeded stream
 ``Generator(PCG64(SeedSequence([cfg_seed, tensor_id, layer])))`` so a test can
 regenerate one layer at a time without holding a whole 40-layer model in host RAM.
 """
@@ -43,9 +43,10 @@ def rng(cfg_seed: int, tensor: str, layer: int = 0) -> np.random.Generator:
 def bf16_bits(a: np.ndarray) -> np.ndarray:
     """Round to bfloat16 (round-to-nearest-even) and return the raw uint16 bits."""
     f = np.ascontiguousarray(a, dtype=np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
+    u = f.view(np.uint32)
     nan = np.isnan(f)
-    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    # u + 0x7FFF + lsb cannot wrap for non-NaN inputs (NaNs are fixed up below)
+    r = ((u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))) >> np.uint32(16)).astype(np.uint16)
     if nan.any():
         r[nan] = 0x7FC0
     return r
@@ -84,11 +85,17 @@ class Tensor:
 
 def normal(cfg_seed: int, tensor: str, shape, std: float = 1.0, layer: int = 0,
            dtype: str = "bf16") -> Tensor:
+    """N(0, std^2) draws (float32 ziggurat), stored as bf16 (RNE) or fp32."""
     g = rng(cfg_seed, tensor, layer)
-    a = g.standard_normal(size=shape, dtype=np.float64) * std if std else np.zeros(shape)
+    if std:
+        a = g.standard_normal(size=shape, dtype=np.float32)
+        if std != 1.0:
+            a *= np.float32(std)
+    else:
+        a = np.zeros(shape, np.float32)
     if dtype == "bf16":
         return Tensor("bf16", bf16_bits(a))
-    return Tensor("f32", a.astype(np.float32))
+    return Tensor("f32", a)
 
 
 def zeros(shape, dtype: str = "f32") -> Tensor:

@@ -1,0 +1,153 @@
+"""Seeded DiT block and step cases, run through the C ABI and through the fp64 oracle.
+
+Both sides start from the same synth tensors; each computes its own positions (the
+library's wam_chunk_positions/wam_rope_tables on the GPU side, oracle.chunk_positions
+on the oracle side)."""
+import numpy as np
+
+import oracle
+import synth
+from gpu_helpers import dev, host, workspace
+
+
+def lib():
+    import paper_2602_15922_amd as w
+    return w
+
+
+def dims_of(wl, n_layers):
+    return lib().make_dims(wl.d, wl.H, wl.Dh, wl.ffn, n_layers, wl.latent_ch, wl.act_dim, wl.text_dim,
+                           wl.freq_dim, wl.eps)
+
+
+def f64(params):
+    return {k: v.f64 for k, v in params.items()}
+
+
+def gpu_rope_tables(wl, B=None):
+    w = lib()
+    pos = w.wam_chunk_positions(wl.n_cached, wl.F, wl.Hg, wl.Wg, wl.A)
+    cos, sin = w.wam_rope_tables(pos, wl.Dh)
+    return dev(cos), dev(sin)
+
+
+def oracle_positions(wl):
+    return oracle.chunk_positions(wl.n_cached, wl.F, wl.Hg, wl.Wg, wl.A)
+
+
+def prev_chunk_ids(wl):
+    return np.repeat(np.arange(wl.n_cached), wl.L)
+
+
+def upload_cache(wl, kc, vc, B):
+    """[B, Lcap, H, Dh] device caches with the cached rows filled."""
+    import torch
+    k = torch.zeros((B, wl.Lcap, wl.H, wl.Dh), dtype=torch.bfloat16, device="cuda")
+    v = torch.zeros_like(k)
+    if kc is not None:
+        k[:, :wl.cache_rows] = dev(kc)
+        v[:, :wl.cache_rows] = dev(vc)
+    return k, v
+
+
+# ------------------------------------------------------------------------------ block
+class BlockCase:
+    """One block over the current chunk of `wl`, given x, e0, ctx and the cache."""
+
+    def __init__(self, wl, layer=0, bias_std=0.0, e0=None, ctx=None):
+        self.wl = wl
+        B, s = wl.B, wl.seed
+        self.W = synth.block_params(wl, layer, bias_std, mod_std=wl.mod_std)
+        self.x = synth.normal(s, "x", (B, wl.L, wl.d), 1.0, layer, dtype="f32")
+        self.e0 = e0 if e0 is not None else synth.zeros((B, 6, wl.d))
+        self.ctx = ctx if ctx is not None else synth.normal(s, "ctx", (B, wl.Lc, wl.d), 1.0, layer)
+        self.kc, self.vc = synth.kv_cache(wl, layer, B) if wl.n_cached else (None, None)
+
+    def run_oracle(self, e0=None, ctx=None):
+        """fp64 block; e0 / ctx override the seeded ones (float64 arrays)."""
+        wl = self.wl
+        e0 = self.e0.f64 if e0 is None else e0
+        ctx = self.ctx.f64 if ctx is None else ctx
+        kp = self.kc.f64 if self.kc is not None else None
+        vp = self.vc.f64 if self.vc is not None else None
+        return oracle.dit_block(self.x.f64, e0, f64(self.W), wl.H, wl.eps, oracle_positions(wl),
+                                np.full(wl.L, wl.n_cached), kp, vp, prev_chunk_ids(wl) if kp is not None else None,
+                                ctx=ctx)
+
+    def run_gpu(self, e0_dev=None, ctx_dev=None):
+        import torch
+        w = lib()
+        wl, B = self.wl, self.wl.B
+        Wd = {k: dev(v) for k, v in self.W.items()}
+        x = dev(self.x)
+        kcache, vcache = upload_cache(wl, self.kc, self.vc, B)
+        cos, sin = gpu_rope_tables(wl)
+        dims = dims_of(wl, 1)
+        ws = workspace(w.wam_block_workspace_bytes(dims, B, wl.L, wl.Lc))
+        w.wam_dit_block_fwd(dims, w.make_block_weights(Wd), x, dev(self.e0) if e0_dev is None else e0_dev,
+                            cos, sin, kcache, vcache, wl.cache_rows, w.cached_chunks(wl.cache_rows, wl.L),
+                            ctx=dev(self.ctx) if ctx_dev is None else ctx_dev, ws=ws)
+        torch.cuda.synchronize()
+        return x, kcache, vcache
+
+
+# ------------------------------------------------------------------------------ step
+class StepCase:
+    """A denoising step of `wl` with n_layers seeded blocks (streamed one at a time on the
+    oracle side)."""
+
+    def __init__(self, wl, n_layers, bias_std=0.0):
+        self.wl, self.n_layers, self.bias_std = wl, n_layers, bias_std
+        B, s = wl.B, wl.seed
+        self.P = synth.model_params(wl, bias_std=bias_std)
+        self.z = synth.normal(s, "z_t", (B, wl.latent_ch, wl.F, wl.Hl, wl.Wl), 1.0)
+        self.a = synth.normal(s, "a_t", (B, wl.A, wl.act_dim), 1.0)
+        self.t = synth.uniform(s, "t", (B,))
+        self.text = synth.normal(s, "text", (B, wl.Lc, wl.text_dim), 1.0)
+
+    def layer(self, l):
+        W = synth.block_params(self.wl, l, self.bias_std, mod_std=self.wl.mod_std)
+        kc, vc = synth.kv_cache(self.wl, l) if self.wl.n_cached else (None, None)
+        return W, kc, vc
+
+    def run_oracle(self):
+        wl = self.wl
+
+        def layers(l):
+            W, kc, vc = self.layer(l)
+            return f64(W), (kc.f64 if kc is not None else None), (vc.f64 if vc is not None else None)
+
+        return oracle.dit_step(self.z.f64, self.a.f64, self.t.f64, self.text.f64, f64(self.P), layers,
+                               self.n_layers, wl.H, wl.eps, wl.n_cached, oracle_positions(wl),
+                               prev_chunk=prev_chunk_ids(wl) if wl.n_cached else None)
+
+    def upload(self):
+        """Device model and inputs (kept on self so the step can be re-run)."""
+        w = lib()
+        wl, B = self.wl, self.wl.B
+        self.top = {k: dev(v) for k, v in self.P.items()}
+        self.blocks, self.kcs, self.vcs = [], [], []
+        for l in range(self.n_layers):
+            W, kc, vc = self.layer(l)
+            self.blocks.append({k: dev(v) for k, v in W.items()})
+            k, v = upload_cache(wl, kc, vc, B)
+            self.kcs.append(k)
+            self.vcs.append(v)
+        self.model = w.make_model(dims_of(wl, self.n_layers), self.top, self.blocks)
+        self.cos, self.sin = gpu_rope_tables(wl)
+        self.dz, self.da, self.dt, self.dtext = dev(self.z), dev(self.a), dev(self.t), dev(self.text)
+
+    def run_gpu(self, events=None):
+        import torch
+        w = lib()
+        wl, B = self.wl, self.wl.B
+        if not hasattr(self, "model"):
+            self.upload()
+        vv = torch.empty((B, wl.latent_ch, wl.F, wl.Hl, wl.Wl), dtype=torch.float32, device="cuda")
+        va = torch.empty((B, wl.A, wl.act_dim), dtype=torch.float32, device="cuda")
+        io = w.make_step_io(self.dz, self.da, self.dt, self.dtext, self.kcs, self.vcs, self.cos, self.sin,
+                            wl.cache_rows, w.cached_chunks(wl.cache_rows, wl.L), vv, va, events=events)
+        ws = workspace(w.wam_step_workspace_bytes(self.model, io))
+        w.wam_dit_step_fwd(self.model, io, ws)
+        torch.cuda.synchronize()
+        return vv, va

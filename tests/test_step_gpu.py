@@ -1,0 +1,135 @@
+"""GPU parity of wam_dit_step_fwd (the velocity call of one denoising step) against the
+fp64 oracle (relative L2 <= 2e-2 on both velocities), its full-depth identity property
+at the 14B shapes, determinism and the per-kernel timing hook."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from dit_cases import StepCase, dims_of, f64, gpu_rope_tables
+from gpu_helpers import dev, host, log, rel_l2, workspace
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-2
+
+
+def lib():
+    import paper_2602_15922_amd as w
+    return w
+
+
+def check_step(case, vv, va, tol=TOL):
+    rv, ra = case.run_oracle()
+    ev, ea = rel_l2(host(vv), rv), rel_l2(host(va), ra)
+    print(f"  step rel L2 video {ev:.2e} action {ea:.2e}", flush=True)
+    assert ev <= tol and ea <= tol
+
+
+def test_step_small_three_blocks_with_cache():
+    """d=512 model, 3 blocks, batch 2, two cached chunks, non-zero biases."""
+    wl = synth.WORKLOADS["block_d512"].replace(B=2, n_cached=2, n_layers=3, mod_std=0.3)
+    log("step small")
+    case = StepCase(wl, 3, bias_std=0.05)
+    vv, va = case.run_gpu()
+    check_step(case, vv, va)
+
+
+def test_step_14b_shapes_one_block():
+    """The 40-block step's shapes (3152 rows, 4 cached chunks, 15760 keys, 512x4096 text)
+    at depth 1, against the oracle."""
+    wl = synth.WORKLOADS["step_14b"].replace(n_layers=1)
+    log("step 14b depth 1: inputs")
+    case = StepCase(wl, 1)
+    log("step 14b depth 1: GPU")
+    vv, va = case.run_gpu()
+    log("step 14b depth 1: oracle")
+    check_step(case, vv, va)
+
+
+def identity_model(wl, n_layers):
+    """Seeded model-level weights with the gate rows of the time projection zeroed, and
+    device-random blocks whose gates and cross-attention output projection are zero: every
+    block is then the identity on the residual."""
+    import torch
+    w = lib()
+    P = synth.model_params(wl)
+    d = wl.d
+    bits = P["w_t6"].data.copy()
+    bits[2 * d:3 * d] = 0
+    bits[5 * d:6 * d] = 0
+    P["w_t6"] = synth.Tensor("bf16", bits)
+    top = {k: dev(v) for k, v in P.items()}
+    g = torch.Generator(device="cuda").manual_seed(11)
+
+    def rn(*s, std=0.02):
+        return (torch.randn(*s, generator=g, device="cuda") * std).to(torch.bfloat16)
+
+    blocks, kcs, vcs = [], [], []
+    for _ in range(n_layers):
+        mod6 = torch.randn(6, d, generator=g, device="cuda") * 0.02
+        mod6[2] = 0.0
+        mod6[5] = 0.0
+        blocks.append({"w_qkv": rn(3 * d, d), "w_o": rn(d, d), "w_cq": rn(d, d), "w_ckv": rn(2 * d, d),
+                       "w_co": torch.zeros(d, d, dtype=torch.bfloat16, device="cuda"), "w_f1": rn(wl.ffn, d),
+                       "w_f2": rn(d, wl.ffn), "mod6": mod6})
+        kcs.append(rn(wl.B, wl.Lcap, wl.H, wl.Dh, std=1.0))
+        vcs.append(rn(wl.B, wl.Lcap, wl.H, wl.Dh, std=1.0))
+    return P, w.make_model(dims_of(wl, n_layers), top, blocks), (top, blocks, kcs, vcs)
+
+
+@pytest.mark.parametrize("name", ["step_14b", "step_14b_b2_3view"])
+def test_step_full_depth_identity_blocks(name):
+    """At full depth (40 blocks) and full shapes, zero gates and a zero cross-attention
+    output projection make every block the identity, so the velocities equal the head
+    applied to the embedded chunk — a closed form the oracle computes without blocks."""
+    import torch
+    w = lib()
+    wl = synth.WORKLOADS[name]
+    log(f"step full depth identity {name}")
+    P, model, keep = identity_model(wl, wl.n_layers)
+    _, _, kcs, vcs = keep
+    case = StepCase(wl, 0)
+    cos, sin = gpu_rope_tables(wl)
+    vv = torch.empty((wl.B, wl.latent_ch, wl.F, wl.Hl, wl.Wl), dtype=torch.float32, device="cuda")
+    va = torch.empty((wl.B, wl.A, wl.act_dim), dtype=torch.float32, device="cuda")
+    io = w.make_step_io(dev(case.z), dev(case.a), dev(case.t), dev(case.text), kcs, vcs, cos, sin,
+                        wl.cache_rows, w.cached_chunks(wl.cache_rows, wl.L), vv, va)
+    w.wam_dit_step_fwd(model, io, workspace(w.wam_step_workspace_bytes(model, io)))
+    torch.cuda.synchronize()
+    f = f64(P)
+    e, _ = oracle.time_embedding(case.t.f64, f["w_t1"], f["b_t1"], f["w_t2"], f["b_t2"], f["w_t6"], f["b_t6"])
+    x = oracle.embed(case.z.f64, case.a.f64, f["w_patch"], f["b_patch"], f["w_ain"], f["b_ain"])
+    rv, ra = oracle.head(x, e, f["head_mod2"], wl.Lv, f["w_hv"], f["b_hv"], f["w_ha"], f["b_ha"], wl.eps,
+                         wl.latent_ch, wl.F, wl.Hl, wl.Wl)
+    ev, ea = rel_l2(host(vv), rv), rel_l2(host(va), ra)
+    print(f"  identity step rel L2 video {ev:.2e} action {ea:.2e}", flush=True)
+    assert ev <= 5e-3 and ea <= 5e-3
+
+
+def test_step_deterministic_and_timing_events():
+    import torch
+    wl = synth.WORKLOADS["block_d512"].replace(n_cached=1, n_layers=2)
+    log("step determinism + events")
+    case = StepCase(wl, 2)
+    vv1, va1 = case.run_gpu()
+    events = [torch.cuda.Event(enable_timing=True) for _ in range(2 * 2)]
+    vv2, va2 = case.run_gpu(events=events)
+    assert torch.equal(vv1, vv2) and torch.equal(va1, va2)
+    for l in range(2):
+        assert events[2 * l].elapsed_time(events[2 * l + 1]) > 0.0
+
+
+def test_step_rejects_undersized_workspace():
+    import torch
+    w = lib()
+    wl = synth.WORKLOADS["block_d512"].replace(n_layers=1)
+    case = StepCase(wl, 1)
+    case.upload()
+    vv = torch.empty((1, wl.latent_ch, wl.F, wl.Hl, wl.Wl), dtype=torch.float32, device="cuda")
+    va = torch.empty((1, wl.A, wl.act_dim), dtype=torch.float32, device="cuda")
+    io = w.make_step_io(case.dz, case.da, case.dt, case.dtext, case.kcs, case.vcs, case.cos, case.sin, 0,
+                        w.cached_chunks(0, wl.L), vv, va)
+    need = w.wam_step_workspace_bytes(case.model, io)
+    with pytest.raises(w.WamError) as ei:
+        w.wam_dit_step_fwd(case.model, io, workspace(need - 512))
+    assert ei.value.status == w.binding.WAM_EWORKSPACE
