@@ -5,14 +5,23 @@
 // largest prefix of a query tile are never visited; only tiles that straddle a
 // query row's prefix end are masked.
 //
-// Work split: one workgroup = 4 wavefronts = 128 query rows of one (batch, head);
-// each wavefront owns 32 query rows and walks all visible key tiles of 64 keys.
-// The score tile is computed transposed, S^T = K Q^T, so that a lane owns one
-// query and the softmax row statistics stay inside the lane (plus one exchange
-// with the partner lane l^32).  The output is accumulated transposed as well,
-// O^T = V^T P^T, so the per-query rescale is again lane-local.  K tiles sit in LDS
-// row-major, V tiles transposed ([dh][key]); both XOR-swizzled so the MFMA operand
-// reads are bank-conflict free.
+// Work split: a workgroup of 4 wavefronts owns 128 query rows of one (batch, head),
+// 32 rows per wavefront, so a wavefront's whole state (Q fragments, score tile,
+// probabilities and the fp32 output accumulators) stays in ordinary VGPRs and two
+// wavefronts share each SIMD: one's softmax overlaps the other's MFMAs.  Key tiles of
+// 64 keys are double-buffered in LDS and fetched with direct global->LDS loads (no
+// staging registers): the next tile is in flight while the current one is consumed,
+// with one barrier per tile.  The score
+// tile is computed transposed, S^T = K Q^T, so a lane owns one query and its softmax
+// statistics stay in the lane (plus the partner lane l^32 holding the other half of
+// the keys); the output is accumulated transposed as well, O^T = V^T P^T, so the
+// rescale is lane-local too.  V stays row-major in LDS and its transposed MFMA
+// operand is read with the gfx950 transposing LDS load (ds_read_b64_tr_b16).  The
+// reference maximum is only raised when a tile exceeds it by more than 2^8 in the
+// exp2 domain, which leaves the result exact (o = acc / l for any reference) and skips
+// almost every accumulator rescale.  Both tiles are XOR-swizzled in 16-byte chunks
+// (K by row&7 for the row-wise operand reads, V by 2*(row&3) for the 4-row transposing
+// reads), applied on the load side by choosing each lane's source chunk.
 #include "common.h"
 #include "kernels.h"
 
@@ -21,6 +30,12 @@ namespace {
 
 constexpr int BM = 128;  // query rows per workgroup
 constexpr int BN = 64;   // keys per tile
+constexpr int NT = 256;  // threads per workgroup
+constexpr float RESCALE_LOG2 = 8.0f;  // allowed growth of exp2 arguments before a rescale
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __attribute__((address_space(3))) void lds_void;
 
 WAM_DEV int kend_of(const AttnArgs& a, int row) {
   int e = a.kend[a.n_q_chunks - 1];
@@ -29,84 +44,126 @@ WAM_DEV int kend_of(const AttnArgs& a, int row) {
   return e;
 }
 
+// One K tile and one V tile (BN keys from key kb) into LDS with direct global->LDS
+// loads: 16 bytes per lane, lane l of a wave instruction landing at LDS unit base + l.
+// Rows past Lk are clamped to the last key (their scores are masked, so their values
+// never count).  koff/voff are the lanes' loop-invariant source offsets.
 template <int DH>
-__global__ __launch_bounds__(256) void attn_fwd(const AttnArgs a) {
-  constexpr int KS = DH / 16;  // MFMA k-steps over the head dim
-  constexpr int MT = DH / 32;  // 32-row tiles of the transposed output
-  constexpr int CPR = DH / 8;  // 16-byte chunks per K row
-  __shared__ __attribute__((aligned(16))) bf16 Ks[BN * DH];
-  __shared__ __attribute__((aligned(16))) bf16 Vt[DH * BN];
+WAM_DEV void fetch_tile(bf16* Ks, const bf16* kp, const bf16* vp, int64_t kv_ts, int Lk, int kb, int w,
+                        const int* koff, const int* voff, const int* krow) {
+  constexpr int KCH = BN * (DH / 8) / NT;
+  bf16* Vs = Ks + BN * DH;
+  const bf16* kt = kp + (int64_t)kb * kv_ts;
+  const bf16* vt = vp + (int64_t)kb * kv_ts;
+  const bool full = kb + BN <= Lk;  // uniform: no row of this tile needs clamping
+#pragma unroll
+  for (int i = 0; i < KCH; ++i) {
+    const int base = (w * KCH + i) * 64;  // wave-uniform first unit of this instruction
+    int shift = 0;
+    if (!full) {
+      const int over = kb + krow[i] - (Lk - 1);
+      shift = over > 0 ? -over * (int)kv_ts : 0;
+    }
+    __builtin_amdgcn_global_load_lds(kt + koff[i] + shift, (lds_void*)(Ks + base * 8), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(vt + voff[i] + shift, (lds_void*)(Vs + base * 8), 16, 0, 0);
+  }
+}
+
+template <int DH>
+__global__ __launch_bounds__(NT) void attn_fwd(const AttnArgs a, int nqt) {
+  constexpr int KS = DH / 16;         // MFMA k-steps over the head dim
+  constexpr int MT = DH / 32;         // 32-row tiles of the transposed output
+  constexpr int CPR = DH / 8;         // 16-byte chunks per K/V row
+  constexpr int KCH = BN * CPR / NT;  // 16-byte chunks of K (and of V) per thread
+  constexpr int TILE = 2 * BN * DH;   // K tile + V tile, elements
+  __shared__ __attribute__((aligned(16))) bf16 smem[2 * TILE];
+
+  // XCD-aware mapping: give each XCD a contiguous range of (q-tile, head) pairs so
+  // the workgroups sharing a head's K/V share an L2.
+  const int nblk = gridDim.x, bi = blockIdx.x, xcd = bi & 7, slot = bi >> 3;
+  const int per = nblk >> 3, rem = nblk & 7;
+  const int lid = xcd * per + (xcd < rem ? xcd : rem) + slot;
+  const int qt = lid % nqt, hb = lid / nqt, h = hb % a.H, b = hb / a.H;
+  const int q0 = qt * BM;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int hh = lane >> 5, l32 = lane & 31;
-  const int b = blockIdx.z, h = blockIdx.y, q0 = blockIdx.x * BM;
 
   const int qrow = q0 + 32 * w + l32;
   const int qrow_c = qrow < a.Lq ? qrow : a.Lq - 1;
   const int row_kend = kend_of(a, qrow_c);
+  bf16x8 qf[KS];
+  {
+    const bf16* qp = static_cast<const bf16*>(a.q) + b * a.q_bs + (int64_t)qrow_c * a.q_ts + h * DH + 8 * hh;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = load_bf16x8(qp + 16 * ks);
+  }
   const int last = (q0 + BM < a.Lq ? q0 + BM : a.Lq) - 1;
   const int kend_max = kend_of(a, last);
   const int kend_min = kend_of(a, q0);
 
-  const bf16* qb = static_cast<const bf16*>(a.q) + b * a.q_bs + (int64_t)qrow_c * a.q_ts + h * DH + 8 * hh;
-  bf16x8 qf[KS];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) qf[ks] = load_bf16x8(qb + 16 * ks);
+  const bf16* kp = static_cast<const bf16*>(a.k) + b * a.kv_bs + h * DH;
+  const bf16* vp = static_cast<const bf16*>(a.v) + b * a.kv_bs + h * DH;
 
-  const bf16* kb_ptr = static_cast<const bf16*>(a.k) + b * a.kv_bs + h * DH;
-  const bf16* vb_ptr = static_cast<const bf16*>(a.v) + b * a.kv_bs + h * DH;
+  // ---- per-lane source offsets of the tile fetch (loop-invariant)
+  int koff[KCH], voff[KCH], krow[KCH];  // loop-invariant per-lane source offsets
+#pragma unroll
+  for (int i = 0; i < KCH; ++i) {
+    const int u = (w * KCH + i) * 64 + lane, row = u / CPR, pch = u % CPR;
+    krow[i] = row;
+    koff[i] = row * (int)a.kv_ts + ((pch ^ (row & 7)) * 8);
+    voff[i] = row * (int)a.kv_ts + ((pch ^ (2 * (row & 3))) * 8);
+  }
+
+
+  // V^T fragment addressing (per lane, loop-invariant): in each 16-lane group, lane j
+  // points at row (rb + j/4), dims (db + 4*(j%4) .. +3); the transposing load then
+  // hands lane i the four keys rb..rb+3 of dim db+i.
+  const int grp = lane >> 4, j16 = lane & 15;
+  int voffs[MT][2][2][2];  // [mt][nt][hf][e]
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int col = 32 * mt + 16 * (grp & 1) + 4 * (j16 & 3);
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int r = 32 * nt + 16 * hf + 4 * (grp >> 1) + (j16 >> 2) + 8 * e;
+          voffs[mt][nt][hf][e] = r * DH + (((col >> 3) ^ (2 * (r & 3))) * 8) + 4 * ((col >> 2) & 1);
+        }
+  }
 
   f32x16 acc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x16{};
-  float m_i = -INFINITY, l_i = 0.f;
-  const float c = a.c;
+  float m_ref = -INFINITY, l_part = 0.f;
+  const float c = a.c, thr = RESCALE_LOG2 / c;
 
   const int ntiles = (kend_max + BN - 1) / BN;
+  fetch_tile<DH>(smem, kp, vp, a.kv_ts, a.Lk, 0, w, koff, voff, krow);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
   for (int t = 0; t < ntiles; ++t) {
-    const int kb = t * BN;
-    __syncthreads();
-    // ---- K tile -> LDS, row-major [key][dh], 16-byte chunks swizzled by key
-#pragma unroll
-    for (int i = 0; i < (BN * CPR) / 256; ++i) {
-      const int cidx = tid + 256 * i;
-      const int key = cidx / CPR, ch = cidx % CPR;
-      const int gk = kb + key;
-      bf16x8 val = {};
-      if (gk < a.Lk) val = load_bf16x8(kb_ptr + (int64_t)gk * a.kv_ts + ch * 8);
-      *reinterpret_cast<bf16x8*>(&Ks[key * DH + ((ch ^ (key & 7)) * 8)]) = val;
-    }
-    // ---- V tile -> LDS transposed [dh][key]; a thread moves 4 keys x 8 dims
-    if (tid < (BN / 4) * CPR) {
-      const int kg = tid % (BN / 4), c8 = tid / (BN / 4);
-      bf16x8 r[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int gk = kb + 4 * kg + i;
-        r[i] = gk < a.Lk ? load_bf16x8(vb_ptr + (int64_t)gk * a.kv_ts + c8 * 8) : bf16x8{};
-      }
-#pragma unroll
-      for (int dd = 0; dd < 8; ++dd) {
-        const int dh = 8 * c8 + dd;
-        bf16x4 col = {r[0][dd], r[1][dd], r[2][dd], r[3][dd]};
-        *reinterpret_cast<bf16x4*>(&Vt[dh * BN + ((kg ^ (dh & 15)) * 4)]) = col;
-      }
-    }
-    __syncthreads();
+    const int cur = t & 1, kb = t * BN;
+    if (t + 1 < ntiles) fetch_tile<DH>(smem + (cur ^ 1) * TILE, kp, vp, a.kv_ts, a.Lk, kb + BN, w, koff, voff, krow);
+    const bf16* Ks = smem + cur * TILE;
+    const bf16* Vs = Ks + BN * DH;
 
     // ---- S^T = K Q^T for two 32-key sub-tiles
-    f32x16 s[2];
+    f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
-      s[nt] = f32x16{};
       const int key = 32 * nt + l32;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[key * DH + (((2 * ks + hh) ^ (key & 7)) * 8)]);
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[key * DH + (((2 * ks + hh) ^ (key & 7)) * 8)]);
         s[nt] = mfma32(kf, qf[ks], s[nt]);
       }
     }
-    // ---- mask keys past this query's visible prefix (only on straddling tiles)
+
+    // ---- mask keys past this query's visible prefix (straddling tiles only)
     if (kb + BN > kend_min) {
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt)
@@ -116,51 +173,56 @@ __global__ __launch_bounds__(256) void attn_fwd(const AttnArgs a) {
           if (key >= row_kend) s[nt][r] = -INFINITY;
         }
     }
-    // ---- online softmax (lane-local for its query, plus the partner lane)
-    float mx = -INFINITY;
+
+    // ---- online softmax with a lazily raised reference maximum
+    float mx = s[0][0];
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[nt][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_i, mx);
-    const float ms = (m_new == -INFINITY) ? 0.f : m_new * c;
-    const float alpha = exp2_fast(m_i * c - ms);
-    float rs = 0.f;
+    const bool raise = mx > m_ref + thr || (m_ref == -INFINITY && mx != -INFINITY);
+    if (__any(raise)) {
+      const float m_new = raise ? mx : m_ref;
+      const float alpha = m_ref == -INFINITY ? 0.f : exp2_fast((m_ref - m_new) * c);
+      m_ref = m_new;
+      l_part *= alpha;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) acc[mt] *= alpha;
+    }
+    const float ms = m_ref == -INFINITY ? 0.f : m_ref * c;
     bf16x8 pb[2][2];
+    float rs = 0.f;
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2_fast(s[nt][r] * c - ms);
+        const float p = exp2_fast(__builtin_fmaf(s[nt][r], c, -ms));
         rs += p;
         pb[nt][r >> 3][r & 7] = (bf16)p;
       }
-    rs += __shfl_xor(rs, 32, 64);
-    l_i = l_i * alpha + rs;
-    m_i = m_new;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[mt] *= alpha;
+    l_part += rs;
 
     // ---- O^T += V^T P^T
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int dh = 32 * mt + l32;
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {
-          const int u0 = (32 * nt + 16 * hf + 4 * hh) >> 2;
-          bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vt[dh * BN + ((u0 ^ (dh & 15)) * 4)]);
-          bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vt[dh * BN + (((u0 + 2) ^ (dh & 15)) * 4)]);
-          bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-          acc[mt] = mfma32(vf, pb[nt][hf], acc[mt]);
+          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(Vs + voffs[mt][nt][hf][0]));
+          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(Vs + voffs[mt][nt][hf][1]));
+          const s16x4 v8[2] = {lo, hi};
+          acc[mt] = mfma32(*reinterpret_cast<const bf16x8*>(v8), pb[nt][hf], acc[mt]);
         }
-    }
+
+    if (t + 1 < ntiles) __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
   }
 
+  const float l = l_part + __shfl_xor(l_part, 32, 64);
   if (qrow < a.Lq) {
-    const float inv = 1.0f / l_i;
+    const float inv = 1.0f / l;
     bf16* ob = static_cast<bf16*>(a.o) + b * a.o_bs + (int64_t)qrow * a.o_ts + h * DH;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -176,11 +238,12 @@ __global__ __launch_bounds__(256) void attn_fwd(const AttnArgs a) {
 }  // namespace
 
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
-  dim3 grid((a.Lq + BM - 1) / BM, a.H, a.B);
+  const int nqt = (a.Lq + BM - 1) / BM;
+  const long nblk = (long)nqt * a.H * a.B;
   if (a.Dh == 128)
-    hipLaunchKernelGGL(attn_fwd<128>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attn_fwd<128>, dim3((unsigned)nblk), dim3(NT), 0, s, a, nqt);
   else
-    hipLaunchKernelGGL(attn_fwd<64>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attn_fwd<64>, dim3((unsigned)nblk), dim3(NT), 0, s, a, nqt);
   return hipGetLastError();
 }
 
