@@ -69,7 +69,11 @@ WAM_DEV void fetch_tile(bf16* Ks, const bf16* kp, const bf16* vp, int64_t kv_ts,
   }
 }
 
-template <int DH>
+// CHUNKED: the keys form more than one chunk (cached chunks plus the current one), so a
+// query's visible prefix is looked up from its chunk; otherwise (cross-attention to the
+// text, or a single chunk) every query sees all Lk keys and only the ragged last tile
+// is masked.
+template <int DH, bool CHUNKED>
 __global__ __launch_bounds__(NT) void attn_fwd(const AttnArgs a, int nqt) {
   constexpr int KS = DH / 16;         // MFMA k-steps over the head dim
   constexpr int MT = DH / 32;         // 32-row tiles of the transposed output
@@ -91,7 +95,7 @@ __global__ __launch_bounds__(NT) void attn_fwd(const AttnArgs a, int nqt) {
 
   const int qrow = q0 + 32 * w + l32;
   const int qrow_c = qrow < a.Lq ? qrow : a.Lq - 1;
-  const int row_kend = kend_of(a, qrow_c);
+  const int row_kend = CHUNKED ? kend_of(a, qrow_c) : a.Lk;
   bf16x8 qf[KS];
   {
     const bf16* qp = static_cast<const bf16*>(a.q) + b * a.q_bs + (int64_t)qrow_c * a.q_ts + h * DH + 8 * hh;
@@ -99,8 +103,8 @@ __global__ __launch_bounds__(NT) void attn_fwd(const AttnArgs a, int nqt) {
     for (int ks = 0; ks < KS; ++ks) qf[ks] = load_bf16x8(qp + 16 * ks);
   }
   const int last = (q0 + BM < a.Lq ? q0 + BM : a.Lq) - 1;
-  const int kend_max = kend_of(a, last);
-  const int kend_min = kend_of(a, q0);
+  const int kend_max = CHUNKED ? kend_of(a, last) : a.Lk;
+  const int kend_min = CHUNKED ? kend_of(a, q0) : a.Lk;
 
   const bf16* kp = static_cast<const bf16*>(a.k) + b * a.kv_bs + h * DH;
   const bf16* vp = static_cast<const bf16*>(a.v) + b * a.kv_bs + h * DH;
@@ -239,11 +243,15 @@ __global__ __launch_bounds__(NT) void attn_fwd(const AttnArgs a, int nqt) {
 
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   const int nqt = (a.Lq + BM - 1) / BM;
-  const long nblk = (long)nqt * a.H * a.B;
-  if (a.Dh == 128)
-    hipLaunchKernelGGL(attn_fwd<128>, dim3((unsigned)nblk), dim3(NT), 0, s, a, nqt);
-  else
-    hipLaunchKernelGGL(attn_fwd<64>, dim3((unsigned)nblk), dim3(NT), 0, s, a, nqt);
+  const dim3 grid((unsigned)((long)nqt * a.H * a.B)), block(NT);
+  const bool chunked = a.n_k_chunks > 1;
+  if (a.Dh == 128) {
+    if (chunked) hipLaunchKernelGGL((attn_fwd<128, true>), grid, block, 0, s, a, nqt);
+    else hipLaunchKernelGGL((attn_fwd<128, false>), grid, block, 0, s, a, nqt);
+  } else {
+    if (chunked) hipLaunchKernelGGL((attn_fwd<64, true>), grid, block, 0, s, a, nqt);
+    else hipLaunchKernelGGL((attn_fwd<64, false>), grid, block, 0, s, a, nqt);
+  }
   return hipGetLastError();
 }
 

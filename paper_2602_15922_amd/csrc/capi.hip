@@ -125,6 +125,7 @@ wam_status attn_checked(const wam_attn_desc& d, const void* q, const void* k, co
   a.B = d.B; a.H = d.H; a.Dh = d.Dh; a.Lq = d.Lq; a.Lk = d.Lk;
   const float scale = d.scale > 0.f ? d.scale : 1.0f / std::sqrt((float)d.Dh);
   a.c = scale * 1.4426950408889634f;
+  a.n_k_chunks = d.ch.n_k_chunks;
   a.n_q_chunks = d.ch.n_q_chunks;
   for (int i = 0; i <= d.ch.n_q_chunks; ++i) a.q_off[i] = d.ch.q_off[i];
   HIPCHECK(launch_attn(a, s));

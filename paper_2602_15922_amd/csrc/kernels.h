@@ -16,6 +16,7 @@ struct AttnArgs {
   int64_t q_ts, q_bs, kv_ts, kv_bs, o_ts, o_bs;
   int32_t B, H, Dh, Lq, Lk;
   float c;  // softmax scale * log2(e)
+  int32_t n_k_chunks;
   int32_t n_q_chunks;
   int32_t q_off[WAM_MAX_CHUNKS + 1];
   int32_t kend[WAM_MAX_CHUNKS];  // visible key prefix [0, kend) of each query chunk
