@@ -19,9 +19,9 @@
 // operand is read with the gfx950 transposing LDS load (ds_read_b64_tr_b16).  The
 // reference maximum is only raised when a tile exceeds it by more than 2^8 in the
 // exp2 domain, which leaves the result exact (o = acc / l for any reference) and skips
-// almost every accumulator rescale.  Both tiles are XOR-swizzled in 16-byte chunks
-// (K by row&7 for the row-wise operand reads, V by 2*(row&3) for the 4-row transposing
-// reads), applied on the load side by choosing each lane's source chunk.
+// almost every accumulator rescale.  Both tiles are XOR-swizzled in 16-byte chunks so
+// the operand reads are bank-conflict free (kswz/vswz below), applied on the load side
+// by choosing each lane's source chunk.
 #include "common.h"
 #include "kernels.h"
 
@@ -48,6 +48,18 @@ WAM_DEV int kend_of(const AttnArgs& a, int row) {
 // loads: 16 bytes per lane, lane l of a wave instruction landing at LDS unit base + l.
 // Rows past Lk are clamped to the last key (their scores are masked, so their values
 // never count).  koff/voff are the lanes' loop-invariant source offsets.
+// LDS swizzles (XOR of the 16-byte chunk index).  gfx950 LDS serves 256 bytes (64
+// banks) per cycle: 16 lanes of a 16-byte read, 32 lanes of an 8-byte read.
+//  K: the fragment read has 16 lanes on 16 consecutive rows at one logical chunk;
+//     with 256-byte rows (Dh=128) XOR by row&15, with 128-byte rows by (row>>1)&7.
+//  V: a transposing read covers 4 consecutive rows x 64 bytes per 32 lanes, so the
+//     4 rows' 64-byte groups must fall in different quarters of the 256-byte line:
+//     XOR by 4*(row&3) (Dh=128) or 4*((row>>1)&1) (Dh=64, two rows per line).
+template <int DH>
+WAM_DEV int kswz(int row, int ch) { return DH == 128 ? (ch ^ (row & 15)) : (ch ^ ((row >> 1) & 7)); }
+template <int DH>
+WAM_DEV int vswz(int row, int ch) { return DH == 128 ? (ch ^ (4 * (row & 3))) : (ch ^ (4 * ((row >> 1) & 1))); }
+
 template <int DH>
 WAM_DEV void fetch_tile(bf16* Ks, const bf16* kp, const bf16* vp, int64_t kv_ts, int Lk, int kb, int w,
                         const int* koff, const int* voff, const int* krow) {
@@ -69,12 +81,91 @@ WAM_DEV void fetch_tile(bf16* Ks, const bf16* kp, const bf16* vp, int64_t kv_ts,
   }
 }
 
+// One 64-key tile for one wavefront's 32 queries: S^T = K Q^T, optional prefix mask,
+// online softmax with a lazily raised reference, O^T += V^T P^T.  Ks/Vs are the tile's
+// LDS buffers; kofs[ks] is the lane's byte offset of its K fragment for k-step ks
+// (keys 0..31; +32 rows for the second sub-tile), vofs[mt] the lane's byte offset of
+// its transposing V read for output tile mt (row groups added as constants).
+template <int DH, bool MASK>
+WAM_DEV void attn_tile(const char* Ks, const char* Vs, const bf16x8* qf, f32x16* acc, float& m_ref,
+                       float& l_part, const int* kofs, const int* vofs, float c, float thr, int kb,
+                       int row_kend, int hh) {
+  constexpr int KS = DH / 16, MT = DH / 32, ROWB = DH * 2;  // ROWB: bytes per K/V row
+  f32x16 s[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + kofs[ks] + nt * 32 * ROWB);
+      s[nt] = mfma32(kf, qf[ks], s[nt]);
+    }
+  if (MASK) {
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kb + 32 * nt + 8 * (r >> 2) + 4 * hh + (r & 3);
+        if (key >= row_kend) s[nt][r] = -INFINITY;
+      }
+  }
+  float mx = s[0][0];
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[nt][r]);
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const bool raise = mx > m_ref + thr || (m_ref == -INFINITY && mx != -INFINITY);
+  if (__any(raise)) {
+    const float m_new = raise ? mx : m_ref;
+    const float alpha = m_ref == -INFINITY ? 0.f : exp2_fast((m_ref - m_new) * c);
+    m_ref = m_new;
+    l_part *= alpha;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt] *= alpha;
+  }
+  const float ms = m_ref == -INFINITY ? 0.f : m_ref * c;
+  bf16x8 pb[2][2];
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) pb[nt][r >> 3][r & 7] = (bf16)exp2_fast(__builtin_fmaf(s[nt][r], c, -ms));
+  // row sum of exactly the bf16 probabilities the PV product uses, two per dot2
+  const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16x2 pr = {pb[nt][hf][2 * e], pb[nt][hf][2 * e + 1]};
+        l_part = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, l_part, false);
+      }
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const char* vr = Vs + vofs[mt] + (32 * nt + 16 * hf) * ROWB;
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vr));
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vr + 8 * ROWB));
+        const s16x4 v8[2] = {lo, hi};
+        acc[mt] = mfma32(*reinterpret_cast<const bf16x8*>(v8), pb[nt][hf], acc[mt]);
+      }
+}
+
+// Wait for this wave's direct loads of the next tile, then sync the workgroup.
+WAM_DEV void tile_sync() {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+}
+
 // CHUNKED: the keys form more than one chunk (cached chunks plus the current one), so a
 // query's visible prefix is looked up from its chunk; otherwise (cross-attention to the
 // text, or a single chunk) every query sees all Lk keys and only the ragged last tile
 // is masked.
 template <int DH, bool CHUNKED>
-__global__ __launch_bounds__(NT) void attn_fwd(const AttnArgs a, int nqt) {
+__global__ __launch_bounds__(NT, 2) void attn_fwd(const AttnArgs a, int nqt) {
   constexpr int KS = DH / 16;         // MFMA k-steps over the head dim
   constexpr int MT = DH / 32;         // 32-row tiles of the transposed output
   constexpr int CPR = DH / 8;         // 16-byte chunks per K/V row
@@ -110,33 +201,34 @@ __global__ __launch_bounds__(NT) void attn_fwd(const AttnArgs a, int nqt) {
   const bf16* vp = static_cast<const bf16*>(a.v) + b * a.kv_bs + h * DH;
 
   // ---- per-lane source offsets of the tile fetch (loop-invariant)
-  int koff[KCH], voff[KCH], krow[KCH];  // loop-invariant per-lane source offsets
+  int koff[KCH], voff[KCH], krow[KCH];
 #pragma unroll
   for (int i = 0; i < KCH; ++i) {
     const int u = (w * KCH + i) * 64 + lane, row = u / CPR, pch = u % CPR;
     krow[i] = row;
-    koff[i] = row * (int)a.kv_ts + ((pch ^ (row & 7)) * 8);
-    voff[i] = row * (int)a.kv_ts + ((pch ^ (2 * (row & 3))) * 8);
+    koff[i] = row * (int)a.kv_ts + kswz<DH>(row, pch) * 8;
+    voff[i] = row * (int)a.kv_ts + vswz<DH>(row, pch) * 8;
   }
 
-
-  // V^T fragment addressing (per lane, loop-invariant): in each 16-lane group, lane j
-  // points at row (rb + j/4), dims (db + 4*(j%4) .. +3); the transposing load then
-  // hands lane i the four keys rb..rb+3 of dim db+i.
+  // ---- per-lane LDS operand offsets (bytes, loop-invariant)
+  // K fragment of k-step ks: row l32, logical chunk 2*ks + hh (the swizzle of rows
+  // l32 and l32 + 32 is the same).
+  int kofs[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) kofs[ks] = l32 * DH * 2 + kswz<DH>(l32, 2 * ks + hh) * 16;
+  // V^T: in each 16-lane group, lane j points at row (rb + j/4), dims (db + 4*(j%4)
+  // .. +3); the transposing load then hands lane i the four keys rb..rb+3 of dim db+i.
+  // Row group rb = 32*nt + 16*hf + 4*(grp>>1) (+8 for the second half), dims of output
+  // tile mt at db = 32*mt + 16*(grp&1).  The swizzle only depends on the lane.
   const int grp = lane >> 4, j16 = lane & 15;
-  int voffs[MT][2][2][2];  // [mt][nt][hf][e]
+  int vofs[MT];
+  {
+    const int r0 = 4 * (grp >> 1) + (j16 >> 2);
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int col = 32 * mt + 16 * (grp & 1) + 4 * (j16 & 3);
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const int r = 32 * nt + 16 * hf + 4 * (grp >> 1) + (j16 >> 2) + 8 * e;
-          voffs[mt][nt][hf][e] = r * DH + (((col >> 3) ^ (2 * (r & 3))) * 8) + 4 * ((col >> 2) & 1);
-        }
+    for (int mt = 0; mt < MT; ++mt) {
+      const int col = 32 * mt + 16 * (grp & 1) + 4 * (j16 & 3);
+      vofs[mt] = r0 * DH * 2 + vswz<DH>(r0, col >> 3) * 16 + 8 * ((col >> 2) & 1);
+    }
   }
 
   f32x16 acc[MT];
@@ -146,82 +238,23 @@ __global__ __launch_bounds__(NT) void attn_fwd(const AttnArgs a, int nqt) {
   const float c = a.c, thr = RESCALE_LOG2 / c;
 
   const int ntiles = (kend_max + BN - 1) / BN;
+  const int n_plain = kend_min / BN < ntiles ? kend_min / BN : ntiles;  // tiles no row masks
   fetch_tile<DH>(smem, kp, vp, a.kv_ts, a.Lk, 0, w, koff, voff, krow);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
+  tile_sync();
+  int t = 0;
+  for (; t < n_plain; ++t) {
     const int cur = t & 1, kb = t * BN;
     if (t + 1 < ntiles) fetch_tile<DH>(smem + (cur ^ 1) * TILE, kp, vp, a.kv_ts, a.Lk, kb + BN, w, koff, voff, krow);
-    const bf16* Ks = smem + cur * TILE;
-    const bf16* Vs = Ks + BN * DH;
-
-    // ---- S^T = K Q^T for two 32-key sub-tiles
-    f32x16 s[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      const int key = 32 * nt + l32;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[key * DH + (((2 * ks + hh) ^ (key & 7)) * 8)]);
-        s[nt] = mfma32(kf, qf[ks], s[nt]);
-      }
-    }
-
-    // ---- mask keys past this query's visible prefix (straddling tiles only)
-    if (kb + BN > kend_min) {
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kb + 32 * nt + 8 * (r >> 2) + 4 * hh + (r & 3);
-          if (key >= row_kend) s[nt][r] = -INFINITY;
-        }
-    }
-
-    // ---- online softmax with a lazily raised reference maximum
-    float mx = s[0][0];
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[nt][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const bool raise = mx > m_ref + thr || (m_ref == -INFINITY && mx != -INFINITY);
-    if (__any(raise)) {
-      const float m_new = raise ? mx : m_ref;
-      const float alpha = m_ref == -INFINITY ? 0.f : exp2_fast((m_ref - m_new) * c);
-      m_ref = m_new;
-      l_part *= alpha;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[mt] *= alpha;
-    }
-    const float ms = m_ref == -INFINITY ? 0.f : m_ref * c;
-    bf16x8 pb[2][2];
-    float rs = 0.f;
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = exp2_fast(__builtin_fmaf(s[nt][r], c, -ms));
-        rs += p;
-        pb[nt][r >> 3][r & 7] = (bf16)p;
-      }
-    l_part += rs;
-
-    // ---- O^T += V^T P^T
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(Vs + voffs[mt][nt][hf][0]));
-          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(Vs + voffs[mt][nt][hf][1]));
-          const s16x4 v8[2] = {lo, hi};
-          acc[mt] = mfma32(*reinterpret_cast<const bf16x8*>(v8), pb[nt][hf], acc[mt]);
-        }
-
-    if (t + 1 < ntiles) __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    const char* Ks = reinterpret_cast<const char*>(smem + cur * TILE);
+    attn_tile<DH, false>(Ks, Ks + BN * DH * 2, qf, acc, m_ref, l_part, kofs, vofs, c, thr, kb, row_kend, hh);
+    tile_sync();
+  }
+  for (; t < ntiles; ++t) {
+    const int cur = t & 1, kb = t * BN;
+    if (t + 1 < ntiles) fetch_tile<DH>(smem + (cur ^ 1) * TILE, kp, vp, a.kv_ts, a.Lk, kb + BN, w, koff, voff, krow);
+    const char* Ks = reinterpret_cast<const char*>(smem + cur * TILE);
+    attn_tile<DH, true>(Ks, Ks + BN * DH * 2, qf, acc, m_ref, l_part, kofs, vofs, c, thr, kb, row_kend, hh);
+    tile_sync();
   }
 
   const float l = l_part + __shfl_xor(l_part, 32, 64);

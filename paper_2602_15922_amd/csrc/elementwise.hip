@@ -8,61 +8,77 @@ namespace wam {
 namespace {
 
 // ---------------------------------------------------------------------------------
-// LayerNorm (biased variance, eps) of fp32 rows -> optional affine -> AdaLN
-// modulation -> bf16.  One wavefront per row; the row stays in registers between the
-// mean pass, the variance pass and the output pass, so x is read from HBM once.
+// LayerNorm (biased variance, eps) of fp32 rows, then the optional affine and the
+// AdaLN modulation, to bf16.  Both are folded into one per-column affine,
+//   y = LN(x) * P + Q,  P = gamma (1 + scale),  Q = beta (1 + scale) + shift,
+// computed once per workgroup into LDS: a workgroup owns LN_ROWS rows of one sample,
+// so the modulation vectors are read once per LN_ROWS rows instead of once per row.
+// One wavefront per row; the row stays in registers between the mean, variance and
+// output passes, so x is read from HBM once.
 // ---------------------------------------------------------------------------------
-constexpr int LN_MAXV = 32;  // d <= 32 * 256
+constexpr int LN_MAXV = 32;   // d <= 32 * 256
+constexpr int LN_ROWS = 16;   // rows per workgroup (4 per wavefront)
 
-__global__ __launch_bounds__(256) void ln_mod_kernel(const LnArgs a) {
+__global__ __launch_bounds__(256) void ln_mod_kernel(const LnArgs a, int blocks_per_batch) {
+  __shared__ __attribute__((aligned(16))) float PQ[2 * LN_MAXV * 256];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + w;
-  if (row >= a.rows) return;
-  const int b = row / a.rows_per_batch;
-  const int nv = a.d >> 8;
-  const float* xr = a.x + (int64_t)row * a.d;
-  f32x4 v[LN_MAXV];
-  float s = 0.f;
-#pragma unroll
-  for (int i = 0; i < LN_MAXV; ++i)
-    if (i < nv) {
-      v[i] = *reinterpret_cast<const f32x4*>(xr + (i * 64 + lane) * 4);
-      s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
-    }
-  const float mean = wave_sum(s) / (float)a.d;
-  float q = 0.f;
-#pragma unroll
-  for (int i = 0; i < LN_MAXV; ++i)
-    if (i < nv) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float t = v[i][j] - mean;
-        q += t * t;
-      }
-    }
-  const float var = wave_sum(q) / (float)a.d;
-  const float rstd = rsqrtf(var + a.eps);
+  const int b = blockIdx.x / blocks_per_batch;
+  const int r0 = (blockIdx.x % blocks_per_batch) * LN_ROWS;
+  const int d = a.d, nv = d >> 8;
   const int64_t mb = (int64_t)b * a.mod_stride;
-  bf16* hr = static_cast<bf16*>(a.h) + (int64_t)row * a.d;
+  float* P = PQ;
+  float* Q = PQ + d;
+  for (int c = threadIdx.x * 4; c < d; c += 1024) {
+    f32x4 g = {1.f, 1.f, 1.f, 1.f}, bt = {0.f, 0.f, 0.f, 0.f}, sc = {0.f, 0.f, 0.f, 0.f}, sh = {0.f, 0.f, 0.f, 0.f};
+    if (a.gamma) g = *reinterpret_cast<const f32x4*>(a.gamma + c);
+    if (a.beta) bt = *reinterpret_cast<const f32x4*>(a.beta + c);
+    if (a.scale_a) sc += *reinterpret_cast<const f32x4*>(a.scale_a + c);
+    if (a.scale_v) sc += *reinterpret_cast<const f32x4*>(a.scale_v + mb + c);
+    if (a.shift_a) sh += *reinterpret_cast<const f32x4*>(a.shift_a + c);
+    if (a.shift_v) sh += *reinterpret_cast<const f32x4*>(a.shift_v + mb + c);
+    const f32x4 one = {1.f, 1.f, 1.f, 1.f};
+    *reinterpret_cast<f32x4*>(P + c) = g * (one + sc);
+    *reinterpret_cast<f32x4*>(Q + c) = bt * (one + sc) + sh;
+  }
+  __syncthreads();
+  for (int rr = w; rr < LN_ROWS; rr += 4) {
+    const int rloc = r0 + rr;
+    if (rloc >= a.rows_per_batch) break;
+    const int64_t row = (int64_t)b * a.rows_per_batch + rloc;
+    const float* xr = a.x + row * d;
+    f32x4 v[LN_MAXV];
+    float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < LN_MAXV; ++i)
-    if (i < nv) {
-      const int col = (i * 64 + lane) * 4;
-      f32x4 y;
+    for (int i = 0; i < LN_MAXV; ++i)
+      if (i < nv) {
+        v[i] = *reinterpret_cast<const f32x4*>(xr + (i * 64 + lane) * 4);
+        s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
+      }
+    const float mean = wave_sum(s) / (float)d;
+    float q = 0.f;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) y[j] = (v[i][j] - mean) * rstd;
-      if (a.gamma) y *= *reinterpret_cast<const f32x4*>(a.gamma + col);
-      if (a.beta) y += *reinterpret_cast<const f32x4*>(a.beta + col);
-      f32x4 sc = {0.f, 0.f, 0.f, 0.f}, sh = {0.f, 0.f, 0.f, 0.f};
-      if (a.scale_a) sc += *reinterpret_cast<const f32x4*>(a.scale_a + col);
-      if (a.scale_v) sc += *reinterpret_cast<const f32x4*>(a.scale_v + mb + col);
-      if (a.shift_a) sh += *reinterpret_cast<const f32x4*>(a.shift_a + col);
-      if (a.shift_v) sh += *reinterpret_cast<const f32x4*>(a.shift_v + mb + col);
-      bf16x4 o;
+    for (int i = 0; i < LN_MAXV; ++i)
+      if (i < nv) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) o[j] = (bf16)(y[j] * (1.f + sc[j]) + sh[j]);
-      *reinterpret_cast<bf16x4*>(hr + col) = o;
-    }
+        for (int j = 0; j < 4; ++j) {
+          const float t = v[i][j] - mean;
+          q += t * t;
+        }
+      }
+    const float rstd = rsqrtf(wave_sum(q) / (float)d + a.eps);
+    bf16* hr = static_cast<bf16*>(a.h) + row * d;
+#pragma unroll
+    for (int i = 0; i < LN_MAXV; ++i)
+      if (i < nv) {
+        const int col = (i * 64 + lane) * 4;
+        const f32x4 pp = *reinterpret_cast<const f32x4*>(P + col);
+        const f32x4 qq = *reinterpret_cast<const f32x4*>(Q + col);
+        bf16x4 o;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = (bf16)((v[i][j] - mean) * rstd * pp[j] + qq[j]);
+        *reinterpret_cast<bf16x4*>(hr + col) = o;
+      }
+  }
 }
 
 // ---------------------------------------------------------------------------------
@@ -184,7 +200,9 @@ __global__ void unpatchify_kernel(int B, int C, int F, int Hl, int Wl, const flo
 
 hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s) {
   if (a.rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(ln_mod_kernel, dim3((a.rows + 3) / 4), dim3(256), 0, s, a);
+  const int B = a.rows / a.rows_per_batch;
+  const int bpb = (a.rows_per_batch + LN_ROWS - 1) / LN_ROWS;
+  hipLaunchKernelGGL(ln_mod_kernel, dim3((unsigned)(B * bpb)), dim3(256), 0, s, a, bpb);
   return hipGetLastError();
 }
 

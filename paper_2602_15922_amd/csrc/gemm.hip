@@ -3,29 +3,41 @@
 // A [M][K] and W [N][K] are both K-contiguous, which is exactly the operand layout
 // of the 32x32x16 bf16 MFMA (8 consecutive k per lane for A rows and W rows), so no
 // transpose is ever needed.  A workgroup of 4 wavefronts (2x2) computes a BM x BN
-// tile; BK=64 slices of A and W are staged through double-buffered LDS (one barrier
-// per slice) with the next slice's global loads in flight during the MFMAs.  LDS rows
-// are 128 bytes (64 bf16) with 16-byte chunks XOR-swizzled by row, which makes the
-// fragment reads (32 rows, same chunk) bank-conflict free.  Tail rows/columns are
-// clamped on load and skipped on store; a K tail is zero-filled.
+// tile.  BK-wide slices of A and W are fetched with direct global->LDS loads into a
+// ring of STAGES LDS buffers: the loads of slice t+STAGES-1 are issued while slice t
+// is consumed, so each load has STAGES-1 slices of MFMA work to land (no staging
+// registers, one barrier per slice, waits on the vector-memory counter only for the
+// slice about to be used).  Within a slice the fragment reads of the next 16-wide
+// k-step are issued before the current step's MFMAs.  LDS rows are BK bf16 with
+// 16-byte chunks XOR-swizzled by row so the fragment reads (32 consecutive rows, same
+// chunk) are bank-conflict free; since lane l of a direct load lands at LDS unit
+// base+l, the swizzle is applied by choosing each lane's source chunk.  Tail
+// rows/columns are clamped on load and skipped on store; a K tail is zeroed in LDS
+// after it lands.
 #include "common.h"
 #include "kernels.h"
 
 namespace wam {
 namespace {
 
-constexpr int BK = 64;
-
-template <int BM, int BN>
+template <int BM_, int BN_, int BK_, int STAGES_>
 struct Cfg {
-  static constexpr int WM = 2, WN = 2;               // wave grid
-  static constexpr int TM = BM / WM / 32;            // 32x32 tiles per wave, rows
-  static constexpr int TN = BN / WN / 32;            // 32x32 tiles per wave, cols
-  static constexpr int A_CH = BM * BK / 8 / 256;     // 16-byte chunks per thread (A)
-  static constexpr int B_CH = BN * BK / 8 / 256;     // 16-byte chunks per thread (W)
+  static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_;
+  static constexpr int WM = 2, WN = 2;            // wave grid
+  static constexpr int TM = BM / WM / 32;         // 32x32 tiles per wave, rows
+  static constexpr int TN = BN / WN / 32;         // 32x32 tiles per wave, cols
+  static constexpr int CPR = BK / 8;              // 16-byte chunks per LDS row
+  static constexpr int NIA = BM * CPR / 256;      // direct-load instructions per wave (A)
+  static constexpr int NIB = BN * CPR / 256;      // (W)
+  static constexpr int STAGE = (BM + BN) * BK;    // elements per stage
+  // XOR pattern.  gfx950 LDS serves 256 bytes (64 banks) per cycle, i.e. 16 lanes of a
+  // 16-byte read; the 16 consecutive rows those lanes read at one logical chunk must land
+  // on 16 distinct 16-byte bank slots.  128-byte rows (8 chunks): two rows share a
+  // 256-byte bank line, so XOR the chunk by (row>>1)&7; 64-byte rows (4 chunks): XOR
+  // by (row>>2)&3.
+  static WAM_DEV int pch(int row, int ch) { return CPR == 8 ? (ch ^ ((row >> 1) & 7)) : (ch ^ ((row >> 2) & 3)); }
+  static WAM_DEV int swz(int row, int ch) { return row * BK + (pch(row, ch) << 3); }
 };
-
-WAM_DEV int swz(int row, int ch) { return row * BK + ((ch ^ (row & 7)) << 3); }
 
 // Exact row -> (group, row-in-group) split for a runtime divisor: a float reciprocal
 // estimate, corrected by one step (rows < 2^23).
@@ -84,13 +96,34 @@ WAM_DEV void epilogue4(const GemmArgs& g, const float inv_o, const float inv_g, 
   }
 }
 
-template <int BM, int BN, int EPI>
+typedef __attribute__((address_space(3))) void lds_void;
+
+// One BK slice of NI*64*4 16-byte units into LDS with direct loads.  Wave w's
+// instruction c fills units [(w*NI + c)*64, +64); lane l's unit is read from
+// src[c] (its row, already offset to its logical chunk kl[c]) at column k0, or, when
+// that chunk lies past K, from the row's last chunk (such units are zeroed once they
+// have landed).
+template <int NI>
+WAM_DEV void fetch_slice(bf16* dst, const bf16* base, const int64_t* src, const int* kl, int k0, int K, int w) {
+#pragma unroll
+  for (int c = 0; c < NI; ++c) {
+    const int k = k0 + kl[c] < K ? k0 : K - 8 - kl[c];
+    __builtin_amdgcn_global_load_lds(base + src[c] + k, (lds_void*)(dst + (w * NI + c) * 512), 16, 0, 0);
+  }
+}
+
+// s_waitcnt on the vector-memory counter only (vmcnt <= n; LDS and export counters
+// left unconstrained), gfx9 encoding.
+#define WAM_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (((n) >> 4) << 14)) | (7 << 4) | (15 << 8))
+// s_waitcnt on the LDS/scalar counter only (lgkmcnt = 0)
+#define WAM_WAIT_LGKMCNT0() __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4))
+
+template <typename C, int EPI>
 __global__ __launch_bounds__(256) void gemm_nt(const GemmArgs g, int tiles_m, int tiles_n) {
-  using C = Cfg<BM, BN>;
-  // one LDS allocation: two A slices, two W slices; reused for epilogue staging
-  __shared__ __attribute__((aligned(16))) bf16 smem[2 * (BM + BN) * BK];
-  auto As = [&](int buf) { return smem + buf * (BM * BK); };
-  auto Bs = [&](int buf) { return smem + 2 * BM * BK + buf * (BN * BK); };
+  constexpr int BM = C::BM, BN = C::BN, BK = C::BK, S = C::STAGES;
+  __shared__ __attribute__((aligned(16))) bf16 smem[S * C::STAGE];
+  auto As = [&](int buf) { return smem + buf * C::STAGE; };
+  auto Bs = [&](int buf) { return smem + buf * C::STAGE + BM * BK; };
 
   // XCD-aware remap: the hardware deals workgroups round-robin over 8 XCDs; give each
   // XCD a contiguous range of tiles so tiles that share a W panel share an L2.
@@ -108,38 +141,44 @@ __global__ __launch_bounds__(256) void gemm_nt(const GemmArgs g, int tiles_m, in
   const bf16* A = static_cast<const bf16*>(g.A);
   const bf16* W = static_cast<const bf16*>(g.W);
 
-  // per-thread global row offsets (constant over the K loop)
-  const int kc = tid & 7;  // 16-byte chunk inside a BK slice
-  int64_t a_off[C::A_CH], b_off[C::B_CH];
+  // Direct-load sources (loop-invariant).  Unit u of a slice is row u/CPR, physical
+  // chunk u%CPR, which holds logical chunk pch(row, u%CPR) (the XOR is an involution).
+  constexpr int RPI = 64 / C::CPR;  // rows covered by one wave instruction
+  const int lrow = lane / C::CPR;
+  int64_t a_src[C::NIA], b_src[C::NIB];
 #pragma unroll
-  for (int c = 0; c < C::A_CH; ++c) {
-    int r = m0 + (tid >> 3) + 32 * c;
+  for (int c = 0; c < C::NIA; ++c) {
+    const int row = (w * C::NIA + c) * RPI + lrow;
+    int r = m0 + row;
     r = r < g.M ? r : g.M - 1;
-    a_off[c] = (int64_t)(r / g.a_rows) * g.a_bs + (int64_t)(r % g.a_rows) * g.lda;
+    a_src[c] = (int64_t)(r / g.a_rows) * g.a_bs + (int64_t)(r % g.a_rows) * g.lda + C::pch(row, lane % C::CPR) * 8;
   }
 #pragma unroll
-  for (int c = 0; c < C::B_CH; ++c) {
-    int r = n0 + (tid >> 3) + 32 * c;
+  for (int c = 0; c < C::NIB; ++c) {
+    const int row = (w * C::NIB + c) * RPI + lrow;
+    int r = n0 + row;
     r = r < g.N ? r : g.N - 1;
-    b_off[c] = (int64_t)r * g.ldw;
+    b_src[c] = (int64_t)r * g.ldw + C::pch(row, lane % C::CPR) * 8;
   }
-
-  bf16x8 ra[C::A_CH], rb[C::B_CH];
-  auto gload = [&](int k0) {
-    const int k = k0 + kc * 8;
-    const bool ok = k < g.K;
+  // logical column offset of each of the lane's units (for the K-tail test)
+  int kla[C::NIA], klb[C::NIB];
 #pragma unroll
-    for (int c = 0; c < C::A_CH; ++c) ra[c] = ok ? load_bf16x8(A + a_off[c] + k) : bf16x8{};
+  for (int c = 0; c < C::NIA; ++c) kla[c] = C::pch((w * C::NIA + c) * RPI + lrow, lane % C::CPR) * 8;
 #pragma unroll
-    for (int c = 0; c < C::B_CH; ++c) rb[c] = ok ? load_bf16x8(W + b_off[c] + k) : bf16x8{};
+  for (int c = 0; c < C::NIB; ++c) klb[c] = C::pch((w * C::NIB + c) * RPI + lrow, lane % C::CPR) * 8;
+  auto fetch = [&](int kt) {  // plain LDS code only (the direct-load builtin is in fetch_slice)
+    const int buf = kt % S;
+    fetch_slice<C::NIA>(As(buf), A, a_src, kla, kt * BK, g.K, w);
+    fetch_slice<C::NIB>(Bs(buf), W, b_src, klb, kt * BK, g.K, w);
   };
-  auto lstore = [&](int buf) {
+  auto zero_tail = [&](int kt) {  // only for a slice that runs past K
+    const int buf = kt % S;
 #pragma unroll
-    for (int c = 0; c < C::A_CH; ++c)
-      *reinterpret_cast<bf16x8*>(&As(buf)[swz((tid >> 3) + 32 * c, kc)]) = ra[c];
+    for (int c = 0; c < C::NIA; ++c)
+      if (kt * BK + kla[c] >= g.K) *reinterpret_cast<bf16x8*>(As(buf) + ((w * C::NIA + c) * 64 + lane) * 8) = bf16x8{};
 #pragma unroll
-    for (int c = 0; c < C::B_CH; ++c)
-      *reinterpret_cast<bf16x8*>(&Bs(buf)[swz((tid >> 3) + 32 * c, kc)]) = rb[c];
+    for (int c = 0; c < C::NIB; ++c)
+      if (kt * BK + klb[c] >= g.K) *reinterpret_cast<bf16x8*>(Bs(buf) + ((w * C::NIB + c) * 64 + lane) * 8) = bf16x8{};
   };
 
   f32x16 acc[C::TM][C::TN];
@@ -149,37 +188,61 @@ __global__ __launch_bounds__(256) void gemm_nt(const GemmArgs g, int tiles_m, in
     for (int b = 0; b < C::TN; ++b) acc[a][b] = f32x16{};
 
   const int nk = (g.K + BK - 1) / BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
+  constexpr int NI = C::NIA + C::NIB;  // direct-load instructions per slice per wave
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 fa[C::TM], fb[C::TN];
+  for (int p = 0; p < S - 1; ++p)
+    if (p < nk) fetch(p);
+  for (int kt = 0; kt < nk; ++kt) {
+    // slice kt has landed once at most the younger prefetched slices are in flight
+    const int younger = (nk - 1 - kt) < (S - 2) ? (nk - 1 - kt) : (S - 2);
+    if (younger >= 2) WAM_WAIT_VMCNT(2 * NI);
+    else if (younger == 1) WAM_WAIT_VMCNT(NI);
+    else WAM_WAIT_VMCNT(0);
+    if ((kt + 1) * BK > g.K) {
+      zero_tail(kt);
+      WAM_WAIT_LGKMCNT0();
+    }
+    // Slice kt is visible to all waves and slice kt-1's buffer is free once every wave
+    // is here: each wave has waited for its own loads of slice kt above, and its reads
+    // of slice kt-1 were consumed by its MFMAs.  A plain s_barrier (the __syncthreads
+    // fence would also wait for the prefetched slices still in flight).
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if (kt + S - 1 < nk) fetch(kt + S - 1);
+    const int cur = kt % S;
+
+    // fragments double-buffered in registers: the reads of k-step ks+1 are in flight
+    // while the MFMAs of k-step ks run
+    bf16x8 fa[2][C::TM], fb[2][C::TN];
+    auto read_frags = [&](int ks, int slot) {
 #pragma unroll
       for (int a = 0; a < C::TM; ++a)
-        fa[a] = *reinterpret_cast<const bf16x8*>(
-            &As(cur)[swz(wm * (BM / C::WM) + a * 32 + l32, 2 * ks + hh)]);
+        fa[slot][a] = *reinterpret_cast<const bf16x8*>(&As(cur)[C::swz(wm * (BM / C::WM) + a * 32 + l32, 2 * ks + hh)]);
 #pragma unroll
       for (int b = 0; b < C::TN; ++b)
-        fb[b] = *reinterpret_cast<const bf16x8*>(
-            &Bs(cur)[swz(wn * (BN / C::WN) + b * 32 + l32, 2 * ks + hh)]);
+        fb[slot][b] = *reinterpret_cast<const bf16x8*>(&Bs(cur)[C::swz(wn * (BN / C::WN) + b * 32 + l32, 2 * ks + hh)]);
+    };
+    read_frags(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      if (ks + 1 < BK / 16) read_frags(ks + 1, (ks + 1) & 1);
 #pragma unroll
       for (int a = 0; a < C::TM; ++a)
 #pragma unroll
-        for (int b = 0; b < C::TN; ++b) acc[a][b] = mfma32(fa[a], fb[b], acc[a][b]);
+        for (int b = 0; b < C::TN; ++b) acc[a][b] = mfma32(fa[ks & 1][a], fb[ks & 1][b], acc[a][b]);
+      // fence the k-step: the next step's LDS reads stay in this step's region
+      __builtin_amdgcn_sched_barrier(0);
     }
-    if (kt + 1 < nk) lstore(cur ^ 1);
-    __syncthreads();
   }
+  __syncthreads();  // all waves done with the operand ring before it is reused
 
   // ---- epilogue: each wave stages 32 rows x WCOLS of its tile through LDS (reusing
   // the operand buffers) so every lane then owns 4 consecutive columns of one row and
   // the stores are 8/16-byte vectors over contiguous row segments.
-  constexpr int WCOLS = BN / C::WN, SROW = WCOLS + 4;
-  static_assert(C::WM * C::WN * 32 * SROW * 4 <= 2 * (BM + BN) * BK * 2, "staging does not fit");
+  // rows padded by 8 floats: the two half-waves (rows 4 apart) use disjoint banks
+  constexpr int WCOLS = BN / C::WN, SROW = WCOLS + 8;
+  static_assert(C::WM * C::WN * 32 * SROW * 4 <= S * C::STAGE * 2, "staging does not fit");
   float* stage = reinterpret_cast<float*>(smem) + w * 32 * SROW;
   const float inv_o = 1.0f / (float)g.o_rows, inv_g = 1.0f / (float)g.gate_rows;
   const int row_base = m0 + wm * (BM / C::WM), col_base = n0 + wn * WCOLS;
@@ -202,15 +265,15 @@ __global__ __launch_bounds__(256) void gemm_nt(const GemmArgs g, int tiles_m, in
   }
 }
 
-template <int BM, int BN>
+template <typename Cf>
 hipError_t launch_cfg(const GemmArgs& g, hipStream_t s) {
-  const int tm = (g.M + BM - 1) / BM, tn = (g.N + BN - 1) / BN;
+  const int tm = (g.M + Cf::BM - 1) / Cf::BM, tn = (g.N + Cf::BN - 1) / Cf::BN;
   dim3 grid(tm * tn), block(256);
   switch (g.epi) {
-    case WAM_EPI_BF16: hipLaunchKernelGGL((gemm_nt<BM, BN, WAM_EPI_BF16>), grid, block, 0, s, g, tm, tn); break;
-    case WAM_EPI_GELU_BF16: hipLaunchKernelGGL((gemm_nt<BM, BN, WAM_EPI_GELU_BF16>), grid, block, 0, s, g, tm, tn); break;
-    case WAM_EPI_RESID_F32: hipLaunchKernelGGL((gemm_nt<BM, BN, WAM_EPI_RESID_F32>), grid, block, 0, s, g, tm, tn); break;
-    default: hipLaunchKernelGGL((gemm_nt<BM, BN, WAM_EPI_F32>), grid, block, 0, s, g, tm, tn); break;
+    case WAM_EPI_BF16: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_BF16>), grid, block, 0, s, g, tm, tn); break;
+    case WAM_EPI_GELU_BF16: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_GELU_BF16>), grid, block, 0, s, g, tm, tn); break;
+    case WAM_EPI_RESID_F32: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_RESID_F32>), grid, block, 0, s, g, tm, tn); break;
+    default: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_F32>), grid, block, 0, s, g, tm, tn); break;
   }
   return hipGetLastError();
 }
@@ -233,9 +296,9 @@ hipError_t launch_gemm(const GemmArgs& gin, hipStream_t s) {
     const float cost = (float)((tiles + 255) / 256) * opts[i].bm * opts[i].bn / opts[i].eff;
     if (i == 0 || cost < best_cost) { best = i; best_cost = cost; }
   }
-  if (best == 0) return launch_cfg<256, 256>(g, s);
-  if (best == 1) return launch_cfg<128, 256>(g, s);
-  return launch_cfg<128, 128>(g, s);
+  if (best == 0) return launch_cfg<Cfg<256, 256, 32, 4>>(g, s);
+  if (best == 1) return launch_cfg<Cfg<128, 256, 64, 3>>(g, s);
+  return launch_cfg<Cfg<128, 128, 64, 3>>(g, s);
 }
 
 }  // namespace wam
