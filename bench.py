@@ -10,8 +10,10 @@ cross-attention K/V of the text) and the output head.
 
 Prints one JSON line: steps/s, plus the self-attention kernel's achieved bf16 TFLOP/s
 against the MFMA peak (per-launch durations from HIP events recorded around every
-self-attention launch inside the timed steps), and the fp64 oracle timed on the host
-cores on a bounded sample (one full-shape block), scaled to steps/s.
+self-attention launch inside the timed steps) and its HBM bytes per launch (from the
+committed counter profile; null once the kernel source differs from the profiled one),
+and the fp64 oracle timed on the host cores on a bounded sample (one full-shape block),
+scaled to steps/s.
 """
 import argparse
 import json
@@ -33,6 +35,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--workload", default=WORKLOAD)
+    p.add_argument("--probe-attn", type=int, default=0, metavar="N",
+                   help="counter-collection mode: one plain 1 GiB device copy, then N self-attention "
+                        "launches at the workload's shape; prints what ran and exits")
     return p.parse_args()
 
 
@@ -83,6 +88,27 @@ def build_model(wl, torch):
     return model, (top, blocks), kcs, vcs, inputs
 
 
+def attn_traffic():
+    """HBM bytes per self-attention launch from the committed counter profile, or None
+    when the attention kernel's source has changed since the counters were taken."""
+    import hashlib
+    prof = os.path.join(ROOT, "profiles", "attn_fwd_step_14b_traffic.md")
+    if not os.path.exists(prof):
+        return None
+    fields = {}
+    for line in open(prof):
+        if ":" in line and line.split(":")[0] in ("traffic_bytes_per_launch", "kernel_source_sha256"):
+            k, v = line.split(":", 1)
+            fields[k] = v.strip()
+    h = hashlib.sha256()
+    for f in ("attn.hip", "common.h"):
+        with open(os.path.join(ROOT, "paper_2602_15922_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    if fields.get("kernel_source_sha256") != h.hexdigest():
+        return None
+    return int(fields["traffic_bytes_per_launch"])
+
+
 def cpu_baseline(wl):
     """The fp64 oracle on one full-shape block of the workload (a 1/40 sample of the
     step's blocks), scaled to steps/s; inputs come from the seeded generators."""
@@ -110,6 +136,33 @@ def cpu_baseline(wl):
                       f"x{wl.n_layers} blocks; embeddings and head not timed"}
 
 
+def probe_attn(wl, n):
+    """Launch a plain device-to-device copy of known size (the calibration for HBM byte
+    counters) and n self-attention launches of the step's shape (queries of one chunk
+    against the cached chunks plus itself), with nothing else on the GPU in between."""
+    import torch
+    import paper_2602_15922_amd as w
+    torch.cuda.set_device(0)
+    g = torch.Generator(device="cuda").manual_seed(7)
+    copy_bytes = 1 << 30
+    src = torch.randn(copy_bytes // 2, generator=g, device="cuda", dtype=torch.bfloat16)
+    dst = torch.empty_like(src)
+    q = torch.randn(wl.B, wl.L, wl.H, wl.Dh, generator=g, device="cuda", dtype=torch.bfloat16)
+    k = torch.randn(wl.B, wl.Lk, wl.H, wl.Dh, generator=g, device="cuda", dtype=torch.bfloat16)
+    v = torch.randn_like(k)
+    o = torch.empty_like(q)
+    chunks = w.cached_chunks(wl.cache_rows, wl.L)
+    torch.cuda.synchronize()
+    torch.mul(src, 1, out=dst)  # one elementwise kernel: reads and writes copy_bytes
+    torch.cuda.synchronize()
+    for _ in range(n):
+        w.wam_attn_blockcausal(q, k, v, o, chunks)
+    torch.cuda.synchronize()
+    assert torch.isfinite(o).all()
+    print(json.dumps({"probe": "attn", "workload": wl.name, "copy_bytes": copy_bytes, "attn_launches": n,
+                      "q": list(q.shape), "kv": list(k.shape)}), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -122,6 +175,8 @@ def main():
     import paper_2602_15922_amd as w
 
     wl = synth.WORKLOADS[args.workload]
+    if args.probe_attn:
+        return probe_attn(wl, args.probe_attn)
     torch.cuda.set_device(0)
     model, keep, kcs, vcs, inp = build_model(wl, torch)
     B, d = wl.B, wl.d
@@ -176,7 +231,8 @@ def main():
                    "global_batch": B, "seq_len": wl.L, "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "mfma", "kernel": "attn_fwd (block-causal self-attention)",
                      "achieved": round(attn_tflops, 1), "peak": MI355X_BF16_DENSE_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(attn_tflops / MI355X_BF16_DENSE_TFLOPS, 4), "traffic": None,
+                     "frac": round(attn_tflops / MI355X_BF16_DENSE_TFLOPS, 4),
+                     "traffic": attn_traffic() if wl.name == WORKLOAD else None, "traffic_unit": "bytes",
                      "avg_launch_ms": round(attn_avg, 4), "flop_per_launch": attn_flop},
         "step_tflops": round(step_flop / (ms * 1e-3) / 1e12, 1),
         "step_mfma_frac": round(step_flop / (ms * 1e-3) / 1e12 / MI355X_BF16_DENSE_TFLOPS, 4),

@@ -238,6 +238,31 @@ wam_status wam_dit_step_fwd(const wam_model* m, const wam_step_io* io, void* ws,
                             size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------------
+ * wam_dit_update_fwd — the cache-update pass u_theta([z, a]; KV, c, t, update=True)
+ * (Algorithm 2: the context prefill, and the injection of each real observation after
+ * a chunk is executed).
+ *
+ * Same wam_step_io as wam_dit_step_fwd, with z_t holding CLEAN latents and t the
+ * timestep the caller uses for clean content (the library does not interpret t).
+ * Algorithm 2 passes no actions (A = 0); A > 0 is accepted and appends the action
+ * rows too.  The call writes, for every layer l, the K (after RoPE) and V of the
+ * L = Lv + A current rows into rows [cache_len, cache_len + L) of k_cache[l] and
+ * v_cache[l]; no other cache row and no output buffer is written (v_video and
+ * v_action are ignored and may be NULL).  The caller then advances its cache_len by L.
+ *
+ * Several chunks may be appended in one call: z_t holds their frames back to back,
+ * ch lists them as query chunks (each row sees the cached chunks and the current rows
+ * of its own and earlier chunks, Figure 10b) and rope_cos/rope_sin give every row its
+ * own position.  The head is skipped and the last layer stops after its K/V
+ * projection (nothing downstream reads the rest).  Validation, errors and
+ * asynchronous semantics are those of wam_dit_step_fwd; attn_events, when non-NULL,
+ * holds 2*n_layers events of which the last layer's pair is left unrecorded.
+ * ------------------------------------------------------------------------------ */
+size_t wam_update_workspace_bytes(const wam_model* m, const wam_step_io* io);
+wam_status wam_dit_update_fwd(const wam_model* m, const wam_step_io* io, void* ws,
+                              size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------
  * Pieces of the step, exported for testing each kernel on its own.
  * ------------------------------------------------------------------------------ */
 

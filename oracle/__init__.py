@@ -23,4 +23,4 @@ from .layers import linear, layernorm, modulate, gelu_tanh, silu, timestep_sinus
 from .rope import rope_split, rope_angles, apply_rope, chunk_positions  # noqa: F401
 from .attention import attention  # noqa: F401
 from .model import (time_embedding, text_projection, patchify, unpatchify,  # noqa: F401
-                    embed, dit_block, head, dit_step)
+                    embed, dit_block, head, dit_step, dit_update)

@@ -141,3 +141,27 @@ def dit_step(z_t, a_t, t, text, P, layers, n_layers, H, eps, chunk_index, pos,
     Lv = F * (Hl // 2) * (Wl // 2)
     return head(x, e, P["head_mod2"], Lv, P["w_hv"], P["b_hv"], P["w_ha"], P["b_ha"],
                 eps, C, F, Hl, Wl)
+
+
+def dit_update(z, a, t, text, P, layers, n_layers, H, eps, pos, q_chunk, prev_chunk=None, ctx=None):
+    """u_theta([z, a]; KV, c, t, update=True): the cache-update pass of the
+    closed-loop algorithm (Appendix C, Algorithm 2), run on clean observed latents
+    (the algorithm passes no actions, i.e. a with zero rows; the chunk's timestep t
+    is whatever the caller uses for clean content).
+
+    The current rows may span several chunks (q_chunk holds each row's chunk id,
+    pos its RoPE position); each attends to the cached rows and to the current rows
+    of its own and earlier chunks (Figure 10b).  Returns [(k_l, v_l)] per layer: the
+    K (after RoPE) and V of the current rows that the pass appends to layer l's
+    cache.  The velocities of this call are discarded by the algorithm and are not
+    computed."""
+    e, e0 = time_embedding(t, P["w_t1"], P["b_t1"], P["w_t2"], P["b_t2"], P["w_t6"], P["b_t6"])
+    if ctx is None:
+        ctx = text_projection(text, P["w_x1"], P["b_x1"], P["w_x2"], P["b_x2"])
+    x = embed(z, a, P["w_patch"], P["b_patch"], P["w_ain"], P["b_ain"])
+    new_kv = []
+    for layer in range(n_layers):
+        W, kp, vp = layers(layer)
+        x, k, v = dit_block(x, e0, W, H, eps, pos, q_chunk, kp, vp, prev_chunk, ctx=ctx)
+        new_kv.append((k, v))
+    return new_kv

@@ -4,4 +4,5 @@ The compute path is the HIP library ``libwamdit.so`` (hand-written gfx950 kernel
 behind a C ABI declared in ``include/wamdit.h``); this package is its ctypes binding.
 """
 from .binding import *  # noqa: F401,F403
-from .binding import lib, WamError, make_chunks, cached_chunks, make_dims, make_model  # noqa: F401
+from .binding import (lib, WamError, make_chunks, cached_chunks, append_chunks, make_dims,  # noqa: F401
+                      make_model)

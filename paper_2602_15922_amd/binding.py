@@ -21,6 +21,7 @@ WAM_EPI_BF16, WAM_EPI_GELU_BF16, WAM_EPI_RESID_F32, WAM_EPI_F32 = range(4)
 EXPORTED = (
     "wam_last_error", "wam_abi_version", "wam_attn_blockcausal", "wam_block_workspace_bytes",
     "wam_dit_block_fwd", "wam_step_workspace_bytes", "wam_dit_step_fwd",
+    "wam_update_workspace_bytes", "wam_dit_update_fwd",
     "wam_time_embed_workspace_bytes", "wam_time_embed_fwd", "wam_text_proj_workspace_bytes",
     "wam_text_proj_fwd", "wam_adaln_ln_mod", "wam_rope_qkv", "wam_gemm_bf16",
     "wam_embed_workspace_bytes", "wam_embed_fwd", "wam_head_workspace_bytes", "wam_head_fwd",
@@ -109,12 +110,13 @@ def lib():
         L = C.CDLL(LIB_PATH)
         L.wam_last_error.restype = C.c_char_p
         L.wam_abi_version.restype = _i32
-        for name in ("wam_block_workspace_bytes", "wam_step_workspace_bytes",
+        for name in ("wam_block_workspace_bytes", "wam_step_workspace_bytes", "wam_update_workspace_bytes",
                      "wam_time_embed_workspace_bytes", "wam_text_proj_workspace_bytes",
                      "wam_embed_workspace_bytes", "wam_head_workspace_bytes"):
             getattr(L, name).restype = _sz
         L.wam_block_workspace_bytes.argtypes = [C.POINTER(wam_dims), _i32, _i32, _i32]
         L.wam_step_workspace_bytes.argtypes = [C.POINTER(wam_model), C.POINTER(wam_step_io)]
+        L.wam_update_workspace_bytes.argtypes = [C.POINTER(wam_model), C.POINTER(wam_step_io)]
         L.wam_time_embed_workspace_bytes.argtypes = [C.POINTER(wam_dims), _i32]
         L.wam_text_proj_workspace_bytes.argtypes = [C.POINTER(wam_dims), _i32, _i32]
         L.wam_embed_workspace_bytes.argtypes = [C.POINTER(wam_dims), _i32, _i32, _i32, _i32]
@@ -123,6 +125,7 @@ def lib():
         L.wam_dit_block_fwd.argtypes = [C.POINTER(wam_dims), C.POINTER(wam_block_weights),
                                         C.POINTER(wam_block_io), _vp, _sz, _vp]
         L.wam_dit_step_fwd.argtypes = [C.POINTER(wam_model), C.POINTER(wam_step_io), _vp, _sz, _vp]
+        L.wam_dit_update_fwd.argtypes = [C.POINTER(wam_model), C.POINTER(wam_step_io), _vp, _sz, _vp]
         L.wam_time_embed_fwd.argtypes = [C.POINTER(wam_model), _i32, _vp, _vp, _vp, _vp, _sz, _vp]
         L.wam_text_proj_fwd.argtypes = [C.POINTER(wam_model), _i32, _i32, _vp, _vp, _vp, _sz, _vp]
         L.wam_adaln_ln_mod.argtypes = [_i32, _i32, _i32, C.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
@@ -186,6 +189,14 @@ def cached_chunks(cache_len: int, L: int) -> wam_chunks:
     if cache_len:
         return make_chunks([cache_len, L], [L], [1])
     return make_chunks([L], [L], [0])
+
+
+def append_chunks(cached_sizes, new_sizes) -> wam_chunks:
+    """Query chunks of the given sizes appended after cached chunks of the given sizes
+    (global ids follow key-row order): the layout of a multi-chunk update pass."""
+    n = len(cached_sizes)
+    return make_chunks(list(cached_sizes) + list(new_sizes), list(new_sizes),
+                       list(range(n, n + len(new_sizes))))
 
 
 # ------------------------------------------------------------------------------------------
@@ -358,6 +369,16 @@ def wam_step_workspace_bytes(model: wam_model, io: wam_step_io) -> int:
 
 def wam_dit_step_fwd(model: wam_model, io: wam_step_io, ws, stream=None):
     _check(lib().wam_dit_step_fwd(C.byref(model), C.byref(io), _p(ws), ws.numel(), _stream(stream)))
+
+
+def wam_update_workspace_bytes(model: wam_model, io: wam_step_io) -> int:
+    return lib().wam_update_workspace_bytes(C.byref(model), C.byref(io))
+
+
+def wam_dit_update_fwd(model: wam_model, io: wam_step_io, ws, stream=None):
+    """Cache-update pass: appends every layer's K/V of the io's clean rows at
+    [cache_len, cache_len + L); v_video / v_action of io are not written."""
+    _check(lib().wam_dit_update_fwd(C.byref(model), C.byref(io), _p(ws), ws.numel(), _stream(stream)))
 
 
 def wam_chunk_positions(c, F, Hg, Wg, A):

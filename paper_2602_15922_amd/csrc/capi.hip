@@ -301,6 +301,29 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   return WAM_OK;
 }
 
+// The part of a block that an update pass needs from its last layer: AdaLN #1, the K|V
+// columns of the QKV projection, and RoPE on k with the cache append.
+wam_status block_kv_run(const wam_dims& D, const wam_block_weights& W, const wam_block_io& io, char* ws,
+                        hipStream_t s) {
+  const int d = D.d, B = io.B, L = io.L, M = B * L;
+  const BlockWs lay = block_ws(D, B, L, io.Lc);
+  void* h = ws + lay.h;
+  char* big = ws + lay.big;  // [M][3d] bf16
+  const float* m6 = W.mod6;
+  const float* e0 = io.e0;
+  const int64_t ms = 6 * (int64_t)d;
+  LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h};
+  HIPCHECK(launch_ln_mod(ln, s));
+  // rows d..3d of W_qkv (the k and v outputs) into columns d..3d of the [M][3d] buffer
+  const char* wkv = static_cast<const char*>(W.w_qkv) + (size_t)d * d * 2;
+  const float* bkv = W.b_qkv ? W.b_qkv + d : nullptr;
+  TRY(gemm_checked(gemm(M, 2 * d, d, WAM_EPI_BF16, h, d, wkv, bkv, big + (size_t)d * 2, 3 * d), s));
+  RopeArgs ra{B, L, D.H, D.Dh, io.Lcap, io.cache_len, big, io.rope_cos, io.rope_sin, nullptr, io.k_cache,
+              io.v_cache};
+  HIPCHECK(launch_rope_qkv(ra, s));
+  return WAM_OK;
+}
+
 // ---------------------------------------------------------------------------------
 // model-level pieces
 // ---------------------------------------------------------------------------------
@@ -425,7 +448,7 @@ wam_status check_ws(const void* ws, size_t have, size_t need) {
   return WAM_OK;
 }
 
-wam_status check_step(const wam_model& m, const wam_step_io& io) {
+wam_status check_step(const wam_model& m, const wam_step_io& io, bool head) {
   TRY(check_model_common(m));
   const wam_dims& D = m.dims;
   CHECK(D.n_layers >= 0, WAM_EINVAL, "n_layers < 0");
@@ -440,13 +463,15 @@ wam_status check_step(const wam_model& m, const wam_step_io& io) {
   int32_t kend[WAM_MAX_CHUNKS];
   TRY(check_chunks(io.ch, (int32_t)L, (int32_t)(io.cache_len + L), kend));
   TRY(need_ptr(io.z_t, "z_t")); TRY(need_ptr(io.t, "t")); TRY(need_ptr(io.text, "text"));
-  if (io.A > 0) { TRY(need_ptr(io.a_t, "a_t")); TRY(need_ptr(io.v_action, "v_action")); }
+  if (io.A > 0) TRY(need_ptr(io.a_t, "a_t"));
+  if (io.A > 0 && head) TRY(need_ptr(io.v_action, "v_action"));
   TRY(need_ptr(io.rope_cos, "rope_cos")); TRY(need_ptr(io.rope_sin, "rope_sin"));
-  TRY(need_ptr(io.v_video, "v_video"));
+  if (head) TRY(need_ptr(io.v_video, "v_video"));
   TRY(need_ptr(m.w_t1, "w_t1")); TRY(need_ptr(m.w_t2, "w_t2")); TRY(need_ptr(m.w_t6, "w_t6"));
   TRY(need_ptr(m.w_x1, "w_x1")); TRY(need_ptr(m.w_x2, "w_x2")); TRY(need_ptr(m.w_patch, "w_patch"));
-  TRY(need_ptr(m.w_hv, "w_hv")); TRY(need_ptr(m.head_mod2, "head_mod2"));
-  if (io.A > 0) { TRY(need_ptr(m.w_ain, "w_ain")); TRY(need_ptr(m.w_ha, "w_ha")); }
+  if (head) { TRY(need_ptr(m.w_hv, "w_hv")); TRY(need_ptr(m.head_mod2, "head_mod2")); }
+  if (io.A > 0) TRY(need_ptr(m.w_ain, "w_ain"));
+  if (io.A > 0 && head) TRY(need_ptr(m.w_ha, "w_ha"));
   if (D.n_layers > 0) {
     CHECK(m.blocks != nullptr, WAM_EINVAL, "blocks is NULL");
     CHECK(io.k_cache != nullptr && io.v_cache != nullptr, WAM_EINVAL, "k_cache/v_cache arrays are NULL");
@@ -612,7 +637,7 @@ size_t wam_step_workspace_bytes(const wam_model* m, const wam_step_io* io) {
 wam_status wam_dit_step_fwd(const wam_model* m, const wam_step_io* io, void* ws, size_t ws_bytes,
                             hipStream_t stream) {
   CHECK(m && io, WAM_EINVAL, "NULL model/io");
-  TRY(check_step(*m, *io));
+  TRY(check_step(*m, *io, true));
   const StepWs lay = step_ws(*m, *io);
   TRY(check_ws(ws, ws_bytes, lay.total));
   const wam_dims& D = m->dims;
@@ -638,6 +663,45 @@ wam_status wam_dit_step_fwd(const wam_model* m, const wam_step_io* io, void* ws,
     TRY(block_run(D, m->blocks[l], b, w + lay.block, stream, ev0, ev1));
   }
   TRY(head_run(*m, io->B, io->F, io->Hl, io->Wl, io->A, x, e, io->v_video, io->v_action, piece, stream));
+  return WAM_OK;
+}
+
+size_t wam_update_workspace_bytes(const wam_model* m, const wam_step_io* io) {
+  return wam_step_workspace_bytes(m, io);
+}
+
+wam_status wam_dit_update_fwd(const wam_model* m, const wam_step_io* io, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
+  CHECK(m && io, WAM_EINVAL, "NULL model/io");
+  TRY(check_step(*m, *io, false));
+  const StepWs lay = step_ws(*m, *io);
+  TRY(check_ws(ws, ws_bytes, lay.total));
+  const wam_dims& D = m->dims;
+  char* w = static_cast<char*>(ws);
+  float* x = reinterpret_cast<float*>(w + lay.x);
+  float* e = reinterpret_cast<float*>(w + lay.e);
+  float* e0 = reinterpret_cast<float*>(w + lay.e0);
+  void* ctx = w + lay.ctx;
+  char* piece = w + lay.piece;
+  const int32_t Lv = io->F * (io->Hl / 2) * (io->Wl / 2), L = Lv + io->A;
+
+  TRY(time_run(*m, io->B, io->t, e, e0, piece, stream));
+  if (!io->ctx_kv && D.n_layers > 1) TRY(text_run(*m, io->B, io->Lc, io->text, ctx, piece, stream));
+  TRY(embed_run(*m, io->B, io->F, io->Hl, io->Wl, io->A, io->z_t, io->a_t, x, piece, stream));
+  for (int l = 0; l < D.n_layers; ++l) {
+    wam_block_io b{};
+    b.x = x; b.e0 = e0; b.rope_cos = io->rope_cos; b.rope_sin = io->rope_sin;
+    b.k_cache = io->k_cache[l]; b.v_cache = io->v_cache[l]; b.Lcap = io->Lcap; b.cache_len = io->cache_len;
+    b.ch = io->ch; b.ctx = ctx; b.ctx_kv = io->ctx_kv ? io->ctx_kv[l] : nullptr;
+    b.B = io->B; b.L = L; b.Lc = io->Lc;
+    if (l + 1 == D.n_layers) {
+      TRY(block_kv_run(D, m->blocks[l], b, w + lay.block, stream));
+    } else {
+      hipEvent_t ev0 = io->attn_events ? io->attn_events[2 * l] : nullptr;
+      hipEvent_t ev1 = io->attn_events ? io->attn_events[2 * l + 1] : nullptr;
+      TRY(block_run(D, m->blocks[l], b, w + lay.block, stream, ev0, ev1));
+    }
+  }
   return WAM_OK;
 }
 

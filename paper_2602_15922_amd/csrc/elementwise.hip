@@ -11,24 +11,25 @@ namespace {
 // LayerNorm (biased variance, eps) of fp32 rows, then the optional affine and the
 // AdaLN modulation, to bf16.  Both are folded into one per-column affine,
 //   y = LN(x) * P + Q,  P = gamma (1 + scale),  Q = beta (1 + scale) + shift,
-// computed once per workgroup into LDS: a workgroup owns LN_ROWS rows of one sample,
-// so the modulation vectors are read once per LN_ROWS rows instead of once per row.
-// One wavefront per row; the row stays in registers between the mean, variance and
-// output passes, so x is read from HBM once.
+// computed once per workgroup into LDS (2*d floats): a workgroup owns LN_ROWS rows of
+// one sample, so the modulation vectors are read once per LN_ROWS rows.  One wavefront
+// per row, so a 3152-row call keeps ~3150 rows in flight at once; the row stays in
+// registers (NV float4 per lane, NV = d/256) between the mean, variance and output
+// passes, so x is read from HBM once.
 // ---------------------------------------------------------------------------------
-constexpr int LN_MAXV = 32;   // d <= 32 * 256
-constexpr int LN_ROWS = 16;   // rows per workgroup (4 per wavefront)
+constexpr int LN_ROWS = 4;  // rows (= wavefronts) per workgroup
 
-__global__ __launch_bounds__(256) void ln_mod_kernel(const LnArgs a, int blocks_per_batch) {
-  __shared__ __attribute__((aligned(16))) float PQ[2 * LN_MAXV * 256];
+template <int NV>
+__global__ __launch_bounds__(LN_ROWS * 64) void ln_mod_kernel(const LnArgs a, int blocks_per_batch) {
+  extern __shared__ __attribute__((aligned(16))) float PQ[];  // [2][d]
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int b = blockIdx.x / blocks_per_batch;
-  const int r0 = (blockIdx.x % blocks_per_batch) * LN_ROWS;
+  const int rloc = (blockIdx.x % blocks_per_batch) * LN_ROWS + w;
   const int d = a.d, nv = d >> 8;
   const int64_t mb = (int64_t)b * a.mod_stride;
   float* P = PQ;
   float* Q = PQ + d;
-  for (int c = threadIdx.x * 4; c < d; c += 1024) {
+  for (int c = threadIdx.x * 4; c < d; c += LN_ROWS * 256) {
     f32x4 g = {1.f, 1.f, 1.f, 1.f}, bt = {0.f, 0.f, 0.f, 0.f}, sc = {0.f, 0.f, 0.f, 0.f}, sh = {0.f, 0.f, 0.f, 0.f};
     if (a.gamma) g = *reinterpret_cast<const f32x4*>(a.gamma + c);
     if (a.beta) bt = *reinterpret_cast<const f32x4*>(a.beta + c);
@@ -41,44 +42,41 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const LnArgs a, int blocks_
     *reinterpret_cast<f32x4*>(Q + c) = bt * (one + sc) + sh;
   }
   __syncthreads();
-  for (int rr = w; rr < LN_ROWS; rr += 4) {
-    const int rloc = r0 + rr;
-    if (rloc >= a.rows_per_batch) break;
-    const int64_t row = (int64_t)b * a.rows_per_batch + rloc;
-    const float* xr = a.x + row * d;
-    f32x4 v[LN_MAXV];
-    float s = 0.f;
+  if (rloc >= a.rows_per_batch) return;
+  const int64_t row = (int64_t)b * a.rows_per_batch + rloc;
+  const float* xr = a.x + row * d;
+  f32x4 v[NV];
+  float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < LN_MAXV; ++i)
-      if (i < nv) {
-        v[i] = *reinterpret_cast<const f32x4*>(xr + (i * 64 + lane) * 4);
-        s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
+  for (int i = 0; i < NV; ++i)
+    if (i < nv) {
+      v[i] = *reinterpret_cast<const f32x4*>(xr + (i * 64 + lane) * 4);
+      s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
+    }
+  const float mean = wave_sum(s) / (float)d;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+    if (i < nv) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float t = v[i][j] - mean;
+        q += t * t;
       }
-    const float mean = wave_sum(s) / (float)d;
-    float q = 0.f;
+    }
+  const float rstd = rsqrtf(wave_sum(q) / (float)d + a.eps);
+  bf16* hr = static_cast<bf16*>(a.h) + row * d;
 #pragma unroll
-    for (int i = 0; i < LN_MAXV; ++i)
-      if (i < nv) {
+  for (int i = 0; i < NV; ++i)
+    if (i < nv) {
+      const int col = (i * 64 + lane) * 4;
+      const f32x4 pp = *reinterpret_cast<const f32x4*>(P + col);
+      const f32x4 qq = *reinterpret_cast<const f32x4*>(Q + col);
+      bf16x4 o;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float t = v[i][j] - mean;
-          q += t * t;
-        }
-      }
-    const float rstd = rsqrtf(wave_sum(q) / (float)d + a.eps);
-    bf16* hr = static_cast<bf16*>(a.h) + row * d;
-#pragma unroll
-    for (int i = 0; i < LN_MAXV; ++i)
-      if (i < nv) {
-        const int col = (i * 64 + lane) * 4;
-        const f32x4 pp = *reinterpret_cast<const f32x4*>(P + col);
-        const f32x4 qq = *reinterpret_cast<const f32x4*>(Q + col);
-        bf16x4 o;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) o[j] = (bf16)((v[i][j] - mean) * rstd * pp[j] + qq[j]);
-        *reinterpret_cast<bf16x4*>(hr + col) = o;
-      }
-  }
+      for (int j = 0; j < 4; ++j) o[j] = (bf16)((v[i][j] - mean) * rstd * pp[j] + qq[j]);
+      *reinterpret_cast<bf16x4*>(hr + col) = o;
+    }
 }
 
 // ---------------------------------------------------------------------------------
@@ -96,7 +94,8 @@ __global__ __launch_bounds__(256) void rope_qkv_kernel(const RopeArgs a) {
   const int col = c * 8;            // column inside the d-wide q/k/v slice
   const int pair0 = (col % a.Dh) >> 1;  // first rotation pair inside the head
   const bf16* src = static_cast<const bf16*>(a.qkv) + bl * 3 * d + col;
-  const bf16x8 qv = load_bf16x8(src), kv = load_bf16x8(src + d), vv = load_bf16x8(src + 2 * d);
+  const bf16x8 qv = a.q_out ? load_bf16x8(src) : bf16x8{};
+  const bf16x8 kv = load_bf16x8(src + d), vv = load_bf16x8(src + 2 * d);
   const f32x4 cs = *reinterpret_cast<const f32x4*>(a.cos_t + (int64_t)l * (a.Dh >> 1) + pair0);
   const f32x4 sn = *reinterpret_cast<const f32x4*>(a.sin_t + (int64_t)l * (a.Dh >> 1) + pair0);
   bf16x8 qo, ko;
@@ -109,7 +108,7 @@ __global__ __launch_bounds__(256) void rope_qkv_kernel(const RopeArgs a) {
     ko[2 * p] = (bf16)(k0 * cs[p] - k1 * sn[p]);
     ko[2 * p + 1] = (bf16)(k0 * sn[p] + k1 * cs[p]);
   }
-  *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.q_out) + bl * d + col) = qo;
+  if (a.q_out) *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.q_out) + bl * d + col) = qo;
   const int64_t crow = ((int64_t)b * a.Lcap + a.row0 + l) * d + col;
   *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.k_cache) + crow) = ko;
   *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.v_cache) + crow) = vv;
@@ -202,7 +201,13 @@ hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s) {
   if (a.rows == 0) return hipSuccess;
   const int B = a.rows / a.rows_per_batch;
   const int bpb = (a.rows_per_batch + LN_ROWS - 1) / LN_ROWS;
-  hipLaunchKernelGGL(ln_mod_kernel, dim3((unsigned)(B * bpb)), dim3(256), 0, s, a, bpb);
+  const dim3 grid((unsigned)(B * bpb)), block(LN_ROWS * 64);
+  const size_t lds = (size_t)2 * a.d * sizeof(float);  // d <= 8192: at most 64 KB
+  const int nv = a.d / 256;
+  if (nv <= 2) hipLaunchKernelGGL(ln_mod_kernel<2>, grid, block, lds, s, a, bpb);
+  else if (nv <= 8) hipLaunchKernelGGL(ln_mod_kernel<8>, grid, block, lds, s, a, bpb);
+  else if (nv <= 20) hipLaunchKernelGGL(ln_mod_kernel<20>, grid, block, lds, s, a, bpb);
+  else hipLaunchKernelGGL(ln_mod_kernel<32>, grid, block, lds, s, a, bpb);
   return hipGetLastError();
 }
 

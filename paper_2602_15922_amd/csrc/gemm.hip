@@ -2,9 +2,10 @@
 //
 // A [M][K] and W [N][K] are both K-contiguous, which is exactly the operand layout
 // of the 32x32x16 bf16 MFMA (8 consecutive k per lane for A rows and W rows), so no
-// transpose is ever needed.  A workgroup of 4 wavefronts (2x2) computes a BM x BN
-// tile.  BK-wide slices of A and W are fetched with direct global->LDS loads into a
-// ring of STAGES LDS buffers: the loads of slice t+STAGES-1 are issued while slice t
+// transpose is ever needed.  A workgroup of WM x WN wavefronts computes a BM x BN
+// tile.  The large tiles use 8 wavefronts (two per SIMD), so one wavefront's barrier
+// and LDS waits overlap the other's MFMAs.  BK-wide slices of A and W are fetched
+// with direct global->LDS loads into a ring of STAGES LDS buffers: the loads of slice t+STAGES-1 are issued while slice t
 // is consumed, so each load has STAGES-1 slices of MFMA work to land (no staging
 // registers, one barrier per slice, waits on the vector-memory counter only for the
 // slice about to be used).  Within a slice the fragment reads of the next 16-wide
@@ -20,16 +21,19 @@
 namespace wam {
 namespace {
 
-template <int BM_, int BN_, int BK_, int STAGES_>
+template <int BM_, int BN_, int BK_, int STAGES_, int WM_, int WN_, int OCC_>
 struct Cfg {
   static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_;
-  static constexpr int WM = 2, WN = 2;            // wave grid
+  static constexpr int WM = WM_, WN = WN_;        // wave grid
+  static constexpr int OCC = OCC_;                // wavefronts per SIMD the kernel is built for
+  static constexpr int NW = WM * WN, NT = NW * 64;
   static constexpr int TM = BM / WM / 32;         // 32x32 tiles per wave, rows
   static constexpr int TN = BN / WN / 32;         // 32x32 tiles per wave, cols
   static constexpr int CPR = BK / 8;              // 16-byte chunks per LDS row
-  static constexpr int NIA = BM * CPR / 256;      // direct-load instructions per wave (A)
-  static constexpr int NIB = BN * CPR / 256;      // (W)
+  static constexpr int NIA = BM * CPR / (NW * 64);  // direct-load instructions per wave (A)
+  static constexpr int NIB = BN * CPR / (NW * 64);  // (W)
   static constexpr int STAGE = (BM + BN) * BK;    // elements per stage
+  static_assert(NIA * NW * 64 == BM * CPR && NIB * NW * 64 == BN * CPR, "slice not a whole number of wave loads");
   // XOR pattern.  gfx950 LDS serves 256 bytes (64 banks) per cycle, i.e. 16 lanes of a
   // 16-byte read; the 16 consecutive rows those lanes read at one logical chunk must land
   // on 16 distinct 16-byte bank slots.  128-byte rows (8 chunks): two rows share a
@@ -119,7 +123,7 @@ WAM_DEV void fetch_slice(bf16* dst, const bf16* base, const int64_t* src, const 
 #define WAM_WAIT_LGKMCNT0() __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4))
 
 template <typename C, int EPI>
-__global__ __launch_bounds__(256) void gemm_nt(const GemmArgs g, int tiles_m, int tiles_n) {
+__global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int tiles_m, int tiles_n) {
   constexpr int BM = C::BM, BN = C::BN, BK = C::BK, S = C::STAGES;
   __shared__ __attribute__((aligned(16))) bf16 smem[S * C::STAGE];
   auto As = [&](int buf) { return smem + buf * C::STAGE; };
@@ -134,7 +138,7 @@ __global__ __launch_bounds__(256) void gemm_nt(const GemmArgs g, int tiles_m, in
   const int tm = lid % tiles_m, tn = lid / tiles_m;  // consecutive tiles share a W panel
   const int m0 = tm * BM, n0 = tn * BN;
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;  // w < C::NW
   const int hh = lane >> 5, l32 = lane & 31;
   const int wm = w / C::WN, wn = w % C::WN;
 
@@ -166,7 +170,7 @@ __global__ __launch_bounds__(256) void gemm_nt(const GemmArgs g, int tiles_m, in
   for (int c = 0; c < C::NIA; ++c) kla[c] = C::pch((w * C::NIA + c) * RPI + lrow, lane % C::CPR) * 8;
 #pragma unroll
   for (int c = 0; c < C::NIB; ++c) klb[c] = C::pch((w * C::NIB + c) * RPI + lrow, lane % C::CPR) * 8;
-  auto fetch = [&](int kt) {  // plain LDS code only (the direct-load builtin is in fetch_slice)
+  auto fetch = [&](int kt) {  // no device builtins in lambdas (they drop the host kernel stub)
     const int buf = kt % S;
     fetch_slice<C::NIA>(As(buf), A, a_src, kla, kt * BK, g.K, w);
     fetch_slice<C::NIB>(Bs(buf), W, b_src, klb, kt * BK, g.K, w);
@@ -268,7 +272,7 @@ __global__ __launch_bounds__(256) void gemm_nt(const GemmArgs g, int tiles_m, in
 template <typename Cf>
 hipError_t launch_cfg(const GemmArgs& g, hipStream_t s) {
   const int tm = (g.M + Cf::BM - 1) / Cf::BM, tn = (g.N + Cf::BN - 1) / Cf::BN;
-  dim3 grid(tm * tn), block(256);
+  dim3 grid(tm * tn), block(Cf::NT);
   switch (g.epi) {
     case WAM_EPI_BF16: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_BF16>), grid, block, 0, s, g, tm, tn); break;
     case WAM_EPI_GELU_BF16: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_GELU_BF16>), grid, block, 0, s, g, tm, tn); break;
@@ -285,20 +289,21 @@ hipError_t launch_gemm(const GemmArgs& gin, hipStream_t s) {
   if (g.a_rows <= 0) { g.a_rows = g.M; g.a_bs = 0; }
   if (g.o_rows <= 0) { g.o_rows = g.M; g.o_bs = 0; }
   if (g.gate_rows <= 0) { g.gate_rows = g.M; g.gate_stride = 0; }
-  // Pick the tile whose rounds of 256 concurrent workgroups cost least, weighting
-  // smaller tiles by their lower MFMA efficiency (measured).
-  struct Opt { int bm, bn; float eff; };
-  const Opt opts[3] = {{256, 256, 1.0f}, {128, 256, 0.85f}, {128, 128, 0.6f}};
+  // Pick the tile whose rounds of concurrent workgroups cost least (per_cu workgroups
+  // of a tile fit one CU), weighting tiles by their measured MFMA efficiency.
+  struct Opt { int bm, bn, per_cu; float eff; };
+  const Opt opts[3] = {{256, 256, 1, 1.0f}, {128, 256, 1, 0.85f}, {128, 128, 2, 0.6f}};
   int best = 0;
   float best_cost = 0.f;
   for (int i = 0; i < 3; ++i) {
     const long tiles = (long)((g.M + opts[i].bm - 1) / opts[i].bm) * ((g.N + opts[i].bn - 1) / opts[i].bn);
-    const float cost = (float)((tiles + 255) / 256) * opts[i].bm * opts[i].bn / opts[i].eff;
+    const long slots = 256L * opts[i].per_cu;
+    const float cost = (float)((tiles + slots - 1) / slots) * opts[i].bm * opts[i].bn * opts[i].per_cu / opts[i].eff;
     if (i == 0 || cost < best_cost) { best = i; best_cost = cost; }
   }
-  if (best == 0) return launch_cfg<Cfg<256, 256, 32, 4>>(g, s);
-  if (best == 1) return launch_cfg<Cfg<128, 256, 64, 3>>(g, s);
-  return launch_cfg<Cfg<128, 128, 64, 3>>(g, s);
+  if (best == 0) return launch_cfg<Cfg<256, 256, 32, 4, 2, 4, 2>>(g, s);
+  if (best == 1) return launch_cfg<Cfg<128, 256, 64, 3, 2, 4, 2>>(g, s);
+  return launch_cfg<Cfg<128, 128, 64, 2, 2, 2, 2>>(g, s);
 }
 
 }  // namespace wam

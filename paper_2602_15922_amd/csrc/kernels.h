@@ -55,7 +55,7 @@ struct RopeArgs {
   int32_t B, L, H, Dh, Lcap, row0;
   const void* qkv;
   const float *cos_t, *sin_t;
-  void *q_out, *k_cache, *v_cache;
+  void *q_out, *k_cache, *v_cache;  // q_out NULL: q is neither rotated nor stored
 };
 hipError_t launch_rope_qkv(const RopeArgs& a, hipStream_t s);
 

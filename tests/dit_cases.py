@@ -151,3 +151,87 @@ class StepCase:
         w.wam_dit_step_fwd(self.model, io, ws)
         torch.cuda.synchronize()
         return vv, va
+
+
+# ------------------------------------------------------------------------------ update pass
+class UpdateCase:
+    """The cache-update pass over `n_new` clean video-only chunks of `wl` (wl.A must be 0),
+    appended after wl.n_cached seeded cached chunks, through n_layers seeded blocks."""
+
+    def __init__(self, wl, n_layers, n_new, t_clean=1.0, bias_std=0.0, spare_rows=64):
+        assert wl.A == 0
+        self.wl, self.n_layers, self.n_new, self.bias_std = wl, n_layers, n_new, bias_std
+        B, s = wl.B, wl.seed
+        self.P = synth.model_params(wl, bias_std=bias_std)
+        self.z = synth.normal(s, "z_clean", (B, wl.latent_ch, wl.F * n_new, wl.Hl, wl.Wl), 1.0)
+        self.a = synth.zeros((B, 0, wl.act_dim), "bf16")
+        self.t = synth.Tensor("f32", np.full(B, t_clean, dtype=np.float32))
+        self.text = synth.normal(s, "text", (B, wl.Lc, wl.text_dim), 1.0)
+        self.L = n_new * wl.L
+        self.Lcap = wl.cache_rows + self.L + spare_rows
+        self.chunk_ids = np.arange(wl.n_cached, wl.n_cached + n_new)
+
+    def layer(self, l):
+        W = synth.block_params(self.wl, l, self.bias_std, mod_std=self.wl.mod_std)
+        kc, vc = synth.kv_cache(self.wl, l) if self.wl.n_cached else (None, None)
+        return W, kc, vc
+
+    def positions_oracle(self):
+        wl = self.wl
+        return np.concatenate([oracle.chunk_positions(int(c), wl.F, wl.Hg, wl.Wg, 0) for c in self.chunk_ids])
+
+    def run_oracle(self):
+        wl = self.wl
+
+        def layers(l):
+            W, kc, vc = self.layer(l)
+            return f64(W), (kc.f64 if kc is not None else None), (vc.f64 if vc is not None else None)
+
+        return oracle.dit_update(self.z.f64, self.a.f64, self.t.f64, self.text.f64, f64(self.P), layers,
+                                 self.n_layers, wl.H, wl.eps, self.positions_oracle(),
+                                 np.repeat(self.chunk_ids, wl.L),
+                                 prev_chunk=prev_chunk_ids(wl) if wl.n_cached else None)
+
+    def upload(self):
+        import torch
+        w = lib()
+        wl, B = self.wl, self.wl.B
+        self.top = {k: dev(v) for k, v in self.P.items()}
+        self.blocks, self.kcs, self.vcs = [], [], []
+        for l in range(self.n_layers):
+            W, kc, vc = self.layer(l)
+            self.blocks.append({k: dev(v) for k, v in W.items()})
+            k = torch.zeros((B, self.Lcap, wl.H, wl.Dh), dtype=torch.bfloat16, device="cuda")
+            v = torch.zeros_like(k)
+            if kc is not None:
+                k[:, :wl.cache_rows] = dev(kc)
+                v[:, :wl.cache_rows] = dev(vc)
+            self.kcs.append(k)
+            self.vcs.append(v)
+        self.model = w.make_model(dims_of(wl, self.n_layers), self.top, self.blocks)
+        self.dz, self.da, self.dt, self.dtext = dev(self.z), dev(self.a), dev(self.t), dev(self.text)
+
+    def run_gpu(self, chunks_at_once=None):
+        """Appends the new chunks `chunks_at_once` at a time (default: all in one call).
+        Returns the per-layer device caches."""
+        import torch
+        w = lib()
+        wl = self.wl
+        if not hasattr(self, "model"):
+            self.upload()
+        step = chunks_at_once or self.n_new
+        cache_len = wl.cache_rows
+        for c0 in range(0, self.n_new, step):
+            ids = self.chunk_ids[c0:c0 + step]
+            pos = np.concatenate([w.wam_chunk_positions(int(c), wl.F, wl.Hg, wl.Wg, 0) for c in ids])
+            cos, sin = w.wam_rope_tables(pos, wl.Dh)
+            cos, sin = dev(cos), dev(sin)
+            z = self.dz[:, :, c0 * wl.F:(c0 + len(ids)) * wl.F].contiguous()
+            chunks = w.append_chunks([wl.L] * (wl.n_cached + c0), [wl.L] * len(ids))
+            io = w.make_step_io(z, self.da, self.dt, self.dtext, self.kcs, self.vcs, cos, sin, cache_len,
+                                chunks, None, None)
+            ws = workspace(w.wam_update_workspace_bytes(self.model, io))
+            w.wam_dit_update_fwd(self.model, io, ws)
+            torch.cuda.synchronize()
+            cache_len += len(ids) * wl.L
+        return self.kcs, self.vcs

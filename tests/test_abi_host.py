@@ -95,6 +95,8 @@ def test_gemm_and_block_reject_bad_arguments():
     bad = w.make_dims(d=500, H=5, Dh=100, ffn=2048, n_layers=1)
     assert L.wam_dit_block_fwd(C.byref(bad), C.byref(wts), C.byref(io), None, 0, None) == b.WAM_EUNSUPPORTED
     assert L.wam_block_workspace_bytes(C.byref(dims), 1, 144, 32) > 0
+    assert L.wam_dit_step_fwd(None, None, None, 0, None) == b.WAM_EINVAL
+    assert L.wam_dit_update_fwd(None, None, None, 0, None) == b.WAM_EINVAL
 
 
 def test_rope_tables_and_positions_agree_with_the_oracle():

@@ -464,6 +464,124 @@ def test_step_identity_blocks_reduce_to_embed_and_head():
                 assert np.allclose(va[b, tok - Lv], P["w_ha"] @ ht + P["b_ha"], atol=1e-10)
 
 
+# ----------------------------------------------------------------------------- update pass
+def small_model_params(g, d, C, ad, tdim):
+    return {"w_t1": g.standard_normal((d, 256)) * 0.1, "b_t1": g.standard_normal(d) * 0.1,
+            "w_t2": g.standard_normal((d, d)) * 0.1, "b_t2": g.standard_normal(d) * 0.1,
+            "w_t6": g.standard_normal((6 * d, d)) * 0.1, "b_t6": g.standard_normal(6 * d) * 0.1,
+            "w_x1": g.standard_normal((d, tdim)) * 0.1, "b_x1": np.zeros(d),
+            "w_x2": g.standard_normal((d, d)) * 0.1, "b_x2": np.zeros(d),
+            "w_patch": g.standard_normal((d, C * 4)), "b_patch": g.standard_normal(d),
+            "w_ain": g.standard_normal((d, ad)), "b_ain": g.standard_normal(d),
+            "w_hv": g.standard_normal((C * 4, d)), "b_hv": g.standard_normal(C * 4),
+            "w_ha": g.standard_normal((ad, d)), "b_ha": g.standard_normal(ad),
+            "head_mod2": g.standard_normal((2, d)) * 0.1}
+
+
+def test_update_two_chunks_equal_two_sequential_updates():
+    """Algorithm 2's cache update with two clean chunks in one call (block-causal mask,
+    Figure 10b) appends exactly what two successive single-chunk updates append, each
+    layer seeing its own cache (section 3.1, Model Inference)."""
+    g = np.random.default_rng(110)
+    B, C, F, Hl, Wl, ad, d, H, n_layers, Lc, tdim = 2, 4, 2, 4, 6, 5, 16, 2, 3, 3, 12
+    P = small_model_params(g, d, C, ad, tdim)
+    Ws = [small_block_weights(d, 32, 111 + l) for l in range(n_layers)]
+    Hg, Wg = Hl // 2, Wl // 2
+    Lch = F * Hg * Wg
+    # one cached chunk (id 0) per layer, then clean chunks 1 and 2 (video only)
+    kc0 = [g.standard_normal((B, Lch, H, d // H)) for _ in range(n_layers)]
+    vc0 = [g.standard_normal((B, Lch, H, d // H)) for _ in range(n_layers)]
+    z = g.standard_normal((B, C, 2 * F, Hl, Wl))  # frames of chunks 1 and 2
+    a = np.zeros((B, 0, ad))
+    t = np.array([1.0, 1.0])
+    text = g.standard_normal((B, Lc, tdim))
+    pos = np.concatenate([chunk_positions(1, F, Hg, Wg, 0), chunk_positions(2, F, Hg, Wg, 0)])
+    q_chunk = np.repeat([1, 2], Lch)
+    joint = oracle.dit_update(z, a, t, text, P, lambda l: (Ws[l], kc0[l], vc0[l]), n_layers, H, 1e-6,
+                              pos, q_chunk, prev_chunk=np.zeros(Lch, int))
+    first = oracle.dit_update(z[:, :, :F], a, t, text, P, lambda l: (Ws[l], kc0[l], vc0[l]), n_layers, H,
+                              1e-6, pos[:Lch], q_chunk[:Lch], prev_chunk=np.zeros(Lch, int))
+    kc1 = [np.concatenate([kc0[l], first[l][0]], 1) for l in range(n_layers)]
+    vc1 = [np.concatenate([vc0[l], first[l][1]], 1) for l in range(n_layers)]
+    second = oracle.dit_update(z[:, :, F:], a, t, text, P, lambda l: (Ws[l], kc1[l], vc1[l]), n_layers, H,
+                               1e-6, pos[Lch:], q_chunk[Lch:], prev_chunk=np.repeat([0, 1], Lch))
+    for l in range(n_layers):
+        assert np.allclose(joint[l][0][:, :Lch], first[l][0], atol=1e-12)
+        assert np.allclose(joint[l][1][:, :Lch], first[l][1], atol=1e-12)
+        assert np.allclose(joint[l][0][:, Lch:], second[l][0], atol=1e-12)
+        assert np.allclose(joint[l][1][:, Lch:], second[l][1], atol=1e-12)
+    # chunk 1's rows must not see chunk 2: perturbing chunk 2's latents leaves them unchanged
+    z2 = z.copy()
+    z2[:, :, F:] += 1.0
+    pert = oracle.dit_update(z2, a, t, text, P, lambda l: (Ws[l], kc0[l], vc0[l]), n_layers, H, 1e-6,
+                             pos, q_chunk, prev_chunk=np.zeros(Lch, int))
+    for l in range(n_layers):
+        assert np.array_equal(pert[l][0][:, :Lch], joint[l][0][:, :Lch])
+        assert not np.allclose(pert[l][0][:, Lch:], joint[l][0][:, Lch:])
+
+
+def test_update_identity_blocks_closed_form():
+    """With every block the identity (zero gates, W_co = b_co = 0), each layer's residual
+    input is the patch embedding of the clean latents, so the appended K and V of layer l
+    are that layer's projection of LN(x)(1+scale)+shift, with K rotated pair by pair at
+    the token's (frame, row, column) position; written out here token by token."""
+    g = np.random.default_rng(120)
+    B, C, F, Hl, Wl, ad, d, H, n_layers, Lc, tdim = 1, 2, 2, 4, 4, 3, 12, 1, 2, 2, 8
+    Dh = d // H
+    P = small_model_params(g, d, C, ad, tdim)
+    for gate in (2, 5):
+        P["w_t6"][gate * d:(gate + 1) * d] = 0.0
+        P["b_t6"][gate * d:(gate + 1) * d] = 0.0
+    Ws = []
+    for l in range(n_layers):
+        W = small_block_weights(d, 24, 121 + l)
+        W["mod6"][2] = W["mod6"][5] = 0.0
+        W["w_co"] = np.zeros((d, d))
+        W["b_co"] = np.zeros(d)
+        Ws.append(W)
+    z = g.standard_normal((B, C, F, Hl, Wl))
+    t = np.array([0.6])
+    text = g.standard_normal((B, Lc, tdim))
+    c = 3  # chunk index of the clean chunk; no cache rows
+    Hg, Wg = Hl // 2, Wl // 2
+    pos = chunk_positions(c, F, Hg, Wg, 0)
+    kv = oracle.dit_update(z, np.zeros((B, 0, ad)), t, text, P, lambda l: (Ws[l], None, None), n_layers, H,
+                           1e-6, pos, np.full(F * Hg * Wg, c))
+    # e0 by hand
+    s = np.array([math.cos(1000 * t[0] * 10000 ** (-k / 128)) for k in range(128)]
+                 + [math.sin(1000 * t[0] * 10000 ** (-k / 128)) for k in range(128)])
+    h1 = P["w_t1"] @ s + P["b_t1"]
+    h1 = h1 / (1 + np.exp(-h1))
+    e = P["w_t2"] @ h1 + P["b_t2"]
+    se = e / (1 + np.exp(-e))
+    e0 = (P["w_t6"] @ se + P["b_t6"]).reshape(6, d)
+    seg = (Dh - 4 * (Dh // 6), 2 * (Dh // 6), 2 * (Dh // 6))
+    for l in range(n_layers):
+        m = Ws[l]["mod6"] + e0
+        for tok in range(F * Hg * Wg):
+            f, rem = divmod(tok, Hg * Wg)
+            r, s_ = divmod(rem, Wg)
+            feat = np.array([z[0, ch, f, 2 * r + ph, 2 * s_ + pw] for ch in range(C) for ph in range(2)
+                             for pw in range(2)])
+            xt = P["w_patch"] @ feat + P["b_patch"]
+            ht = (xt - xt.mean()) / math.sqrt(xt.var() + 1e-6) * (1 + m[1]) + m[0]
+            kraw = Ws[l]["w_qkv"][d:2 * d] @ ht + Ws[l]["b_qkv"][d:2 * d]
+            vraw = Ws[l]["w_qkv"][2 * d:] @ ht + Ws[l]["b_qkv"][2 * d:]
+            p3 = (F * c + f, r, s_)
+            krot = kraw.copy()
+            for hd in range(H):
+                base = hd * Dh
+                for ax in range(3):
+                    for i in range(seg[ax] // 2):
+                        ang = p3[ax] * 10000.0 ** (-2.0 * i / seg[ax])
+                        x0, x1 = kraw[base + 2 * i], kraw[base + 2 * i + 1]
+                        krot[base + 2 * i] = x0 * math.cos(ang) - x1 * math.sin(ang)
+                        krot[base + 2 * i + 1] = x0 * math.sin(ang) + x1 * math.cos(ang)
+                    base += seg[ax]
+            assert np.allclose(kv[l][0][0, tok].reshape(d), krot, atol=1e-10)
+            assert np.allclose(kv[l][1][0, tok].reshape(d), vraw, atol=1e-10)
+
+
 # ----------------------------------------------------------------------------- shared input generator
 def test_bf16_rounding_matches_torch():
     torch = pytest.importorskip("torch")

@@ -1,0 +1,157 @@
+"""GPU parity of wam_dit_update_fwd (the cache-update pass of Algorithm 2) against the
+fp64 oracle: the K/V rows it appends for every layer (relative L2 <= 2e-2, the block
+tolerance), that it writes nothing else, that several chunks in one masked call append
+what successive single-chunk calls append, and the prefill -> denoising-step flow."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from dit_cases import UpdateCase, dims_of, f64
+from gpu_helpers import dev, host, log, rel_l2, workspace
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-2
+
+
+def lib():
+    import paper_2602_15922_amd as w
+    return w
+
+
+def check_appended(case, kcs, vcs, ref, tol=TOL):
+    wl = case.wl
+    r0, r1 = wl.cache_rows, wl.cache_rows + case.L
+    for l, (k_ref, v_ref) in enumerate(ref):
+        ek = rel_l2(host(kcs[l][:, r0:r1]), k_ref)
+        ev = rel_l2(host(vcs[l][:, r0:r1]), v_ref)
+        print(f"  layer {l}: appended K rel L2 {ek:.2e}, V {ev:.2e}", flush=True)
+        assert ek <= tol and ev <= tol
+
+
+def check_untouched(case, kcs, vcs):
+    """Rows before cache_len keep the seeded cache; rows past the appended ones stay zero."""
+    wl = case.wl
+    r1 = wl.cache_rows + case.L
+    for l in range(case.n_layers):
+        _, kc, vc = case.layer(l)
+        if kc is not None:
+            assert np.array_equal(host(kcs[l][:, :wl.cache_rows]), kc.f64)
+            assert np.array_equal(host(vcs[l][:, :wl.cache_rows]), vc.f64)
+        assert not kcs[l][:, r1:].any().item() and not vcs[l][:, r1:].any().item()
+
+
+def small_wl(**kw):
+    base = dict(B=2, A=0, n_cached=1, n_layers=3, mod_std=0.3)
+    base.update(kw)
+    return synth.WORKLOADS["block_d512"].replace(**base)
+
+
+def test_update_two_chunks_in_one_call():
+    """d=512 model, 3 layers (the last one takes the K/V-only path), batch 2, one cached
+    chunk, two clean chunks appended in one block-causal call."""
+    wl = small_wl()
+    log("update small: two chunks at once")
+    case = UpdateCase(wl, 3, 2, bias_std=0.05)
+    kcs, vcs = case.run_gpu()
+    log("update small: oracle")
+    check_appended(case, kcs, vcs, case.run_oracle())
+    check_untouched(case, kcs, vcs)
+
+
+def test_update_joint_equals_sequential():
+    """Two chunks in one masked call vs one chunk per call: rows of each chunk see exactly
+    the same keys either way, so the appended K/V agree (to within kernel rounding)."""
+    wl = small_wl()
+    log("update small: joint")
+    joint = UpdateCase(wl, 3, 2, bias_std=0.05)
+    kj, vj = joint.run_gpu()
+    log("update small: sequential")
+    seq = UpdateCase(wl, 3, 2, bias_std=0.05)
+    ks, vs = seq.run_gpu(chunks_at_once=1)
+    for l in range(3):
+        a, b = host(kj[l]), host(ks[l])
+        same = np.array_equal(a, b) and np.array_equal(host(vj[l]), host(vs[l]))
+        e = max(rel_l2(a, b), rel_l2(host(vj[l]), host(vs[l])))
+        print(f"  layer {l}: joint vs sequential rel L2 {e:.2e} (bitwise equal: {same})", flush=True)
+        assert e <= 1e-3
+
+
+def test_update_single_layer_no_cache():
+    """The first prefill of an episode: no cache, one chunk, a one-layer model (the whole
+    pass is the K/V-only path)."""
+    wl = small_wl(n_cached=0, n_layers=1, B=1)
+    log("update small: first prefill, depth 1")
+    case = UpdateCase(wl, 1, 1)
+    kcs, vcs = case.run_gpu()
+    check_appended(case, kcs, vcs, case.run_oracle())
+    check_untouched(case, kcs, vcs)
+
+
+def test_prefill_then_denoising_step():
+    """Algorithm 2's order: a clean chunk is appended by the update pass, then a denoising
+    step of the next chunk (video + action tokens) attends to it; the velocities match the
+    oracle running the same two calls."""
+    import torch
+    w = lib()
+    wl = small_wl(n_cached=1, n_layers=2, B=2)
+    log("prefill -> step: update")
+    case = UpdateCase(wl, 2, 1, spare_rows=wl.L + 16)
+    kcs, vcs = case.run_gpu()
+    # the step: chunk id 2 with 16 action tokens, cache = [seeded chunk 0, appended chunk 1]
+    A = 16
+    c = wl.n_cached + 1
+    s = wl.seed
+    z = synth.normal(s, "z_t", (wl.B, wl.latent_ch, wl.F, wl.Hl, wl.Wl), 1.0)
+    a = synth.normal(s, "a_t", (wl.B, A, wl.act_dim), 1.0)
+    t = synth.uniform(s, "t", (wl.B,))
+    cache_len = wl.cache_rows + case.L
+    Lstep = wl.L + A
+    pos = w.wam_chunk_positions(c, wl.F, wl.Hg, wl.Wg, A)
+    cos, sin = w.wam_rope_tables(pos, wl.Dh)
+    vv = torch.empty((wl.B, wl.latent_ch, wl.F, wl.Hl, wl.Wl), dtype=torch.float32, device="cuda")
+    va = torch.empty((wl.B, A, wl.act_dim), dtype=torch.float32, device="cuda")
+    io = w.make_step_io(dev(z), dev(a), dev(t), case.dtext, kcs, vcs, dev(cos), dev(sin), cache_len,
+                        w.append_chunks([wl.L] * c, [Lstep]), vv, va)
+    log("prefill -> step: step")
+    w.wam_dit_step_fwd(case.model, io, workspace(w.wam_step_workspace_bytes(case.model, io)))
+    torch.cuda.synchronize()
+
+    log("prefill -> step: oracle")
+    new = case.run_oracle()
+
+    def layers(l):
+        W, kc, vc = case.layer(l)
+        return f64(W), np.concatenate([kc.f64, new[l][0]], 1), np.concatenate([vc.f64, new[l][1]], 1)
+
+    rv, ra = oracle.dit_step(z.f64, a.f64, t.f64, case.text.f64, f64(case.P), layers, 2, wl.H, wl.eps, c,
+                             oracle.chunk_positions(c, wl.F, wl.Hg, wl.Wg, A),
+                             prev_chunk=np.repeat(np.arange(c), wl.L))
+    ev, ea = rel_l2(host(vv), rv), rel_l2(host(va), ra)
+    print(f"  step after prefill: rel L2 video {ev:.2e} action {ea:.2e}", flush=True)
+    assert ev <= TOL and ea <= TOL
+
+
+def test_update_14b_shapes_two_layers():
+    """The 14B block shapes: one clean chunk of 3120 video rows appended after two cached
+    ones (9360 keys), 512x4096 text, two layers (full block, then the K/V-only path)."""
+    wl = synth.WORKLOADS["block_14b"].replace(A=0, n_cached=2, n_layers=2)
+    log("update 14b: inputs + GPU")
+    case = UpdateCase(wl, 2, 1)
+    kcs, vcs = case.run_gpu()
+    log("update 14b: oracle")
+    check_appended(case, kcs, vcs, case.run_oracle())
+    check_untouched(case, kcs, vcs)
+
+
+def test_update_rejects_overflowing_cache():
+    w = lib()
+    wl = small_wl(n_cached=1, n_layers=1, B=1)
+    case = UpdateCase(wl, 1, 1, spare_rows=0)
+    case.upload()
+    pos = w.wam_chunk_positions(1, wl.F, wl.Hg, wl.Wg, 0)
+    cos, sin = (dev(x) for x in w.wam_rope_tables(pos, wl.Dh))
+    io = w.make_step_io(case.dz, case.da, case.dt, case.dtext, case.kcs, case.vcs, cos, sin, wl.cache_rows + 1,
+                        w.append_chunks([wl.L + 1], [wl.L]), None, None)
+    with pytest.raises(w.WamError, match="exceeds Lcap"):
+        w.wam_dit_update_fwd(case.model, io, workspace(w.wam_update_workspace_bytes(case.model, io)))
