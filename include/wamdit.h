@@ -96,8 +96,10 @@ typedef struct {
  * q_batch_stride; k, v: [B] x [Lk] x [H][Dh] bf16 sharing kv_tok_stride and
  * kv_batch_stride (k and v may be two halves of one [.., 2*d] buffer); o: written,
  * [B] x [Lq] x [H][Dh] bf16.  scale <= 0 selects 1/sqrt(Dh).  Dh must be 64 or 128.
- * Lq = 0 or B = 0 is a no-op.  o must not overlap q, k or v.  Deterministic: the
- * same inputs give bitwise the same output (no atomics, no split-K).
+ * Lq = 0 or B = 0 is a no-op.  o must not overlap q, k or v.  One sample's keys
+ * must span less than 2 GiB (Lk * kv_tok_stride * 2 bytes < 2^31; else
+ * WAM_EUNSUPPORTED).  Deterministic: the same inputs give bitwise the same output
+ * (no atomics, no split-K).
  * ------------------------------------------------------------------------------ */
 typedef struct {
   int32_t B, H, Dh, Lq, Lk;

@@ -9,9 +9,12 @@
 // 32 rows per wavefront, so a wavefront's whole state (Q fragments, score tile,
 // probabilities and the fp32 output accumulators) stays in ordinary VGPRs and two
 // wavefronts share each SIMD: one's softmax overlaps the other's MFMAs.  Key tiles of
-// 64 keys are double-buffered in LDS and fetched with direct global->LDS loads (no
-// staging registers): the next tile is in flight while the current one is consumed,
-// with one barrier per tile.  The score
+// 64 keys are double-buffered in LDS and fetched with buffer loads straight into LDS
+// (no staging registers; a scalar resource descriptor, a loop-invariant 32-bit lane
+// offset and a scalar per-tile offset, so the fetch costs no vector ALU work): the next
+// tile is in flight while the current one is consumed, with one barrier per tile.  The
+// main loop handles two tiles per iteration, one per LDS buffer, so every LDS operand
+// address is a lane base plus an immediate.  The score
 // tile is computed transposed, S^T = K Q^T, so a lane owns one query and its softmax
 // statistics stay in the lane (plus the partner lane l^32 holding the other half of
 // the keys); the output is accumulated transposed as well, O^T = V^T P^T, so the
@@ -61,23 +64,28 @@ template <int DH>
 WAM_DEV int vswz(int row, int ch) { return DH == 128 ? (ch ^ (4 * (row & 3))) : (ch ^ (4 * ((row >> 1) & 1))); }
 
 template <int DH>
-WAM_DEV void fetch_tile(bf16* Ks, const bf16* kp, const bf16* vp, int64_t kv_ts, int Lk, int kb, int w,
-                        const int* koff, const int* voff, const int* krow) {
+WAM_DEV void fetch_tile(bf16* Ks, __amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr, int kv_tsb, int Lk,
+                        int kb, int w, const int* koff, const int* voff, const int* krow) {
   constexpr int KCH = BN * (DH / 8) / NT;
   bf16* Vs = Ks + BN * DH;
-  const bf16* kt = kp + (int64_t)kb * kv_ts;
-  const bf16* vt = vp + (int64_t)kb * kv_ts;
-  const bool full = kb + BN <= Lk;  // uniform: no row of this tile needs clamping
+  const int soff = kb * kv_tsb;  // wave-uniform byte offset of the tile's first key row
+  if (kb + BN <= Lk) {
 #pragma unroll
-  for (int i = 0; i < KCH; ++i) {
-    const int base = (w * KCH + i) * 64;  // wave-uniform first unit of this instruction
-    int shift = 0;
-    if (!full) {
-      const int over = kb + krow[i] - (Lk - 1);
-      shift = over > 0 ? -over * (int)kv_ts : 0;
+    for (int i = 0; i < KCH; ++i) {
+      const int base = (w * KCH + i) * 64;  // wave-uniform first unit of this instruction
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void*)(Ks + base * 8), 16, koff[i], soff, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void*)(Vs + base * 8), 16, voff[i], soff, 0, 0);
     }
-    __builtin_amdgcn_global_load_lds(kt + koff[i] + shift, (lds_void*)(Ks + base * 8), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(vt + voff[i] + shift, (lds_void*)(Vs + base * 8), 16, 0, 0);
+  } else {
+    // ragged last tile: rows past Lk re-read the last key row (their scores are masked)
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int base = (w * KCH + i) * 64;
+      const int over = kb + krow[i] - (Lk - 1);
+      const int shift = over > 0 ? -over * kv_tsb : 0;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void*)(Ks + base * 8), 16, koff[i] + shift, soff, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void*)(Vs + base * 8), 16, voff[i] + shift, soff, 0, 0);
+    }
   }
 }
 
@@ -160,6 +168,21 @@ WAM_DEV void tile_sync() {
   __syncthreads();
 }
 
+// Key tile t from LDS buffer `cur` (a compile-time constant in the main loop), with tile
+// t+1 fetched into the other buffer meanwhile.
+template <int DH, bool MASK>
+WAM_DEV void attn_step(bf16* smem, int cur, __amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr, int kv_tsb,
+                       int Lk, int t, int ntiles, int w, const int* koff, const int* voff, const int* krow,
+                       const bf16x8* qf, f32x16* acc, float& m_ref, float& l_part, const int* kofs,
+                       const int* vofs, float c, float thr, int row_kend, int hh) {
+  constexpr int TILE = 2 * BN * DH;
+  const int kb = t * BN;
+  if (t + 1 < ntiles) fetch_tile<DH>(smem + (cur ^ 1) * TILE, kr, vr, kv_tsb, Lk, kb + BN, w, koff, voff, krow);
+  const char* Ks = reinterpret_cast<const char*>(smem + cur * TILE);
+  attn_tile<DH, MASK>(Ks, Ks + BN * DH * 2, qf, acc, m_ref, l_part, kofs, vofs, c, thr, kb, row_kend, hh);
+  tile_sync();
+}
+
 // CHUNKED: the keys form more than one chunk (cached chunks plus the current one), so a
 // query's visible prefix is looked up from its chunk; otherwise (cross-attention to the
 // text, or a single chunk) every query sees all Lk keys and only the ragged last tile
@@ -181,7 +204,8 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd(const AttnArgs a, int nqt) {
   const int qt = lid % nqt, hb = lid / nqt, h = hb % a.H, b = hb / a.H;
   const int q0 = qt * BM;
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, in a scalar register
   const int hh = lane >> 5, l32 = lane & 31;
 
   const int qrow = q0 + 32 * w + l32;
@@ -197,17 +221,22 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd(const AttnArgs a, int nqt) {
   const int kend_max = CHUNKED ? kend_of(a, last) : a.Lk;
   const int kend_min = CHUNKED ? kend_of(a, q0) : a.Lk;
 
+  // buffer resources over this (batch, head)'s keys: every offset the kernel forms is
+  // below Lk * row bytes (< 2^31, checked by the host), so the range check never fires
   const bf16* kp = static_cast<const bf16*>(a.k) + b * a.kv_bs + h * DH;
   const bf16* vp = static_cast<const bf16*>(a.v) + b * a.kv_bs + h * DH;
+  const int kv_tsb = 2 * (int)a.kv_ts;  // bytes per key row
+  const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc((void*)kp, (short)0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc((void*)vp, (short)0, 0x7fffffff, 0x00020000);
 
-  // ---- per-lane source offsets of the tile fetch (loop-invariant)
+  // ---- per-lane byte offsets of the tile fetch (loop-invariant)
   int koff[KCH], voff[KCH], krow[KCH];
 #pragma unroll
   for (int i = 0; i < KCH; ++i) {
     const int u = (w * KCH + i) * 64 + lane, row = u / CPR, pch = u % CPR;
     krow[i] = row;
-    koff[i] = row * (int)a.kv_ts + kswz<DH>(row, pch) * 8;
-    voff[i] = row * (int)a.kv_ts + vswz<DH>(row, pch) * 8;
+    koff[i] = row * kv_tsb + kswz<DH>(row, pch) * 16;
+    voff[i] = row * kv_tsb + vswz<DH>(row, pch) * 16;
   }
 
   // ---- per-lane LDS operand offsets (bytes, loop-invariant)
@@ -239,23 +268,21 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd(const AttnArgs a, int nqt) {
 
   const int ntiles = (kend_max + BN - 1) / BN;
   const int n_plain = kend_min / BN < ntiles ? kend_min / BN : ntiles;  // tiles no row masks
-  fetch_tile<DH>(smem, kp, vp, a.kv_ts, a.Lk, 0, w, koff, voff, krow);
+  fetch_tile<DH>(smem, kr, vr, kv_tsb, a.Lk, 0, w, koff, voff, krow);
   tile_sync();
+  // unmasked tiles in pairs (tile t in buffer 0, t+1 in buffer 1)
   int t = 0;
-  for (; t < n_plain; ++t) {
-    const int cur = t & 1, kb = t * BN;
-    if (t + 1 < ntiles) fetch_tile<DH>(smem + (cur ^ 1) * TILE, kp, vp, a.kv_ts, a.Lk, kb + BN, w, koff, voff, krow);
-    const char* Ks = reinterpret_cast<const char*>(smem + cur * TILE);
-    attn_tile<DH, false>(Ks, Ks + BN * DH * 2, qf, acc, m_ref, l_part, kofs, vofs, c, thr, kb, row_kend, hh);
-    tile_sync();
+  for (; t + 2 <= n_plain; t += 2) {
+    attn_step<DH, false>(smem, 0, kr, vr, kv_tsb, a.Lk, t, ntiles, w, koff, voff, krow, qf, acc, m_ref, l_part,
+                         kofs, vofs, c, thr, row_kend, hh);
+    attn_step<DH, false>(smem, 1, kr, vr, kv_tsb, a.Lk, t + 1, ntiles, w, koff, voff, krow, qf, acc, m_ref,
+                         l_part, kofs, vofs, c, thr, row_kend, hh);
   }
-  for (; t < ntiles; ++t) {
-    const int cur = t & 1, kb = t * BN;
-    if (t + 1 < ntiles) fetch_tile<DH>(smem + (cur ^ 1) * TILE, kp, vp, a.kv_ts, a.Lk, kb + BN, w, koff, voff, krow);
-    const char* Ks = reinterpret_cast<const char*>(smem + cur * TILE);
-    attn_tile<DH, true>(Ks, Ks + BN * DH * 2, qf, acc, m_ref, l_part, kofs, vofs, c, thr, kb, row_kend, hh);
-    tile_sync();
-  }
+  // the rest (at most one unmasked tile, then the tiles that straddle a prefix end),
+  // masked: the mask is a no-op on keys every row sees
+  for (; t < ntiles; ++t)
+    attn_step<DH, true>(smem, t & 1, kr, vr, kv_tsb, a.Lk, t, ntiles, w, koff, voff, krow, qf, acc, m_ref, l_part,
+                        kofs, vofs, c, thr, row_kend, hh);
 
   const float l = l_part + __shfl_xor(l_part, 32, 64);
   if (qrow < a.Lq) {

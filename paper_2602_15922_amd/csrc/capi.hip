@@ -118,6 +118,9 @@ wam_status attn_checked(const wam_attn_desc& d, const void* q, const void* k, co
                      d.o_batch_stride >= (int64_t)d.Lq * d.o_tok_stride &&
                      d.kv_batch_stride >= (int64_t)d.Lk * d.kv_tok_stride),
         WAM_EINVAL, "batch strides smaller than one sample");
+  CHECK((int64_t)d.Lk * d.kv_tok_stride * 2 <= INT32_MAX, WAM_EUNSUPPORTED,
+        "one sample's keys span %lld bytes (Lk * kv_tok_stride * 2 must stay below 2^31)",
+        (long long)d.Lk * d.kv_tok_stride * 2);
   a.q = q; a.k = k; a.v = v; a.o = o;
   a.q_ts = d.q_tok_stride; a.q_bs = d.q_batch_stride;
   a.kv_ts = d.kv_tok_stride; a.kv_bs = d.kv_batch_stride;
