@@ -310,7 +310,8 @@ wam_status wam_rope_qkv(int32_t B, int32_t L, int32_t H, int32_t Dh, const void*
  * out at out + (m / out_rows)*out_batch_stride + (m % out_rows)*ldo (a_rows or
  * out_rows = 0: plain, i.e. row m at m*lda / m*ldo).  K % 8 == 0; lda, ldw and
  * a_batch_stride multiples of 8; ldo, out_batch_stride and gate_stride multiples of 4;
- * bias and gate pointers 16-byte aligned. */
+ * bias and gate pointers 16-byte aligned.  The rows of A read and all of W must each
+ * span less than 2 GiB from their base pointer (else WAM_EUNSUPPORTED). */
 enum { WAM_EPI_BF16 = 0, WAM_EPI_GELU_BF16 = 1, WAM_EPI_RESID_F32 = 2, WAM_EPI_F32 = 3 };
 typedef struct {
   int32_t M, N, K, epilogue;

@@ -163,6 +163,15 @@ wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s) {
   TRY(opt_ptr(g.bias, "bias"));
   TRY(opt_ptr(g.gate_a, "gate_a"));
   TRY(opt_ptr(g.gate_v, "gate_v"));
+  {
+    // the kernels address A and W with 32-bit byte offsets from their base pointers
+    const int64_t ar = g.a_rows > 0 ? g.a_rows : g.M;
+    const int64_t a_end = (g.a_rows > 0 ? (int64_t)(g.M - 1) / ar * g.a_batch_stride : 0) +
+                          (std::min<int64_t>(ar, g.M) - 1) * g.lda + g.K;
+    const int64_t w_end = (int64_t)(g.N - 1) * g.ldw + g.K;
+    CHECK(2 * a_end <= INT32_MAX && 2 * w_end <= INT32_MAX, WAM_EUNSUPPORTED,
+          "A or W spans 2 GiB or more (A %lld bytes, W %lld bytes)", (long long)(2 * a_end), (long long)(2 * w_end));
+  }
   GemmArgs a{};
   a.M = g.M; a.N = g.N; a.K = g.K; a.epi = g.epilogue;
   a.A = g.A; a.lda = g.lda; a.a_bs = g.a_batch_stride; a.a_rows = g.a_rows;

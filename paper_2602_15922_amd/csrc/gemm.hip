@@ -5,10 +5,13 @@
 // transpose is ever needed.  A workgroup of WM x WN wavefronts computes a BM x BN
 // tile.  The large tiles use 8 wavefronts (two per SIMD), so one wavefront's barrier
 // and LDS waits overlap the other's MFMAs.  BK-wide slices of A and W are fetched
-// with direct global->LDS loads into a ring of STAGES LDS buffers: the loads of slice t+STAGES-1 are issued while slice t
-// is consumed, so each load has STAGES-1 slices of MFMA work to land (no staging
-// registers, one barrier per slice, waits on the vector-memory counter only for the
-// slice about to be used).  Within a slice the fragment reads of the next 16-wide
+// with buffer loads straight into LDS (a scalar resource, a loop-invariant 32-bit lane
+// offset and a scalar slice offset: no vector ALU work per load) into a ring of STAGES
+// LDS buffers; the steady-state loop handles STAGES slices per iteration so each
+// stage's LDS offsets are immediates.  The loads of slice t+STAGES-1 are issued while
+// slice t is consumed, so each load has STAGES-1 slices of MFMA work to land (no
+// staging registers, one barrier per slice, waits on the vector-memory counter only
+// for the slice about to be used).  Within a slice the fragment reads of the next 16-wide
 // k-step are issued before the current step's MFMAs.  LDS rows are BK bf16 with
 // 16-byte chunks XOR-swizzled by row so the fragment reads (32 consecutive rows, same
 // chunk) are bank-conflict free; since lane l of a direct load lands at LDS unit
@@ -102,32 +105,128 @@ WAM_DEV void epilogue4(const GemmArgs& g, const float inv_o, const float inv_g, 
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// One BK slice of NI*64*4 16-byte units into LDS with direct loads.  Wave w's
-// instruction c fills units [(w*NI + c)*64, +64); lane l's unit is read from
-// src[c] (its row, already offset to its logical chunk kl[c]) at column k0, or, when
-// that chunk lies past K, from the row's last chunk (such units are zeroed once they
-// have landed).
-template <int NI>
-WAM_DEV void fetch_slice(bf16* dst, const bf16* base, const int64_t* src, const int* kl, int k0, int K, int w) {
-#pragma unroll
-  for (int c = 0; c < NI; ++c) {
-    const int k = k0 + kl[c] < K ? k0 : K - 8 - kl[c];
-    __builtin_amdgcn_global_load_lds(base + src[c] + k, (lds_void*)(dst + (w * NI + c) * 512), 16, 0, 0);
-  }
-}
-
 // s_waitcnt on the vector-memory counter only (vmcnt <= n; LDS and export counters
 // left unconstrained), gfx9 encoding.
 #define WAM_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (((n) >> 4) << 14)) | (7 << 4) | (15 << 8))
 // s_waitcnt on the LDS/scalar counter only (lgkmcnt = 0)
 #define WAM_WAIT_LGKMCNT0() __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4))
 
+// 16 bytes per lane from a buffer straight into LDS (lane l lands at lds + 16*l).  A
+// plain function: the builtin's operands must not depend on a template parameter.
+WAM_DEV void load_lds16(__amdgpu_buffer_rsrc_t r, bf16* lds, int voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds, 16, voff, soff, 0, 0);
+}
+
+// Per-workgroup state of the main loop: the operand base pointers and the lanes'
+// loop-invariant byte offsets of their load units and LDS fragment reads.
+template <typename C>
+struct GemmLane {
+  const void *A, *W;
+  int a_off[C::NIA], b_off[C::NIB];  // byte offset of the lane's unit (row + logical chunk)
+  int kla[C::NIA], klb[C::NIB];      // logical column of the lane's unit inside a slice
+  int fa_off[C::BK / 16], fb_off[C::BK / 16];  // LDS byte offset of the lane's fragment per k-step
+  int w;
+};
+
+// One BK slice into ring stage `buf` with buffer loads straight into LDS: lane l of
+// wave w's instruction c fills unit (w*NI + c)*64 + l.  Full slices need no per-lane
+// work (scalar slice offset + loop-invariant lane offset); in a slice that runs past K
+// a unit whose chunk lies past K re-reads the row's last in-range chunk instead (it is
+// zeroed in LDS once landed).
+template <typename C>
+WAM_DEV void fetch_slice(bf16* smem, int buf, const GemmLane<C>& L, int kt, int K) {
+  // buffer resources over all of A and W (offsets < 2^31 bytes, checked by the host)
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(L.A), (short)0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(L.W), (short)0, 0x7fffffff, 0x00020000);
+  bf16* As = smem + buf * C::STAGE;
+  bf16* Bs = As + C::BM * C::BK;
+  const int k0 = kt * C::BK, soff = 2 * k0;
+  if (k0 + C::BK <= K) {
+#pragma unroll
+    for (int c = 0; c < C::NIA; ++c)
+      load_lds16(ra, As + (L.w * C::NIA + c) * 512, L.a_off[c], soff);
+#pragma unroll
+    for (int c = 0; c < C::NIB; ++c)
+      load_lds16(rb, Bs + (L.w * C::NIB + c) * 512, L.b_off[c], soff);
+  } else {
+#pragma unroll
+    for (int c = 0; c < C::NIA; ++c) {
+      const int sh = k0 + L.kla[c] < K ? 0 : 2 * (K - 8 - L.kla[c] - k0);
+      load_lds16(ra, As + (L.w * C::NIA + c) * 512, L.a_off[c] + sh, soff);
+    }
+#pragma unroll
+    for (int c = 0; c < C::NIB; ++c) {
+      const int sh = k0 + L.klb[c] < K ? 0 : 2 * (K - 8 - L.klb[c] - k0);
+      load_lds16(rb, Bs + (L.w * C::NIB + c) * 512, L.b_off[c] + sh, soff);
+    }
+  }
+}
+
+// Zero the units of a landed slice whose chunks lie past K (only in the last slice).
+template <typename C>
+WAM_DEV void zero_tail(bf16* smem, int buf, const GemmLane<C>& L, int kt, int K, int lane) {
+  bf16* As = smem + buf * C::STAGE;
+  bf16* Bs = As + C::BM * C::BK;
+#pragma unroll
+  for (int c = 0; c < C::NIA; ++c)
+    if (kt * C::BK + L.kla[c] >= K) *reinterpret_cast<bf16x8*>(As + ((L.w * C::NIA + c) * 64 + lane) * 8) = bf16x8{};
+#pragma unroll
+  for (int c = 0; c < C::NIB; ++c)
+    if (kt * C::BK + L.klb[c] >= K) *reinterpret_cast<bf16x8*>(Bs + ((L.w * C::NIB + c) * 64 + lane) * 8) = bf16x8{};
+}
+
+// The MFMAs of one landed slice in ring stage `cur`.  Fragments are double-buffered in
+// registers: the reads of k-step ks+1 are in flight while the MFMAs of k-step ks run.
+// With `cur` a compile-time constant every LDS read is a lane offset plus an immediate.
+template <typename C>
+WAM_DEV void mma_slice(const bf16* smem, int cur, const GemmLane<C>& L, f32x16 (*acc)[C::TN]) {
+  const char* As = reinterpret_cast<const char*>(smem + cur * C::STAGE);
+  const char* Bs = As + C::BM * C::BK * 2;
+  constexpr int RB = 32 * C::BK * 2;  // bytes of 32 LDS rows
+  bf16x8 fa[2][C::TM], fb[2][C::TN];
+  auto read_frags = [&](int ks, int slot) {
+#pragma unroll
+    for (int a = 0; a < C::TM; ++a) fa[slot][a] = *reinterpret_cast<const bf16x8*>(As + L.fa_off[ks] + a * RB);
+#pragma unroll
+    for (int b = 0; b < C::TN; ++b) fb[slot][b] = *reinterpret_cast<const bf16x8*>(Bs + L.fb_off[ks] + b * RB);
+  };
+  read_frags(0, 0);
+#pragma unroll
+  for (int ks = 0; ks < C::BK / 16; ++ks) {
+    if (ks + 1 < C::BK / 16) read_frags(ks + 1, (ks + 1) & 1);
+#pragma unroll
+    for (int a = 0; a < C::TM; ++a)
+#pragma unroll
+      for (int b = 0; b < C::TN; ++b) acc[a][b] = mfma32(fa[ks & 1][a], fb[ks & 1][b], acc[a][b]);
+    // fence the k-step: the next step's LDS reads stay in this step's region
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// One main-loop iteration in steady state (slice kt in stage CUR; one younger slice in
+// flight when S = 3, S-2 in general): wait for slice kt, barrier, prefetch slice
+// kt+S-1 into the stage freed by slice kt-1, then the slice's MFMAs.
+template <typename C, int CUR>
+WAM_DEV void steady_step(bf16* smem, const GemmLane<C>& L, int kt, int K, f32x16 (*acc)[C::TN]) {
+  constexpr int S = C::STAGES, NI = C::NIA + C::NIB;
+  WAM_WAIT_VMCNT((S - 2) * NI);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  fetch_slice<C>(smem, (CUR + S - 1) % S, L, kt + S - 1, K);
+  mma_slice<C>(smem, CUR, L, acc);
+}
+
+template <typename C, int CUR>
+WAM_DEV void steady_group(bf16* smem, const GemmLane<C>& L, int kt, int K, f32x16 (*acc)[C::TN]) {
+  steady_step<C, CUR>(smem, L, kt + CUR, K, acc);
+  if constexpr (CUR + 1 < C::STAGES) steady_group<C, CUR + 1>(smem, L, kt, K, acc);
+}
+
 template <typename C, int EPI>
 __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int tiles_m, int tiles_n) {
   constexpr int BM = C::BM, BN = C::BN, BK = C::BK, S = C::STAGES;
   __shared__ __attribute__((aligned(16))) bf16 smem[S * C::STAGE];
-  auto As = [&](int buf) { return smem + buf * C::STAGE; };
-  auto Bs = [&](int buf) { return smem + buf * C::STAGE + BM * BK; };
 
   // XCD-aware remap: the hardware deals workgroups round-robin over 8 XCDs; give each
   // XCD a contiguous range of tiles so tiles that share a W panel share an L2.
@@ -138,52 +237,43 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int t
   const int tm = lid % tiles_m, tn = lid / tiles_m;  // consecutive tiles share a W panel
   const int m0 = tm * BM, n0 = tn * BN;
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;  // w < C::NW
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, w < C::NW
   const int hh = lane >> 5, l32 = lane & 31;
   const int wm = w / C::WN, wn = w % C::WN;
 
-  const bf16* A = static_cast<const bf16*>(g.A);
-  const bf16* W = static_cast<const bf16*>(g.W);
-
-  // Direct-load sources (loop-invariant).  Unit u of a slice is row u/CPR, physical
-  // chunk u%CPR, which holds logical chunk pch(row, u%CPR) (the XOR is an involution).
+  GemmLane<C> L;
+  L.A = g.A;
+  L.W = g.W;
+  L.w = w;
+  // Load units: unit u of a slice is row u/CPR, physical chunk u%CPR, which holds
+  // logical chunk pch(row, u%CPR) (the XOR is an involution).
   constexpr int RPI = 64 / C::CPR;  // rows covered by one wave instruction
   const int lrow = lane / C::CPR;
-  int64_t a_src[C::NIA], b_src[C::NIB];
 #pragma unroll
   for (int c = 0; c < C::NIA; ++c) {
     const int row = (w * C::NIA + c) * RPI + lrow;
     int r = m0 + row;
     r = r < g.M ? r : g.M - 1;
-    a_src[c] = (int64_t)(r / g.a_rows) * g.a_bs + (int64_t)(r % g.a_rows) * g.lda + C::pch(row, lane % C::CPR) * 8;
+    L.kla[c] = C::pch(row, lane % C::CPR) * 8;
+    L.a_off[c] = (int)(2 * ((int64_t)(r / g.a_rows) * g.a_bs + (int64_t)(r % g.a_rows) * g.lda + L.kla[c]));
   }
 #pragma unroll
   for (int c = 0; c < C::NIB; ++c) {
     const int row = (w * C::NIB + c) * RPI + lrow;
     int r = n0 + row;
     r = r < g.N ? r : g.N - 1;
-    b_src[c] = (int64_t)r * g.ldw + C::pch(row, lane % C::CPR) * 8;
+    L.klb[c] = C::pch(row, lane % C::CPR) * 8;
+    L.b_off[c] = (int)(2 * ((int64_t)r * g.ldw + L.klb[c]));
   }
-  // logical column offset of each of the lane's units (for the K-tail test)
-  int kla[C::NIA], klb[C::NIB];
+  // Fragment reads: rows (wm*BM/WM + a*32 + l32) of A and (wn*BN/WN + b*32 + l32) of W
+  // at logical chunk 2*ks + hh; the XOR only depends on l32 (32-row steps keep it).
 #pragma unroll
-  for (int c = 0; c < C::NIA; ++c) kla[c] = C::pch((w * C::NIA + c) * RPI + lrow, lane % C::CPR) * 8;
-#pragma unroll
-  for (int c = 0; c < C::NIB; ++c) klb[c] = C::pch((w * C::NIB + c) * RPI + lrow, lane % C::CPR) * 8;
-  auto fetch = [&](int kt) {  // no device builtins in lambdas (they drop the host kernel stub)
-    const int buf = kt % S;
-    fetch_slice<C::NIA>(As(buf), A, a_src, kla, kt * BK, g.K, w);
-    fetch_slice<C::NIB>(Bs(buf), W, b_src, klb, kt * BK, g.K, w);
-  };
-  auto zero_tail = [&](int kt) {  // only for a slice that runs past K
-    const int buf = kt % S;
-#pragma unroll
-    for (int c = 0; c < C::NIA; ++c)
-      if (kt * BK + kla[c] >= g.K) *reinterpret_cast<bf16x8*>(As(buf) + ((w * C::NIA + c) * 64 + lane) * 8) = bf16x8{};
-#pragma unroll
-    for (int c = 0; c < C::NIB; ++c)
-      if (kt * BK + klb[c] >= g.K) *reinterpret_cast<bf16x8*>(Bs(buf) + ((w * C::NIB + c) * 64 + lane) * 8) = bf16x8{};
-  };
+  for (int ks = 0; ks < BK / 16; ++ks) {
+    const int ra = wm * (BM / C::WM) + l32, rb = wn * (BN / C::WN) + l32;
+    L.fa_off[ks] = 2 * C::swz(ra, 2 * ks + hh);
+    L.fb_off[ks] = 2 * C::swz(rb, 2 * ks + hh);
+  }
 
   f32x16 acc[C::TM][C::TN];
 #pragma unroll
@@ -192,52 +282,33 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int t
     for (int b = 0; b < C::TN; ++b) acc[a][b] = f32x16{};
 
   const int nk = (g.K + BK - 1) / BK;
-  constexpr int NI = C::NIA + C::NIB;  // direct-load instructions per slice per wave
+  constexpr int NI = C::NIA + C::NIB;  // loads per slice per wave
 #pragma unroll
   for (int p = 0; p < S - 1; ++p)
-    if (p < nk) fetch(p);
-  for (int kt = 0; kt < nk; ++kt) {
-    // slice kt has landed once at most the younger prefetched slices are in flight
+    if (p < nk) fetch_slice<C>(smem, p, L, p, g.K);
+  int kt = 0;
+  // steady state, S slices per iteration so each stage index is a constant; every
+  // slice here has S-2 younger slices in flight at its wait and prefetches a slice < nk
+  for (; kt + 2 * S - 2 < nk; kt += S) steady_group<C, 0>(smem, L, kt, g.K, acc);
+  // the remaining slices (fewer younger slices in flight; the last may run past K)
+  for (; kt < nk; ++kt) {
     const int younger = (nk - 1 - kt) < (S - 2) ? (nk - 1 - kt) : (S - 2);
     if (younger >= 2) WAM_WAIT_VMCNT(2 * NI);
     else if (younger == 1) WAM_WAIT_VMCNT(NI);
     else WAM_WAIT_VMCNT(0);
     if ((kt + 1) * BK > g.K) {
-      zero_tail(kt);
+      zero_tail<C>(smem, kt % S, L, kt, g.K, lane);
       WAM_WAIT_LGKMCNT0();
     }
-    // Slice kt is visible to all waves and slice kt-1's buffer is free once every wave
+    // Slice kt is visible to all waves and slice kt-1's stage is free once every wave
     // is here: each wave has waited for its own loads of slice kt above, and its reads
     // of slice kt-1 were consumed by its MFMAs.  A plain s_barrier (the __syncthreads
     // fence would also wait for the prefetched slices still in flight).
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    if (kt + S - 1 < nk) fetch(kt + S - 1);
-    const int cur = kt % S;
-
-    // fragments double-buffered in registers: the reads of k-step ks+1 are in flight
-    // while the MFMAs of k-step ks run
-    bf16x8 fa[2][C::TM], fb[2][C::TN];
-    auto read_frags = [&](int ks, int slot) {
-#pragma unroll
-      for (int a = 0; a < C::TM; ++a)
-        fa[slot][a] = *reinterpret_cast<const bf16x8*>(&As(cur)[C::swz(wm * (BM / C::WM) + a * 32 + l32, 2 * ks + hh)]);
-#pragma unroll
-      for (int b = 0; b < C::TN; ++b)
-        fb[slot][b] = *reinterpret_cast<const bf16x8*>(&Bs(cur)[C::swz(wn * (BN / C::WN) + b * 32 + l32, 2 * ks + hh)]);
-    };
-    read_frags(0, 0);
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      if (ks + 1 < BK / 16) read_frags(ks + 1, (ks + 1) & 1);
-#pragma unroll
-      for (int a = 0; a < C::TM; ++a)
-#pragma unroll
-        for (int b = 0; b < C::TN; ++b) acc[a][b] = mfma32(fa[ks & 1][a], fb[ks & 1][b], acc[a][b]);
-      // fence the k-step: the next step's LDS reads stay in this step's region
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    if (kt + S - 1 < nk) fetch_slice<C>(smem, (kt + S - 1) % S, L, kt + S - 1, g.K);
+    mma_slice<C>(smem, kt % S, L, acc);
   }
   __syncthreads();  // all waves done with the operand ring before it is reused
 
@@ -289,20 +360,11 @@ hipError_t launch_gemm(const GemmArgs& gin, hipStream_t s) {
   if (g.a_rows <= 0) { g.a_rows = g.M; g.a_bs = 0; }
   if (g.o_rows <= 0) { g.o_rows = g.M; g.o_bs = 0; }
   if (g.gate_rows <= 0) { g.gate_rows = g.M; g.gate_stride = 0; }
-  // Pick the tile whose rounds of concurrent workgroups cost least (per_cu workgroups
-  // of a tile fit one CU), weighting tiles by their measured MFMA efficiency.
-  struct Opt { int bm, bn, per_cu; float eff; };
-  const Opt opts[3] = {{256, 256, 1, 1.0f}, {128, 256, 1, 0.85f}, {128, 128, 2, 0.6f}};
-  int best = 0;
-  float best_cost = 0.f;
-  for (int i = 0; i < 3; ++i) {
-    const long tiles = (long)((g.M + opts[i].bm - 1) / opts[i].bm) * ((g.N + opts[i].bn - 1) / opts[i].bn);
-    const long slots = 256L * opts[i].per_cu;
-    const float cost = (float)((tiles + slots - 1) / slots) * opts[i].bm * opts[i].bn * opts[i].per_cu / opts[i].eff;
-    if (i == 0 || cost < best_cost) { best = i; best_cost = cost; }
-  }
-  if (best == 0) return launch_cfg<Cfg<256, 256, 32, 4, 2, 4, 2>>(g, s);
-  if (best == 1) return launch_cfg<Cfg<128, 256, 64, 3, 2, 4, 2>>(g, s);
+  // 128x256 tiles (8 wavefronts, 3-stage ring, one workgroup per CU) measure best on
+  // every shape that fills the chip; below one round of them (e.g. the 512-row text
+  // projections) 128x128 tiles, two workgroups per CU, spread the work wider.
+  const long tiles = (long)((g.M + 127) / 128) * ((g.N + 255) / 256);
+  if (tiles >= 256) return launch_cfg<Cfg<128, 256, 64, 3, 2, 4, 2>>(g, s);
   return launch_cfg<Cfg<128, 128, 64, 2, 2, 2, 2>>(g, s);
 }
 
