@@ -12,7 +12,9 @@ intermediate rounding, written for a reader to check by eye against the paper:
   attention rule "the current chunk sees every earlier chunk and itself"
   (section 3.1, Model Inference; Appendix C, Figure 10);
 * the velocity call u_theta(x_t; KV, c, t) of the closed-loop inference algorithm
-  (Appendix C, Algorithm 2, the denoising-loop forward with update=False);
+  (Appendix C, Algorithm 2, the denoising-loop forward with update=False), its cache
+  update pass (update=True) and the denoising loop around it (solver step, guidance,
+  DiT caching);
 * the block internals the paper leaves unstated (AdaLN-modulated LayerNorm, 3D RoPE,
   cross-attention to text, tanh-GELU FFN) follow the readings listed in the design doc.
 
@@ -24,3 +26,4 @@ from .rope import rope_split, rope_angles, apply_rope, chunk_positions  # noqa: 
 from .attention import attention  # noqa: F401
 from .model import (time_embedding, text_projection, patchify, unpatchify,  # noqa: F401
                     embed, dit_block, head, dit_step, dit_update)
+from .denoise import euler_step, cfg_combine, cosine_similarity, denoise  # noqa: F401

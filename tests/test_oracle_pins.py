@@ -582,6 +582,77 @@ def test_update_identity_blocks_closed_form():
             assert np.allclose(kv[l][1][0, tok].reshape(d), vraw, atol=1e-10)
 
 
+# ----------------------------------------------------------------------------- denoising loop
+def test_euler_follows_the_straight_path_of_eq2():
+    """With the path's own velocity z1 - z0 (constant along Eq. 2's interpolation), every
+    Euler step lands on the path: after step i the state is t_{i+1} z1 + (1 - t_{i+1}) z0,
+    and the last step reaches the clean sample z1, for any schedule."""
+    g = np.random.default_rng(130)
+    z0, z1 = g.standard_normal((3, 5)), g.standard_normal((3, 5))
+    ts = np.array([0.0, 0.03, 0.2, 0.21, 0.6, 0.95, 1.0])
+    x = z0.copy()
+    for i in range(len(ts) - 1):
+        x = oracle.euler_step(x, z1 - z0, ts[i], ts[i + 1])
+        assert np.allclose(x, ts[i + 1] * z1 + (1 - ts[i + 1]) * z0, atol=1e-14)
+    xN, computed = oracle.denoise(z0, lambda xin, t: z1 - z0, ts)
+    assert np.allclose(xN, z1, atol=1e-14) and all(computed)
+
+
+def test_euler_closed_form_on_a_linear_ode():
+    """dx/dt = -x with N uniform Euler steps from 0 to 1 gives x0 (1 - 1/N)^N exactly
+    (and tends to x0/e)."""
+    x0 = np.array([1.5, -2.0, 0.25])
+    for N in (1, 4, 16):
+        ts = np.linspace(0.0, 1.0, N + 1)
+        xN, _ = oracle.denoise(x0, lambda xin, t: -xin, ts)
+        assert np.allclose(xN, x0 * (1 - 1 / N) ** N, rtol=1e-13)
+
+
+def test_cfg_combine_and_cosine_similarity():
+    g = np.random.default_rng(131)
+    vc, vu = g.standard_normal(7), g.standard_normal(7)
+    assert np.allclose(oracle.cfg_combine(vc, vu, 1.0), vc, atol=1e-15)
+    assert np.array_equal(oracle.cfg_combine(vc, vu, 0.0), vu)
+    s = 4.5
+    assert np.allclose(oracle.cfg_combine(vc, vu, s), [vu[i] + s * (vc[i] - vu[i]) for i in range(7)], atol=1e-15)
+    a, b = g.standard_normal(9), g.standard_normal(9)
+    dot = sum(a[i] * b[i] for i in range(9))
+    na = math.sqrt(sum(x * x for x in a))
+    nb = math.sqrt(sum(x * x for x in b))
+    assert abs(oracle.cosine_similarity(a, b) - dot / (na * nb)) < 1e-14
+    assert abs(oracle.cosine_similarity(a, 3 * a) - 1) < 1e-15
+    assert abs(oracle.cosine_similarity(a, -a) + 1) < 1e-15
+    assert oracle.cosine_similarity(np.array([1.0, 0.0]), np.array([0.0, 2.0])) == 0.0
+
+
+def test_dit_caching_skips_a_window_after_similar_velocities():
+    """Algorithm 2 with DiT caching: once two successive computed velocities are more
+    similar than tau, the next `window` steps reuse the latest one."""
+    calls = []
+
+    def const_v(xin, t):
+        calls.append(t)
+        return np.ones(4)
+
+    ts = np.linspace(0, 1, 9)
+    x, computed = oracle.denoise(np.zeros(4), const_v, ts, tau=0.9, window=2)
+    assert computed == [True, True, False, False, True, False, False, True]
+    assert len(calls) == 4 and np.allclose(x, 1.0)
+    # tau above 1 never skips; tau <= 0 disables caching
+    for tau in (1.5, 0.0):
+        _, computed = oracle.denoise(np.zeros(4), const_v, ts, tau=tau, window=2)
+        assert all(computed)
+    # dissimilar successive velocities never trigger a skip
+    flip = {"s": 1.0}
+
+    def alt_v(xin, t):
+        flip["s"] = -flip["s"]
+        return flip["s"] * np.ones(4)
+
+    _, computed = oracle.denoise(np.zeros(4), alt_v, ts, tau=0.5, window=3)
+    assert all(computed)
+
+
 # ----------------------------------------------------------------------------- shared input generator
 def test_bf16_rounding_matches_torch():
     torch = pytest.importorskip("torch")
