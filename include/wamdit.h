@@ -265,6 +265,67 @@ wam_status wam_dit_update_fwd(const wam_model* m, const wam_step_io* io, void* w
                               size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------------
+ * The denoising loop around the step (Algorithm 2): the noisy chunk moves along the
+ * straight path of Eq. 2 from t = 0 (noise) to t = 1 (clean) by explicit Euler steps
+ * x <- x + (t_next - t) v, optionally with classifier-free guidance
+ * v = v_u + s (v_c - v_u) and DiT caching (Appendix D.1).
+ *
+ * The state x is fp32 [nx][n_video + n_action] per chunk: the latent elements
+ * (latent_ch*F*Hl*Wl, in z_t's order) followed by the action elements (A*act_dim);
+ * nx = 1 with guidance (the pair shares one state), else B.
+ * ------------------------------------------------------------------------------ */
+typedef struct {
+  int32_t B;          /* samples per network call (the step's batch) */
+  int32_t cfg;        /* 1: guidance pair, B == 2, sample 0 conditional, sample 1 unconditional */
+  float cfg_scale;    /* s */
+  int64_t n_video;    /* latent elements per sample */
+  int64_t n_action;   /* action elements per sample */
+} wam_flow_dims;
+
+/* One solver step: v_eff from the step outputs v_video [B][n_video] / v_action
+ * [B][n_action] (fp32, device), combined by guidance when cfg, or taken directly from
+ * v_in [nx][n] (a cached velocity; then v_video / v_action are ignored); all three NULL
+ * leaves x unchanged.  x += (t_next - t) v_eff in place; v_out (optional, [nx][n])
+ * receives v_eff; z_next [B][n_video] and a_next [B][n_action] (bf16, the next step's
+ * z_t / a_t) receive round-to-nearest-even(x) for every sample (both halves of a
+ * guidance pair).  Asynchronous; no workspace. */
+wam_status wam_flow_step(const wam_flow_dims* d, const float* v_video, const float* v_action,
+                         const float* v_in, float* x, float* v_out, float t, float t_next,
+                         void* z_next, void* a_next, hipStream_t stream);
+
+/* Cosine similarity <a, b> / (|a| |b|) of n fp32 values into out[0] (device; 0 when a
+ * norm is 0), accumulated in fp64 in a fixed order (deterministic).  ws of
+ * wam_cosine_workspace_bytes() device bytes. */
+size_t wam_cosine_workspace_bytes(void);
+wam_status wam_cosine_similarity(const float* a, const float* b, int64_t n, void* ws,
+                                 size_t ws_bytes, float* out, hipStream_t stream);
+
+typedef struct {
+  int32_t n_steps;        /* N >= 1 solver steps */
+  const float* t_sched;   /* HOST [N + 1] scheduler times t_0 .. t_N */
+  int32_t cfg;            /* guidance pair (io->B == 2) */
+  float cfg_scale;
+  float cache_tau;        /* DiT caching: after a computed step whose velocity has cosine  */
+  int32_t cache_window;   /* similarity > cache_tau with the previous computed one, the next */
+                          /* cache_window steps reuse it; cache_window = 0: caching off     */
+  float* x;               /* device fp32 state [nx][n_video + n_action]: noise in, x_N out */
+  int32_t* computed;      /* optional HOST [N]: 1 where step i called the network           */
+} wam_denoise_params;
+
+/* wam_denoise_chunk — the N-step denoising loop of one chunk: per step, the network
+ * call wam_dit_step_fwd(io) at t_i (io->t [B] is written by the loop; io->z_t and
+ * io->a_t are rewritten from x before every call; io->v_video / v_action receive the
+ * step's raw velocities), then wam_flow_step.  The cache rows [cache_len, cache_len+L)
+ * are rewritten by every computed step, as by a single step.  With caching off the loop
+ * never synchronizes (it can be captured in a graph); with caching on it synchronizes
+ * the stream once per computed step after the first to read the similarity.  Same
+ * validation and errors as wam_dit_step_fwd, plus the loop's own parameters. */
+size_t wam_denoise_workspace_bytes(const wam_model* m, const wam_step_io* io,
+                                   const wam_denoise_params* p);
+wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wam_denoise_params* p,
+                             void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------
  * Pieces of the step, exported for testing each kernel on its own.
  * ------------------------------------------------------------------------------ */
 

@@ -36,13 +36,13 @@ def cosine_similarity(a, b):
     return float(a @ b / den) if den > 0 else 0.0
 
 
-def denoise(x0, velocity, t_sched, tau=0.0, window=1, to_model_input=None):
+def denoise(x0, velocity, t_sched, tau=None, window=1, to_model_input=None):
     """Algorithm 2's denoising loop for one chunk.
 
     x0: initial noise (any array); velocity(x_in, t) -> v, the network's (already
     guidance-combined) velocity at model input x_in and time t; t_sched: the N+1
-    scheduler times t_0 .. t_N; tau <= 0 turns DiT caching off.  Returns (x_N, computed)
-    with computed[i] True where step i called the network."""
+    scheduler times t_0 .. t_N; tau None (or window 0) turns DiT caching off.  Returns
+    (x_N, computed) with computed[i] True where step i called the network."""
     x = np.array(x0, dtype=np.float64)
     v_last = None     # most recent computed velocity
     v_before = None   # the computed velocity before it
@@ -59,7 +59,8 @@ def denoise(x0, velocity, t_sched, tau=0.0, window=1, to_model_input=None):
             v = np.asarray(velocity(x_in, t), dtype=np.float64)
             v_before, v_last = v_last, v
             computed.append(True)
-            if tau > 0 and v_before is not None and cosine_similarity(v_last, v_before) > tau:
+            if tau is not None and window > 0 and v_before is not None and \
+                    cosine_similarity(v_last, v_before) > tau:
                 skip = window
         x = euler_step(x, v, t, t_next)
     return x, computed

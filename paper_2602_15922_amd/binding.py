@@ -21,7 +21,8 @@ WAM_EPI_BF16, WAM_EPI_GELU_BF16, WAM_EPI_RESID_F32, WAM_EPI_F32 = range(4)
 EXPORTED = (
     "wam_last_error", "wam_abi_version", "wam_attn_blockcausal", "wam_block_workspace_bytes",
     "wam_dit_block_fwd", "wam_step_workspace_bytes", "wam_dit_step_fwd",
-    "wam_update_workspace_bytes", "wam_dit_update_fwd",
+    "wam_update_workspace_bytes", "wam_dit_update_fwd", "wam_flow_step", "wam_cosine_workspace_bytes",
+    "wam_cosine_similarity", "wam_denoise_workspace_bytes", "wam_denoise_chunk",
     "wam_time_embed_workspace_bytes", "wam_time_embed_fwd", "wam_text_proj_workspace_bytes",
     "wam_text_proj_fwd", "wam_adaln_ln_mod", "wam_rope_qkv", "wam_gemm_bf16",
     "wam_embed_workspace_bytes", "wam_embed_fwd", "wam_head_workspace_bytes", "wam_head_fwd",
@@ -90,6 +91,15 @@ class wam_step_io(C.Structure):
                 ("v_video", _vp), ("v_action", _vp), ("attn_events", C.POINTER(_vp))]
 
 
+class wam_flow_dims(C.Structure):
+    _fields_ = [("B", _i32), ("cfg", _i32), ("cfg_scale", C.c_float), ("n_video", _i64), ("n_action", _i64)]
+
+
+class wam_denoise_params(C.Structure):
+    _fields_ = [("n_steps", _i32), ("t_sched", _fp), ("cfg", _i32), ("cfg_scale", C.c_float),
+                ("cache_tau", C.c_float), ("cache_window", _i32), ("x", _vp), ("computed", C.POINTER(_i32))]
+
+
 class wam_gemm_desc(C.Structure):
     _fields_ = [("M", _i32), ("N", _i32), ("K", _i32), ("epilogue", _i32),
                 ("A", _vp), ("lda", _i64), ("a_batch_stride", _i64), ("a_rows", _i32),
@@ -111,6 +121,7 @@ def lib():
         L.wam_last_error.restype = C.c_char_p
         L.wam_abi_version.restype = _i32
         for name in ("wam_block_workspace_bytes", "wam_step_workspace_bytes", "wam_update_workspace_bytes",
+                     "wam_cosine_workspace_bytes", "wam_denoise_workspace_bytes",
                      "wam_time_embed_workspace_bytes", "wam_text_proj_workspace_bytes",
                      "wam_embed_workspace_bytes", "wam_head_workspace_bytes"):
             getattr(L, name).restype = _sz
@@ -126,6 +137,14 @@ def lib():
                                         C.POINTER(wam_block_io), _vp, _sz, _vp]
         L.wam_dit_step_fwd.argtypes = [C.POINTER(wam_model), C.POINTER(wam_step_io), _vp, _sz, _vp]
         L.wam_dit_update_fwd.argtypes = [C.POINTER(wam_model), C.POINTER(wam_step_io), _vp, _sz, _vp]
+        L.wam_flow_step.argtypes = [C.POINTER(wam_flow_dims), _vp, _vp, _vp, _vp, _vp, C.c_float, C.c_float, _vp,
+                                    _vp, _vp]
+        L.wam_cosine_workspace_bytes.argtypes = []
+        L.wam_cosine_similarity.argtypes = [_vp, _vp, _i64, _vp, _sz, _vp, _vp]
+        L.wam_denoise_workspace_bytes.argtypes = [C.POINTER(wam_model), C.POINTER(wam_step_io),
+                                                  C.POINTER(wam_denoise_params)]
+        L.wam_denoise_chunk.argtypes = [C.POINTER(wam_model), C.POINTER(wam_step_io), C.POINTER(wam_denoise_params),
+                                        _vp, _sz, _vp]
         L.wam_time_embed_fwd.argtypes = [C.POINTER(wam_model), _i32, _vp, _vp, _vp, _vp, _sz, _vp]
         L.wam_text_proj_fwd.argtypes = [C.POINTER(wam_model), _i32, _i32, _vp, _vp, _vp, _sz, _vp]
         L.wam_adaln_ln_mod.argtypes = [_i32, _i32, _i32, C.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
@@ -379,6 +398,44 @@ def wam_dit_update_fwd(model: wam_model, io: wam_step_io, ws, stream=None):
     """Cache-update pass: appends every layer's K/V of the io's clean rows at
     [cache_len, cache_len + L); v_video / v_action of io are not written."""
     _check(lib().wam_dit_update_fwd(C.byref(model), C.byref(io), _p(ws), ws.numel(), _stream(stream)))
+
+
+def wam_flow_step(dims: wam_flow_dims, x, z_next, a_next, t, t_next, v_video=None, v_action=None, v_in=None,
+                  v_out=None, stream=None):
+    _check(lib().wam_flow_step(C.byref(dims), _p(v_video), _p(v_action), _p(v_in), _p(x), _p(v_out), t, t_next,
+                               _p(z_next), _p(a_next), _stream(stream)))
+
+
+def wam_cosine_workspace_bytes() -> int:
+    return lib().wam_cosine_workspace_bytes()
+
+
+def wam_cosine_similarity(a, b, out, ws, stream=None):
+    """out[0] = cos(a, b) over all elements (device fp32 tensors)."""
+    _check(lib().wam_cosine_similarity(_p(a), _p(b), a.numel(), _p(ws), ws.numel(), _p(out), _stream(stream)))
+
+
+def make_denoise_params(t_sched, x, cfg=False, cfg_scale=1.0, cache_tau=0.0, cache_window=0):
+    """Host-side loop parameters; t_sched a float sequence of N+1 times, x the device state."""
+    import numpy as np
+    t = np.ascontiguousarray(np.asarray(t_sched, dtype=np.float32))
+    n = len(t) - 1
+    computed = np.zeros(n, np.int32)
+    p = wam_denoise_params(n_steps=n, t_sched=t.ctypes.data_as(_fp), cfg=int(cfg), cfg_scale=cfg_scale,
+                           cache_tau=cache_tau, cache_window=cache_window, x=_p(x),
+                           computed=computed.ctypes.data_as(C.POINTER(_i32)))
+    p._keep = (t, computed)
+    p.computed_steps = computed
+    return p
+
+
+def wam_denoise_workspace_bytes(model: wam_model, io: wam_step_io, params: wam_denoise_params) -> int:
+    return lib().wam_denoise_workspace_bytes(C.byref(model), C.byref(io), C.byref(params))
+
+
+def wam_denoise_chunk(model: wam_model, io: wam_step_io, params: wam_denoise_params, ws, stream=None):
+    _check(lib().wam_denoise_chunk(C.byref(model), C.byref(io), C.byref(params), _p(ws), ws.numel(),
+                                   _stream(stream)))
 
 
 def wam_chunk_positions(c, F, Hg, Wg, A):

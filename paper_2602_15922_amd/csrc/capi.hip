@@ -502,6 +502,68 @@ wam_status check_step(const wam_model& m, const wam_step_io& io, bool head) {
   return WAM_OK;
 }
 
+// The launch sequence of one step; arguments already validated.
+wam_status step_run(const wam_model& m, const wam_step_io& io, char* w, hipStream_t stream) {
+  const StepWs lay = step_ws(m, io);
+  const wam_dims& D = m.dims;
+  float* x = reinterpret_cast<float*>(w + lay.x);
+  float* e = reinterpret_cast<float*>(w + lay.e);
+  float* e0 = reinterpret_cast<float*>(w + lay.e0);
+  void* ctx = w + lay.ctx;
+  char* piece = w + lay.piece;
+  const int32_t Lv = io.F * (io.Hl / 2) * (io.Wl / 2), L = Lv + io.A;
+
+  TRY(time_run(m, io.B, io.t, e, e0, piece, stream));
+  if (!io.ctx_kv) TRY(text_run(m, io.B, io.Lc, io.text, ctx, piece, stream));
+  TRY(embed_run(m, io.B, io.F, io.Hl, io.Wl, io.A, io.z_t, io.a_t, x, piece, stream));
+  for (int l = 0; l < D.n_layers; ++l) {
+    wam_block_io b{};
+    b.x = x; b.e0 = e0; b.rope_cos = io.rope_cos; b.rope_sin = io.rope_sin;
+    b.k_cache = io.k_cache[l]; b.v_cache = io.v_cache[l]; b.Lcap = io.Lcap; b.cache_len = io.cache_len;
+    b.ch = io.ch; b.ctx = ctx; b.ctx_kv = io.ctx_kv ? io.ctx_kv[l] : nullptr;
+    b.B = io.B; b.L = L; b.Lc = io.Lc;
+    hipEvent_t ev0 = io.attn_events ? io.attn_events[2 * l] : nullptr;
+    hipEvent_t ev1 = io.attn_events ? io.attn_events[2 * l + 1] : nullptr;
+    TRY(block_run(D, m.blocks[l], b, w + lay.block, stream, ev0, ev1));
+  }
+  TRY(head_run(m, io.B, io.F, io.Hl, io.Wl, io.A, x, e, io.v_video, io.v_action, piece, stream));
+  return WAM_OK;
+}
+
+// ---------------------------------------------------------------------------------
+// denoising loop
+// ---------------------------------------------------------------------------------
+wam_status check_flow_dims(const wam_flow_dims& d) {
+  CHECK(d.B >= 1 && d.n_video >= 0 && d.n_action >= 0, WAM_EINVAL, "flow dims B=%d n_video=%lld n_action=%lld",
+        d.B, (long long)d.n_video, (long long)d.n_action);
+  CHECK(!d.cfg || d.B == 2, WAM_EINVAL, "guidance needs a pair (B == 2), got B=%d", d.B);
+  return WAM_OK;
+}
+
+FlowArgs flow_args(const wam_flow_dims& d) {
+  FlowArgs f{};
+  f.B = d.B; f.cfg = d.cfg ? 1 : 0; f.cfg_scale = d.cfg_scale;
+  f.n_video = d.n_video; f.n_action = d.n_action;
+  return f;
+}
+
+struct DenoiseWs {
+  size_t step, va, vb, cos, cos_out, total;
+};
+DenoiseWs denoise_ws(const wam_model& m, const wam_step_io& io, const wam_denoise_params& p) {
+  const int64_t nx = p.cfg ? 1 : io.B;
+  const int64_t n = (int64_t)m.dims.latent_ch * io.F * io.Hl * io.Wl + (int64_t)io.A * m.dims.act_dim;
+  DenoiseWs w{};
+  size_t off = 0;
+  w.step = off; off += step_ws(m, io).total;
+  w.va = off; off += align256((size_t)nx * n * 4);
+  w.vb = off; off += align256((size_t)nx * n * 4);
+  w.cos = off; off += align256(cosine_workspace_bytes());
+  w.cos_out = off; off += 256;
+  w.total = off;
+  return w;
+}
+
 }  // namespace
 
 // =================================================================================
@@ -650,32 +712,8 @@ wam_status wam_dit_step_fwd(const wam_model* m, const wam_step_io* io, void* ws,
                             hipStream_t stream) {
   CHECK(m && io, WAM_EINVAL, "NULL model/io");
   TRY(check_step(*m, *io, true));
-  const StepWs lay = step_ws(*m, *io);
-  TRY(check_ws(ws, ws_bytes, lay.total));
-  const wam_dims& D = m->dims;
-  char* w = static_cast<char*>(ws);
-  float* x = reinterpret_cast<float*>(w + lay.x);
-  float* e = reinterpret_cast<float*>(w + lay.e);
-  float* e0 = reinterpret_cast<float*>(w + lay.e0);
-  void* ctx = w + lay.ctx;
-  char* piece = w + lay.piece;
-  const int32_t Lv = io->F * (io->Hl / 2) * (io->Wl / 2), L = Lv + io->A;
-
-  TRY(time_run(*m, io->B, io->t, e, e0, piece, stream));
-  if (!io->ctx_kv) TRY(text_run(*m, io->B, io->Lc, io->text, ctx, piece, stream));
-  TRY(embed_run(*m, io->B, io->F, io->Hl, io->Wl, io->A, io->z_t, io->a_t, x, piece, stream));
-  for (int l = 0; l < D.n_layers; ++l) {
-    wam_block_io b{};
-    b.x = x; b.e0 = e0; b.rope_cos = io->rope_cos; b.rope_sin = io->rope_sin;
-    b.k_cache = io->k_cache[l]; b.v_cache = io->v_cache[l]; b.Lcap = io->Lcap; b.cache_len = io->cache_len;
-    b.ch = io->ch; b.ctx = ctx; b.ctx_kv = io->ctx_kv ? io->ctx_kv[l] : nullptr;
-    b.B = io->B; b.L = L; b.Lc = io->Lc;
-    hipEvent_t ev0 = io->attn_events ? io->attn_events[2 * l] : nullptr;
-    hipEvent_t ev1 = io->attn_events ? io->attn_events[2 * l + 1] : nullptr;
-    TRY(block_run(D, m->blocks[l], b, w + lay.block, stream, ev0, ev1));
-  }
-  TRY(head_run(*m, io->B, io->F, io->Hl, io->Wl, io->A, x, e, io->v_video, io->v_action, piece, stream));
-  return WAM_OK;
+  TRY(check_ws(ws, ws_bytes, step_ws(*m, *io).total));
+  return step_run(*m, *io, static_cast<char*>(ws), stream);
 }
 
 size_t wam_update_workspace_bytes(const wam_model* m, const wam_step_io* io) {
@@ -712,6 +750,104 @@ wam_status wam_dit_update_fwd(const wam_model* m, const wam_step_io* io, void* w
       hipEvent_t ev0 = io->attn_events ? io->attn_events[2 * l] : nullptr;
       hipEvent_t ev1 = io->attn_events ? io->attn_events[2 * l + 1] : nullptr;
       TRY(block_run(D, m->blocks[l], b, w + lay.block, stream, ev0, ev1));
+    }
+  }
+  return WAM_OK;
+}
+
+wam_status wam_flow_step(const wam_flow_dims* d, const float* v_video, const float* v_action, const float* v_in,
+                         float* x, float* v_out, float t, float t_next, void* z_next, void* a_next,
+                         hipStream_t stream) {
+  CHECK(d != nullptr, WAM_EINVAL, "NULL dims");
+  TRY(check_flow_dims(*d));
+  TRY(need_ptr(x, "x"));
+  if (d->n_video > 0) TRY(need_ptr(z_next, "z_next"));
+  if (d->n_action > 0) TRY(need_ptr(a_next, "a_next"));
+  if (!v_in && (v_video || v_action)) {
+    if (d->n_video > 0) TRY(need_ptr(v_video, "v_video"));
+    if (d->n_action > 0) TRY(need_ptr(v_action, "v_action"));
+  }
+  FlowArgs f = flow_args(*d);
+  f.dt = t_next - t;
+  f.v_in = v_in;
+  if (!v_in) { f.v_video = v_video; f.v_action = v_action; }
+  f.x = x; f.v_out = v_out; f.z_next = z_next; f.a_next = a_next;
+  HIPCHECK(launch_flow_step(f, stream));
+  return WAM_OK;
+}
+
+size_t wam_cosine_workspace_bytes(void) { return cosine_workspace_bytes(); }
+
+wam_status wam_cosine_similarity(const float* a, const float* b, int64_t n, void* ws, size_t ws_bytes, float* out,
+                                 hipStream_t stream) {
+  CHECK(n >= 0, WAM_EINVAL, "n < 0");
+  TRY(need_ptr(out, "out"));
+  if (n > 0) { TRY(need_ptr(a, "a")); TRY(need_ptr(b, "b")); }
+  CHECK(ws != nullptr && ws_bytes >= cosine_workspace_bytes(), WAM_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
+        cosine_workspace_bytes());
+  HIPCHECK(launch_cosine(a, b, n, ws, out, stream));
+  return WAM_OK;
+}
+
+size_t wam_denoise_workspace_bytes(const wam_model* m, const wam_step_io* io, const wam_denoise_params* p) {
+  if (!m || !io || !p || io->B < 0 || io->F < 0 || io->Hl < 0 || io->Wl < 0 || io->A < 0 || io->Lc < 0) return 0;
+  return denoise_ws(*m, *io, *p).total;
+}
+
+wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wam_denoise_params* p, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
+  CHECK(m && io && p, WAM_EINVAL, "NULL model/io/params");
+  TRY(check_step(*m, *io, true));
+  CHECK(p->n_steps >= 1, WAM_EINVAL, "n_steps=%d must be >= 1", p->n_steps);
+  CHECK(p->t_sched != nullptr, WAM_EINVAL, "t_sched is NULL");
+  CHECK(p->cache_window >= 0, WAM_EINVAL, "cache_window < 0");
+  TRY(need_ptr(p->x, "x"));
+  wam_flow_dims fd{};
+  fd.B = io->B; fd.cfg = p->cfg; fd.cfg_scale = p->cfg_scale;
+  fd.n_video = (int64_t)m->dims.latent_ch * io->F * io->Hl * io->Wl;
+  fd.n_action = (int64_t)io->A * m->dims.act_dim;
+  TRY(check_flow_dims(fd));
+  const DenoiseWs lay = denoise_ws(*m, *io, *p);
+  TRY(check_ws(ws, ws_bytes, lay.total));
+  char* w = static_cast<char*>(ws);
+  float* vbuf[2] = {reinterpret_cast<float*>(w + lay.va), reinterpret_cast<float*>(w + lay.vb)};
+  float* cs_dev = reinterpret_cast<float*>(w + lay.cos_out);
+  void* z = const_cast<void*>(io->z_t);
+  void* a = const_cast<void*>(io->a_t);
+  float* t_dev = const_cast<float*>(io->t);
+  const int64_t n = (int64_t)(p->cfg ? 1 : io->B) * (fd.n_video + fd.n_action);
+  const bool caching = p->cache_window > 0;
+
+  // the model inputs of the first call from the initial state
+  FlowArgs q = flow_args(fd);
+  q.x = p->x; q.z_next = z; q.a_next = a;
+  HIPCHECK(launch_flow_step(q, stream));
+  int last = -1, before = -1;  // slots of the latest and the previous computed velocity
+  int skip = 0;
+  for (int i = 0; i < p->n_steps; ++i) {
+    FlowArgs f = flow_args(fd);
+    f.dt = p->t_sched[i + 1] - p->t_sched[i];
+    f.x = p->x; f.z_next = z; f.a_next = a;
+    if (skip > 0) {
+      f.v_in = vbuf[last];
+      HIPCHECK(launch_flow_step(f, stream));
+      --skip;
+      if (p->computed) p->computed[i] = 0;
+      continue;
+    }
+    HIPCHECK(launch_fill(t_dev, io->B, p->t_sched[i], stream));
+    TRY(step_run(*m, *io, w + lay.step, stream));
+    before = last;
+    last = before == 0 ? 1 : 0;
+    f.v_video = io->v_video; f.v_action = io->v_action; f.v_out = vbuf[last];
+    HIPCHECK(launch_flow_step(f, stream));
+    if (p->computed) p->computed[i] = 1;
+    if (caching && before >= 0) {
+      HIPCHECK(launch_cosine(vbuf[last], vbuf[before], n, w + lay.cos, cs_dev, stream));
+      float cs = 0.f;
+      HIPCHECK(hipMemcpyAsync(&cs, cs_dev, sizeof(float), hipMemcpyDeviceToHost, stream));
+      HIPCHECK(hipStreamSynchronize(stream));
+      if (cs > p->cache_tau) skip = p->cache_window;
     }
   }
   return WAM_OK;

@@ -1,0 +1,123 @@
+// The denoising loop's own kernels for gfx950: the flow-matching solver step with
+// classifier-free guidance, the cosine similarity behind DiT caching, and the
+// timestep fill.  All HBM-bound elementwise work over one chunk's latents and actions.
+#include "common.h"
+#include "kernels.h"
+
+namespace wam {
+namespace {
+
+// Element k of the effective velocity of state sample j (k < n_video: the latent,
+// else the action part).  With guidance (state sample 0 from step samples 0 = cond
+// and 1 = uncond): v_u + s (v_c - v_u).
+WAM_DEV float eff_velocity(const FlowArgs& a, int j, int64_t k) {
+  if (a.v_in) return a.v_in[(int64_t)j * (a.n_video + a.n_action) + k];
+  const bool vid = k < a.n_video;
+  const float* base = vid ? a.v_video : a.v_action;
+  const int64_t n = vid ? a.n_video : a.n_action;
+  const int64_t kk = vid ? k : k - a.n_video;
+  if (a.cfg) {
+    const float vc = base[kk], vu = base[n + kk];
+    return vu + a.cfg_scale * (vc - vu);
+  }
+  return base[(int64_t)j * n + kk];
+}
+
+// x <- x + dt v_eff (in place), v_eff optionally kept, and the bf16 model inputs of the
+// next step rewritten from x for every step sample (both halves of a guidance pair).
+__global__ __launch_bounds__(256) void flow_step_kernel(const FlowArgs a) {
+  const int64_t n = a.n_video + a.n_action;
+  const int nx = a.cfg ? 1 : a.B;
+  const int64_t total = (int64_t)nx * n;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+    const int j = (int)(e / n);
+    const int64_t k = e - (int64_t)j * n;
+    float x = a.x[e];
+    if (a.v_video || a.v_action || a.v_in) {
+      const float v = eff_velocity(a, j, k);
+      if (a.v_out) a.v_out[e] = v;
+      x = __builtin_fmaf(a.dt, v, x);
+      a.x[e] = x;
+    }
+    const bf16 xb = (bf16)x;
+    const int b0 = a.cfg ? 0 : j, b1 = a.cfg ? a.B : j + 1;
+    for (int b = b0; b < b1; ++b) {
+      if (k < a.n_video) static_cast<bf16*>(a.z_next)[(int64_t)b * a.n_video + k] = xb;
+      else static_cast<bf16*>(a.a_next)[(int64_t)b * a.n_action + (k - a.n_video)] = xb;
+    }
+  }
+}
+
+// Deterministic cosine similarity: a fixed grid of COS_BLOCKS workgroups each writes its
+// (a.b, a.a, b.b) partial sums in fp64, then one workgroup adds them in a fixed order.
+constexpr int COS_BLOCKS = 512;
+
+__global__ __launch_bounds__(256) void cos_partial_kernel(const float* __restrict__ x, const float* __restrict__ y,
+                                                          int64_t n, double* __restrict__ part) {
+  double s[3] = {0.0, 0.0, 0.0};
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)COS_BLOCKS * 256) {
+    const double u = x[i], v = y[i];
+    s[0] += u * v;
+    s[1] += u * u;
+    s[2] += v * v;
+  }
+  __shared__ double red[3][256];
+  for (int c = 0; c < 3; ++c) red[c][threadIdx.x] = s[c];
+  __syncthreads();
+  for (int o = 128; o >= 1; o >>= 1) {
+    if ((int)threadIdx.x < o)
+      for (int c = 0; c < 3; ++c) red[c][threadIdx.x] += red[c][threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x < 3) part[blockIdx.x * 3 + threadIdx.x] = red[threadIdx.x][0];
+}
+
+__global__ __launch_bounds__(256) void cos_final_kernel(const double* __restrict__ part, float* __restrict__ out) {
+  __shared__ double red[3][256];
+  for (int c = 0; c < 3; ++c) {
+    double v = 0.0;
+    for (int i = threadIdx.x; i < COS_BLOCKS; i += 256) v += part[i * 3 + c];
+    red[c][threadIdx.x] = v;
+  }
+  __syncthreads();
+  for (int o = 128; o >= 1; o >>= 1) {
+    if ((int)threadIdx.x < o)
+      for (int c = 0; c < 3; ++c) red[c][threadIdx.x] += red[c][threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double den = sqrt(red[1][0]) * sqrt(red[2][0]);
+    out[0] = den > 0.0 ? (float)(red[0][0] / den) : 0.f;
+  }
+}
+
+__global__ void fill_kernel(float* p, int n, float v) {
+  if ((int)threadIdx.x < n) p[threadIdx.x] = v;
+}
+
+}  // namespace
+
+hipError_t launch_flow_step(const FlowArgs& a, hipStream_t s) {
+  const int64_t total = (int64_t)(a.cfg ? 1 : a.B) * (a.n_video + a.n_action);
+  if (total == 0) return hipSuccess;
+  const int64_t want = (total + 255) / 256;
+  const unsigned grid = (unsigned)(want < 4096 ? want : 4096);
+  hipLaunchKernelGGL(flow_step_kernel, dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+size_t cosine_workspace_bytes() { return (size_t)COS_BLOCKS * 3 * sizeof(double); }
+
+hipError_t launch_cosine(const float* x, const float* y, int64_t n, void* ws, float* out, hipStream_t s) {
+  double* part = static_cast<double*>(ws);
+  hipLaunchKernelGGL(cos_partial_kernel, dim3(COS_BLOCKS), dim3(256), 0, s, x, y, n, part);
+  hipLaunchKernelGGL(cos_final_kernel, dim3(1), dim3(256), 0, s, part, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill(float* p, int n, float v, hipStream_t s) {
+  hipLaunchKernelGGL(fill_kernel, dim3(1), dim3(64), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+}  // namespace wam

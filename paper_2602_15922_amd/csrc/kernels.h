@@ -72,4 +72,24 @@ hipError_t launch_patchify(int32_t B, int32_t C, int32_t F, int32_t Hl, int32_t 
 hipError_t launch_unpatchify(int32_t B, int32_t C, int32_t F, int32_t Hl, int32_t Wl,
                              const float* tok, float* out, hipStream_t s);
 
+// Solver step of the denoising loop over one chunk.  State x [nx][n_video + n_action]
+// fp32 (nx = 1 with guidance, else B); velocity from the step outputs v_video [B][n_video]
+// and v_action [B][n_action] (guidance: sample 0 cond, 1 uncond) or directly from v_in
+// [nx][n]; both NULL: x unchanged.  v_out (optional) receives the effective velocity;
+// z_next [B][n_video] / a_next [B][n_action] bf16 receive round(x) for every step sample.
+struct FlowArgs {
+  int32_t B, cfg;
+  float cfg_scale, dt;
+  int64_t n_video, n_action;
+  const float *v_video, *v_action, *v_in;
+  float *x, *v_out;
+  void *z_next, *a_next;
+};
+hipError_t launch_flow_step(const FlowArgs& a, hipStream_t s);
+// cosine similarity of x and y (n floats) into out[0]; ws of cosine_workspace_bytes()
+size_t cosine_workspace_bytes();
+hipError_t launch_cosine(const float* x, const float* y, int64_t n, void* ws, float* out, hipStream_t s);
+// p[0..n) = v for n <= 64
+hipError_t launch_fill(float* p, int n, float v, hipStream_t s);
+
 }  // namespace wam

@@ -41,6 +41,11 @@ def test_struct_sizes_match_the_header_layout():
     assert C.sizeof(b.wam_chunks) == 4 * (1 + 17 + 1 + 17 + 16)
     assert C.sizeof(b.wam_dims) == 10 * 4
     assert C.sizeof(b.wam_block_weights) == 17 * 8
+    # sizes printed by a C++ compile of include/wamdit.h
+    assert C.sizeof(b.wam_flow_dims) == 32
+    assert C.sizeof(b.wam_denoise_params) == 48
+    assert C.sizeof(b.wam_step_io) == 336
+    assert C.sizeof(b.wam_model) == 200
 
 
 def _status(fn, *args):
@@ -97,6 +102,10 @@ def test_gemm_and_block_reject_bad_arguments():
     assert L.wam_block_workspace_bytes(C.byref(dims), 1, 144, 32) > 0
     assert L.wam_dit_step_fwd(None, None, None, 0, None) == b.WAM_EINVAL
     assert L.wam_dit_update_fwd(None, None, None, 0, None) == b.WAM_EINVAL
+    assert L.wam_denoise_chunk(None, None, None, None, 0, None) == b.WAM_EINVAL
+    fd = b.wam_flow_dims(B=3, cfg=1, cfg_scale=2.0, n_video=8, n_action=0)
+    assert L.wam_flow_step(C.byref(fd), None, None, None, 4096, None, 0.0, 0.1, 8192, None, None) == b.WAM_EINVAL
+    assert L.wam_cosine_similarity(4096, 8192, 16, None, 0, 12288, None) == b.WAM_EWORKSPACE
 
 
 def test_rope_tables_and_positions_agree_with_the_oracle():

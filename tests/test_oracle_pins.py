@@ -638,9 +638,9 @@ def test_dit_caching_skips_a_window_after_similar_velocities():
     x, computed = oracle.denoise(np.zeros(4), const_v, ts, tau=0.9, window=2)
     assert computed == [True, True, False, False, True, False, False, True]
     assert len(calls) == 4 and np.allclose(x, 1.0)
-    # tau above 1 never skips; tau <= 0 disables caching
-    for tau in (1.5, 0.0):
-        _, computed = oracle.denoise(np.zeros(4), const_v, ts, tau=tau, window=2)
+    # tau above 1 never skips; no tau or a zero window disables caching
+    for tau, window in ((1.5, 2), (None, 2), (0.5, 0)):
+        _, computed = oracle.denoise(np.zeros(4), const_v, ts, tau=tau, window=window)
         assert all(computed)
     # dissimilar successive velocities never trigger a skip
     flip = {"s": 1.0}
