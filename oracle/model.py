@@ -60,7 +60,9 @@ def dit_block(x, e0, W, H, eps, pos, q_chunk, k_prev=None, v_prev=None, prev_chu
               ctx=None, ctx_kv=None):
     """One DiT block over the current chunk rows.
 
-    x (B, L, d) residual; e0 (B, 6, d) time modulation; W the block's weights;
+    x (B, L, d) residual; e0 (B, 6, d) time modulation, or (B, L, 6, d) for a
+    per-token modulation (DreamZero-Flash: video and action tokens at their own
+    timesteps, Appendix D.3); W the block's weights;
     pos (L, 3) RoPE positions and q_chunk (L,) chunk ids of the current rows;
     k_prev / v_prev (B, Lp, H, Dh) the cached K (after RoPE) and V of earlier rows,
     prev_chunk (Lp,) their chunk ids; ctx (B, Lc, d) projected text, or ctx_kv
@@ -71,8 +73,12 @@ def dit_block(x, e0, W, H, eps, pos, q_chunk, k_prev=None, v_prev=None, prev_chu
     """
     B, L, d = x.shape
     Dh = d // H
-    m = W["mod6"][None] + e0
-    sh1, sc1, g1, sh2, sc2, g2 = (m[:, i][:, None, :] for i in range(6))
+    if e0.ndim == 4:
+        m = W["mod6"][None, None] + e0
+        sh1, sc1, g1, sh2, sc2, g2 = (m[:, :, i] for i in range(6))
+    else:
+        m = W["mod6"][None] + e0
+        sh1, sc1, g1, sh2, sc2, g2 = (m[:, i][:, None, :] for i in range(6))
 
     # self-attention against cache + current chunk
     qkv = linear(modulate(x, sh1, sc1, eps), W["w_qkv"], W["b_qkv"])
@@ -109,26 +115,34 @@ def dit_block(x, e0, W, H, eps, pos, q_chunk, k_prev=None, v_prev=None, prev_chu
 
 
 def head(x, e, head_mod2, Lv, w_hv, b_hv, w_ha, b_ha, eps, C, F, Hl, Wl):
-    """Output head: AdaLN with (shift, scale) = head_mod2 + e, then the video
-    decoder (Linear to patch features, unpatchified) on the first Lv rows and the
-    action decoder (Linear) on the rest."""
-    m = head_mod2[None] + e[:, None, :]
-    h = modulate(x, m[:, 0][:, None, :], m[:, 1][:, None, :], eps)
+    """Output head: AdaLN with (shift, scale) = head_mod2 + e (e of shape (B, d), or
+    (B, L, d) per token), then the video decoder (Linear to patch features,
+    unpatchified) on the first Lv rows and the action decoder (Linear) on the rest."""
+    e = e[:, None, :] if e.ndim == 2 else e
+    m = head_mod2[None, None] + e[:, :, None, :]
+    h = modulate(x, m[:, :, 0], m[:, :, 1], eps)
     v_video = unpatchify(linear(h[:, :Lv], w_hv, b_hv), C, F, Hl, Wl)
     v_action = linear(h[:, Lv:], w_ha, b_ha)
     return v_video, v_action
 
 
 def dit_step(z_t, a_t, t, text, P, layers, n_layers, H, eps, chunk_index, pos,
-             prev_chunk=None, q_chunk=None, ctx=None):
+             prev_chunk=None, q_chunk=None, ctx=None, t_action=None):
     """u_theta([z_t, a_t]; KV, c, t, update=False) for one chunk.
 
     z_t (B, C, F, Hl, Wl) noisy latents; a_t (B, A, act_dim) noisy actions; t (B,);
     text (B, Lc, text_dim) text features; P the model-level weights; layers(l)
     returns (W_l, k_prev_l, v_prev_l), so callers can stream one layer at a time.
-    Returns (v_video, v_action)."""
+    t_action (B,), when given, is the action tokens' own timestep (DreamZero-Flash,
+    Appendix D.3): their AdaLN and head modulation come from it, the video tokens'
+    from t.  Returns (v_video, v_action)."""
     B, C, F, Hl, Wl = z_t.shape
     e, e0 = time_embedding(t, P["w_t1"], P["b_t1"], P["w_t2"], P["b_t2"], P["w_t6"], P["b_t6"])
+    if t_action is not None:
+        ea, e0a = time_embedding(t_action, P["w_t1"], P["b_t1"], P["w_t2"], P["b_t2"], P["w_t6"], P["b_t6"])
+        Lv_, A_ = F * (Hl // 2) * (Wl // 2), a_t.shape[1]
+        e = np.concatenate([np.repeat(e[:, None], Lv_, 1), np.repeat(ea[:, None], A_, 1)], axis=1)
+        e0 = np.concatenate([np.repeat(e0[:, None], Lv_, 1), np.repeat(e0a[:, None], A_, 1)], axis=1)
     if ctx is None:
         ctx = text_projection(text, P["w_x1"], P["b_x1"], P["w_x2"], P["b_x2"])
     x = embed(z_t, a_t, P["w_patch"], P["b_patch"], P["w_ain"], P["b_ain"])

@@ -582,6 +582,103 @@ def test_update_identity_blocks_closed_form():
             assert np.allclose(kv[l][1][0, tok].reshape(d), vraw, atol=1e-10)
 
 
+# ----------------------------------------------------------------------------- DreamZero-Flash
+def flash_case(seed):
+    g = np.random.default_rng(seed)
+    B, C, F, Hl, Wl, A, ad, d, H, tdim, Lc = 2, 2, 2, 4, 4, 3, 5, 16, 2, 12, 4
+    P = small_model_params(g, d, C, ad, tdim)
+    Ws = [small_block_weights(d, 32, seed + 1 + l) for l in range(2)]
+    z, a = g.standard_normal((B, C, F, Hl, Wl)), g.standard_normal((B, A, ad))
+    text = g.standard_normal((B, Lc, tdim))
+    kp = g.standard_normal((B, 6, H, d // H))
+    pos = chunk_positions(1, F, Hl // 2, Wl // 2, A)
+    return P, Ws, z, a, text, kp, pos, H
+
+
+def test_flash_equal_timesteps_reduce_to_the_shared_step():
+    P, Ws, z, a, text, kp, pos, H = flash_case(160)
+    t = np.array([0.3, 0.9])
+    run = lambda ta: oracle.dit_step(z, a, t, text, P, lambda l: (Ws[l], kp, kp), 2, H, 1e-6, 1, pos,
+                                     prev_chunk=np.zeros(6, int), t_action=ta)
+    v0, a0 = run(None)
+    v1, a1 = run(t.copy())
+    assert np.allclose(v0, v1, atol=1e-12) and np.allclose(a0, a1, atol=1e-12)
+    # a different action timestep changes both outputs (the action rows feed attention)
+    v2, a2 = run(np.array([0.7, 0.1]))
+    assert not np.allclose(a0, a2) and not np.allclose(v0, v2)
+
+
+def test_block_per_token_modulation_is_row_wise():
+    """With the self-attention gate and the cross-attention output at zero the block acts
+    on each token alone, so a per-token modulation must give every row what a uniform
+    modulation equal to that row's gives it."""
+    g = np.random.default_rng(161)
+    B, L, d, H = 2, 5, 16, 2
+    W = small_block_weights(d, 32, 162)
+    W["mod6"][2] = 0.0
+    W["w_co"] = np.zeros((d, d))
+    W["b_co"] = np.zeros(d)
+    x = g.standard_normal((B, L, d))
+    e0 = g.standard_normal((B, L, 6, d)) * 0.5
+    e0[:, :, 2] = 0.0
+    ctx = g.standard_normal((B, 3, d))
+    pos = chunk_positions(0, 1, 1, 3, 2)
+    ch = np.zeros(L, int)
+    out, _, _ = oracle.dit_block(x, e0, W, H, 1e-6, pos, ch, ctx=ctx)
+    for i in range(L):
+        row, _, _ = oracle.dit_block(x, e0[:, i], W, H, 1e-6, pos, ch, ctx=ctx)
+        assert np.allclose(out[:, i], row[:, i], atol=1e-12)
+
+
+def test_flash_identity_blocks_closed_form():
+    """Identity blocks: the velocity is the head applied to the embeddings, with the video
+    rows modulated by e(t) and the action rows by e(t_action), written out per token."""
+    P, Ws, z, a, text, kp, pos, H = flash_case(163)
+    d = P["w_t2"].shape[0]
+    for gate in (2, 5):
+        P["w_t6"][gate * d:(gate + 1) * d] = 0.0
+        P["b_t6"][gate * d:(gate + 1) * d] = 0.0
+    for W in Ws:
+        W["mod6"][2] = W["mod6"][5] = 0.0
+        W["w_co"] = np.zeros((d, d))
+        W["b_co"] = np.zeros(d)
+    B, C, F, Hl, Wl = z.shape
+    A = a.shape[1]
+    t, ta = np.array([0.2, 0.6]), np.array([0.95, 0.05])
+    vv, va = oracle.dit_step(z, a, t, text, P, lambda l: (Ws[l], kp, kp), 2, H, 1e-6, 1, pos,
+                             prev_chunk=np.zeros(6, int), t_action=ta)
+
+    def e_of(tt):
+        s = np.array([math.cos(1000 * tt * 10000 ** (-k / 128)) for k in range(128)]
+                     + [math.sin(1000 * tt * 10000 ** (-k / 128)) for k in range(128)])
+        h1 = P["w_t1"] @ s + P["b_t1"]
+        h1 = h1 / (1 + np.exp(-h1))
+        return P["w_t2"] @ h1 + P["b_t2"]
+
+    Hg, Wg = Hl // 2, Wl // 2
+    for b in range(B):
+        ev, ea = e_of(t[b]), e_of(ta[b])
+        for tok in range(F * Hg * Wg + A):
+            e = ev if tok < F * Hg * Wg else ea
+            sh, sc = P["head_mod2"][0] + e, P["head_mod2"][1] + e
+            if tok < F * Hg * Wg:
+                f, rem = divmod(tok, Hg * Wg)
+                r, s_ = divmod(rem, Wg)
+                feat = np.array([z[b, c, f, 2 * r + ph, 2 * s_ + pw] for c in range(C) for ph in range(2)
+                                 for pw in range(2)])
+                xt = P["w_patch"] @ feat + P["b_patch"]
+            else:
+                xt = P["w_ain"] @ a[b, tok - F * Hg * Wg] + P["b_ain"]
+            ht = (xt - xt.mean()) / math.sqrt(xt.var() + 1e-6) * (1 + sc) + sh
+            if tok < F * Hg * Wg:
+                out = P["w_hv"] @ ht + P["b_hv"]
+                got = np.array([vv[b, c, f, 2 * r + ph, 2 * s_ + pw] for c in range(C) for ph in range(2)
+                                for pw in range(2)])
+                assert np.allclose(got, out, atol=1e-10)
+            else:
+                assert np.allclose(va[b, tok - F * Hg * Wg], P["w_ha"] @ ht + P["b_ha"], atol=1e-10)
+
+
 # ----------------------------------------------------------------------------- denoising loop
 def test_euler_follows_the_straight_path_of_eq2():
     """With the path's own velocity z1 - z0 (constant along Eq. 2's interpolation), every
