@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define WAM_ABI_VERSION 1
+#define WAM_ABI_VERSION 2
 #define WAM_MAX_CHUNKS 16
 
 typedef enum {
@@ -218,6 +218,10 @@ typedef struct {
  * attn_events  optional HOST array of 2*n_layers hipEvent_t: when non-NULL,
  *          events[2l] and events[2l+1] are recorded on `stream` just before and just
  *          after block l's self-attention kernel (for per-kernel timing).
+ * t_action optional [B] fp32 device: the action tokens' own timestep (DreamZero-Flash,
+ *          Appendix D.3).  When non-NULL (and A > 0) the action rows' AdaLN modulation,
+ *          gates and head modulation come from t_action's time embedding and the video
+ *          rows' from t's; NULL: every row uses t.
  * ------------------------------------------------------------------------------ */
 typedef struct {
   const void* z_t;
@@ -233,6 +237,7 @@ typedef struct {
   float* v_video;
   float* v_action;
   hipEvent_t* attn_events;
+  const float* t_action;
 } wam_step_io;
 
 size_t wam_step_workspace_bytes(const wam_model* m, const wam_step_io* io);

@@ -88,7 +88,7 @@ class wam_step_io(C.Structure):
                 ("rope_cos", _vp), ("rope_sin", _vp),
                 ("B", _i32), ("F", _i32), ("Hl", _i32), ("Wl", _i32), ("A", _i32), ("Lc", _i32),
                 ("Lcap", _i32), ("cache_len", _i32), ("ch", wam_chunks),
-                ("v_video", _vp), ("v_action", _vp), ("attn_events", C.POINTER(_vp))]
+                ("v_video", _vp), ("v_action", _vp), ("attn_events", C.POINTER(_vp)), ("t_action", _vp)]
 
 
 class wam_flow_dims(C.Structure):
@@ -356,12 +356,12 @@ def _ptr_array(ts):
 
 
 def make_step_io(z_t, a_t, t, text, k_caches, v_caches, rope_cos, rope_sin, cache_len, chunks, v_video,
-                 v_action, ctx_kv=None, events=None) -> wam_step_io:
+                 v_action, ctx_kv=None, events=None, t_action=None) -> wam_step_io:
     B, _, F, Hl, Wl = z_t.shape
     io = wam_step_io(z_t=_p(z_t), a_t=_p(a_t), t=_p(t), text=_p(text), rope_cos=_p(rope_cos),
                      rope_sin=_p(rope_sin), B=B, F=F, Hl=Hl, Wl=Wl, A=a_t.shape[1], Lc=text.shape[1],
                      Lcap=k_caches[0].shape[1] if k_caches else 0, cache_len=cache_len, ch=chunks,
-                     v_video=_p(v_video), v_action=_p(v_action))
+                     v_video=_p(v_video), v_action=_p(v_action), t_action=_p(t_action))
     kc, vc = _ptr_array(k_caches), _ptr_array(v_caches)
     io.k_cache = C.cast(kc, C.POINTER(_vp))
     io.v_cache = C.cast(vc, C.POINTER(_vp))

@@ -145,7 +145,7 @@ wam_chunks single_chunk(int32_t Lq, int32_t Lk) {
 // ---------------------------------------------------------------------------------
 // GEMM
 // ---------------------------------------------------------------------------------
-wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s) {
+wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s, int32_t gate_split = 0, int64_t gate_alt = 0) {
   CHECK(g.M >= 0 && g.N >= 1 && g.K >= 8 && g.K % 8 == 0, WAM_EINVAL,
         "GEMM sizes M=%d N=%d K=%d (need N>=1, K>=8, K%%8==0)", g.M, g.N, g.K);
   CHECK(g.epilogue >= WAM_EPI_BF16 && g.epilogue <= WAM_EPI_F32, WAM_EINVAL, "unknown epilogue %d", g.epilogue);
@@ -178,6 +178,7 @@ wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s) {
   a.W = g.W; a.ldw = g.ldw; a.bias = g.bias;
   a.out = g.out; a.ldo = g.ldo; a.o_bs = g.out_batch_stride; a.o_rows = g.out_rows;
   a.gate_a = g.gate_a; a.gate_v = g.gate_v; a.gate_stride = g.gate_stride; a.gate_rows = g.gate_rows;
+  a.gate_split = gate_split; a.gate_alt = gate_alt;
   HIPCHECK(launch_gemm(a, s));
   return WAM_OK;
 }
@@ -241,8 +242,10 @@ wam_status check_block_io(const wam_dims& D, const wam_block_weights& w, const w
 }
 
 // The launch sequence of one block; arguments already validated.
+// seg/alt: rows >= seg of a sample (0: none) take their per-sample modulation (e0) from
+// e0 + alt (the action tokens' own timestep).
 wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_block_io& io, char* ws,
-                     hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+                     hipStream_t s, hipEvent_t ev0, hipEvent_t ev1, int32_t seg = 0, int64_t alt = 0) {
   const int d = D.d, B = io.B, L = io.L, M = B * L;
   const BlockWs lay = block_ws(D, B, L, io.Lc);
   void* h = ws + lay.h;
@@ -255,7 +258,7 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   const int64_t ms = 6 * (int64_t)d;
 
   // 1. AdaLN: h = LN(x)(1 + scale1) + shift1
-  LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h};
+  LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h, seg, alt};
   HIPCHECK(launch_ln_mod(ln, s));
   // 2. fused QKV projection
   TRY(gemm_checked(gemm(M, 3 * d, d, WAM_EPI_BF16, h, d, W.w_qkv, W.b_qkv, big, 3 * d), s));
@@ -276,7 +279,7 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   {
     wam_gemm_desc g = gemm(M, d, d, WAM_EPI_RESID_F32, o, d, W.w_o, W.b_o, io.x, d);
     g.gate_a = m6 + 2 * d; g.gate_v = e0 + 2 * d; g.gate_stride = ms; g.gate_rows = L;
-    TRY(gemm_checked(g, s));
+    TRY(gemm_checked(g, s, seg, alt));
   }
   // 6. cross-attention LayerNorm (affine, no modulation)
   LnArgs lc{M, L, d, D.eps, io.x, W.lnc_gamma, W.lnc_beta, nullptr, nullptr, nullptr, nullptr, 0, h};
@@ -300,7 +303,7 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   // 10. x += o W_co^T + b_co (no gate)
   TRY(gemm_checked(gemm(M, d, d, WAM_EPI_RESID_F32, o, d, W.w_co, W.b_co, io.x, d), s));
   // 11. AdaLN #2
-  LnArgs l2{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 3 * d, e0 + 3 * d, m6 + 4 * d, e0 + 4 * d, ms, h};
+  LnArgs l2{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 3 * d, e0 + 3 * d, m6 + 4 * d, e0 + 4 * d, ms, h, seg, alt};
   HIPCHECK(launch_ln_mod(l2, s));
   // 12. FFN up-projection with tanh-GELU
   TRY(gemm_checked(gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, big, D.ffn), s));
@@ -308,7 +311,7 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   {
     wam_gemm_desc g = gemm(M, d, D.ffn, WAM_EPI_RESID_F32, big, D.ffn, W.w_f2, W.b_f2, io.x, d);
     g.gate_a = m6 + 5 * d; g.gate_v = e0 + 5 * d; g.gate_stride = ms; g.gate_rows = L;
-    TRY(gemm_checked(g, s));
+    TRY(gemm_checked(g, s, seg, alt));
   }
   return WAM_OK;
 }
@@ -316,7 +319,7 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
 // The part of a block that an update pass needs from its last layer: AdaLN #1, the K|V
 // columns of the QKV projection, and RoPE on k with the cache append.
 wam_status block_kv_run(const wam_dims& D, const wam_block_weights& W, const wam_block_io& io, char* ws,
-                        hipStream_t s) {
+                        hipStream_t s, int32_t seg = 0, int64_t alt = 0) {
   const int d = D.d, B = io.B, L = io.L, M = B * L;
   const BlockWs lay = block_ws(D, B, L, io.Lc);
   void* h = ws + lay.h;
@@ -324,7 +327,7 @@ wam_status block_kv_run(const wam_dims& D, const wam_block_weights& W, const wam
   const float* m6 = W.mod6;
   const float* e0 = io.e0;
   const int64_t ms = 6 * (int64_t)d;
-  LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h};
+  LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h, seg, alt};
   HIPCHECK(launch_ln_mod(ln, s));
   // rows d..3d of W_qkv (the k and v outputs) into columns d..3d of the [M][3d] buffer
   const char* wkv = static_cast<const char*>(W.w_qkv) + (size_t)d * d * 2;
@@ -408,14 +411,16 @@ HeadWs head_ws(const wam_dims& D, int32_t B, int32_t F, int32_t Hl, int32_t Wl, 
   return w;
 }
 
+// e_alt: the action rows' embedding is e + e_alt (0: the same as the video rows')
 wam_status head_run(const wam_model& m, int32_t B, int32_t F, int32_t Hl, int32_t Wl, int32_t A, const float* x,
-                    const float* e, float* v_video, float* v_action, char* ws, hipStream_t s) {
+                    const float* e, float* v_video, float* v_action, char* ws, hipStream_t s, int64_t e_alt = 0) {
   const wam_dims& D = m.dims;
   const int d = D.d, P = D.latent_ch * 4, Lv = F * (Hl / 2) * (Wl / 2), L = Lv + A;
   const HeadWs lay = head_ws(D, B, F, Hl, Wl, A);
   char* h = ws + lay.h;
   float* tok = reinterpret_cast<float*>(ws + lay.tok);
-  LnArgs ln{B * L, L, d, D.eps, x, nullptr, nullptr, m.head_mod2, e, m.head_mod2 + d, e, d, h};
+  LnArgs ln{B * L, L, d, D.eps, x, nullptr, nullptr, m.head_mod2, e, m.head_mod2 + d, e, d, h,
+            e_alt ? Lv : 0, e_alt};
   HIPCHECK(launch_ln_mod(ln, s));
   wam_gemm_desc gv = gemm(B * Lv, P, d, WAM_EPI_F32, h, d, m.w_hv, m.b_hv, tok, P);
   gv.a_rows = Lv; gv.a_batch_stride = (int64_t)L * d;
@@ -439,8 +444,9 @@ StepWs step_ws(const wam_model& m, const wam_step_io& io) {
   StepWs w{};
   size_t off = 0;
   w.x = off; off += align256(M * D.d * 4);
-  w.e = off; off += align256((size_t)io.B * D.d * 4);
-  w.e0 = off; off += align256((size_t)io.B * 6 * D.d * 4);
+  // time embeddings of t, then (DreamZero-Flash) of t_action
+  w.e = off; off += align256((size_t)2 * io.B * D.d * 4);
+  w.e0 = off; off += align256((size_t)2 * io.B * 6 * D.d * 4);
   w.ctx = off; off += align256((size_t)io.B * io.Lc * D.d * 2);
   // scratch for the time MLP, text projection, embedding and head (used one at a time)
   size_t piece = time_ws(D, io.B);
@@ -514,6 +520,10 @@ wam_status step_run(const wam_model& m, const wam_step_io& io, char* w, hipStrea
   const int32_t Lv = io.F * (io.Hl / 2) * (io.Wl / 2), L = Lv + io.A;
 
   TRY(time_run(m, io.B, io.t, e, e0, piece, stream));
+  // DreamZero-Flash: the action rows' modulation comes from their own timestep
+  const bool flash = io.t_action != nullptr && io.A > 0;
+  const int64_t alt_e = flash ? (int64_t)io.B * D.d : 0, alt_e0 = flash ? (int64_t)io.B * 6 * D.d : 0;
+  if (flash) TRY(time_run(m, io.B, io.t_action, e + alt_e, e0 + alt_e0, piece, stream));
   if (!io.ctx_kv) TRY(text_run(m, io.B, io.Lc, io.text, ctx, piece, stream));
   TRY(embed_run(m, io.B, io.F, io.Hl, io.Wl, io.A, io.z_t, io.a_t, x, piece, stream));
   for (int l = 0; l < D.n_layers; ++l) {
@@ -524,9 +534,9 @@ wam_status step_run(const wam_model& m, const wam_step_io& io, char* w, hipStrea
     b.B = io.B; b.L = L; b.Lc = io.Lc;
     hipEvent_t ev0 = io.attn_events ? io.attn_events[2 * l] : nullptr;
     hipEvent_t ev1 = io.attn_events ? io.attn_events[2 * l + 1] : nullptr;
-    TRY(block_run(D, m.blocks[l], b, w + lay.block, stream, ev0, ev1));
+    TRY(block_run(D, m.blocks[l], b, w + lay.block, stream, ev0, ev1, flash ? Lv : 0, alt_e0));
   }
-  TRY(head_run(m, io.B, io.F, io.Hl, io.Wl, io.A, x, e, io.v_video, io.v_action, piece, stream));
+  TRY(head_run(m, io.B, io.F, io.Hl, io.Wl, io.A, x, e, io.v_video, io.v_action, piece, stream, alt_e));
   return WAM_OK;
 }
 
@@ -736,6 +746,9 @@ wam_status wam_dit_update_fwd(const wam_model* m, const wam_step_io* io, void* w
   const int32_t Lv = io->F * (io->Hl / 2) * (io->Wl / 2), L = Lv + io->A;
 
   TRY(time_run(*m, io->B, io->t, e, e0, piece, stream));
+  const bool flash = io->t_action != nullptr && io->A > 0;
+  const int64_t alt_e0 = flash ? (int64_t)io->B * 6 * D.d : 0;
+  if (flash) TRY(time_run(*m, io->B, io->t_action, e + (int64_t)io->B * D.d, e0 + alt_e0, piece, stream));
   if (!io->ctx_kv && D.n_layers > 1) TRY(text_run(*m, io->B, io->Lc, io->text, ctx, piece, stream));
   TRY(embed_run(*m, io->B, io->F, io->Hl, io->Wl, io->A, io->z_t, io->a_t, x, piece, stream));
   for (int l = 0; l < D.n_layers; ++l) {
@@ -745,11 +758,11 @@ wam_status wam_dit_update_fwd(const wam_model* m, const wam_step_io* io, void* w
     b.ch = io->ch; b.ctx = ctx; b.ctx_kv = io->ctx_kv ? io->ctx_kv[l] : nullptr;
     b.B = io->B; b.L = L; b.Lc = io->Lc;
     if (l + 1 == D.n_layers) {
-      TRY(block_kv_run(D, m->blocks[l], b, w + lay.block, stream));
+      TRY(block_kv_run(D, m->blocks[l], b, w + lay.block, stream, flash ? Lv : 0, alt_e0));
     } else {
       hipEvent_t ev0 = io->attn_events ? io->attn_events[2 * l] : nullptr;
       hipEvent_t ev1 = io->attn_events ? io->attn_events[2 * l + 1] : nullptr;
-      TRY(block_run(D, m->blocks[l], b, w + lay.block, stream, ev0, ev1));
+      TRY(block_run(D, m->blocks[l], b, w + lay.block, stream, ev0, ev1, flash ? Lv : 0, alt_e0));
     }
   }
   return WAM_OK;
@@ -801,6 +814,7 @@ wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wa
   CHECK(p->n_steps >= 1, WAM_EINVAL, "n_steps=%d must be >= 1", p->n_steps);
   CHECK(p->t_sched != nullptr, WAM_EINVAL, "t_sched is NULL");
   CHECK(p->cache_window >= 0, WAM_EINVAL, "cache_window < 0");
+  CHECK(io->t_action == nullptr, WAM_EUNSUPPORTED, "the loop runs one schedule for both modalities (t_action must be NULL)");
   TRY(need_ptr(p->x, "x"));
   wam_flow_dims fd{};
   fd.B = io->B; fd.cfg = p->cfg; fd.cfg_scale = p->cfg_scale;

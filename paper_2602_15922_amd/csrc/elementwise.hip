@@ -12,7 +12,9 @@ namespace {
 // AdaLN modulation, to bf16.  Both are folded into one per-column affine,
 //   y = LN(x) * P + Q,  P = gamma (1 + scale),  Q = beta (1 + scale) + shift,
 // computed once per workgroup into LDS (2*d floats): a workgroup owns LN_ROWS rows of
-// one sample, so the modulation vectors are read once per LN_ROWS rows.  One wavefront
+// one sample and one row segment (a sample's rows may form two segments with their own
+// per-sample modulation: video and action tokens at their own timesteps), so the
+// modulation vectors are read once per LN_ROWS rows.  One wavefront
 // per row, so a 3152-row call keeps ~3150 rows in flight at once; the row stays in
 // registers (NV float4 per lane, NV = d/256) between the mean, variance and output
 // passes, so x is read from HBM once.
@@ -20,13 +22,17 @@ namespace {
 constexpr int LN_ROWS = 4;  // rows (= wavefronts) per workgroup
 
 template <int NV>
-__global__ __launch_bounds__(LN_ROWS * 64) void ln_mod_kernel(const LnArgs a, int blocks_per_batch) {
+__global__ __launch_bounds__(LN_ROWS * 64) void ln_mod_kernel(const LnArgs a, int blocks_per_batch, int seg,
+                                                              int seg_blocks) {
   extern __shared__ __attribute__((aligned(16))) float PQ[];  // [2][d]
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int b = blockIdx.x / blocks_per_batch;
-  const int rloc = (blockIdx.x % blocks_per_batch) * LN_ROWS + w;
+  const int b = blockIdx.x / blocks_per_batch, j = blockIdx.x % blocks_per_batch;
+  // a workgroup's rows lie in one segment: [0, seg) or [seg, rows_per_batch)
+  const bool second = j >= seg_blocks;
+  const int rloc = second ? seg + (j - seg_blocks) * LN_ROWS + w : j * LN_ROWS + w;
+  const int rend = second ? a.rows_per_batch : seg;
   const int d = a.d, nv = d >> 8;
-  const int64_t mb = (int64_t)b * a.mod_stride;
+  const int64_t mb = (int64_t)b * a.mod_stride + (second ? a.alt_off : 0);
   float* P = PQ;
   float* Q = PQ + d;
   for (int c = threadIdx.x * 4; c < d; c += LN_ROWS * 256) {
@@ -42,7 +48,7 @@ __global__ __launch_bounds__(LN_ROWS * 64) void ln_mod_kernel(const LnArgs a, in
     *reinterpret_cast<f32x4*>(Q + c) = bt * (one + sc) + sh;
   }
   __syncthreads();
-  if (rloc >= a.rows_per_batch) return;
+  if (rloc >= rend) return;
   const int64_t row = (int64_t)b * a.rows_per_batch + rloc;
   const float* xr = a.x + row * d;
   f32x4 v[NV];
@@ -200,14 +206,16 @@ __global__ void unpatchify_kernel(int B, int C, int F, int Hl, int Wl, const flo
 hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s) {
   if (a.rows == 0) return hipSuccess;
   const int B = a.rows / a.rows_per_batch;
-  const int bpb = (a.rows_per_batch + LN_ROWS - 1) / LN_ROWS;
+  const int seg = a.seg_rows > 0 && a.seg_rows < a.rows_per_batch ? a.seg_rows : a.rows_per_batch;
+  const int sb0 = (seg + LN_ROWS - 1) / LN_ROWS;
+  const int bpb = sb0 + (a.rows_per_batch - seg + LN_ROWS - 1) / LN_ROWS;
   const dim3 grid((unsigned)(B * bpb)), block(LN_ROWS * 64);
   const size_t lds = (size_t)2 * a.d * sizeof(float);  // d <= 8192: at most 64 KB
   const int nv = a.d / 256;
-  if (nv <= 2) hipLaunchKernelGGL(ln_mod_kernel<2>, grid, block, lds, s, a, bpb);
-  else if (nv <= 8) hipLaunchKernelGGL(ln_mod_kernel<8>, grid, block, lds, s, a, bpb);
-  else if (nv <= 20) hipLaunchKernelGGL(ln_mod_kernel<20>, grid, block, lds, s, a, bpb);
-  else hipLaunchKernelGGL(ln_mod_kernel<32>, grid, block, lds, s, a, bpb);
+  if (nv <= 2) hipLaunchKernelGGL(ln_mod_kernel<2>, grid, block, lds, s, a, bpb, seg, sb0);
+  else if (nv <= 8) hipLaunchKernelGGL(ln_mod_kernel<8>, grid, block, lds, s, a, bpb, seg, sb0);
+  else if (nv <= 20) hipLaunchKernelGGL(ln_mod_kernel<20>, grid, block, lds, s, a, bpb, seg, sb0);
+  else hipLaunchKernelGGL(ln_mod_kernel<32>, grid, block, lds, s, a, bpb, seg, sb0);
   return hipGetLastError();
 }
 

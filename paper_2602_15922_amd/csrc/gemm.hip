@@ -56,6 +56,16 @@ WAM_DEV int64_t group_off(int row, int rows, float inv, int64_t group_stride, in
   return (int64_t)q * group_stride + (int64_t)r * ld;
 }
 
+// Offset of row `row`'s per-group gate vector: its group's stride, plus gate_alt for
+// the rows of a group at or past gate_split.
+WAM_DEV int64_t gate_off(const GemmArgs& g, int row, float inv) {
+  int q = (int)(((float)row + 0.5f) * inv);
+  int r = row - q * g.gate_rows;
+  if (r < 0) { q -= 1; r += g.gate_rows; }
+  else if (r >= g.gate_rows) { q += 1; r -= g.gate_rows; }
+  return (int64_t)q * g.gate_stride + (g.gate_split > 0 && r >= g.gate_split ? g.gate_alt : 0);
+}
+
 // Epilogue of four consecutive columns [col, col+4) of one output row.
 template <int EPI>
 WAM_DEV void epilogue4(const GemmArgs& g, const float inv_o, const float inv_g, int row, int col, f32x4 v) {
@@ -73,7 +83,7 @@ WAM_DEV void epilogue4(const GemmArgs& g, const float inv_o, const float inv_g, 
       if (g.gate_a || g.gate_v) {
         gt = g.gate_a ? *reinterpret_cast<const f32x4*>(g.gate_a + col) : f32x4{0.f, 0.f, 0.f, 0.f};
         if (g.gate_v)
-          gt += *reinterpret_cast<const f32x4*>(g.gate_v + group_off(row, g.gate_rows, inv_g, g.gate_stride, 0) + col);
+          gt += *reinterpret_cast<const f32x4*>(g.gate_v + gate_off(g, row, inv_g) + col);
       }
       f32x4* o = reinterpret_cast<f32x4*>(static_cast<float*>(g.out) + orow + col);
       *o = *o + gt * v;
@@ -93,7 +103,7 @@ WAM_DEV void epilogue4(const GemmArgs& g, const float inv_o, const float inv_g, 
       float gt = 1.f;
       if (g.gate_a || g.gate_v) {
         gt = g.gate_a ? g.gate_a[col + j] : 0.f;
-        if (g.gate_v) gt += g.gate_v[group_off(row, g.gate_rows, inv_g, g.gate_stride, 0) + col + j];
+        if (g.gate_v) gt += g.gate_v[gate_off(g, row, inv_g) + col + j];
       }
       float* o = static_cast<float*>(g.out) + orow + col + j;
       *o = *o + gt * x;

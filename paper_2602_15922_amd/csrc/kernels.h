@@ -38,6 +38,9 @@ struct GemmArgs {
   const float* gate_v;
   int64_t gate_stride;
   int32_t gate_rows;
+  // rows r >= gate_split of a gate group (0: none) read gate_v + gate_alt instead
+  int32_t gate_split;
+  int64_t gate_alt;
 };
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 
@@ -48,6 +51,10 @@ struct LnArgs {
   const float *gamma, *beta, *shift_a, *shift_v, *scale_a, *scale_v;
   int64_t mod_stride;
   void* h;
+  // rows >= seg_rows of a sample (seg_rows <= 0 or >= rows_per_batch: none) take their
+  // per-sample modulation from shift_v / scale_v + alt_off
+  int32_t seg_rows;
+  int64_t alt_off;
 };
 hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s);
 

@@ -20,7 +20,7 @@ TENSOR_IDS = {
     # activations / inputs
     "x": 1, "e0": 2, "ctx": 3, "text": 4, "t": 5, "z_t": 6, "a_t": 7,
     "q": 8, "k": 9, "v": 10, "k_cache": 11, "v_cache": 12, "o_init": 13,
-    "pos_perm": 14, "probe": 15, "z_clean": 16,
+    "pos_perm": 14, "probe": 15, "z_clean": 16, "t_action": 17,
     # per-block weights
     "w_qkv": 20, "b_qkv": 21, "w_o": 22, "b_o": 23, "w_cq": 24, "b_cq": 25,
     "w_ckv": 26, "b_ckv": 27, "w_co": 28, "b_co": 29, "w_f1": 30, "b_f1": 31,

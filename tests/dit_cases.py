@@ -96,13 +96,15 @@ class StepCase:
     """A denoising step of `wl` with n_layers seeded blocks (streamed one at a time on the
     oracle side)."""
 
-    def __init__(self, wl, n_layers, bias_std=0.0):
+    def __init__(self, wl, n_layers, bias_std=0.0, flash=False):
         self.wl, self.n_layers, self.bias_std = wl, n_layers, bias_std
         B, s = wl.B, wl.seed
         self.P = synth.model_params(wl, bias_std=bias_std)
         self.z = synth.normal(s, "z_t", (B, wl.latent_ch, wl.F, wl.Hl, wl.Wl), 1.0)
         self.a = synth.normal(s, "a_t", (B, wl.A, wl.act_dim), 1.0)
         self.t = synth.uniform(s, "t", (B,))
+        # DreamZero-Flash: the action tokens at their own timestep
+        self.t_action = synth.uniform(s, "t_action", (B,)) if flash else None
         self.text = synth.normal(s, "text", (B, wl.Lc, wl.text_dim), 1.0)
 
     def layer(self, l):
@@ -119,7 +121,8 @@ class StepCase:
 
         return oracle.dit_step(self.z.f64, self.a.f64, self.t.f64, self.text.f64, f64(self.P), layers,
                                self.n_layers, wl.H, wl.eps, wl.n_cached, oracle_positions(wl),
-                               prev_chunk=prev_chunk_ids(wl) if wl.n_cached else None)
+                               prev_chunk=prev_chunk_ids(wl) if wl.n_cached else None,
+                               t_action=self.t_action.f64 if self.t_action is not None else None)
 
     def upload(self):
         """Device model and inputs (kept on self so the step can be re-run)."""
@@ -136,8 +139,10 @@ class StepCase:
         self.model = w.make_model(dims_of(wl, self.n_layers), self.top, self.blocks)
         self.cos, self.sin = gpu_rope_tables(wl)
         self.dz, self.da, self.dt, self.dtext = dev(self.z), dev(self.a), dev(self.t), dev(self.text)
+        self.dta = dev(self.t_action) if self.t_action is not None else None
 
-    def run_gpu(self, events=None):
+    def run_gpu(self, events=None, t_action=None):
+        """t_action: a device [B] timestep overriding the case's own (None: the case's)."""
         import torch
         w = lib()
         wl, B = self.wl, self.wl.B
@@ -146,7 +151,8 @@ class StepCase:
         vv = torch.empty((B, wl.latent_ch, wl.F, wl.Hl, wl.Wl), dtype=torch.float32, device="cuda")
         va = torch.empty((B, wl.A, wl.act_dim), dtype=torch.float32, device="cuda")
         io = w.make_step_io(self.dz, self.da, self.dt, self.dtext, self.kcs, self.vcs, self.cos, self.sin,
-                            wl.cache_rows, w.cached_chunks(wl.cache_rows, wl.L), vv, va, events=events)
+                            wl.cache_rows, w.cached_chunks(wl.cache_rows, wl.L), vv, va, events=events,
+                            t_action=t_action if t_action is not None else self.dta)
         ws = workspace(w.wam_step_workspace_bytes(self.model, io))
         w.wam_dit_step_fwd(self.model, io, ws)
         torch.cuda.synchronize()
