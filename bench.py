@@ -12,8 +12,9 @@ Prints one JSON line: steps/s, plus the self-attention kernel's achieved bf16 TF
 against the MFMA peak (per-launch durations from HIP events recorded around every
 self-attention launch inside the timed steps) and its HBM bytes per launch (from the
 committed counter profile; null once the kernel source differs from the profiled one),
-and the fp64 oracle timed on the host cores on a bounded sample (one full-shape block),
-scaled to steps/s.
+the fp64 oracle timed on the host cores on a bounded sample (one full-shape block),
+scaled to steps/s, and (`extras`) the Flash step, the cache-update pass and a 4-step
+denoising loop on the same model.
 """
 import argparse
 import json
@@ -34,6 +35,8 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-extras", action="store_true",
+                   help="skip the Flash step / update pass / denoising loop timings")
     p.add_argument("--workload", default=WORKLOAD)
     p.add_argument("--probe-attn", type=int, default=0, metavar="N",
                    help="counter-collection mode: one plain 1 GiB device copy, then N self-attention "
@@ -107,6 +110,66 @@ def attn_traffic():
     if fields.get("kernel_source_sha256") != h.hexdigest():
         return None
     return int(fields["traffic_bytes_per_launch"])
+
+
+def extras(wl, model, kcs, vcs, inp, torch, reps=3):
+    """Timings of the other entry points on the same model and workload (milliseconds,
+    HIP events on the current stream, after one warm-up call each): the DreamZero-Flash
+    step (actions at their own timestep), the cache-update pass over one clean video-only
+    chunk (3120 rows after the cached ones), and a 4-step Euler denoising loop."""
+    import numpy as np
+    import paper_2602_15922_amd as w
+    B = wl.B
+    dev = "cuda"
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    out = {}
+    vv = torch.empty((B, wl.latent_ch, wl.F, wl.Hl, wl.Wl), dtype=torch.float32, device=dev)
+    va = torch.empty((B, wl.A, wl.act_dim), dtype=torch.float32, device=dev)
+    chunks = w.cached_chunks(wl.cache_rows, wl.L)
+    t_act = torch.full((B,), 0.9, device=dev)
+    io_f = w.make_step_io(inp["z"], inp["a"], inp["t"], inp["text"], kcs, vcs, inp["cos"], inp["sin"],
+                          wl.cache_rows, chunks, vv, va, t_action=t_act)
+    ws = torch.empty(w.wam_step_workspace_bytes(model, io_f), dtype=torch.uint8, device=dev)
+    out["flash_step_ms"] = round(timed(lambda: w.wam_dit_step_fwd(model, io_f, ws)), 3)
+
+    # update pass: the clean chunk's video rows only (Algorithm 2 passes no actions)
+    Lu = wl.Lv
+    a0 = torch.empty((B, 0, wl.act_dim), dtype=torch.bfloat16, device=dev)
+    pos = w.wam_chunk_positions(wl.n_cached, wl.F, wl.Hg, wl.Wg, 0)
+    cu, su = (torch.from_numpy(x).to(dev) for x in w.wam_rope_tables(pos, wl.Dh))
+    io_u = w.make_step_io(inp["z"], a0, inp["t"], inp["text"], kcs, vcs, cu, su, wl.cache_rows,
+                          w.cached_chunks(wl.cache_rows, Lu), None, None)
+    ws_u = torch.empty(w.wam_update_workspace_bytes(model, io_u), dtype=torch.uint8, device=dev)
+    out["update_pass_ms"] = round(timed(lambda: w.wam_dit_update_fwd(model, io_u, ws_u)), 3)
+
+    # 4-step Euler loop of one chunk, no guidance, no caching
+    n = wl.latent_ch * wl.F * wl.Hl * wl.Wl + wl.A * wl.act_dim
+    x = torch.randn(B, n, device=dev)
+    x0 = x.clone()
+    tl = torch.zeros(B, device=dev)
+    io_l = w.make_step_io(inp["z"], inp["a"], tl, inp["text"], kcs, vcs, inp["cos"], inp["sin"],
+                          wl.cache_rows, chunks, vv, va)
+    p = w.make_denoise_params(np.linspace(0.0, 1.0, 5), x)
+    ws_l = torch.empty(w.wam_denoise_workspace_bytes(model, io_l, p), dtype=torch.uint8, device=dev)
+
+    def loop():
+        x.copy_(x0)
+        w.wam_denoise_chunk(model, io_l, p, ws_l)
+
+    out["denoise_4step_ms"] = round(timed(loop), 3)
+    assert torch.isfinite(x).all()
+    return out
 
 
 def cpu_baseline(wl):
@@ -238,6 +301,8 @@ def main():
         "step_mfma_frac": round(step_flop / (ms * 1e-3) / 1e12 / MI355X_BF16_DENSE_TFLOPS, 4),
         "wall_s_timed": round(wall, 3),
     }
+    if not args.no_extras:
+        rec["extras"] = extras(wl, model, kcs, vcs, inp, torch)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(rec), flush=True)
