@@ -27,3 +27,4 @@ from .attention import attention  # noqa: F401
 from .model import (time_embedding, text_projection, patchify, unpatchify,  # noqa: F401
                     embed, dit_block, head, dit_step, dit_update)
 from .denoise import euler_step, cfg_combine, cosine_similarity, denoise  # noqa: F401
+from . import fp8  # noqa: F401

@@ -750,6 +750,48 @@ def test_dit_caching_skips_a_window_after_similar_velocities():
     assert all(computed)
 
 
+# ----------------------------------------------------------------------------- FP8 (E4M3)
+def test_e4m3_grid_matches_torch_float8():
+    """The E4M3 value set against torch's float8_e4m3fn decoding of every finite code."""
+    torch = pytest.importorskip("torch")
+    vals = oracle.fp8.e4m3_values()
+    assert len(vals) == 127 and vals[-1] == 448.0 and vals[1] == 2.0 ** -9 and np.all(np.diff(vals) > 0)
+    codes = torch.arange(0, 127, dtype=torch.uint8).view(torch.float8_e4m3fn)
+    assert np.array_equal(codes.to(torch.float64).numpy(), vals)
+
+
+def test_e4m3_rounding_matches_torch_and_ties_go_even():
+    torch = pytest.importorskip("torch")
+    g = np.random.default_rng(170)
+    x = np.concatenate([g.standard_normal(20000) * s for s in (0.003, 0.1, 1.0, 30.0, 150.0)])
+    x = np.clip(x, -448.0, 448.0).astype(np.float32).astype(np.float64)
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).to(torch.float64).numpy()
+    assert np.array_equal(oracle.fp8.round_e4m3(x), ref)
+    vals = oracle.fp8.e4m3_values()
+    mid = (vals[:-1] + vals[1:]) / 2
+    got = oracle.fp8.round_e4m3(mid)
+    even = np.where(np.arange(len(vals) - 1) % 2 == 0, vals[:-1], vals[1:])
+    assert np.array_equal(got, even)
+    assert np.array_equal(oracle.fp8.round_e4m3(np.array([500.0, -1e6, 448.0])), [448.0, -448.0, 448.0])
+
+
+def test_fp8_row_quantization_error_bound():
+    """Per-row scales map each row's largest magnitude to 448 exactly; every element in
+    the normal range is reproduced within half a unit of its 3-bit mantissa (2^-4)."""
+    g = np.random.default_rng(171)
+    x = g.standard_normal((16, 300))
+    x[3] = 0.0
+    q, s = oracle.fp8.quantize_rows(x)
+    assert s[3] == 1.0 and not q[3].any()
+    rows = [r for r in range(16) if r != 3]
+    assert np.allclose(np.max(np.abs(q[rows]), axis=1), 448.0)
+    deq = q * s[:, None]
+    normal = np.abs(x / s[:, None]) >= 2.0 ** -6
+    assert np.all(np.abs(deq - x)[normal] <= 2.0 ** -4 * np.abs(x)[normal] + 1e-300)
+    y = oracle.fp8.fp8_linear(q[:2], s[:2], q[2:5], s[2:5])
+    assert np.allclose(y, (q[:2] * s[:2, None]) @ (q[2:5] * s[2:5, None]).T, atol=1e-12)
+
+
 # ----------------------------------------------------------------------------- shared input generator
 def test_bf16_rounding_matches_torch():
     torch = pytest.importorskip("torch")
