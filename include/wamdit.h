@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define WAM_ABI_VERSION 2
+#define WAM_ABI_VERSION 3
 #define WAM_MAX_CHUNKS 16
 
 typedef enum {
@@ -130,12 +130,25 @@ typedef struct {
  * the block's modulation table added to the per-sample time modulation e0, rows
  * (shift1, scale1, gate1, shift2, scale2, gate2); lnc_gamma, lnc_beta [d] the affine
  * of the cross-attention LayerNorm (NULL = 1 and 0). */
+typedef struct wam_block_fp8 wam_block_fp8;
 typedef struct {
   const void *w_qkv, *w_o, *w_cq, *w_ckv, *w_co, *w_f1, *w_f2;
   const float *b_qkv, *b_o, *b_cq, *b_ckv, *b_co, *b_f1, *b_f2;
   const float* mod6;
   const float *lnc_gamma, *lnc_beta;
+  const wam_block_fp8* fp8;  /* optional FP8 copies of the seven projections (below) */
 } wam_block_weights;
+
+/* FP8 copies of a block's projections: E4M3 [out][in] contiguous (each bf16 matrix's rows
+ * quantized with wam_quantize_rows_fp8) with their per-output-channel scales.  When a
+ * block's weights carry them, its seven projections (QKV, O, cross-Q, cross-K|V, cross-O,
+ * FFN1, FFN2) run as FP8 GEMMs: every activation is quantized per row into the workspace
+ * right before its projection; LayerNorm, RoPE, both attentions, the epilogues and the
+ * fp32 residual are unchanged (the bf16 matrices are then not read). */
+struct wam_block_fp8 {
+  const void *w_qkv, *w_o, *w_cq, *w_ckv, *w_co, *w_f1, *w_f2;
+  const float *s_qkv, *s_o, *s_cq, *s_ckv, *s_co, *s_f1, *s_f2;
+};
 
 /* ------------------------------------------------------------------------------
  * wam_dit_block_fwd — one DiT block over the current rows (in place on x).
@@ -396,6 +409,27 @@ typedef struct {
 } wam_gemm_desc;
 
 wam_status wam_gemm_bf16(const wam_gemm_desc* g, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * FP8 (E4M3) operands.  The paper's deployment quantizes to FP8 E4M3 (Appendix D.2);
+ * here E4M3 is the OCP 8-bit float (bias 7, 3 mantissa bits, largest 448, no
+ * infinities).
+ *
+ * wam_quantize_rows_fp8: per-row quantization of bf16 x [M][K] (row stride ldx, K and
+ * ldx multiples of 8): scale[m] = max_k |x[m][k]| / 448 (1 for an all-zero row) and
+ * q[m][k] = E4M3(x[m][k] * (448 / max_k |x[m][k]|)) rounded to nearest, ties to even
+ * (fp32 arithmetic); q has row stride ldq bytes (a multiple of 16).  Used for
+ * activations (per token) and for weights (per output channel, rows of W [N][K]).
+ *
+ * wam_gemm_fp8: the GEMM of wam_gemm_bf16 with E4M3 operands: A [M][K] and W [N][K]
+ * bytes (lda, ldw, a_batch_stride and K multiples of 16), fp32 accumulation of the
+ * exact products, then v = acc * a_scale[m] * w_scale[n] + bias[n] and the same
+ * epilogues.  a_scale [M] and w_scale [N] fp32 device arrays are required.
+ * ------------------------------------------------------------------------------ */
+wam_status wam_quantize_rows_fp8(int32_t M, int32_t K, const void* x, int64_t ldx, void* q,
+                                 int64_t ldq, float* scale, hipStream_t stream);
+wam_status wam_gemm_fp8(const wam_gemm_desc* g, const float* a_scale, const float* w_scale,
+                        hipStream_t stream);
 
 /* Patch and action embedding into the fp32 residual x [B][Lv+A][d]. */
 size_t wam_embed_workspace_bytes(const wam_dims* dims, int32_t B, int32_t F, int32_t Hl, int32_t Wl);

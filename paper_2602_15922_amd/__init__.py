@@ -5,4 +5,4 @@ behind a C ABI declared in ``include/wamdit.h``); this package is its ctypes bin
 """
 from .binding import *  # noqa: F401,F403
 from .binding import (lib, WamError, make_chunks, cached_chunks, append_chunks, make_dims,  # noqa: F401
-                      make_model, make_denoise_params)
+                      make_model, make_denoise_params, make_block_fp8)

@@ -22,7 +22,8 @@ EXPORTED = (
     "wam_last_error", "wam_abi_version", "wam_attn_blockcausal", "wam_block_workspace_bytes",
     "wam_dit_block_fwd", "wam_step_workspace_bytes", "wam_dit_step_fwd",
     "wam_update_workspace_bytes", "wam_dit_update_fwd", "wam_flow_step", "wam_cosine_workspace_bytes",
-    "wam_cosine_similarity", "wam_denoise_workspace_bytes", "wam_denoise_chunk",
+    "wam_cosine_similarity", "wam_denoise_workspace_bytes", "wam_denoise_chunk", "wam_quantize_rows_fp8",
+    "wam_gemm_fp8",
     "wam_time_embed_workspace_bytes", "wam_time_embed_fwd", "wam_text_proj_workspace_bytes",
     "wam_text_proj_fwd", "wam_adaln_ln_mod", "wam_rope_qkv", "wam_gemm_bf16",
     "wam_embed_workspace_bytes", "wam_embed_fwd", "wam_head_workspace_bytes", "wam_head_fwd",
@@ -61,8 +62,13 @@ BLOCK_MATS = ("w_qkv", "w_o", "w_cq", "w_ckv", "w_co", "w_f1", "w_f2")
 BLOCK_VECS = ("b_qkv", "b_o", "b_cq", "b_ckv", "b_co", "b_f1", "b_f2", "mod6", "lnc_gamma", "lnc_beta")
 
 
+class wam_block_fp8(C.Structure):
+    _fields_ = [(n, _vp) for n in BLOCK_MATS] + [("s" + n[1:], _vp) for n in BLOCK_MATS]
+
+
 class wam_block_weights(C.Structure):
-    _fields_ = [(n, _vp) for n in BLOCK_MATS] + [(n, _vp) for n in BLOCK_VECS]
+    _fields_ = [(n, _vp) for n in BLOCK_MATS] + [(n, _vp) for n in BLOCK_VECS] + \
+               [("fp8", C.POINTER(wam_block_fp8))]
 
 
 class wam_block_io(C.Structure):
@@ -151,6 +157,8 @@ def lib():
                                        _i64, _vp, _vp]
         L.wam_rope_qkv.argtypes = [_i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp]
         L.wam_gemm_bf16.argtypes = [C.POINTER(wam_gemm_desc), _vp]
+        L.wam_gemm_fp8.argtypes = [C.POINTER(wam_gemm_desc), _vp, _vp, _vp]
+        L.wam_quantize_rows_fp8.argtypes = [_i32, _i32, _vp, _i64, _vp, _i64, _vp, _vp]
         L.wam_embed_fwd.argtypes = [C.POINTER(wam_model), _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp,
                                     _vp, _sz, _vp]
         L.wam_head_fwd.argtypes = [C.POINTER(wam_model), _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp,
@@ -253,6 +261,26 @@ def wam_gemm_bf16(A, W, out, epilogue: int, bias=None, gate_a=None, gate_v=None,
     _check(lib().wam_gemm_bf16(C.byref(g), _stream(stream)))
 
 
+def wam_quantize_rows_fp8(x, q, scale, stream=None):
+    """Per-row E4M3 quantization of bf16 x [M, K] into uint8 q [M, >=K] and fp32 scale [M]."""
+    M, K = x.shape
+    _check(lib().wam_quantize_rows_fp8(M, K, _p(x), x.stride(0), _p(q), q.stride(0), _p(scale), _stream(stream)))
+
+
+def wam_gemm_fp8(A, W, out, epilogue: int, a_scale, w_scale, bias=None, gate_a=None, gate_v=None, gate_stride=0,
+                 gate_rows=0, M=None, lda=None, a_rows=0, a_batch_stride=0, ldo=None, out_rows=0,
+                 out_batch_stride=0, stream=None):
+    """out = epilogue((A8 W8^T) * a_scale[m] * w_scale[n] + bias); A [M, K] and W [N, K] uint8 E4M3 codes."""
+    N, K = W.shape
+    g = wam_gemm_desc(M=A.shape[0] if M is None else M, N=N, K=K, epilogue=epilogue,
+                      A=_p(A), lda=A.stride(0) if lda is None else lda, a_batch_stride=a_batch_stride,
+                      a_rows=a_rows, W=_p(W), ldw=W.stride(0), bias=_p(bias), out=_p(out),
+                      ldo=out.stride(0) if ldo is None else ldo, out_batch_stride=out_batch_stride,
+                      out_rows=out_rows, gate_a=_p(gate_a), gate_v=_p(gate_v), gate_stride=gate_stride,
+                      gate_rows=gate_rows)
+    _check(lib().wam_gemm_fp8(C.byref(g), _p(a_scale), _p(w_scale), _stream(stream)))
+
+
 def wam_adaln_ln_mod(x, h, eps, rows_per_batch, gamma=None, beta=None, shift_a=None, shift_v=None,
                      scale_a=None, scale_v=None, mod_stride=0, stream=None):
     d = x.shape[-1]
@@ -275,19 +303,46 @@ def make_dims(d, H, Dh, ffn, n_layers, latent_ch=16, act_dim=16, text_dim=4096, 
 
 
 def make_block_weights(t: dict) -> wam_block_weights:
-    """t: name -> device tensor (missing vectors = NULL)."""
+    """t: name -> device tensor (missing vectors = NULL); t["fp8"], when present, the dict
+    make_block_fp8 returns (the block's projections then run as FP8 GEMMs)."""
     w = wam_block_weights()
     for n in BLOCK_MATS + BLOCK_VECS:
         setattr(w, n, _p(t.get(n)))
+    f8 = t.get("fp8")
+    if f8 is not None:
+        f = wam_block_fp8()
+        for n in BLOCK_MATS:
+            setattr(f, n, _p(f8.get(n)))
+            setattr(f, "s" + n[1:], _p(f8.get("s" + n[1:])))
+        w.fp8 = C.pointer(f)
+        w._fp8 = f
     return w
+
+
+def make_block_fp8(t: dict, stream=None) -> dict:
+    """E4M3 copies of a block's bf16 projection matrices (device tensors in t), one scale per
+    output channel, made on the device with wam_quantize_rows_fp8."""
+    import torch
+    out = {}
+    for n in BLOCK_MATS:
+        if t.get(n) is None:
+            continue
+        W = t[n]
+        N, K = W.shape
+        q = torch.empty((N, K), dtype=torch.uint8, device=W.device)
+        s = torch.empty(N, dtype=torch.float32, device=W.device)
+        wam_quantize_rows_fp8(W, q, s, stream=stream)
+        out[n], out["s" + n[1:]] = q, s
+    return out
 
 
 def make_model(dims: wam_dims, top: dict, blocks: list) -> wam_model:
     m = wam_model()
     m.dims = dims
-    arr = (wam_block_weights * max(1, len(blocks)))(*[make_block_weights(b) for b in blocks])
+    ws = [make_block_weights(b) for b in blocks]
+    arr = (wam_block_weights * max(1, len(blocks)))(*ws)
     m.blocks = C.cast(arr, C.POINTER(wam_block_weights))
-    m._keep = arr  # keep the host array alive with the struct
+    m._keep = (arr, ws)  # keep the host arrays (and any FP8 structs) alive with the model
     for n in MODEL_MATS + MODEL_VECS + ("head_mod2",):
         setattr(m, n, _p(top.get(n)))
     return m

@@ -145,19 +145,27 @@ wam_chunks single_chunk(int32_t Lq, int32_t Lk) {
 // ---------------------------------------------------------------------------------
 // GEMM
 // ---------------------------------------------------------------------------------
-wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s, int32_t gate_split = 0, int64_t gate_alt = 0) {
-  CHECK(g.M >= 0 && g.N >= 1 && g.K >= 8 && g.K % 8 == 0, WAM_EINVAL,
-        "GEMM sizes M=%d N=%d K=%d (need N>=1, K>=8, K%%8==0)", g.M, g.N, g.K);
+// fp8: A and W are E4M3 bytes with per-row a_scale [M] and per-column w_scale [N].
+wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s, int32_t gate_split = 0, int64_t gate_alt = 0,
+                        const float* a_scale = nullptr, const float* w_scale = nullptr) {
+  const bool fp8 = a_scale != nullptr;
+  const int eb = fp8 ? 1 : 2, epc = 16 / eb;  // bytes per element, elements per 16 bytes
+  CHECK(g.M >= 0 && g.N >= 1 && g.K >= epc && g.K % epc == 0, WAM_EINVAL,
+        "GEMM sizes M=%d N=%d K=%d (need N>=1, K>=%d, K%%%d==0)", g.M, g.N, g.K, epc, epc);
   CHECK(g.epilogue >= WAM_EPI_BF16 && g.epilogue <= WAM_EPI_F32, WAM_EINVAL, "unknown epilogue %d", g.epilogue);
   if (g.M == 0) return WAM_OK;
   TRY(need_ptr(g.A, "A"));
   TRY(need_ptr(g.W, "W"));
   TRY(need_ptr(g.out, "out"));
-  CHECK(g.lda >= g.K && g.lda % 8 == 0 && g.ldw >= g.K && g.ldw % 8 == 0, WAM_EINVAL,
-        "lda/ldw must be >= K and multiples of 8");
+  CHECK(g.lda >= g.K && g.lda % epc == 0 && g.ldw >= g.K && g.ldw % epc == 0, WAM_EINVAL,
+        "lda/ldw must be >= K and multiples of %d", epc);
   CHECK(g.ldo >= g.N, WAM_EINVAL, "ldo < N");
   CHECK(g.a_rows >= 0 && g.out_rows >= 0 && g.gate_rows >= 0, WAM_EINVAL, "negative row groups");
-  CHECK(g.a_batch_stride % 8 == 0, WAM_EINVAL, "a_batch_stride must be a multiple of 8");
+  CHECK(g.a_batch_stride % epc == 0, WAM_EINVAL, "a_batch_stride must be a multiple of %d", epc);
+  if (fp8) {
+    TRY(need_ptr(a_scale, "a_scale"));
+    TRY(need_ptr(w_scale, "w_scale"));
+  }
   CHECK(g.ldo % 4 == 0 && g.out_batch_stride % 4 == 0 && g.gate_stride % 4 == 0, WAM_EINVAL,
         "ldo, out_batch_stride and gate_stride must be multiples of 4");
   TRY(opt_ptr(g.bias, "bias"));
@@ -169,8 +177,9 @@ wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s, int32_t gate_spli
     const int64_t a_end = (g.a_rows > 0 ? (int64_t)(g.M - 1) / ar * g.a_batch_stride : 0) +
                           (std::min<int64_t>(ar, g.M) - 1) * g.lda + g.K;
     const int64_t w_end = (int64_t)(g.N - 1) * g.ldw + g.K;
-    CHECK(2 * a_end <= INT32_MAX && 2 * w_end <= INT32_MAX, WAM_EUNSUPPORTED,
-          "A or W spans 2 GiB or more (A %lld bytes, W %lld bytes)", (long long)(2 * a_end), (long long)(2 * w_end));
+    CHECK(eb * a_end <= INT32_MAX && eb * w_end <= INT32_MAX, WAM_EUNSUPPORTED,
+          "A or W spans 2 GiB or more (A %lld bytes, W %lld bytes)", (long long)(eb * a_end),
+          (long long)(eb * w_end));
   }
   GemmArgs a{};
   a.M = g.M; a.N = g.N; a.K = g.K; a.epi = g.epilogue;
@@ -179,6 +188,7 @@ wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s, int32_t gate_spli
   a.out = g.out; a.ldo = g.ldo; a.o_bs = g.out_batch_stride; a.o_rows = g.out_rows;
   a.gate_a = g.gate_a; a.gate_v = g.gate_v; a.gate_stride = g.gate_stride; a.gate_rows = g.gate_rows;
   a.gate_split = gate_split; a.gate_alt = gate_alt;
+  a.fp8 = fp8 ? 1 : 0; a.a_scale = a_scale; a.w_scale = w_scale;
   HIPCHECK(launch_gemm(a, s));
   return WAM_OK;
 }
@@ -195,11 +205,13 @@ wam_gemm_desc gemm(int M, int N, int K, int epi, const void* A, int64_t lda, con
 // block
 // ---------------------------------------------------------------------------------
 struct BlockWs {
-  size_t h, big, q, o, ckv, total;
+  size_t h, big, q, o, ckv, q8, qs, total;
 };
+// q8 / qs: an activation quantized to E4M3 for an FP8 projection and its row scales.
 BlockWs block_ws(const wam_dims& D, int32_t B, int32_t L, int32_t Lc) {
   const size_t M = (size_t)B * L, d = D.d;
   const size_t wide = (size_t)(3 * D.d > D.ffn ? 3 * D.d : D.ffn);
+  const size_t rows = std::max(M, (size_t)B * Lc), kmax = (size_t)std::max(D.d, (D.ffn + 15) / 16 * 16);
   BlockWs w{};
   size_t off = 0;
   w.h = off; off += align256(M * d * 2);
@@ -207,18 +219,43 @@ BlockWs block_ws(const wam_dims& D, int32_t B, int32_t L, int32_t Lc) {
   w.q = off; off += align256(M * d * 2);
   w.o = off; off += align256(M * d * 2);
   w.ckv = off; off += align256((size_t)B * Lc * 2 * d * 2);
+  w.q8 = off; off += align256(rows * kmax);
+  w.qs = off; off += align256(rows * 4);
   w.total = off;
   return w;
 }
 
+// One projection of a block: the bf16 GEMM, or, with FP8 weights w8 / s8, the
+// activation rows quantized to E4M3 into q8 / qs and the FP8 GEMM.
+wam_status proj(const wam_gemm_desc& g0, const void* w8, const float* s8, char* q8, float* qs, hipStream_t s,
+                int32_t gate_split = 0, int64_t gate_alt = 0) {
+  if (!w8) return gemm_checked(g0, s, gate_split, gate_alt);
+  const int64_t ldq = (g0.K + 15) / 16 * 16;
+  HIPCHECK(launch_quant_rows(g0.M, g0.K, g0.A, g0.lda, q8, ldq, qs, s));
+  wam_gemm_desc g = g0;
+  g.A = q8; g.lda = ldq; g.a_rows = 0; g.a_batch_stride = 0;
+  g.W = w8; g.ldw = g0.K;
+  return gemm_checked(g, s, gate_split, gate_alt, qs, s8);
+}
+
 wam_status check_block_weights(const wam_block_weights& w) {
-  TRY(need_ptr(w.w_qkv, "w_qkv")); TRY(need_ptr(w.w_o, "w_o")); TRY(need_ptr(w.w_cq, "w_cq"));
-  TRY(need_ptr(w.w_co, "w_co")); TRY(need_ptr(w.w_f1, "w_f1")); TRY(need_ptr(w.w_f2, "w_f2"));
+  if (!w.fp8) {  // with FP8 copies the bf16 matrices are not read
+    TRY(need_ptr(w.w_qkv, "w_qkv")); TRY(need_ptr(w.w_o, "w_o")); TRY(need_ptr(w.w_cq, "w_cq"));
+    TRY(need_ptr(w.w_co, "w_co")); TRY(need_ptr(w.w_f1, "w_f1")); TRY(need_ptr(w.w_f2, "w_f2"));
+  }
   TRY(need_ptr(w.mod6, "mod6"));
   TRY(opt_ptr(w.w_ckv, "w_ckv"));
   TRY(opt_ptr(w.b_qkv, "b_qkv")); TRY(opt_ptr(w.b_o, "b_o")); TRY(opt_ptr(w.b_cq, "b_cq"));
   TRY(opt_ptr(w.b_ckv, "b_ckv")); TRY(opt_ptr(w.b_co, "b_co")); TRY(opt_ptr(w.b_f1, "b_f1"));
   TRY(opt_ptr(w.b_f2, "b_f2")); TRY(opt_ptr(w.lnc_gamma, "lnc_gamma")); TRY(opt_ptr(w.lnc_beta, "lnc_beta"));
+  if (w.fp8) {
+    const wam_block_fp8& f = *w.fp8;
+    TRY(need_ptr(f.w_qkv, "fp8 w_qkv")); TRY(need_ptr(f.w_o, "fp8 w_o")); TRY(need_ptr(f.w_cq, "fp8 w_cq"));
+    TRY(need_ptr(f.w_co, "fp8 w_co")); TRY(need_ptr(f.w_f1, "fp8 w_f1")); TRY(need_ptr(f.w_f2, "fp8 w_f2"));
+    TRY(need_ptr(f.s_qkv, "fp8 s_qkv")); TRY(need_ptr(f.s_o, "fp8 s_o")); TRY(need_ptr(f.s_cq, "fp8 s_cq"));
+    TRY(need_ptr(f.s_co, "fp8 s_co")); TRY(need_ptr(f.s_f1, "fp8 s_f1")); TRY(need_ptr(f.s_f2, "fp8 s_f2"));
+    TRY(opt_ptr(f.w_ckv, "fp8 w_ckv")); TRY(opt_ptr(f.s_ckv, "fp8 s_ckv"));
+  }
   return WAM_OK;
 }
 
@@ -236,7 +273,8 @@ wam_status check_block_io(const wam_dims& D, const wam_block_weights& w, const w
     TRY(need_ptr(io.ctx_kv, "ctx_kv"));
   } else {
     TRY(need_ptr(io.ctx, "ctx"));
-    TRY(need_ptr(w.w_ckv, "w_ckv"));
+    if (w.fp8) { TRY(need_ptr(w.fp8->w_ckv, "fp8 w_ckv")); TRY(need_ptr(w.fp8->s_ckv, "fp8 s_ckv")); }
+    else TRY(need_ptr(w.w_ckv, "w_ckv"));
   }
   return WAM_OK;
 }
@@ -253,6 +291,9 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   void* q = ws + lay.q;
   void* o = ws + lay.o;
   void* ckv = ws + lay.ckv;
+  char* q8 = ws + lay.q8;
+  float* qs = reinterpret_cast<float*>(ws + lay.qs);
+  const wam_block_fp8* F8 = W.fp8;
   const float* m6 = W.mod6;
   const float* e0 = io.e0;
   const int64_t ms = 6 * (int64_t)d;
@@ -261,7 +302,8 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h, seg, alt};
   HIPCHECK(launch_ln_mod(ln, s));
   // 2. fused QKV projection
-  TRY(gemm_checked(gemm(M, 3 * d, d, WAM_EPI_BF16, h, d, W.w_qkv, W.b_qkv, big, 3 * d), s));
+  TRY(proj(gemm(M, 3 * d, d, WAM_EPI_BF16, h, d, W.w_qkv, W.b_qkv, big, 3 * d), F8 ? F8->w_qkv : nullptr,
+           F8 ? F8->s_qkv : nullptr, q8, qs, s));
   // 3. RoPE on q, k; k, v appended to the cache rows of this chunk
   RopeArgs ra{B, L, D.H, D.Dh, io.Lcap, io.cache_len, big, io.rope_cos, io.rope_sin, q, io.k_cache, io.v_cache};
   HIPCHECK(launch_rope_qkv(ra, s));
@@ -279,17 +321,19 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   {
     wam_gemm_desc g = gemm(M, d, d, WAM_EPI_RESID_F32, o, d, W.w_o, W.b_o, io.x, d);
     g.gate_a = m6 + 2 * d; g.gate_v = e0 + 2 * d; g.gate_stride = ms; g.gate_rows = L;
-    TRY(gemm_checked(g, s, seg, alt));
+    TRY(proj(g, F8 ? F8->w_o : nullptr, F8 ? F8->s_o : nullptr, q8, qs, s, seg, alt));
   }
   // 6. cross-attention LayerNorm (affine, no modulation)
   LnArgs lc{M, L, d, D.eps, io.x, W.lnc_gamma, W.lnc_beta, nullptr, nullptr, nullptr, nullptr, 0, h};
   HIPCHECK(launch_ln_mod(lc, s));
   // 7. cross query
-  TRY(gemm_checked(gemm(M, d, d, WAM_EPI_BF16, h, d, W.w_cq, W.b_cq, q, d), s));
+  TRY(proj(gemm(M, d, d, WAM_EPI_BF16, h, d, W.w_cq, W.b_cq, q, d), F8 ? F8->w_cq : nullptr,
+           F8 ? F8->s_cq : nullptr, q8, qs, s));
   // 8. cross K|V of the text (unless precomputed for this block)
   const void* kv = io.ctx_kv;
   if (!kv) {
-    TRY(gemm_checked(gemm(B * io.Lc, 2 * d, d, WAM_EPI_BF16, io.ctx, d, W.w_ckv, W.b_ckv, ckv, 2 * d), s));
+    TRY(proj(gemm(B * io.Lc, 2 * d, d, WAM_EPI_BF16, io.ctx, d, W.w_ckv, W.b_ckv, ckv, 2 * d),
+             F8 ? F8->w_ckv : nullptr, F8 ? F8->s_ckv : nullptr, q8, qs, s));
     kv = ckv;
   }
   // 9. cross-attention: every text token visible
@@ -301,17 +345,19 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   cd.ch = single_chunk(L, io.Lc);
   TRY(attn_checked(cd, q, kv, static_cast<const char*>(kv) + (size_t)d * 2, o, s));
   // 10. x += o W_co^T + b_co (no gate)
-  TRY(gemm_checked(gemm(M, d, d, WAM_EPI_RESID_F32, o, d, W.w_co, W.b_co, io.x, d), s));
+  TRY(proj(gemm(M, d, d, WAM_EPI_RESID_F32, o, d, W.w_co, W.b_co, io.x, d), F8 ? F8->w_co : nullptr,
+           F8 ? F8->s_co : nullptr, q8, qs, s));
   // 11. AdaLN #2
   LnArgs l2{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 3 * d, e0 + 3 * d, m6 + 4 * d, e0 + 4 * d, ms, h, seg, alt};
   HIPCHECK(launch_ln_mod(l2, s));
   // 12. FFN up-projection with tanh-GELU
-  TRY(gemm_checked(gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, big, D.ffn), s));
+  TRY(proj(gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, big, D.ffn), F8 ? F8->w_f1 : nullptr,
+           F8 ? F8->s_f1 : nullptr, q8, qs, s));
   // 13. x += gate2 * (u W_f2^T + b_f2)
   {
     wam_gemm_desc g = gemm(M, d, D.ffn, WAM_EPI_RESID_F32, big, D.ffn, W.w_f2, W.b_f2, io.x, d);
     g.gate_a = m6 + 5 * d; g.gate_v = e0 + 5 * d; g.gate_stride = ms; g.gate_rows = L;
-    TRY(gemm_checked(g, s, seg, alt));
+    TRY(proj(g, F8 ? F8->w_f2 : nullptr, F8 ? F8->s_f2 : nullptr, q8, qs, s, seg, alt));
   }
   return WAM_OK;
 }
@@ -330,9 +376,12 @@ wam_status block_kv_run(const wam_dims& D, const wam_block_weights& W, const wam
   LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h, seg, alt};
   HIPCHECK(launch_ln_mod(ln, s));
   // rows d..3d of W_qkv (the k and v outputs) into columns d..3d of the [M][3d] buffer
-  const char* wkv = static_cast<const char*>(W.w_qkv) + (size_t)d * d * 2;
+  const wam_block_fp8* F8 = W.fp8;
+  const char* wkv = F8 ? nullptr : static_cast<const char*>(W.w_qkv) + (size_t)d * d * 2;
   const float* bkv = W.b_qkv ? W.b_qkv + d : nullptr;
-  TRY(gemm_checked(gemm(M, 2 * d, d, WAM_EPI_BF16, h, d, wkv, bkv, big + (size_t)d * 2, 3 * d), s));
+  TRY(proj(gemm(M, 2 * d, d, WAM_EPI_BF16, h, d, wkv, bkv, big + (size_t)d * 2, 3 * d),
+           F8 ? static_cast<const char*>(F8->w_qkv) + (size_t)d * d : nullptr, F8 ? F8->s_qkv + d : nullptr,
+           ws + lay.q8, reinterpret_cast<float*>(ws + lay.qs), s));
   RopeArgs ra{B, L, D.H, D.Dh, io.Lcap, io.cache_len, big, io.rope_cos, io.rope_sin, nullptr, io.k_cache,
               io.v_cache};
   HIPCHECK(launch_rope_qkv(ra, s));
@@ -501,6 +550,8 @@ wam_status check_step(const wam_model& m, const wam_step_io& io, bool head) {
           "k_cache/v_cache[%d] NULL or misaligned", l);
     if (io.ctx_kv) {
       CHECK(io.ctx_kv[l] && al16(io.ctx_kv[l]), WAM_EINVAL, "ctx_kv[%d] NULL or misaligned", l);
+    } else if (m.blocks[l].fp8) {
+      TRY(need_ptr(m.blocks[l].fp8->w_ckv, "fp8 w_ckv")); TRY(need_ptr(m.blocks[l].fp8->s_ckv, "fp8 s_ckv"));
     } else {
       TRY(need_ptr(m.blocks[l].w_ckv, "w_ckv"));
     }
@@ -593,6 +644,23 @@ wam_status wam_attn_blockcausal(const wam_attn_desc* desc, const void* q, const 
 wam_status wam_gemm_bf16(const wam_gemm_desc* g, hipStream_t stream) {
   CHECK(g != nullptr, WAM_EINVAL, "desc is NULL");
   return gemm_checked(*g, stream);
+}
+
+wam_status wam_gemm_fp8(const wam_gemm_desc* g, const float* a_scale, const float* w_scale, hipStream_t stream) {
+  CHECK(g != nullptr, WAM_EINVAL, "NULL descriptor");
+  CHECK(a_scale != nullptr && w_scale != nullptr, WAM_EINVAL, "a_scale and w_scale are required");
+  return gemm_checked(*g, stream, 0, 0, a_scale, w_scale);
+}
+
+wam_status wam_quantize_rows_fp8(int32_t M, int32_t K, const void* x, int64_t ldx, void* q, int64_t ldq,
+                                 float* scale, hipStream_t stream) {
+  CHECK(M >= 0 && K >= 8 && K % 8 == 0, WAM_EINVAL, "M=%d K=%d (need K >= 8, K %% 8 == 0)", M, K);
+  CHECK(ldx >= K && ldx % 8 == 0 && ldq >= K && ldq % 16 == 0, WAM_EINVAL,
+        "ldx must be >= K and a multiple of 8; ldq >= K and a multiple of 16");
+  if (M == 0) return WAM_OK;
+  TRY(need_ptr(x, "x")); TRY(need_ptr(q, "q")); TRY(need_ptr(scale, "scale"));
+  HIPCHECK(launch_quant_rows(M, K, x, ldx, q, ldq, scale, stream));
+  return WAM_OK;
 }
 
 wam_status wam_adaln_ln_mod(int32_t B, int32_t rows_per_batch, int32_t d, float eps, const float* x,

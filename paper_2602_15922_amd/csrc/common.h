@@ -11,6 +11,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
 
 #define WAM_DEV __device__ __forceinline__
 
@@ -20,6 +21,14 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 //   C/D:       register r holds D[m = 8*(r/4) + 4h + r%4][n = l%32]
 WAM_DEV f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// 32x32x64 FP8 (E4M3 x E4M3) MFMA (gfx950), unit block scales.  Lane l, h = l/32:
+//   A operand: A[m = l%32][k = 32h .. 32h+31]   (32 consecutive k of one row, 32 bytes)
+//   B operand: B[k = 32h .. 32h+31][n = l%32]
+//   C/D:       as for mfma32
+WAM_DEV f32x16 mfma32_fp8(i32x8 a, i32x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
 }
 
 WAM_DEV float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }

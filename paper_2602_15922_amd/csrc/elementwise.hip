@@ -86,6 +86,44 @@ __global__ __launch_bounds__(LN_ROWS * 64) void ln_mod_kernel(const LnArgs a, in
 }
 
 // ---------------------------------------------------------------------------------
+// Per-row E4M3 quantization for the FP8 GEMMs: one wavefront per row of K bf16 values,
+// amax over the row, inv = 448 / amax (fp32), q = E4M3(x * inv) rounded to nearest even
+// (|x * inv| <= 448 by construction), scale = amax / 448 (1 for an all-zero row).
+// Each lane converts 8 consecutive values per step into one 8-byte store.
+// ---------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void quant_rows_kernel(int M, int K, const bf16* __restrict__ x, int64_t ldx,
+                                                         uint8_t* __restrict__ q, int64_t ldq,
+                                                         float* __restrict__ scale) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + w;
+  if (row >= M) return;
+  const bf16* xr = x + (int64_t)row * ldx;
+  float amax = 0.f;
+  for (int k = lane * 8; k < K; k += 512) {
+    const bf16x8 v = load_bf16x8(xr + k);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf((float)v[j]));
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+  const float inv = amax > 0.f ? 448.0f / amax : 1.0f;
+  if (lane == 0) scale[row] = amax > 0.f ? amax / 448.0f : 1.0f;
+  uint8_t* qr = q + (int64_t)row * ldq;
+  for (int k = lane * 8; k < K; k += 512) {
+    const bf16x8 v = load_bf16x8(xr + k);
+    float f[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) f[j] = fminf(fmaxf((float)v[j] * inv, -448.0f), 448.0f);
+    int lo = 0, hi = 0;
+    lo = __builtin_amdgcn_cvt_pk_fp8_f32(f[0], f[1], lo, false);
+    lo = __builtin_amdgcn_cvt_pk_fp8_f32(f[2], f[3], lo, true);
+    hi = __builtin_amdgcn_cvt_pk_fp8_f32(f[4], f[5], hi, false);
+    hi = __builtin_amdgcn_cvt_pk_fp8_f32(f[6], f[7], hi, true);
+    *reinterpret_cast<u32x2*>(qr + k) = u32x2{(uint32_t)lo, (uint32_t)hi};
+  }
+}
+
+// ---------------------------------------------------------------------------------
 // 3D RoPE + KV append.  A thread owns 8 consecutive dims (4 rotation pairs) of one
 // head of one token and moves the q, k and v slices of the fused QKV row: q rotated
 // to q_out, k rotated and v copied into the cache rows [row0, row0 + L).
@@ -216,6 +254,14 @@ hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s) {
   else if (nv <= 8) hipLaunchKernelGGL(ln_mod_kernel<8>, grid, block, lds, s, a, bpb, seg, sb0);
   else if (nv <= 20) hipLaunchKernelGGL(ln_mod_kernel<20>, grid, block, lds, s, a, bpb, seg, sb0);
   else hipLaunchKernelGGL(ln_mod_kernel<32>, grid, block, lds, s, a, bpb, seg, sb0);
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_rows(int32_t M, int32_t K, const void* x, int64_t ldx, void* q, int64_t ldq, float* scale,
+                             hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  hipLaunchKernelGGL(quant_rows_kernel, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, s, M, K,
+                     static_cast<const bf16*>(x), ldx, static_cast<uint8_t*>(q), ldq, scale);
   return hipGetLastError();
 }
 

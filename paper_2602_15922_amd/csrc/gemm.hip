@@ -24,18 +24,26 @@
 namespace wam {
 namespace {
 
-template <int BM_, int BN_, int BK_, int STAGES_, int WM_, int WN_, int OCC_>
+// EB: operand bytes per element, 2 (bf16: 32x32x16 MFMA) or 1 (FP8 E4M3: the 32x32x64
+// f8f6f4 MFMA, scales applied in the epilogue).
+template <int BM_, int BN_, int BK_, int STAGES_, int WM_, int WN_, int OCC_, int EB_ = 2>
 struct Cfg {
   static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_;
   static constexpr int WM = WM_, WN = WN_;        // wave grid
   static constexpr int OCC = OCC_;                // wavefronts per SIMD the kernel is built for
+  static constexpr int EB = EB_;
   static constexpr int NW = WM * WN, NT = NW * 64;
   static constexpr int TM = BM / WM / 32;         // 32x32 tiles per wave, rows
   static constexpr int TN = BN / WN / 32;         // 32x32 tiles per wave, cols
-  static constexpr int CPR = BK / 8;              // 16-byte chunks per LDS row
+  static constexpr int ROWB = BK * EB;            // bytes per LDS row
+  static constexpr int CPR = ROWB / 16;           // 16-byte chunks per LDS row
+  static constexpr int EPC = 16 / EB;             // elements per chunk
+  static constexpr int KCH = EB == 2 ? 2 : 4;     // chunks per MFMA k-step (16 bf16 / 64 fp8)
+  static constexpr int FCH = KCH / 2;             // chunks of one lane's fragment
+  static constexpr int KS = CPR / KCH;            // MFMA k-steps per slice
   static constexpr int NIA = BM * CPR / (NW * 64);  // direct-load instructions per wave (A)
   static constexpr int NIB = BN * CPR / (NW * 64);  // (W)
-  static constexpr int STAGE = (BM + BN) * BK;    // elements per stage
+  static constexpr int STAGE = (BM + BN) * ROWB;  // bytes per stage
   static_assert(NIA * NW * 64 == BM * CPR && NIB * NW * 64 == BN * CPR, "slice not a whole number of wave loads");
   // XOR pattern.  gfx950 LDS serves 256 bytes (64 banks) per cycle, i.e. 16 lanes of a
   // 16-byte read; the 16 consecutive rows those lanes read at one logical chunk must land
@@ -43,7 +51,7 @@ struct Cfg {
   // 256-byte bank line, so XOR the chunk by (row>>1)&7; 64-byte rows (4 chunks): XOR
   // by (row>>2)&3.
   static WAM_DEV int pch(int row, int ch) { return CPR == 8 ? (ch ^ ((row >> 1) & 7)) : (ch ^ ((row >> 2) & 3)); }
-  static WAM_DEV int swz(int row, int ch) { return row * BK + (pch(row, ch) << 3); }
+  static WAM_DEV int swz(int row, int ch) { return row * ROWB + (pch(row, ch) << 4); }  // bytes
 };
 
 // Exact row -> (group, row-in-group) split for a runtime divisor: a float reciprocal
@@ -71,7 +79,9 @@ template <int EPI>
 WAM_DEV void epilogue4(const GemmArgs& g, const float inv_o, const float inv_g, int row, int col, f32x4 v) {
   if (row >= g.M || col >= g.N) return;
   const int64_t orow = group_off(row, g.o_rows, inv_o, g.o_bs, g.ldo);
+  if (g.a_scale) v *= g.a_scale[row];  // FP8 operands: per-row and per-column scales
   if (col + 4 <= g.N) {
+    if (g.w_scale) v *= *reinterpret_cast<const f32x4*>(g.w_scale + col);
     if (g.bias) v += *reinterpret_cast<const f32x4*>(g.bias + col);
     if constexpr (EPI == WAM_EPI_BF16 || EPI == WAM_EPI_GELU_BF16) {
       bf16x4 o;
@@ -94,7 +104,7 @@ WAM_DEV void epilogue4(const GemmArgs& g, const float inv_o, const float inv_g, 
   }
   // ragged last columns
   for (int j = 0; j < 4 && col + j < g.N; ++j) {
-    float x = v[j] + (g.bias ? g.bias[col + j] : 0.f);
+    float x = v[j] * (g.w_scale ? g.w_scale[col + j] : 1.f) + (g.bias ? g.bias[col + j] : 0.f);
     if constexpr (EPI == WAM_EPI_BF16) {
       static_cast<bf16*>(g.out)[orow + col + j] = (bf16)x;
     } else if constexpr (EPI == WAM_EPI_GELU_BF16) {
@@ -123,7 +133,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 // 16 bytes per lane from a buffer straight into LDS (lane l lands at lds + 16*l).  A
 // plain function: the builtin's operands must not depend on a template parameter.
-WAM_DEV void load_lds16(__amdgpu_buffer_rsrc_t r, bf16* lds, int voff, int soff) {
+WAM_DEV void load_lds16(__amdgpu_buffer_rsrc_t r, char* lds, int voff, int soff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds, 16, voff, soff, 0, 0);
 }
 
@@ -133,8 +143,8 @@ template <typename C>
 struct GemmLane {
   const void *A, *W;
   int a_off[C::NIA], b_off[C::NIB];  // byte offset of the lane's unit (row + logical chunk)
-  int kla[C::NIA], klb[C::NIB];      // logical column of the lane's unit inside a slice
-  int fa_off[C::BK / 16], fb_off[C::BK / 16];  // LDS byte offset of the lane's fragment per k-step
+  int kla[C::NIA], klb[C::NIB];      // logical column (elements) of the lane's unit in a slice
+  int fa_off[C::KS][C::FCH], fb_off[C::KS][C::FCH];  // LDS byte offsets of the lane's fragment
   int w;
 };
 
@@ -144,72 +154,103 @@ struct GemmLane {
 // a unit whose chunk lies past K re-reads the row's last in-range chunk instead (it is
 // zeroed in LDS once landed).
 template <typename C>
-WAM_DEV void fetch_slice(bf16* smem, int buf, const GemmLane<C>& L, int kt, int K) {
+WAM_DEV void fetch_slice(char* smem, int buf, const GemmLane<C>& L, int kt, int K) {
   // buffer resources over all of A and W (offsets < 2^31 bytes, checked by the host)
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(L.A), (short)0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(L.W), (short)0, 0x7fffffff, 0x00020000);
-  bf16* As = smem + buf * C::STAGE;
-  bf16* Bs = As + C::BM * C::BK;
-  const int k0 = kt * C::BK, soff = 2 * k0;
+  char* As = smem + buf * C::STAGE;
+  char* Bs = As + C::BM * C::ROWB;
+  const int k0 = kt * C::BK, soff = C::EB * k0;
   if (k0 + C::BK <= K) {
 #pragma unroll
     for (int c = 0; c < C::NIA; ++c)
-      load_lds16(ra, As + (L.w * C::NIA + c) * 512, L.a_off[c], soff);
+      load_lds16(ra, As + (L.w * C::NIA + c) * 1024, L.a_off[c], soff);
 #pragma unroll
     for (int c = 0; c < C::NIB; ++c)
-      load_lds16(rb, Bs + (L.w * C::NIB + c) * 512, L.b_off[c], soff);
+      load_lds16(rb, Bs + (L.w * C::NIB + c) * 1024, L.b_off[c], soff);
   } else {
 #pragma unroll
     for (int c = 0; c < C::NIA; ++c) {
-      const int sh = k0 + L.kla[c] < K ? 0 : 2 * (K - 8 - L.kla[c] - k0);
-      load_lds16(ra, As + (L.w * C::NIA + c) * 512, L.a_off[c] + sh, soff);
+      const int sh = k0 + L.kla[c] < K ? 0 : C::EB * (K - C::EPC - L.kla[c] - k0);
+      load_lds16(ra, As + (L.w * C::NIA + c) * 1024, L.a_off[c] + sh, soff);
     }
 #pragma unroll
     for (int c = 0; c < C::NIB; ++c) {
-      const int sh = k0 + L.klb[c] < K ? 0 : 2 * (K - 8 - L.klb[c] - k0);
-      load_lds16(rb, Bs + (L.w * C::NIB + c) * 512, L.b_off[c] + sh, soff);
+      const int sh = k0 + L.klb[c] < K ? 0 : C::EB * (K - C::EPC - L.klb[c] - k0);
+      load_lds16(rb, Bs + (L.w * C::NIB + c) * 1024, L.b_off[c] + sh, soff);
     }
   }
 }
 
 // Zero the units of a landed slice whose chunks lie past K (only in the last slice).
 template <typename C>
-WAM_DEV void zero_tail(bf16* smem, int buf, const GemmLane<C>& L, int kt, int K, int lane) {
-  bf16* As = smem + buf * C::STAGE;
-  bf16* Bs = As + C::BM * C::BK;
+WAM_DEV void zero_tail(char* smem, int buf, const GemmLane<C>& L, int kt, int K, int lane) {
+  char* As = smem + buf * C::STAGE;
+  char* Bs = As + C::BM * C::ROWB;
 #pragma unroll
   for (int c = 0; c < C::NIA; ++c)
-    if (kt * C::BK + L.kla[c] >= K) *reinterpret_cast<bf16x8*>(As + ((L.w * C::NIA + c) * 64 + lane) * 8) = bf16x8{};
+    if (kt * C::BK + L.kla[c] >= K) *reinterpret_cast<u32x4*>(As + ((L.w * C::NIA + c) * 64 + lane) * 16) = u32x4{};
 #pragma unroll
   for (int c = 0; c < C::NIB; ++c)
-    if (kt * C::BK + L.klb[c] >= K) *reinterpret_cast<bf16x8*>(Bs + ((L.w * C::NIB + c) * 64 + lane) * 8) = bf16x8{};
+    if (kt * C::BK + L.klb[c] >= K) *reinterpret_cast<u32x4*>(Bs + ((L.w * C::NIB + c) * 64 + lane) * 16) = u32x4{};
 }
 
 // The MFMAs of one landed slice in ring stage `cur`.  Fragments are double-buffered in
 // registers: the reads of k-step ks+1 are in flight while the MFMAs of k-step ks run.
 // With `cur` a compile-time constant every LDS read is a lane offset plus an immediate.
 template <typename C>
-WAM_DEV void mma_slice(const bf16* smem, int cur, const GemmLane<C>& L, f32x16 (*acc)[C::TN]) {
-  const char* As = reinterpret_cast<const char*>(smem + cur * C::STAGE);
-  const char* Bs = As + C::BM * C::BK * 2;
-  constexpr int RB = 32 * C::BK * 2;  // bytes of 32 LDS rows
-  bf16x8 fa[2][C::TM], fb[2][C::TN];
-  auto read_frags = [&](int ks, int slot) {
+WAM_DEV void mma_slice(const char* smem, int cur, const GemmLane<C>& L, f32x16 (*acc)[C::TN]) {
+  const char* As = smem + cur * C::STAGE;
+  const char* Bs = As + C::BM * C::ROWB;
+  constexpr int RB = 32 * C::ROWB;  // bytes of 32 LDS rows
+  if constexpr (C::EB == 2) {
+    bf16x8 fa[2][C::TM], fb[2][C::TN];
+    auto read_frags = [&](int ks, int slot) {
 #pragma unroll
-    for (int a = 0; a < C::TM; ++a) fa[slot][a] = *reinterpret_cast<const bf16x8*>(As + L.fa_off[ks] + a * RB);
+      for (int a = 0; a < C::TM; ++a) fa[slot][a] = *reinterpret_cast<const bf16x8*>(As + L.fa_off[ks][0] + a * RB);
 #pragma unroll
-    for (int b = 0; b < C::TN; ++b) fb[slot][b] = *reinterpret_cast<const bf16x8*>(Bs + L.fb_off[ks] + b * RB);
-  };
-  read_frags(0, 0);
+      for (int b = 0; b < C::TN; ++b) fb[slot][b] = *reinterpret_cast<const bf16x8*>(Bs + L.fb_off[ks][0] + b * RB);
+    };
+    read_frags(0, 0);
 #pragma unroll
-  for (int ks = 0; ks < C::BK / 16; ++ks) {
-    if (ks + 1 < C::BK / 16) read_frags(ks + 1, (ks + 1) & 1);
+    for (int ks = 0; ks < C::KS; ++ks) {
+      if (ks + 1 < C::KS) read_frags(ks + 1, (ks + 1) & 1);
 #pragma unroll
-    for (int a = 0; a < C::TM; ++a)
+      for (int a = 0; a < C::TM; ++a)
 #pragma unroll
-      for (int b = 0; b < C::TN; ++b) acc[a][b] = mfma32(fa[ks & 1][a], fb[ks & 1][b], acc[a][b]);
-    // fence the k-step: the next step's LDS reads stay in this step's region
-    __builtin_amdgcn_sched_barrier(0);
+        for (int b = 0; b < C::TN; ++b) acc[a][b] = mfma32(fa[ks & 1][a], fb[ks & 1][b], acc[a][b]);
+      // fence the k-step: the next step's LDS reads stay in this step's region
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
+    // FP8: a lane's fragment is 32 consecutive k (two 16-byte chunks) of its row
+    i32x8 fa[2][C::TM], fb[2][C::TN];
+    auto frag = [&](const char* base) {
+      const u32x4 lo = *reinterpret_cast<const u32x4*>(base);
+      return lo;
+    };
+    auto read_frags = [&](int ks, int slot) {
+#pragma unroll
+      for (int a = 0; a < C::TM; ++a) {
+        const u32x4 lo = frag(As + L.fa_off[ks][0] + a * RB), hi = frag(As + L.fa_off[ks][1] + a * RB);
+        fa[slot][a] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+      }
+#pragma unroll
+      for (int b = 0; b < C::TN; ++b) {
+        const u32x4 lo = frag(Bs + L.fb_off[ks][0] + b * RB), hi = frag(Bs + L.fb_off[ks][1] + b * RB);
+        fb[slot][b] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+      }
+    };
+    read_frags(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      if (ks + 1 < C::KS) read_frags(ks + 1, (ks + 1) & 1);
+#pragma unroll
+      for (int a = 0; a < C::TM; ++a)
+#pragma unroll
+        for (int b = 0; b < C::TN; ++b) acc[a][b] = mfma32_fp8(fa[ks & 1][a], fb[ks & 1][b], acc[a][b]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
 }
 
@@ -217,7 +258,7 @@ WAM_DEV void mma_slice(const bf16* smem, int cur, const GemmLane<C>& L, f32x16 (
 // flight when S = 3, S-2 in general): wait for slice kt, barrier, prefetch slice
 // kt+S-1 into the stage freed by slice kt-1, then the slice's MFMAs.
 template <typename C, int CUR>
-WAM_DEV void steady_step(bf16* smem, const GemmLane<C>& L, int kt, int K, f32x16 (*acc)[C::TN]) {
+WAM_DEV void steady_step(char* smem, const GemmLane<C>& L, int kt, int K, f32x16 (*acc)[C::TN]) {
   constexpr int S = C::STAGES, NI = C::NIA + C::NIB;
   WAM_WAIT_VMCNT((S - 2) * NI);
   asm volatile("" ::: "memory");
@@ -228,7 +269,7 @@ WAM_DEV void steady_step(bf16* smem, const GemmLane<C>& L, int kt, int K, f32x16
 }
 
 template <typename C, int CUR>
-WAM_DEV void steady_group(bf16* smem, const GemmLane<C>& L, int kt, int K, f32x16 (*acc)[C::TN]) {
+WAM_DEV void steady_group(char* smem, const GemmLane<C>& L, int kt, int K, f32x16 (*acc)[C::TN]) {
   steady_step<C, CUR>(smem, L, kt + CUR, K, acc);
   if constexpr (CUR + 1 < C::STAGES) steady_group<C, CUR + 1>(smem, L, kt, K, acc);
 }
@@ -236,7 +277,7 @@ WAM_DEV void steady_group(bf16* smem, const GemmLane<C>& L, int kt, int K, f32x1
 template <typename C, int EPI>
 __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int tiles_m, int tiles_n) {
   constexpr int BM = C::BM, BN = C::BN, BK = C::BK, S = C::STAGES;
-  __shared__ __attribute__((aligned(16))) bf16 smem[S * C::STAGE];
+  __shared__ __attribute__((aligned(16))) char smem[S * C::STAGE];
 
   // XCD-aware remap: the hardware deals workgroups round-robin over 8 XCDs; give each
   // XCD a contiguous range of tiles so tiles that share a W panel share an L2.
@@ -265,25 +306,27 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int t
     const int row = (w * C::NIA + c) * RPI + lrow;
     int r = m0 + row;
     r = r < g.M ? r : g.M - 1;
-    L.kla[c] = C::pch(row, lane % C::CPR) * 8;
-    L.a_off[c] = (int)(2 * ((int64_t)(r / g.a_rows) * g.a_bs + (int64_t)(r % g.a_rows) * g.lda + L.kla[c]));
+    L.kla[c] = C::pch(row, lane % C::CPR) * C::EPC;
+    L.a_off[c] = (int)(C::EB * ((int64_t)(r / g.a_rows) * g.a_bs + (int64_t)(r % g.a_rows) * g.lda + L.kla[c]));
   }
 #pragma unroll
   for (int c = 0; c < C::NIB; ++c) {
     const int row = (w * C::NIB + c) * RPI + lrow;
     int r = n0 + row;
     r = r < g.N ? r : g.N - 1;
-    L.klb[c] = C::pch(row, lane % C::CPR) * 8;
-    L.b_off[c] = (int)(2 * ((int64_t)r * g.ldw + L.klb[c]));
+    L.klb[c] = C::pch(row, lane % C::CPR) * C::EPC;
+    L.b_off[c] = (int)(C::EB * ((int64_t)r * g.ldw + L.klb[c]));
   }
   // Fragment reads: rows (wm*BM/WM + a*32 + l32) of A and (wn*BN/WN + b*32 + l32) of W
-  // at logical chunk 2*ks + hh; the XOR only depends on l32 (32-row steps keep it).
+  // at logical chunks KCH*ks + FCH*hh + f; the XOR only depends on l32 (32-row steps keep it).
 #pragma unroll
-  for (int ks = 0; ks < BK / 16; ++ks) {
-    const int ra = wm * (BM / C::WM) + l32, rb = wn * (BN / C::WN) + l32;
-    L.fa_off[ks] = 2 * C::swz(ra, 2 * ks + hh);
-    L.fb_off[ks] = 2 * C::swz(rb, 2 * ks + hh);
-  }
+  for (int ks = 0; ks < C::KS; ++ks)
+#pragma unroll
+    for (int f = 0; f < C::FCH; ++f) {
+      const int ra = wm * (BM / C::WM) + l32, rb = wn * (BN / C::WN) + l32;
+      L.fa_off[ks][f] = C::swz(ra, C::KCH * ks + C::FCH * hh + f);
+      L.fb_off[ks][f] = C::swz(rb, C::KCH * ks + C::FCH * hh + f);
+    }
 
   f32x16 acc[C::TM][C::TN];
 #pragma unroll
@@ -327,7 +370,7 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int t
   // the stores are 8/16-byte vectors over contiguous row segments.
   // rows padded by 8 floats: the two half-waves (rows 4 apart) use disjoint banks
   constexpr int WCOLS = BN / C::WN, SROW = WCOLS + 8;
-  static_assert(C::WM * C::WN * 32 * SROW * 4 <= S * C::STAGE * 2, "staging does not fit");
+  static_assert(C::WM * C::WN * 32 * SROW * 4 <= S * C::STAGE, "staging does not fit");
   float* stage = reinterpret_cast<float*>(smem) + w * 32 * SROW;
   const float inv_o = 1.0f / (float)g.o_rows, inv_g = 1.0f / (float)g.gate_rows;
   const int row_base = m0 + wm * (BM / C::WM), col_base = n0 + wn * WCOLS;
@@ -374,6 +417,10 @@ hipError_t launch_gemm(const GemmArgs& gin, hipStream_t s) {
   // every shape that fills the chip; below one round of them (e.g. the 512-row text
   // projections) 128x128 tiles, two workgroups per CU, spread the work wider.
   const long tiles = (long)((g.M + 127) / 128) * ((g.N + 255) / 256);
+  if (g.fp8) {  // the same tiles; a 128-wide FP8 slice fills the bytes of a 64-wide bf16 one
+    if (tiles >= 256) return launch_cfg<Cfg<128, 256, 128, 3, 2, 4, 2, 1>>(g, s);
+    return launch_cfg<Cfg<128, 128, 128, 2, 2, 2, 2, 1>>(g, s);
+  }
   if (tiles >= 256) return launch_cfg<Cfg<128, 256, 64, 3, 2, 4, 2>>(g, s);
   return launch_cfg<Cfg<128, 128, 64, 2, 2, 2, 2>>(g, s);
 }

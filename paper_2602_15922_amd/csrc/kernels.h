@@ -41,6 +41,9 @@ struct GemmArgs {
   // rows r >= gate_split of a gate group (0: none) read gate_v + gate_alt instead
   int32_t gate_split;
   int64_t gate_alt;
+  // FP8 operands (E4M3 A and W, one byte per element): acc * a_scale[m] * w_scale[n]
+  int32_t fp8;
+  const float *a_scale, *w_scale;
 };
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 
@@ -78,6 +81,10 @@ hipError_t launch_patchify(int32_t B, int32_t C, int32_t F, int32_t Hl, int32_t 
 // tokens [B][Lv][C*4] fp32 -> video [B][C][F][Hl][Wl] fp32
 hipError_t launch_unpatchify(int32_t B, int32_t C, int32_t F, int32_t Hl, int32_t Wl,
                              const float* tok, float* out, hipStream_t s);
+
+// Per-row E4M3 quantization of bf16 rows [M][K] (K % 8 == 0): q [M][ldq] bytes, scale [M].
+hipError_t launch_quant_rows(int32_t M, int32_t K, const void* x, int64_t ldx, void* q, int64_t ldq, float* scale,
+                             hipStream_t s);
 
 // Solver step of the denoising loop over one chunk.  State x [nx][n_video + n_action]
 // fp32 (nx = 1 with guidance, else B); velocity from the step outputs v_video [B][n_video]

@@ -74,11 +74,13 @@ class BlockCase:
                                 np.full(wl.L, wl.n_cached), kp, vp, prev_chunk_ids(wl) if kp is not None else None,
                                 ctx=ctx)
 
-    def run_gpu(self, e0_dev=None, ctx_dev=None):
+    def run_gpu(self, e0_dev=None, ctx_dev=None, fp8=False):
         import torch
         w = lib()
         wl, B = self.wl, self.wl.B
         Wd = {k: dev(v) for k, v in self.W.items()}
+        if fp8:
+            Wd["fp8"] = w.make_block_fp8(Wd)
         x = dev(self.x)
         kcache, vcache = upload_cache(wl, self.kc, self.vc, B)
         cos, sin = gpu_rope_tables(wl)
@@ -124,15 +126,19 @@ class StepCase:
                                prev_chunk=prev_chunk_ids(wl) if wl.n_cached else None,
                                t_action=self.t_action.f64 if self.t_action is not None else None)
 
-    def upload(self):
-        """Device model and inputs (kept on self so the step can be re-run)."""
+    def upload(self, fp8=False):
+        """Device model and inputs (kept on self so the step can be re-run); fp8: the
+        blocks carry E4M3 copies of their projections."""
         w = lib()
         wl, B = self.wl, self.wl.B
         self.top = {k: dev(v) for k, v in self.P.items()}
         self.blocks, self.kcs, self.vcs = [], [], []
         for l in range(self.n_layers):
             W, kc, vc = self.layer(l)
-            self.blocks.append({k: dev(v) for k, v in W.items()})
+            Wd = {k: dev(v) for k, v in W.items()}
+            if fp8:
+                Wd["fp8"] = w.make_block_fp8(Wd)
+            self.blocks.append(Wd)
             k, v = upload_cache(wl, kc, vc, B)
             self.kcs.append(k)
             self.vcs.append(v)

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_function():
     for name in declared:
         assert hasattr(L, name), name
     assert sorted(w.binding.EXPORTED) == declared
-    assert w.wam_abi_version() == 2
+    assert w.wam_abi_version() == 3
 
 
 def test_struct_sizes_match_the_header_layout():
@@ -40,7 +40,8 @@ def test_struct_sizes_match_the_header_layout():
     b = w.binding
     assert C.sizeof(b.wam_chunks) == 4 * (1 + 17 + 1 + 17 + 16)
     assert C.sizeof(b.wam_dims) == 10 * 4
-    assert C.sizeof(b.wam_block_weights) == 17 * 8
+    assert C.sizeof(b.wam_block_weights) == 18 * 8
+    assert C.sizeof(b.wam_block_fp8) == 14 * 8
     # sizes printed by a C++ compile of include/wamdit.h
     assert C.sizeof(b.wam_flow_dims) == 32
     assert C.sizeof(b.wam_denoise_params) == 48
