@@ -13,8 +13,8 @@ against the MFMA peak (per-launch durations from HIP events recorded around ever
 self-attention launch inside the timed steps) and its HBM bytes per launch (from the
 committed counter profile; null once the kernel source differs from the profiled one),
 the fp64 oracle timed on the host cores on a bounded sample (one full-shape block),
-scaled to steps/s, and (`extras`) the Flash step, the cache-update pass and a 4-step
-denoising loop on the same model.
+scaled to steps/s, and (`extras`) the Flash step, the cache-update pass, a 4-step
+denoising loop and the step with FP8 projections on the same model.
 """
 import argparse
 import json
@@ -112,11 +112,12 @@ def attn_traffic():
     return int(fields["traffic_bytes_per_launch"])
 
 
-def extras(wl, model, kcs, vcs, inp, torch, reps=3):
+def extras(wl, model, keep, kcs, vcs, inp, torch, reps=3):
     """Timings of the other entry points on the same model and workload (milliseconds,
     HIP events on the current stream, after one warm-up call each): the DreamZero-Flash
     step (actions at their own timestep), the cache-update pass over one clean video-only
-    chunk (3120 rows after the cached ones), and a 4-step Euler denoising loop."""
+    chunk (3120 rows after the cached ones), a 4-step Euler denoising loop, and the step
+    with every block's seven projections as FP8 (E4M3) GEMMs."""
     import numpy as np
     import paper_2602_15922_amd as w
     B = wl.B
@@ -169,6 +170,17 @@ def extras(wl, model, kcs, vcs, inp, torch, reps=3):
 
     out["denoise_4step_ms"] = round(timed(loop), 3)
     assert torch.isfinite(x).all()
+
+    # FP8 projections: E4M3 copies of every block's matrices, made on the device
+    top, blocks = keep
+    blocks8 = [dict(b, fp8=w.make_block_fp8(b)) for b in blocks]
+    model8 = w.make_model(model.dims, top, blocks8)
+    io8 = w.make_step_io(inp["z"], inp["a"], inp["t"], inp["text"], kcs, vcs, inp["cos"], inp["sin"],
+                         wl.cache_rows, chunks, vv, va)
+    ws8 = torch.empty(w.wam_step_workspace_bytes(model8, io8), dtype=torch.uint8, device=dev)
+    out["fp8_step_ms"] = round(timed(lambda: w.wam_dit_step_fwd(model8, io8, ws8)), 3)
+    assert torch.isfinite(vv).all()
+    del blocks8, model8, ws8
     return out
 
 
@@ -302,7 +314,7 @@ def main():
         "wall_s_timed": round(wall, 3),
     }
     if not args.no_extras:
-        rec["extras"] = extras(wl, model, kcs, vcs, inp, torch)
+        rec["extras"] = extras(wl, model, keep, kcs, vcs, inp, torch)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(rec), flush=True)
