@@ -60,7 +60,8 @@ class Workload:
 
     @property
     def Lcap(self):
-        return self.Lk
+        """KV cache capacity in tokens: Lk rounded up to a multiple of 8."""
+        return (self.Lk + 7) // 8 * 8
 
     @property
     def patch_dim(self):
