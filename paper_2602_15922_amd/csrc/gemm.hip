@@ -74,35 +74,12 @@ WAM_DEV int64_t gate_off(const GemmArgs& g, int row, float inv) {
   return (int64_t)q * g.gate_stride + (g.gate_split > 0 && r >= g.gate_split ? g.gate_alt : 0);
 }
 
-// Epilogue of four consecutive columns [col, col+4) of one output row.
+// Epilogue of the last, partial group of columns [col, N) of one output row (col < N <
+// col + 4): element by element.
 template <int EPI>
-WAM_DEV void epilogue4(const GemmArgs& g, const float inv_o, const float inv_g, int row, int col, f32x4 v) {
-  if (row >= g.M || col >= g.N) return;
+WAM_DEV void epilogue_ragged(const GemmArgs& g, const float inv_o, const float inv_g, int row, int col, f32x4 v) {
   const int64_t orow = group_off(row, g.o_rows, inv_o, g.o_bs, g.ldo);
   if (g.a_scale) v *= g.a_scale[row];  // FP8 operands: per-row and per-column scales
-  if (col + 4 <= g.N) {
-    if (g.w_scale) v *= *reinterpret_cast<const f32x4*>(g.w_scale + col);
-    if (g.bias) v += *reinterpret_cast<const f32x4*>(g.bias + col);
-    if constexpr (EPI == WAM_EPI_BF16 || EPI == WAM_EPI_GELU_BF16) {
-      bf16x4 o;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) o[j] = (bf16)(EPI == WAM_EPI_GELU_BF16 ? gelu_tanh_f(v[j]) : v[j]);
-      *reinterpret_cast<bf16x4*>(static_cast<bf16*>(g.out) + orow + col) = o;
-    } else if constexpr (EPI == WAM_EPI_RESID_F32) {
-      f32x4 gt = {1.f, 1.f, 1.f, 1.f};
-      if (g.gate_a || g.gate_v) {
-        gt = g.gate_a ? *reinterpret_cast<const f32x4*>(g.gate_a + col) : f32x4{0.f, 0.f, 0.f, 0.f};
-        if (g.gate_v)
-          gt += *reinterpret_cast<const f32x4*>(g.gate_v + gate_off(g, row, inv_g) + col);
-      }
-      f32x4* o = reinterpret_cast<f32x4*>(static_cast<float*>(g.out) + orow + col);
-      *o = *o + gt * v;
-    } else {
-      *reinterpret_cast<f32x4*>(static_cast<float*>(g.out) + orow + col) = v;
-    }
-    return;
-  }
-  // ragged last columns
   for (int j = 0; j < 4 && col + j < g.N; ++j) {
     float x = v[j] * (g.w_scale ? g.w_scale[col + j] : 1.f) + (g.bias ? g.bias[col + j] : 0.f);
     if constexpr (EPI == WAM_EPI_BF16) {
@@ -367,27 +344,104 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int t
 
   // ---- epilogue: each wave stages 32 rows x WCOLS of its tile through LDS (reusing
   // the operand buffers) so every lane then owns 4 consecutive columns of one row and
-  // the stores are 8/16-byte vectors over contiguous row segments.
+  // the stores are 8/16-byte vectors over contiguous row segments.  A lane keeps the
+  // same four columns for the whole tile, so the per-column operands (scales, bias,
+  // shared gate) are loaded once; the per-row ones (row scale, per-group gate, the
+  // residual) are loaded for all of a slab's rows before its first store.  Interleaved
+  // with the stores, each load would wait for the store before it: the compiler cannot
+  // prove that the output does not alias those arrays.
   // rows padded by 8 floats: the two half-waves (rows 4 apart) use disjoint banks
   constexpr int WCOLS = BN / C::WN, SROW = WCOLS + 8;
+  constexpr int CG = WCOLS / 4, RP = 64 / CG, NP = 32 / RP;  // column groups, rows per pass, passes
+  static_assert(64 % CG == 0 && 32 % RP == 0, "a lane's columns must not change between passes");
   static_assert(C::WM * C::WN * 32 * SROW * 4 <= S * C::STAGE, "staging does not fit");
+  constexpr bool RESID = EPI == WAM_EPI_RESID_F32;
   float* stage = reinterpret_cast<float*>(smem) + w * 32 * SROW;
   const float inv_o = 1.0f / (float)g.o_rows, inv_g = 1.0f / (float)g.gate_rows;
   const int row_base = m0 + wm * (BM / C::WM), col_base = n0 + wn * WCOLS;
+  const int cl = 4 * (lane % CG), col = col_base + cl, rl = lane / CG;
+  const bool col_full = col + 4 <= g.N;
+  f32x4 cmul = {1.f, 1.f, 1.f, 1.f}, cadd = {0.f, 0.f, 0.f, 0.f}, cgate = {1.f, 1.f, 1.f, 1.f};
+  if (col_full) {
+    if (g.w_scale) cmul = *reinterpret_cast<const f32x4*>(g.w_scale + col);
+    if (g.bias) cadd = *reinterpret_cast<const f32x4*>(g.bias + col);
+    if (RESID && (g.gate_a || g.gate_v))
+      cgate = g.gate_a ? *reinterpret_cast<const f32x4*>(g.gate_a + col) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
 #pragma unroll
   for (int a = 0; a < C::TM; ++a) {
+    // per-row operands of this slab's rows (clamped to the last row; only stored rows use
+    // them), in flight while the accumulators go through LDS
+    // (raw values only: nothing here waits for a load; the sums and products come after)
+    float rmul[NP];
+    f32x4 gv[NP], prev[NP];
+    int rows[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const int row = row_base + a * 32 + p * RP + rl;
+      rows[p] = row < g.M ? row : g.M - 1;
+      rmul[p] = 1.f;
+      gv[p] = prev[p] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    if (col_full) {
+      if (g.a_scale) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) rmul[p] = g.a_scale[rows[p]];
+      }
+      if constexpr (RESID) {
+        if (g.gate_v) {
+#pragma unroll
+          for (int p = 0; p < NP; ++p)
+            gv[p] = *reinterpret_cast<const f32x4*>(g.gate_v + gate_off(g, rows[p], inv_g) + col);
+        }
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+          prev[p] = *reinterpret_cast<const f32x4*>(static_cast<const float*>(g.out) +
+                                                    group_off(rows[p], g.o_rows, inv_o, g.o_bs, g.ldo) + col);
+      }
+    }
 #pragma unroll
     for (int b = 0; b < C::TN; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
         stage[(8 * (r >> 2) + 4 * hh + (r & 3)) * SROW + b * 32 + l32] = acc[a][b][r];
     __syncthreads();
+    if (col_full) {
+      // One store per pass, all of them after the loads above.  In a slab whose 32 rows
+      // are all inside M (every slab but those of the last row tile) the stores are
+      // unconditional: with no branch between them each store waits only for its own
+      // operands, not for the completion of every earlier store.
+      auto store = [&](int p) {
+        const int rloc = p * RP + rl;
+        f32x4 v = *reinterpret_cast<const f32x4*>(&stage[rloc * SROW + cl]);
+        const int64_t orow = group_off(rows[p], g.o_rows, inv_o, g.o_bs, g.ldo);
+        v = v * rmul[p] * cmul + cadd;
+        if constexpr (EPI == WAM_EPI_BF16 || EPI == WAM_EPI_GELU_BF16) {
+          bf16x4 o;
 #pragma unroll
-    for (int p = 0; p < 32 * WCOLS / 256; ++p) {
-      const int idx = p * 64 + lane;
-      const int rloc = idx / (WCOLS / 4), c4 = idx % (WCOLS / 4);
-      const f32x4 v = *reinterpret_cast<const f32x4*>(&stage[rloc * SROW + c4 * 4]);
-      epilogue4<EPI>(g, inv_o, inv_g, row_base + a * 32 + rloc, col_base + c4 * 4, v);
+          for (int j = 0; j < 4; ++j) o[j] = (bf16)(EPI == WAM_EPI_GELU_BF16 ? gelu_tanh_f(v[j]) : v[j]);
+          *reinterpret_cast<bf16x4*>(static_cast<bf16*>(g.out) + orow + col) = o;
+        } else if constexpr (RESID) {
+          *reinterpret_cast<f32x4*>(static_cast<float*>(g.out) + orow + col) = prev[p] + (cgate + gv[p]) * v;
+        } else {
+          *reinterpret_cast<f32x4*>(static_cast<float*>(g.out) + orow + col) = v;
+        }
+      };
+      if (row_base + a * 32 + 32 <= g.M) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) store(p);
+      } else {
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+          if (row_base + a * 32 + p * RP + rl < g.M) store(p);
+      }
+    } else if (col < g.N) {  // the matrix's last, partial column group (rare)
+#pragma unroll 1
+      for (int p = 0; p < NP; ++p) {
+        const int rloc = p * RP + rl, row = row_base + a * 32 + rloc;
+        const f32x4 v = *reinterpret_cast<const f32x4*>(&stage[rloc * SROW + cl]);
+        if (row < g.M) epilogue_ragged<EPI>(g, inv_o, inv_g, row, col, v);
+      }
     }
     __syncthreads();
   }

@@ -83,6 +83,7 @@ GEMM_SHAPES = [
     (300, 200, 136),     # small tiles, ragged M, N and K (K % 64 != 0)
     (3152, 5192, 520),   # big tiles (>= 256 of them), ragged M, N and K
     (17, 16, 16),        # the action embedding's K
+    (130, 203, 72),      # N % 4 != 0: the last column group is stored element by element
 ]
 
 
@@ -97,32 +98,37 @@ def test_gemm_epilogues(M, N, K, epi):
     bias = synth.normal(7, "b_qkv", (N,), 0.1, K, dtype="f32")
     acc = oracle.linear(A.f64, W.f64, bias.f64)
     Ad, Wd, bd = dev(A), dev(W), dev(bias)
+    N4 = (N + 3) // 4 * 4  # output and gate row strides must be multiples of 4
     if epi in ("bf16", "gelu"):
-        out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+        out = torch.zeros((M, N4), dtype=torch.bfloat16, device="cuda")
         w.wam_gemm_bf16(Ad, Wd, out, w.WAM_EPI_BF16 if epi == "bf16" else w.WAM_EPI_GELU_BF16, bias=bd)
         torch.cuda.synchronize()
         ref = acc if epi == "bf16" else oracle.gelu_tanh(acc)
-        assert rel_l2(host(out), ref) <= 3e-3
+        assert rel_l2(host(out[:, :N]), ref) <= 3e-3
+        assert not out[:, N:].any()  # padding columns untouched
     elif epi == "f32":
-        out = torch.empty((M, N), dtype=torch.float32, device="cuda")
+        out = torch.zeros((M, N4), dtype=torch.float32, device="cuda")
         w.wam_gemm_bf16(Ad, Wd, out, w.WAM_EPI_F32, bias=bd)
         torch.cuda.synchronize()
-        assert rel_l2(host(out), acc) <= 1e-5
+        assert rel_l2(host(out[:, :N]), acc) <= 1e-5
+        assert not out[:, N:].any()
     else:
         # x += (gate_a + gate_v[batch]) * (A W^T + b), batches of `rows` rows
         rows = max(1, M // 3)
         nb = (M + rows - 1) // rows
-        x0 = synth.normal(7, "e0", (M, N), 1.0, K, dtype="f32")
+        x0 = synth.normal(7, "e0", (M, N4), 1.0, K, dtype="f32")
         ga = synth.normal(7, "mod6", (N,), 0.5, K, dtype="f32")
-        gv = synth.normal(7, "mod6", (nb, 2 * N), 0.5, K + 1, dtype="f32")
+        gv = synth.normal(7, "mod6", (nb, 2 * N4), 0.5, K + 1, dtype="f32")
         out = dev(x0)
         gvd = dev(gv)
-        w.wam_gemm_bf16(Ad, Wd, out, w.WAM_EPI_RESID_F32, bias=bd, gate_a=dev(ga), gate_v=gvd[:, N:],
-                        gate_stride=2 * N, gate_rows=rows)
+        w.wam_gemm_bf16(Ad, Wd, out, w.WAM_EPI_RESID_F32, bias=bd, gate_a=dev(ga), gate_v=gvd[:, N4:],
+                        gate_stride=2 * N4, gate_rows=rows)
         torch.cuda.synchronize()
-        gate = ga.f64[None] + gv.f64[np.arange(M) // rows, N:]
-        ref = x0.f64 + gate * acc
-        assert rel_l2(host(out) - x0.f64, ref - x0.f64) <= 1e-5
+        gate = ga.f64[None] + gv.f64[np.arange(M) // rows, N4:N4 + N]
+        ref = x0.f64[:, :N] + gate * acc
+        got = host(out)
+        assert rel_l2(got[:, :N] - x0.f64[:, :N], ref - x0.f64[:, :N]) <= 1e-5
+        assert np.array_equal(got[:, N:], x0.f64[:, N:])
 
 
 def test_gemm_row_remap():
