@@ -17,12 +17,15 @@ namespace {
 // modulation vectors are read once per LN_ROWS rows.  One wavefront
 // per row, so a 3152-row call keeps ~3150 rows in flight at once; the row stays in
 // registers (NV float4 per lane, NV = d/256) between the mean, variance and output
-// passes, so x is read from HBM once.
+// passes, so x is read from HBM once.  Each wavefront issues its row's loads before the
+// workgroup builds P and Q, and the barrier after that waits for the LDS writes only,
+// so the row is in flight while the modulation vectors are read.
 // ---------------------------------------------------------------------------------
 constexpr int LN_ROWS = 4;  // rows (= wavefronts) per workgroup
 
 template <int NV>
-__global__ __launch_bounds__(LN_ROWS * 64) void ln_mod_kernel(const LnArgs a, int blocks_per_batch, int seg,
+// (4 wavefronts per SIMD up to d = 5120: a row, 80 VGPRs, fits with the rest in 128)
+__global__ __launch_bounds__(LN_ROWS * 64, NV <= 20 ? 4 : 2) void ln_mod_kernel(const LnArgs a, int blocks_per_batch, int seg,
                                                               int seg_blocks) {
   extern __shared__ __attribute__((aligned(16))) float PQ[];  // [2][d]
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -33,6 +36,13 @@ __global__ __launch_bounds__(LN_ROWS * 64) void ln_mod_kernel(const LnArgs a, in
   const int rend = second ? a.rows_per_batch : seg;
   const int d = a.d, nv = d >> 8;
   const int64_t mb = (int64_t)b * a.mod_stride + (second ? a.alt_off : 0);
+  const bool active = rloc < rend;
+  const int64_t row = (int64_t)b * a.rows_per_batch + (active ? rloc : rend - 1);
+  const float* xr = a.x + row * d;
+  f32x4 v[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+    if (i < nv) v[i] = *reinterpret_cast<const f32x4*>(xr + (i * 64 + lane) * 4);
   float* P = PQ;
   float* Q = PQ + d;
   for (int c = threadIdx.x * 4; c < d; c += LN_ROWS * 256) {
@@ -47,18 +57,16 @@ __global__ __launch_bounds__(LN_ROWS * 64) void ln_mod_kernel(const LnArgs a, in
     *reinterpret_cast<f32x4*>(P + c) = g * (one + sc);
     *reinterpret_cast<f32x4*>(Q + c) = bt * (one + sc) + sh;
   }
-  __syncthreads();
-  if (rloc >= rend) return;
-  const int64_t row = (int64_t)b * a.rows_per_batch + rloc;
-  const float* xr = a.x + row * d;
-  f32x4 v[NV];
+  // LDS writes visible to the workgroup (the row loads stay in flight)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));  // lgkmcnt(0) only
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  if (!active) return;
   float s = 0.f;
 #pragma unroll
   for (int i = 0; i < NV; ++i)
-    if (i < nv) {
-      v[i] = *reinterpret_cast<const f32x4*>(xr + (i * 64 + lane) * 4);
-      s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
-    }
+    if (i < nv) s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
   const float mean = wave_sum(s) / (float)d;
   float q = 0.f;
 #pragma unroll
