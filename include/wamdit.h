@@ -348,10 +348,14 @@ typedef struct {
  * call wam_dit_step_fwd(io) at t_i (io->t [B] is written by the loop; io->z_t and
  * io->a_t are rewritten from x before every call; io->v_video / v_action receive the
  * step's raw velocities), then wam_flow_step.  The cache rows [cache_len, cache_len+L)
- * are rewritten by every computed step, as by a single step.  With caching off the loop
- * never synchronizes (it can be captured in a graph); with caching on it synchronizes
- * the stream once per computed step after the first to read the similarity.  Same
- * validation and errors as wam_dit_step_fwd, plus the loop's own parameters. */
+ * are rewritten by every computed step, as by a single step.  The text conditions every
+ * step alike, so when io->ctx_kv is NULL the loop projects the text and each block's
+ * cross-attention K|V once, before the first step, into its workspace (n_layers * B *
+ * Lc * 2d bf16 more) and every step reads them; results are those of independent
+ * steps.  With caching off the loop never synchronizes (it can be captured in a graph);
+ * with caching on it synchronizes the stream once per computed step after the first to
+ * read the similarity.  Same validation and errors as wam_dit_step_fwd, plus the loop's
+ * own parameters. */
 size_t wam_denoise_workspace_bytes(const wam_model* m, const wam_step_io* io,
                                    const wam_denoise_params* p);
 wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wam_denoise_params* p,

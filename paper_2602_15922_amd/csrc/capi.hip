@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <vector>
 
 #include "kernels.h"
 
@@ -621,7 +622,7 @@ FlowArgs flow_args(const wam_flow_dims& d) {
 }
 
 struct DenoiseWs {
-  size_t step, va, vb, cos, cos_out, total;
+  size_t step, va, vb, cos, cos_out, kv, kv_layer, total;
 };
 DenoiseWs denoise_ws(const wam_model& m, const wam_step_io& io, const wam_denoise_params& p) {
   const int64_t nx = p.cfg ? 1 : io.B;
@@ -633,6 +634,9 @@ DenoiseWs denoise_ws(const wam_model& m, const wam_step_io& io, const wam_denois
   w.vb = off; off += align256((size_t)nx * n * 4);
   w.cos = off; off += align256(cosine_workspace_bytes());
   w.cos_out = off; off += 256;
+  // the text's cross K|V of every block, computed once per chunk (unless supplied)
+  w.kv_layer = io.ctx_kv ? 0 : align256((size_t)io.B * io.Lc * 2 * m.dims.d * 2);
+  w.kv = off; off += (size_t)std::max(m.dims.n_layers, 0) * w.kv_layer;
   w.total = off;
   return w;
 }
@@ -912,6 +916,33 @@ wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wa
   const int64_t n = (int64_t)(p->cfg ? 1 : io->B) * (fd.n_video + fd.n_action);
   const bool caching = p->cache_window > 0;
 
+  // The text and so every block's cross-attention K|V are the same at every step of
+  // the chunk: unless the caller supplied them, project them once here and let each
+  // step read them (the same GEMMs a step would run, so the results are unchanged).
+  wam_step_io sio = *io;
+  std::vector<const void*> kv_ptrs;
+  if (!io->ctx_kv && m->dims.n_layers > 0) {
+    const wam_dims& D = m->dims;
+    const StepWs sl = step_ws(*m, *io);
+    char* sw = w + lay.step;
+    const int32_t L = io->F * (io->Hl / 2) * (io->Wl / 2) + io->A;
+    const BlockWs bl = block_ws(D, io->B, L, io->Lc);
+    char* q8 = sw + sl.block + bl.q8;
+    float* qs = reinterpret_cast<float*>(sw + sl.block + bl.qs);
+    void* ctx = sw + sl.ctx;
+    TRY(text_run(*m, io->B, io->Lc, io->text, ctx, sw + sl.piece, stream));
+    kv_ptrs.resize(D.n_layers);
+    for (int l = 0; l < D.n_layers; ++l) {
+      void* kv = w + lay.kv + (size_t)l * lay.kv_layer;
+      const wam_block_weights& W = m->blocks[l];
+      const wam_block_fp8* F8 = W.fp8;
+      TRY(proj(gemm(io->B * io->Lc, 2 * D.d, D.d, WAM_EPI_BF16, ctx, D.d, W.w_ckv, W.b_ckv, kv, 2 * D.d),
+               F8 ? F8->w_ckv : nullptr, F8 ? F8->s_ckv : nullptr, q8, qs, stream));
+      kv_ptrs[l] = kv;
+    }
+    sio.ctx_kv = kv_ptrs.data();
+  }
+
   // the model inputs of the first call from the initial state
   FlowArgs q = flow_args(fd);
   q.x = p->x; q.z_next = z; q.a_next = a;
@@ -930,7 +961,7 @@ wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wa
       continue;
     }
     HIPCHECK(launch_fill(t_dev, io->B, p->t_sched[i], stream));
-    TRY(step_run(*m, *io, w + lay.step, stream));
+    TRY(step_run(*m, sio, w + lay.step, stream));
     before = last;
     last = before == 0 ? 1 : 0;
     f.v_video = io->v_video; f.v_action = io->v_action; f.v_out = vbuf[last];
