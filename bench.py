@@ -74,7 +74,7 @@ def build_model(wl, torch):
             b[n] = zf(k)
         blocks.append(b)
         kcs.append(rn(wl.B, wl.Lcap, wl.H, wl.Dh, std=1.0))
-        vcs.append(rn(wl.B, wl.H, wl.Dh, wl.Lcap, std=1.0))  # V cache, transposed
+        vcs.append(rn(wl.B, wl.Lcap, wl.H, wl.Dh, std=1.0))
     dims = w.make_dims(d, wl.H, wl.Dh, wl.ffn, wl.n_layers, wl.latent_ch, wl.act_dim, wl.text_dim,
                        wl.freq_dim, wl.eps)
     model = w.make_model(dims, top, blocks)
@@ -214,8 +214,7 @@ def cpu_baseline(wl):
 def probe_attn(wl, n):
     """Launch a plain device-to-device copy of known size (the calibration for HBM byte
     counters) and n self-attention launches of the step's shape (queries of one chunk
-    against the cached chunks plus itself, V in the cache's transposed layout), with
-    nothing else on the GPU in between."""
+    against the cached chunks plus itself), with nothing else on the GPU in between."""
     import torch
     import paper_2602_15922_amd as w
     torch.cuda.set_device(0)
@@ -225,14 +224,14 @@ def probe_attn(wl, n):
     dst = torch.empty_like(src)
     q = torch.randn(wl.B, wl.L, wl.H, wl.Dh, generator=g, device="cuda", dtype=torch.bfloat16)
     k = torch.randn(wl.B, wl.Lk, wl.H, wl.Dh, generator=g, device="cuda", dtype=torch.bfloat16)
-    v = torch.randn(wl.B, wl.H, wl.Dh, wl.Lcap, generator=g, device="cuda", dtype=torch.bfloat16)
+    v = torch.randn_like(k)
     o = torch.empty_like(q)
     chunks = w.cached_chunks(wl.cache_rows, wl.L)
     torch.cuda.synchronize()
     torch.mul(src, 1, out=dst)  # one elementwise kernel: reads and writes copy_bytes
     torch.cuda.synchronize()
     for _ in range(n):
-        w.wam_attn_blockcausal(q, k, v, o, chunks, v_transposed=True)
+        w.wam_attn_blockcausal(q, k, v, o, chunks)
     torch.cuda.synchronize()
     assert torch.isfinite(o).all()
     print(json.dumps({"probe": "attn", "workload": wl.name, "copy_bytes": copy_bytes, "attn_launches": n,

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define WAM_ABI_VERSION 4
+#define WAM_ABI_VERSION 3
 #define WAM_MAX_CHUNKS 16
 
 typedef enum {
@@ -100,14 +100,6 @@ typedef struct {
  * must span less than 2 GiB (Lk * kv_tok_stride * 2 bytes < 2^31; else
  * WAM_EUNSUPPORTED).  Deterministic: the same inputs give bitwise the same output
  * (no atomics, no split-K).
- *
- * v_transposed = 1 takes v as V^T instead: [B][H][Dh][v_ld] bf16, contiguous, row
- * (b, h, j) holding dim j of every key (the layout of the self-attention V cache; the
- * kernel then reads its output-product operand with plain 16-byte LDS reads).  The kv
- * strides then describe k only.  v_ld is a multiple of 8 and >= Lk rounded up to 8;
- * the keys [Lk, round_up(Lk, 8)) of each row are read but carry no weight (they need
- * not be initialized); v 16-byte aligned; Dh * v_ld * 2 bytes < 2^31.
- * v_transposed = 0 (zero-initialized descriptor): v as described above, v_ld unused.
  * ------------------------------------------------------------------------------ */
 typedef struct {
   int32_t B, H, Dh, Lq, Lk;
@@ -116,8 +108,6 @@ typedef struct {
   int64_t o_tok_stride, o_batch_stride;
   float scale;
   wam_chunks ch;
-  int32_t v_transposed;
-  int64_t v_ld;
 } wam_attn_desc;
 
 wam_status wam_attn_blockcausal(const wam_attn_desc* desc, const void* q, const void* k,
@@ -174,14 +164,11 @@ struct wam_block_fp8 {
  * e0     [B][6][d] fp32 per-sample time modulation.
  * rope_cos, rope_sin  [L][Dh/2] fp32, built with wam_rope_tables for the rows'
  *        positions (all samples share positions).
- * k_cache  [B][Lcap][H][Dh] bf16, K stored after RoPE (token-major).
- * v_cache  [B][H][Dh][Lcap] bf16, V stored transposed (row (b, h, j) holds dim j of
- *        every cached token), the layout the self-attention's output product reads.
- *        Lcap is a multiple of 8.  Token rows [0, cache_len) of both caches are read;
- *        rows [cache_len, cache_len+L) are overwritten with the current rows' K and V.
- *        The caller advances cache_len by L only for a cache-update pass; a denoising
- *        step leaves it, so the next step overwrites the same rows.
- *        cache_len + L <= Lcap.
+ * k_cache, v_cache  [B][Lcap][H][Dh] bf16, K stored after RoPE.  Rows
+ *        [0, cache_len) are read; rows [cache_len, cache_len+L) are overwritten with
+ *        the current rows' K and V.  The caller advances cache_len by L only for a
+ *        cache-update pass; a denoising step leaves it, so the next step overwrites
+ *        the same rows.  cache_len + L <= Lcap.
  * ch     key/query chunks of the self-attention: Lk = cache_len + L, Lq = L.
  * ctx    [B][Lc][d] bf16 projected text; or ctx_kv [B][Lc][2d] bf16 its cross K|V
  *        already projected with this block's w_ckv (then ctx may be NULL and w_ckv
@@ -234,9 +221,8 @@ typedef struct {
  * a_t      [B][A][act_dim] bf16 noisy actions.
  * t        [B] fp32 timestep per sample (one per chunk, section 3.1).
  * text     [B][Lc][text_dim] bf16 text features.
- * k_cache, v_cache  HOST arrays of n_layers device pointers: k_cache[l] [B][Lcap][H][Dh]
- *          and v_cache[l] [B][H][Dh][Lcap] (transposed) bf16, Lcap a multiple of 8,
- *          semantics as in wam_dit_block_fwd.
+ * k_cache, v_cache  HOST arrays of n_layers device pointers, each [B][Lcap][H][Dh]
+ *          bf16, semantics as in wam_dit_block_fwd.
  * ctx_kv   optional HOST array of n_layers device pointers [B][Lc][2d] bf16 holding
  *          each block's precomputed cross K|V of this text (NULL: computed here).
  * rope_cos, rope_sin  [L][Dh/2] fp32 tables of the rows' positions.
@@ -389,9 +375,8 @@ wam_status wam_adaln_ln_mod(int32_t B, int32_t rows_per_batch, int32_t d, float 
 
 /* 3D RoPE on a fused QKV projection and KV-cache append.
  * qkv [B][L][3][H][Dh] bf16 (q | k | v per token); rope_cos/sin [L][Dh/2] fp32.
- * Writes q_out [B][L][H][Dh] (rotated q), rotated k into k_cache rows [row0, row0+L)
- * of [B][Lcap][H][Dh], and v transposed into columns [row0, row0+L) of v_cache
- * [B][H][Dh][Lcap] (v_cache[b][h][j][row0 + l] = v of token l, dim j). */
+ * Writes q_out [B][L][H][Dh] (rotated q), rotated k into k_cache rows
+ * [row0, row0+L) and v into v_cache rows [row0, row0+L) of [B][Lcap][H][Dh]. */
 wam_status wam_rope_qkv(int32_t B, int32_t L, int32_t H, int32_t Dh, const void* qkv,
                         const float* rope_cos, const float* rope_sin, void* q_out,
                         void* k_cache, void* v_cache, int32_t Lcap, int32_t row0,

@@ -50,8 +50,7 @@ class wam_attn_desc(C.Structure):
                 ("q_tok_stride", _i64), ("q_batch_stride", _i64),
                 ("kv_tok_stride", _i64), ("kv_batch_stride", _i64),
                 ("o_tok_stride", _i64), ("o_batch_stride", _i64),
-                ("scale", C.c_float), ("ch", wam_chunks),
-                ("v_transposed", _i32), ("v_ld", _i64)]
+                ("scale", C.c_float), ("ch", wam_chunks)]
 
 
 class wam_dims(C.Structure):
@@ -234,21 +233,15 @@ def wam_abi_version() -> int:
     return lib().wam_abi_version()
 
 
-def wam_attn_blockcausal(q, k, v, o, chunks: wam_chunks, scale: float = 0.0, stream=None, v_transposed=False,
-                         Lk=None):
-    """q, o: [B, Lq, H, Dh] bf16 views; k: [B, Lk, H, Dh] bf16 view (token strides taken from
-    the tensors; heads contiguous); v: as k, or with v_transposed a contiguous V^T
-    [B, H, Dh, v_ld] (Lk then from k unless given)."""
+def wam_attn_blockcausal(q, k, v, o, chunks: wam_chunks, scale: float = 0.0, stream=None):
+    """q, o: [B, Lq, H, Dh] bf16 views; k, v: [B, Lk, H, Dh] bf16 views (token strides taken
+    from the tensors; heads contiguous)."""
     B, Lq, H, Dh = q.shape
-    d = wam_attn_desc(B=B, H=H, Dh=Dh, Lq=Lq, Lk=k.shape[1] if Lk is None else Lk,
+    d = wam_attn_desc(B=B, H=H, Dh=Dh, Lq=Lq, Lk=k.shape[1],
                       q_tok_stride=q.stride(1), q_batch_stride=q.stride(0),
                       kv_tok_stride=k.stride(1), kv_batch_stride=k.stride(0),
                       o_tok_stride=o.stride(1), o_batch_stride=o.stride(0), scale=scale, ch=chunks)
-    if v_transposed:
-        if not v.is_contiguous() or tuple(v.shape[:3]) != (B, H, Dh):
-            raise ValueError("transposed v must be a contiguous [B, H, Dh, v_ld] tensor")
-        d.v_transposed, d.v_ld = 1, v.shape[3]
-    elif v.stride(1) != k.stride(1) or v.stride(0) != k.stride(0):
+    if v.stride(1) != k.stride(1) or v.stride(0) != k.stride(0):
         raise ValueError("k and v must share token and batch strides")
     _check(lib().wam_attn_blockcausal(C.byref(d), _p(q), _p(k), _p(v), _p(o), _stream(stream)))
 
@@ -298,7 +291,7 @@ def wam_adaln_ln_mod(x, h, eps, rows_per_batch, gamma=None, beta=None, shift_a=N
 
 
 def wam_rope_qkv(qkv, cos_t, sin_t, q_out, k_cache, v_cache, row0, H, Dh, stream=None):
-    """qkv [B, L, 3*H*Dh] bf16; k_cache [B, Lcap, H, Dh] and v_cache [B, H, Dh, Lcap] bf16."""
+    """qkv [B, L, 3*H*Dh] bf16; caches [B, Lcap, H, Dh] bf16."""
     B, L = qkv.shape[0], qkv.shape[1]
     _check(lib().wam_rope_qkv(B, L, H, Dh, _p(qkv), _p(cos_t), _p(sin_t), _p(q_out), _p(k_cache),
                               _p(v_cache), k_cache.shape[1], row0, _stream(stream)))
@@ -361,9 +354,8 @@ def wam_block_workspace_bytes(dims: wam_dims, B: int, L: int, Lc: int) -> int:
 
 def wam_dit_block_fwd(dims: wam_dims, weights: wam_block_weights, x, e0, rope_cos, rope_sin, k_cache,
                       v_cache, cache_len, chunks: wam_chunks, ctx=None, ctx_kv=None, ws=None, stream=None):
-    """x [B, L, d] fp32 (in place); k_cache [B, Lcap, H, Dh], v_cache [B, H, Dh, Lcap] bf16;
-    ctx [B, Lc, d] bf16 or ctx_kv [B, Lc, 2d]; ws a uint8 device tensor of at least
-    wam_block_workspace_bytes."""
+    """x [B, L, d] fp32 (in place); caches [B, Lcap, H, Dh] bf16; ctx [B, Lc, d] bf16 or ctx_kv
+    [B, Lc, 2d]; ws a uint8 device tensor of at least wam_block_workspace_bytes."""
     B, L = x.shape[0], x.shape[1]
     Lc = (ctx if ctx is not None else ctx_kv).shape[1]
     io = wam_block_io(x=_p(x), e0=_p(e0), rope_cos=_p(rope_cos), rope_sin=_p(rope_sin),

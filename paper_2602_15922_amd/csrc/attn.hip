@@ -18,15 +18,9 @@
 // tile is computed transposed, S^T = K Q^T, so a lane owns one query and its softmax
 // statistics stay in the lane (plus the partner lane l^32 holding the other half of
 // the keys); the output is accumulated transposed as well, O^T = V^T P^T, so the
-// rescale is lane-local too.  V comes in one of two layouts:
-//  * token-major ([key][dim], as K): V stays row-major in LDS and its transposed MFMA
-//    operand is read with the gfx950 transposing LDS load (ds_read_b64_tr_b16);
-//  * transposed ([dim][key], the layout of the self-attention V cache): the operand
-//    is a plain 16-byte LDS read of 8 consecutive keys.  For that the score rows are
-//    produced in a permuted key order (perm16 below) so that each lane's 8
-//    probabilities of an MFMA k-block are 8 consecutive keys, exactly the B operand
-//    of the output product, with no data movement between the two products.
-// The reference maximum is only raised when a tile exceeds it by more than 2^8 in the
+// rescale is lane-local too.  V stays row-major in LDS and its transposed MFMA
+// operand is read with the gfx950 transposing LDS load (ds_read_b64_tr_b16).  The
+// reference maximum is only raised when a tile exceeds it by more than 2^8 in the
 // exp2 domain, which leaves the result exact (o = acc / l for any reference) and skips
 // almost every accumulator rescale.  Both tiles are XOR-swizzled in 16-byte chunks so
 // the operand reads are bank-conflict free (kswz/vswz below), applied on the load side
@@ -45,6 +39,15 @@ constexpr float RESCALE_LOG2 = 8.0f;  // allowed growth of exp2 arguments before
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 typedef __attribute__((address_space(3))) void lds_void;
+
+// The value held by lane l ^ 32 (the lane with the same query and the other half of the
+// keys): one v_permlane32_swap, which exchanges the upper half of its first operand with
+// the lower half of its second, instead of a round trip through LDS (ds_bpermute).
+WAM_DEV float other_half(float v) {
+  const unsigned u = __float_as_uint(v);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
+}
 
 WAM_DEV int kend_of(const AttnArgs& a, int row) {
   int e = a.kend[a.n_q_chunks - 1];
@@ -69,72 +72,28 @@ WAM_DEV int kswz(int row, int ch) { return DH == 128 ? (ch ^ (row & 15)) : (ch ^
 template <int DH>
 WAM_DEV int vswz(int row, int ch) { return DH == 128 ? (ch ^ (4 * (row & 3))) : (ch ^ (4 * ((row >> 1) & 1))); }
 
-//  V^T (transposed layout): a 16-byte read covers 8 keys of one dim row (128-byte rows,
-//     16 lanes on 16 consecutive rows at one logical chunk): XOR by (row>>1)&7.
-WAM_DEV int vtswz(int row, int ch) { return ch ^ ((row >> 1) & 7); }
-
-// Score row m of a 32-key sub-tile holds key perm16(m): within each 16 rows the second
-// and third groups of 4 are swapped.  An MFMA result register r of lane (l32, hh) is
-// row 8*(r/4) + 4*hh + r%4, so registers 8*hf .. 8*hf+7 of the lane then hold keys
-// 16*hf + 8*hh .. +7 in order.
-WAM_DEV int perm16(int m) {
-  const int g = (m >> 2) & 3;
-  return (m & ~15) | ((g == 1 ? 2 : g == 2 ? 1 : g) << 2) | (m & 3);
-}
-
-// VT: vr addresses this (batch, head)'s V^T rows of v_ld keys; vkey[i] is the first
-// key of the lane's 8-key chunk inside the tile.  Chunks starting at or past Lk8 (Lk
-// rounded up to 8, <= the row length) re-read the chunk at Lk8 - 8 of the same row.
-template <int DH, bool VT>
+template <int DH>
 WAM_DEV void fetch_tile(bf16* Ks, __amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr, int kv_tsb, int Lk,
-                        int kb, int w, const int* koff, const int* voff, const int* krow, const int* vkey) {
+                        int kb, int w, const int* koff, const int* voff, const int* krow) {
   constexpr int KCH = BN * (DH / 8) / NT;
   bf16* Vs = Ks + BN * DH;
   const int soff = kb * kv_tsb;  // wave-uniform byte offset of the tile's first key row
-  const int vsoff = VT ? 2 * kb : soff;
   if (kb + BN <= Lk) {
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
       const int base = (w * KCH + i) * 64;  // wave-uniform first unit of this instruction
       __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void*)(Ks + base * 8), 16, koff[i], soff, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void*)(Vs + base * 8), 16, voff[i], vsoff, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void*)(Vs + base * 8), 16, voff[i], soff, 0, 0);
     }
   } else {
     // ragged last tile: rows past Lk re-read the last key row (their scores are masked)
-    const int Lk8 = (Lk + 7) & ~7;
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
       const int base = (w * KCH + i) * 64;
       const int over = kb + krow[i] - (Lk - 1);
       const int shift = over > 0 ? -over * kv_tsb : 0;
-      int vshift = shift;
-      if (VT) {  // kb <= Lk8 - 8, so the shifted chunk stays inside the row
-        const int vover = kb + vkey[i] - (Lk8 - 8);
-        vshift = vover > 0 ? -2 * vover : 0;
-      }
       __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void*)(Ks + base * 8), 16, koff[i] + shift, soff, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void*)(Vs + base * 8), 16, voff[i] + vshift, vsoff, 0,
-                                               0);
-    }
-  }
-}
-
-// V^T tile whose keys run past Lk (Lk % 8 != 0): keys [Lk, Lk8) of the chunk re-read
-// above are whatever the row holds there; their probabilities are 0, but 0 * NaN would
-// not be, so they are cleared in LDS (followed by a barrier before any read).
-template <int DH>
-WAM_DEV void clear_vt_tail(bf16* Vs, int kb, int Lk) {
-  const int k0 = Lk - kb;  // first local key to clear, in (0, BN)
-#pragma unroll
-  for (int i = 0; i < DH * 8 / NT; ++i) {
-    const int u = i * NT + threadIdx.x, row = u >> 3, lc = u & 7;
-    if (8 * lc + 7 >= k0) {
-      bf16x8* p = reinterpret_cast<bf16x8*>(Vs + row * BN + 8 * vtswz(row, lc));
-      bf16x8 v = *p;
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (8 * lc + e >= k0) v[e] = (bf16)0.0f;
-      *p = v;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void*)(Vs + base * 8), 16, voff[i] + shift, soff, 0, 0);
     }
   }
 }
@@ -144,7 +103,7 @@ WAM_DEV void clear_vt_tail(bf16* Vs, int kb, int Lk) {
 // LDS buffers; kofs[ks] is the lane's byte offset of its K fragment for k-step ks
 // (keys 0..31; +32 rows for the second sub-tile), vofs[mt] the lane's byte offset of
 // its transposing V read for output tile mt (row groups added as constants).
-template <int DH, bool MASK, bool VT>
+template <int DH, bool MASK>
 WAM_DEV void attn_tile(const char* Ks, const char* Vs, const bf16x8* qf, f32x16* acc, float& m_ref,
                        float& l_part, const int* kofs, const int* vofs, float c, float thr, int kb,
                        int row_kend, int hh) {
@@ -162,8 +121,7 @@ WAM_DEV void attn_tile(const char* Ks, const char* Vs, const bf16x8* qf, f32x16*
     for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int m = 8 * (r >> 2) + 4 * hh + (r & 3);
-        const int key = kb + 32 * nt + (VT ? perm16(m) : m);
+        const int key = kb + 32 * nt + 8 * (r >> 2) + 4 * hh + (r & 3);
         if (key >= row_kend) s[nt][r] = -INFINITY;
       }
   }
@@ -172,7 +130,7 @@ WAM_DEV void attn_tile(const char* Ks, const char* Vs, const bf16x8* qf, f32x16*
   for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[nt][r]);
-  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  mx = fmaxf(mx, other_half(mx));
   const bool raise = mx > m_ref + thr || (m_ref == -INFINITY && mx != -INFINITY);
   if (__any(raise)) {
     const float m_new = raise ? mx : m_ref;
@@ -205,16 +163,11 @@ WAM_DEV void attn_tile(const char* Ks, const char* Vs, const bf16x8* qf, f32x16*
     for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        if (VT) {  // dims 32*mt + l32, keys 32*nt + 16*hf + 8*hh .. +7: one 16-byte read
-          const bf16x8 vf = *reinterpret_cast<const bf16x8*>(Vs + vofs[2 * nt + hf] + mt * 32 * BN * 2);
-          acc[mt] = mfma32(vf, pb[nt][hf], acc[mt]);
-        } else {
-          const char* vr = Vs + vofs[mt] + (32 * nt + 16 * hf) * ROWB;
-          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vr));
-          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vr + 8 * ROWB));
-          const s16x4 v8[2] = {lo, hi};
-          acc[mt] = mfma32(*reinterpret_cast<const bf16x8*>(v8), pb[nt][hf], acc[mt]);
-        }
+        const char* vr = Vs + vofs[mt] + (32 * nt + 16 * hf) * ROWB;
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vr));
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vr + 8 * ROWB));
+        const s16x4 v8[2] = {lo, hi};
+        acc[mt] = mfma32(*reinterpret_cast<const bf16x8*>(v8), pb[nt][hf], acc[mt]);
       }
 }
 
@@ -226,21 +179,16 @@ WAM_DEV void tile_sync() {
 
 // Key tile t from LDS buffer `cur` (a compile-time constant in the main loop), with tile
 // t+1 fetched into the other buffer meanwhile.
-template <int DH, bool MASK, bool VT>
+template <int DH, bool MASK>
 WAM_DEV void attn_step(bf16* smem, int cur, __amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr, int kv_tsb,
                        int Lk, int t, int ntiles, int w, const int* koff, const int* voff, const int* krow,
-                       const int* vkey, const bf16x8* qf, f32x16* acc, float& m_ref, float& l_part,
-                       const int* kofs, const int* vofs, float c, float thr, int row_kend, int hh) {
+                       const bf16x8* qf, f32x16* acc, float& m_ref, float& l_part, const int* kofs,
+                       const int* vofs, float c, float thr, int row_kend, int hh) {
   constexpr int TILE = 2 * BN * DH;
   const int kb = t * BN;
-  if (t + 1 < ntiles)
-    fetch_tile<DH, VT>(smem + (cur ^ 1) * TILE, kr, vr, kv_tsb, Lk, kb + BN, w, koff, voff, krow, vkey);
-  if (VT && MASK && kb + BN > Lk && (Lk & 7)) {  // the last tile only (t + 1 == ntiles)
-    clear_vt_tail<DH>(smem + cur * TILE + BN * DH, kb, Lk);
-    __syncthreads();
-  }
+  if (t + 1 < ntiles) fetch_tile<DH>(smem + (cur ^ 1) * TILE, kr, vr, kv_tsb, Lk, kb + BN, w, koff, voff, krow);
   const char* Ks = reinterpret_cast<const char*>(smem + cur * TILE);
-  attn_tile<DH, MASK, VT>(Ks, Ks + BN * DH * 2, qf, acc, m_ref, l_part, kofs, vofs, c, thr, kb, row_kend, hh);
+  attn_tile<DH, MASK>(Ks, Ks + BN * DH * 2, qf, acc, m_ref, l_part, kofs, vofs, c, thr, kb, row_kend, hh);
   tile_sync();
 }
 
@@ -248,8 +196,7 @@ WAM_DEV void attn_step(bf16* smem, int cur, __amdgpu_buffer_rsrc_t kr, __amdgpu_
 // query's visible prefix is looked up from its chunk; otherwise (cross-attention to the
 // text, or a single chunk) every query sees all Lk keys and only the ragged last tile
 // is masked.
-// VT: V given transposed, [B][H][DH][v_ld] (keys contiguous per dim).
-template <int DH, bool CHUNKED, bool VT>
+template <int DH, bool CHUNKED>
 __global__ __launch_bounds__(NT, 2) void attn_fwd(const AttnArgs a, int nqt) {
   constexpr int KS = DH / 16;         // MFMA k-steps over the head dim
   constexpr int MT = DH / 32;         // 32-row tiles of the transposed output
@@ -284,51 +231,36 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd(const AttnArgs a, int nqt) {
   const int kend_min = CHUNKED ? kend_of(a, q0) : a.Lk;
 
   // buffer resources over this (batch, head)'s keys: every offset the kernel forms is
-  // below Lk * row bytes (V^T: DH * v_ld * 2 bytes; both < 2^31, checked by the host),
-  // so the range check never fires
+  // below Lk * row bytes (< 2^31, checked by the host), so the range check never fires
   const bf16* kp = static_cast<const bf16*>(a.k) + b * a.kv_bs + h * DH;
-  const bf16* vp = VT ? static_cast<const bf16*>(a.v) + ((int64_t)b * a.H + h) * DH * a.v_ld
-                      : static_cast<const bf16*>(a.v) + b * a.kv_bs + h * DH;
+  const bf16* vp = static_cast<const bf16*>(a.v) + b * a.kv_bs + h * DH;
   const int kv_tsb = 2 * (int)a.kv_ts;  // bytes per key row
   const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc((void*)kp, (short)0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc((void*)vp, (short)0, 0x7fffffff, 0x00020000);
 
   // ---- per-lane byte offsets of the tile fetch (loop-invariant)
-  int koff[KCH], voff[KCH], krow[KCH], vkey[KCH];
+  int koff[KCH], voff[KCH], krow[KCH];
 #pragma unroll
   for (int i = 0; i < KCH; ++i) {
     const int u = (w * KCH + i) * 64 + lane, row = u / CPR, pch = u % CPR;
     krow[i] = row;
     koff[i] = row * kv_tsb + kswz<DH>(row, pch) * 16;
-    if (VT) {  // V^T tile: DH dim rows x 8 chunks of 8 keys (BN * CPR == DH * 8 units)
-      const int vrow = u >> 3, lc = vtswz(vrow, u & 7);
-      vkey[i] = 8 * lc;
-      voff[i] = (vrow * (int)a.v_ld + 8 * lc) * 2;
-    } else {
-      vkey[i] = 0;
-      voff[i] = row * kv_tsb + vswz<DH>(row, pch) * 16;
-    }
+    voff[i] = row * kv_tsb + vswz<DH>(row, pch) * 16;
   }
 
   // ---- per-lane LDS operand offsets (bytes, loop-invariant)
-  // K fragment of k-step ks: row prow (l32, or perm16(l32) for V^T), logical chunk
-  // 2*ks + hh (the swizzle of rows r and r + 32 is the same).
-  const int prow = VT ? perm16(l32) : l32;
+  // K fragment of k-step ks: row l32, logical chunk 2*ks + hh (the swizzle of rows
+  // l32 and l32 + 32 is the same).
   int kofs[KS];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) kofs[ks] = prow * DH * 2 + kswz<DH>(prow, 2 * ks + hh) * 16;
-  int vofs[4];
-  if (VT) {
-    // A operand of k-block (nt, hf): dim row l32 (+32*mt), logical chunk 4*nt + 2*hf + hh
-#pragma unroll
-    for (int j = 0; j < 4; ++j) vofs[j] = l32 * BN * 2 + vtswz(l32, 2 * j + hh) * 16;
-  } else {
-    // V^T from row-major V: in each 16-lane group, lane j points at row (rb + j/4), dims
-    // (db + 4*(j%4) .. +3); the transposing load then hands lane i the four keys
-    // rb..rb+3 of dim db+i.  Row group rb = 32*nt + 16*hf + 4*(grp>>1) (+8 for the second
-    // half), dims of output tile mt at db = 32*mt + 16*(grp&1).  The swizzle only
-    // depends on the lane.
-    const int grp = lane >> 4, j16 = lane & 15;
+  for (int ks = 0; ks < KS; ++ks) kofs[ks] = l32 * DH * 2 + kswz<DH>(l32, 2 * ks + hh) * 16;
+  // V^T: in each 16-lane group, lane j points at row (rb + j/4), dims (db + 4*(j%4)
+  // .. +3); the transposing load then hands lane i the four keys rb..rb+3 of dim db+i.
+  // Row group rb = 32*nt + 16*hf + 4*(grp>>1) (+8 for the second half), dims of output
+  // tile mt at db = 32*mt + 16*(grp&1).  The swizzle only depends on the lane.
+  const int grp = lane >> 4, j16 = lane & 15;
+  int vofs[MT];
+  {
     const int r0 = 4 * (grp >> 1) + (j16 >> 2);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -345,23 +277,23 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd(const AttnArgs a, int nqt) {
 
   const int ntiles = (kend_max + BN - 1) / BN;
   const int n_plain = kend_min / BN < ntiles ? kend_min / BN : ntiles;  // tiles no row masks
-  fetch_tile<DH, VT>(smem, kr, vr, kv_tsb, a.Lk, 0, w, koff, voff, krow, vkey);
+  fetch_tile<DH>(smem, kr, vr, kv_tsb, a.Lk, 0, w, koff, voff, krow);
   tile_sync();
   // unmasked tiles in pairs (tile t in buffer 0, t+1 in buffer 1)
   int t = 0;
   for (; t + 2 <= n_plain; t += 2) {
-    attn_step<DH, false, VT>(smem, 0, kr, vr, kv_tsb, a.Lk, t, ntiles, w, koff, voff, krow, vkey, qf, acc, m_ref,
-                             l_part, kofs, vofs, c, thr, row_kend, hh);
-    attn_step<DH, false, VT>(smem, 1, kr, vr, kv_tsb, a.Lk, t + 1, ntiles, w, koff, voff, krow, vkey, qf, acc,
-                             m_ref, l_part, kofs, vofs, c, thr, row_kend, hh);
+    attn_step<DH, false>(smem, 0, kr, vr, kv_tsb, a.Lk, t, ntiles, w, koff, voff, krow, qf, acc, m_ref, l_part,
+                         kofs, vofs, c, thr, row_kend, hh);
+    attn_step<DH, false>(smem, 1, kr, vr, kv_tsb, a.Lk, t + 1, ntiles, w, koff, voff, krow, qf, acc, m_ref,
+                         l_part, kofs, vofs, c, thr, row_kend, hh);
   }
   // the rest (at most one unmasked tile, then the tiles that straddle a prefix end),
   // masked: the mask is a no-op on keys every row sees
   for (; t < ntiles; ++t)
-    attn_step<DH, true, VT>(smem, t & 1, kr, vr, kv_tsb, a.Lk, t, ntiles, w, koff, voff, krow, vkey, qf, acc,
-                            m_ref, l_part, kofs, vofs, c, thr, row_kend, hh);
+    attn_step<DH, true>(smem, t & 1, kr, vr, kv_tsb, a.Lk, t, ntiles, w, koff, voff, krow, qf, acc, m_ref, l_part,
+                        kofs, vofs, c, thr, row_kend, hh);
 
-  const float l = l_part + __shfl_xor(l_part, 32, 64);
+  const float l = l_part + other_half(l_part);
   if (qrow < a.Lq) {
     const float inv = 1.0f / l;
     bf16* ob = static_cast<bf16*>(a.o) + b * a.o_bs + (int64_t)qrow * a.o_ts + h * DH;
@@ -382,21 +314,13 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   const int nqt = (a.Lq + BM - 1) / BM;
   const dim3 grid((unsigned)((long)nqt * a.H * a.B)), block(NT);
   const bool chunked = a.n_k_chunks > 1;
-#define WAM_ATTN_LAUNCH(DH, CH, VT) hipLaunchKernelGGL((attn_fwd<DH, CH, VT>), grid, block, 0, s, a, nqt)
   if (a.Dh == 128) {
-    if (a.vt) {
-      if (chunked) WAM_ATTN_LAUNCH(128, true, true); else WAM_ATTN_LAUNCH(128, false, true);
-    } else {
-      if (chunked) WAM_ATTN_LAUNCH(128, true, false); else WAM_ATTN_LAUNCH(128, false, false);
-    }
+    if (chunked) hipLaunchKernelGGL((attn_fwd<128, true>), grid, block, 0, s, a, nqt);
+    else hipLaunchKernelGGL((attn_fwd<128, false>), grid, block, 0, s, a, nqt);
   } else {
-    if (a.vt) {
-      if (chunked) WAM_ATTN_LAUNCH(64, true, true); else WAM_ATTN_LAUNCH(64, false, true);
-    } else {
-      if (chunked) WAM_ATTN_LAUNCH(64, true, false); else WAM_ATTN_LAUNCH(64, false, false);
-    }
+    if (chunked) hipLaunchKernelGGL((attn_fwd<64, true>), grid, block, 0, s, a, nqt);
+    else hipLaunchKernelGGL((attn_fwd<64, false>), grid, block, 0, s, a, nqt);
   }
-#undef WAM_ATTN_LAUNCH
   return hipGetLastError();
 }
 

@@ -122,16 +122,7 @@ wam_status attn_checked(const wam_attn_desc& d, const void* q, const void* k, co
   CHECK((int64_t)d.Lk * d.kv_tok_stride * 2 <= INT32_MAX, WAM_EUNSUPPORTED,
         "one sample's keys span %lld bytes (Lk * kv_tok_stride * 2 must stay below 2^31)",
         (long long)d.Lk * d.kv_tok_stride * 2);
-  CHECK(d.v_transposed == 0 || d.v_transposed == 1, WAM_EINVAL, "v_transposed=%d (0 or 1)", d.v_transposed);
-  if (d.v_transposed) {
-    CHECK(d.v_ld % 8 == 0 && d.v_ld >= ((int64_t)d.Lk + 7) / 8 * 8, WAM_EINVAL,
-          "v_ld=%lld must be a multiple of 8 and >= Lk=%d rounded up to 8", (long long)d.v_ld, d.Lk);
-    CHECK((int64_t)d.Dh * d.v_ld * 2 <= INT32_MAX, WAM_EUNSUPPORTED,
-          "one head's V^T spans %lld bytes (Dh * v_ld * 2 must stay below 2^31)", (long long)d.Dh * d.v_ld * 2);
-  }
   a.q = q; a.k = k; a.v = v; a.o = o;
-  a.vt = d.v_transposed;
-  a.v_ld = d.v_transposed ? d.v_ld : 0;
   a.q_ts = d.q_tok_stride; a.q_bs = d.q_batch_stride;
   a.kv_ts = d.kv_tok_stride; a.kv_bs = d.kv_batch_stride;
   a.o_ts = d.o_tok_stride; a.o_bs = d.o_batch_stride;
@@ -274,7 +265,6 @@ wam_status check_block_io(const wam_dims& D, const wam_block_weights& w, const w
   CHECK(io.B <= 8, WAM_EUNSUPPORTED, "B=%d > 8", io.B);
   CHECK(io.cache_len >= 0 && (int64_t)io.cache_len + io.L <= io.Lcap, WAM_EINVAL,
         "cache_len=%d + L=%d exceeds Lcap=%d", io.cache_len, io.L, io.Lcap);
-  CHECK(io.Lcap % 8 == 0, WAM_EINVAL, "Lcap=%d must be a multiple of 8", io.Lcap);
   int32_t kend[WAM_MAX_CHUNKS];
   TRY(check_chunks(io.ch, io.L, io.cache_len + io.L, kend));
   TRY(need_ptr(io.x, "x")); TRY(need_ptr(io.e0, "e0"));
@@ -325,7 +315,6 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   ad.kv_tok_stride = d; ad.kv_batch_stride = (int64_t)io.Lcap * d;
   ad.o_tok_stride = d; ad.o_batch_stride = (int64_t)L * d;
   ad.ch = io.ch;
-  ad.v_transposed = 1; ad.v_ld = io.Lcap;
   if (ev0) HIPCHECK(hipEventRecord(ev0, s));
   TRY(attn_checked(ad, q, io.k_cache, io.v_cache, o, s));
   if (ev1) HIPCHECK(hipEventRecord(ev1, s));
@@ -539,7 +528,6 @@ wam_status check_step(const wam_model& m, const wam_step_io& io, bool head) {
   CHECK(L < (1 << 30), WAM_EINVAL, "chunk too long");
   CHECK(io.cache_len >= 0 && io.cache_len + L <= io.Lcap, WAM_EINVAL, "cache_len=%d + L=%lld exceeds Lcap=%d",
         io.cache_len, (long long)L, io.Lcap);
-  CHECK(io.Lcap % 8 == 0, WAM_EINVAL, "Lcap=%d must be a multiple of 8", io.Lcap);
   int32_t kend[WAM_MAX_CHUNKS];
   TRY(check_chunks(io.ch, (int32_t)L, (int32_t)(io.cache_len + L), kend));
   TRY(need_ptr(io.z_t, "z_t")); TRY(need_ptr(io.t, "t")); TRY(need_ptr(io.text, "text"));

@@ -132,64 +132,38 @@ __global__ __launch_bounds__(256) void quant_rows_kernel(int M, int K, const bf1
 }
 
 // ---------------------------------------------------------------------------------
-// 3D RoPE + KV append.  A workgroup owns ROPE_TL tokens of one (batch, head).  Phase 1:
-// a thread moves 8 consecutive dims (4 rotation pairs) of one token: q rotated to
-// q_out, k rotated into the K cache rows [row0, row0 + L) (16-byte loads and stores),
-// and v staged transposed in LDS.  Phase 2: the V cache is [B][H][Dh][Lcap], so each
-// head dim receives a run of up to ROPE_TL consecutive tokens, written 8 tokens per
-// 16-byte store when the run is 16-byte aligned (row0 and Lcap multiples of 8).
+// 3D RoPE + KV append.  A thread owns 8 consecutive dims (4 rotation pairs) of one
+// head of one token and moves the q, k and v slices of the fused QKV row: q rotated
+// to q_out, k rotated and v copied into the cache rows [row0, row0 + L).
 // ---------------------------------------------------------------------------------
-constexpr int ROPE_TL = 64;
-constexpr int ROPE_PITCH = ROPE_TL + 8;  // LDS row of one head dim, 16-byte multiple
-
-__global__ __launch_bounds__(256) void rope_qkv_kernel(const RopeArgs a, int ntl) {
-  __shared__ __attribute__((aligned(16))) bf16 vts[128 * ROPE_PITCH];
-  const int tl = blockIdx.x % ntl, bh = blockIdx.x / ntl, h = bh % a.H, b = bh / a.H;
-  const int l0 = tl * ROPE_TL;
-  const int nl = a.L - l0 < ROPE_TL ? a.L - l0 : ROPE_TL;
-  const int Dh = a.Dh, cpr = Dh >> 3, d = a.H * Dh;
-  for (int u = threadIdx.x; u < ROPE_TL * cpr; u += 256) {
-    const int li = u / cpr, c = u % cpr;
-    if (li >= nl) continue;
-    const int l = l0 + li;
-    const int64_t bl = (int64_t)b * a.L + l;
-    const int col = h * Dh + 8 * c;  // column inside the d-wide q/k/v slice
-    const int pair0 = 4 * c;         // first rotation pair inside the head
-    const bf16* src = static_cast<const bf16*>(a.qkv) + bl * 3 * d + col;
-    const bf16x8 qv = a.q_out ? load_bf16x8(src) : bf16x8{};
-    const bf16x8 kv = load_bf16x8(src + d), vv = load_bf16x8(src + 2 * d);
-    const f32x4 cs = *reinterpret_cast<const f32x4*>(a.cos_t + (int64_t)l * (Dh >> 1) + pair0);
-    const f32x4 sn = *reinterpret_cast<const f32x4*>(a.sin_t + (int64_t)l * (Dh >> 1) + pair0);
-    bf16x8 qo, ko;
+__global__ __launch_bounds__(256) void rope_qkv_kernel(const RopeArgs a) {
+  const int d = a.H * a.Dh, d8 = d >> 3;
+  const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (id >= (int64_t)a.B * a.L * d8) return;
+  const int c = (int)(id % d8);
+  const int64_t bl = id / d8;
+  const int l = (int)(bl % a.L), b = (int)(bl / a.L);
+  const int col = c * 8;            // column inside the d-wide q/k/v slice
+  const int pair0 = (col % a.Dh) >> 1;  // first rotation pair inside the head
+  const bf16* src = static_cast<const bf16*>(a.qkv) + bl * 3 * d + col;
+  const bf16x8 qv = a.q_out ? load_bf16x8(src) : bf16x8{};
+  const bf16x8 kv = load_bf16x8(src + d), vv = load_bf16x8(src + 2 * d);
+  const f32x4 cs = *reinterpret_cast<const f32x4*>(a.cos_t + (int64_t)l * (a.Dh >> 1) + pair0);
+  const f32x4 sn = *reinterpret_cast<const f32x4*>(a.sin_t + (int64_t)l * (a.Dh >> 1) + pair0);
+  bf16x8 qo, ko;
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const float q0 = (float)qv[2 * p], q1 = (float)qv[2 * p + 1];
-      const float k0 = (float)kv[2 * p], k1 = (float)kv[2 * p + 1];
-      qo[2 * p] = (bf16)(q0 * cs[p] - q1 * sn[p]);
-      qo[2 * p + 1] = (bf16)(q0 * sn[p] + q1 * cs[p]);
-      ko[2 * p] = (bf16)(k0 * cs[p] - k1 * sn[p]);
-      ko[2 * p + 1] = (bf16)(k0 * sn[p] + k1 * cs[p]);
-    }
-    if (a.q_out) *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.q_out) + bl * d + col) = qo;
-    const int64_t krow = ((int64_t)b * a.Lcap + a.row0 + l) * d + col;
-    *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.k_cache) + krow) = ko;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) vts[(8 * c + e) * ROPE_PITCH + li] = vv[e];
+  for (int p = 0; p < 4; ++p) {
+    const float q0 = (float)qv[2 * p], q1 = (float)qv[2 * p + 1];
+    const float k0 = (float)kv[2 * p], k1 = (float)kv[2 * p + 1];
+    qo[2 * p] = (bf16)(q0 * cs[p] - q1 * sn[p]);
+    qo[2 * p + 1] = (bf16)(q0 * sn[p] + q1 * cs[p]);
+    ko[2 * p] = (bf16)(k0 * cs[p] - k1 * sn[p]);
+    ko[2 * p + 1] = (bf16)(k0 * sn[p] + k1 * cs[p]);
   }
-  __syncthreads();
-  bf16* vbase = static_cast<bf16*>(a.v_cache) + ((int64_t)b * a.H + h) * Dh * a.Lcap + a.row0 + l0;
-  const bool vec = ((a.row0 | a.Lcap) & 7) == 0;
-  for (int u = threadIdx.x; u < Dh * (ROPE_TL / 8); u += 256) {
-    const int j = u / (ROPE_TL / 8), li0 = 8 * (u % (ROPE_TL / 8));
-    if (li0 >= nl) continue;
-    bf16* dst = vbase + (int64_t)j * a.Lcap + li0;
-    const bf16* srow = vts + j * ROPE_PITCH + li0;
-    if (vec && li0 + 8 <= nl) {
-      *reinterpret_cast<bf16x8*>(dst) = *reinterpret_cast<const bf16x8*>(srow);
-    } else {
-      for (int e = 0; e < 8 && li0 + e < nl; ++e) dst[e] = srow[e];
-    }
-  }
+  if (a.q_out) *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.q_out) + bl * d + col) = qo;
+  const int64_t crow = ((int64_t)b * a.Lcap + a.row0 + l) * d + col;
+  *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.k_cache) + crow) = ko;
+  *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.v_cache) + crow) = vv;
 }
 
 // ---------------------------------------------------------------------------------
@@ -300,9 +274,9 @@ hipError_t launch_quant_rows(int32_t M, int32_t K, const void* x, int64_t ldx, v
 }
 
 hipError_t launch_rope_qkv(const RopeArgs& a, hipStream_t s) {
-  if ((int64_t)a.B * a.L == 0) return hipSuccess;
-  const int ntl = (a.L + ROPE_TL - 1) / ROPE_TL;
-  hipLaunchKernelGGL(rope_qkv_kernel, dim3((unsigned)((int64_t)ntl * a.H * a.B)), dim3(256), 0, s, a, ntl);
+  const int64_t n = (int64_t)a.B * a.L * (a.H * a.Dh / 8);
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_qkv_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -20,9 +20,6 @@ struct AttnArgs {
   int32_t n_q_chunks;
   int32_t q_off[WAM_MAX_CHUNKS + 1];
   int32_t kend[WAM_MAX_CHUNKS];  // visible key prefix [0, kend) of each query chunk
-  // vt: v is V^T, [B][H][Dh][v_ld] (v_ld % 8 == 0, v_ld >= Lk rounded up to 8)
-  int32_t vt;
-  int64_t v_ld;
 };
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s);
 
@@ -68,9 +65,7 @@ struct RopeArgs {
   int32_t B, L, H, Dh, Lcap, row0;
   const void* qkv;
   const float *cos_t, *sin_t;
-  // k_cache [B][Lcap][H][Dh], v_cache transposed [B][H][Dh][Lcap]; q_out NULL: q is
-  // neither rotated nor stored
-  void *q_out, *k_cache, *v_cache;
+  void *q_out, *k_cache, *v_cache;  // q_out NULL: q is neither rotated nor stored
 };
 hipError_t launch_rope_qkv(const RopeArgs& a, hipStream_t s);
 

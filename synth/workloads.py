@@ -60,8 +60,7 @@ class Workload:
 
     @property
     def Lcap(self):
-        """KV cache capacity in tokens: Lk rounded up to a multiple of 8."""
-        return (self.Lk + 7) // 8 * 8
+        return self.Lk
 
     @property
     def patch_dim(self):

@@ -7,7 +7,7 @@ import numpy as np
 
 import oracle
 import synth
-from gpu_helpers import dev, host, new_caches, v_tokens, workspace
+from gpu_helpers import dev, host, workspace
 
 
 def lib():
@@ -39,13 +39,14 @@ def prev_chunk_ids(wl):
     return np.repeat(np.arange(wl.n_cached), wl.L)
 
 
-def upload_cache(wl, kc, vc, B, Lcap=None):
-    """Device caches (K [B, Lcap, H, Dh], V transposed [B, H, Dh, Lcap]) with the cached
-    rows filled from token-major kc, vc [B, cache_rows, H, Dh]."""
-    k, v = new_caches(B, wl.Lcap if Lcap is None else Lcap, wl.H, wl.Dh)
+def upload_cache(wl, kc, vc, B):
+    """[B, Lcap, H, Dh] device caches with the cached rows filled."""
+    import torch
+    k = torch.zeros((B, wl.Lcap, wl.H, wl.Dh), dtype=torch.bfloat16, device="cuda")
+    v = torch.zeros_like(k)
     if kc is not None:
         k[:, :wl.cache_rows] = dev(kc)
-        v_tokens(v)[:, :wl.cache_rows] = dev(vc)
+        v[:, :wl.cache_rows] = dev(vc)
     return k, v
 
 
@@ -179,7 +180,7 @@ class UpdateCase:
         self.t = synth.Tensor("f32", np.full(B, t_clean, dtype=np.float32))
         self.text = synth.normal(s, "text", (B, wl.Lc, wl.text_dim), 1.0)
         self.L = n_new * wl.L
-        self.Lcap = (wl.cache_rows + self.L + spare_rows + 7) // 8 * 8
+        self.Lcap = wl.cache_rows + self.L + spare_rows
         self.chunk_ids = np.arange(wl.n_cached, wl.n_cached + n_new)
 
     def layer(self, l):
@@ -204,6 +205,7 @@ class UpdateCase:
                                  prev_chunk=prev_chunk_ids(wl) if wl.n_cached else None)
 
     def upload(self):
+        import torch
         w = lib()
         wl, B = self.wl, self.wl.B
         self.top = {k: dev(v) for k, v in self.P.items()}
@@ -211,7 +213,11 @@ class UpdateCase:
         for l in range(self.n_layers):
             W, kc, vc = self.layer(l)
             self.blocks.append({k: dev(v) for k, v in W.items()})
-            k, v = upload_cache(wl, kc, vc, B, self.Lcap)
+            k = torch.zeros((B, self.Lcap, wl.H, wl.Dh), dtype=torch.bfloat16, device="cuda")
+            v = torch.zeros_like(k)
+            if kc is not None:
+                k[:, :wl.cache_rows] = dev(kc)
+                v[:, :wl.cache_rows] = dev(vc)
             self.kcs.append(k)
             self.vcs.append(v)
         self.model = w.make_model(dims_of(wl, self.n_layers), self.top, self.blocks)

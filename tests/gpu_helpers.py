@@ -35,20 +35,6 @@ def rel_l2(got, ref):
     return float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300))
 
 
-def new_caches(B, Lcap, H, Dh):
-    """Zeroed device KV caches of one layer: K token-major [B, Lcap, H, Dh], V transposed
-    [B, H, Dh, Lcap] (the library's cache layouts)."""
-    import torch
-    k = torch.zeros((B, Lcap, H, Dh), dtype=torch.bfloat16, device="cuda")
-    v = torch.zeros((B, H, Dh, Lcap), dtype=torch.bfloat16, device="cuda")
-    return k, v
-
-
-def v_tokens(v_cache):
-    """Token-major [B, Lcap, H, Dh] view of a transposed V cache [B, H, Dh, Lcap]."""
-    return v_cache.permute(0, 3, 1, 2)
-
-
 def workspace(nbytes):
     import torch
     # 256-byte aligned by the caching allocator

@@ -1,6 +1,6 @@
-"""GPU parity of wam_attn_blockcausal against the fp64 oracle (relative L2 <= 5e-3), with V
-token-major and transposed (the V cache layout), plus the bitwise properties the kernel
-guarantees: determinism and independence from future chunks (Figure 10b)."""
+"""GPU parity of wam_attn_blockcausal against the fp64 oracle (relative L2 <= 5e-3),
+plus the bitwise properties the kernel guarantees: determinism and independence from
+future chunks (Figure 10b)."""
 import numpy as np
 import pytest
 
@@ -28,24 +28,11 @@ def chunk_ids(sizes):
     return np.repeat(np.arange(len(sizes)), sizes)
 
 
-def transposed(v, pad=8, fill=float("nan")):
-    """V [B, Lk, H, Dh] (device) as V^T [B, H, Dh, v_ld], v_ld = Lk rounded up to 8 plus
-    `pad`; the padding keys hold `fill` (NaN: they must carry no weight)."""
-    import torch
-    B, Lk, H, Dh = v.shape
-    vt = torch.full((B, H, Dh, (Lk + 7) // 8 * 8 + pad), fill, dtype=torch.bfloat16, device="cuda")
-    vt[..., :Lk] = v.permute(0, 2, 3, 1)
-    return vt
-
-
-def run(q, k, v, ch, vt=False):
+def run(q, k, v, ch):
     import torch
     w = lib()
     o = torch.empty(q.shape, dtype=torch.bfloat16, device="cuda")
-    if vt:
-        w.wam_attn_blockcausal(q, k, transposed(v), o, ch, v_transposed=True)
-    else:
-        w.wam_attn_blockcausal(q, k, v, o, ch)
+    w.wam_attn_blockcausal(q, k, v, o, ch)
     torch.cuda.synchronize()
     return o
 
@@ -61,9 +48,8 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("vt", [False, True], ids=["v", "vT"])
 @pytest.mark.parametrize("name,B,H,Dh,ks,qc", CASES)
-def test_attention_matches_oracle(name, B, H, Dh, ks, qc, vt):
+def test_attention_matches_oracle(name, B, H, Dh, ks, qc):
     case = [c[0] for c in CASES].index(name)
     w = lib()
     k_chunk = chunk_ids(ks)
@@ -72,9 +58,9 @@ def test_attention_matches_oracle(name, B, H, Dh, ks, qc, vt):
     q_chunk = k_chunk[q_rows]
     Lq, Lk = len(q_rows), int(off[-1])
     q, k, v = qkv(100 + case, B, Lq, Lk, H, Dh)
-    log(f"attn {name} B={B} H={H} Dh={Dh} Lq={Lq} Lk={Lk} vt={vt}")
+    log(f"attn {name} B={B} H={H} Dh={Dh} Lq={Lq} Lk={Lk}")
     ch = w.make_chunks(ks, [ks[c] for c in qc], qc)
-    o = host(run(dev(q), dev(k), dev(v), ch, vt))
+    o = host(run(dev(q), dev(k), dev(v), ch))
     for b in range(B):
         ref = oracle.attention(q.f64[b], k.f64[b], v.f64[b], q_chunk, k_chunk)
         err = rel_l2(o[b], ref)
@@ -149,20 +135,6 @@ def test_attention_kv_cache_equivalence_on_gpu():
         assert torch.equal(o, full[:, off[c]:off[c + 1]]), c
 
 
-def test_attention_transposed_v_validation():
-    """v_ld below Lk rounded up to 8, or not a multiple of 8, is rejected."""
-    import torch
-    w = lib()
-    q = torch.zeros((1, 4, 1, 64), dtype=torch.bfloat16, device="cuda")
-    k = torch.zeros((1, 13, 1, 64), dtype=torch.bfloat16, device="cuda")
-    o = torch.zeros_like(q)
-    ch = w.make_chunks([13], [4], [0])
-    for ld in (13, 8, 20):
-        vt = torch.zeros((1, 1, 64, ld), dtype=torch.bfloat16, device="cuda")
-        with pytest.raises(w.WamError, match="v_ld"):
-            w.wam_attn_blockcausal(q, k, vt, o, ch, v_transposed=True)
-
-
 def test_attention_empty_is_noop():
     import torch
     w = lib()
@@ -181,31 +153,29 @@ def sampled_rows(bounds, extra, n_random, rng):
     return np.array(sorted(r for r in rows if 0 <= r < bounds[-1][1]))
 
 
-@pytest.mark.parametrize("vt", [False, True], ids=["v", "vT"])
-def test_attention_full_size_cached_chunk(vt):
+def test_attention_full_size_cached_chunk():
     """40 heads x 128, 3152 queries of chunk 2 against 9456 keys (two cached chunks of
     3152 plus the current one), Q/K/V ~ N(0,1); oracle on sampled query rows."""
     wl = synth.WORKLOADS["attn_q3152_k9456"]
     w = lib()
     B, H, Dh, L, Lk = 1, wl.H, wl.Dh, wl.L, wl.Lk
     q, k, v = qkv(0, B, L, Lk, H, Dh, seed=wl.seed)
-    log(f"attn full size Lq={L} Lk={Lk} vt={vt}")
-    o = host(run(dev(q), dev(k), dev(v), w.cached_chunks(wl.cache_rows, L), vt))
+    log(f"attn full size Lq={L} Lk={Lk}")
+    o = host(run(dev(q), dev(k), dev(v), w.cached_chunks(wl.cache_rows, L)))
     rows = sampled_rows([(0, L)], [127, 128, 3071, 3072], 40, np.random.default_rng(0))
     ref = oracle.attention(q.f64[0, rows], k.f64[0], v.f64[0], np.full(len(rows), 2), np.repeat([0, 1, 2], L))
     assert rel_l2(o[0, rows], ref) <= TOL
 
 
-@pytest.mark.parametrize("vt", [False, True], ids=["v", "vT"])
-def test_attention_full_size_masked_three_chunks(vt):
+def test_attention_full_size_masked_three_chunks():
     """The same 9456 rows as queries in three chunks of 3152 (block-causal prefill)."""
     wl = synth.WORKLOADS["attn_q3152_k9456"]
     w = lib()
     B, H, Dh, L = 1, wl.H, wl.Dh, wl.L
     Lk = 3 * L
     q, k, v = qkv(1, B, Lk, Lk, H, Dh, seed=wl.seed)
-    log(f"attn full size masked Lq=Lk={Lk} vt={vt}")
-    o = host(run(dev(q), dev(k), dev(v), w.make_chunks([L] * 3, [L] * 3, [0, 1, 2]), vt))
+    log(f"attn full size masked Lq=Lk={Lk}")
+    o = host(run(dev(q), dev(k), dev(v), w.make_chunks([L] * 3, [L] * 3, [0, 1, 2])))
     rows = sampled_rows([(0, L), (L, 2 * L), (2 * L, 3 * L)], [3135, 3136, 3200, 6271, 6272], 30,
                         np.random.default_rng(1))
     kc = np.repeat([0, 1, 2], L)

@@ -73,7 +73,7 @@ def identity_model(wl, n_layers):
                        "w_co": torch.zeros(d, d, dtype=torch.bfloat16, device="cuda"), "w_f1": rn(wl.ffn, d),
                        "w_f2": rn(d, wl.ffn), "mod6": mod6})
         kcs.append(rn(wl.B, wl.Lcap, wl.H, wl.Dh, std=1.0))
-        vcs.append(rn(wl.B, wl.H, wl.Dh, wl.Lcap, std=1.0))  # transposed
+        vcs.append(rn(wl.B, wl.Lcap, wl.H, wl.Dh, std=1.0))
     return P, w.make_model(dims_of(wl, n_layers), top, blocks), (top, blocks, kcs, vcs)
 
 

@@ -8,7 +8,7 @@ import pytest
 import oracle
 import synth
 from dit_cases import UpdateCase, dims_of, f64
-from gpu_helpers import dev, host, log, rel_l2, v_tokens, workspace
+from gpu_helpers import dev, host, log, rel_l2, workspace
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-2
@@ -24,7 +24,7 @@ def check_appended(case, kcs, vcs, ref, tol=TOL):
     r0, r1 = wl.cache_rows, wl.cache_rows + case.L
     for l, (k_ref, v_ref) in enumerate(ref):
         ek = rel_l2(host(kcs[l][:, r0:r1]), k_ref)
-        ev = rel_l2(host(v_tokens(vcs[l])[:, r0:r1]), v_ref)
+        ev = rel_l2(host(vcs[l][:, r0:r1]), v_ref)
         print(f"  layer {l}: appended K rel L2 {ek:.2e}, V {ev:.2e}", flush=True)
         assert ek <= tol and ev <= tol
 
@@ -37,8 +37,8 @@ def check_untouched(case, kcs, vcs):
         _, kc, vc = case.layer(l)
         if kc is not None:
             assert np.array_equal(host(kcs[l][:, :wl.cache_rows]), kc.f64)
-            assert np.array_equal(host(v_tokens(vcs[l])[:, :wl.cache_rows]), vc.f64)
-        assert not kcs[l][:, r1:].any().item() and not vcs[l][..., r1:].any().item()
+            assert np.array_equal(host(vcs[l][:, :wl.cache_rows]), vc.f64)
+        assert not kcs[l][:, r1:].any().item() and not vcs[l][:, r1:].any().item()
 
 
 def small_wl(**kw):
