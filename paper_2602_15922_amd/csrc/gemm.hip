@@ -462,21 +462,42 @@ hipError_t launch_cfg(const GemmArgs& g, hipStream_t s) {
 
 }  // namespace
 
+// Compute units of the current device (queried once per device).
+int cu_count() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    cus[dev] = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0 ? n : 256;
+  }
+  return cus[dev];
+}
+
 hipError_t launch_gemm(const GemmArgs& gin, hipStream_t s) {
   GemmArgs g = gin;
   if (g.a_rows <= 0) { g.a_rows = g.M; g.a_bs = 0; }
   if (g.o_rows <= 0) { g.o_rows = g.M; g.o_bs = 0; }
   if (g.gate_rows <= 0) { g.gate_rows = g.M; g.gate_stride = 0; }
-  // 128x256 tiles (8 wavefronts, 3-stage ring, one workgroup per CU) measure best on
-  // every shape that fills the chip; below one round of them (e.g. the 512-row text
-  // projections) 128x128 tiles, two workgroups per CU, spread the work wider.
+  // 128x256 tiles (8 wavefronts, 3-stage ring, one workgroup per CU) on every shape that
+  // fills the chip; below one round of them (e.g. the 512-row text projections) 128x128
+  // tiles, two workgroups per CU, spread the work wider.
+  const long cus = cu_count();
   const long tiles = (long)((g.M + 127) / 128) * ((g.N + 255) / 256);
   if (g.fp8) {  // the same tiles; a 128-wide FP8 slice fills the bytes of a 64-wide bf16 one
-    if (tiles >= 256) return launch_cfg<Cfg<128, 256, 128, 3, 2, 4, 2, 1>>(g, s);
+    if (tiles >= cus) return launch_cfg<Cfg<128, 256, 128, 3, 2, 4, 2, 1>>(g, s);
     return launch_cfg<Cfg<128, 128, 128, 2, 2, 2, 2, 1>>(g, s);
   }
-  if (tiles >= 256) return launch_cfg<Cfg<128, 256, 64, 3, 2, 4, 2>>(g, s);
-  return launch_cfg<Cfg<128, 128, 64, 2, 2, 2, 2>>(g, s);
+  if (tiles < cus) return launch_cfg<Cfg<128, 128, 64, 2, 2, 2, 2>>(g, s);
+  // 256x256 tiles (8 wavefronts of 128x64, 2-stage ring) do a round of work in ~11/6 the
+  // time of a round of 128x256 tiles (measured on the FFN1 shape, launches interleaved):
+  // more efficient per flop, but twice as coarse.  Take them when their whole rounds
+  // cost less, e.g. FFN1 at M = 3152 (702 tiles = 3 rounds against 1350 = 6 rounds of
+  // the smaller tiles) but not QKV (780 tiles = 4 rounds against 1500 = 6).
+  const long tiles256 = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
+  const long rounds128 = (tiles + cus - 1) / cus, rounds256 = (tiles256 + cus - 1) / cus;
+  if (11 * rounds256 < 6 * rounds128) return launch_cfg<Cfg<256, 256, 64, 2, 2, 4, 2>>(g, s);
+  return launch_cfg<Cfg<128, 256, 64, 3, 2, 4, 2>>(g, s);
 }
 
 }  // namespace wam

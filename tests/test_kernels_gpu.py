@@ -79,6 +79,7 @@ GEMM_SHAPES = [
     (3152, 5192, 520),   # big tiles (>= 256 of them), ragged M, N and K
     (17, 16, 16),        # the action embedding's K
     (130, 203, 72),      # N % 4 != 0: the last column group is stored element by element
+    (1000, 10200, 520),  # 256x256 tiles (160 of them beat 320 of 128x256), ragged M, N and K
 ]
 
 
