@@ -489,14 +489,16 @@ hipError_t launch_gemm(const GemmArgs& gin, hipStream_t s) {
     return launch_cfg<Cfg<128, 128, 128, 2, 2, 2, 2, 1>>(g, s);
   }
   if (tiles < cus) return launch_cfg<Cfg<128, 128, 64, 2, 2, 2, 2>>(g, s);
-  // 256x256 tiles (8 wavefronts of 128x64, 2-stage ring) do a round of work in ~11/6 the
-  // time of a round of 128x256 tiles (measured on the FFN1 shape, launches interleaved):
-  // more efficient per flop, but twice as coarse.  Take them when their whole rounds
-  // cost less, e.g. FFN1 at M = 3152 (702 tiles = 3 rounds against 1350 = 6 rounds of
-  // the smaller tiles) but not QKV (780 tiles = 4 rounds against 1500 = 6).
-  const long tiles256 = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
-  const long rounds128 = (tiles + cus - 1) / cus, rounds256 = (tiles256 + cus - 1) / cus;
-  if (11 * rounds256 < 6 * rounds128) return launch_cfg<Cfg<256, 256, 64, 2, 2, 4, 2>>(g, s);
+  // Taller tiles are more efficient per flop but coarser.  Measured with launches
+  // interleaved, a round of 128x256, 192x256 (8 wavefronts of 96x64, 2-stage ring) and
+  // 256x256 tiles (8 wavefronts of 128x64, 2 stages) takes time in the ratio 18 : 26 : 33
+  // for 1 : 1.5 : 2 times the work; take the height whose whole rounds cost least.  At
+  // M = 3152: QKV 1020 tiles of 192 rows in 4 rounds (487 -> 469 us), FFN1 702 of 256 rows
+  // in 3 rounds (480 -> 439 us), O and FFN2 keep 128 rows (500 tiles, 2 rounds).
+  auto rounds = [&](int bm) { return ((long)((g.M + bm - 1) / bm) * ((g.N + 255) / 256) + cus - 1) / cus; };
+  const long c128 = 18 * rounds(128), c192 = 26 * rounds(192), c256 = 33 * rounds(256);
+  if (c256 < c128 && c256 <= c192) return launch_cfg<Cfg<256, 256, 64, 2, 2, 4, 2>>(g, s);
+  if (c192 < c128) return launch_cfg<Cfg<192, 256, 64, 2, 2, 4, 2>>(g, s);
   return launch_cfg<Cfg<128, 256, 64, 3, 2, 4, 2>>(g, s);
 }
 

@@ -76,10 +76,11 @@ def test_rope_qkv_and_cache_append(Dh, H, B, L, c):
 # ----------------------------------------------------------------------------- GEMM epilogues
 GEMM_SHAPES = [
     (300, 200, 136),     # small tiles, ragged M, N and K (K % 64 != 0)
-    (3152, 5192, 520),   # big tiles (>= 256 of them), ragged M, N and K
+    (3152, 5100, 520),   # 128x256 tiles (500 of them, 2 rounds), ragged M, N and K
     (17, 16, 16),        # the action embedding's K
     (130, 203, 72),      # N % 4 != 0: the last column group is stored element by element
-    (1000, 10200, 520),  # 256x256 tiles (160 of them beat 320 of 128x256), ragged M, N and K
+    (1000, 12700, 520),  # 256x256 tiles (200, one round, beat 300 of 192 rows), ragged M, N and K
+    (570, 15300, 136),   # 192x256 tiles (180 of them beat 300 of 128x256), ragged M, N and K
 ]
 
 
