@@ -98,6 +98,19 @@ def normal(cfg_seed: int, tensor: str, shape, std: float = 1.0, layer: int = 0,
     return Tensor("f32", a)
 
 
+def device_normal(cfg_seed: int, tensor: str, shape, std: float = 1.0, layer: int = 0):
+    """N(0, std^2) bf16 drawn on the GPU from a seeded stream (torch's generator seeded
+    from SeedSequence([cfg_seed, tensor_id, layer])), for inputs too large to draw on
+    the host in a test's time (a 65744-key cache is 337M values per sample).  Both sides
+    read the same device tensor: the oracle gets its host copy."""
+    import torch
+    seed = int(np.random.SeedSequence([int(cfg_seed), TENSOR_IDS[tensor], int(layer)]).generate_state(1,
+                                                                                                   np.uint64)[0])
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed & 0x7FFFFFFFFFFFFFFF)
+    return (torch.randn(shape, generator=g, device="cuda", dtype=torch.float32) * std).to(torch.bfloat16)
+
+
 def zeros(shape, dtype: str = "f32") -> Tensor:
     if dtype == "bf16":
         return Tensor("bf16", np.zeros(shape, np.uint16))

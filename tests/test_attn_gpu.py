@@ -181,3 +181,30 @@ def test_attention_full_size_masked_three_chunks():
     kc = np.repeat([0, 1, 2], L)
     ref = oracle.attention(q.f64[0, rows], k.f64[0], v.f64[0], kc[rows], kc)
     assert rel_l2(o[0, rows], ref) <= TOL
+
+
+def test_attention_b2_3view_sampled_rows():
+    """The two-sample, three-view configuration at full shape: batch 2, 9392 queries
+    (2 frames x 30 x 156 patches + 32 actions) of chunk 6 against 65744 keys (six cached
+    chunks plus the chunk), 40 heads of 128.  Inputs are drawn on the device from seeded
+    streams (the host generator would take minutes at this size); the fp64 oracle runs on
+    sampled query rows of both samples, every head, against all keys."""
+    import torch
+    wl = synth.WORKLOADS["step_14b_b2_3view"]
+    w = lib()
+    B, H, Dh, L, Lk = wl.B, wl.H, wl.Dh, wl.L, wl.Lk
+    log(f"attn b2 3-view B={B} Lq={L} Lk={Lk}: inputs")
+    q = synth.device_normal(wl.seed, "q", (B, L, H, Dh))
+    k = synth.device_normal(wl.seed, "k", (B, Lk, H, Dh))
+    v = synth.device_normal(wl.seed, "v", (B, Lk, H, Dh))
+    log("attn b2 3-view: GPU")
+    o = run(q, k, v, w.cached_chunks(wl.cache_rows, L))
+    rows = sampled_rows([(0, L)], [127, 128, 9215, 9216], 20, np.random.default_rng(4))
+    kc = np.repeat(np.arange(wl.n_cached + 1), L)
+    for b in range(B):
+        log(f"attn b2 3-view: oracle, sample {b}")
+        ref = oracle.attention(host(q[b, rows]), host(k[b]), host(v[b]), np.full(len(rows), wl.n_cached), kc)
+        err = rel_l2(host(o[b, rows]), ref)
+        print(f"  sample {b}: {len(rows)} rows, rel L2 {err:.2e}", flush=True)
+        assert err <= TOL
+        torch.cuda.synchronize()
