@@ -484,21 +484,28 @@ hipError_t launch_gemm(const GemmArgs& gin, hipStream_t s) {
   // tiles, two workgroups per CU, spread the work wider.
   const long cus = cu_count();
   const long tiles = (long)((g.M + 127) / 128) * ((g.N + 255) / 256);
-  if (g.fp8) {  // the same tiles; a 128-wide FP8 slice fills the bytes of a 64-wide bf16 one
-    if (tiles >= cus) return launch_cfg<Cfg<128, 256, 128, 3, 2, 4, 2, 1>>(g, s);
-    return launch_cfg<Cfg<128, 128, 128, 2, 2, 2, 2, 1>>(g, s);
+  if (tiles < cus) {
+    if (g.fp8) return launch_cfg<Cfg<128, 128, 128, 2, 2, 2, 2, 1>>(g, s);
+    return launch_cfg<Cfg<128, 128, 64, 2, 2, 2, 2>>(g, s);
   }
-  if (tiles < cus) return launch_cfg<Cfg<128, 128, 64, 2, 2, 2, 2>>(g, s);
   // Taller tiles are more efficient per flop but coarser.  Measured with launches
   // interleaved, a round of 128x256, 192x256 (8 wavefronts of 96x64, 2-stage ring) and
   // 256x256 tiles (8 wavefronts of 128x64, 2 stages) takes time in the ratio 18 : 26 : 33
   // for 1 : 1.5 : 2 times the work; take the height whose whole rounds cost least.  At
   // M = 3152: QKV 1020 tiles of 192 rows in 4 rounds (487 -> 469 us), FFN1 702 of 256 rows
   // in 3 rounds (480 -> 439 us), O and FFN2 keep 128 rows (500 tiles, 2 rounds).
+  // FP8 takes the same tiles with 128-wide slices (the bytes of a 64-wide bf16 slice).
   auto rounds = [&](int bm) { return ((long)((g.M + bm - 1) / bm) * ((g.N + 255) / 256) + cus - 1) / cus; };
   const long c128 = 18 * rounds(128), c192 = 26 * rounds(192), c256 = 33 * rounds(256);
-  if (c256 < c128 && c256 <= c192) return launch_cfg<Cfg<256, 256, 64, 2, 2, 4, 2>>(g, s);
-  if (c192 < c128) return launch_cfg<Cfg<192, 256, 64, 2, 2, 4, 2>>(g, s);
+  if (c256 < c128 && c256 <= c192) {
+    if (g.fp8) return launch_cfg<Cfg<256, 256, 128, 2, 2, 4, 2, 1>>(g, s);
+    return launch_cfg<Cfg<256, 256, 64, 2, 2, 4, 2>>(g, s);
+  }
+  if (c192 < c128) {
+    if (g.fp8) return launch_cfg<Cfg<192, 256, 128, 2, 2, 4, 2, 1>>(g, s);
+    return launch_cfg<Cfg<192, 256, 64, 2, 2, 4, 2>>(g, s);
+  }
+  if (g.fp8) return launch_cfg<Cfg<128, 256, 128, 3, 2, 4, 2, 1>>(g, s);
   return launch_cfg<Cfg<128, 256, 64, 3, 2, 4, 2>>(g, s);
 }
 
