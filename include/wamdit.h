@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define WAM_ABI_VERSION 3
+#define WAM_ABI_VERSION 4
 #define WAM_MAX_CHUNKS 16
 
 typedef enum {
@@ -327,7 +327,7 @@ typedef struct {
   int32_t cache_window;   /* similarity > cache_tau with the previous computed one, the next */
                           /* cache_window steps reuse it; cache_window = 0: caching off     */
   float* x;               /* device fp32 state [nx][n_video + n_action]: noise in, x_N out */
-  int32_t* computed;      /* optional HOST [N]: 1 where step i called the network           */
+  int32_t* computed;      /* optional DEVICE [N] int32: 1 where step i called the network    */
 } wam_denoise_params;
 
 /* wam_denoise_chunk — the N-step denoising loop of one chunk: per step, the network
@@ -338,10 +338,12 @@ typedef struct {
  * step alike, so when io->ctx_kv is NULL the loop projects the text and each block's
  * cross-attention K|V once, before the first step, into its workspace (n_layers * B *
  * Lc * 2d bf16 more) and every step reads them; results are those of independent
- * steps.  With caching off the loop never synchronizes (it can be captured in a graph);
- * with caching on it synchronizes the stream once per computed step after the first to
- * read the similarity.  Same validation and errors as wam_dit_step_fwd, plus the loop's
- * own parameters. */
+ * steps.  DiT caching is decided on the device: after each computed step the cosine
+ * similarity of its velocity with the previous computed one is reduced on the GPU, and a
+ * reused step's kernels read that decision from the workspace and return at entry.  The
+ * loop never synchronizes or allocates, so a caller can capture a whole call in a graph
+ * (the schedule t_sched is read on the host when the call is made, or captured).  Same
+ * validation and errors as wam_dit_step_fwd, plus the loop's own parameters. */
 size_t wam_denoise_workspace_bytes(const wam_model* m, const wam_step_io* io,
                                    const wam_denoise_params* p);
 wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wam_denoise_params* p,

@@ -471,14 +471,17 @@ def wam_cosine_similarity(a, b, out, ws, stream=None):
 
 
 def make_denoise_params(t_sched, x, cfg=False, cfg_scale=1.0, cache_tau=0.0, cache_window=0):
-    """Host-side loop parameters; t_sched a float sequence of N+1 times, x the device state."""
+    """Loop parameters; t_sched a float sequence of N+1 times (kept on the host), x the
+    device state.  `p.computed` is a device int32 [N] tensor the loop fills with 1 where a
+    step called the network (read it after the stream has finished)."""
     import numpy as np
+    import torch
     t = np.ascontiguousarray(np.asarray(t_sched, dtype=np.float32))
     n = len(t) - 1
-    computed = np.zeros(n, np.int32)
+    computed = torch.zeros(n, dtype=torch.int32, device=x.device)
     p = wam_denoise_params(n_steps=n, t_sched=t.ctypes.data_as(_fp), cfg=int(cfg), cfg_scale=cfg_scale,
                            cache_tau=cache_tau, cache_window=cache_window, x=_p(x),
-                           computed=computed.ctypes.data_as(C.POINTER(_i32)))
+                           computed=C.cast(C.c_void_p(computed.data_ptr()), C.POINTER(_i32)))
     p._keep = (t, computed)
     p.computed_steps = computed
     return p

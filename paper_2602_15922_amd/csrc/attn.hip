@@ -204,6 +204,7 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd(const AttnArgs a, int nqt) {
   constexpr int KCH = BN * CPR / NT;  // 16-byte chunks of K (and of V) per thread
   constexpr int TILE = 2 * BN * DH;   // K tile + V tile, elements
   __shared__ __attribute__((aligned(16))) bf16 smem[2 * TILE];
+  if (skip_step(a.skip)) return;
 
   // XCD-aware mapping: give each XCD a contiguous range of (q-tile, head) pairs so
   // the workgroups sharing a head's K/V share an L2.

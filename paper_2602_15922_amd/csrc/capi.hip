@@ -18,6 +18,20 @@ namespace {
 
 thread_local std::string g_err;
 
+// Inside the denoising loop with DiT caching, every kernel of a step is launched with
+// the loop's device flag (a reused step's kernels return at entry; the decision stays
+// on the device).  Set by SkipScope around one step; NULL everywhere else.
+thread_local const int32_t* t_skip = nullptr;
+struct SkipScope {
+  explicit SkipScope(const int32_t* f) { t_skip = f; }
+  ~SkipScope() { t_skip = nullptr; }
+};
+template <class Args>
+const Args& pred(Args& a) {
+  a.skip = t_skip;
+  return a;
+}
+
 wam_status fail(wam_status st, const char* fmt, ...) {
   char buf[512];
   va_list ap;
@@ -132,7 +146,7 @@ wam_status attn_checked(const wam_attn_desc& d, const void* q, const void* k, co
   a.n_k_chunks = d.ch.n_k_chunks;
   a.n_q_chunks = d.ch.n_q_chunks;
   for (int i = 0; i <= d.ch.n_q_chunks; ++i) a.q_off[i] = d.ch.q_off[i];
-  HIPCHECK(launch_attn(a, s));
+  HIPCHECK(launch_attn(pred(a), s));
   return WAM_OK;
 }
 
@@ -190,7 +204,7 @@ wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s, int32_t gate_spli
   a.gate_a = g.gate_a; a.gate_v = g.gate_v; a.gate_stride = g.gate_stride; a.gate_rows = g.gate_rows;
   a.gate_split = gate_split; a.gate_alt = gate_alt;
   a.fp8 = fp8 ? 1 : 0; a.a_scale = a_scale; a.w_scale = w_scale;
-  HIPCHECK(launch_gemm(a, s));
+  HIPCHECK(launch_gemm(pred(a), s));
   return WAM_OK;
 }
 
@@ -232,7 +246,7 @@ wam_status proj(const wam_gemm_desc& g0, const void* w8, const float* s8, char* 
                 int32_t gate_split = 0, int64_t gate_alt = 0) {
   if (!w8) return gemm_checked(g0, s, gate_split, gate_alt);
   const int64_t ldq = (g0.K + 15) / 16 * 16;
-  HIPCHECK(launch_quant_rows(g0.M, g0.K, g0.A, g0.lda, q8, ldq, qs, s));
+  HIPCHECK(launch_quant_rows(g0.M, g0.K, g0.A, g0.lda, q8, ldq, qs, s, t_skip));
   wam_gemm_desc g = g0;
   g.A = q8; g.lda = ldq; g.a_rows = 0; g.a_batch_stride = 0;
   g.W = w8; g.ldw = g0.K;
@@ -301,13 +315,13 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
 
   // 1. AdaLN: h = LN(x)(1 + scale1) + shift1
   LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h, seg, alt};
-  HIPCHECK(launch_ln_mod(ln, s));
+  HIPCHECK(launch_ln_mod(pred(ln), s));
   // 2. fused QKV projection
   TRY(proj(gemm(M, 3 * d, d, WAM_EPI_BF16, h, d, W.w_qkv, W.b_qkv, big, 3 * d), F8 ? F8->w_qkv : nullptr,
            F8 ? F8->s_qkv : nullptr, q8, qs, s));
   // 3. RoPE on q, k; k, v appended to the cache rows of this chunk
   RopeArgs ra{B, L, D.H, D.Dh, io.Lcap, io.cache_len, big, io.rope_cos, io.rope_sin, q, io.k_cache, io.v_cache};
-  HIPCHECK(launch_rope_qkv(ra, s));
+  HIPCHECK(launch_rope_qkv(pred(ra), s));
   // 4. block-causal self-attention over cache rows [0, cache_len + L)
   wam_attn_desc ad{};
   ad.B = B; ad.H = D.H; ad.Dh = D.Dh; ad.Lq = L; ad.Lk = io.cache_len + L;
@@ -326,7 +340,7 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   }
   // 6. cross-attention LayerNorm (affine, no modulation)
   LnArgs lc{M, L, d, D.eps, io.x, W.lnc_gamma, W.lnc_beta, nullptr, nullptr, nullptr, nullptr, 0, h};
-  HIPCHECK(launch_ln_mod(lc, s));
+  HIPCHECK(launch_ln_mod(pred(lc), s));
   // 7. cross query
   TRY(proj(gemm(M, d, d, WAM_EPI_BF16, h, d, W.w_cq, W.b_cq, q, d), F8 ? F8->w_cq : nullptr,
            F8 ? F8->s_cq : nullptr, q8, qs, s));
@@ -350,7 +364,7 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
            F8 ? F8->s_co : nullptr, q8, qs, s));
   // 11. AdaLN #2
   LnArgs l2{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 3 * d, e0 + 3 * d, m6 + 4 * d, e0 + 4 * d, ms, h, seg, alt};
-  HIPCHECK(launch_ln_mod(l2, s));
+  HIPCHECK(launch_ln_mod(pred(l2), s));
   // 12. FFN up-projection with tanh-GELU
   TRY(proj(gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, big, D.ffn), F8 ? F8->w_f1 : nullptr,
            F8 ? F8->s_f1 : nullptr, q8, qs, s));
@@ -375,7 +389,7 @@ wam_status block_kv_run(const wam_dims& D, const wam_block_weights& W, const wam
   const float* e0 = io.e0;
   const int64_t ms = 6 * (int64_t)d;
   LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h, seg, alt};
-  HIPCHECK(launch_ln_mod(ln, s));
+  HIPCHECK(launch_ln_mod(pred(ln), s));
   // rows d..3d of W_qkv (the k and v outputs) into columns d..3d of the [M][3d] buffer
   const wam_block_fp8* F8 = W.fp8;
   const char* wkv = F8 ? nullptr : static_cast<const char*>(W.w_qkv) + (size_t)d * d * 2;
@@ -385,7 +399,7 @@ wam_status block_kv_run(const wam_dims& D, const wam_block_weights& W, const wam
            ws + lay.q8, reinterpret_cast<float*>(ws + lay.qs), s));
   RopeArgs ra{B, L, D.H, D.Dh, io.Lcap, io.cache_len, big, io.rope_cos, io.rope_sin, nullptr, io.k_cache,
               io.v_cache};
-  HIPCHECK(launch_rope_qkv(ra, s));
+  HIPCHECK(launch_rope_qkv(pred(ra), s));
   return WAM_OK;
 }
 
@@ -411,10 +425,10 @@ wam_status time_run(const wam_model& m, int32_t B, const float* t, float* e, flo
   const wam_dims& D = m.dims;
   float* sinus = reinterpret_cast<float*>(ws);
   float* hid = sinus + (size_t)B * D.freq_dim;
-  HIPCHECK(launch_sinusoid(B, D.freq_dim, t, sinus, s));
-  HIPCHECK(launch_gemv(B, D.d, D.freq_dim, sinus, GEMV_ACT_NONE, m.w_t1, m.b_t1, hid, s));
-  HIPCHECK(launch_gemv(B, D.d, D.d, hid, GEMV_ACT_SILU, m.w_t2, m.b_t2, e, s));
-  HIPCHECK(launch_gemv(B, 6 * D.d, D.d, e, GEMV_ACT_SILU, m.w_t6, m.b_t6, e0, s));
+  HIPCHECK(launch_sinusoid(B, D.freq_dim, t, sinus, s, t_skip));
+  HIPCHECK(launch_gemv(B, D.d, D.freq_dim, sinus, GEMV_ACT_NONE, m.w_t1, m.b_t1, hid, s, t_skip));
+  HIPCHECK(launch_gemv(B, D.d, D.d, hid, GEMV_ACT_SILU, m.w_t2, m.b_t2, e, s, t_skip));
+  HIPCHECK(launch_gemv(B, 6 * D.d, D.d, e, GEMV_ACT_SILU, m.w_t6, m.b_t6, e0, s, t_skip));
   return WAM_OK;
 }
 
@@ -436,7 +450,7 @@ wam_status embed_run(const wam_model& m, int32_t B, int32_t F, int32_t Hl, int32
                      const void* a, float* x, char* ws, hipStream_t s) {
   const wam_dims& D = m.dims;
   const int P = D.latent_ch * 4, Lv = F * (Hl / 2) * (Wl / 2), L = Lv + A;
-  HIPCHECK(launch_patchify(B, D.latent_ch, F, Hl, Wl, z, ws, s));
+  HIPCHECK(launch_patchify(B, D.latent_ch, F, Hl, Wl, z, ws, s, t_skip));
   wam_gemm_desc g = gemm(B * Lv, D.d, P, WAM_EPI_F32, ws, P, m.w_patch, m.b_patch, x, D.d);
   g.out_rows = Lv; g.out_batch_stride = (int64_t)L * D.d;
   TRY(gemm_checked(g, s));
@@ -471,11 +485,11 @@ wam_status head_run(const wam_model& m, int32_t B, int32_t F, int32_t Hl, int32_
   float* tok = reinterpret_cast<float*>(ws + lay.tok);
   LnArgs ln{B * L, L, d, D.eps, x, nullptr, nullptr, m.head_mod2, e, m.head_mod2 + d, e, d, h,
             e_alt ? Lv : 0, e_alt};
-  HIPCHECK(launch_ln_mod(ln, s));
+  HIPCHECK(launch_ln_mod(pred(ln), s));
   wam_gemm_desc gv = gemm(B * Lv, P, d, WAM_EPI_F32, h, d, m.w_hv, m.b_hv, tok, P);
   gv.a_rows = Lv; gv.a_batch_stride = (int64_t)L * d;
   TRY(gemm_checked(gv, s));
-  HIPCHECK(launch_unpatchify(B, D.latent_ch, F, Hl, Wl, tok, v_video, s));
+  HIPCHECK(launch_unpatchify(B, D.latent_ch, F, Hl, Wl, tok, v_video, s, t_skip));
   if (A > 0) {
     wam_gemm_desc ga = gemm(B * A, D.act_dim, d, WAM_EPI_F32, h + (size_t)Lv * d * 2, d, m.w_ha, m.b_ha,
                             v_action, D.act_dim);
@@ -610,7 +624,7 @@ FlowArgs flow_args(const wam_flow_dims& d) {
 }
 
 struct DenoiseWs {
-  size_t step, va, vb, cos, cos_out, kv, kv_layer, total;
+  size_t step, va, vb, cos, cos_out, state, kv, kv_layer, total;
 };
 DenoiseWs denoise_ws(const wam_model& m, const wam_step_io& io, const wam_denoise_params& p) {
   const int64_t nx = p.cfg ? 1 : io.B;
@@ -622,6 +636,7 @@ DenoiseWs denoise_ws(const wam_model& m, const wam_step_io& io, const wam_denois
   w.vb = off; off += align256((size_t)nx * n * 4);
   w.cos = off; off += align256(cosine_workspace_bytes());
   w.cos_out = off; off += 256;
+  w.state = off; off += 256;
   // the text's cross K|V of every block, computed once per chunk (unless supplied)
   w.kv_layer = io.ctx_kv ? 0 : align256((size_t)io.B * io.Lc * 2 * m.dims.d * 2);
   w.kv = off; off += (size_t)std::max(m.dims.n_layers, 0) * w.kv_layer;
@@ -896,8 +911,11 @@ wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wa
   const DenoiseWs lay = denoise_ws(*m, *io, *p);
   TRY(check_ws(ws, ws_bytes, lay.total));
   char* w = static_cast<char*>(ws);
-  float* vbuf[2] = {reinterpret_cast<float*>(w + lay.va), reinterpret_cast<float*>(w + lay.vb)};
+  // vcur: the latest computed velocity (what a reused step applies), vprev: the one before
+  float* vcur = reinterpret_cast<float*>(w + lay.va);
+  float* vprev = reinterpret_cast<float*>(w + lay.vb);
   float* cs_dev = reinterpret_cast<float*>(w + lay.cos_out);
+  int32_t* st = reinterpret_cast<int32_t*>(w + lay.state);
   void* z = const_cast<void*>(io->z_t);
   void* a = const_cast<void*>(io->a_t);
   float* t_dev = const_cast<float*>(io->t);
@@ -935,33 +953,27 @@ wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wa
   FlowArgs q = flow_args(fd);
   q.x = p->x; q.z_next = z; q.a_next = a;
   HIPCHECK(launch_flow_step(q, stream));
-  int last = -1, before = -1;  // slots of the latest and the previous computed velocity
-  int skip = 0;
+  // With caching the reuse decision lives in st on the device: a reused step's kernels
+  // return at entry, the solver step applies vcur, and nothing waits for the host.
+  if (caching || p->computed) HIPCHECK(launch_loop_init(st, stream));
   for (int i = 0; i < p->n_steps; ++i) {
+    HIPCHECK(launch_fill(t_dev, io->B, p->t_sched[i], stream));
+    {
+      SkipScope scope(caching ? st : nullptr);
+      TRY(step_run(*m, sio, w + lay.step, stream));
+    }
     FlowArgs f = flow_args(fd);
     f.dt = p->t_sched[i + 1] - p->t_sched[i];
     f.x = p->x; f.z_next = z; f.a_next = a;
-    if (skip > 0) {
-      f.v_in = vbuf[last];
-      HIPCHECK(launch_flow_step(f, stream));
-      --skip;
-      if (p->computed) p->computed[i] = 0;
-      continue;
+    f.v_video = io->v_video; f.v_action = io->v_action;
+    if (caching) {
+      f.v_in = vcur; f.v_out = vcur; f.skip = st;
     }
-    HIPCHECK(launch_fill(t_dev, io->B, p->t_sched[i], stream));
-    TRY(step_run(*m, sio, w + lay.step, stream));
-    before = last;
-    last = before == 0 ? 1 : 0;
-    f.v_video = io->v_video; f.v_action = io->v_action; f.v_out = vbuf[last];
     HIPCHECK(launch_flow_step(f, stream));
-    if (p->computed) p->computed[i] = 1;
-    if (caching && before >= 0) {
-      HIPCHECK(launch_cosine(vbuf[last], vbuf[before], n, w + lay.cos, cs_dev, stream));
-      float cs = 0.f;
-      HIPCHECK(hipMemcpyAsync(&cs, cs_dev, sizeof(float), hipMemcpyDeviceToHost, stream));
-      HIPCHECK(hipStreamSynchronize(stream));
-      if (cs > p->cache_tau) skip = p->cache_window;
-    }
+    if (caching) HIPCHECK(launch_cosine(vcur, vprev, n, w + lay.cos, cs_dev, stream, st));
+    if (caching || p->computed)
+      HIPCHECK(launch_loop_decide(st, cs_dev, p->cache_tau, p->cache_window, p->computed, i, stream));
+    if (caching) HIPCHECK(launch_copy_if(st + 2, vcur, vprev, n, stream));
   }
   return WAM_OK;
 }

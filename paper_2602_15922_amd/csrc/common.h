@@ -31,6 +31,10 @@ WAM_DEV f32x16 mfma32_fp8(i32x8 a, i32x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
 }
 
+// The denoising loop launches a step's kernels with a device flag: while it is > 0 the
+// step reuses an earlier velocity and every workgroup returns at entry.
+WAM_DEV bool skip_step(const int32_t* skip) { return skip != nullptr && *skip > 0; }
+
 WAM_DEV float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
 WAM_DEV bf16x8 load_bf16x8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }

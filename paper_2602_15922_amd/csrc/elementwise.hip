@@ -28,6 +28,7 @@ template <int NV>
 __global__ __launch_bounds__(LN_ROWS * 64, NV <= 20 ? 4 : 2) void ln_mod_kernel(const LnArgs a, int blocks_per_batch, int seg,
                                                               int seg_blocks) {
   extern __shared__ __attribute__((aligned(16))) float PQ[];  // [2][d]
+  if (skip_step(a.skip)) return;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int b = blockIdx.x / blocks_per_batch, j = blockIdx.x % blocks_per_batch;
   // a workgroup's rows lie in one segment: [0, seg) or [seg, rows_per_batch)
@@ -101,10 +102,10 @@ __global__ __launch_bounds__(LN_ROWS * 64, NV <= 20 ? 4 : 2) void ln_mod_kernel(
 // ---------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void quant_rows_kernel(int M, int K, const bf16* __restrict__ x, int64_t ldx,
                                                          uint8_t* __restrict__ q, int64_t ldq,
-                                                         float* __restrict__ scale) {
+                                                         float* __restrict__ scale, const int32_t* skip) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + w;
-  if (row >= M) return;
+  if (row >= M || skip_step(skip)) return;
   const bf16* xr = x + (int64_t)row * ldx;
   float amax = 0.f;
   for (int k = lane * 8; k < K; k += 512) {
@@ -139,7 +140,7 @@ __global__ __launch_bounds__(256) void quant_rows_kernel(int M, int K, const bf1
 __global__ __launch_bounds__(256) void rope_qkv_kernel(const RopeArgs a) {
   const int d = a.H * a.Dh, d8 = d >> 3;
   const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (id >= (int64_t)a.B * a.L * d8) return;
+  if (id >= (int64_t)a.B * a.L * d8 || skip_step(a.skip)) return;
   const int c = (int)(id % d8);
   const int64_t bl = id / d8;
   const int l = (int)(bl % a.L), b = (int)(bl / a.L);
@@ -174,10 +175,11 @@ constexpr int GEMV_MAXB = 8;
 
 __global__ __launch_bounds__(256) void gemv_kernel(int B, int N, int K, const float* __restrict__ x,
                                                    int act, const bf16* __restrict__ W,
-                                                   const float* __restrict__ bias, float* __restrict__ out) {
+                                                   const float* __restrict__ bias, float* __restrict__ out,
+                                                   const int32_t* skip) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int n = blockIdx.x * 4 + w;
-  if (n >= N) return;
+  if (n >= N || skip_step(skip)) return;
   float acc[GEMV_MAXB];
 #pragma unroll
   for (int b = 0; b < GEMV_MAXB; ++b) acc[b] = 0.f;
@@ -206,9 +208,9 @@ __global__ __launch_bounds__(256) void gemv_kernel(int B, int N, int K, const fl
 
 // [cos(1000 t w_k), sin(1000 t w_k)], w_k = 10000^(-k/half); evaluated in double so the
 // large arguments (up to 1000 rad) keep full fp32 accuracy.
-__global__ void sinusoid_kernel(int B, int fd, const float* t, float* out) {
+__global__ void sinusoid_kernel(int B, int fd, const float* t, float* out, const int32_t* skip) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= B * fd) return;
+  if (i >= B * fd || skip_step(skip)) return;
   const int b = i / fd, k = i % fd, half = fd / 2;
   const int kk = k < half ? k : k - half;
   const double omega = pow(10000.0, -(double)kk / (double)half);
@@ -217,11 +219,12 @@ __global__ void sinusoid_kernel(int B, int fd, const float* t, float* out) {
 }
 
 // token (f, r, s) feature (c, ph, pw) <- z[b][c][f][2r+ph][2s+pw]
-__global__ void patchify_kernel(int B, int C, int F, int Hl, int Wl, const bf16* z, bf16* tok) {
+__global__ void patchify_kernel(int B, int C, int F, int Hl, int Wl, const bf16* z, bf16* tok,
+                                const int32_t* skip) {
   const int Hg = Hl / 2, Wg = Wl / 2, P = C * 4;
   const int64_t n = (int64_t)B * F * Hg * Wg * P;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
+  if (i >= n || skip_step(skip)) return;
   const int fe = (int)(i % P);
   int64_t t = i / P;
   const int s = (int)(t % Wg); t /= Wg;
@@ -232,11 +235,12 @@ __global__ void patchify_kernel(int B, int C, int F, int Hl, int Wl, const bf16*
   tok[i] = z[((((int64_t)b * C + c) * F + f) * Hl + 2 * r + ph) * Wl + 2 * s + pw];
 }
 
-__global__ void unpatchify_kernel(int B, int C, int F, int Hl, int Wl, const float* tok, float* out) {
+__global__ void unpatchify_kernel(int B, int C, int F, int Hl, int Wl, const float* tok, float* out,
+                                  const int32_t* skip) {
   const int Hg = Hl / 2, Wg = Wl / 2;
   const int64_t n = (int64_t)B * C * F * Hl * Wl;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
+  if (i >= n || skip_step(skip)) return;
   int64_t t = i;
   const int xw = (int)(t % Wl); t /= Wl;
   const int y = (int)(t % Hl); t /= Hl;
@@ -266,10 +270,10 @@ hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_quant_rows(int32_t M, int32_t K, const void* x, int64_t ldx, void* q, int64_t ldq, float* scale,
-                             hipStream_t s) {
+                             hipStream_t s, const int32_t* skip) {
   if (M == 0) return hipSuccess;
   hipLaunchKernelGGL(quant_rows_kernel, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, s, M, K,
-                     static_cast<const bf16*>(x), ldx, static_cast<uint8_t*>(q), ldq, scale);
+                     static_cast<const bf16*>(x), ldx, static_cast<uint8_t*>(q), ldq, scale, skip);
   return hipGetLastError();
 }
 
@@ -281,30 +285,30 @@ hipError_t launch_rope_qkv(const RopeArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_gemv(int32_t B, int32_t N, int32_t K, const float* x, int32_t act, const void* W,
-                       const float* bias, float* out, hipStream_t s) {
+                       const float* bias, float* out, hipStream_t s, const int32_t* skip) {
   hipLaunchKernelGGL(gemv_kernel, dim3((N + 3) / 4), dim3(256), 0, s, B, N, K, x, act,
-                     static_cast<const bf16*>(W), bias, out);
+                     static_cast<const bf16*>(W), bias, out, skip);
   return hipGetLastError();
 }
 
-hipError_t launch_sinusoid(int32_t B, int32_t fd, const float* t, float* out, hipStream_t s) {
-  hipLaunchKernelGGL(sinusoid_kernel, dim3((B * fd + 255) / 256), dim3(256), 0, s, B, fd, t, out);
+hipError_t launch_sinusoid(int32_t B, int32_t fd, const float* t, float* out, hipStream_t s, const int32_t* skip) {
+  hipLaunchKernelGGL(sinusoid_kernel, dim3((B * fd + 255) / 256), dim3(256), 0, s, B, fd, t, out, skip);
   return hipGetLastError();
 }
 
 hipError_t launch_patchify(int32_t B, int32_t C, int32_t F, int32_t Hl, int32_t Wl, const void* z,
-                           void* tok, hipStream_t s) {
+                           void* tok, hipStream_t s, const int32_t* skip) {
   const int64_t n = (int64_t)B * F * (Hl / 2) * (Wl / 2) * C * 4;
   hipLaunchKernelGGL(patchify_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, B, C, F,
-                     Hl, Wl, static_cast<const bf16*>(z), static_cast<bf16*>(tok));
+                     Hl, Wl, static_cast<const bf16*>(z), static_cast<bf16*>(tok), skip);
   return hipGetLastError();
 }
 
 hipError_t launch_unpatchify(int32_t B, int32_t C, int32_t F, int32_t Hl, int32_t Wl, const float* tok,
-                             float* out, hipStream_t s) {
+                             float* out, hipStream_t s, const int32_t* skip) {
   const int64_t n = (int64_t)B * C * F * Hl * Wl;
   hipLaunchKernelGGL(unpatchify_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, B, C, F,
-                     Hl, Wl, tok, out);
+                     Hl, Wl, tok, out, skip);
   return hipGetLastError();
 }
 

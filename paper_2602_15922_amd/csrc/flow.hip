@@ -10,8 +10,8 @@ namespace {
 // Element k of the effective velocity of state sample j (k < n_video: the latent,
 // else the action part).  With guidance (state sample 0 from step samples 0 = cond
 // and 1 = uncond): v_u + s (v_c - v_u).
-WAM_DEV float eff_velocity(const FlowArgs& a, int j, int64_t k) {
-  if (a.v_in) return a.v_in[(int64_t)j * (a.n_video + a.n_action) + k];
+WAM_DEV float eff_velocity(const FlowArgs& a, bool reuse, int j, int64_t k) {
+  if (reuse) return a.v_in[(int64_t)j * (a.n_video + a.n_action) + k];
   const bool vid = k < a.n_video;
   const float* base = vid ? a.v_video : a.v_action;
   const int64_t n = vid ? a.n_video : a.n_action;
@@ -29,12 +29,14 @@ __global__ __launch_bounds__(256) void flow_step_kernel(const FlowArgs a) {
   const int64_t n = a.n_video + a.n_action;
   const int nx = a.cfg ? 1 : a.B;
   const int64_t total = (int64_t)nx * n;
+  // with the loop's flag, the velocity is reused while the flag is set
+  const bool reuse = a.skip ? *a.skip > 0 : a.v_in != nullptr;
   for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
     const int j = (int)(e / n);
     const int64_t k = e - (int64_t)j * n;
     float x = a.x[e];
     if (a.v_video || a.v_action || a.v_in) {
-      const float v = eff_velocity(a, j, k);
+      const float v = eff_velocity(a, reuse, j, k);
       if (a.v_out) a.v_out[e] = v;
       x = __builtin_fmaf(a.dt, v, x);
       a.x[e] = x;
@@ -53,7 +55,9 @@ __global__ __launch_bounds__(256) void flow_step_kernel(const FlowArgs a) {
 constexpr int COS_BLOCKS = 512;
 
 __global__ __launch_bounds__(256) void cos_partial_kernel(const float* __restrict__ x, const float* __restrict__ y,
-                                                          int64_t n, double* __restrict__ part) {
+                                                          int64_t n, double* __restrict__ part,
+                                                          const int32_t* skip) {
+  if (skip_step(skip)) return;
   double s[3] = {0.0, 0.0, 0.0};
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)COS_BLOCKS * 256) {
     const double u = x[i], v = y[i];
@@ -72,7 +76,9 @@ __global__ __launch_bounds__(256) void cos_partial_kernel(const float* __restric
   if (threadIdx.x < 3) part[blockIdx.x * 3 + threadIdx.x] = red[threadIdx.x][0];
 }
 
-__global__ __launch_bounds__(256) void cos_final_kernel(const double* __restrict__ part, float* __restrict__ out) {
+__global__ __launch_bounds__(256) void cos_final_kernel(const double* __restrict__ part, float* __restrict__ out,
+                                                        const int32_t* skip) {
+  if (skip_step(skip)) return;
   __shared__ double red[3][256];
   for (int c = 0; c < 3; ++c) {
     double v = 0.0;
@@ -95,6 +101,30 @@ __global__ void fill_kernel(float* p, int n, float v) {
   if ((int)threadIdx.x < n) p[threadIdx.x] = v;
 }
 
+// DiT caching decided on the device (state layout in kernels.h), so the loop needs no
+// host round trip and can be captured in a graph.
+__global__ void loop_init_kernel(int32_t* state) {
+  if (threadIdx.x < 3) state[threadIdx.x] = 0;
+}
+
+__global__ void loop_decide_kernel(int32_t* state, const float* cs, float tau, int32_t window, int32_t* computed,
+                                   int32_t i) {
+  if (threadIdx.x != 0) return;
+  const int32_t left = state[0], done = state[1];
+  const int32_t c = left > 0 ? 0 : 1;
+  if (left > 0) state[0] = left - 1;
+  else if (window > 0 && done >= 1 && cs[0] > tau) state[0] = window;
+  state[1] = done + c;
+  state[2] = c;
+  if (computed) computed[i] = c;
+}
+
+__global__ __launch_bounds__(256) void copy_if_kernel(const int32_t* flag, const float* __restrict__ src,
+                                                      float* __restrict__ dst, int64_t n) {
+  if (*flag == 0) return;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < n; e += (int64_t)gridDim.x * 256) dst[e] = src[e];
+}
+
 }  // namespace
 
 hipError_t launch_flow_step(const FlowArgs& a, hipStream_t s) {
@@ -108,15 +138,35 @@ hipError_t launch_flow_step(const FlowArgs& a, hipStream_t s) {
 
 size_t cosine_workspace_bytes() { return (size_t)COS_BLOCKS * 3 * sizeof(double); }
 
-hipError_t launch_cosine(const float* x, const float* y, int64_t n, void* ws, float* out, hipStream_t s) {
+hipError_t launch_cosine(const float* x, const float* y, int64_t n, void* ws, float* out, hipStream_t s,
+                         const int32_t* skip) {
   double* part = static_cast<double*>(ws);
-  hipLaunchKernelGGL(cos_partial_kernel, dim3(COS_BLOCKS), dim3(256), 0, s, x, y, n, part);
-  hipLaunchKernelGGL(cos_final_kernel, dim3(1), dim3(256), 0, s, part, out);
+  hipLaunchKernelGGL(cos_partial_kernel, dim3(COS_BLOCKS), dim3(256), 0, s, x, y, n, part, skip);
+  hipLaunchKernelGGL(cos_final_kernel, dim3(1), dim3(256), 0, s, part, out, skip);
   return hipGetLastError();
 }
 
 hipError_t launch_fill(float* p, int n, float v, hipStream_t s) {
   hipLaunchKernelGGL(fill_kernel, dim3(1), dim3(64), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_loop_init(int32_t* state, hipStream_t s) {
+  hipLaunchKernelGGL(loop_init_kernel, dim3(1), dim3(64), 0, s, state);
+  return hipGetLastError();
+}
+
+hipError_t launch_loop_decide(int32_t* state, const float* cs, float tau, int32_t window, int32_t* computed,
+                              int32_t i, hipStream_t s) {
+  hipLaunchKernelGGL(loop_decide_kernel, dim3(1), dim3(64), 0, s, state, cs, tau, window, computed, i);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_if(const int32_t* flag, const float* src, float* dst, int64_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int64_t want = (n + 255) / 256;
+  const unsigned grid = (unsigned)(want < 2048 ? want : 2048);
+  hipLaunchKernelGGL(copy_if_kernel, dim3(grid), dim3(256), 0, s, flag, src, dst, n);
   return hipGetLastError();
 }
 

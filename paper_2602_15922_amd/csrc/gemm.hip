@@ -255,6 +255,7 @@ template <typename C, int EPI>
 __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int tiles_m, int tiles_n) {
   constexpr int BM = C::BM, BN = C::BN, BK = C::BK, S = C::STAGES;
   __shared__ __attribute__((aligned(16))) char smem[S * C::STAGE];
+  if (skip_step(g.skip)) return;
 
   // XCD-aware remap: the hardware deals workgroups round-robin over 8 XCDs; give each
   // XCD a contiguous range of tiles so tiles that share a W panel share an L2.

@@ -20,6 +20,8 @@ struct AttnArgs {
   int32_t n_q_chunks;
   int32_t q_off[WAM_MAX_CHUNKS + 1];
   int32_t kend[WAM_MAX_CHUNKS];  // visible key prefix [0, kend) of each query chunk
+  // device flag of the denoising loop: while *skip > 0 every workgroup exits at entry (NULL: never)
+  const int32_t* skip;
 };
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s);
 
@@ -44,6 +46,8 @@ struct GemmArgs {
   // FP8 operands (E4M3 A and W, one byte per element): acc * a_scale[m] * w_scale[n]
   int32_t fp8;
   const float *a_scale, *w_scale;
+  // device flag of the denoising loop: while *skip > 0 every workgroup exits at entry (NULL: never)
+  const int32_t* skip;
 };
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 
@@ -58,6 +62,8 @@ struct LnArgs {
   // per-sample modulation from shift_v / scale_v + alt_off
   int32_t seg_rows;
   int64_t alt_off;
+  // device flag of the denoising loop: while *skip > 0 every workgroup exits at entry (NULL: never)
+  const int32_t* skip;
 };
 hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s);
 
@@ -66,30 +72,34 @@ struct RopeArgs {
   const void* qkv;
   const float *cos_t, *sin_t;
   void *q_out, *k_cache, *v_cache;  // q_out NULL: q is neither rotated nor stored
+  // device flag of the denoising loop: while *skip > 0 every workgroup exits at entry (NULL: never)
+  const int32_t* skip;
 };
 hipError_t launch_rope_qkv(const RopeArgs& a, hipStream_t s);
 
 // out[b][n] = act(x[b][:]) . W[n][:] + bias[n]  (fp32 in/out, bf16 W [N][K])
 enum { GEMV_ACT_NONE = 0, GEMV_ACT_SILU = 1 };
 hipError_t launch_gemv(int32_t B, int32_t N, int32_t K, const float* x, int32_t act,
-                       const void* W, const float* bias, float* out, hipStream_t s);
+                       const void* W, const float* bias, float* out, hipStream_t s, const int32_t* skip = nullptr);
 // [B][freq_dim] sinusoid of 1000*t
-hipError_t launch_sinusoid(int32_t B, int32_t freq_dim, const float* t, float* out, hipStream_t s);
+hipError_t launch_sinusoid(int32_t B, int32_t freq_dim, const float* t, float* out, hipStream_t s,
+                           const int32_t* skip = nullptr);
 // latent [B][C][F][Hl][Wl] bf16 -> tokens [B][F*Hg*Wg][C*4] bf16
 hipError_t launch_patchify(int32_t B, int32_t C, int32_t F, int32_t Hl, int32_t Wl,
-                           const void* z, void* tok, hipStream_t s);
+                           const void* z, void* tok, hipStream_t s, const int32_t* skip = nullptr);
 // tokens [B][Lv][C*4] fp32 -> video [B][C][F][Hl][Wl] fp32
 hipError_t launch_unpatchify(int32_t B, int32_t C, int32_t F, int32_t Hl, int32_t Wl,
-                             const float* tok, float* out, hipStream_t s);
+                             const float* tok, float* out, hipStream_t s, const int32_t* skip = nullptr);
 
 // Per-row E4M3 quantization of bf16 rows [M][K] (K % 8 == 0): q [M][ldq] bytes, scale [M].
 hipError_t launch_quant_rows(int32_t M, int32_t K, const void* x, int64_t ldx, void* q, int64_t ldq, float* scale,
-                             hipStream_t s);
+                             hipStream_t s, const int32_t* skip = nullptr);
 
 // Solver step of the denoising loop over one chunk.  State x [nx][n_video + n_action]
 // fp32 (nx = 1 with guidance, else B); velocity from the step outputs v_video [B][n_video]
 // and v_action [B][n_action] (guidance: sample 0 cond, 1 uncond) or directly from v_in
-// [nx][n]; both NULL: x unchanged.  v_out (optional) receives the effective velocity;
+// [nx][n]; both NULL: x unchanged.  With skip set, the device flag chooses: v_in while
+// *skip > 0, else the step outputs.  v_out (optional) receives the effective velocity;
 // z_next [B][n_video] / a_next [B][n_action] bf16 receive round(x) for every step sample.
 struct FlowArgs {
   int32_t B, cfg;
@@ -98,12 +108,25 @@ struct FlowArgs {
   const float *v_video, *v_action, *v_in;
   float *x, *v_out;
   void *z_next, *a_next;
+  const int32_t* skip;
 };
 hipError_t launch_flow_step(const FlowArgs& a, hipStream_t s);
 // cosine similarity of x and y (n floats) into out[0]; ws of cosine_workspace_bytes()
 size_t cosine_workspace_bytes();
-hipError_t launch_cosine(const float* x, const float* y, int64_t n, void* ws, float* out, hipStream_t s);
+hipError_t launch_cosine(const float* x, const float* y, int64_t n, void* ws, float* out, hipStream_t s,
+                         const int32_t* skip = nullptr);
 // p[0..n) = v for n <= 64
 hipError_t launch_fill(float* p, int n, float v, hipStream_t s);
+
+// The loop's DiT-caching state on the device, three int32: [0] steps still to reuse
+// (the flag every kernel of a step reads), [1] computed steps so far, [2] 1 if the
+// latest step was computed.  init zeroes it; decide runs after step i's solver update:
+// a reused step counts [0] down, a computed one (the cosine similarity cs of its velocity
+// with the previous computed one, valid when [1] >= 1) sets [0] = window when cs > tau;
+// computed[i] (optional) receives [2].  copy_if copies n floats while *flag != 0.
+hipError_t launch_loop_init(int32_t* state, hipStream_t s);
+hipError_t launch_loop_decide(int32_t* state, const float* cs, float tau, int32_t window, int32_t* computed,
+                              int32_t i, hipStream_t s);
+hipError_t launch_copy_if(const int32_t* flag, const float* src, float* dst, int64_t n, hipStream_t s);
 
 }  // namespace wam

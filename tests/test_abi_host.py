@@ -32,7 +32,7 @@ def test_library_exports_every_declared_function():
     for name in declared:
         assert hasattr(L, name), name
     assert sorted(w.binding.EXPORTED) == declared
-    assert w.wam_abi_version() == 3
+    assert w.wam_abi_version() == 4
 
 
 def test_struct_sizes_match_the_header_layout():
