@@ -10,7 +10,13 @@ this is the reading used for the FP8 path here:
 * activations are quantized per row (per token) with scale = max|row| / 448, weights
   per output channel the same way; a zero row gets scale 1;
 * an FP8 GEMM computes sum_k q_a[m][k] q_w[n][k] exactly and multiplies by
-  scale_a[m] scale_w[n].
+  scale_a[m] scale_w[n];
+* attention in FP8 (the paper quantizes QKV and the softmax): q and k in 32-element
+  blocks along the head dimension, each block with its own power-of-two scale 2^e
+  (an 8-bit biased exponent, as the OCP microscaling formats define it), e the
+  smallest integer with max|block| <= 448 * 2^e, so no element saturates; v with one
+  scale per tensor, code = E4M3(x * (1 / scale)) with the reciprocal and the product
+  rounded to fp32.
 """
 import numpy as np
 
@@ -57,3 +63,46 @@ def fp8_linear(q_a, s_a, q_w, s_w, bias=None):
     """y[m][n] = (sum_k q_a[m][k] q_w[n][k]) s_a[m] s_w[n] + bias[n]."""
     y = (q_a @ q_w.T) * s_a[..., None] * s_w
     return y if bias is None else y + bias
+
+
+MX_BLOCK = 32
+MX_EMIN, MX_EMAX = -127, 127   # exponent range of the 8-bit biased scale (bias 127)
+
+
+def mx_exponent(amax):
+    """Shared exponent of each block with maximum magnitude amax: the smallest integer e
+    with amax <= 448 * 2^e, clamped to [-127, 127]; 0 for an all-zero block."""
+    amax = np.asarray(amax, dtype=np.float64)
+    out = np.zeros(amax.shape, dtype=np.int64)
+    for idx in np.ndindex(amax.shape):
+        a = float(amax[idx])
+        if a == 0.0:
+            continue
+        _, E = np.frexp(a)             # a = f 2^E, 0.5 <= f < 1, so 2^(E-1) <= a < 2^E
+        e = int(E) - 1 - 8             # a / 2^e in [256, 512)
+        if a > E4M3_MAX * 2.0 ** e:
+            e += 1
+        out[idx] = min(max(e, MX_EMIN), MX_EMAX)
+    return out
+
+
+def quantize_mx(x):
+    """Block quantization along the last axis (length a multiple of 32): returns
+    (q, e) with e [..., n/32] the block exponents and q the E4M3 values of x / 2^e."""
+    x = np.asarray(x, dtype=np.float64)
+    blocks = x.reshape(x.shape[:-1] + (x.shape[-1] // MX_BLOCK, MX_BLOCK))
+    e = mx_exponent(np.max(np.abs(blocks), axis=-1))
+    q = round_e4m3(blocks * 2.0 ** (-e[..., None].astype(np.float64)))
+    return q.reshape(x.shape), e
+
+
+def decode_mx(q, e):
+    """x ~ q * 2^e with each exponent applied to its 32-element block."""
+    return np.asarray(q, dtype=np.float64) * np.repeat(2.0 ** np.asarray(e, dtype=np.float64), MX_BLOCK, axis=-1)
+
+
+def quantize_scaled(x, scale):
+    """One-scale E4M3 quantization evaluated in fp32: round_e4m3(fp32(x * fp32(1/scale)))."""
+    inv = np.float32(1.0) / np.float32(scale)
+    y = np.asarray(x, dtype=np.float32) * inv
+    return round_e4m3(y.astype(np.float64))

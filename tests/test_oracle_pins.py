@@ -792,6 +792,77 @@ def test_fp8_row_quantization_error_bound():
     assert np.allclose(y, (q[:2] * s[:2, None]) @ (q[2:5] * s[2:5, None]).T, atol=1e-12)
 
 
+def test_mx_exponent_is_smallest_without_saturation():
+    """The block exponent against a brute-force search for the smallest e in [-127, 127]
+    with max|block| <= 448 * 2^e, at the boundaries 448 * 2^e and 224 * 2^e (the largest
+    magnitude that still takes the exponent below) and over random magnitudes."""
+    f = oracle.fp8.mx_exponent
+
+    def brute(a):
+        if a == 0.0:
+            return 0
+        for e in range(-127, 128):
+            if a <= 448.0 * 2.0 ** e:
+                return e
+        return 127
+
+    for e in (-20, -3, 0, 1, 7, 40):
+        top = 448.0 * 2.0 ** e
+        assert f(top) == e and f(np.nextafter(top, np.inf)) == e + 1
+        assert f(224.0 * 2.0 ** e) == e - 1 and f(np.nextafter(224.0 * 2.0 ** e, np.inf)) == e
+    g = np.random.default_rng(172)
+    amax = np.abs(g.standard_normal(500)) * 10.0 ** g.uniform(-30, 30, 500)
+    assert np.array_equal(f(amax), [brute(a) for a in amax])
+    assert f(0.0) == 0 and f(2.0 ** -140) == -127 and f(3.0e38) == brute(3.0e38)
+
+
+def test_mx_block_quantization():
+    """32-element blocks along the last axis: codes equal torch's float8_e4m3fn rounding of
+    x / 2^e, each block's largest scaled magnitude lies in (224, 448], every normal-range
+    element is within half a mantissa unit, a block whose maximum is exactly 448 * 2^e gets
+    the per-row quantizer's codes, and blocks do not influence each other."""
+    torch = pytest.importorskip("torch")
+    g = np.random.default_rng(173)
+    x = g.standard_normal((6, 256)) * np.repeat(10.0 ** g.uniform(-4, 4, (6, 8)), 32, axis=1)
+    x = x.astype(np.float32).astype(np.float64)
+    x[2, 64:96] = 0.0
+    q, e = oracle.fp8.quantize_mx(x)
+    assert e.shape == (6, 8) and e[2, 2] == 0 and not q[2, 64:96].any()
+    scaled = x * np.repeat(2.0 ** -e.astype(np.float64), 32, axis=1)
+    ref = torch.from_numpy(scaled).to(torch.float8_e4m3fn).to(torch.float64).numpy()
+    assert np.array_equal(q, ref)
+    bmax = np.max(np.abs(scaled.reshape(6, 8, 32)), axis=-1)
+    nz = bmax > 0
+    assert np.all(bmax[nz] > 224.0) and np.all(bmax[nz] <= 448.0)
+    deq = oracle.fp8.decode_mx(q, e)
+    normal = np.abs(scaled) >= 2.0 ** -6
+    assert np.all(np.abs(deq - x)[normal] <= 2.0 ** -4 * np.abs(x)[normal])
+    blk = g.standard_normal(32)
+    blk *= 448.0 * 2.0 ** 5 / np.max(np.abs(blk))
+    qb, eb = oracle.fp8.quantize_mx(blk)
+    qr, sr = oracle.fp8.quantize_rows(blk[None])
+    assert eb[0] == 5 and sr[0] == 2.0 ** 5 and np.array_equal(qb, qr[0])
+    x2 = x.copy()
+    x2[:, 32:64] *= 1000.0
+    q2, e2 = oracle.fp8.quantize_mx(x2)
+    keep = np.ones(256, bool)
+    keep[32:64] = False
+    assert np.array_equal(q2[:, keep], q[:, keep]) and np.array_equal(np.delete(e2, 1, 1), np.delete(e, 1, 1))
+
+
+def test_scaled_quantization_in_fp32():
+    """One-scale quantization: torch's float8 conversion of the fp32 product x * (1/s),
+    and for a power-of-two scale the exact quotient's rounding."""
+    torch = pytest.importorskip("torch")
+    g = np.random.default_rng(174)
+    x = (g.standard_normal(5000) * 3.0).astype(np.float32)
+    s = 0.0123
+    inv = torch.tensor(1.0, dtype=torch.float32) / torch.tensor(s, dtype=torch.float32)
+    ref = (torch.from_numpy(x) * inv).clamp(-448.0, 448.0).to(torch.float8_e4m3fn).to(torch.float64).numpy()
+    assert np.array_equal(oracle.fp8.quantize_scaled(x, s), ref)
+    assert np.array_equal(oracle.fp8.quantize_scaled(x, 0.125), oracle.fp8.round_e4m3(x.astype(np.float64) / 0.125))
+
+
 # ----------------------------------------------------------------------------- shared input generator
 def test_bf16_rounding_matches_torch():
     torch = pytest.importorskip("torch")
