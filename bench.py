@@ -117,8 +117,10 @@ def extras(wl, model, keep, kcs, vcs, inp, torch, reps=3):
     HIP events on the current stream, after one warm-up call each): the DreamZero-Flash
     step (actions at their own timestep), the cache-update pass over one clean video-only
     chunk (3120 rows after the cached ones), a 4-step Euler denoising loop, the step with
-    the text's projection and cross K|V cached per episode (computed once, passed in), and
-    the step with every block's seven projections as FP8 (E4M3) GEMMs."""
+    the text's projection and cross K|V cached per episode (computed once, passed in), the
+    step with every block's seven projections as FP8 (E4M3) GEMMs, and that step with an FP8
+    KV cache (self-attention in FP8; also its average self-attention launch, from events
+    recorded around each launch of the last timed call)."""
     import numpy as np
     import paper_2602_15922_amd as w
     B = wl.B
@@ -197,7 +199,35 @@ def extras(wl, model, keep, kcs, vcs, inp, torch, reps=3):
     ws8 = torch.empty(w.wam_step_workspace_bytes(model8, io8), dtype=torch.uint8, device=dev)
     out["fp8_step_ms"] = round(timed(lambda: w.wam_dit_step_fwd(model8, io8, ws8)), 3)
     assert torch.isfinite(vv).all()
-    del blocks8, model8, ws8
+
+    # FP8 projections and an FP8 KV cache (FP8 self-attention): E4M3 caches made from the
+    # bf16 ones with the library's quantizers, V's per-layer scale max|V| / 448 over the
+    # rows the step reads and writes (the bf16 steps above wrote this chunk's rows: a
+    # calibration pass)
+    rows = wl.cache_rows + wl.L
+    k8s, kes, v8s, vsc = [], [], [], []
+    for kc, vc in zip(kcs, vcs):
+        Bc, Lcap, H, Dh = kc.shape
+        k8 = torch.empty((Bc, Lcap, H, Dh), dtype=torch.uint8, device=dev)
+        ke = torch.empty((Bc, Lcap, H), dtype=torch.int32, device=dev)
+        w.wam_quantize_mx_fp8(kc.view(Bc * Lcap, H * Dh), k8.view(Bc * Lcap, H * Dh),
+                              ke.view(torch.uint8).view(Bc * Lcap, H * 4))
+        vs = float(vc[:, :rows].abs().max().float()) / 448.0
+        v8 = torch.empty_like(k8)
+        w.wam_quantize_scaled_fp8(vc, vs, v8)
+        k8s.append(k8)
+        kes.append(ke)
+        v8s.append(v8)
+        vsc.append(vs)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * wl.n_layers)]
+    io8a = w.make_step_io(inp["z"], inp["a"], inp["t"], inp["text"], k8s, v8s, inp["cos"], inp["sin"],
+                          wl.cache_rows, chunks, vv, va, events=ev, k_exps=kes, v_scales=vsc)
+    out["fp8_attn_step_ms"] = round(timed(lambda: w.wam_dit_step_fwd(model8, io8a, ws8)), 3)
+    torch.cuda.synchronize()
+    out["fp8_attn_kernel_ms"] = round(sum(ev[2 * l].elapsed_time(ev[2 * l + 1]) for l in range(wl.n_layers))
+                                      / wl.n_layers, 4)
+    assert torch.isfinite(vv).all()
+    del blocks8, model8, ws8, k8s, v8s, kes
     return out
 
 

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define WAM_ABI_VERSION 4
+#define WAM_ABI_VERSION 5
 #define WAM_MAX_CHUNKS 16
 
 typedef enum {
@@ -112,6 +112,42 @@ typedef struct {
 
 wam_status wam_attn_blockcausal(const wam_attn_desc* desc, const void* q, const void* k,
                                 const void* v, void* o, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * FP8 attention operands (section 3.2.4 and Appendix D.2 run QKV and the softmax in FP8;
+ * the formats below are this library's reading).  E4M3 is the OCP 8-bit float (bias 7,
+ * largest 448, no infinities), rounded to nearest even.
+ *   MX blocks (q, k): 32 consecutive elements share a power-of-two scale 2^e with e the
+ *     smallest integer such that max|x| <= 448 * 2^e (clamped to [-127, 127]; 0 for a
+ *     zero block), stored as the byte e + 127; codes E4M3(x * 2^-e).  A head of Dh = 128
+ *     has four blocks, so its exponents form one uint32 (byte j: dims [32j, 32j+32)).
+ *   One scale (v): codes E4M3(fp32(x * fp32(1 / scale))), saturating at +-448.
+ *
+ * wam_quantize_mx_fp8 — MX codes of bf16 rows x [rows][ldx] (cols % 32 == 0, ldx % 8 ==
+ *   0, x 16-byte aligned): q8 [rows][ldq] bytes (ldq % 8 == 0, 8-byte aligned), exps
+ *   [rows][cols/32] bytes, contiguous.
+ * wam_quantize_scaled_fp8 — one-scale codes of n bf16 values (n % 8 == 0).
+ * ------------------------------------------------------------------------------ */
+wam_status wam_quantize_mx_fp8(int32_t rows, int32_t cols, const void* x, int64_t ldx, void* q8,
+                               int64_t ldq, void* exps, hipStream_t stream);
+wam_status wam_quantize_scaled_fp8(int64_t n, const void* x, float scale, void* q8,
+                                   hipStream_t stream);
+
+/* wam_attn_blockcausal_fp8 — the attention of wam_attn_blockcausal (same chunk rule and
+ * descriptor) on FP8 operands, Dh = 128 only:
+ *   q8, k8, v8  E4M3 codes addressed like the bf16 operands with one byte per element
+ *               (strides in bytes, multiples of 128; 16-byte aligned);
+ *   q_exp, k_exp  uint32 block exponents of q and k, one per (token, head), addressed
+ *               with the code strides divided by 128 (4-byte aligned);
+ *   v_scale     v = code * v_scale;  o  bf16 as in wam_attn_blockcausal.
+ * Scores use the exact products of the decoded q and k (fp32 accumulation); the
+ * probabilities are rounded to E4M3 before the value product, relative to a running
+ * maximum that is raised whenever a tile exceeds it by 2^2 in the exp2 domain (so they
+ * stay below 2^8 after a fixed 2^6 scaling), and the normaliser is the sum of those
+ * rounded probabilities.  Deterministic. */
+wam_status wam_attn_blockcausal_fp8(const wam_attn_desc* desc, const void* q8, const void* q_exp,
+                                    const void* k8, const void* k_exp, const void* v8, float v_scale,
+                                    void* o, hipStream_t stream);
 
 /* ------------------------------------------------------------------------------
  * Model dimensions.  d = H*Dh, d % 256 == 0, Dh in {64, 128}; latent_ch*4 patch
@@ -186,6 +222,9 @@ typedef struct {
   const void* ctx;
   const void* ctx_kv;
   int32_t B, L, Lc;
+  void* k_exp;     /* optional: an FP8 KV cache (Dh = 128): k_cache / v_cache then hold E4M3 */
+  float v_scale;   /* codes [B][Lcap][H][Dh] bytes, k_exp [B][Lcap][H] uint32 the K block  */
+                   /* exponents, v = code * v_scale; the self-attention runs in FP8        */
 } wam_block_io;
 
 size_t wam_block_workspace_bytes(const wam_dims* dims, int32_t B, int32_t L, int32_t Lc);
@@ -251,6 +290,9 @@ typedef struct {
   float* v_action;
   hipEvent_t* attn_events;
   const float* t_action;
+  void* const* k_exp;     /* optional HOST array of n_layers FP8 K exponent caches (then   */
+  const float* v_scale;   /* k_cache / v_cache hold E4M3 codes; v_scale HOST [n_layers]),  */
+                          /* as in wam_block_io                                            */
 } wam_step_io;
 
 size_t wam_step_workspace_bytes(const wam_model* m, const wam_step_io* io);
@@ -383,6 +425,16 @@ wam_status wam_rope_qkv(int32_t B, int32_t L, int32_t H, int32_t Dh, const void*
                         const float* rope_cos, const float* rope_sin, void* q_out,
                         void* k_cache, void* v_cache, int32_t Lcap, int32_t row0,
                         hipStream_t stream);
+
+/* wam_rope_qkv_fp8 — the same rotation and append into an FP8 cache (Dh = 128): the
+ * rotated q (fp32) as MX codes q8 [B][L][H][Dh] bytes with exponents q_exp [B][L][H]
+ * uint32 (both NULL: q is not written), the rotated k as MX codes into rows
+ * [row0, row0+L) of k8_cache [B][Lcap][H][Dh] bytes and k_exp [B][Lcap][H] uint32, v as
+ * one-scale codes (v_scale) into v8_cache.  Formats as for wam_quantize_mx_fp8. */
+wam_status wam_rope_qkv_fp8(int32_t B, int32_t L, int32_t H, int32_t Dh, const void* qkv,
+                            const float* rope_cos, const float* rope_sin, void* q8, void* q_exp,
+                            void* k8_cache, void* k_exp, void* v8_cache, float v_scale,
+                            int32_t Lcap, int32_t row0, hipStream_t stream);
 
 /* GEMM with fused epilogue: acc[m][n] = sum_k A[m][k] W[n][k] (bf16 in, fp32 acc),
  * v = acc + bias[n] (bias NULL = 0), then by epilogue:

@@ -73,17 +73,11 @@ def mx_exponent(amax):
     """Shared exponent of each block with maximum magnitude amax: the smallest integer e
     with amax <= 448 * 2^e, clamped to [-127, 127]; 0 for an all-zero block."""
     amax = np.asarray(amax, dtype=np.float64)
-    out = np.zeros(amax.shape, dtype=np.int64)
-    for idx in np.ndindex(amax.shape):
-        a = float(amax[idx])
-        if a == 0.0:
-            continue
-        _, E = np.frexp(a)             # a = f 2^E, 0.5 <= f < 1, so 2^(E-1) <= a < 2^E
-        e = int(E) - 1 - 8             # a / 2^e in [256, 512)
-        if a > E4M3_MAX * 2.0 ** e:
-            e += 1
-        out[idx] = min(max(e, MX_EMIN), MX_EMAX)
-    return out
+    _, E = np.frexp(amax)              # amax = f 2^E, 0.5 <= f < 1, so 2^(E-1) <= amax < 2^E
+    e = E.astype(np.int64) - 1 - 8     # amax / 2^e in [256, 512)
+    e = np.where(amax > E4M3_MAX * np.ldexp(1.0, e), e + 1, e)
+    e = np.clip(e, MX_EMIN, MX_EMAX)
+    return np.where(amax == 0, 0, e)
 
 
 def quantize_mx(x):

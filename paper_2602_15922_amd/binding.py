@@ -27,7 +27,8 @@ EXPORTED = (
     "wam_time_embed_workspace_bytes", "wam_time_embed_fwd", "wam_text_proj_workspace_bytes",
     "wam_text_proj_fwd", "wam_adaln_ln_mod", "wam_rope_qkv", "wam_gemm_bf16",
     "wam_embed_workspace_bytes", "wam_embed_fwd", "wam_head_workspace_bytes", "wam_head_fwd",
-    "wam_chunk_positions", "wam_rope_tables",
+    "wam_chunk_positions", "wam_rope_tables", "wam_attn_blockcausal_fp8", "wam_quantize_mx_fp8",
+    "wam_quantize_scaled_fp8", "wam_rope_qkv_fp8",
 )
 
 _vp, _fp, _i32, _i64, _sz = C.c_void_p, C.POINTER(C.c_float), C.c_int32, C.c_int64, C.c_size_t
@@ -75,7 +76,7 @@ class wam_block_io(C.Structure):
     _fields_ = [("x", _vp), ("e0", _vp), ("rope_cos", _vp), ("rope_sin", _vp),
                 ("k_cache", _vp), ("v_cache", _vp), ("Lcap", _i32), ("cache_len", _i32),
                 ("ch", wam_chunks), ("ctx", _vp), ("ctx_kv", _vp),
-                ("B", _i32), ("L", _i32), ("Lc", _i32)]
+                ("B", _i32), ("L", _i32), ("Lc", _i32), ("k_exp", _vp), ("v_scale", C.c_float)]
 
 
 MODEL_MATS = ("w_t1", "w_t2", "w_t6", "w_x1", "w_x2", "w_patch", "w_ain", "w_hv", "w_ha")
@@ -94,7 +95,8 @@ class wam_step_io(C.Structure):
                 ("rope_cos", _vp), ("rope_sin", _vp),
                 ("B", _i32), ("F", _i32), ("Hl", _i32), ("Wl", _i32), ("A", _i32), ("Lc", _i32),
                 ("Lcap", _i32), ("cache_len", _i32), ("ch", wam_chunks),
-                ("v_video", _vp), ("v_action", _vp), ("attn_events", C.POINTER(_vp)), ("t_action", _vp)]
+                ("v_video", _vp), ("v_action", _vp), ("attn_events", C.POINTER(_vp)), ("t_action", _vp),
+                ("k_exp", C.POINTER(_vp)), ("v_scale", _fp)]
 
 
 class wam_flow_dims(C.Structure):
@@ -165,6 +167,12 @@ def lib():
                                    _vp, _vp, _sz, _vp]
         L.wam_chunk_positions.argtypes = [_i32, _i32, _i32, _i32, _i32, C.POINTER(_i32)]
         L.wam_rope_tables.argtypes = [C.POINTER(_i32), _i32, _i32, C.c_double, _fp, _fp]
+        L.wam_attn_blockcausal_fp8.argtypes = [C.POINTER(wam_attn_desc), _vp, _vp, _vp, _vp, _vp, C.c_float, _vp,
+                                               _vp]
+        L.wam_quantize_mx_fp8.argtypes = [_i32, _i32, _vp, _i64, _vp, _i64, _vp, _vp]
+        L.wam_quantize_scaled_fp8.argtypes = [_i64, _vp, C.c_float, _vp, _vp]
+        L.wam_rope_qkv_fp8.argtypes = [_i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, C.c_float,
+                                       _i32, _i32, _vp]
         for name in EXPORTED[2:]:
             if not name.endswith("_bytes"):
                 getattr(L, name).restype = C.c_int
@@ -244,6 +252,45 @@ def wam_attn_blockcausal(q, k, v, o, chunks: wam_chunks, scale: float = 0.0, str
     if v.stride(1) != k.stride(1) or v.stride(0) != k.stride(0):
         raise ValueError("k and v must share token and batch strides")
     _check(lib().wam_attn_blockcausal(C.byref(d), _p(q), _p(k), _p(v), _p(o), _stream(stream)))
+
+
+def wam_attn_blockcausal_fp8(q8, q_exp, k8, k_exp, v8, v_scale, o, chunks: wam_chunks, scale: float = 0.0,
+                             stream=None):
+    """FP8 attention (Dh = 128): q8 [B, Lq, H, 128] and k8, v8 [B, Lk, H, 128] uint8 E4M3 code
+    views, q_exp [B, Lq, H] and k_exp [B, Lk, H] int32 block exponents (one byte per 32
+    dims), o [B, Lq, H, 128] bf16; strides taken from the tensors."""
+    B, Lq, H, Dh = q8.shape
+    d = wam_attn_desc(B=B, H=H, Dh=Dh, Lq=Lq, Lk=k8.shape[1],
+                      q_tok_stride=q8.stride(1), q_batch_stride=q8.stride(0),
+                      kv_tok_stride=k8.stride(1), kv_batch_stride=k8.stride(0),
+                      o_tok_stride=o.stride(1), o_batch_stride=o.stride(0), scale=scale, ch=chunks)
+    if v8.stride(1) != k8.stride(1) or v8.stride(0) != k8.stride(0):
+        raise ValueError("k8 and v8 must share token and batch strides")
+    for e, c in ((q_exp, q8), (k_exp, k8)):
+        if e.stride(1) * Dh != c.stride(1) or e.stride(0) * Dh != c.stride(0):
+            raise ValueError("exponent strides must be the code strides / Dh")
+    _check(lib().wam_attn_blockcausal_fp8(C.byref(d), _p(q8), _p(q_exp), _p(k8), _p(k_exp), _p(v8), v_scale,
+                                          _p(o), _stream(stream)))
+
+
+def wam_quantize_mx_fp8(x, q8, exps, stream=None):
+    """MX-style E4M3 codes of bf16 rows x [M, K] (K % 32 == 0) into uint8 q8 [M, >=K] and
+    uint8 exps [M, K/32] (biased block exponents)."""
+    M, K = x.shape
+    _check(lib().wam_quantize_mx_fp8(M, K, _p(x), x.stride(0), _p(q8), q8.stride(0), _p(exps), _stream(stream)))
+
+
+def wam_quantize_scaled_fp8(x, scale, q8, stream=None):
+    """One-scale E4M3 codes of a contiguous bf16 tensor into a uint8 tensor of the same size."""
+    _check(lib().wam_quantize_scaled_fp8(x.numel(), _p(x), scale, _p(q8), _stream(stream)))
+
+
+def wam_rope_qkv_fp8(qkv, cos_t, sin_t, q8, q_exp, k8_cache, k_exp, v8_cache, v_scale, row0, H, Dh, stream=None):
+    """qkv [B, L, 3*H*Dh] bf16; code caches [B, Lcap, H, Dh] uint8, k_exp [B, Lcap, H] int32;
+    q8 [B, L, H, Dh] uint8 and q_exp [B, L, H] int32 (or both None)."""
+    B, L = qkv.shape[0], qkv.shape[1]
+    _check(lib().wam_rope_qkv_fp8(B, L, H, Dh, _p(qkv), _p(cos_t), _p(sin_t), _p(q8), _p(q_exp), _p(k8_cache),
+                                  _p(k_exp), _p(v8_cache), v_scale, k8_cache.shape[1], row0, _stream(stream)))
 
 
 def wam_gemm_bf16(A, W, out, epilogue: int, bias=None, gate_a=None, gate_v=None, gate_stride=0,
@@ -411,7 +458,9 @@ def _ptr_array(ts):
 
 
 def make_step_io(z_t, a_t, t, text, k_caches, v_caches, rope_cos, rope_sin, cache_len, chunks, v_video,
-                 v_action, ctx_kv=None, events=None, t_action=None) -> wam_step_io:
+                 v_action, ctx_kv=None, events=None, t_action=None, k_exps=None, v_scales=None) -> wam_step_io:
+    """Step inputs/outputs; with k_exps (per-layer [B, Lcap, H] int32) and v_scales (per-layer
+    floats) the caches are FP8 code caches and the self-attention runs in FP8."""
     B, _, F, Hl, Wl = z_t.shape
     io = wam_step_io(z_t=_p(z_t), a_t=_p(a_t), t=_p(t), text=_p(text), rope_cos=_p(rope_cos),
                      rope_sin=_p(rope_sin), B=B, F=F, Hl=Hl, Wl=Wl, A=a_t.shape[1], Lc=text.shape[1],
@@ -425,6 +474,12 @@ def make_step_io(z_t, a_t, t, text, k_caches, v_caches, rope_cos, rope_sin, cach
         ck = _ptr_array(ctx_kv)
         io.ctx_kv = C.cast(ck, C.POINTER(_vp))
         keep.append(ck)
+    if k_exps is not None:
+        ke = _ptr_array(k_exps)
+        vs = (C.c_float * len(v_scales))(*[float(v) for v in v_scales])
+        io.k_exp = C.cast(ke, C.POINTER(_vp))
+        io.v_scale = C.cast(vs, _fp)
+        keep += [ke, vs]
     if events is not None:
         # torch's Event.elapsed_time() only reads events torch has seen recorded; record
         # each once here so the library's later hipEventRecord on them can be read back.

@@ -9,7 +9,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libwamdit.so")
-SOURCES = ["attn.hip", "gemm.hip", "elementwise.hip", "flow.hip", "capi.hip"]
+SOURCES = ["attn.hip", "attn_fp8.hip", "gemm.hip", "elementwise.hip", "flow.hip", "capi.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-I", INCLUDE,

@@ -150,6 +150,58 @@ wam_status attn_checked(const wam_attn_desc& d, const void* q, const void* k, co
   return WAM_OK;
 }
 
+bool al4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3) == 0; }
+
+// FP8 attention (Dh = 128): codes addressed like the bf16 operands with one byte per
+// element; each (token, head) has one uint32 of block exponents, so the exponent arrays'
+// strides are the code strides / Dh.
+wam_status attn_fp8_checked(const wam_attn_desc& d, const void* q, const void* qe, const void* k, const void* ke,
+                            const void* v, float v_scale, void* o, hipStream_t s) {
+  CHECK(d.Dh == 128, WAM_EUNSUPPORTED, "FP8 attention needs Dh=128 (got %d)", d.Dh);
+  CHECK(d.B >= 0 && d.H >= 1 && d.Lq >= 0 && d.Lk >= 0, WAM_EINVAL, "negative size (B=%d H=%d Lq=%d Lk=%d)",
+        d.B, d.H, d.Lq, d.Lk);
+  CHECK(std::isfinite(v_scale) && v_scale > 0.f, WAM_EINVAL, "v_scale=%g must be positive and finite",
+        (double)v_scale);
+  AttnFp8Args f{};
+  AttnArgs& a = f.a;
+  TRY(check_chunks(d.ch, d.Lq, d.Lk, a.kend));
+  if (d.B == 0 || d.Lq == 0) return WAM_OK;
+  TRY(need_ptr(q, "q8")); TRY(need_ptr(qe, "q_exp")); TRY(need_ptr(k, "k8")); TRY(need_ptr(ke, "k_exp"));
+  TRY(need_ptr(v, "v8")); TRY(need_ptr(o, "o"));
+  CHECK(al16(q) && al16(k) && al16(v) && al16(o) && al4(qe) && al4(ke), WAM_EINVAL,
+        "q8/k8/v8/o must be 16-byte and q_exp/k_exp 4-byte aligned");
+  const int64_t hd = (int64_t)d.H * d.Dh;
+  CHECK(d.q_tok_stride >= hd && d.kv_tok_stride >= hd && d.o_tok_stride >= hd, WAM_EINVAL,
+        "token strides must be >= H*Dh=%lld", (long long)hd);
+  CHECK(d.q_tok_stride % 128 == 0 && d.kv_tok_stride % 128 == 0 && d.q_batch_stride % 128 == 0 &&
+            d.kv_batch_stride % 128 == 0,
+        WAM_EINVAL, "q and k/v strides must be multiples of Dh=128 bytes");
+  CHECK(d.o_tok_stride % 8 == 0 && d.o_batch_stride % 8 == 0, WAM_EINVAL, "o strides must be multiples of 8");
+  CHECK(d.B == 1 || (d.q_batch_stride >= (int64_t)d.Lq * d.q_tok_stride &&
+                     d.o_batch_stride >= (int64_t)d.Lq * d.o_tok_stride &&
+                     d.kv_batch_stride >= (int64_t)d.Lk * d.kv_tok_stride),
+        WAM_EINVAL, "batch strides smaller than one sample");
+  CHECK((int64_t)d.Lk * d.kv_tok_stride <= INT32_MAX, WAM_EUNSUPPORTED,
+        "one sample's keys span %lld bytes (must stay below 2^31)", (long long)d.Lk * d.kv_tok_stride);
+  a.q = q; a.k = k; a.v = v; a.o = o;
+  a.q_ts = d.q_tok_stride; a.q_bs = d.q_batch_stride;
+  a.kv_ts = d.kv_tok_stride; a.kv_bs = d.kv_batch_stride;
+  a.o_ts = d.o_tok_stride; a.o_bs = d.o_batch_stride;
+  a.B = d.B; a.H = d.H; a.Dh = d.Dh; a.Lq = d.Lq; a.Lk = d.Lk;
+  const float scale = d.scale > 0.f ? d.scale : 1.0f / std::sqrt((float)d.Dh);
+  a.c = scale * 1.4426950408889634f;
+  a.n_k_chunks = d.ch.n_k_chunks;
+  a.n_q_chunks = d.ch.n_q_chunks;
+  for (int i = 0; i <= d.ch.n_q_chunks; ++i) a.q_off[i] = d.ch.q_off[i];
+  a.skip = t_skip;
+  f.q_exp = qe; f.k_exp = ke;
+  f.qe_ts = d.q_tok_stride / 128; f.qe_bs = d.q_batch_stride / 128;
+  f.ke_ts = d.kv_tok_stride / 128; f.ke_bs = d.kv_batch_stride / 128;
+  f.v_scale = v_scale;
+  HIPCHECK(launch_attn_fp8(f, s));
+  return WAM_OK;
+}
+
 wam_chunks single_chunk(int32_t Lq, int32_t Lk) {
   wam_chunks c{};
   c.n_k_chunks = 1; c.k_off[0] = 0; c.k_off[1] = Lk;
@@ -284,6 +336,12 @@ wam_status check_block_io(const wam_dims& D, const wam_block_weights& w, const w
   TRY(need_ptr(io.x, "x")); TRY(need_ptr(io.e0, "e0"));
   TRY(need_ptr(io.rope_cos, "rope_cos")); TRY(need_ptr(io.rope_sin, "rope_sin"));
   TRY(need_ptr(io.k_cache, "k_cache")); TRY(need_ptr(io.v_cache, "v_cache"));
+  if (io.k_exp) {
+    CHECK(D.Dh == 128, WAM_EUNSUPPORTED, "an FP8 KV cache needs Dh=128 (got %d)", D.Dh);
+    CHECK(std::isfinite(io.v_scale) && io.v_scale > 0.f, WAM_EINVAL, "v_scale=%g must be positive and finite",
+          (double)io.v_scale);
+    CHECK(al16(io.k_cache) && al16(io.v_cache) && al4(io.k_exp), WAM_EINVAL, "FP8 cache pointers misaligned");
+  }
   if (io.ctx_kv) {
     TRY(need_ptr(io.ctx_kv, "ctx_kv"));
   } else {
@@ -319,9 +377,16 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   // 2. fused QKV projection
   TRY(proj(gemm(M, 3 * d, d, WAM_EPI_BF16, h, d, W.w_qkv, W.b_qkv, big, 3 * d), F8 ? F8->w_qkv : nullptr,
            F8 ? F8->s_qkv : nullptr, q8, qs, s));
-  // 3. RoPE on q, k; k, v appended to the cache rows of this chunk
+  // 3. RoPE on q, k; k, v appended to the cache rows of this chunk (with an FP8 cache:
+  // q and k encoded in 32-dim blocks, q into the q buffer with its exponents behind it)
+  void* qe = static_cast<char*>(q) + (size_t)M * d;
   RopeArgs ra{B, L, D.H, D.Dh, io.Lcap, io.cache_len, big, io.rope_cos, io.rope_sin, q, io.k_cache, io.v_cache};
-  HIPCHECK(launch_rope_qkv(pred(ra), s));
+  if (io.k_exp) {
+    RopeFp8Args rf{pred(ra), qe, io.k_exp, 1.0f / io.v_scale};
+    HIPCHECK(launch_rope_qkv_fp8(rf, s));
+  } else {
+    HIPCHECK(launch_rope_qkv(pred(ra), s));
+  }
   // 4. block-causal self-attention over cache rows [0, cache_len + L)
   wam_attn_desc ad{};
   ad.B = B; ad.H = D.H; ad.Dh = D.Dh; ad.Lq = L; ad.Lk = io.cache_len + L;
@@ -330,7 +395,8 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   ad.o_tok_stride = d; ad.o_batch_stride = (int64_t)L * d;
   ad.ch = io.ch;
   if (ev0) HIPCHECK(hipEventRecord(ev0, s));
-  TRY(attn_checked(ad, q, io.k_cache, io.v_cache, o, s));
+  if (io.k_exp) TRY(attn_fp8_checked(ad, q, qe, io.k_cache, io.k_exp, io.v_cache, io.v_scale, o, s));
+  else TRY(attn_checked(ad, q, io.k_cache, io.v_cache, o, s));
   if (ev1) HIPCHECK(hipEventRecord(ev1, s));
   // 5. x += gate1 * (o W_o^T + b_o)
   {
@@ -399,7 +465,12 @@ wam_status block_kv_run(const wam_dims& D, const wam_block_weights& W, const wam
            ws + lay.q8, reinterpret_cast<float*>(ws + lay.qs), s));
   RopeArgs ra{B, L, D.H, D.Dh, io.Lcap, io.cache_len, big, io.rope_cos, io.rope_sin, nullptr, io.k_cache,
               io.v_cache};
-  HIPCHECK(launch_rope_qkv(pred(ra), s));
+  if (io.k_exp) {
+    RopeFp8Args rf{pred(ra), nullptr, io.k_exp, 1.0f / io.v_scale};
+    HIPCHECK(launch_rope_qkv_fp8(rf, s));
+  } else {
+    HIPCHECK(launch_rope_qkv(pred(ra), s));
+  }
   return WAM_OK;
 }
 
@@ -563,6 +634,13 @@ wam_status check_step(const wam_model& m, const wam_step_io& io, bool head) {
     if (st != WAM_OK) return fail(st, "block %d: %s", l, g_err.c_str());
     CHECK(io.k_cache[l] && io.v_cache[l] && al16(io.k_cache[l]) && al16(io.v_cache[l]), WAM_EINVAL,
           "k_cache/v_cache[%d] NULL or misaligned", l);
+    if (io.k_exp) {
+      CHECK(D.Dh == 128, WAM_EUNSUPPORTED, "an FP8 KV cache needs Dh=128 (got %d)", D.Dh);
+      CHECK(io.v_scale != nullptr, WAM_EINVAL, "k_exp given without v_scale");
+      CHECK(io.k_exp[l] && al4(io.k_exp[l]), WAM_EINVAL, "k_exp[%d] NULL or misaligned", l);
+      CHECK(std::isfinite(io.v_scale[l]) && io.v_scale[l] > 0.f, WAM_EINVAL, "v_scale[%d]=%g must be positive", l,
+            (double)io.v_scale[l]);
+    }
     if (io.ctx_kv) {
       CHECK(io.ctx_kv[l] && al16(io.ctx_kv[l]), WAM_EINVAL, "ctx_kv[%d] NULL or misaligned", l);
     } else if (m.blocks[l].fp8) {
@@ -598,6 +676,7 @@ wam_status step_run(const wam_model& m, const wam_step_io& io, char* w, hipStrea
     b.k_cache = io.k_cache[l]; b.v_cache = io.v_cache[l]; b.Lcap = io.Lcap; b.cache_len = io.cache_len;
     b.ch = io.ch; b.ctx = ctx; b.ctx_kv = io.ctx_kv ? io.ctx_kv[l] : nullptr;
     b.B = io.B; b.L = L; b.Lc = io.Lc;
+    b.k_exp = io.k_exp ? io.k_exp[l] : nullptr; b.v_scale = io.v_scale ? io.v_scale[l] : 1.0f;
     hipEvent_t ev0 = io.attn_events ? io.attn_events[2 * l] : nullptr;
     hipEvent_t ev1 = io.attn_events ? io.attn_events[2 * l + 1] : nullptr;
     TRY(block_run(D, m.blocks[l], b, w + lay.block, stream, ev0, ev1, flash ? Lv : 0, alt_e0));
@@ -713,6 +792,56 @@ wam_status wam_rope_qkv(int32_t B, int32_t L, int32_t H, int32_t Dh, const void*
   TRY(need_ptr(q_out, "q_out")); TRY(need_ptr(k_cache, "k_cache")); TRY(need_ptr(v_cache, "v_cache"));
   RopeArgs a{B, L, H, Dh, Lcap, row0, qkv, rope_cos, rope_sin, q_out, k_cache, v_cache};
   HIPCHECK(launch_rope_qkv(a, stream));
+  return WAM_OK;
+}
+
+wam_status wam_attn_blockcausal_fp8(const wam_attn_desc* desc, const void* q8, const void* q_exp, const void* k8,
+                                    const void* k_exp, const void* v8, float v_scale, void* o, hipStream_t stream) {
+  CHECK(desc != nullptr, WAM_EINVAL, "NULL descriptor");
+  return attn_fp8_checked(*desc, q8, q_exp, k8, k_exp, v8, v_scale, o, stream);
+}
+
+wam_status wam_quantize_mx_fp8(int32_t rows, int32_t cols, const void* x, int64_t ldx, void* q8, int64_t ldq,
+                               void* exps, hipStream_t stream) {
+  CHECK(rows >= 0 && cols >= 0 && cols % 32 == 0, WAM_EINVAL, "rows=%d cols=%d (cols a multiple of 32)", rows,
+        cols);
+  CHECK(ldx >= cols && ldx % 8 == 0 && ldq >= cols && ldq % 8 == 0, WAM_EINVAL,
+        "ldx=%lld ldq=%lld must be >= cols and multiples of 8", (long long)ldx, (long long)ldq);
+  if ((int64_t)rows * cols == 0) return WAM_OK;
+  TRY(need_ptr(x, "x")); TRY(need_ptr(q8, "q8")); TRY(need_ptr(exps, "exps"));
+  CHECK(al16(x) && (reinterpret_cast<uintptr_t>(q8) & 7) == 0, WAM_EINVAL, "x must be 16-byte, q8 8-byte aligned");
+  HIPCHECK(launch_quant_mx(rows, cols, x, ldx, q8, ldq, exps, stream));
+  return WAM_OK;
+}
+
+wam_status wam_quantize_scaled_fp8(int64_t n, const void* x, float scale, void* q8, hipStream_t stream) {
+  CHECK(n >= 0 && n % 8 == 0, WAM_EINVAL, "n=%lld must be a non-negative multiple of 8", (long long)n);
+  CHECK(std::isfinite(scale) && scale > 0.f, WAM_EINVAL, "scale=%g must be positive and finite", (double)scale);
+  if (n == 0) return WAM_OK;
+  TRY(need_ptr(x, "x")); TRY(need_ptr(q8, "q8"));
+  CHECK(al16(x) && (reinterpret_cast<uintptr_t>(q8) & 7) == 0, WAM_EINVAL, "x must be 16-byte, q8 8-byte aligned");
+  HIPCHECK(launch_quant_scaled(n, x, 1.0f / scale, q8, stream));
+  return WAM_OK;
+}
+
+wam_status wam_rope_qkv_fp8(int32_t B, int32_t L, int32_t H, int32_t Dh, const void* qkv, const float* rope_cos,
+                            const float* rope_sin, void* q8, void* q_exp, void* k8_cache, void* k_exp,
+                            void* v8_cache, float v_scale, int32_t Lcap, int32_t row0, hipStream_t stream) {
+  CHECK(Dh == 128, WAM_EUNSUPPORTED, "the FP8 append needs Dh=128 (got %d)", Dh);
+  CHECK(B >= 0 && L >= 0 && H >= 1, WAM_EINVAL, "bad sizes B=%d L=%d H=%d", B, L, H);
+  CHECK(row0 >= 0 && (int64_t)row0 + L <= Lcap, WAM_EINVAL, "row0=%d + L=%d exceeds Lcap=%d", row0, L, Lcap);
+  CHECK(std::isfinite(v_scale) && v_scale > 0.f, WAM_EINVAL, "v_scale=%g must be positive and finite",
+        (double)v_scale);
+  CHECK((q8 == nullptr) == (q_exp == nullptr), WAM_EINVAL, "q8 and q_exp must both be given or both be NULL");
+  if ((int64_t)B * L == 0) return WAM_OK;
+  TRY(need_ptr(qkv, "qkv")); TRY(need_ptr(rope_cos, "rope_cos")); TRY(need_ptr(rope_sin, "rope_sin"));
+  TRY(need_ptr(k8_cache, "k8_cache")); TRY(need_ptr(k_exp, "k_exp")); TRY(need_ptr(v8_cache, "v8_cache"));
+  CHECK(al16(qkv) && (reinterpret_cast<uintptr_t>(k8_cache) & 7) == 0 &&
+            (reinterpret_cast<uintptr_t>(v8_cache) & 7) == 0 && (!q8 || (reinterpret_cast<uintptr_t>(q8) & 7) == 0),
+        WAM_EINVAL, "qkv must be 16-byte, code buffers 8-byte aligned");
+  RopeArgs a{B, L, H, Dh, Lcap, row0, qkv, rope_cos, rope_sin, q8, k8_cache, v8_cache};
+  RopeFp8Args f{a, q_exp, k_exp, 1.0f / v_scale};
+  HIPCHECK(launch_rope_qkv_fp8(f, stream));
   return WAM_OK;
 }
 
@@ -844,6 +973,7 @@ wam_status wam_dit_update_fwd(const wam_model* m, const wam_step_io* io, void* w
     b.k_cache = io->k_cache[l]; b.v_cache = io->v_cache[l]; b.Lcap = io->Lcap; b.cache_len = io->cache_len;
     b.ch = io->ch; b.ctx = ctx; b.ctx_kv = io->ctx_kv ? io->ctx_kv[l] : nullptr;
     b.B = io->B; b.L = L; b.Lc = io->Lc;
+    b.k_exp = io->k_exp ? io->k_exp[l] : nullptr; b.v_scale = io->v_scale ? io->v_scale[l] : 1.0f;
     if (l + 1 == D.n_layers) {
       TRY(block_kv_run(D, m->blocks[l], b, w + lay.block, stream, flash ? Lv : 0, alt_e0));
     } else {

@@ -23,9 +23,11 @@ WAM_DEV f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// 32x32x64 FP8 (E4M3 x E4M3) MFMA (gfx950), unit block scales.  Lane l, h = l/32:
-//   A operand: A[m = l%32][k = 32h .. 32h+31]   (32 consecutive k of one row, 32 bytes)
-//   B operand: B[k = 32h .. 32h+31][n = l%32]
+// 32x32x64 FP8 (E4M3 x E4M3) MFMA (gfx950), unit block scales.  Lane l, h = l/32, holds
+// 32 bytes of row m = l%32 of A (column n = l%32 of B); A's and B's bytes at the same
+// lane half and position are multiplied together.  With unit scales any k order shared
+// by both operands gives the product; block scales group bytes 0-15 of both halves
+// (scale from half 0) and bytes 16-31 of both halves (scale from half 1).
 //   C/D:       as for mfma32
 WAM_DEV f32x16 mfma32_fp8(i32x8 a, i32x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);

@@ -133,6 +133,75 @@ __global__ __launch_bounds__(256) void quant_rows_kernel(int M, int K, const bf1
 }
 
 // ---------------------------------------------------------------------------------
+// FP8 operands of the attention.  MX-style blocks: 32 consecutive elements share the
+// scale 2^e, e the smallest integer with max|x| <= 448 * 2^e (clamped to [-127, 127];
+// 0 for a zero block), stored biased by 127 in one byte; codes E4M3(x * 2^-e), exact
+// scaling and round to nearest even.  One thread converts 8 elements; the 4 threads of
+// a block (consecutive lanes) share its maximum through two lane exchanges.
+// ---------------------------------------------------------------------------------
+WAM_DEV int mx_exp_biased(float amax) {
+  if (!(amax > 0.f)) return 127;
+  int E;
+  const float f = frexpf(amax, &E);  // amax = f 2^E, f in [0.5, 1): amax / 2^(E-9) = 512 f
+  int e = E - 9 + (f > 0.875f ? 1 : 0);
+  e = e < -127 ? -127 : (e > 127 ? 127 : e);
+  return e + 127;
+}
+
+WAM_DEV u32x2 e4m3x8(const float* f, float mul) {
+  float y[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) y[j] = fminf(fmaxf(f[j] * mul, -448.0f), 448.0f);
+  int lo = __builtin_amdgcn_cvt_pk_fp8_f32(y[0], y[1], 0, false);
+  lo = __builtin_amdgcn_cvt_pk_fp8_f32(y[2], y[3], lo, true);
+  int hi = __builtin_amdgcn_cvt_pk_fp8_f32(y[4], y[5], 0, false);
+  hi = __builtin_amdgcn_cvt_pk_fp8_f32(y[6], y[7], hi, true);
+  return u32x2{(uint32_t)lo, (uint32_t)hi};
+}
+
+// 8 values of one 32-element block -> 8 codes; returns the block's biased exponent.
+WAM_DEV int mx_encode8(const float* f, u32x2& codes) {
+  float amax = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(f[j]));
+  amax = fmaxf(amax, __shfl_xor(amax, 1, 64));
+  amax = fmaxf(amax, __shfl_xor(amax, 2, 64));
+  const int eb = mx_exp_biased(amax);
+  codes = e4m3x8(f, ldexpf(1.0f, 127 - eb));
+  return eb;
+}
+
+__global__ __launch_bounds__(256) void quant_mx_kernel(int rows, int cols, const bf16* __restrict__ x, int64_t ldx,
+                                                       uint8_t* __restrict__ q, int64_t ldq,
+                                                       uint8_t* __restrict__ ex) {
+  const int c8 = cols >> 3;
+  const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (id >= (int64_t)rows * c8) return;  // rows * c8 is a multiple of 4: whole blocks
+  const int64_t r = id / c8;
+  const int c = (int)(id - r * c8) * 8;
+  const bf16x8 v = load_bf16x8(x + r * ldx + c);
+  float f[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = (float)v[j];
+  u32x2 codes;
+  const int eb = mx_encode8(f, codes);
+  *reinterpret_cast<u32x2*>(q + r * ldq + c) = codes;
+  if ((c & 31) == 0) ex[r * (cols >> 5) + (c >> 5)] = (uint8_t)eb;
+}
+
+// One-scale codes E4M3(x * inv), 8 elements per thread.
+__global__ __launch_bounds__(256) void quant_scaled_kernel(int64_t n8, const bf16* __restrict__ x, float inv,
+                                                           uint8_t* __restrict__ q) {
+  const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (id >= n8) return;
+  const bf16x8 v = load_bf16x8(x + id * 8);
+  float f[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = (float)v[j];
+  *reinterpret_cast<u32x2*>(q + id * 8) = e4m3x8(f, inv);
+}
+
+// ---------------------------------------------------------------------------------
 // 3D RoPE + KV append.  A thread owns 8 consecutive dims (4 rotation pairs) of one
 // head of one token and moves the q, k and v slices of the fused QKV row: q rotated
 // to q_out, k rotated and v copied into the cache rows [row0, row0 + L).
@@ -165,6 +234,53 @@ __global__ __launch_bounds__(256) void rope_qkv_kernel(const RopeArgs a) {
   const int64_t crow = ((int64_t)b * a.Lcap + a.row0 + l) * d + col;
   *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.k_cache) + crow) = ko;
   *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.v_cache) + crow) = vv;
+}
+
+// RoPE + KV append with FP8 outputs for the FP8 attention: the rotated q and k (fp32)
+// are encoded in 32-dim blocks into q8 / the K code cache with their exponents (one
+// byte per block, four per (token, head) at Dh = 128), v as E4M3(v * v_inv) into the
+// V code cache.  Same thread layout as rope_qkv_kernel: the 4 threads of a 32-dim
+// block are consecutive lanes.
+__global__ __launch_bounds__(256) void rope_qkv_fp8_kernel(const RopeFp8Args f) {
+  const RopeArgs& a = f.r;
+  const int d = a.H * a.Dh, d8 = d >> 3, d32 = d >> 5;
+  const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (id >= (int64_t)a.B * a.L * d8 || skip_step(a.skip)) return;  // whole 4-thread blocks
+  const int c = (int)(id % d8);
+  const int64_t bl = id / d8;
+  const int l = (int)(bl % a.L), b = (int)(bl / a.L);
+  const int col = c * 8;
+  const int pair0 = (col % a.Dh) >> 1;
+  const bf16* src = static_cast<const bf16*>(a.qkv) + bl * 3 * d + col;
+  const bf16x8 qv = a.q_out ? load_bf16x8(src) : bf16x8{};
+  const bf16x8 kv = load_bf16x8(src + d), vv = load_bf16x8(src + 2 * d);
+  const f32x4 cs = *reinterpret_cast<const f32x4*>(a.cos_t + (int64_t)l * (a.Dh >> 1) + pair0);
+  const f32x4 sn = *reinterpret_cast<const f32x4*>(a.sin_t + (int64_t)l * (a.Dh >> 1) + pair0);
+  float qo[8], ko[8], vo[8];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const float q0 = (float)qv[2 * p], q1 = (float)qv[2 * p + 1];
+    const float k0 = (float)kv[2 * p], k1 = (float)kv[2 * p + 1];
+    qo[2 * p] = q0 * cs[p] - q1 * sn[p];
+    qo[2 * p + 1] = q0 * sn[p] + q1 * cs[p];
+    ko[2 * p] = k0 * cs[p] - k1 * sn[p];
+    ko[2 * p + 1] = k0 * sn[p] + k1 * cs[p];
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) vo[j] = (float)vv[j];
+  const bool lead = (col & 31) == 0;
+  if (a.q_out) {  // uniform over the launch
+    u32x2 codes;
+    const int eb = mx_encode8(qo, codes);
+    *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(a.q_out) + bl * d + col) = codes;
+    if (lead) static_cast<uint8_t*>(f.q_exp)[bl * d32 + (col >> 5)] = (uint8_t)eb;
+  }
+  const int64_t crow = (int64_t)b * a.Lcap + a.row0 + l;
+  u32x2 codes;
+  const int eb = mx_encode8(ko, codes);
+  *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(a.k_cache) + crow * d + col) = codes;
+  if (lead) static_cast<uint8_t*>(f.k_exp)[crow * d32 + (col >> 5)] = (uint8_t)eb;
+  *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(a.v_cache) + crow * d + col) = e4m3x8(vo, f.v_inv);
 }
 
 // ---------------------------------------------------------------------------------
@@ -309,6 +425,31 @@ hipError_t launch_unpatchify(int32_t B, int32_t C, int32_t F, int32_t Hl, int32_
   const int64_t n = (int64_t)B * C * F * Hl * Wl;
   hipLaunchKernelGGL(unpatchify_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, B, C, F,
                      Hl, Wl, tok, out, skip);
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_mx(int32_t rows, int32_t cols, const void* x, int64_t ldx, void* q, int64_t ldq, void* ex,
+                           hipStream_t s) {
+  const int64_t n = (int64_t)rows * (cols / 8);
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(quant_mx_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, rows, cols,
+                     static_cast<const bf16*>(x), ldx, static_cast<uint8_t*>(q), ldq, static_cast<uint8_t*>(ex));
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_scaled(int64_t n, const void* x, float inv, void* q, hipStream_t s) {
+  const int64_t n8 = n / 8;
+  if (n8 == 0) return hipSuccess;
+  hipLaunchKernelGGL(quant_scaled_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, s, n8,
+                     static_cast<const bf16*>(x), inv, static_cast<uint8_t*>(q));
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_qkv_fp8(const RopeFp8Args& f, hipStream_t s) {
+  const RopeArgs& a = f.r;
+  const int64_t n = (int64_t)a.B * a.L * (a.H * a.Dh / 8);
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_qkv_fp8_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, f);
   return hipGetLastError();
 }
 

@@ -25,6 +25,18 @@ struct AttnArgs {
 };
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s);
 
+// FP8 attention (Dh = 128): a.q / a.k / a.v point at E4M3 codes (strides in bytes), a.o
+// at bf16 output; q_exp / k_exp hold one uint32 per (token, head), byte j the biased
+// exponent (scale 2^(byte - 127)) of dims [32 j, 32 j + 32), strides in uint32 units;
+// v = code * v_scale.
+struct AttnFp8Args {
+  AttnArgs a;
+  const void *q_exp, *k_exp;
+  int64_t qe_ts, qe_bs, ke_ts, ke_bs;
+  float v_scale;
+};
+hipError_t launch_attn_fp8(const AttnFp8Args& f, hipStream_t s);
+
 struct GemmArgs {
   int32_t M, N, K, epi;
   const void* A;
@@ -76,6 +88,22 @@ struct RopeArgs {
   const int32_t* skip;
 };
 hipError_t launch_rope_qkv(const RopeArgs& a, hipStream_t s);
+
+// RoPE + append for the FP8 attention (Dh = 128): r.q_out -> q codes [B*L][d] bytes with
+// q_exp [B*L][d/32] bytes, r.k_cache / r.v_cache -> E4M3 code caches [B][Lcap][d] bytes
+// with k_exp [B][Lcap][d/32] bytes (32-dim blocks, biased exponents); v codes E4M3(v * v_inv).
+struct RopeFp8Args {
+  RopeArgs r;
+  void *q_exp, *k_exp;
+  float v_inv;
+};
+hipError_t launch_rope_qkv_fp8(const RopeFp8Args& f, hipStream_t s);
+// MX-style E4M3 codes of bf16 rows [rows][ldx] (cols % 32 == 0): q [rows][ldq] bytes,
+// ex [rows][cols/32] biased block exponents.
+hipError_t launch_quant_mx(int32_t rows, int32_t cols, const void* x, int64_t ldx, void* q, int64_t ldq, void* ex,
+                           hipStream_t s);
+// One-scale E4M3 codes q[i] = E4M3(x[i] * inv) of n bf16 values (n % 8 == 0).
+hipError_t launch_quant_scaled(int64_t n, const void* x, float inv, void* q, hipStream_t s);
 
 // out[b][n] = act(x[b][:]) . W[n][:] + bias[n]  (fp32 in/out, bf16 W [N][K])
 enum { GEMV_ACT_NONE = 0, GEMV_ACT_SILU = 1 };

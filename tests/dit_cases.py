@@ -147,8 +147,32 @@ class StepCase:
         self.dz, self.da, self.dt, self.dtext = dev(self.z), dev(self.a), dev(self.t), dev(self.text)
         self.dta = dev(self.t_action) if self.t_action is not None else None
 
-    def run_gpu(self, events=None, t_action=None):
-        """t_action: a device [B] timestep overriding the case's own (None: the case's)."""
+    def make_fp8_cache(self):
+        """E4M3 code caches of the current bf16 caches, through the library's quantizers:
+        K in 32-dim blocks, V with one scale per layer, max|V| / 448 over the rows a step
+        reads and writes (taken after a step with the bf16 cache, a calibration pass)."""
+        import torch
+        w = lib()
+        rows = self.wl.cache_rows + self.wl.L
+        self.k8s, self.kes, self.v8s, self.vsc = [], [], [], []
+        for kc, vc in zip(self.kcs, self.vcs):
+            Bc, Lcap, H, Dh = kc.shape
+            k8 = torch.empty((Bc, Lcap, H, Dh), dtype=torch.uint8, device="cuda")
+            ke = torch.empty((Bc, Lcap, H), dtype=torch.int32, device="cuda")
+            w.wam_quantize_mx_fp8(kc.view(Bc * Lcap, H * Dh), k8.view(Bc * Lcap, H * Dh),
+                                  ke.view(torch.uint8).view(Bc * Lcap, H * 4))
+            vs = float(vc[:, :rows].abs().max().float()) / 448.0
+            v8 = torch.empty_like(k8)
+            w.wam_quantize_scaled_fp8(vc, vs, v8)
+            self.k8s.append(k8)
+            self.kes.append(ke)
+            self.v8s.append(v8)
+            self.vsc.append(vs)
+        torch.cuda.synchronize()
+
+    def run_gpu(self, events=None, t_action=None, fp8_cache=False):
+        """t_action: a device [B] timestep overriding the case's own (None: the case's);
+        fp8_cache: run on the E4M3 caches of make_fp8_cache (FP8 self-attention)."""
         import torch
         w = lib()
         wl, B = self.wl, self.wl.B
@@ -156,9 +180,11 @@ class StepCase:
             self.upload()
         vv = torch.empty((B, wl.latent_ch, wl.F, wl.Hl, wl.Wl), dtype=torch.float32, device="cuda")
         va = torch.empty((B, wl.A, wl.act_dim), dtype=torch.float32, device="cuda")
-        io = w.make_step_io(self.dz, self.da, self.dt, self.dtext, self.kcs, self.vcs, self.cos, self.sin,
+        kcs, vcs = (self.k8s, self.v8s) if fp8_cache else (self.kcs, self.vcs)
+        io = w.make_step_io(self.dz, self.da, self.dt, self.dtext, kcs, vcs, self.cos, self.sin,
                             wl.cache_rows, w.cached_chunks(wl.cache_rows, wl.L), vv, va, events=events,
-                            t_action=t_action if t_action is not None else self.dta)
+                            t_action=t_action if t_action is not None else self.dta,
+                            k_exps=self.kes if fp8_cache else None, v_scales=self.vsc if fp8_cache else None)
         ws = workspace(w.wam_step_workspace_bytes(self.model, io))
         w.wam_dit_step_fwd(self.model, io, ws)
         torch.cuda.synchronize()

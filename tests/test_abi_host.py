@@ -32,7 +32,7 @@ def test_library_exports_every_declared_function():
     for name in declared:
         assert hasattr(L, name), name
     assert sorted(w.binding.EXPORTED) == declared
-    assert w.wam_abi_version() == 4
+    assert w.wam_abi_version() == 5
 
 
 def test_struct_sizes_match_the_header_layout():
@@ -45,7 +45,8 @@ def test_struct_sizes_match_the_header_layout():
     # sizes printed by a C++ compile of include/wamdit.h
     assert C.sizeof(b.wam_flow_dims) == 32
     assert C.sizeof(b.wam_denoise_params) == 48
-    assert C.sizeof(b.wam_step_io) == 344
+    assert C.sizeof(b.wam_step_io) == 360
+    assert C.sizeof(b.wam_block_io) == 312
     assert C.sizeof(b.wam_model) == 200
 
 
