@@ -41,6 +41,8 @@ def parse():
     p.add_argument("--probe-attn", type=int, default=0, metavar="N",
                    help="counter-collection mode: one plain 1 GiB device copy, then N self-attention "
                         "launches at the workload's shape; prints what ran and exits")
+    p.add_argument("--probe-attn-fp8", type=int, default=0, metavar="N",
+                   help="the same with the FP8 self-attention (operands quantized by the library)")
     return p.parse_args()
 
 
@@ -285,6 +287,42 @@ def probe_attn(wl, n):
                       "q": list(q.shape), "kv": list(k.shape)}), flush=True)
 
 
+def probe_attn_fp8(wl, n):
+    """The same as probe_attn for the FP8 attention: the calibration copy, the operands
+    quantized by the library (MX blocks for q and k, one scale for v), then n FP8
+    self-attention launches of the step's shape."""
+    import torch
+    import paper_2602_15922_amd as w
+    torch.cuda.set_device(0)
+    g = torch.Generator(device="cuda").manual_seed(7)
+    copy_bytes = 1 << 30
+    src = torch.randn(copy_bytes // 2, generator=g, device="cuda", dtype=torch.bfloat16)
+    dst = torch.empty_like(src)
+    B, L, Lk, H, Dh = wl.B, wl.L, wl.Lk, wl.H, wl.Dh
+    ops = {}
+    for name, rows in (("q", L), ("k", Lk)):
+        x = torch.randn(B * rows, H * Dh, generator=g, device="cuda", dtype=torch.bfloat16)
+        c = torch.empty((B, rows, H, Dh), dtype=torch.uint8, device="cuda")
+        e = torch.empty((B, rows, H), dtype=torch.int32, device="cuda")
+        w.wam_quantize_mx_fp8(x, c.view(B * rows, H * Dh), e.view(torch.uint8).view(B * rows, H * 4))
+        ops[name] = (c, e)
+    v = torch.randn(B, Lk, H, Dh, generator=g, device="cuda", dtype=torch.bfloat16)
+    vs = float(v.abs().max().float()) / 448.0
+    v8 = torch.empty((B, Lk, H, Dh), dtype=torch.uint8, device="cuda")
+    w.wam_quantize_scaled_fp8(v, vs, v8)
+    o = torch.empty((B, L, H, Dh), dtype=torch.bfloat16, device="cuda")
+    chunks = w.cached_chunks(wl.cache_rows, L)
+    torch.cuda.synchronize()
+    torch.mul(src, 1, out=dst)
+    torch.cuda.synchronize()
+    for _ in range(n):
+        w.wam_attn_blockcausal_fp8(ops["q"][0], ops["q"][1], ops["k"][0], ops["k"][1], v8, vs, o, chunks)
+    torch.cuda.synchronize()
+    assert torch.isfinite(o).all()
+    print(json.dumps({"probe": "attn_fp8", "workload": wl.name, "copy_bytes": copy_bytes, "attn_launches": n,
+                      "q": [B, L, H, Dh], "kv": [B, Lk, H, Dh]}), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -299,6 +337,8 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     if args.probe_attn:
         return probe_attn(wl, args.probe_attn)
+    if args.probe_attn_fp8:
+        return probe_attn_fp8(wl, args.probe_attn_fp8)
     torch.cuda.set_device(0)
     model, keep, kcs, vcs, inp = build_model(wl, torch)
     B, d = wl.B, wl.d

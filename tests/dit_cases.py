@@ -51,6 +51,30 @@ def upload_cache(wl, kc, vc, B):
 
 
 # ------------------------------------------------------------------------------ block
+def fp8_caches(kcs, vcs, rows):
+    """E4M3 code caches of bf16 caches [B, Lcap, H, 128] through the library's quantizers:
+    K in 32-dim blocks (int32 exponent words [B, Lcap, H]), V with one scale per layer,
+    max|V| / 448 over rows [0, rows).  Returns (k8s, kes, v8s, v_scales)."""
+    import torch
+    w = lib()
+    k8s, kes, v8s, vsc = [], [], [], []
+    for kc, vc in zip(kcs, vcs):
+        Bc, Lcap, H, Dh = kc.shape
+        k8 = torch.empty((Bc, Lcap, H, Dh), dtype=torch.uint8, device="cuda")
+        ke = torch.empty((Bc, Lcap, H), dtype=torch.int32, device="cuda")
+        w.wam_quantize_mx_fp8(kc.view(Bc * Lcap, H * Dh), k8.view(Bc * Lcap, H * Dh),
+                              ke.view(torch.uint8).view(Bc * Lcap, H * 4))
+        vs = float(vc[:, :rows].abs().max().float()) / 448.0
+        v8 = torch.empty_like(k8)
+        w.wam_quantize_scaled_fp8(vc, vs, v8)
+        k8s.append(k8)
+        kes.append(ke)
+        v8s.append(v8)
+        vsc.append(vs)
+    torch.cuda.synchronize()
+    return k8s, kes, v8s, vsc
+
+
 class BlockCase:
     """One block over the current chunk of `wl`, given x, e0, ctx and the cache."""
 
@@ -148,27 +172,9 @@ class StepCase:
         self.dta = dev(self.t_action) if self.t_action is not None else None
 
     def make_fp8_cache(self):
-        """E4M3 code caches of the current bf16 caches, through the library's quantizers:
-        K in 32-dim blocks, V with one scale per layer, max|V| / 448 over the rows a step
-        reads and writes (taken after a step with the bf16 cache, a calibration pass)."""
-        import torch
-        w = lib()
-        rows = self.wl.cache_rows + self.wl.L
-        self.k8s, self.kes, self.v8s, self.vsc = [], [], [], []
-        for kc, vc in zip(self.kcs, self.vcs):
-            Bc, Lcap, H, Dh = kc.shape
-            k8 = torch.empty((Bc, Lcap, H, Dh), dtype=torch.uint8, device="cuda")
-            ke = torch.empty((Bc, Lcap, H), dtype=torch.int32, device="cuda")
-            w.wam_quantize_mx_fp8(kc.view(Bc * Lcap, H * Dh), k8.view(Bc * Lcap, H * Dh),
-                                  ke.view(torch.uint8).view(Bc * Lcap, H * 4))
-            vs = float(vc[:, :rows].abs().max().float()) / 448.0
-            v8 = torch.empty_like(k8)
-            w.wam_quantize_scaled_fp8(vc, vs, v8)
-            self.k8s.append(k8)
-            self.kes.append(ke)
-            self.v8s.append(v8)
-            self.vsc.append(vs)
-        torch.cuda.synchronize()
+        """E4M3 code caches of the current bf16 caches (fp8_caches), V's scale over the rows
+        a step reads and writes (taken after a step with the bf16 cache, a calibration pass)."""
+        self.k8s, self.kes, self.v8s, self.vsc = fp8_caches(self.kcs, self.vcs, self.wl.cache_rows + self.wl.L)
 
     def run_gpu(self, events=None, t_action=None, fp8_cache=False):
         """t_action: a device [B] timestep overriding the case's own (None: the case's);
@@ -249,9 +255,10 @@ class UpdateCase:
         self.model = w.make_model(dims_of(wl, self.n_layers), self.top, self.blocks)
         self.dz, self.da, self.dt, self.dtext = dev(self.z), dev(self.a), dev(self.t), dev(self.text)
 
-    def run_gpu(self, chunks_at_once=None):
+    def run_gpu(self, chunks_at_once=None, fp8_cache=None):
         """Appends the new chunks `chunks_at_once` at a time (default: all in one call).
-        Returns the per-layer device caches."""
+        Returns the per-layer device caches.  fp8_cache: (k8s, kes, v8s, v_scales) E4M3
+        caches to append to instead of the bf16 ones (then those are returned)."""
         import torch
         w = lib()
         wl = self.wl
@@ -266,10 +273,15 @@ class UpdateCase:
             cos, sin = dev(cos), dev(sin)
             z = self.dz[:, :, c0 * wl.F:(c0 + len(ids)) * wl.F].contiguous()
             chunks = w.append_chunks([wl.L] * (wl.n_cached + c0), [wl.L] * len(ids))
-            io = w.make_step_io(z, self.da, self.dt, self.dtext, self.kcs, self.vcs, cos, sin, cache_len,
-                                chunks, None, None)
+            if fp8_cache is None:
+                io = w.make_step_io(z, self.da, self.dt, self.dtext, self.kcs, self.vcs, cos, sin, cache_len,
+                                    chunks, None, None)
+            else:
+                k8s, kes, v8s, vsc = fp8_cache
+                io = w.make_step_io(z, self.da, self.dt, self.dtext, k8s, v8s, cos, sin, cache_len, chunks, None,
+                                    None, k_exps=kes, v_scales=vsc)
             ws = workspace(w.wam_update_workspace_bytes(self.model, io))
             w.wam_dit_update_fwd(self.model, io, ws)
             torch.cuda.synchronize()
             cache_len += len(ids) * wl.L
-        return self.kcs, self.vcs
+        return (self.kcs, self.vcs) if fp8_cache is None else (fp8_cache[0], fp8_cache[2])

@@ -128,3 +128,37 @@ def test_loader_fails_loudly_without_the_library(monkeypatch, tmp_path):
     monkeypatch.setattr(w.binding, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         w.binding.lib()
+
+
+def test_fp8_entry_points_reject_bad_arguments_without_a_gpu():
+    """Every check below fails before any launch (fake device addresses, no GPU)."""
+    w = lib()
+    b = w.binding
+    L = w.lib()
+
+    def attn(Dh=128, v_scale=1.0, q=4096, qe=8192, k=12288, ke=16384, v=20480, o=24576, **kw):
+        d = b.wam_attn_desc(B=1, H=2, Dh=Dh, Lq=10, Lk=20, q_tok_stride=256, q_batch_stride=2560,
+                            kv_tok_stride=256, kv_batch_stride=5120, o_tok_stride=256, o_batch_stride=2560,
+                            scale=0.0, ch=w.make_chunks([10, 10], [10], [1]))
+        for k_, v_ in kw.items():
+            setattr(d, k_, v_)
+        return L.wam_attn_blockcausal_fp8(C.byref(d), q, qe, k, ke, v, v_scale, o, None)
+
+    assert attn(Dh=64) == b.WAM_EUNSUPPORTED
+    assert attn(v_scale=0.0) == b.WAM_EINVAL and b"v_scale" in L.wam_last_error()
+    assert attn(v_scale=float("nan")) == b.WAM_EINVAL
+    assert attn(qe=0) == b.WAM_EINVAL and b"q_exp is NULL" in L.wam_last_error()
+    assert attn(q=4100) == b.WAM_EINVAL and b"aligned" in L.wam_last_error()
+    assert attn(ke=8194) == b.WAM_EINVAL and b"aligned" in L.wam_last_error()
+    assert attn(q_tok_stride=320) == b.WAM_EINVAL  # not a multiple of Dh bytes
+    assert attn(Lk=21) == b.WAM_EINVAL  # chunks do not cover Lk
+    q = L.wam_quantize_mx_fp8
+    assert q(4, 33, 4096, 40, 8192, 40, 12288, None) == b.WAM_EINVAL  # cols % 32
+    assert q(4, 64, 4096, 68, 8192, 64, 12288, None) == b.WAM_EINVAL  # ldx % 8
+    assert q(4, 64, 4100, 64, 8192, 64, 12288, None) == b.WAM_EINVAL  # x alignment
+    assert L.wam_quantize_scaled_fp8(7, 4096, 1.0, 8192, None) == b.WAM_EINVAL
+    assert L.wam_quantize_scaled_fp8(8, 4096, -1.0, 8192, None) == b.WAM_EINVAL
+    r = L.wam_rope_qkv_fp8
+    assert r(1, 4, 2, 64, 4096, 8192, 8192, 0, 0, 12288, 16384, 20480, 1.0, 8, 0, None) == b.WAM_EUNSUPPORTED
+    assert r(1, 4, 2, 128, 4096, 8192, 8192, 24576, 0, 12288, 16384, 20480, 1.0, 8, 0, None) == b.WAM_EINVAL
+    assert r(1, 4, 2, 128, 4096, 8192, 8192, 0, 0, 12288, 16384, 20480, 1.0, 8, 5, None) == b.WAM_EINVAL  # row0+L>Lcap

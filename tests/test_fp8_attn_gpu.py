@@ -315,3 +315,39 @@ def test_fp8_cache_step_14b_shapes_one_block(fp8_proj):
     ev, ea = rel_l2(host(vv), rv), rel_l2(host(va), ra)
     print(f"  fp8 cache step rel L2 video {ev:.3e} action {ea:.3e}", flush=True)
     assert ev <= FP8_TOL_STEP and ea <= FP8_TOL_STEP
+
+
+def test_fp8_cache_update_pass_14b_shapes():
+    """The cache-update pass writing an FP8 cache at the 14B block shapes: 3120 clean video
+    rows after two cached chunks (9360 keys), two layers (a full block with the FP8
+    self-attention, then the K/V-only last layer).  The appended K (decoded blocks) and V
+    (codes times the layer's scale) against the oracle's unquantized pass; the cached rows'
+    codes untouched.  V's scales come from a bf16 pass over the same rows (calibration),
+    whose appended rows are then cleared from the FP8 caches."""
+    import torch
+    from dit_cases import UpdateCase, fp8_caches
+    wl = synth.WORKLOADS["block_14b"].replace(A=0, n_cached=2, n_layers=2)
+    log("fp8 update 14b: inputs + calibration pass")
+    case = UpdateCase(wl, 2, 1)
+    case.upload()
+    case.run_gpu()
+    r0, r1 = wl.cache_rows, wl.cache_rows + case.L
+    k8s, kes, v8s, vsc = fp8_caches(case.kcs, case.vcs, r1)
+    before = [(k8[:, :r0].clone(), ke[:, :r0].clone(), v8[:, :r0].clone()) for k8, ke, v8 in zip(k8s, kes, v8s)]
+    for k8, ke, v8 in zip(k8s, kes, v8s):
+        k8[:, r0:].zero_()
+        ke[:, r0:].zero_()
+        v8[:, r0:].zero_()
+    log("fp8 update 14b: GPU")
+    case.run_gpu(fp8_cache=(k8s, kes, v8s, vsc))
+    log("fp8 update 14b: oracle")
+    ref = case.run_oracle()
+    for l, (k_ref, v_ref) in enumerate(ref):
+        kd = oracle.fp8.decode_mx(decode(k8s[l][:, r0:r1]), exps_host(kes[l][:, r0:r1]))
+        vd = decode(v8s[l][:, r0:r1]) * vsc[l]
+        ek, ev = rel_l2(kd, k_ref), rel_l2(vd, v_ref)
+        print(f"  layer {l}: appended K rel L2 {ek:.2e}, V {ev:.2e}", flush=True)
+        assert ek <= FP8_TOL_STEP and ev <= FP8_TOL_STEP
+        k8, ke, v8 = before[l]
+        assert torch.equal(k8s[l][:, :r0], k8) and torch.equal(kes[l][:, :r0], ke) and torch.equal(v8s[l][:, :r0], v8)
+        assert not k8s[l][:, r1:].any() and not v8s[l][:, r1:].any()
