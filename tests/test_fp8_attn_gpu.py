@@ -274,6 +274,51 @@ def test_attention_fp8_full_size_sampled_rows():
     assert err <= TOL_RANDOM
 
 
+def test_attention_fp8_b2_3view_sampled_rows():
+    """The two-sample, three-view configuration: batch 2, 9392 queries of chunk 6 against
+    65744 keys, 40 heads of 128.  Inputs are drawn on the device from seeded streams and
+    quantized by the library's own quantizers (bit-exact against the oracle's above); the
+    fp64 oracle attends with the decoded operands on sampled query rows of both samples,
+    every head, all keys."""
+    import torch
+    w = lib()
+    wl = synth.WORKLOADS["step_14b_b2_3view"]
+    B, H, Dh, L, Lk = wl.B, wl.H, wl.Dh, wl.L, wl.Lk
+    log(f"attn fp8 b2 3-view B={B} Lq={L} Lk={Lk}: inputs")
+    ops = {}
+    for name, rows in (("q", L), ("k", Lk)):
+        x = synth.device_normal(wl.seed, name, (B, rows, H, Dh))
+        c = torch.empty((B, rows, H, Dh), dtype=torch.uint8, device="cuda")
+        e = torch.empty((B, rows, H), dtype=torch.int32, device="cuda")
+        w.wam_quantize_mx_fp8(x.view(B * rows, H * Dh), c.view(B * rows, H * Dh),
+                              e.view(torch.uint8).view(B * rows, H * 4))
+        ops[name] = (c, e)
+        del x
+    v = synth.device_normal(wl.seed, "v", (B, Lk, H, Dh))
+    vs = float(v.abs().max().float()) / 448.0
+    v8 = torch.empty((B, Lk, H, Dh), dtype=torch.uint8, device="cuda")
+    w.wam_quantize_scaled_fp8(v, vs, v8)
+    del v
+    log("attn fp8 b2 3-view: GPU")
+    o = torch.empty((B, L, H, Dh), dtype=torch.bfloat16, device="cuda")
+    w.wam_attn_blockcausal_fp8(ops["q"][0], ops["q"][1], ops["k"][0], ops["k"][1], v8, vs, o,
+                               w.cached_chunks(wl.cache_rows, L))
+    torch.cuda.synchronize()
+    g = np.random.default_rng(4)
+    rows = np.unique(np.concatenate([[0, 127, 128, 9215, 9216, L - 1], g.integers(0, L, 18)]))
+    kc = np.repeat(np.arange(wl.n_cached + 1), L)
+    for b in range(B):
+        log(f"attn fp8 b2 3-view: oracle, sample {b}")
+        qd = oracle.fp8.decode_mx(decode(ops["q"][0][b, rows]), exps_host(ops["q"][1][b, rows]))
+        kd = oracle.fp8.decode_mx(decode(ops["k"][0][b]), exps_host(ops["k"][1][b]))
+        vd = decode(v8[b]) * vs
+        ref = oracle.attention(qd, kd, vd, np.full(len(rows), wl.n_cached), kc)
+        err = rel_l2(host(o[b, rows]), ref)
+        print(f"  sample {b}: {len(rows)} rows, rel L2 {err:.2e}", flush=True)
+        assert err <= TOL_RANDOM
+        del kd, vd
+
+
 def test_attention_fp8_rejects_bad_arguments():
     import torch
     w = lib()
