@@ -19,7 +19,8 @@
 // statistics stay in the lane (plus the partner lane l^32 holding the other half of
 // the keys); the output is accumulated transposed as well, O^T = V^T P^T, so the
 // rescale is lane-local too.  V stays row-major in LDS and its transposed MFMA
-// operand is read with the gfx950 transposing LDS load (ds_read_b64_tr_b16).  The
+// operand is read with the gfx950 transposing LDS load (ds_read_b64_tr_b16, issued as
+// asm two MFMAs ahead so it waits on nothing but its own LDS reads).  The
 // reference maximum is only raised when a tile exceeds it by more than 2^8 in the
 // exp2 domain, which leaves the result exact (o = acc / l for any reference) and skips
 // almost every accumulator rescale.  Both tiles are XOR-swizzled in 16-byte chunks so
@@ -37,7 +38,6 @@ constexpr int NT = 256;  // threads per workgroup
 constexpr float RESCALE_LOG2 = 8.0f;  // allowed growth of exp2 arguments before a rescale
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
 // The value held by lane l ^ 32 (the lane with the same query and the other half of the
@@ -96,6 +96,65 @@ WAM_DEV void fetch_tile(bf16* Ks, __amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsr
       __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void*)(Vs + base * 8), 16, voff[i] + shift, soff, 0, 0);
     }
   }
+}
+
+// V^T fragments through inline asm.  The compiler cannot prove that these LDS reads miss
+// the direct-to-LDS prefetch of the next tile still in flight, so before its own form of
+// the transposing read it waits for all outstanding vector memory, i.e. for the next
+// tile's loads, every tile.  Issued as asm, the reads wait only on the LDS counter, which
+// the code below sets itself: the reads of P.V MFMA i+2 are issued before MFMA i, which
+// then waits until at most the 4 younger reads are outstanding (LDS reads complete in
+// order).  The asm results are tied through the wait so nothing reads them earlier.
+template <int OFF>
+WAM_DEV s16x4 tr16(unsigned addr) {
+  s16x4 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+WAM_DEV unsigned lds_addr(const void* p) {
+  return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char*)(p);
+}
+template <int N>
+WAM_DEV void wait_lgkm(s16x4& a, s16x4& b) {
+  asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(a), "+v"(b) : "i"(N));
+}
+
+// the two reads of P.V MFMA i = (mt, nt, hf): keys 32 nt + 16 hf + (0..7, 8..15) of dims
+// 32 mt + (lane's 4), from the lane's base address of output tile mt
+template <int DH, int I>
+WAM_DEV void vread(const unsigned* va, s16x4* lo, s16x4* hi) {
+  constexpr int ROWB = DH * 2, mt = I >> 2, nt = (I >> 1) & 1, hf = I & 1, off = (32 * nt + 16 * hf) * ROWB;
+  lo[I % 3] = tr16<off>(va[mt]);
+  hi[I % 3] = tr16<off + 8 * ROWB>(va[mt]);
+}
+
+template <int DH, int I>
+WAM_DEV void pv_steps(const unsigned* va, s16x4* lo, s16x4* hi, const bf16x8 (*pb)[2], f32x16* acc) {
+  constexpr int NMF = DH / 8, mt = I >> 2, nt = (I >> 1) & 1, hf = I & 1;  // NMF = 4 MT MFMAs
+  if constexpr (I + 2 < NMF) {
+    vread<DH, I + 2>(va, lo, hi);
+    wait_lgkm<4>(lo[I % 3], hi[I % 3]);
+  } else if constexpr (I + 1 < NMF) {
+    wait_lgkm<2>(lo[I % 3], hi[I % 3]);
+  } else {
+    wait_lgkm<0>(lo[I % 3], hi[I % 3]);
+  }
+  const s16x4 v8[2] = {lo[I % 3], hi[I % 3]};
+  acc[mt] = mfma32(*reinterpret_cast<const bf16x8*>(v8), pb[nt][hf], acc[mt]);
+  if constexpr (I + 1 < NMF) pv_steps<DH, I + 1>(va, lo, hi, pb, acc);
+}
+
+// O^T += V^T P^T for one tile: 4 MT MFMAs, each with its two transposing V reads
+template <int DH>
+WAM_DEV void pv_tile(const char* Vs, const int* vofs, const bf16x8 (*pb)[2], f32x16* acc) {
+  constexpr int MT = DH / 32;
+  unsigned va[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) va[mt] = lds_addr(Vs + vofs[mt]);
+  s16x4 lo[3], hi[3];
+  vread<DH, 0>(va, lo, hi);
+  vread<DH, 1>(va, lo, hi);
+  pv_steps<DH, 0>(va, lo, hi, pb, acc);
 }
 
 // One 64-key tile for one wavefront's 32 queries: S^T = K Q^T, optional prefix mask,
@@ -157,18 +216,7 @@ WAM_DEV void attn_tile(const char* Ks, const char* Vs, const bf16x8* qf, f32x16*
         const bf16x2 pr = {pb[nt][hf][2 * e], pb[nt][hf][2 * e + 1]};
         l_part = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, l_part, false);
       }
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        const char* vr = Vs + vofs[mt] + (32 * nt + 16 * hf) * ROWB;
-        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vr));
-        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vr + 8 * ROWB));
-        const s16x4 v8[2] = {lo, hi};
-        acc[mt] = mfma32(*reinterpret_cast<const bf16x8*>(v8), pb[nt][hf], acc[mt]);
-      }
+  pv_tile<DH>(Vs, vofs, pb, acc);
 }
 
 // Wait for this wave's direct loads of the next tile, then sync the workgroup.
