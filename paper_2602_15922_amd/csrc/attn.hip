@@ -144,6 +144,55 @@ WAM_DEV void pv_steps(const unsigned* va, s16x4* lo, s16x4* hi, const bf16x8 (*p
   if constexpr (I + 1 < NMF) pv_steps<DH, I + 1>(va, lo, hi, pb, acc);
 }
 
+// K fragments of the score MFMAs, likewise as asm: the compiler's schedule issued each
+// read one MFMA ahead of its use, exposing the LDS latency once the tile's other stall was
+// gone; here the read of score MFMA i+3 is issued before MFMA i (measured best of 2, 3, 5
+// and 7 ahead).  Score MFMA i = (ks = i/2, nt = i%2) alternates the two accumulators.
+constexpr int KAHEAD = 3;
+template <int OFF>
+WAM_DEV bf16x8 kread(unsigned addr) {
+  bf16x8 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+template <int N>
+WAM_DEV void wait_k(bf16x8& a) {
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(a) : "i"(N));
+}
+template <int DH, int I>
+WAM_DEV void kload(const unsigned* ka, bf16x8* kf) {
+  constexpr int ks = I >> 1, nt = I & 1;
+  kf[I % (KAHEAD + 1)] = kread<nt * 32 * DH * 2>(ka[ks]);
+}
+template <int DH, int I>
+WAM_DEV void score_steps(const unsigned* ka, bf16x8* kf, const bf16x8* qf, f32x16* s) {
+  constexpr int NS = DH / 8, ks = I >> 1, nt = I & 1;  // NS = 2 KS score MFMAs
+  if constexpr (I + KAHEAD < NS) {
+    kload<DH, I + KAHEAD>(ka, kf);
+    wait_k<KAHEAD>(kf[I % (KAHEAD + 1)]);
+  } else {
+    wait_k<NS - 1 - I>(kf[I % (KAHEAD + 1)]);
+  }
+  s[nt] = mfma32(kf[I % (KAHEAD + 1)], qf[ks], s[nt]);
+  if constexpr (I + 1 < NS) score_steps<DH, I + 1>(ka, kf, qf, s);
+}
+template <int DH, int I>
+WAM_DEV void kloads(const unsigned* ka, bf16x8* kf) {
+  kload<DH, I>(ka, kf);
+  if constexpr (I + 1 < KAHEAD) kloads<DH, I + 1>(ka, kf);
+}
+// S^T = K Q^T for one tile (keys 0..31 into s[0], 32..63 into s[1])
+template <int DH>
+WAM_DEV void scores_tile(const char* Ks, const int* kofs, const bf16x8* qf, f32x16* s) {
+  constexpr int KS = DH / 16;
+  unsigned ka[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) ka[ks] = lds_addr(Ks + kofs[ks]);
+  bf16x8 kf[KAHEAD + 1];
+  kloads<DH, 0>(ka, kf);
+  score_steps<DH, 0>(ka, kf, qf, s);
+}
+
 // O^T += V^T P^T for one tile: 4 MT MFMAs, each with its two transposing V reads
 template <int DH>
 WAM_DEV void pv_tile(const char* Vs, const int* vofs, const bf16x8 (*pb)[2], f32x16* acc) {
@@ -166,15 +215,9 @@ template <int DH, bool MASK>
 WAM_DEV void attn_tile(const char* Ks, const char* Vs, const bf16x8* qf, f32x16* acc, float& m_ref,
                        float& l_part, const int* kofs, const int* vofs, float c, float thr, int kb,
                        int row_kend, int hh) {
-  constexpr int KS = DH / 16, MT = DH / 32, ROWB = DH * 2;  // ROWB: bytes per K/V row
+  constexpr int MT = DH / 32;
   f32x16 s[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-  for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + kofs[ks] + nt * 32 * ROWB);
-      s[nt] = mfma32(kf, qf[ks], s[nt]);
-    }
+  scores_tile<DH>(Ks, kofs, qf, s);
   if (MASK) {
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt)
