@@ -26,5 +26,6 @@ from .rope import rope_split, rope_angles, apply_rope, chunk_positions  # noqa: 
 from .attention import attention  # noqa: F401
 from .model import (time_embedding, text_projection, patchify, unpatchify,  # noqa: F401
                     embed, dit_block, head, dit_step, dit_update)
-from .denoise import euler_step, cfg_combine, cosine_similarity, denoise  # noqa: F401
+from .denoise import (euler_step, cfg_combine, cosine_similarity, denoise,  # noqa: F401
+                      unipc_lambda, unipc_update, unipc_denoise)
 from . import fp8  # noqa: F401

@@ -750,6 +750,119 @@ def test_dit_caching_skips_a_window_after_similar_velocities():
     assert all(computed)
 
 
+def _gauss_flow(mu, sd, z):
+    """Straight-path flow of Eq. 2 from N(0, 1) noise to N(mu, sd^2) data: its exact
+    velocity field E[x1 - x0 | x_t] and the closed-form trajectory x_t = t mu +
+    sqrt(t^2 sd^2 + (1 - t)^2) z of the noise sample z."""
+    var = lambda t: t * t * sd * sd + (1 - t) ** 2
+    vel = lambda x, t: mu + (t * sd * sd - (1 - t)) / var(t) * (x - t * mu)
+    path = lambda t: t * mu + np.sqrt(var(t)) * z
+    return vel, path
+
+
+def _lambda_grid(t0, t1, n):
+    lam = np.linspace(math.log(t0 / (1 - t0)), math.log(t1 / (1 - t1)), n + 1)
+    return [float(v) for v in 1 / (1 + np.exp(-lam))]
+
+
+def test_unipc_predictor_of_order_one_is_euler():
+    """UniP-1 on the straight path (no corrector) is the explicit Euler step: for any
+    velocity field, state by state."""
+    g = np.random.default_rng(175)
+    x0 = g.standard_normal(6)
+    vel = lambda x, t: np.sin(3 * x) + t * x - 0.5
+    ts = [0.02, 0.1, 0.25, 0.5, 0.8, 0.97, 1.0]
+    xe, _ = oracle.denoise(x0, vel, ts)
+    xu, _ = oracle.unipc_denoise(x0, vel, ts, order=1, corrector=False)
+    assert np.allclose(xu, xe, rtol=1e-13, atol=1e-13)
+    assert np.allclose(oracle.unipc_update(x0, 0.3, 0.55, x0 + 0.7 * vel(x0, 0.3)),
+                       oracle.euler_step(x0, vel(x0, 0.3), 0.3, 0.55), atol=1e-14)
+
+
+def test_unipc_update_is_exact_for_polynomial_data_predictions():
+    """With data predictions m(lambda) a polynomial P of degree K in lambda = log(t/(1-t)),
+    the ODE dx/dt = (m - x)/(1 - t) integrates in closed form, x_t / sigma_t - x_s / sigma_s
+    = F(lambda_t) - F(lambda_s) with F = e^lambda sum_k (-1)^k P^(k) (repeated integration
+    by parts); one UniPC update with K other data predictions reproduces it, whether the
+    points lie before t_s (predictor) or include t itself (corrector)."""
+    g = np.random.default_rng(176)
+    lam = lambda t: math.log(t / (1 - t))
+    for K in range(4):
+        c = g.standard_normal((K + 1, 3))                      # P(lambda) = sum_j c_j lambda^j
+        P = lambda u: sum(c[j] * u ** j for j in range(K + 1))
+
+        def F(u):
+            out, d = 0.0, c.copy()
+            for k in range(K + 1):
+                out = out + (-1) ** k * sum(d[j] * u ** j for j in range(len(d)))
+                d = np.array([j * d[j] for j in range(1, len(d))]) if len(d) > 1 else np.zeros((0, 3))
+            return math.exp(u) * out
+
+        x_s = g.standard_normal(3)
+        for t_s, t, pts in ((0.4, 0.62, [0.3, 0.21, 0.1]), (0.4, 0.62, [0.62, 0.3, 0.21]),
+                            (0.15, 0.5, [0.5, 0.08, 0.04])):
+            pts = pts[:K]
+            exact = (1 - t) * (x_s / (1 - t_s) + F(lam(t)) - F(lam(t_s)))
+            got = oracle.unipc_update(x_s, t_s, t, P(lam(t_s)), [(tj, P(lam(tj))) for tj in pts])
+            assert np.allclose(got, exact, rtol=1e-9, atol=1e-9), (K, t_s, t, pts)
+
+
+def test_unipc_constant_data_prediction_is_exact_at_every_order():
+    """Straight paths to one clean sample (m constant): every order lands on the path at
+    every corrected state and returns the clean sample at t = 1."""
+    g = np.random.default_rng(177)
+    x1, z = g.standard_normal(5), g.standard_normal(5)
+    ts = [0.05, 0.2, 0.45, 0.7, 0.9, 1.0]
+    for order in (1, 2, 3):
+        states = []
+        xN, computed = oracle.unipc_denoise(ts[0] * x1 + (1 - ts[0]) * z, lambda x, t: (x1 - x) / (1 - t), ts,
+                                            order=order, states=states)
+        assert np.allclose(xN, x1, atol=1e-12) and all(computed) and len(states) == len(ts) - 2
+        for i, st in enumerate(states, start=1):
+            assert np.allclose(st, ts[i] * x1 + (1 - ts[i]) * z, atol=1e-12)
+
+
+def test_unipc_converges_at_order_p_plus_one():
+    """On Gaussian data, whose flow is known in closed form, halving the steps of a grid
+    uniform in lambda divides the error by ~2^q: q = 1 for Euler and q = p + 1 for UniPC-p
+    (the corrector adds one order); without the corrector UniP-p is of order at least p."""
+    z = np.linspace(-2.0, 2.0, 9)
+    vel, path = _gauss_flow(0.7, 0.4, z)
+
+    def err(n, **kw):
+        ts = _lambda_grid(0.05, 0.95, n)
+        if kw:
+            xN, _ = oracle.unipc_denoise(path(ts[0]), vel, ts, **kw)
+        else:
+            xN, _ = oracle.denoise(path(ts[0]), vel, ts)
+        return np.abs(xN - path(ts[-1])).max()
+
+    def rate(**kw):
+        return math.log2(err(32, **kw) / err(64, **kw))
+
+    assert 0.9 < rate() < 1.1
+    assert 1.9 < rate(order=1) < 2.1
+    assert 2.9 < rate(order=2) < 3.2
+    assert 3.7 < rate(order=3) < 4.3
+    assert 1.9 < rate(order=2, corrector=False) < 2.2
+    assert 2.8 < rate(order=3, corrector=False)
+    # the corrected higher orders are also far more accurate at few steps
+    assert err(8, order=2) < 0.3 * err(8)
+
+
+def test_unipc_with_caching_and_schedule_checks():
+    """Caching decisions follow the same rule as the Euler loop; schedules that start at
+    t = 0 (lambda = -inf) or are not increasing are rejected."""
+    ts = list(np.linspace(0.05, 1.0, 9))
+    _, computed = oracle.unipc_denoise(np.zeros(4), lambda x, t: np.ones(4), ts, tau=0.9, window=2)
+    assert computed == [True, True, False, False, True, False, False, True]
+    for bad in ([0.0, 0.5, 1.0], [0.1, 0.5, 0.5, 1.0], [0.2, 0.1, 1.0]):
+        with pytest.raises(ValueError):
+            oracle.unipc_denoise(np.zeros(2), lambda x, t: x, bad)
+    with pytest.raises(ValueError):
+        oracle.unipc_denoise(np.zeros(2), lambda x, t: x, [0.1, 1.0], order=4)
+
+
 # ----------------------------------------------------------------------------- FP8 (E4M3)
 def test_e4m3_grid_matches_torch_float8():
     """The E4M3 value set against torch's float8_e4m3fn decoding of every finite code."""
