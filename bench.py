@@ -175,6 +175,16 @@ def extras(wl, model, keep, kcs, vcs, inp, torch, reps=3):
 
     out["denoise_4step_ms"] = round(timed(loop), 3)
     assert torch.isfinite(x).all()
+    # the same loop with UniPC of order 2 (its schedule starts just after t = 0)
+    p_u = w.make_denoise_params([0.02, 0.27, 0.51, 0.76, 1.0], x, solver=w.binding.WAM_SOLVER_UNIPC, order=2)
+    ws_u2 = torch.empty(w.wam_denoise_workspace_bytes(model, io_l, p_u), dtype=torch.uint8, device=dev)
+
+    def loop_u():
+        x.copy_(x0)
+        w.wam_denoise_chunk(model, io_l, p_u, ws_u2)
+
+    out["denoise_4step_unipc_ms"] = round(timed(loop_u), 3)
+    assert torch.isfinite(x).all()
 
     # the step with the text conditioning cached per episode: the text projection and every
     # block's cross K|V computed once (by the library's own entry points) and passed in

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define WAM_ABI_VERSION 5
+#define WAM_ABI_VERSION 6
 #define WAM_MAX_CHUNKS 16
 
 typedef enum {
@@ -327,7 +327,7 @@ wam_status wam_dit_update_fwd(const wam_model* m, const wam_step_io* io, void* w
 /* ------------------------------------------------------------------------------
  * The denoising loop around the step (Algorithm 2): the noisy chunk moves along the
  * straight path of Eq. 2 from t = 0 (noise) to t = 1 (clean) by explicit Euler steps
- * x <- x + (t_next - t) v, optionally with classifier-free guidance
+ * x <- x + (t_next - t) v, or by UniPC (below), optionally with classifier-free guidance
  * v = v_u + s (v_c - v_u) and DiT caching (Appendix D.1).
  *
  * The state x is fp32 [nx][n_video + n_action] per chunk: the latent elements
@@ -353,6 +353,43 @@ wam_status wam_flow_step(const wam_flow_dims* d, const float* v_video, const flo
                          const float* v_in, float* x, float* v_out, float t, float t_next,
                          void* z_next, void* a_next, hipStream_t stream);
 
+/* UniPC, the multistep predictor-corrector solver the paper deploys (Flow-UniPC; its
+ * formulas are those of Zhao et al., 2023, in the data-prediction form with
+ * B(h) = e^h - 1), on the straight path: alpha_t = t, sigma_t = 1 - t,
+ * lambda = log(t / (1 - t)), and the data prediction of velocity v at state x and time t
+ * is m = x + (1 - t) v.  Step i (from t_i to t_(i+1)) first corrects the state at t_i
+ * with the new prediction m_i (every step after the first; no extra network call), then
+ * predicts the state at t_(i+1) from m_i and up to two earlier predictions.  The order
+ * warms up as min(order, i + 1) and is 1 for a step that ends at t = 1 (which returns
+ * its data prediction); UniPC of order p converges at order p + 1.  The schedule must
+ * satisfy 0 < t_0 < t_1 < ... < t_N <= 1.
+ *
+ * wam_unipc_plan (HOST, no GPU work) writes one wam_unipc_coef per step: the step's
+ * weights, computed in double precision and stored as fp32.  wam_unipc_step applies
+ * step `step` to the state (device, fp32 [nx][n], as wam_flow_step):
+ *   m     = x + s_v v_eff                       (v_eff as in wam_flow_step)
+ *   x_c   = correct ? c_x x_last + c_new m + sum_q c_m[q] m_(step-1-q) : x
+ *   x     = p_x x_c + p_new m + sum_q p_m[q] m_(step-1-q)
+ *   x_last = x_c;  m_ring[step % 4] = m;  z_next / a_next = bf16(x) as in wam_flow_step
+ * m_ring: 4 device buffers of nx*n fp32 owned by the caller; m_j lives in m_ring[j % 4],
+ * so steps must be applied in order on one stream.  x_last: one more such buffer.
+ * Errors: WAM_EINVAL for a bad schedule or order, NULL buffers a step needs, or a
+ * correcting first step. */
+typedef struct {
+  float s_v;          /* 1 - t_i */
+  int32_t correct;    /* 1: apply the corrector */
+  float c_x, c_new;   /* corrector weights of x_last and m_i */
+  float c_m[3];       /* corrector weights of m_(i-1), m_(i-2), m_(i-3) */
+  float p_x, p_new;   /* predictor weights of x_c and m_i */
+  float p_m[2];       /* predictor weights of m_(i-1), m_(i-2) */
+} wam_unipc_coef;
+wam_status wam_unipc_plan(const float* t_sched, int32_t n_steps, int32_t order,
+                          wam_unipc_coef* out);
+wam_status wam_unipc_step(const wam_flow_dims* d, const float* v_video, const float* v_action,
+                          const float* v_in, float* x, float* x_last, float* const* m_ring,
+                          int32_t step, const wam_unipc_coef* c, float* v_out, void* z_next,
+                          void* a_next, hipStream_t stream);
+
 /* Cosine similarity <a, b> / (|a| |b|) of n fp32 values into out[0] (device; 0 when a
  * norm is 0), accumulated in fp64 in a fixed order (deterministic).  ws of
  * wam_cosine_workspace_bytes() device bytes. */
@@ -370,12 +407,18 @@ typedef struct {
                           /* cache_window steps reuse it; cache_window = 0: caching off     */
   float* x;               /* device fp32 state [nx][n_video + n_action]: noise in, x_N out */
   int32_t* computed;      /* optional DEVICE [N] int32: 1 where step i called the network    */
+  int32_t solver;         /* WAM_SOLVER_EULER or WAM_SOLVER_UNIPC                            */
+  int32_t solver_order;   /* UniPC order 1..3 (ignored by Euler)                             */
 } wam_denoise_params;
+#define WAM_SOLVER_EULER 0
+#define WAM_SOLVER_UNIPC 1
 
 /* wam_denoise_chunk — the N-step denoising loop of one chunk: per step, the network
  * call wam_dit_step_fwd(io) at t_i (io->t [B] is written by the loop; io->z_t and
  * io->a_t are rewritten from x before every call; io->v_video / v_action receive the
- * step's raw velocities), then wam_flow_step.  The cache rows [cache_len, cache_len+L)
+ * step's raw velocities), then wam_flow_step (or wam_unipc_step, with the weights of
+ * wam_unipc_plan and the history buffers in the workspace: 5 * nx * n fp32 more).  A
+ * reused step's velocity enters UniPC like a computed one.  The cache rows [cache_len, cache_len+L)
  * are rewritten by every computed step, as by a single step.  The text conditions every
  * step alike, so when io->ctx_kv is NULL the loop projects the text and each block's
  * cross-attention K|V once, before the first step, into its workspace (n_layers * B *

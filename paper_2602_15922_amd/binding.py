@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_HERE, "libwamdit.so")
 WAM_MAX_CHUNKS = 16
 WAM_OK, WAM_EINVAL, WAM_EUNSUPPORTED, WAM_EWORKSPACE, WAM_EHIP = range(5)
 WAM_EPI_BF16, WAM_EPI_GELU_BF16, WAM_EPI_RESID_F32, WAM_EPI_F32 = range(4)
+WAM_SOLVER_EULER, WAM_SOLVER_UNIPC = range(2)
 
 EXPORTED = (
     "wam_last_error", "wam_abi_version", "wam_attn_blockcausal", "wam_block_workspace_bytes",
@@ -28,7 +29,7 @@ EXPORTED = (
     "wam_text_proj_fwd", "wam_adaln_ln_mod", "wam_rope_qkv", "wam_gemm_bf16",
     "wam_embed_workspace_bytes", "wam_embed_fwd", "wam_head_workspace_bytes", "wam_head_fwd",
     "wam_chunk_positions", "wam_rope_tables", "wam_attn_blockcausal_fp8", "wam_quantize_mx_fp8",
-    "wam_quantize_scaled_fp8", "wam_rope_qkv_fp8",
+    "wam_quantize_scaled_fp8", "wam_rope_qkv_fp8", "wam_unipc_plan", "wam_unipc_step",
 )
 
 _vp, _fp, _i32, _i64, _sz = C.c_void_p, C.POINTER(C.c_float), C.c_int32, C.c_int64, C.c_size_t
@@ -105,7 +106,13 @@ class wam_flow_dims(C.Structure):
 
 class wam_denoise_params(C.Structure):
     _fields_ = [("n_steps", _i32), ("t_sched", _fp), ("cfg", _i32), ("cfg_scale", C.c_float),
-                ("cache_tau", C.c_float), ("cache_window", _i32), ("x", _vp), ("computed", C.POINTER(_i32))]
+                ("cache_tau", C.c_float), ("cache_window", _i32), ("x", _vp), ("computed", C.POINTER(_i32)),
+                ("solver", _i32), ("solver_order", _i32)]
+
+
+class wam_unipc_coef(C.Structure):
+    _fields_ = [("s_v", C.c_float), ("correct", _i32), ("c_x", C.c_float), ("c_new", C.c_float),
+                ("c_m", C.c_float * 3), ("p_x", C.c_float), ("p_new", C.c_float), ("p_m", C.c_float * 2)]
 
 
 class wam_gemm_desc(C.Structure):
@@ -173,6 +180,9 @@ def lib():
         L.wam_quantize_scaled_fp8.argtypes = [_i64, _vp, C.c_float, _vp, _vp]
         L.wam_rope_qkv_fp8.argtypes = [_i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, C.c_float,
                                        _i32, _i32, _vp]
+        L.wam_unipc_plan.argtypes = [_fp, _i32, _i32, C.POINTER(wam_unipc_coef)]
+        L.wam_unipc_step.argtypes = [C.POINTER(wam_flow_dims), _vp, _vp, _vp, _vp, _vp, C.POINTER(_vp), _i32,
+                                     C.POINTER(wam_unipc_coef), _vp, _vp, _vp, _vp]
         for name in EXPORTED[2:]:
             if not name.endswith("_bytes"):
                 getattr(L, name).restype = C.c_int
@@ -525,10 +535,31 @@ def wam_cosine_similarity(a, b, out, ws, stream=None):
     _check(lib().wam_cosine_similarity(_p(a), _p(b), a.numel(), _p(ws), ws.numel(), _p(out), _stream(stream)))
 
 
-def make_denoise_params(t_sched, x, cfg=False, cfg_scale=1.0, cache_tau=0.0, cache_window=0):
+def wam_unipc_plan(t_sched, order=2):
+    """Host: the UniPC weights of every step of the schedule (N+1 times), a ctypes array."""
+    import numpy as np
+    t = np.ascontiguousarray(np.asarray(t_sched, dtype=np.float32))
+    n = len(t) - 1
+    out = (wam_unipc_coef * max(n, 1))()
+    _check(lib().wam_unipc_plan(t.ctypes.data_as(_fp), n, order, out))
+    return out
+
+
+def wam_unipc_step(dims: wam_flow_dims, v_video, v_action, v_in, x, x_last, m_ring, step, coef, v_out,
+                   z_next, a_next, stream=None):
+    """One UniPC step (device tensors; m_ring a list of 4 state-sized fp32 tensors, coef one
+    wam_unipc_coef of wam_unipc_plan's output)."""
+    ring = (_vp * 4)(*[_p(t) for t in m_ring])
+    _check(lib().wam_unipc_step(C.byref(dims), _p(v_video), _p(v_action), _p(v_in), _p(x), _p(x_last), ring,
+                                step, C.byref(coef), _p(v_out), _p(z_next), _p(a_next), _stream(stream)))
+
+
+def make_denoise_params(t_sched, x, cfg=False, cfg_scale=1.0, cache_tau=0.0, cache_window=0,
+                        solver=WAM_SOLVER_EULER, order=2):
     """Loop parameters; t_sched a float sequence of N+1 times (kept on the host), x the
-    device state.  `p.computed` is a device int32 [N] tensor the loop fills with 1 where a
-    step called the network (read it after the stream has finished)."""
+    device state, solver WAM_SOLVER_EULER or WAM_SOLVER_UNIPC (of the given order).
+    `p.computed` is a device int32 [N] tensor the loop fills with 1 where a step called
+    the network (read it after the stream has finished)."""
     import numpy as np
     import torch
     t = np.ascontiguousarray(np.asarray(t_sched, dtype=np.float32))
@@ -536,7 +567,8 @@ def make_denoise_params(t_sched, x, cfg=False, cfg_scale=1.0, cache_tau=0.0, cac
     computed = torch.zeros(n, dtype=torch.int32, device=x.device)
     p = wam_denoise_params(n_steps=n, t_sched=t.ctypes.data_as(_fp), cfg=int(cfg), cfg_scale=cfg_scale,
                            cache_tau=cache_tau, cache_window=cache_window, x=_p(x),
-                           computed=C.cast(C.c_void_p(computed.data_ptr()), C.POINTER(_i32)))
+                           computed=C.cast(C.c_void_p(computed.data_ptr()), C.POINTER(_i32)),
+                           solver=solver, solver_order=order)
     p._keep = (t, computed)
     p.computed_steps = computed
     return p

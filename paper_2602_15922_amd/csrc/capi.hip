@@ -702,8 +702,146 @@ FlowArgs flow_args(const wam_flow_dims& d) {
   return f;
 }
 
+// UniPC on the straight path (alpha_t = t, sigma_t = 1 - t, lambda = log(alpha/sigma)).
+// The exact solution from t_s is x_t = (sigma_t/sigma_s) x_s + sigma_t times the integral
+// of e^lambda m over [lambda_s, lambda_t], m = x + (1 - t) v the data prediction.
+// Expanding m in lambda turns the integral into alpha_t sum_k m^(k) I_k(h), with
+// I_0 = 1 - e^-h and I_k = h^k/k! - I_(k-1).  An update with K other predictions m_j (at
+// lambda_s + r_j h) uses the divided differences (m_j - m_s)/r_j, weighted by the
+// solution a of sum_j a_j r_j^(k-1) = k! I_k / (h^k I_0), k = 1..K, so that it is exact
+// for m of degree <= K in lambda.  The update as weights on x_s, m_s and the m_j:
+struct UnipcW {
+  double x, s, m[3];
+};
+
+double unipc_lambda(double t) { return std::log(t) - std::log1p(-t); }
+
+// Solve the K x K system R a = b (K <= 3) by Gaussian elimination with partial pivoting.
+bool solve_small(double R[3][3], double* b, int K, double* a) {
+  for (int c = 0; c < K; ++c) {
+    int piv = c;
+    for (int r = c + 1; r < K; ++r)
+      if (std::fabs(R[r][c]) > std::fabs(R[piv][c])) piv = r;
+    if (!(std::fabs(R[piv][c]) > 0.0)) return false;
+    if (piv != c) {
+      for (int q = 0; q < K; ++q) std::swap(R[c][q], R[piv][q]);
+      std::swap(b[c], b[piv]);
+    }
+    for (int r = c + 1; r < K; ++r) {
+      const double f = R[r][c] / R[c][c];
+      for (int q = c; q < K; ++q) R[r][q] -= f * R[c][q];
+      b[r] -= f * b[c];
+    }
+  }
+  for (int c = K - 1; c >= 0; --c) {
+    double v = b[c];
+    for (int q = c + 1; q < K; ++q) v -= R[c][q] * a[q];
+    a[c] = v / R[c][c];
+  }
+  return true;
+}
+
+bool unipc_weights(double ts, double t, const double* tp, int K, UnipcW& w) {
+  const double e = (ts * (1.0 - t)) / ((1.0 - ts) * t);  // e^-h (0 at t = 1)
+  const double i0 = 1.0 - e;
+  w.x = (1.0 - t) / (1.0 - ts);
+  w.s = t * i0;
+  w.m[0] = w.m[1] = w.m[2] = 0.0;
+  if (K == 0) return true;
+  const double h = unipc_lambda(t) - unipc_lambda(ts);
+  double ik = i0, fact = 1.0, hk = 1.0, rhs[3], r[3], R[3][3], a[3];
+  for (int k = 1; k <= K; ++k) {
+    fact *= k;
+    hk *= h;
+    ik = hk / fact - ik;
+    rhs[k - 1] = fact * ik / (hk * i0);
+  }
+  for (int j = 0; j < K; ++j) r[j] = (unipc_lambda(tp[j]) - unipc_lambda(ts)) / h;
+  for (int k = 0; k < K; ++k)
+    for (int j = 0; j < K; ++j) R[k][j] = std::pow(r[j], k);
+  if (!solve_small(R, rhs, K, a)) return false;
+  for (int j = 0; j < K; ++j) {
+    w.m[j] = t * i0 * a[j] / r[j];
+    w.s -= w.m[j];
+  }
+  return std::isfinite(w.x) && std::isfinite(w.s) && std::isfinite(w.m[0]) && std::isfinite(w.m[1]) &&
+         std::isfinite(w.m[2]);
+}
+
+// The weights of every step of a schedule: step i corrects the state at t_i (after the
+// first step) with the order of the predictor that produced it, then predicts t_(i+1) at
+// order min(order, i + 1), or 1 when t_(i+1) = 1 (lambda is infinite there).
+wam_status unipc_plan(const float* t_sched, int32_t n, int32_t order, wam_unipc_coef* out) {
+  CHECK(t_sched != nullptr && out != nullptr, WAM_EINVAL, "NULL schedule or output");
+  CHECK(n >= 1, WAM_EINVAL, "n_steps=%d must be >= 1", n);
+  CHECK(order >= 1 && order <= 3, WAM_EINVAL, "UniPC order %d not in 1..3", order);
+  CHECK(t_sched[0] > 0.f && t_sched[n] <= 1.f, WAM_EINVAL, "UniPC needs 0 < t_0 and t_N <= 1 (got %g, %g)",
+        (double)t_sched[0], (double)t_sched[n]);
+  for (int i = 0; i < n; ++i)
+    CHECK(t_sched[i] < t_sched[i + 1], WAM_EINVAL, "schedule not increasing at %d (%g, %g)", i,
+          (double)t_sched[i], (double)t_sched[i + 1]);
+  int p_prev = 0;
+  for (int i = 0; i < n; ++i) {
+    const double t = t_sched[i], tn = t_sched[i + 1];
+    wam_unipc_coef c{};
+    c.s_v = (float)(1.0 - t);
+    double tp[3];
+    UnipcW w;
+    if (i > 0) {  // corrector: from t_(i-1) with m_(i-2) .. m_(i-p_prev) and the new m_i
+      for (int k = 1; k < p_prev; ++k) tp[k - 1] = t_sched[i - 1 - k];
+      tp[p_prev - 1] = t;
+      CHECK(unipc_weights(t_sched[i - 1], t, tp, p_prev, w), WAM_EINVAL, "UniPC weights of step %d not finite", i);
+      c.correct = 1;
+      c.c_x = (float)w.x;
+      c.c_m[0] = (float)w.s;
+      for (int k = 1; k < p_prev; ++k) c.c_m[k] = (float)w.m[k - 1];
+      c.c_new = (float)w.m[p_prev - 1];
+    }
+    const int p = t_sched[i + 1] == 1.f ? 1 : std::min(order, i + 1);
+    for (int k = 1; k < p; ++k) tp[k - 1] = t_sched[i - k];
+    CHECK(unipc_weights(t, tn, tp, p - 1, w), WAM_EINVAL, "UniPC weights of step %d not finite", i);
+    c.p_x = (float)w.x;
+    c.p_new = (float)w.s;
+    for (int k = 1; k < p; ++k) c.p_m[k - 1] = (float)w.m[k - 1];
+    out[i] = c;
+    p_prev = p;
+  }
+  return WAM_OK;
+}
+
+// One UniPC step's launch arguments; m_ring[j % 4] holds the data prediction of step j.
+wam_status unipc_args(const wam_flow_dims& d, float* x, float* x_last, float* const* m_ring, int32_t step,
+                      const wam_unipc_coef& c, UnipcArgs& u) {
+  CHECK(step >= 0, WAM_EINVAL, "step %d < 0", step);
+  CHECK(!c.correct || step >= 1, WAM_EINVAL, "the first step has nothing to correct");
+  TRY(need_ptr(x, "x"));
+  TRY(need_ptr(x_last, "x_last"));
+  CHECK(m_ring != nullptr && m_ring[step % 4] != nullptr, WAM_EINVAL, "m_ring[%d] is NULL", step % 4);
+  u = UnipcArgs{};
+  u.f = flow_args(d);
+  u.f.x = x;
+  u.x_last = x_last;
+  u.m_out = m_ring[step % 4];
+  for (int q = 0; q < 3; ++q) {
+    const bool used = (c.correct && c.c_m[q] != 0.f) || (q < 2 && c.p_m[q] != 0.f);
+    if (!used) continue;
+    CHECK(step - 1 - q >= 0, WAM_EINVAL, "step %d has no data prediction %d steps back", step, q + 1);
+    CHECK(m_ring[(step - 1 - q) % 4] != nullptr, WAM_EINVAL, "m_ring[%d] is NULL", (step - 1 - q) % 4);
+    u.m_hist[q] = m_ring[(step - 1 - q) % 4];
+  }
+  u.s_v = c.s_v;
+  u.correct = c.correct;
+  u.c_x = c.c_x;
+  u.c_new = c.c_new;
+  for (int q = 0; q < 3; ++q) u.c_m[q] = c.c_m[q];
+  u.p_x = c.p_x;
+  u.p_new = c.p_new;
+  for (int q = 0; q < 2; ++q) u.p_m[q] = c.p_m[q];
+  return WAM_OK;
+}
+
 struct DenoiseWs {
-  size_t step, va, vb, cos, cos_out, state, kv, kv_layer, total;
+  size_t step, va, vb, cos, cos_out, state, xl, ring, kv, kv_layer, total;
 };
 DenoiseWs denoise_ws(const wam_model& m, const wam_step_io& io, const wam_denoise_params& p) {
   const int64_t nx = p.cfg ? 1 : io.B;
@@ -716,6 +854,10 @@ DenoiseWs denoise_ws(const wam_model& m, const wam_step_io& io, const wam_denois
   w.cos = off; off += align256(cosine_workspace_bytes());
   w.cos_out = off; off += 256;
   w.state = off; off += 256;
+  // UniPC: the corrected state of the previous step and a ring of 4 data predictions
+  const bool unipc = p.solver == WAM_SOLVER_UNIPC;
+  w.xl = off; off += unipc ? align256((size_t)nx * n * 4) : 0;
+  w.ring = off; off += unipc ? 4 * align256((size_t)nx * n * 4) : 0;
   // the text's cross K|V of every block, computed once per chunk (unless supplied)
   w.kv_layer = io.ctx_kv ? 0 : align256((size_t)io.B * io.Lc * 2 * m.dims.d * 2);
   w.kv = off; off += (size_t)std::max(m.dims.n_layers, 0) * w.kv_layer;
@@ -1006,6 +1148,30 @@ wam_status wam_flow_step(const wam_flow_dims* d, const float* v_video, const flo
   return WAM_OK;
 }
 
+wam_status wam_unipc_plan(const float* t_sched, int32_t n_steps, int32_t order, wam_unipc_coef* out) {
+  return unipc_plan(t_sched, n_steps, order, out);
+}
+
+wam_status wam_unipc_step(const wam_flow_dims* d, const float* v_video, const float* v_action, const float* v_in,
+                          float* x, float* x_last, float* const* m_ring, int32_t step, const wam_unipc_coef* c,
+                          float* v_out, void* z_next, void* a_next, hipStream_t stream) {
+  CHECK(d != nullptr && c != nullptr, WAM_EINVAL, "NULL dims or coefficients");
+  TRY(check_flow_dims(*d));
+  if (d->n_video > 0) TRY(need_ptr(z_next, "z_next"));
+  if (d->n_action > 0) TRY(need_ptr(a_next, "a_next"));
+  if (!v_in) {
+    if (d->n_video > 0) TRY(need_ptr(v_video, "v_video"));
+    if (d->n_action > 0) TRY(need_ptr(v_action, "v_action"));
+  }
+  UnipcArgs u;
+  TRY(unipc_args(*d, x, x_last, m_ring, step, *c, u));
+  u.f.v_in = v_in;
+  if (!v_in) { u.f.v_video = v_video; u.f.v_action = v_action; }
+  u.f.v_out = v_out; u.f.z_next = z_next; u.f.a_next = a_next;
+  HIPCHECK(launch_unipc_step(u, stream));
+  return WAM_OK;
+}
+
 size_t wam_cosine_workspace_bytes(void) { return cosine_workspace_bytes(); }
 
 wam_status wam_cosine_similarity(const float* a, const float* b, int64_t n, void* ws, size_t ws_bytes, float* out,
@@ -1032,7 +1198,11 @@ wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wa
   CHECK(p->t_sched != nullptr, WAM_EINVAL, "t_sched is NULL");
   CHECK(p->cache_window >= 0, WAM_EINVAL, "cache_window < 0");
   CHECK(io->t_action == nullptr, WAM_EUNSUPPORTED, "the loop runs one schedule for both modalities (t_action must be NULL)");
+  CHECK(p->solver == WAM_SOLVER_EULER || p->solver == WAM_SOLVER_UNIPC, WAM_EINVAL, "unknown solver %d", p->solver);
   TRY(need_ptr(p->x, "x"));
+  const bool unipc = p->solver == WAM_SOLVER_UNIPC;
+  std::vector<wam_unipc_coef> plan(unipc ? p->n_steps : 0);
+  if (unipc) TRY(unipc_plan(p->t_sched, p->n_steps, p->solver_order, plan.data()));
   wam_flow_dims fd{};
   fd.B = io->B; fd.cfg = p->cfg; fd.cfg_scale = p->cfg_scale;
   fd.n_video = (int64_t)m->dims.latent_ch * io->F * io->Hl * io->Wl;
@@ -1051,6 +1221,11 @@ wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wa
   float* t_dev = const_cast<float*>(io->t);
   const int64_t n = (int64_t)(p->cfg ? 1 : io->B) * (fd.n_video + fd.n_action);
   const bool caching = p->cache_window > 0;
+  float* xl = reinterpret_cast<float*>(w + lay.xl);
+  float* ring[4];
+  for (int q = 0; q < 4; ++q) ring[q] = reinterpret_cast<float*>(w + lay.ring + q * align256((size_t)n * 4));
+  std::vector<UnipcArgs> uargs(plan.size());
+  for (size_t i = 0; i < plan.size(); ++i) TRY(unipc_args(fd, p->x, xl, ring, (int32_t)i, plan[i], uargs[i]));
 
   // The text and so every block's cross-attention K|V are the same at every step of
   // the chunk: unless the caller supplied them, project them once here and let each
@@ -1099,7 +1274,13 @@ wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wa
     if (caching) {
       f.v_in = vcur; f.v_out = vcur; f.skip = st;
     }
-    HIPCHECK(launch_flow_step(f, stream));
+    if (unipc) {
+      UnipcArgs u = uargs[i];
+      u.f = f;
+      HIPCHECK(launch_unipc_step(u, stream));
+    } else {
+      HIPCHECK(launch_flow_step(f, stream));
+    }
     if (caching) HIPCHECK(launch_cosine(vcur, vprev, n, w + lay.cos, cs_dev, stream, st));
     if (caching || p->computed)
       HIPCHECK(launch_loop_decide(st, cs_dev, p->cache_tau, p->cache_window, p->computed, i, stream));

@@ -1,5 +1,5 @@
-// The denoising loop's own kernels for gfx950: the flow-matching solver step with
-// classifier-free guidance, the cosine similarity behind DiT caching, and the
+// The denoising loop's own kernels for gfx950: the flow-matching solver steps (Euler and
+// UniPC) with classifier-free guidance, the cosine similarity behind DiT caching, and the
 // timestep fill.  All HBM-bound elementwise work over one chunk's latents and actions.
 #include "common.h"
 #include "kernels.h"
@@ -46,6 +46,46 @@ __global__ __launch_bounds__(256) void flow_step_kernel(const FlowArgs a) {
     for (int b = b0; b < b1; ++b) {
       if (k < a.n_video) static_cast<bf16*>(a.z_next)[(int64_t)b * a.n_video + k] = xb;
       else static_cast<bf16*>(a.a_next)[(int64_t)b * a.n_action + (k - a.n_video)] = xb;
+    }
+  }
+}
+
+// One UniPC step (corrector, then predictor) per element of the state; the weights are
+// the host's, so the kernel is a fixed linear combination of at most five fp32 vectors.
+// The history buffers are read before m_out is written, and m_out never aliases them.
+__global__ __launch_bounds__(256) void unipc_step_kernel(const UnipcArgs a) {
+  const FlowArgs& f = a.f;
+  const int64_t n = f.n_video + f.n_action;
+  const int nx = f.cfg ? 1 : f.B;
+  const int64_t total = (int64_t)nx * n;
+  const bool reuse = f.skip ? *f.skip > 0 : f.v_in != nullptr;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+    const int j = (int)(e / n);
+    const int64_t k = e - (int64_t)j * n;
+    const float v = eff_velocity(f, reuse, j, k);
+    if (f.v_out) f.v_out[e] = v;
+    const float x = f.x[e];
+    const float m = __builtin_fmaf(a.s_v, v, x);
+    float h[3];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) h[q] = a.m_hist[q] ? a.m_hist[q][e] : 0.f;
+    float xc = x;
+    if (a.correct) {
+      xc = __builtin_fmaf(a.c_x, a.x_last[e], a.c_new * m);
+#pragma unroll
+      for (int q = 0; q < 3; ++q) xc = __builtin_fmaf(a.c_m[q], h[q], xc);
+    }
+    float xn = __builtin_fmaf(a.p_x, xc, a.p_new * m);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) xn = __builtin_fmaf(a.p_m[q], h[q], xn);
+    a.x_last[e] = xc;
+    a.m_out[e] = m;
+    f.x[e] = xn;
+    const bf16 xb = (bf16)xn;
+    const int b0 = f.cfg ? 0 : j, b1 = f.cfg ? f.B : j + 1;
+    for (int b = b0; b < b1; ++b) {
+      if (k < f.n_video) static_cast<bf16*>(f.z_next)[(int64_t)b * f.n_video + k] = xb;
+      else static_cast<bf16*>(f.a_next)[(int64_t)b * f.n_action + (k - f.n_video)] = xb;
     }
   }
 }
@@ -133,6 +173,15 @@ hipError_t launch_flow_step(const FlowArgs& a, hipStream_t s) {
   const int64_t want = (total + 255) / 256;
   const unsigned grid = (unsigned)(want < 4096 ? want : 4096);
   hipLaunchKernelGGL(flow_step_kernel, dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_unipc_step(const UnipcArgs& a, hipStream_t s) {
+  const int64_t total = (int64_t)(a.f.cfg ? 1 : a.f.B) * (a.f.n_video + a.f.n_action);
+  if (total == 0) return hipSuccess;
+  const int64_t want = (total + 255) / 256;
+  const unsigned grid = (unsigned)(want < 4096 ? want : 4096);
+  hipLaunchKernelGGL(unipc_step_kernel, dim3(grid), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

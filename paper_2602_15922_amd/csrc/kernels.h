@@ -139,6 +139,21 @@ struct FlowArgs {
   const int32_t* skip;
 };
 hipError_t launch_flow_step(const FlowArgs& a, hipStream_t s);
+// One UniPC step over the same state: the data prediction m = x + s_v v_eff, the
+// corrector (when `correct`) x_c = c_x x_last + c_new m + sum_j c_m[j] m_hist[j], then the
+// predictor x <- p_x x_c + p_new m + sum_j p_m[j] m_hist[j]; x_last <- x_c, m_out <- m.
+// m_hist[j] holds the data prediction j + 1 steps back (NULL where its weights are 0).
+struct UnipcArgs {
+  FlowArgs f;          // velocities, guidance, x, v_out, model inputs, skip flag (dt unused)
+  float* x_last;
+  float* m_out;
+  const float* m_hist[3];
+  float s_v;
+  int32_t correct;
+  float c_x, c_new, c_m[3];
+  float p_x, p_new, p_m[2];
+};
+hipError_t launch_unipc_step(const UnipcArgs& a, hipStream_t s);
 // cosine similarity of x and y (n floats) into out[0]; ws of cosine_workspace_bytes()
 size_t cosine_workspace_bytes();
 hipError_t launch_cosine(const float* x, const float* y, int64_t n, void* ws, float* out, hipStream_t s,

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_function():
     for name in declared:
         assert hasattr(L, name), name
     assert sorted(w.binding.EXPORTED) == declared
-    assert w.wam_abi_version() == 5
+    assert w.wam_abi_version() == 6
 
 
 def test_struct_sizes_match_the_header_layout():
@@ -44,7 +44,8 @@ def test_struct_sizes_match_the_header_layout():
     assert C.sizeof(b.wam_block_fp8) == 14 * 8
     # sizes printed by a C++ compile of include/wamdit.h
     assert C.sizeof(b.wam_flow_dims) == 32
-    assert C.sizeof(b.wam_denoise_params) == 48
+    assert C.sizeof(b.wam_denoise_params) == 56
+    assert C.sizeof(b.wam_unipc_coef) == 44
     assert C.sizeof(b.wam_step_io) == 360
     assert C.sizeof(b.wam_block_io) == 312
     assert C.sizeof(b.wam_model) == 200
@@ -162,3 +163,74 @@ def test_fp8_entry_points_reject_bad_arguments_without_a_gpu():
     assert r(1, 4, 2, 64, 4096, 8192, 8192, 0, 0, 12288, 16384, 20480, 1.0, 8, 0, None) == b.WAM_EUNSUPPORTED
     assert r(1, 4, 2, 128, 4096, 8192, 8192, 24576, 0, 12288, 16384, 20480, 1.0, 8, 0, None) == b.WAM_EINVAL
     assert r(1, 4, 2, 128, 4096, 8192, 8192, 0, 0, 12288, 16384, 20480, 1.0, 8, 5, None) == b.WAM_EINVAL  # row0+L>Lcap
+
+
+def _apply_unipc_weights(coef, x0, vels):
+    """The documented semantics of wam_unipc_step applied in numpy: returns the final
+    state and the corrected states."""
+    x, x_last, ring, states = np.array(x0, dtype=np.float64), None, {}, []
+    for i, v in enumerate(vels):
+        c = coef[i]
+        m = x + c.s_v * v
+        hist = [ring.get(i - 1 - q) for q in range(3)]
+        xc = x
+        if c.correct:
+            xc = c.c_x * x_last + c.c_new * m + sum(c.c_m[q] * hist[q] for q in range(3) if c.c_m[q] != 0.0)
+            states.append(xc)
+        x = c.p_x * xc + c.p_new * m + sum(c.p_m[q] * hist[q] for q in range(2) if c.p_m[q] != 0.0)
+        ring[i], x_last = m, xc
+    return x, states
+
+
+def test_unipc_plan_reproduces_the_oracle_solver():
+    """The library's host-side UniPC weights, applied as the step kernel applies them,
+    follow the oracle's UniPC over whole schedules (orders 1-3, ending inside (0, 1) or
+    at 1) up to the fp32 rounding of the weights."""
+    w = lib()
+    g = np.random.default_rng(178)
+    for ts in ([0.02, 0.1, 0.23, 0.41, 0.6, 0.78, 0.93, 1.0], [0.3, 0.35, 0.5, 0.52, 0.7, 0.9],
+               [0.5, 1.0], [0.001, 0.002, 0.5]):
+        ts = [float(t) for t in np.float32(ts)]
+        vels = [g.standard_normal(50) for _ in range(len(ts) - 1)]
+        x0 = g.standard_normal(50)
+        for order in (1, 2, 3):
+            it = iter(vels)
+            states = []
+            ref, _ = oracle.unipc_denoise(x0, lambda x, t: next(it), ts, order=order, states=states)
+            got, got_states = _apply_unipc_weights(w.wam_unipc_plan(ts, order), x0, vels)
+            scale = 1.0 + np.abs(ref).max()
+            assert np.abs(got - ref).max() < 1e-5 * scale, (ts, order)
+            assert len(got_states) == len(states)
+            for a, b in zip(got_states, states):
+                assert np.abs(a - b).max() < 1e-5 * scale
+
+
+def test_unipc_plan_and_step_reject_bad_arguments_without_a_gpu():
+    w = lib()
+    b = w.binding
+    L = w.lib()
+    out = (b.wam_unipc_coef * 4)()
+
+    def plan(ts, order=2, n=None):
+        t = np.asarray(ts, dtype=np.float32)
+        return L.wam_unipc_plan(t.ctypes.data_as(C.POINTER(C.c_float)), len(t) - 1 if n is None else n, order, out)
+
+    assert plan([0.1, 0.5, 1.0]) == b.WAM_OK
+    for ts in ([0.0, 0.5, 1.0], [0.1, 0.5, 0.5], [0.5, 0.2, 1.0], [0.1, 0.5, 1.5]):
+        assert plan(ts) == b.WAM_EINVAL, ts
+    assert plan([0.1, 0.5, 1.0], order=0) == b.WAM_EINVAL
+    assert plan([0.1, 0.5, 1.0], order=4) == b.WAM_EINVAL
+    assert plan([0.1], n=0) == b.WAM_EINVAL
+    assert L.wam_unipc_plan(None, 2, 2, out) == b.WAM_EINVAL
+    # a correcting first step, and a missing history buffer, are rejected before any launch
+    d = b.wam_flow_dims(B=1, cfg=0, cfg_scale=1.0, n_video=8, n_action=0)
+    ring = (C.c_void_p * 4)(4096, 8192, 12288, 16384)
+    c = b.wam_unipc_coef(s_v=0.5, correct=1, c_x=1.0)
+    assert L.wam_unipc_step(C.byref(d), 4096, None, None, 4096, 4096, ring, 0, C.byref(c), None, 4096, None,
+                            None) == b.WAM_EINVAL
+    c = b.wam_unipc_coef(s_v=0.5, correct=0, p_x=1.0)
+    c.p_m[1] = 0.5
+    assert L.wam_unipc_step(C.byref(d), 4096, None, None, 4096, 4096, ring, 1, C.byref(c), None, 4096, None,
+                            None) == b.WAM_EINVAL
+    assert L.wam_unipc_step(C.byref(d), None, None, None, 4096, 4096, ring, 0, C.byref(b.wam_unipc_coef()), None,
+                            4096, None, None) == b.WAM_EINVAL
