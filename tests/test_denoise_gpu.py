@@ -196,10 +196,15 @@ def test_denoise_loop_graph_replay():
     with eager loop calls between the replays: every replay and every eager call gives the
     same final state and computed / reused pattern, bit for bit, and that result matches
     the oracle's loop."""
+    graph_replay_check(LoopCase(small_wl(), 2), list(np.linspace(0.0, 1.0, 7)))
+
+
+def graph_replay_check(case, ts):
+    """Capture one loop call with caching (tau -1, window 1) as a HIP graph, replay it
+    three times between eager calls, and check every result bitwise against the eager
+    call and the eager call against the oracle."""
     import torch
     w = lib()
-    case = LoopCase(small_wl(), 2)
-    ts = list(np.linspace(0.0, 1.0, 7))
     s = case.gpu_loop_setup(ts, tau=-1.0, window=1)
     x0 = s["x"].clone()
     flags = s["p"].computed_steps

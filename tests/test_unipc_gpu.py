@@ -7,7 +7,7 @@ import pytest
 
 import oracle
 from gpu_helpers import dev, host, log, rel_l2
-from test_denoise_gpu import LoopCase, bf16_round, small_wl
+from test_denoise_gpu import LoopCase, bf16_round, graph_replay_check, small_wl
 
 pytestmark = pytest.mark.gpu
 TOL_STEP = 1e-5   # fp32 kernel with fp32 weights against fp64 (weights rounded to 2^-24)
@@ -129,3 +129,12 @@ def test_denoise_loop_unipc_guidance_and_caching():
     case = UnipcLoopCase(small_wl(B=2), 2, cfg_scale=3.0)
     case.order = 3
     check_unipc_loop(case, [float(t) for t in np.float32(np.linspace(0.04, 1.0, 7))], tau=-1.0, window=1)
+
+
+def test_denoise_loop_unipc_graph_replay():
+    """A UniPC loop call with DiT caching captured as a HIP graph: the history buffers are
+    written before they are read in every call, so each replay equals the eager call bit
+    for bit (and the eager call matches the oracle)."""
+    case = UnipcLoopCase(small_wl(), 2)
+    case.order = 2
+    graph_replay_check(case, [float(t) for t in np.float32(np.linspace(0.05, 1.0, 7))])
