@@ -263,7 +263,10 @@ typedef struct {
  * k_cache, v_cache  HOST arrays of n_layers device pointers, each [B][Lcap][H][Dh]
  *          bf16, semantics as in wam_dit_block_fwd.
  * ctx_kv   optional HOST array of n_layers device pointers [B][Lc][2d] bf16 holding
- *          each block's precomputed cross K|V of this text (NULL: computed here).
+ *          each block's precomputed cross K|V of this text (NULL: computed here, for
+ *          every block before the first one, into the workspace: n_layers*B*Lc*2d bf16
+ *          of the size wam_step_workspace_bytes reports; the same products as one GEMM
+ *          per block, batched so that they fill the GPU).
  * rope_cos, rope_sin  [L][Dh/2] fp32 tables of the rows' positions.
  * ch       self-attention chunks (Lk = cache_len + L, Lq = L).
  * v_video  written, [B][latent_ch][F][Hl][Wl] fp32;  v_action  written, [B][A][act_dim] fp32.

@@ -213,8 +213,10 @@ wam_chunks single_chunk(int32_t Lq, int32_t Lk) {
 // GEMM
 // ---------------------------------------------------------------------------------
 // fp8: A and W are E4M3 bytes with per-row a_scale [M] and per-column w_scale [N].
-wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s, int32_t gate_split = 0, int64_t gate_alt = 0,
-                        const float* a_scale = nullptr, const float* w_scale = nullptr) {
+// Validate one GEMM descriptor and fill its launch arguments (a.M = 0: nothing to run).
+wam_status gemm_prep(const wam_gemm_desc& g, GemmArgs& a, int32_t gate_split = 0, int64_t gate_alt = 0,
+                     const float* a_scale = nullptr, const float* w_scale = nullptr) {
+  a = GemmArgs{};
   const bool fp8 = a_scale != nullptr;
   const int eb = fp8 ? 1 : 2, epc = 16 / eb;  // bytes per element, elements per 16 bytes
   CHECK(g.M >= 0 && g.N >= 1 && g.K >= epc && g.K % epc == 0, WAM_EINVAL,
@@ -248,7 +250,6 @@ wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s, int32_t gate_spli
           "A or W spans 2 GiB or more (A %lld bytes, W %lld bytes)", (long long)(eb * a_end),
           (long long)(eb * w_end));
   }
-  GemmArgs a{};
   a.M = g.M; a.N = g.N; a.K = g.K; a.epi = g.epilogue;
   a.A = g.A; a.lda = g.lda; a.a_bs = g.a_batch_stride; a.a_rows = g.a_rows;
   a.W = g.W; a.ldw = g.ldw; a.bias = g.bias;
@@ -256,6 +257,14 @@ wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s, int32_t gate_spli
   a.gate_a = g.gate_a; a.gate_v = g.gate_v; a.gate_stride = g.gate_stride; a.gate_rows = g.gate_rows;
   a.gate_split = gate_split; a.gate_alt = gate_alt;
   a.fp8 = fp8 ? 1 : 0; a.a_scale = a_scale; a.w_scale = w_scale;
+  return WAM_OK;
+}
+
+wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s, int32_t gate_split = 0, int64_t gate_alt = 0,
+                        const float* a_scale = nullptr, const float* w_scale = nullptr) {
+  GemmArgs a;
+  TRY(gemm_prep(g, a, gate_split, gate_alt, a_scale, w_scale));
+  if (a.M == 0) return WAM_OK;
   HIPCHECK(launch_gemm(pred(a), s));
   return WAM_OK;
 }
@@ -570,8 +579,54 @@ wam_status head_run(const wam_model& m, int32_t B, int32_t F, int32_t Hl, int32_
   return WAM_OK;
 }
 
+// Every block's cross-attention K|V of the projected text ctx (B*Lc rows, the same input
+// for every block) into kv + l*kv_layer for the first n blocks: the blocks with bf16
+// weights in grouped launches of up to WAM_GEMM_GROUP_MAX (the tiles and arithmetic of
+// one launch per block, but 512-row products that fill the chip together instead of
+// ~1.25 rounds each), those with FP8 weights one launch each.
+wam_status cross_kv_run(const wam_model& m, int32_t B, int32_t Lc, const void* ctx, char* kv, size_t kv_layer,
+                        int n, char* q8, float* qs, hipStream_t s) {
+  const wam_dims& D = m.dims;
+  GemmGroup gg{};
+  GemmArgs first{};
+  std::vector<GemmArgs> members;
+  members.reserve(n);
+  for (int l = 0; l < n; ++l) {  // validate every bf16 member before the first launch
+    const wam_block_weights& W = m.blocks[l];
+    if (W.fp8) {
+      members.push_back(GemmArgs{});
+      continue;
+    }
+    const wam_gemm_desc g = gemm(B * Lc, 2 * D.d, D.d, WAM_EPI_BF16, ctx, D.d, W.w_ckv, W.b_ckv,
+                                 kv + (size_t)l * kv_layer, 2 * D.d);
+    GemmArgs a;
+    TRY(gemm_prep(g, a));
+    members.push_back(a);
+  }
+  for (int l = 0; l < n; ++l) {
+    const wam_block_weights& W = m.blocks[l];
+    const GemmArgs& a = members[l];
+    if (W.fp8) {
+      TRY(proj(gemm(B * Lc, 2 * D.d, D.d, WAM_EPI_BF16, ctx, D.d, W.w_ckv, W.b_ckv, kv + (size_t)l * kv_layer,
+                    2 * D.d), W.fp8->w_ckv, W.fp8->s_ckv, q8, qs, s));
+      continue;
+    }
+    if (a.M == 0) continue;
+    if (gg.n == 0) first = a;
+    gg.W[gg.n] = a.W;
+    gg.bias[gg.n] = a.bias;
+    gg.out[gg.n] = a.out;
+    if (++gg.n == WAM_GEMM_GROUP_MAX) {
+      HIPCHECK(launch_gemm_group(pred(first), gg, s));
+      gg.n = 0;
+    }
+  }
+  if (gg.n > 0) HIPCHECK(launch_gemm_group(pred(first), gg, s));
+  return WAM_OK;
+}
+
 struct StepWs {
-  size_t x, e, e0, ctx, piece, block, total;
+  size_t x, e, e0, ctx, piece, block, kv, kv_layer, total;
 };
 StepWs step_ws(const wam_model& m, const wam_step_io& io) {
   const wam_dims& D = m.dims;
@@ -590,6 +645,10 @@ StepWs step_ws(const wam_model& m, const wam_step_io& io) {
   piece = std::max(piece, head_ws(D, io.B, io.F, io.Hl, io.Wl, io.A).total);
   w.piece = off; off += align256(piece);
   w.block = off; off += block_ws(D, io.B, (int32_t)L, io.Lc).total;
+  // without ctx_kv: every block's cross K|V, projected before the first block.  Last, so
+  // every other offset is the same with and without it.
+  w.kv_layer = io.ctx_kv ? 0 : align256((size_t)io.B * io.Lc * 2 * D.d * 2);
+  w.kv = off; off += (size_t)std::max(D.n_layers, 0) * w.kv_layer;
   w.total = off;
   return w;
 }
@@ -668,13 +727,18 @@ wam_status step_run(const wam_model& m, const wam_step_io& io, char* w, hipStrea
   const bool flash = io.t_action != nullptr && io.A > 0;
   const int64_t alt_e = flash ? (int64_t)io.B * D.d : 0, alt_e0 = flash ? (int64_t)io.B * 6 * D.d : 0;
   if (flash) TRY(time_run(m, io.B, io.t_action, e + alt_e, e0 + alt_e0, piece, stream));
-  if (!io.ctx_kv) TRY(text_run(m, io.B, io.Lc, io.text, ctx, piece, stream));
+  if (!io.ctx_kv) {
+    TRY(text_run(m, io.B, io.Lc, io.text, ctx, piece, stream));
+    const BlockWs bl = block_ws(D, io.B, L, io.Lc);
+    TRY(cross_kv_run(m, io.B, io.Lc, ctx, w + lay.kv, lay.kv_layer, D.n_layers, w + lay.block + bl.q8,
+                     reinterpret_cast<float*>(w + lay.block + bl.qs), stream));
+  }
   TRY(embed_run(m, io.B, io.F, io.Hl, io.Wl, io.A, io.z_t, io.a_t, x, piece, stream));
   for (int l = 0; l < D.n_layers; ++l) {
     wam_block_io b{};
     b.x = x; b.e0 = e0; b.rope_cos = io.rope_cos; b.rope_sin = io.rope_sin;
     b.k_cache = io.k_cache[l]; b.v_cache = io.v_cache[l]; b.Lcap = io.Lcap; b.cache_len = io.cache_len;
-    b.ch = io.ch; b.ctx = ctx; b.ctx_kv = io.ctx_kv ? io.ctx_kv[l] : nullptr;
+    b.ch = io.ch; b.ctx = ctx; b.ctx_kv = io.ctx_kv ? io.ctx_kv[l] : w + lay.kv + (size_t)l * lay.kv_layer;
     b.B = io.B; b.L = L; b.Lc = io.Lc;
     b.k_exp = io.k_exp ? io.k_exp[l] : nullptr; b.v_scale = io.v_scale ? io.v_scale[l] : 1.0f;
     hipEvent_t ev0 = io.attn_events ? io.attn_events[2 * l] : nullptr;
@@ -841,7 +905,7 @@ wam_status unipc_args(const wam_flow_dims& d, float* x, float* x_last, float* co
 }
 
 struct DenoiseWs {
-  size_t step, va, vb, cos, cos_out, state, xl, ring, kv, kv_layer, total;
+  size_t step, va, vb, cos, cos_out, state, xl, ring, total;
 };
 DenoiseWs denoise_ws(const wam_model& m, const wam_step_io& io, const wam_denoise_params& p) {
   const int64_t nx = p.cfg ? 1 : io.B;
@@ -858,9 +922,6 @@ DenoiseWs denoise_ws(const wam_model& m, const wam_step_io& io, const wam_denois
   const bool unipc = p.solver == WAM_SOLVER_UNIPC;
   w.xl = off; off += unipc ? align256((size_t)nx * n * 4) : 0;
   w.ring = off; off += unipc ? 4 * align256((size_t)nx * n * 4) : 0;
-  // the text's cross K|V of every block, computed once per chunk (unless supplied)
-  w.kv_layer = io.ctx_kv ? 0 : align256((size_t)io.B * io.Lc * 2 * m.dims.d * 2);
-  w.kv = off; off += (size_t)std::max(m.dims.n_layers, 0) * w.kv_layer;
   w.total = off;
   return w;
 }
@@ -1107,13 +1168,20 @@ wam_status wam_dit_update_fwd(const wam_model* m, const wam_step_io* io, void* w
   const bool flash = io->t_action != nullptr && io->A > 0;
   const int64_t alt_e0 = flash ? (int64_t)io->B * 6 * D.d : 0;
   if (flash) TRY(time_run(*m, io->B, io->t_action, e + (int64_t)io->B * D.d, e0 + alt_e0, piece, stream));
-  if (!io->ctx_kv && D.n_layers > 1) TRY(text_run(*m, io->B, io->Lc, io->text, ctx, piece, stream));
+  // the last block only projects its K/V, so the cross K|V of the others
+  if (!io->ctx_kv && D.n_layers > 1) {
+    TRY(text_run(*m, io->B, io->Lc, io->text, ctx, piece, stream));
+    const BlockWs bl = block_ws(D, io->B, L, io->Lc);
+    TRY(cross_kv_run(*m, io->B, io->Lc, ctx, w + lay.kv, lay.kv_layer, D.n_layers - 1, w + lay.block + bl.q8,
+                     reinterpret_cast<float*>(w + lay.block + bl.qs), stream));
+  }
   TRY(embed_run(*m, io->B, io->F, io->Hl, io->Wl, io->A, io->z_t, io->a_t, x, piece, stream));
   for (int l = 0; l < D.n_layers; ++l) {
     wam_block_io b{};
     b.x = x; b.e0 = e0; b.rope_cos = io->rope_cos; b.rope_sin = io->rope_sin;
     b.k_cache = io->k_cache[l]; b.v_cache = io->v_cache[l]; b.Lcap = io->Lcap; b.cache_len = io->cache_len;
-    b.ch = io->ch; b.ctx = ctx; b.ctx_kv = io->ctx_kv ? io->ctx_kv[l] : nullptr;
+    b.ch = io->ch; b.ctx = ctx;
+    b.ctx_kv = io->ctx_kv ? io->ctx_kv[l] : w + lay.kv + (size_t)l * lay.kv_layer;
     b.B = io->B; b.L = L; b.Lc = io->Lc;
     b.k_exp = io->k_exp ? io->k_exp[l] : nullptr; b.v_scale = io->v_scale ? io->v_scale[l] : 1.0f;
     if (l + 1 == D.n_layers) {
@@ -1228,8 +1296,10 @@ wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wa
   for (size_t i = 0; i < plan.size(); ++i) TRY(unipc_args(fd, p->x, xl, ring, (int32_t)i, plan[i], uargs[i]));
 
   // The text and so every block's cross-attention K|V are the same at every step of
-  // the chunk: unless the caller supplied them, project them once here and let each
-  // step read them (the same GEMMs a step would run, so the results are unchanged).
+  // the chunk: unless the caller supplied them, project them once here, into the step
+  // workspace's cross K|V region (the last region, so the step's other offsets are the
+  // same with ctx_kv given), and let each step read them (the same GEMMs a step would
+  // run, so the results are unchanged).
   wam_step_io sio = *io;
   std::vector<const void*> kv_ptrs;
   if (!io->ctx_kv && m->dims.n_layers > 0) {
@@ -1238,19 +1308,12 @@ wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wa
     char* sw = w + lay.step;
     const int32_t L = io->F * (io->Hl / 2) * (io->Wl / 2) + io->A;
     const BlockWs bl = block_ws(D, io->B, L, io->Lc);
-    char* q8 = sw + sl.block + bl.q8;
-    float* qs = reinterpret_cast<float*>(sw + sl.block + bl.qs);
     void* ctx = sw + sl.ctx;
     TRY(text_run(*m, io->B, io->Lc, io->text, ctx, sw + sl.piece, stream));
+    TRY(cross_kv_run(*m, io->B, io->Lc, ctx, sw + sl.kv, sl.kv_layer, D.n_layers, sw + sl.block + bl.q8,
+                     reinterpret_cast<float*>(sw + sl.block + bl.qs), stream));
     kv_ptrs.resize(D.n_layers);
-    for (int l = 0; l < D.n_layers; ++l) {
-      void* kv = w + lay.kv + (size_t)l * lay.kv_layer;
-      const wam_block_weights& W = m->blocks[l];
-      const wam_block_fp8* F8 = W.fp8;
-      TRY(proj(gemm(io->B * io->Lc, 2 * D.d, D.d, WAM_EPI_BF16, ctx, D.d, W.w_ckv, W.b_ckv, kv, 2 * D.d),
-               F8 ? F8->w_ckv : nullptr, F8 ? F8->s_ckv : nullptr, q8, qs, stream));
-      kv_ptrs[l] = kv;
-    }
+    for (int l = 0; l < D.n_layers; ++l) kv_ptrs[l] = sw + sl.kv + (size_t)l * sl.kv_layer;
     sio.ctx_kv = kv_ptrs.data();
   }
 

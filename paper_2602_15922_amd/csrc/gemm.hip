@@ -251,19 +251,19 @@ WAM_DEV void steady_group(char* smem, const GemmLane<C>& L, int kt, int K, f32x1
   if constexpr (CUR + 1 < C::STAGES) steady_group<C, CUR + 1>(smem, L, kt, K, acc);
 }
 
-template <typename C, int EPI>
-__global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int tiles_m, int tiles_n) {
-  constexpr int BM = C::BM, BN = C::BN, BK = C::BK, S = C::STAGES;
-  __shared__ __attribute__((aligned(16))) char smem[S * C::STAGE];
-  if (skip_step(g.skip)) return;
-
-  // XCD-aware remap: the hardware deals workgroups round-robin over 8 XCDs; give each
-  // XCD a contiguous range of tiles so tiles that share a W panel share an L2.
-  const int nblk = tiles_m * tiles_n;
+// XCD-aware remap: the hardware deals workgroups round-robin over 8 XCDs; give each
+// XCD a contiguous range of the nblk tiles so tiles that share a W panel share an L2.
+WAM_DEV int xcd_tile(int nblk) {
   const int i = blockIdx.x, x = i & 7, j = i >> 3;
   const int per = nblk >> 3, rem = nblk & 7;
-  const int lid = x * per + (x < rem ? x : rem) + j;
-  const int tm = lid % tiles_m, tn = lid / tiles_m;  // consecutive tiles share a W panel
+  return x * per + (x < rem ? x : rem) + j;
+}
+
+// One BM x BN output tile (row tile tm, column tile tn) of g.
+template <typename C, int EPI>
+WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn) {
+  constexpr int BM = C::BM, BN = C::BN, BK = C::BK, S = C::STAGES;
+  __shared__ __attribute__((aligned(16))) char smem[S * C::STAGE];
   const int m0 = tm * BM, n0 = tn * BN;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -448,10 +448,42 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int t
   }
 }
 
+template <typename C, int EPI>
+__global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int tiles_m, int tiles_n) {
+  if (skip_step(g.skip)) return;
+  const int lid = xcd_tile(tiles_m * tiles_n);
+  gemm_tile<C, EPI>(g, lid % tiles_m, lid / tiles_m);  // consecutive tiles share a W panel
+}
+
+// gg.n products of the same shape and A, each with its own W, bias and output: one
+// launch whose tiles run group after group (within a group as in gemm_nt).
+template <typename C, int EPI>
+__global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt_group(const GemmArgs g, int tiles_m, int tiles_n,
+                                                               const GemmGroup gg) {
+  if (skip_step(g.skip)) return;
+  const int per_group = tiles_m * tiles_n;
+  const int lid = xcd_tile(per_group * gg.n);
+  const int grp = lid / per_group, r = lid - grp * per_group;
+  GemmArgs gl = g;
+  gl.W = gg.W[grp];
+  gl.bias = gg.bias[grp];
+  gl.out = gg.out[grp];
+  gemm_tile<C, EPI>(gl, r % tiles_m, r / tiles_m);
+}
+
 template <typename Cf>
-hipError_t launch_cfg(const GemmArgs& g, hipStream_t s) {
+hipError_t launch_cfg(const GemmArgs& g, const GemmGroup* gg, hipStream_t s) {
   const int tm = (g.M + Cf::BM - 1) / Cf::BM, tn = (g.N + Cf::BN - 1) / Cf::BN;
-  dim3 grid(tm * tn), block(Cf::NT);
+  dim3 block(Cf::NT);
+  if (gg) {  // grouped: bf16 operands and the bf16 epilogue only
+    if constexpr (Cf::EB == 2) {
+      if (g.epi != WAM_EPI_BF16) return hipErrorInvalidValue;
+      hipLaunchKernelGGL((gemm_nt_group<Cf, WAM_EPI_BF16>), dim3(tm * tn * gg->n), block, 0, s, g, tm, tn, *gg);
+      return hipGetLastError();
+    }
+    return hipErrorInvalidValue;
+  }
+  dim3 grid(tm * tn);
   switch (g.epi) {
     case WAM_EPI_BF16: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_BF16>), grid, block, 0, s, g, tm, tn); break;
     case WAM_EPI_GELU_BF16: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_GELU_BF16>), grid, block, 0, s, g, tm, tn); break;
@@ -475,7 +507,8 @@ int cu_count() {
   return cus[dev];
 }
 
-hipError_t launch_gemm(const GemmArgs& gin, hipStream_t s) {
+namespace {
+hipError_t launch_any(const GemmArgs& gin, const GemmGroup* gg, hipStream_t s) {
   GemmArgs g = gin;
   if (g.a_rows <= 0) { g.a_rows = g.M; g.a_bs = 0; }
   if (g.o_rows <= 0) { g.o_rows = g.M; g.o_bs = 0; }
@@ -484,10 +517,11 @@ hipError_t launch_gemm(const GemmArgs& gin, hipStream_t s) {
   // fills the chip; below one round of them (e.g. the 512-row text projections) 128x128
   // tiles, two workgroups per CU, spread the work wider.
   const long cus = cu_count();
-  const long tiles = (long)((g.M + 127) / 128) * ((g.N + 255) / 256);
+  const long ng = gg ? gg->n : 1;
+  const long tiles = ng * ((g.M + 127) / 128) * ((g.N + 255) / 256);
   if (tiles < cus) {
-    if (g.fp8) return launch_cfg<Cfg<128, 128, 128, 2, 2, 2, 2, 1>>(g, s);
-    return launch_cfg<Cfg<128, 128, 64, 2, 2, 2, 2>>(g, s);
+    if (g.fp8) return launch_cfg<Cfg<128, 128, 128, 2, 2, 2, 2, 1>>(g, gg, s);
+    return launch_cfg<Cfg<128, 128, 64, 2, 2, 2, 2>>(g, gg, s);
   }
   // Taller tiles are more efficient per flop but coarser.  Measured with launches
   // interleaved, a round of 128x256, 192x256 (8 wavefronts of 96x64, 2-stage ring) and
@@ -496,18 +530,26 @@ hipError_t launch_gemm(const GemmArgs& gin, hipStream_t s) {
   // M = 3152: QKV 1020 tiles of 192 rows in 4 rounds (487 -> 469 us), FFN1 702 of 256 rows
   // in 3 rounds (480 -> 439 us), O and FFN2 keep 128 rows (500 tiles, 2 rounds).
   // FP8 takes the same tiles with 128-wide slices (the bytes of a 64-wide bf16 slice).
-  auto rounds = [&](int bm) { return ((long)((g.M + bm - 1) / bm) * ((g.N + 255) / 256) + cus - 1) / cus; };
+  auto rounds = [&](int bm) { return (ng * ((g.M + bm - 1) / bm) * ((g.N + 255) / 256) + cus - 1) / cus; };
   const long c128 = 18 * rounds(128), c192 = 26 * rounds(192), c256 = 33 * rounds(256);
   if (c256 < c128 && c256 <= c192) {
-    if (g.fp8) return launch_cfg<Cfg<256, 256, 128, 2, 2, 4, 2, 1>>(g, s);
-    return launch_cfg<Cfg<256, 256, 64, 2, 2, 4, 2>>(g, s);
+    if (g.fp8) return launch_cfg<Cfg<256, 256, 128, 2, 2, 4, 2, 1>>(g, gg, s);
+    return launch_cfg<Cfg<256, 256, 64, 2, 2, 4, 2>>(g, gg, s);
   }
   if (c192 < c128) {
-    if (g.fp8) return launch_cfg<Cfg<192, 256, 128, 2, 2, 4, 2, 1>>(g, s);
-    return launch_cfg<Cfg<192, 256, 64, 2, 2, 4, 2>>(g, s);
+    if (g.fp8) return launch_cfg<Cfg<192, 256, 128, 2, 2, 4, 2, 1>>(g, gg, s);
+    return launch_cfg<Cfg<192, 256, 64, 2, 2, 4, 2>>(g, gg, s);
   }
-  if (g.fp8) return launch_cfg<Cfg<128, 256, 128, 3, 2, 4, 2, 1>>(g, s);
-  return launch_cfg<Cfg<128, 256, 64, 3, 2, 4, 2>>(g, s);
+  if (g.fp8) return launch_cfg<Cfg<128, 256, 128, 3, 2, 4, 2, 1>>(g, gg, s);
+  return launch_cfg<Cfg<128, 256, 64, 3, 2, 4, 2>>(g, gg, s);
+}
+}  // namespace
+
+hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) { return launch_any(g, nullptr, s); }
+
+hipError_t launch_gemm_group(const GemmArgs& g, const GemmGroup& gg, hipStream_t s) {
+  if (gg.n < 1 || gg.n > WAM_GEMM_GROUP_MAX || g.fp8 || g.epi != WAM_EPI_BF16) return hipErrorInvalidValue;
+  return launch_any(g, &gg, s);
 }
 
 }  // namespace wam

@@ -62,6 +62,16 @@ struct GemmArgs {
   const int32_t* skip;
 };
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
+// n products sharing A and every size and stride, each with its own W, bias and output
+// (bf16 epilogue, bf16 operands), in one launch.
+constexpr int WAM_GEMM_GROUP_MAX = 48;
+struct GemmGroup {
+  int32_t n;
+  const void* W[WAM_GEMM_GROUP_MAX];
+  const float* bias[WAM_GEMM_GROUP_MAX];
+  void* out[WAM_GEMM_GROUP_MAX];
+};
+hipError_t launch_gemm_group(const GemmArgs& g, const GemmGroup& gg, hipStream_t s);
 
 struct LnArgs {
   int32_t rows, rows_per_batch, d;

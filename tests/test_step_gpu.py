@@ -46,18 +46,19 @@ def test_step_14b_shapes_one_block():
     check_step(case, vv, va)
 
 
-def identity_model(wl, n_layers):
+def identity_model(wl, n_layers, identity=True):
     """Seeded model-level weights with the gate rows of the time projection zeroed, and
     device-random blocks whose gates and cross-attention output projection are zero: every
-    block is then the identity on the residual."""
+    block is then the identity on the residual (identity=False: nothing zeroed)."""
     import torch
     w = lib()
     P = synth.model_params(wl)
     d = wl.d
-    bits = P["w_t6"].data.copy()
-    bits[2 * d:3 * d] = 0
-    bits[5 * d:6 * d] = 0
-    P["w_t6"] = synth.Tensor("bf16", bits)
+    if identity:
+        bits = P["w_t6"].data.copy()
+        bits[2 * d:3 * d] = 0
+        bits[5 * d:6 * d] = 0
+        P["w_t6"] = synth.Tensor("bf16", bits)
     top = {k: dev(v) for k, v in P.items()}
     g = torch.Generator(device="cuda").manual_seed(11)
 
@@ -67,11 +68,13 @@ def identity_model(wl, n_layers):
     blocks, kcs, vcs = [], [], []
     for _ in range(n_layers):
         mod6 = torch.randn(6, d, generator=g, device="cuda") * 0.02
-        mod6[2] = 0.0
-        mod6[5] = 0.0
+        if identity:
+            mod6[2] = 0.0
+            mod6[5] = 0.0
+        w_co = torch.zeros(d, d, dtype=torch.bfloat16, device="cuda") if identity else rn(d, d)
         blocks.append({"w_qkv": rn(3 * d, d), "w_o": rn(d, d), "w_cq": rn(d, d), "w_ckv": rn(2 * d, d),
-                       "w_co": torch.zeros(d, d, dtype=torch.bfloat16, device="cuda"), "w_f1": rn(wl.ffn, d),
-                       "w_f2": rn(d, wl.ffn), "mod6": mod6})
+                       "w_co": w_co, "w_f1": rn(wl.ffn, d), "w_f2": rn(d, wl.ffn), "mod6": mod6,
+                       "b_ckv": (torch.randn(2 * d, generator=g, device="cuda") * 0.05)})
         kcs.append(rn(wl.B, wl.Lcap, wl.H, wl.Dh, std=1.0))
         vcs.append(rn(wl.B, wl.Lcap, wl.H, wl.Dh, std=1.0))
     return P, w.make_model(dims_of(wl, n_layers), top, blocks), (top, blocks, kcs, vcs)
@@ -133,3 +136,40 @@ def test_step_rejects_undersized_workspace():
     with pytest.raises(w.WamError) as ei:
         w.wam_dit_step_fwd(case.model, io, workspace(need - 512))
     assert ei.value.status == w.binding.WAM_EWORKSPACE
+
+
+def test_step_cross_kv_projection_over_many_blocks():
+    """With no cross K|V given, the step projects every block's cross-attention K|V from
+    the projected text before the first block, in grouped launches of at most 48 blocks:
+    with 50 blocks (a group of 48 and one of 2) the velocities equal, bit for bit, those
+    of the step given the same K|V from one wam_gemm_bf16 call per block."""
+    import torch
+    w = lib()
+    wl = synth.WORKLOADS["block_d512"].replace(n_cached=1, n_layers=50)
+    log("step cross K|V over 50 blocks")
+    P, model, keep = identity_model(wl, wl.n_layers, identity=False)
+    top, blocks, kcs, vcs = keep
+    case = StepCase(wl, 0)
+    cos, sin = gpu_rope_tables(wl)
+    text = dev(case.text)
+    outs = []
+    for given in (False, True):
+        kvs = None
+        if given:
+            ctx = torch.empty((wl.B, wl.Lc, wl.d), dtype=torch.bfloat16, device="cuda")
+            w.wam_text_proj_fwd(model, text, ctx, workspace(w.wam_text_proj_workspace_bytes(model.dims, wl.B, wl.Lc)))
+            kvs = []
+            for b in blocks:
+                kv = torch.empty((wl.B, wl.Lc, 2 * wl.d), dtype=torch.bfloat16, device="cuda")
+                w.wam_gemm_bf16(ctx.view(-1, wl.d), b["w_ckv"], kv.view(-1, 2 * wl.d), w.WAM_EPI_BF16,
+                                bias=b["b_ckv"])
+                kvs.append(kv)
+        vv = torch.empty((wl.B, wl.latent_ch, wl.F, wl.Hl, wl.Wl), dtype=torch.float32, device="cuda")
+        va = torch.empty((wl.B, wl.A, wl.act_dim), dtype=torch.float32, device="cuda")
+        io = w.make_step_io(dev(case.z), dev(case.a), dev(case.t), text, kcs, vcs, cos, sin, wl.cache_rows,
+                            w.cached_chunks(wl.cache_rows, wl.L), vv, va, ctx_kv=kvs)
+        w.wam_dit_step_fwd(model, io, workspace(w.wam_step_workspace_bytes(model, io)))
+        torch.cuda.synchronize()
+        outs.append((host(vv), host(va)))
+    assert np.all(np.isfinite(outs[0][0])) and np.abs(outs[0][0]).max() > 0
+    assert np.array_equal(outs[0][0], outs[1][0]) and np.array_equal(outs[0][1], outs[1][1])
