@@ -21,7 +21,7 @@ namespace {
 // workgroup builds P and Q, and the barrier after that waits for the LDS writes only,
 // so the row is in flight while the modulation vectors are read.
 // ---------------------------------------------------------------------------------
-constexpr int LN_ROWS = 4;  // rows (= wavefronts) per workgroup
+constexpr int LN_ROWS = 8;  // rows (= wavefronts) per workgroup
 
 template <int NV>
 // (4 wavefronts per SIMD up to d = 5120: a row, 80 VGPRs, fits with the rest in 128)
