@@ -580,48 +580,49 @@ wam_status head_run(const wam_model& m, int32_t B, int32_t F, int32_t Hl, int32_
 }
 
 // Every block's cross-attention K|V of the projected text ctx (B*Lc rows, the same input
-// for every block) into kv + l*kv_layer for the first n blocks: the blocks with bf16
-// weights in grouped launches of up to WAM_GEMM_GROUP_MAX (the tiles and arithmetic of
-// one launch per block, but 512-row products that fill the chip together instead of
-// ~1.25 rounds each), those with FP8 weights one launch each.
+// for every block) into kv + l*kv_layer for the first n blocks, in grouped launches of up
+// to WAM_GEMM_GROUP_MAX blocks: the tiles and arithmetic of one launch per block, but the
+// 512-row products fill the chip together instead of ~1.25 rounds each.  Blocks with bf16
+// weights and blocks with FP8 weights form separate groups; for the FP8 ones the text is
+// quantized once (per-row scales, as for any FP8 projection) and shared.
 wam_status cross_kv_run(const wam_model& m, int32_t B, int32_t Lc, const void* ctx, char* kv, size_t kv_layer,
                         int n, char* q8, float* qs, hipStream_t s) {
   const wam_dims& D = m.dims;
-  GemmGroup gg{};
-  GemmArgs first{};
-  std::vector<GemmArgs> members;
-  members.reserve(n);
-  for (int l = 0; l < n; ++l) {  // validate every bf16 member before the first launch
+  const int M = B * Lc, N = 2 * D.d, K = D.d;
+  const int64_t ldq = (K + 15) / 16 * 16;
+  std::vector<GemmArgs> members(n);
+  bool any_fp8 = false;
+  for (int l = 0; l < n; ++l) {  // validate every member before the first launch
     const wam_block_weights& W = m.blocks[l];
+    wam_gemm_desc g = gemm(M, N, K, WAM_EPI_BF16, ctx, K, W.w_ckv, W.b_ckv, kv + (size_t)l * kv_layer, N);
     if (W.fp8) {
-      members.push_back(GemmArgs{});
-      continue;
-    }
-    const wam_gemm_desc g = gemm(B * Lc, 2 * D.d, D.d, WAM_EPI_BF16, ctx, D.d, W.w_ckv, W.b_ckv,
-                                 kv + (size_t)l * kv_layer, 2 * D.d);
-    GemmArgs a;
-    TRY(gemm_prep(g, a));
-    members.push_back(a);
-  }
-  for (int l = 0; l < n; ++l) {
-    const wam_block_weights& W = m.blocks[l];
-    const GemmArgs& a = members[l];
-    if (W.fp8) {
-      TRY(proj(gemm(B * Lc, 2 * D.d, D.d, WAM_EPI_BF16, ctx, D.d, W.w_ckv, W.b_ckv, kv + (size_t)l * kv_layer,
-                    2 * D.d), W.fp8->w_ckv, W.fp8->s_ckv, q8, qs, s));
-      continue;
-    }
-    if (a.M == 0) continue;
-    if (gg.n == 0) first = a;
-    gg.W[gg.n] = a.W;
-    gg.bias[gg.n] = a.bias;
-    gg.out[gg.n] = a.out;
-    if (++gg.n == WAM_GEMM_GROUP_MAX) {
-      HIPCHECK(launch_gemm_group(pred(first), gg, s));
-      gg.n = 0;
+      g.A = q8; g.lda = ldq; g.W = W.fp8->w_ckv; g.ldw = K;
+      TRY(gemm_prep(g, members[l], 0, 0, qs, W.fp8->s_ckv));
+      any_fp8 = true;
+    } else {
+      TRY(gemm_prep(g, members[l]));
     }
   }
-  if (gg.n > 0) HIPCHECK(launch_gemm_group(pred(first), gg, s));
+  if (M == 0 || n == 0) return WAM_OK;
+  if (any_fp8) HIPCHECK(launch_quant_rows(M, K, ctx, K, q8, ldq, qs, s, t_skip));
+  for (int fp8 = 0; fp8 < 2; ++fp8) {
+    GemmGroup gg{};
+    GemmArgs first{};
+    for (int l = 0; l < n; ++l) {
+      if ((m.blocks[l].fp8 != nullptr) != (fp8 == 1)) continue;
+      const GemmArgs& a = members[l];
+      if (gg.n == 0) first = a;
+      gg.W[gg.n] = a.W;
+      gg.bias[gg.n] = a.bias;
+      gg.out[gg.n] = a.out;
+      gg.w_scale[gg.n] = a.w_scale;
+      if (++gg.n == WAM_GEMM_GROUP_MAX) {
+        HIPCHECK(launch_gemm_group(pred(first), gg, s));
+        gg.n = 0;
+      }
+    }
+    if (gg.n > 0) HIPCHECK(launch_gemm_group(pred(first), gg, s));
+  }
   return WAM_OK;
 }
 

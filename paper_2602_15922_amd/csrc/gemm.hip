@@ -468,6 +468,7 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt_group(const GemmArgs g,
   gl.W = gg.W[grp];
   gl.bias = gg.bias[grp];
   gl.out = gg.out[grp];
+  if constexpr (C::EB == 1) gl.w_scale = gg.w_scale[grp];
   gemm_tile<C, EPI>(gl, r % tiles_m, r / tiles_m);
 }
 
@@ -475,13 +476,10 @@ template <typename Cf>
 hipError_t launch_cfg(const GemmArgs& g, const GemmGroup* gg, hipStream_t s) {
   const int tm = (g.M + Cf::BM - 1) / Cf::BM, tn = (g.N + Cf::BN - 1) / Cf::BN;
   dim3 block(Cf::NT);
-  if (gg) {  // grouped: bf16 operands and the bf16 epilogue only
-    if constexpr (Cf::EB == 2) {
-      if (g.epi != WAM_EPI_BF16) return hipErrorInvalidValue;
-      hipLaunchKernelGGL((gemm_nt_group<Cf, WAM_EPI_BF16>), dim3(tm * tn * gg->n), block, 0, s, g, tm, tn, *gg);
-      return hipGetLastError();
-    }
-    return hipErrorInvalidValue;
+  if (gg) {  // grouped: the bf16 epilogue only
+    if (g.epi != WAM_EPI_BF16) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemm_nt_group<Cf, WAM_EPI_BF16>), dim3(tm * tn * gg->n), block, 0, s, g, tm, tn, *gg);
+    return hipGetLastError();
   }
   dim3 grid(tm * tn);
   switch (g.epi) {
@@ -548,7 +546,7 @@ hipError_t launch_any(const GemmArgs& gin, const GemmGroup* gg, hipStream_t s) {
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) { return launch_any(g, nullptr, s); }
 
 hipError_t launch_gemm_group(const GemmArgs& g, const GemmGroup& gg, hipStream_t s) {
-  if (gg.n < 1 || gg.n > WAM_GEMM_GROUP_MAX || g.fp8 || g.epi != WAM_EPI_BF16) return hipErrorInvalidValue;
+  if (gg.n < 1 || gg.n > WAM_GEMM_GROUP_MAX || g.epi != WAM_EPI_BF16) return hipErrorInvalidValue;
   return launch_any(g, &gg, s);
 }
 

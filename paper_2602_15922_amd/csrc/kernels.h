@@ -62,14 +62,15 @@ struct GemmArgs {
   const int32_t* skip;
 };
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
-// n products sharing A and every size and stride, each with its own W, bias and output
-// (bf16 epilogue, bf16 operands), in one launch.
+// n products sharing A (and, for FP8 operands, its row scales) and every size and stride,
+// each with its own W, bias, output and (FP8) column scales, in one launch; bf16 epilogue.
 constexpr int WAM_GEMM_GROUP_MAX = 48;
 struct GemmGroup {
   int32_t n;
   const void* W[WAM_GEMM_GROUP_MAX];
   const float* bias[WAM_GEMM_GROUP_MAX];
   void* out[WAM_GEMM_GROUP_MAX];
+  const float* w_scale[WAM_GEMM_GROUP_MAX];
 };
 hipError_t launch_gemm_group(const GemmArgs& g, const GemmGroup& gg, hipStream_t s);
 
