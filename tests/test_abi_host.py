@@ -234,3 +234,21 @@ def test_unipc_plan_and_step_reject_bad_arguments_without_a_gpu():
                             None) == b.WAM_EINVAL
     assert L.wam_unipc_step(C.byref(d), None, None, None, 4096, 4096, ring, 0, C.byref(b.wam_unipc_coef()), None,
                             4096, None, None) == b.WAM_EINVAL
+
+
+def test_step_workspace_holds_every_blocks_cross_kv_without_ctx_kv():
+    """Without precomputed cross K|V the step projects every block's into its workspace
+    (the last region): the size grows by exactly n_layers * align256(B * Lc * 2d * 2)
+    bytes, and the update pass and the loop use the same layout."""
+    w = lib()
+    b = w.binding
+    for (d, H, n_layers, B, Lc) in ((5120, 40, 40, 1, 512), (512, 4, 3, 2, 77)):
+        m = b.wam_model()
+        m.dims = w.make_dims(d, H, 128, 4 * d, n_layers)
+        io = b.wam_step_io(B=B, F=2, Hl=8, Wl=8, A=4, Lc=Lc, Lcap=200, cache_len=0)
+        without = w.lib().wam_step_workspace_bytes(C.byref(m), C.byref(io))
+        given = (C.c_void_p * n_layers)(*([4096] * n_layers))
+        io.ctx_kv = C.cast(given, C.POINTER(C.c_void_p))
+        with_kv = w.lib().wam_step_workspace_bytes(C.byref(m), C.byref(io))
+        per_layer = (B * Lc * 2 * d * 2 + 255) // 256 * 256
+        assert without - with_kv == n_layers * per_layer, (d, without, with_kv)
