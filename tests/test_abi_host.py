@@ -239,7 +239,7 @@ def test_unipc_plan_and_step_reject_bad_arguments_without_a_gpu():
 def test_step_workspace_holds_every_blocks_cross_kv_without_ctx_kv():
     """Without precomputed cross K|V the step projects every block's into its workspace
     (the last region): the size grows by exactly n_layers * align256(B * Lc * 2d * 2)
-    bytes, and the update pass and the loop use the same layout."""
+    bytes over the size with ctx_kv given."""
     w = lib()
     b = w.binding
     for (d, H, n_layers, B, Lc) in ((5120, 40, 40, 1, 512), (512, 4, 3, 2, 77)):
