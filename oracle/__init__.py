@@ -15,8 +15,9 @@ intermediate rounding, written for a reader to check by eye against the paper:
   (Appendix C, Algorithm 2, the denoising-loop forward with update=False), its cache
   update pass (update=True) and the denoising loop around it (solver step, guidance,
   DiT caching);
-* the block internals the paper leaves unstated (AdaLN-modulated LayerNorm, 3D RoPE,
-  cross-attention to text, tanh-GELU FFN) follow the readings listed in the design doc.
+* the block internals the paper leaves unstated follow fixed readings, stated with
+  each function: AdaLN-modulated LayerNorm (shift, scale, gate per branch), 3D RoPE,
+  cross-attention to text behind an affine LayerNorm with no gate, tanh-GELU FFN.
 
 Every function is pinned by ``tests/test_oracle_pins.py`` against brute force,
 closed forms, invariants and library routines.

@@ -364,6 +364,7 @@ def test_block_zero_gates():
         W2[n] = W[n] * -3.0 + 1.0
     out2, _, _ = oracle.dit_block(x, e0, W2, H, 1e-6, pos, ch, ctx=ctx)
     assert np.allclose(out, out2, atol=1e-13)
+    assert np.max(np.abs(out - x)) > 1e-2  # the ungated cross-attention branch still moves x
     # ... and with the cross-attention output projection zeroed the block is the identity
     W2["w_co"] = np.zeros_like(W["w_co"])
     W2["b_co"] = np.zeros_like(W["b_co"])
@@ -398,6 +399,189 @@ def test_block_precomputed_cross_kv():
     kv = oracle.linear(ctx, W["w_ckv"], W["b_ckv"])
     b, _, _ = oracle.dit_block(x, e0, W, H, 1e-6, pos, ch, ctx_kv=kv)
     assert np.array_equal(a, b)
+
+
+# ----------------------------------------------------------------------------- every branch live, by hand
+def _ln_by_hand(v, eps):
+    n = len(v)
+    mu = sum(v) / n
+    var = sum((a - mu) ** 2 for a in v) / n
+    return [(a - mu) / math.sqrt(var + eps) for a in v]
+
+
+def _matvec(W, b, v):
+    return [sum(W[r][c] * v[c] for c in range(len(v))) + b[r] for r in range(len(W))]
+
+
+def _softmax_mix(q, keys, vals, scale):
+    s = [scale * sum(qa * ka for qa, ka in zip(q, k)) for k in keys]
+    m = max(s)
+    w = [math.exp(a - m) for a in s]
+    z = sum(w)
+    return [sum(w[j] * vals[j][c] for j in range(len(keys))) / z for c in range(len(vals[0]))]
+
+
+def test_block_every_branch_by_hand():
+    """A block with every branch live, recomputed token by token with scalar loops:
+    gates g1 != g2 (both non-zero), non-zero W_co and b_co, cross LayerNorm with
+    gamma != 1 and beta != 0, non-zero biases, a cached key of an earlier chunk (visible)
+    and one of a later chunk (hidden).  Dh = 6 splits into three one-pair RoPE segments
+    (t | h | w), each turned by its position in radians.  This fixes the block's wiring:
+    g1 scales the self-attention branch and g2 the FFN, the cross branch has no gate and
+    reads LN(x) gamma + beta of the residual after the self-attention update, the FFN reads
+    the residual after the cross update."""
+    d, H, Dh, Fh, eps = 12, 2, 6, 10, 1e-6
+    g = np.random.default_rng(500)
+    W = small_block_weights(d, Fh, 501)
+    e0 = g.standard_normal((1, 6, d)) * 0.5
+    m = W["mod6"] + e0[0]
+    sh1, sc1, g1, sh2, sc2, g2 = (list(m[i]) for i in range(6))
+    assert min(abs(a - b) for a, b in zip(g1, g2)) > 1e-3 and min(map(abs, g1 + g2)) > 1e-3
+    x = g.standard_normal((1, 2, d))
+    pos = np.array([[2, 1, 3], [3, 0, 2]])
+    ctx = g.standard_normal((1, 3, d))
+    k_prev = g.standard_normal((1, 2, H, Dh))
+    v_prev = g.standard_normal((1, 2, H, Dh))
+    prev_chunk = np.array([0, 2])
+    out, k_cur, v_cur = oracle.dit_block(x, e0, W, H, eps, pos, np.array([1, 1]), k_prev, v_prev, prev_chunk,
+                                         ctx=ctx)
+
+    L_ = lambda a: [list(r) for r in np.asarray(a)]  # noqa: E731
+    Wqkv, Wo, Wcq, Wckv, Wco, W1, W2 = (L_(W[n]) for n in ("w_qkv", "w_o", "w_cq", "w_ckv", "w_co", "w_f1", "w_f2"))
+    bqkv, bo, bcq, bckv, bco, b1, b2 = (list(W[n]) for n in ("b_qkv", "b_o", "b_cq", "b_ckv", "b_co", "b_f1", "b_f2"))
+    gam, bet = list(W["lnc_gamma"]), list(W["lnc_beta"])
+
+    def rope(vec, p):  # one head: pairs (0,1) by p_t, (2,3) by p_h, (4,5) by p_w radians
+        r = list(vec)
+        for a in range(3):
+            c, s = math.cos(p[a]), math.sin(p[a])
+            x0, x1 = vec[2 * a], vec[2 * a + 1]
+            r[2 * a], r[2 * a + 1] = x0 * c - x1 * s, x0 * s + x1 * c
+        return r
+
+    # self-attention inputs of both current tokens
+    q_t, k_t, v_t = [], [], []
+    for i in range(2):
+        n1 = _ln_by_hand(list(x[0, i]), eps)
+        h1 = [n1[c] * (1 + sc1[c]) + sh1[c] for c in range(d)]
+        qkv = _matvec(Wqkv, bqkv, h1)
+        q_t.append([rope(qkv[hh * Dh:(hh + 1) * Dh], pos[i]) for hh in range(H)])
+        k_t.append([rope(qkv[d + hh * Dh:d + (hh + 1) * Dh], pos[i]) for hh in range(H)])
+        v_t.append([qkv[2 * d + hh * Dh:2 * d + (hh + 1) * Dh] for hh in range(H)])
+    ctx_k = [_matvec([r for r in Wckv[:d]], bckv[:d], list(ctx[0, j])) for j in range(3)]
+    ctx_v = [_matvec([r for r in Wckv[d:]], bckv[d:], list(ctx[0, j])) for j in range(3)]
+    for i in range(2):
+        # keys visible to chunk 1: the cached row of chunk 0 and both current rows
+        o = []
+        for hh in range(H):
+            keys = [list(k_prev[0, 0, hh]), k_t[0][hh], k_t[1][hh]]
+            vals = [list(v_prev[0, 0, hh]), v_t[0][hh], v_t[1][hh]]
+            o += _softmax_mix(q_t[i][hh], keys, vals, 1 / math.sqrt(Dh))
+        ao = _matvec(Wo, bo, o)
+        x1 = [x[0, i, c] + g1[c] * ao[c] for c in range(d)]
+        nc = _ln_by_hand(x1, eps)
+        hc = [nc[c] * gam[c] + bet[c] for c in range(d)]
+        cq = _matvec(Wcq, bcq, hc)
+        oc = []
+        for hh in range(H):
+            sl = slice(hh * Dh, (hh + 1) * Dh)
+            oc += _softmax_mix(cq[sl], [k[sl] for k in ctx_k], [v[sl] for v in ctx_v], 1 / math.sqrt(Dh))
+        co = _matvec(Wco, bco, oc)
+        x2 = [x1[c] + co[c] for c in range(d)]
+        n2 = _ln_by_hand(x2, eps)
+        h2 = [n2[c] * (1 + sc2[c]) + sh2[c] for c in range(d)]
+        u = [0.5 * a * (1 + math.tanh(math.sqrt(2 / math.pi) * (a + 0.044715 * a ** 3))) for a in _matvec(W1, b1, h2)]
+        f = _matvec(W2, b2, u)
+        x3 = [x2[c] + g2[c] * f[c] for c in range(d)]
+        assert np.max(np.abs(out[0, i] - np.array(x3))) <= 1e-12
+        for hh in range(H):
+            assert np.max(np.abs(k_cur[0, i, hh] - np.array(k_t[i][hh]))) <= 1e-12
+            assert np.max(np.abs(v_cur[0, i, hh] - np.array(v_t[i][hh]))) <= 1e-12
+
+
+def test_block_gate_assignment():
+    """g1 gates only the self-attention branch and g2 only the FFN: with g2 = 0 the FFN
+    weights cannot matter while the O projection does; with g1 = 0 the reverse."""
+    d, H, Fh, B, L = 16, 2, 32, 1, 6
+    base = small_block_weights(d, Fh, 510)
+    x = rnd(B, L, d, seed=511)
+    ctx = rnd(B, 4, d, seed=512)
+    pos = chunk_positions(0, 1, 1, 4, 2)
+    ch = np.zeros(L, int)
+    for zero_gate, dead, live in ((5, ("w_f1", "w_f2", "b_f1", "b_f2"), ("w_o", "b_o")),
+                                  (2, ("w_qkv", "w_o", "b_qkv", "b_o"), ("w_f2", "b_f2"))):
+        W = dict(base)
+        W["mod6"] = base["mod6"].copy()
+        W["mod6"][zero_gate] = 0.0
+        e0 = rnd(B, 6, d, seed=513)
+        e0[:, zero_gate] = 0.0
+        out, _, _ = oracle.dit_block(x, e0, W, H, 1e-6, pos, ch, ctx=ctx)
+        Wd = dict(W)
+        for n in dead:
+            Wd[n] = W[n] * -2.0 + 0.5
+        out_d, _, _ = oracle.dit_block(x, e0, Wd, H, 1e-6, pos, ch, ctx=ctx)
+        assert np.allclose(out, out_d, atol=1e-13)
+        Wl = dict(W)
+        for n in live:
+            Wl[n] = W[n] * -2.0 + 0.5
+        out_l, _, _ = oracle.dit_block(x, e0, Wl, H, 1e-6, pos, ch, ctx=ctx)
+        assert np.max(np.abs(out - out_l)) > 1e-3
+
+
+def test_block_cross_branch_reads_the_affine_layernorm_only():
+    """With g1 = g2 = 0 only the cross-attention branch moves x.  That branch takes no
+    AdaLN shift or scale (changing them changes nothing), and its LayerNorm is affine:
+    with gamma = 0 every token's cross query is W_cq beta + b_cq, so every token receives
+    the same increment."""
+    d, H, Fh, B, L = 16, 2, 32, 1, 7
+    W = small_block_weights(d, Fh, 520)
+    W["mod6"][2] = W["mod6"][5] = 0.0
+    e0 = rnd(B, 6, d, seed=521)
+    e0[:, 2] = e0[:, 5] = 0.0
+    x = rnd(B, L, d, seed=522)
+    ctx = rnd(B, 4, d, seed=523)
+    pos = chunk_positions(0, 1, 1, 5, 2)
+    ch = np.zeros(L, int)
+    out, _, _ = oracle.dit_block(x, e0, W, H, 1e-6, pos, ch, ctx=ctx)
+    assert np.max(np.abs(out - x)) > 1e-2  # the cross branch is live
+    e0b = e0.copy()
+    for i in (0, 1, 3, 4):
+        e0b[:, i] = rnd(B, d, seed=530 + i) * 2.0
+    out_b, _, _ = oracle.dit_block(x, e0b, W, H, 1e-6, pos, ch, ctx=ctx)
+    assert np.allclose(out_b, out, atol=1e-13)
+    Wg = dict(W)
+    Wg["lnc_gamma"] = np.zeros(d)
+    out_g, _, _ = oracle.dit_block(x, e0, Wg, H, 1e-6, pos, ch, ctx=ctx)
+    inc = out_g - x
+    assert np.allclose(inc, inc[:, :1], atol=1e-13)
+    # that shared increment is the cross attention of the query W_cq beta + b_cq
+    cq = W["w_cq"] @ W["lnc_beta"] + W["b_cq"]
+    kv = W["w_ckv"] @ ctx[0].T + W["b_ckv"][:, None]
+    o = []
+    for hh in range(H):
+        sl = slice(hh * 8, (hh + 1) * 8)
+        o += _softmax_mix(list(cq[sl]), [list(kv[:d][sl, j]) for j in range(4)],
+                          [list(kv[d:][sl, j]) for j in range(4)], 1 / math.sqrt(8))
+    assert np.allclose(inc[0, 0], W["w_co"] @ np.array(o) + W["b_co"], atol=1e-12)
+
+
+def test_text_projection_by_hand():
+    """Text features -> context: Linear, then tanh-GELU, then Linear, token by token."""
+    g = np.random.default_rng(540)
+    B, Lc, tdim, d = 2, 3, 7, 5
+    text = g.standard_normal((B, Lc, tdim))
+    w1, b1 = g.standard_normal((d, tdim)), g.standard_normal(d)
+    w2, b2 = g.standard_normal((d, d)) * 0.5, g.standard_normal(d)
+    got = oracle.text_projection(text, w1, b1, w2, b2)
+    for b in range(B):
+        for j in range(Lc):
+            hid = []
+            for r in range(d):
+                a = b1[r] + sum(w1[r, c] * text[b, j, c] for c in range(tdim))
+                hid.append(0.5 * a * (1 + math.tanh(math.sqrt(2 / math.pi) * (a + 0.044715 * a ** 3))))
+            for r in range(d):
+                want = b2[r] + sum(w2[r, c] * hid[c] for c in range(d))
+                assert abs(got[b, j, r] - want) <= 1e-12
 
 
 # ----------------------------------------------------------------------------- step (P12)
