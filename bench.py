@@ -43,6 +43,16 @@ def parse():
                         "launches at the workload's shape; prints what ran and exits")
     p.add_argument("--probe-attn-fp8", type=int, default=0, metavar="N",
                    help="the same with the FP8 self-attention (operands quantized by the library)")
+    p.add_argument("--probe", choices=("gemm", "ln", "rope"), default=None,
+                   help="counter-collection mode: the calibration copy, then --probe-n launches of each "
+                        "of the block's six projections (gemm), of the AdaLN LayerNorm (ln) or of the "
+                        "RoPE/KV-append kernel (rope) at the workload's shapes")
+    p.add_argument("--probe-n", type=int, default=3)
+    p.add_argument("--profile-steps", type=int, default=2,
+                   help="untimed steps after the timed ones with events around every launch of every "
+                        "block (per-role kernel times: the GEMM fractions of the JSON line)")
+    p.add_argument("--pmc-summary", default=None, metavar="DIR",
+                   help="no GPU: print per-kernel averages of a rocprofv3 counter CSV under DIR")
     return p.parse_args()
 
 
@@ -91,6 +101,61 @@ def build_model(wl, torch):
     inputs["cos"] = torch.from_numpy(cos).to(dev)
     inputs["sin"] = torch.from_numpy(sin).to(dev)
     return model, (top, blocks), kcs, vcs, inputs
+
+
+# Per-role algorithmic work of one block launch at the workload's shapes: flops for the
+# matrix kernels (2*M*N*K per projection, 4*Dh per visible (q, k) pair per head for
+# attention), bytes for the memory-bound ones (LayerNorm: fp32 row in, bf16 row out;
+# RoPE/append: the bf16 q|k|v row in, q, k and v out).
+def role_work(wl):
+    M, d, F = wl.B * wl.L, wl.d, wl.ffn
+    return {
+        "ln1": ("GB/s", M * d * 6), "qkv": ("TFLOP/s", 2 * M * d * 3 * d), "rope": ("GB/s", M * 3 * d * 2 * 2),
+        "self_attn": ("TFLOP/s", 4 * wl.H * wl.Dh * M * wl.Lk), "o": ("TFLOP/s", 2 * M * d * d),
+        "lnc": ("GB/s", M * d * 6), "cq": ("TFLOP/s", 2 * M * d * d),
+        "cross_attn": ("TFLOP/s", 4 * wl.H * wl.Dh * M * wl.Lc), "co": ("TFLOP/s", 2 * M * d * d),
+        "ln2": ("GB/s", M * d * 6), "ffn1": ("TFLOP/s", 2 * M * d * F), "ffn2": ("TFLOP/s", 2 * M * F * d),
+    }
+
+
+MI355X_HBM_GBPS = 8000.0  # published HBM3E peak
+
+
+def profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, n_steps):
+    """Per-role average launch time over n_steps untimed steps that record events around
+    every launch of every block, with each role's achieved rate and fraction of its peak
+    (bf16 dense MFMA for GEMMs and attention, HBM for LayerNorm and RoPE)."""
+    import paper_2602_15922_amd as w
+    names = w.binding.BLOCK_EVENT_NAMES
+    nk = len(names)
+    chunks = w.cached_chunks(wl.cache_rows, wl.L)
+    sums = [0.0] * nk
+    ws = None
+    for _ in range(n_steps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * nk * wl.n_layers)]
+        io = w.make_step_io(inp["z"], inp["a"], inp["t"], inp["text"], kcs, vcs, inp["cos"], inp["sin"],
+                            wl.cache_rows, chunks, vv, va, block_events=ev)
+        if ws is None:
+            ws = torch.empty(w.wam_step_workspace_bytes(model, io), dtype=torch.uint8, device="cuda")
+        w.wam_dit_step_fwd(model, io, ws)
+        torch.cuda.synchronize()
+        for l in range(wl.n_layers):
+            for k in range(nk):
+                sums[k] += ev[2 * (l * nk + k)].elapsed_time(ev[2 * (l * nk + k) + 1])
+    work = role_work(wl)
+    out = {}
+    for k, name in enumerate(names):
+        ms = sums[k] / (n_steps * wl.n_layers)
+        unit, amount = work[name]
+        if unit == "TFLOP/s":
+            rate = amount / (ms * 1e-3) / 1e12
+            peak = MI355X_BF16_DENSE_TFLOPS
+        else:
+            rate = amount / (ms * 1e-3) / 1e9
+            peak = MI355X_HBM_GBPS
+        out[name] = {"ms": round(ms, 4), "achieved": round(rate, 1), "unit": unit, "frac": round(rate / peak, 4),
+                     "work_per_launch": amount}
+    return out
 
 
 def attn_traffic():
@@ -249,11 +314,25 @@ def cpu_baseline(wl):
     import numpy as np
     import oracle
     import synth
+    threads, vendor = None, "unknown"
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+        blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if blas:
+            threads = max(i.get("num_threads", 1) for i in blas)
+            vendor = ", ".join(sorted({f"{i.get('internal_api')} {i.get('version')}" for i in blas}))
     except Exception:  # pragma: no cover
-        threads = len(os.sched_getaffinity(0))
+        pass
+    cores = len(os.sched_getaffinity(0))
+    threads = threads or cores
+    cpu_model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:  # pragma: no cover
+        pass
     W = {k: v.f64 for k, v in synth.block_params(wl, 0).items()}
     kc, vc = synth.kv_cache(wl, 0)
     x = synth.normal(wl.seed, "x", (wl.B, wl.L, wl.d), 1.0, dtype="f32").f64
@@ -266,7 +345,8 @@ def cpu_baseline(wl):
     dt = time.perf_counter() - t0
     step_s = dt * wl.n_layers
     return {"value": 1.0 / step_s, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"one full-shape block ({dt:.1f} s fp64 numpy, {threads} BLAS threads), "
+            "affinity_cores": cores, "blas_threads": int(threads), "blas": vendor, "cpu_model": cpu_model,
+            "sample": f"one full-shape block ({dt:.1f} s fp64 numpy on {threads} BLAS threads), "
                       f"x{wl.n_layers} blocks; embeddings and head not timed"}
 
 
@@ -333,8 +413,121 @@ def probe_attn_fp8(wl, n):
                       "q": [B, L, H, Dh], "kv": [B, Lk, H, Dh]}), flush=True)
 
 
+def _calibration_copy(torch, g):
+    """One elementwise kernel that reads and writes 1 GiB: the known traffic that scales
+    the HBM byte counters."""
+    copy_bytes = 1 << 30
+    src = torch.randn(copy_bytes // 2, generator=g, device="cuda", dtype=torch.bfloat16)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.mul(src, 1, out=dst)
+    torch.cuda.synchronize()
+    return copy_bytes
+
+
+def probe_kernels(wl, kind, n):
+    """Counter-collection mode for the non-attention kernels: the calibration copy, then n
+    launches of each of the block's six projections with their epilogues (qkv, o, cq, co,
+    ffn1, ffn2, in that order) at the step's shapes, or n launches of the AdaLN LayerNorm,
+    or of the RoPE/KV-append kernel."""
+    import torch
+    import paper_2602_15922_amd as w
+    torch.cuda.set_device(0)
+    g = torch.Generator(device="cuda").manual_seed(7)
+    M, d, F = wl.B * wl.L, wl.d, wl.ffn
+
+    def rn(*shape, std=1.0):
+        return (torch.randn(*shape, generator=g, device="cuda") * std).to(torch.bfloat16)
+
+    copy_bytes = _calibration_copy(torch, g)
+    ran = []
+    if kind == "gemm":
+        x = torch.randn(M, d, generator=g, device="cuda")
+        gate = torch.randn(6, d, generator=g, device="cuda") * 0.02
+        roles = (("qkv", d, 3 * d, w.WAM_EPI_BF16), ("o", d, d, w.WAM_EPI_RESID_F32),
+                 ("cq", d, d, w.WAM_EPI_BF16), ("co", d, d, w.WAM_EPI_RESID_F32),
+                 ("ffn1", d, F, w.WAM_EPI_GELU_BF16), ("ffn2", F, d, w.WAM_EPI_RESID_F32))
+        for name, K, N, epi in roles:
+            A, Wt = rn(M, K), rn(N, K, std=0.02)
+            bias = torch.zeros(N, device="cuda")
+            out = x if epi == w.WAM_EPI_RESID_F32 else torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+            gated = name in ("o", "ffn2")
+            torch.cuda.synchronize()
+            for _ in range(n):
+                w.wam_gemm_bf16(A, Wt, out, epi, bias=bias, gate_a=gate[2] if gated else None,
+                                gate_v=gate[3] if gated else None, gate_rows=wl.L if gated else 0)
+            torch.cuda.synchronize()
+            ran.append({"role": name, "M": M, "N": N, "K": K, "epilogue": epi, "launches": n})
+            del A, Wt
+        assert torch.isfinite(x).all()
+    elif kind == "ln":
+        x = torch.randn(M, d, generator=g, device="cuda")
+        h = torch.empty(M, d, dtype=torch.bfloat16, device="cuda")
+        mod = torch.randn(4, d, generator=g, device="cuda") * 0.02
+        torch.cuda.synchronize()
+        for _ in range(n):
+            w.wam_adaln_ln_mod(x, h, wl.eps, wl.L, shift_a=mod[0], shift_v=mod[1], scale_a=mod[2], scale_v=mod[3])
+        torch.cuda.synchronize()
+        ran.append({"kernel": "ln_mod", "rows": M, "d": d, "launches": n})
+    else:
+        qkv = rn(wl.B, wl.L, 3 * d)
+        q = torch.empty(wl.B, wl.L, d, dtype=torch.bfloat16, device="cuda")
+        kc = torch.zeros(wl.B, wl.Lcap, wl.H, wl.Dh, dtype=torch.bfloat16, device="cuda")
+        vc = torch.zeros_like(kc)
+        pos = w.wam_chunk_positions(wl.n_cached, wl.F, wl.Hg, wl.Wg, wl.A)
+        cos, sin = (torch.from_numpy(a).to("cuda") for a in w.wam_rope_tables(pos, wl.Dh))
+        torch.cuda.synchronize()
+        for _ in range(n):
+            w.wam_rope_qkv(qkv, cos, sin, q, kc, vc, wl.cache_rows, wl.H, wl.Dh)
+        torch.cuda.synchronize()
+        ran.append({"kernel": "rope_qkv", "rows": M, "d": d, "launches": n})
+    print(json.dumps({"probe": kind, "workload": wl.name, "copy_bytes": copy_bytes, "ran": ran}), flush=True)
+
+
+def pmc_summary(path):
+    """Per-kernel averages of the counters in a rocprofv3 counter-collection CSV (one row
+    per dispatch and counter), in dispatch order of each kernel's first appearance.  The
+    CSV's GRBM_GUI_ACTIVE is the sum over the 8 XCDs, so where the inputs are present it
+    adds rocprofv3's MfmaUtil formula, sum(SQ_VALU_MFMA_BUSY_CYCLES) / (max over XCDs of
+    GRBM_GUI_ACTIVE x 1024 SIMDs), with the max taken as the sum / 8, and the shader clock
+    implied by GRBM_GUI_ACTIVE / 8 over the dispatch's duration."""
+    import csv
+    import glob
+    files = sorted(glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True))
+    if not files:
+        sys.exit(f"no counter_collection.csv under {path}")
+    disp = {}
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            key = (f, int(r["Dispatch_Id"]))
+            dd = disp.setdefault(key, {"kernel": r["Kernel_Name"], "ns": int(r["End_Timestamp"]) -
+                                       int(r["Start_Timestamp"]), "grid": r["Grid_Size"], "c": {}})
+            dd["c"][r["Counter_Name"]] = float(r["Counter_Value"])
+    kern = {}  # (kernel, grid size) -> dispatches: one row per launch shape
+    for key in sorted(disp):
+        dd = disp[key]
+        name = dd["kernel"].replace("(anonymous namespace)::", "").split("(")[0][:100]
+        kern.setdefault(f"{name}` grid {dd['grid']}", []).append(dd)
+    counters = sorted({c for dd in disp.values() for c in dd["c"]})
+    print("| kernel | dispatches | avg µs | " + " | ".join(counters) + " | MfmaUtil % | clock GHz |")
+    print("|---|---:|---:|" + "---:|" * (len(counters) + 2))
+    for name, ds in kern.items():
+        avg = {c: sum(d_["c"].get(c, 0.0) for d_ in ds) / len(ds) for c in counters}
+        us = sum(d_["ns"] for d_ in ds) / len(ds) / 1e3
+        util = clk = ""
+        gui = avg.get("GRBM_GUI_ACTIVE", 0.0) / 8.0
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in avg and gui:
+            util = f"{100.0 * avg['SQ_VALU_MFMA_BUSY_CYCLES'] / (gui * 1024):.1f}"
+        if gui and us > 0:
+            clk = f"{gui / (us * 1e3):.2f}"
+        print(f"| `{name} | {len(ds)} | {us:.1f} | " + " | ".join(f"{avg[c]:.6g}" for c in counters)
+              + f" | {util} | {clk} |")
+
+
 def main():
     args = parse()
+    if args.pmc_summary:
+        return pmc_summary(args.pmc_summary)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: this build runs on one GPU only (no sharding or collectives); "
@@ -349,6 +542,8 @@ def main():
         return probe_attn(wl, args.probe_attn)
     if args.probe_attn_fp8:
         return probe_attn_fp8(wl, args.probe_attn_fp8)
+    if args.probe:
+        return probe_kernels(wl, args.probe, args.probe_n)
     torch.cuda.set_device(0)
     model, keep, kcs, vcs, inp = build_model(wl, torch)
     B, d = wl.B, wl.d
@@ -410,6 +605,12 @@ def main():
         "step_mfma_frac": round(step_flop / (ms * 1e-3) / 1e12 / MI355X_BF16_DENSE_TFLOPS, 4),
         "wall_s_timed": round(wall, 3),
     }
+    if args.profile_steps > 0:
+        roles = profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, args.profile_steps)
+        rec["gemm_roofline"] = {k: roles[k] for k in ("qkv", "o", "cq", "co", "ffn1", "ffn2")}
+        rec["gemm_roofline"]["source"] = (f"events around every launch of every block over {args.profile_steps} "
+                                          "untimed steps after the timed ones; peak: bf16 dense MFMA")
+        rec["kernel_roles"] = {k: roles[k] for k in ("ln1", "rope", "self_attn", "lnc", "cross_attn", "ln2")}
     if not args.no_extras:
         rec["extras"] = extras(wl, model, keep, kcs, vcs, inp, torch)
     if not args.no_cpu_baseline:

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define WAM_ABI_VERSION 6
+#define WAM_ABI_VERSION 7
 #define WAM_MAX_CHUNKS 16
 
 typedef enum {
@@ -273,11 +273,33 @@ typedef struct {
  * attn_events  optional HOST array of 2*n_layers hipEvent_t: when non-NULL,
  *          events[2l] and events[2l+1] are recorded on `stream` just before and just
  *          after block l's self-attention kernel (for per-kernel timing).
+ * block_events optional HOST array of 2*WAM_BLOCK_EVENTS*n_layers hipEvent_t: when
+ *          non-NULL, events[(l*WAM_BLOCK_EVENTS + k)*2] and [.. + 1] are recorded just
+ *          before and just after launch k (wam_block_event) of block l.  A projection
+ *          with FP8 weights includes its activation quantization.  Recording ~24 events
+ *          per block adds launch gaps: meant for profiling steps, not timed ones.
  * t_action optional [B] fp32 device: the action tokens' own timestep (DreamZero-Flash,
  *          Appendix D.3).  When non-NULL (and A > 0) the action rows' AdaLN modulation,
  *          gates and head modulation come from t_action's time embedding and the video
  *          rows' from t's; NULL: every row uses t.
  * ------------------------------------------------------------------------------ */
+/* The launches of a block, in order, that wam_step_io.block_events brackets. */
+typedef enum {
+  WAM_EV_LN1 = 0,        /* AdaLN #1                                   */
+  WAM_EV_QKV = 1,        /* fused QKV projection                       */
+  WAM_EV_ROPE = 2,       /* 3D RoPE + KV-cache append                  */
+  WAM_EV_SELF_ATTN = 3,  /* block-causal self-attention                */
+  WAM_EV_O = 4,          /* output projection + gated residual         */
+  WAM_EV_LNC = 5,        /* cross-attention LayerNorm                  */
+  WAM_EV_CQ = 6,         /* cross-attention query projection           */
+  WAM_EV_CROSS_ATTN = 7, /* cross-attention over the text              */
+  WAM_EV_CO = 8,         /* cross-attention output projection + residual */
+  WAM_EV_LN2 = 9,        /* AdaLN #2                                   */
+  WAM_EV_FFN1 = 10,      /* FFN up-projection + tanh-GELU              */
+  WAM_EV_FFN2 = 11,      /* FFN down-projection + gated residual       */
+  WAM_BLOCK_EVENTS = 12
+} wam_block_event;
+
 typedef struct {
   const void* z_t;
   const void* a_t;
@@ -296,6 +318,7 @@ typedef struct {
   void* const* k_exp;     /* optional HOST array of n_layers FP8 K exponent caches (then   */
   const float* v_scale;   /* k_cache / v_cache hold E4M3 codes; v_scale HOST [n_layers]),  */
                           /* as in wam_block_io                                            */
+  hipEvent_t* block_events;
 } wam_step_io;
 
 size_t wam_step_workspace_bytes(const wam_model* m, const wam_step_io* io);

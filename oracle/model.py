@@ -57,7 +57,7 @@ def embed(z_t, a_t, w_patch, b_patch, w_ain, b_ain):
 
 
 def dit_block(x, e0, W, H, eps, pos, q_chunk, k_prev=None, v_prev=None, prev_chunk=None,
-              ctx=None, ctx_kv=None):
+              ctx=None, ctx_kv=None, rows=None):
     """One DiT block over the current chunk rows.
 
     x (B, L, d) residual; e0 (B, 6, d) time modulation, or (B, L, 6, d) for a
@@ -70,6 +70,12 @@ def dit_block(x, e0, W, H, eps, pos, q_chunk, k_prev=None, v_prev=None, prev_chu
 
     Returns (x_out, k_cur, v_cur): the new residual and the current rows' K (after
     RoPE) and V, i.e. what an update pass would append to the cache.
+
+    rows (optional index array): x_out holds only those rows of the new residual.  Every
+    row's K and V are still computed (each query sees them), but the queries and all
+    token-wise work after the self-attention keys are computed for the listed rows only;
+    the block has no other coupling between rows, so this is a row subset of the full
+    result.
     """
     B, L, d = x.shape
     Dh = d // H
@@ -80,19 +86,28 @@ def dit_block(x, e0, W, H, eps, pos, q_chunk, k_prev=None, v_prev=None, prev_chu
         m = W["mod6"][None] + e0
         sh1, sc1, g1, sh2, sc2, g2 = (m[:, i][:, None, :] for i in range(6))
 
-    # self-attention against cache + current chunk
-    qkv = linear(modulate(x, sh1, sc1, eps), W["w_qkv"], W["b_qkv"])
-    q = qkv[..., 0 * d:1 * d].reshape(B, L, H, Dh)
-    k = qkv[..., 1 * d:2 * d].reshape(B, L, H, Dh)
-    v = qkv[..., 2 * d:3 * d].reshape(B, L, H, Dh)
+    # self-attention against cache + current chunk; the fused projection's output
+    # columns are q | k | v
+    h = modulate(x, sh1, sc1, eps)
+    w_qkv, b_qkv = W["w_qkv"], W["b_qkv"]
+    kv = linear(h, w_qkv[d:], None if b_qkv is None else b_qkv[d:])
+    k = apply_rope(kv[..., :d].reshape(B, L, H, Dh), pos)
+    v = kv[..., d:].reshape(B, L, H, Dh)
+    cur_chunk = np.asarray(q_chunk)
+    if rows is not None:
+        rows = np.asarray(rows)
+        x, h, pos, q_chunk = x[:, rows], h[:, rows], np.asarray(pos)[rows], cur_chunk[rows]
+        L = len(rows)
+        if e0.ndim == 4:
+            sh1, sc1, g1, sh2, sc2, g2 = (a[:, rows] for a in (sh1, sc1, g1, sh2, sc2, g2))
+    q = linear(h, w_qkv[:d], None if b_qkv is None else b_qkv[:d]).reshape(B, L, H, Dh)
     q = apply_rope(q, pos)
-    k = apply_rope(k, pos)
     if k_prev is None:
-        k_all, v_all, k_chunk = k, v, np.asarray(q_chunk)
+        k_all, v_all, k_chunk = k, v, cur_chunk
     else:
         k_all = np.concatenate([k_prev, k], axis=1)
         v_all = np.concatenate([v_prev, v], axis=1)
-        k_chunk = np.concatenate([np.asarray(prev_chunk), np.asarray(q_chunk)])
+        k_chunk = np.concatenate([np.asarray(prev_chunk), cur_chunk])
     o = np.stack([attention(q[b], k_all[b], v_all[b], q_chunk, k_chunk) for b in range(B)])
     x = x + g1 * linear(o.reshape(B, L, d), W["w_o"], W["b_o"])
 
@@ -127,7 +142,7 @@ def head(x, e, head_mod2, Lv, w_hv, b_hv, w_ha, b_ha, eps, C, F, Hl, Wl):
 
 
 def dit_step(z_t, a_t, t, text, P, layers, n_layers, H, eps, chunk_index, pos,
-             prev_chunk=None, q_chunk=None, ctx=None, t_action=None):
+             prev_chunk=None, q_chunk=None, ctx=None, t_action=None, depths=None):
     """u_theta([z_t, a_t]; KV, c, t, update=False) for one chunk.
 
     z_t (B, C, F, Hl, Wl) noisy latents; a_t (B, A, act_dim) noisy actions; t (B,);
@@ -135,7 +150,8 @@ def dit_step(z_t, a_t, t, text, P, layers, n_layers, H, eps, chunk_index, pos,
     returns (W_l, k_prev_l, v_prev_l), so callers can stream one layer at a time.
     t_action (B,), when given, is the action tokens' own timestep (DreamZero-Flash,
     Appendix D.3): their AdaLN and head modulation come from it, the video tokens'
-    from t.  Returns (v_video, v_action)."""
+    from t.  Returns (v_video, v_action); with depths (a list of block counts), the
+    list of (v_video, v_action) the head gives after each of those many blocks."""
     B, C, F, Hl, Wl = z_t.shape
     e, e0 = time_embedding(t, P["w_t1"], P["b_t1"], P["w_t2"], P["b_t2"], P["w_t6"], P["b_t6"])
     if t_action is not None:
@@ -149,12 +165,18 @@ def dit_step(z_t, a_t, t, text, P, layers, n_layers, H, eps, chunk_index, pos,
     L = x.shape[1]
     if q_chunk is None:
         q_chunk = np.full(L, chunk_index)
+    Lv = F * (Hl // 2) * (Wl // 2)
+
+    def velocity(x):
+        return head(x, e, P["head_mod2"], Lv, P["w_hv"], P["b_hv"], P["w_ha"], P["b_ha"], eps, C, F, Hl, Wl)
+
+    taps = []
     for layer in range(n_layers):
         W, kp, vp = layers(layer)
         x, _, _ = dit_block(x, e0, W, H, eps, pos, q_chunk, kp, vp, prev_chunk, ctx=ctx)
-    Lv = F * (Hl // 2) * (Wl // 2)
-    return head(x, e, P["head_mod2"], Lv, P["w_hv"], P["b_hv"], P["w_ha"], P["b_ha"],
-                eps, C, F, Hl, Wl)
+        if depths is not None and layer + 1 in depths:
+            taps.append(velocity(x))
+    return velocity(x) if depths is None else taps
 
 
 def dit_update(z, a, t, text, P, layers, n_layers, H, eps, pos, q_chunk, prev_chunk=None, ctx=None):

@@ -18,6 +18,9 @@ WAM_MAX_CHUNKS = 16
 WAM_OK, WAM_EINVAL, WAM_EUNSUPPORTED, WAM_EWORKSPACE, WAM_EHIP = range(5)
 WAM_EPI_BF16, WAM_EPI_GELU_BF16, WAM_EPI_RESID_F32, WAM_EPI_F32 = range(4)
 WAM_SOLVER_EULER, WAM_SOLVER_UNIPC = range(2)
+# the launches of a block that wam_step_io.block_events brackets (wam_block_event)
+BLOCK_EVENT_NAMES = ("ln1", "qkv", "rope", "self_attn", "o", "lnc", "cq", "cross_attn", "co", "ln2", "ffn1", "ffn2")
+WAM_BLOCK_EVENTS = len(BLOCK_EVENT_NAMES)
 
 EXPORTED = (
     "wam_last_error", "wam_abi_version", "wam_attn_blockcausal", "wam_block_workspace_bytes",
@@ -97,7 +100,7 @@ class wam_step_io(C.Structure):
                 ("B", _i32), ("F", _i32), ("Hl", _i32), ("Wl", _i32), ("A", _i32), ("Lc", _i32),
                 ("Lcap", _i32), ("cache_len", _i32), ("ch", wam_chunks),
                 ("v_video", _vp), ("v_action", _vp), ("attn_events", C.POINTER(_vp)), ("t_action", _vp),
-                ("k_exp", C.POINTER(_vp)), ("v_scale", _fp)]
+                ("k_exp", C.POINTER(_vp)), ("v_scale", _fp), ("block_events", C.POINTER(_vp))]
 
 
 class wam_flow_dims(C.Structure):
@@ -468,9 +471,12 @@ def _ptr_array(ts):
 
 
 def make_step_io(z_t, a_t, t, text, k_caches, v_caches, rope_cos, rope_sin, cache_len, chunks, v_video,
-                 v_action, ctx_kv=None, events=None, t_action=None, k_exps=None, v_scales=None) -> wam_step_io:
+                 v_action, ctx_kv=None, events=None, t_action=None, k_exps=None, v_scales=None,
+                 block_events=None) -> wam_step_io:
     """Step inputs/outputs; with k_exps (per-layer [B, Lcap, H] int32) and v_scales (per-layer
-    floats) the caches are FP8 code caches and the self-attention runs in FP8."""
+    floats) the caches are FP8 code caches and the self-attention runs in FP8.  events: the
+    2*n_layers self-attention events; block_events: 2*WAM_BLOCK_EVENTS*n_layers torch events
+    around every launch of every block."""
     B, _, F, Hl, Wl = z_t.shape
     io = wam_step_io(z_t=_p(z_t), a_t=_p(a_t), t=_p(t), text=_p(text), rope_cos=_p(rope_cos),
                      rope_sin=_p(rope_sin), B=B, F=F, Hl=Hl, Wl=Wl, A=a_t.shape[1], Lc=text.shape[1],
@@ -498,6 +504,12 @@ def make_step_io(z_t, a_t, t, text, k_caches, v_caches, rope_cos, rope_sin, cach
         ev = (_vp * len(events))(*[e.cuda_event for e in events])
         io.attn_events = C.cast(ev, C.POINTER(_vp))
         keep.append(ev)
+    if block_events is not None:
+        for e in block_events:
+            e.record()
+        bev = (_vp * len(block_events))(*[e.cuda_event for e in block_events])
+        io.block_events = C.cast(bev, C.POINTER(_vp))
+        keep.append(bev)
     io._keep = keep
     return io
 

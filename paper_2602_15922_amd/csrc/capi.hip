@@ -1,7 +1,7 @@
 // C ABI of libwamdit: host-side validation, workspace planning and the launch
 // sequences of the DiT block and denoising step.  No memory is allocated and no
 // stream is synchronised here; every entry point validates all arguments before its
-// first launch.
+// first launch (the multi-launch sequences by a dry pass over the whole sequence).
 #include <algorithm>
 #include <cmath>
 #include <cstdarg>
@@ -57,6 +57,20 @@ wam_status fail(wam_status st, const char* fmt, ...) {
   do {                                 \
     wam_status s_ = (expr);            \
     if (s_ != WAM_OK) return s_;       \
+  } while (0)
+
+// A launch sequence (block, step, update pass, loop) first runs dry: every descriptor of
+// every launch is built and validated, nothing is launched or recorded.  Only if that
+// pass returns WAM_OK does the same sequence run for real, so an invalid argument found
+// deep in the sequence never leaves the caller's buffers partly updated.
+thread_local bool t_dry = false;
+struct DryScope {
+  DryScope() { t_dry = true; }
+  ~DryScope() { t_dry = false; }
+};
+#define LAUNCH(expr)          \
+  do {                        \
+    if (!t_dry) HIPCHECK(expr); \
   } while (0)
 
 bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -146,7 +160,7 @@ wam_status attn_checked(const wam_attn_desc& d, const void* q, const void* k, co
   a.n_k_chunks = d.ch.n_k_chunks;
   a.n_q_chunks = d.ch.n_q_chunks;
   for (int i = 0; i <= d.ch.n_q_chunks; ++i) a.q_off[i] = d.ch.q_off[i];
-  HIPCHECK(launch_attn(pred(a), s));
+  LAUNCH(launch_attn(pred(a), s));
   return WAM_OK;
 }
 
@@ -198,7 +212,7 @@ wam_status attn_fp8_checked(const wam_attn_desc& d, const void* q, const void* q
   f.qe_ts = d.q_tok_stride / 128; f.qe_bs = d.q_batch_stride / 128;
   f.ke_ts = d.kv_tok_stride / 128; f.ke_bs = d.kv_batch_stride / 128;
   f.v_scale = v_scale;
-  HIPCHECK(launch_attn_fp8(f, s));
+  LAUNCH(launch_attn_fp8(f, s));
   return WAM_OK;
 }
 
@@ -265,7 +279,7 @@ wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s, int32_t gate_spli
   GemmArgs a;
   TRY(gemm_prep(g, a, gate_split, gate_alt, a_scale, w_scale));
   if (a.M == 0) return WAM_OK;
-  HIPCHECK(launch_gemm(pred(a), s));
+  LAUNCH(launch_gemm(pred(a), s));
   return WAM_OK;
 }
 
@@ -307,7 +321,7 @@ wam_status proj(const wam_gemm_desc& g0, const void* w8, const float* s8, char* 
                 int32_t gate_split = 0, int64_t gate_alt = 0) {
   if (!w8) return gemm_checked(g0, s, gate_split, gate_alt);
   const int64_t ldq = (g0.K + 15) / 16 * 16;
-  HIPCHECK(launch_quant_rows(g0.M, g0.K, g0.A, g0.lda, q8, ldq, qs, s, t_skip));
+  LAUNCH(launch_quant_rows(g0.M, g0.K, g0.A, g0.lda, q8, ldq, qs, s, t_skip));
   wam_gemm_desc g = g0;
   g.A = q8; g.lda = ldq; g.a_rows = 0; g.a_batch_stride = 0;
   g.W = w8; g.ldw = g0.K;
@@ -364,8 +378,23 @@ wam_status check_block_io(const wam_dims& D, const wam_block_weights& w, const w
 // The launch sequence of one block; arguments already validated.
 // seg/alt: rows >= seg of a sample (0: none) take their per-sample modulation (e0) from
 // e0 + alt (the action tokens' own timestep).
+// ev: NULL, or 2*WAM_BLOCK_EVENTS events recorded around the block's launches (its
+// self-attention pair doubles as the step's attn_events pair).
+struct BlockEvents {
+  const hipEvent_t* ev = nullptr;  // [WAM_BLOCK_EVENTS][2]
+  hipEvent_t attn0 = nullptr, attn1 = nullptr;
+};
+wam_status mark(const BlockEvents& e, int kind, int end, hipStream_t s) {
+  if (kind == WAM_EV_SELF_ATTN) {
+    hipEvent_t a = end ? e.attn1 : e.attn0;
+    if (a) LAUNCH(hipEventRecord(a, s));
+  }
+  if (e.ev) LAUNCH(hipEventRecord(e.ev[2 * kind + end], s));
+  return WAM_OK;
+}
+
 wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_block_io& io, char* ws,
-                     hipStream_t s, hipEvent_t ev0, hipEvent_t ev1, int32_t seg = 0, int64_t alt = 0) {
+                     hipStream_t s, const BlockEvents& ev = BlockEvents{}, int32_t seg = 0, int64_t alt = 0) {
   const int d = D.d, B = io.B, L = io.L, M = B * L;
   const BlockWs lay = block_ws(D, B, L, io.Lc);
   void* h = ws + lay.h;
@@ -382,20 +411,26 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
 
   // 1. AdaLN: h = LN(x)(1 + scale1) + shift1
   LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h, seg, alt};
-  HIPCHECK(launch_ln_mod(pred(ln), s));
+  TRY(mark(ev, WAM_EV_LN1, 0, s));
+  LAUNCH(launch_ln_mod(pred(ln), s));
+  TRY(mark(ev, WAM_EV_LN1, 1, s));
   // 2. fused QKV projection
+  TRY(mark(ev, WAM_EV_QKV, 0, s));
   TRY(proj(gemm(M, 3 * d, d, WAM_EPI_BF16, h, d, W.w_qkv, W.b_qkv, big, 3 * d), F8 ? F8->w_qkv : nullptr,
            F8 ? F8->s_qkv : nullptr, q8, qs, s));
+  TRY(mark(ev, WAM_EV_QKV, 1, s));
   // 3. RoPE on q, k; k, v appended to the cache rows of this chunk (with an FP8 cache:
   // q and k encoded in 32-dim blocks, q into the q buffer with its exponents behind it)
   void* qe = static_cast<char*>(q) + (size_t)M * d;
   RopeArgs ra{B, L, D.H, D.Dh, io.Lcap, io.cache_len, big, io.rope_cos, io.rope_sin, q, io.k_cache, io.v_cache};
+  TRY(mark(ev, WAM_EV_ROPE, 0, s));
   if (io.k_exp) {
     RopeFp8Args rf{pred(ra), qe, io.k_exp, 1.0f / io.v_scale};
-    HIPCHECK(launch_rope_qkv_fp8(rf, s));
+    LAUNCH(launch_rope_qkv_fp8(rf, s));
   } else {
-    HIPCHECK(launch_rope_qkv(pred(ra), s));
+    LAUNCH(launch_rope_qkv(pred(ra), s));
   }
+  TRY(mark(ev, WAM_EV_ROPE, 1, s));
   // 4. block-causal self-attention over cache rows [0, cache_len + L)
   wam_attn_desc ad{};
   ad.B = B; ad.H = D.H; ad.Dh = D.Dh; ad.Lq = L; ad.Lk = io.cache_len + L;
@@ -403,22 +438,28 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   ad.kv_tok_stride = d; ad.kv_batch_stride = (int64_t)io.Lcap * d;
   ad.o_tok_stride = d; ad.o_batch_stride = (int64_t)L * d;
   ad.ch = io.ch;
-  if (ev0) HIPCHECK(hipEventRecord(ev0, s));
+  TRY(mark(ev, WAM_EV_SELF_ATTN, 0, s));
   if (io.k_exp) TRY(attn_fp8_checked(ad, q, qe, io.k_cache, io.k_exp, io.v_cache, io.v_scale, o, s));
   else TRY(attn_checked(ad, q, io.k_cache, io.v_cache, o, s));
-  if (ev1) HIPCHECK(hipEventRecord(ev1, s));
+  TRY(mark(ev, WAM_EV_SELF_ATTN, 1, s));
   // 5. x += gate1 * (o W_o^T + b_o)
   {
     wam_gemm_desc g = gemm(M, d, d, WAM_EPI_RESID_F32, o, d, W.w_o, W.b_o, io.x, d);
     g.gate_a = m6 + 2 * d; g.gate_v = e0 + 2 * d; g.gate_stride = ms; g.gate_rows = L;
+    TRY(mark(ev, WAM_EV_O, 0, s));
     TRY(proj(g, F8 ? F8->w_o : nullptr, F8 ? F8->s_o : nullptr, q8, qs, s, seg, alt));
+    TRY(mark(ev, WAM_EV_O, 1, s));
   }
   // 6. cross-attention LayerNorm (affine, no modulation)
   LnArgs lc{M, L, d, D.eps, io.x, W.lnc_gamma, W.lnc_beta, nullptr, nullptr, nullptr, nullptr, 0, h};
-  HIPCHECK(launch_ln_mod(pred(lc), s));
+  TRY(mark(ev, WAM_EV_LNC, 0, s));
+  LAUNCH(launch_ln_mod(pred(lc), s));
+  TRY(mark(ev, WAM_EV_LNC, 1, s));
   // 7. cross query
+  TRY(mark(ev, WAM_EV_CQ, 0, s));
   TRY(proj(gemm(M, d, d, WAM_EPI_BF16, h, d, W.w_cq, W.b_cq, q, d), F8 ? F8->w_cq : nullptr,
            F8 ? F8->s_cq : nullptr, q8, qs, s));
+  TRY(mark(ev, WAM_EV_CQ, 1, s));
   // 8. cross K|V of the text (unless precomputed for this block)
   const void* kv = io.ctx_kv;
   if (!kv) {
@@ -433,21 +474,31 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   cd.kv_tok_stride = 2 * d; cd.kv_batch_stride = (int64_t)io.Lc * 2 * d;
   cd.o_tok_stride = d; cd.o_batch_stride = (int64_t)L * d;
   cd.ch = single_chunk(L, io.Lc);
+  TRY(mark(ev, WAM_EV_CROSS_ATTN, 0, s));
   TRY(attn_checked(cd, q, kv, static_cast<const char*>(kv) + (size_t)d * 2, o, s));
+  TRY(mark(ev, WAM_EV_CROSS_ATTN, 1, s));
   // 10. x += o W_co^T + b_co (no gate)
+  TRY(mark(ev, WAM_EV_CO, 0, s));
   TRY(proj(gemm(M, d, d, WAM_EPI_RESID_F32, o, d, W.w_co, W.b_co, io.x, d), F8 ? F8->w_co : nullptr,
            F8 ? F8->s_co : nullptr, q8, qs, s));
+  TRY(mark(ev, WAM_EV_CO, 1, s));
   // 11. AdaLN #2
   LnArgs l2{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 3 * d, e0 + 3 * d, m6 + 4 * d, e0 + 4 * d, ms, h, seg, alt};
-  HIPCHECK(launch_ln_mod(pred(l2), s));
+  TRY(mark(ev, WAM_EV_LN2, 0, s));
+  LAUNCH(launch_ln_mod(pred(l2), s));
+  TRY(mark(ev, WAM_EV_LN2, 1, s));
   // 12. FFN up-projection with tanh-GELU
+  TRY(mark(ev, WAM_EV_FFN1, 0, s));
   TRY(proj(gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, big, D.ffn), F8 ? F8->w_f1 : nullptr,
            F8 ? F8->s_f1 : nullptr, q8, qs, s));
+  TRY(mark(ev, WAM_EV_FFN1, 1, s));
   // 13. x += gate2 * (u W_f2^T + b_f2)
   {
     wam_gemm_desc g = gemm(M, d, D.ffn, WAM_EPI_RESID_F32, big, D.ffn, W.w_f2, W.b_f2, io.x, d);
     g.gate_a = m6 + 5 * d; g.gate_v = e0 + 5 * d; g.gate_stride = ms; g.gate_rows = L;
+    TRY(mark(ev, WAM_EV_FFN2, 0, s));
     TRY(proj(g, F8 ? F8->w_f2 : nullptr, F8 ? F8->s_f2 : nullptr, q8, qs, s, seg, alt));
+    TRY(mark(ev, WAM_EV_FFN2, 1, s));
   }
   return WAM_OK;
 }
@@ -464,7 +515,7 @@ wam_status block_kv_run(const wam_dims& D, const wam_block_weights& W, const wam
   const float* e0 = io.e0;
   const int64_t ms = 6 * (int64_t)d;
   LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h, seg, alt};
-  HIPCHECK(launch_ln_mod(pred(ln), s));
+  LAUNCH(launch_ln_mod(pred(ln), s));
   // rows d..3d of W_qkv (the k and v outputs) into columns d..3d of the [M][3d] buffer
   const wam_block_fp8* F8 = W.fp8;
   const char* wkv = F8 ? nullptr : static_cast<const char*>(W.w_qkv) + (size_t)d * d * 2;
@@ -476,9 +527,9 @@ wam_status block_kv_run(const wam_dims& D, const wam_block_weights& W, const wam
               io.v_cache};
   if (io.k_exp) {
     RopeFp8Args rf{pred(ra), nullptr, io.k_exp, 1.0f / io.v_scale};
-    HIPCHECK(launch_rope_qkv_fp8(rf, s));
+    LAUNCH(launch_rope_qkv_fp8(rf, s));
   } else {
-    HIPCHECK(launch_rope_qkv(pred(ra), s));
+    LAUNCH(launch_rope_qkv(pred(ra), s));
   }
   return WAM_OK;
 }
@@ -505,10 +556,10 @@ wam_status time_run(const wam_model& m, int32_t B, const float* t, float* e, flo
   const wam_dims& D = m.dims;
   float* sinus = reinterpret_cast<float*>(ws);
   float* hid = sinus + (size_t)B * D.freq_dim;
-  HIPCHECK(launch_sinusoid(B, D.freq_dim, t, sinus, s, t_skip));
-  HIPCHECK(launch_gemv(B, D.d, D.freq_dim, sinus, GEMV_ACT_NONE, m.w_t1, m.b_t1, hid, s, t_skip));
-  HIPCHECK(launch_gemv(B, D.d, D.d, hid, GEMV_ACT_SILU, m.w_t2, m.b_t2, e, s, t_skip));
-  HIPCHECK(launch_gemv(B, 6 * D.d, D.d, e, GEMV_ACT_SILU, m.w_t6, m.b_t6, e0, s, t_skip));
+  LAUNCH(launch_sinusoid(B, D.freq_dim, t, sinus, s, t_skip));
+  LAUNCH(launch_gemv(B, D.d, D.freq_dim, sinus, GEMV_ACT_NONE, m.w_t1, m.b_t1, hid, s, t_skip));
+  LAUNCH(launch_gemv(B, D.d, D.d, hid, GEMV_ACT_SILU, m.w_t2, m.b_t2, e, s, t_skip));
+  LAUNCH(launch_gemv(B, 6 * D.d, D.d, e, GEMV_ACT_SILU, m.w_t6, m.b_t6, e0, s, t_skip));
   return WAM_OK;
 }
 
@@ -530,7 +581,7 @@ wam_status embed_run(const wam_model& m, int32_t B, int32_t F, int32_t Hl, int32
                      const void* a, float* x, char* ws, hipStream_t s) {
   const wam_dims& D = m.dims;
   const int P = D.latent_ch * 4, Lv = F * (Hl / 2) * (Wl / 2), L = Lv + A;
-  HIPCHECK(launch_patchify(B, D.latent_ch, F, Hl, Wl, z, ws, s, t_skip));
+  LAUNCH(launch_patchify(B, D.latent_ch, F, Hl, Wl, z, ws, s, t_skip));
   wam_gemm_desc g = gemm(B * Lv, D.d, P, WAM_EPI_F32, ws, P, m.w_patch, m.b_patch, x, D.d);
   g.out_rows = Lv; g.out_batch_stride = (int64_t)L * D.d;
   TRY(gemm_checked(g, s));
@@ -565,11 +616,11 @@ wam_status head_run(const wam_model& m, int32_t B, int32_t F, int32_t Hl, int32_
   float* tok = reinterpret_cast<float*>(ws + lay.tok);
   LnArgs ln{B * L, L, d, D.eps, x, nullptr, nullptr, m.head_mod2, e, m.head_mod2 + d, e, d, h,
             e_alt ? Lv : 0, e_alt};
-  HIPCHECK(launch_ln_mod(pred(ln), s));
+  LAUNCH(launch_ln_mod(pred(ln), s));
   wam_gemm_desc gv = gemm(B * Lv, P, d, WAM_EPI_F32, h, d, m.w_hv, m.b_hv, tok, P);
   gv.a_rows = Lv; gv.a_batch_stride = (int64_t)L * d;
   TRY(gemm_checked(gv, s));
-  HIPCHECK(launch_unpatchify(B, D.latent_ch, F, Hl, Wl, tok, v_video, s, t_skip));
+  LAUNCH(launch_unpatchify(B, D.latent_ch, F, Hl, Wl, tok, v_video, s, t_skip));
   if (A > 0) {
     wam_gemm_desc ga = gemm(B * A, D.act_dim, d, WAM_EPI_F32, h + (size_t)Lv * d * 2, d, m.w_ha, m.b_ha,
                             v_action, D.act_dim);
@@ -604,7 +655,7 @@ wam_status cross_kv_run(const wam_model& m, int32_t B, int32_t Lc, const void* c
     }
   }
   if (M == 0 || n == 0) return WAM_OK;
-  if (any_fp8) HIPCHECK(launch_quant_rows(M, K, ctx, K, q8, ldq, qs, s, t_skip));
+  if (any_fp8) LAUNCH(launch_quant_rows(M, K, ctx, K, q8, ldq, qs, s, t_skip));
   for (int fp8 = 0; fp8 < 2; ++fp8) {
     GemmGroup gg{};
     GemmArgs first{};
@@ -617,11 +668,11 @@ wam_status cross_kv_run(const wam_model& m, int32_t B, int32_t Lc, const void* c
       gg.out[gg.n] = a.out;
       gg.w_scale[gg.n] = a.w_scale;
       if (++gg.n == WAM_GEMM_GROUP_MAX) {
-        HIPCHECK(launch_gemm_group(pred(first), gg, s));
+        LAUNCH(launch_gemm_group(pred(first), gg, s));
         gg.n = 0;
       }
     }
-    if (gg.n > 0) HIPCHECK(launch_gemm_group(pred(first), gg, s));
+    if (gg.n > 0) LAUNCH(launch_gemm_group(pred(first), gg, s));
   }
   return WAM_OK;
 }
@@ -712,6 +763,16 @@ wam_status check_step(const wam_model& m, const wam_step_io& io, bool head) {
   return WAM_OK;
 }
 
+BlockEvents block_events(const wam_step_io& io, int l) {
+  BlockEvents e;
+  if (io.attn_events) {
+    e.attn0 = io.attn_events[2 * l];
+    e.attn1 = io.attn_events[2 * l + 1];
+  }
+  if (io.block_events) e.ev = io.block_events + (size_t)l * 2 * WAM_BLOCK_EVENTS;
+  return e;
+}
+
 // The launch sequence of one step; arguments already validated.
 wam_status step_run(const wam_model& m, const wam_step_io& io, char* w, hipStream_t stream) {
   const StepWs lay = step_ws(m, io);
@@ -742,9 +803,7 @@ wam_status step_run(const wam_model& m, const wam_step_io& io, char* w, hipStrea
     b.ch = io.ch; b.ctx = ctx; b.ctx_kv = io.ctx_kv ? io.ctx_kv[l] : w + lay.kv + (size_t)l * lay.kv_layer;
     b.B = io.B; b.L = L; b.Lc = io.Lc;
     b.k_exp = io.k_exp ? io.k_exp[l] : nullptr; b.v_scale = io.v_scale ? io.v_scale[l] : 1.0f;
-    hipEvent_t ev0 = io.attn_events ? io.attn_events[2 * l] : nullptr;
-    hipEvent_t ev1 = io.attn_events ? io.attn_events[2 * l + 1] : nullptr;
-    TRY(block_run(D, m.blocks[l], b, w + lay.block, stream, ev0, ev1, flash ? Lv : 0, alt_e0));
+    TRY(block_run(D, m.blocks[l], b, w + lay.block, stream, block_events(io, l), flash ? Lv : 0, alt_e0));
   }
   TRY(head_run(m, io.B, io.F, io.Hl, io.Wl, io.A, x, e, io.v_video, io.v_action, piece, stream, alt_e));
   return WAM_OK;
@@ -927,6 +986,47 @@ DenoiseWs denoise_ws(const wam_model& m, const wam_step_io& io, const wam_denois
   return w;
 }
 
+// The update pass's launch sequence; arguments already validated.
+wam_status update_run(const wam_model* m, const wam_step_io* io, void* ws, hipStream_t stream) {
+  const StepWs lay = step_ws(*m, *io);
+  const wam_dims& D = m->dims;
+  char* w = static_cast<char*>(ws);
+  float* x = reinterpret_cast<float*>(w + lay.x);
+  float* e = reinterpret_cast<float*>(w + lay.e);
+  float* e0 = reinterpret_cast<float*>(w + lay.e0);
+  void* ctx = w + lay.ctx;
+  char* piece = w + lay.piece;
+  const int32_t Lv = io->F * (io->Hl / 2) * (io->Wl / 2), L = Lv + io->A;
+
+  TRY(time_run(*m, io->B, io->t, e, e0, piece, stream));
+  const bool flash = io->t_action != nullptr && io->A > 0;
+  const int64_t alt_e0 = flash ? (int64_t)io->B * 6 * D.d : 0;
+  if (flash) TRY(time_run(*m, io->B, io->t_action, e + (int64_t)io->B * D.d, e0 + alt_e0, piece, stream));
+  // the last block only projects its K/V, so the cross K|V of the others
+  if (!io->ctx_kv && D.n_layers > 1) {
+    TRY(text_run(*m, io->B, io->Lc, io->text, ctx, piece, stream));
+    const BlockWs bl = block_ws(D, io->B, L, io->Lc);
+    TRY(cross_kv_run(*m, io->B, io->Lc, ctx, w + lay.kv, lay.kv_layer, D.n_layers - 1, w + lay.block + bl.q8,
+                     reinterpret_cast<float*>(w + lay.block + bl.qs), stream));
+  }
+  TRY(embed_run(*m, io->B, io->F, io->Hl, io->Wl, io->A, io->z_t, io->a_t, x, piece, stream));
+  for (int l = 0; l < D.n_layers; ++l) {
+    wam_block_io b{};
+    b.x = x; b.e0 = e0; b.rope_cos = io->rope_cos; b.rope_sin = io->rope_sin;
+    b.k_cache = io->k_cache[l]; b.v_cache = io->v_cache[l]; b.Lcap = io->Lcap; b.cache_len = io->cache_len;
+    b.ch = io->ch; b.ctx = ctx;
+    b.ctx_kv = io->ctx_kv ? io->ctx_kv[l] : w + lay.kv + (size_t)l * lay.kv_layer;
+    b.B = io->B; b.L = L; b.Lc = io->Lc;
+    b.k_exp = io->k_exp ? io->k_exp[l] : nullptr; b.v_scale = io->v_scale ? io->v_scale[l] : 1.0f;
+    if (l + 1 == D.n_layers) {
+      TRY(block_kv_run(D, m->blocks[l], b, w + lay.block, stream, flash ? Lv : 0, alt_e0));
+    } else {
+      TRY(block_run(D, m->blocks[l], b, w + lay.block, stream, block_events(*io, l), flash ? Lv : 0, alt_e0));
+    }
+  }
+  return WAM_OK;
+}
+
 }  // namespace
 
 // =================================================================================
@@ -1061,7 +1161,11 @@ wam_status wam_dit_block_fwd(const wam_dims* dims, const wam_block_weights* w, c
   TRY(check_block_weights(*w));
   TRY(check_block_io(*dims, *w, *io));
   TRY(check_ws(ws, ws_bytes, block_ws(*dims, io->B, io->L, io->Lc).total));
-  return block_run(*dims, *w, *io, static_cast<char*>(ws), stream, nullptr, nullptr);
+  {
+    DryScope dry;
+    TRY(block_run(*dims, *w, *io, static_cast<char*>(ws), stream));
+  }
+  return block_run(*dims, *w, *io, static_cast<char*>(ws), stream);
 }
 
 size_t wam_time_embed_workspace_bytes(const wam_dims* dims, int32_t B) {
@@ -1143,6 +1247,10 @@ wam_status wam_dit_step_fwd(const wam_model* m, const wam_step_io* io, void* ws,
   CHECK(m && io, WAM_EINVAL, "NULL model/io");
   TRY(check_step(*m, *io, true));
   TRY(check_ws(ws, ws_bytes, step_ws(*m, *io).total));
+  {
+    DryScope dry;
+    TRY(step_run(*m, *io, static_cast<char*>(ws), stream));
+  }
   return step_run(*m, *io, static_cast<char*>(ws), stream);
 }
 
@@ -1154,46 +1262,12 @@ wam_status wam_dit_update_fwd(const wam_model* m, const wam_step_io* io, void* w
                               hipStream_t stream) {
   CHECK(m && io, WAM_EINVAL, "NULL model/io");
   TRY(check_step(*m, *io, false));
-  const StepWs lay = step_ws(*m, *io);
-  TRY(check_ws(ws, ws_bytes, lay.total));
-  const wam_dims& D = m->dims;
-  char* w = static_cast<char*>(ws);
-  float* x = reinterpret_cast<float*>(w + lay.x);
-  float* e = reinterpret_cast<float*>(w + lay.e);
-  float* e0 = reinterpret_cast<float*>(w + lay.e0);
-  void* ctx = w + lay.ctx;
-  char* piece = w + lay.piece;
-  const int32_t Lv = io->F * (io->Hl / 2) * (io->Wl / 2), L = Lv + io->A;
-
-  TRY(time_run(*m, io->B, io->t, e, e0, piece, stream));
-  const bool flash = io->t_action != nullptr && io->A > 0;
-  const int64_t alt_e0 = flash ? (int64_t)io->B * 6 * D.d : 0;
-  if (flash) TRY(time_run(*m, io->B, io->t_action, e + (int64_t)io->B * D.d, e0 + alt_e0, piece, stream));
-  // the last block only projects its K/V, so the cross K|V of the others
-  if (!io->ctx_kv && D.n_layers > 1) {
-    TRY(text_run(*m, io->B, io->Lc, io->text, ctx, piece, stream));
-    const BlockWs bl = block_ws(D, io->B, L, io->Lc);
-    TRY(cross_kv_run(*m, io->B, io->Lc, ctx, w + lay.kv, lay.kv_layer, D.n_layers - 1, w + lay.block + bl.q8,
-                     reinterpret_cast<float*>(w + lay.block + bl.qs), stream));
+  TRY(check_ws(ws, ws_bytes, step_ws(*m, *io).total));
+  {
+    DryScope dry;
+    TRY(update_run(m, io, ws, stream));
   }
-  TRY(embed_run(*m, io->B, io->F, io->Hl, io->Wl, io->A, io->z_t, io->a_t, x, piece, stream));
-  for (int l = 0; l < D.n_layers; ++l) {
-    wam_block_io b{};
-    b.x = x; b.e0 = e0; b.rope_cos = io->rope_cos; b.rope_sin = io->rope_sin;
-    b.k_cache = io->k_cache[l]; b.v_cache = io->v_cache[l]; b.Lcap = io->Lcap; b.cache_len = io->cache_len;
-    b.ch = io->ch; b.ctx = ctx;
-    b.ctx_kv = io->ctx_kv ? io->ctx_kv[l] : w + lay.kv + (size_t)l * lay.kv_layer;
-    b.B = io->B; b.L = L; b.Lc = io->Lc;
-    b.k_exp = io->k_exp ? io->k_exp[l] : nullptr; b.v_scale = io->v_scale ? io->v_scale[l] : 1.0f;
-    if (l + 1 == D.n_layers) {
-      TRY(block_kv_run(D, m->blocks[l], b, w + lay.block, stream, flash ? Lv : 0, alt_e0));
-    } else {
-      hipEvent_t ev0 = io->attn_events ? io->attn_events[2 * l] : nullptr;
-      hipEvent_t ev1 = io->attn_events ? io->attn_events[2 * l + 1] : nullptr;
-      TRY(block_run(D, m->blocks[l], b, w + lay.block, stream, ev0, ev1, flash ? Lv : 0, alt_e0));
-    }
-  }
-  return WAM_OK;
+  return update_run(m, io, ws, stream);
 }
 
 wam_status wam_flow_step(const wam_flow_dims* d, const float* v_video, const float* v_action, const float* v_in,
@@ -1295,6 +1369,11 @@ wam_status wam_denoise_chunk(const wam_model* m, const wam_step_io* io, const wa
   for (int q = 0; q < 4; ++q) ring[q] = reinterpret_cast<float*>(w + lay.ring + q * align256((size_t)n * 4));
   std::vector<UnipcArgs> uargs(plan.size());
   for (size_t i = 0; i < plan.size(); ++i) TRY(unipc_args(fd, p->x, xl, ring, (int32_t)i, plan[i], uargs[i]));
+
+  {  // every launch of a step validated before the first launch of the loop
+    DryScope dry;
+    TRY(step_run(*m, *io, w + lay.step, stream));
+  }
 
   // The text and so every block's cross-attention K|V are the same at every step of
   // the chunk: unless the caller supplied them, project them once here, into the step

@@ -11,6 +11,9 @@ regenerate one layer at a time without holding a whole 40-layer model in host RA
 """
 from __future__ import annotations
 
+import concurrent.futures
+import os
+
 import numpy as np
 
 from .workloads import WORKLOADS, Workload  # noqa: F401
@@ -98,17 +101,19 @@ def normal(cfg_seed: int, tensor: str, shape, std: float = 1.0, layer: int = 0,
     return Tensor("f32", a)
 
 
-def device_normal(cfg_seed: int, tensor: str, shape, std: float = 1.0, layer: int = 0):
-    """N(0, std^2) bf16 drawn on the GPU from a seeded stream (torch's generator seeded
-    from SeedSequence([cfg_seed, tensor_id, layer])), for inputs too large to draw on
-    the host in a test's time (a 65744-key cache is 337M values per sample).  Both sides
-    read the same device tensor: the oracle gets its host copy."""
+def device_normal(cfg_seed: int, tensor: str, shape, std: float = 1.0, layer: int = 0, dtype: str = "bf16"):
+    """N(0, std^2) drawn on the GPU from a seeded stream (torch's generator seeded
+    from SeedSequence([cfg_seed, tensor_id, layer])), stored as bf16 (RNE) or fp32, for
+    inputs too large to draw on the host in a test's time (a 65744-key cache is 337M
+    values per sample).  Both sides read the same device tensor: the oracle gets its
+    host copy."""
     import torch
     seed = int(np.random.SeedSequence([int(cfg_seed), TENSOR_IDS[tensor], int(layer)]).generate_state(1,
                                                                                                    np.uint64)[0])
     g = torch.Generator(device="cuda")
     g.manual_seed(seed & 0x7FFFFFFFFFFFFFFF)
-    return (torch.randn(shape, generator=g, device="cuda", dtype=torch.float32) * std).to(torch.bfloat16)
+    a = torch.randn(shape, generator=g, device="cuda", dtype=torch.float32) * std
+    return a.to(torch.bfloat16) if dtype == "bf16" else a
 
 
 def zeros(shape, dtype: str = "f32") -> Tensor:
@@ -127,22 +132,33 @@ def uniform(cfg_seed: int, tensor: str, shape, layer: int = 0) -> Tensor:
 # zero unless ``bias_std`` is given (tests use non-zero biases to exercise epilogues).
 # ---------------------------------------------------------------------------------
 
+def _draw_all(jobs: dict) -> dict:
+    """Draw several seeded tensors at once: name -> (normal's positional args, dtype).
+    Every tensor has its own stream, so drawing them on threads (numpy releases the GIL
+    while it fills and rounds large arrays) gives the same values as one by one."""
+    workers = max(1, min(len(jobs), 8, len(os.sched_getaffinity(0))))
+    with concurrent.futures.ThreadPoolExecutor(workers) as ex:
+        futs = {k: ex.submit(normal, *args, dtype=dt) for k, (args, dt) in jobs.items()}
+        return {k: f.result() for k, f in futs.items()}
+
+
 def block_params(wl: "Workload", layer: int, bias_std: float = 0.0,
                  mod_std: float = WEIGHT_STD, seed: int | None = None) -> dict:
     s = wl.seed if seed is None else seed
     d, F = wl.d, wl.ffn
-    p = {
-        "w_qkv": normal(s, "w_qkv", (3 * d, d), WEIGHT_STD, layer),
-        "w_o": normal(s, "w_o", (d, d), WEIGHT_STD, layer),
-        "w_cq": normal(s, "w_cq", (d, d), WEIGHT_STD, layer),
-        "w_ckv": normal(s, "w_ckv", (2 * d, d), WEIGHT_STD, layer),
-        "w_co": normal(s, "w_co", (d, d), WEIGHT_STD, layer),
-        "w_f1": normal(s, "w_f1", (F, d), WEIGHT_STD, layer),
-        "w_f2": normal(s, "w_f2", (d, F), WEIGHT_STD, layer),
-        "mod6": normal(s, "mod6", (6, d), mod_std, layer, dtype="f32"),
-        "lnc_gamma": Tensor("f32", np.ones(d, np.float32)),
-        "lnc_beta": zeros((d,)),
+    jobs = {
+        "w_qkv": ((s, "w_qkv", (3 * d, d), WEIGHT_STD, layer), "bf16"),
+        "w_o": ((s, "w_o", (d, d), WEIGHT_STD, layer), "bf16"),
+        "w_cq": ((s, "w_cq", (d, d), WEIGHT_STD, layer), "bf16"),
+        "w_ckv": ((s, "w_ckv", (2 * d, d), WEIGHT_STD, layer), "bf16"),
+        "w_co": ((s, "w_co", (d, d), WEIGHT_STD, layer), "bf16"),
+        "w_f1": ((s, "w_f1", (F, d), WEIGHT_STD, layer), "bf16"),
+        "w_f2": ((s, "w_f2", (d, F), WEIGHT_STD, layer), "bf16"),
+        "mod6": ((s, "mod6", (6, d), mod_std, layer), "f32"),
     }
+    p = _draw_all(jobs)
+    p["lnc_gamma"] = Tensor("f32", np.ones(d, np.float32))
+    p["lnc_beta"] = zeros((d,))
     for b, n in (("b_qkv", 3 * d), ("b_o", d), ("b_cq", d), ("b_ckv", 2 * d),
                  ("b_co", d), ("b_f1", F), ("b_f2", d)):
         p[b] = normal(s, b, (n,), bias_std, layer, dtype="f32") if bias_std else zeros((n,))
@@ -152,18 +168,18 @@ def block_params(wl: "Workload", layer: int, bias_std: float = 0.0,
 def model_params(wl: "Workload", bias_std: float = 0.0, seed: int | None = None) -> dict:
     s = wl.seed if seed is None else seed
     d = wl.d
-    p = {
-        "w_t1": normal(s, "w_t1", (d, wl.freq_dim), WEIGHT_STD),
-        "w_t2": normal(s, "w_t2", (d, d), WEIGHT_STD),
-        "w_t6": normal(s, "w_t6", (6 * d, d), WEIGHT_STD),
-        "w_x1": normal(s, "w_x1", (d, wl.text_dim), WEIGHT_STD),
-        "w_x2": normal(s, "w_x2", (d, d), WEIGHT_STD),
-        "w_patch": normal(s, "w_patch", (d, wl.patch_dim), WEIGHT_STD),
-        "w_ain": normal(s, "w_ain", (d, wl.act_dim), WEIGHT_STD),
-        "w_hv": normal(s, "w_hv", (wl.patch_dim, d), WEIGHT_STD),
-        "w_ha": normal(s, "w_ha", (wl.act_dim, d), WEIGHT_STD),
-        "head_mod2": normal(s, "head_mod2", (2, d), WEIGHT_STD, dtype="f32"),
-    }
+    p = _draw_all({
+        "w_t1": ((s, "w_t1", (d, wl.freq_dim), WEIGHT_STD), "bf16"),
+        "w_t2": ((s, "w_t2", (d, d), WEIGHT_STD), "bf16"),
+        "w_t6": ((s, "w_t6", (6 * d, d), WEIGHT_STD), "bf16"),
+        "w_x1": ((s, "w_x1", (d, wl.text_dim), WEIGHT_STD), "bf16"),
+        "w_x2": ((s, "w_x2", (d, d), WEIGHT_STD), "bf16"),
+        "w_patch": ((s, "w_patch", (d, wl.patch_dim), WEIGHT_STD), "bf16"),
+        "w_ain": ((s, "w_ain", (d, wl.act_dim), WEIGHT_STD), "bf16"),
+        "w_hv": ((s, "w_hv", (wl.patch_dim, d), WEIGHT_STD), "bf16"),
+        "w_ha": ((s, "w_ha", (wl.act_dim, d), WEIGHT_STD), "bf16"),
+        "head_mod2": ((s, "head_mod2", (2, d), WEIGHT_STD), "f32"),
+    })
     for b, n in (("b_t1", d), ("b_t2", d), ("b_t6", 6 * d), ("b_x1", d), ("b_x2", d),
                  ("b_patch", d), ("b_ain", d), ("b_hv", wl.patch_dim), ("b_ha", wl.act_dim)):
         p[b] = normal(s, b, (n,), bias_std, dtype="f32") if bias_std else zeros((n,))
@@ -176,4 +192,5 @@ def kv_cache(wl: "Workload", layer: int, B: int | None = None, seed: int | None 
     s = wl.seed if seed is None else seed
     B = wl.B if B is None else B
     shape = (B, wl.cache_rows, wl.H, wl.Dh)
-    return normal(s, "k_cache", shape, 1.0, layer), normal(s, "v_cache", shape, 1.0, layer)
+    kv = _draw_all({"k": ((s, "k_cache", shape, 1.0, layer), "bf16"), "v": ((s, "v_cache", shape, 1.0, layer), "bf16")})
+    return kv["k"], kv["v"]

@@ -122,8 +122,11 @@ class StepCase:
     """A denoising step of `wl` with n_layers seeded blocks (streamed one at a time on the
     oracle side)."""
 
-    def __init__(self, wl, n_layers, bias_std=0.0, flash=False):
+    def __init__(self, wl, n_layers, bias_std=0.0, flash=False, keep_layers=False):
+        """keep_layers: draw each layer once and keep it for both sides (instead of
+        drawing it again for the oracle), at the cost of holding every layer in RAM."""
         self.wl, self.n_layers, self.bias_std = wl, n_layers, bias_std
+        self.kept = {} if keep_layers else None
         B, s = wl.B, wl.seed
         self.P = synth.model_params(wl, bias_std=bias_std)
         self.z = synth.normal(s, "z_t", (B, wl.latent_ch, wl.F, wl.Hl, wl.Wl), 1.0)
@@ -134,11 +137,17 @@ class StepCase:
         self.text = synth.normal(s, "text", (B, wl.Lc, wl.text_dim), 1.0)
 
     def layer(self, l):
+        if self.kept is not None and l in self.kept:
+            return self.kept[l]
         W = synth.block_params(self.wl, l, self.bias_std, mod_std=self.wl.mod_std)
         kc, vc = synth.kv_cache(self.wl, l) if self.wl.n_cached else (None, None)
+        if self.kept is not None:
+            self.kept[l] = (W, kc, vc)
         return W, kc, vc
 
-    def run_oracle(self):
+    def run_oracle(self, depths=None):
+        """fp64 velocities; depths: a list of block counts -> the list of velocities after
+        each (one pass over the layers)."""
         wl = self.wl
 
         def layers(l):
@@ -148,7 +157,8 @@ class StepCase:
         return oracle.dit_step(self.z.f64, self.a.f64, self.t.f64, self.text.f64, f64(self.P), layers,
                                self.n_layers, wl.H, wl.eps, wl.n_cached, oracle_positions(wl),
                                prev_chunk=prev_chunk_ids(wl) if wl.n_cached else None,
-                               t_action=self.t_action.f64 if self.t_action is not None else None)
+                               t_action=self.t_action.f64 if self.t_action is not None else None,
+                               depths=depths)
 
     def upload(self, fp8=False):
         """Device model and inputs (kept on self so the step can be re-run); fp8: the
@@ -176,23 +186,26 @@ class StepCase:
         a step reads and writes (taken after a step with the bf16 cache, a calibration pass)."""
         self.k8s, self.kes, self.v8s, self.vsc = fp8_caches(self.kcs, self.vcs, self.wl.cache_rows + self.wl.L)
 
-    def run_gpu(self, events=None, t_action=None, fp8_cache=False):
+    def run_gpu(self, events=None, t_action=None, fp8_cache=False, depth=None):
         """t_action: a device [B] timestep overriding the case's own (None: the case's);
-        fp8_cache: run on the E4M3 caches of make_fp8_cache (FP8 self-attention)."""
+        fp8_cache: run on the E4M3 caches of make_fp8_cache (FP8 self-attention);
+        depth: run only the first `depth` blocks (default: all)."""
         import torch
         w = lib()
         wl, B = self.wl, self.wl.B
         if not hasattr(self, "model"):
             self.upload()
+        n = self.n_layers if depth is None else depth
+        model = self.model if n == self.n_layers else w.make_model(dims_of(wl, n), self.top, self.blocks[:n])
         vv = torch.empty((B, wl.latent_ch, wl.F, wl.Hl, wl.Wl), dtype=torch.float32, device="cuda")
         va = torch.empty((B, wl.A, wl.act_dim), dtype=torch.float32, device="cuda")
         kcs, vcs = (self.k8s, self.v8s) if fp8_cache else (self.kcs, self.vcs)
-        io = w.make_step_io(self.dz, self.da, self.dt, self.dtext, kcs, vcs, self.cos, self.sin,
+        io = w.make_step_io(self.dz, self.da, self.dt, self.dtext, kcs[:n], vcs[:n], self.cos, self.sin,
                             wl.cache_rows, w.cached_chunks(wl.cache_rows, wl.L), vv, va, events=events,
                             t_action=t_action if t_action is not None else self.dta,
-                            k_exps=self.kes if fp8_cache else None, v_scales=self.vsc if fp8_cache else None)
-        ws = workspace(w.wam_step_workspace_bytes(self.model, io))
-        w.wam_dit_step_fwd(self.model, io, ws)
+                            k_exps=self.kes[:n] if fp8_cache else None, v_scales=self.vsc[:n] if fp8_cache else None)
+        ws = workspace(w.wam_step_workspace_bytes(model, io))
+        w.wam_dit_step_fwd(model, io, ws)
         torch.cuda.synchronize()
         return vv, va
 

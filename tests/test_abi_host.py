@@ -32,7 +32,7 @@ def test_library_exports_every_declared_function():
     for name in declared:
         assert hasattr(L, name), name
     assert sorted(w.binding.EXPORTED) == declared
-    assert w.wam_abi_version() == 6
+    assert w.wam_abi_version() == 7
 
 
 def test_struct_sizes_match_the_header_layout():
@@ -46,7 +46,7 @@ def test_struct_sizes_match_the_header_layout():
     assert C.sizeof(b.wam_flow_dims) == 32
     assert C.sizeof(b.wam_denoise_params) == 56
     assert C.sizeof(b.wam_unipc_coef) == 44
-    assert C.sizeof(b.wam_step_io) == 360
+    assert C.sizeof(b.wam_step_io) == 368
     assert C.sizeof(b.wam_block_io) == 312
     assert C.sizeof(b.wam_model) == 200
 
@@ -252,3 +252,55 @@ def test_step_workspace_holds_every_blocks_cross_kv_without_ctx_kv():
         with_kv = w.lib().wam_step_workspace_bytes(C.byref(m), C.byref(io))
         per_layer = (B * Lc * 2 * d * 2 + 255) // 256 * 256
         assert without - with_kv == n_layers * per_layer, (d, without, with_kv)
+
+
+def test_block_validates_its_whole_launch_sequence_before_the_first_launch():
+    """Checks that belong to launches deep inside a block (the attention's 2 GiB key span,
+    an FP8 projection's K % 16) fail before the first launch: with fake device addresses
+    on a host without a GPU, a launch would return WAM_EHIP, so the status shows that
+    nothing was launched (and so nothing of x or the cache was touched)."""
+    w = lib()
+    b = w.binding
+    L = w.lib()
+    fake = iter(range(1 << 20, 1 << 30, 1 << 16))
+
+    def weights(fp8=False):
+        wts = b.wam_block_weights()
+        for n in ("w_qkv", "w_o", "w_cq", "w_ckv", "w_co", "w_f1", "w_f2", "mod6"):
+            setattr(wts, n, next(fake))
+        if fp8:
+            f = b.wam_block_fp8()
+            for n in ("w_qkv", "w_o", "w_cq", "w_ckv", "w_co", "w_f1", "w_f2"):
+                setattr(f, n, next(fake))
+                setattr(f, "s" + n[1:], next(fake))
+            wts.fp8 = C.pointer(f)
+            wts._f = f
+        return wts
+
+    def io(cache_len, Lq):
+        return b.wam_block_io(x=next(fake), e0=next(fake), rope_cos=next(fake), rope_sin=next(fake),
+                              k_cache=next(fake), v_cache=next(fake), Lcap=cache_len + Lq, cache_len=cache_len,
+                              ch=w.cached_chunks(cache_len, Lq), ctx=next(fake), B=1, L=Lq, Lc=512)
+
+    ws = 1 << 32
+    dims = w.make_dims(d=5120, H=40, Dh=128, ffn=13824, n_layers=1)
+    # 209000 cached keys of 5120 bf16: one sample's keys span more than 2 GiB
+    big = io(209000, 1000)
+    st = L.wam_dit_block_fwd(C.byref(dims), C.byref(weights()), C.byref(big), ws, 1 << 40, None)
+    assert st == b.WAM_EUNSUPPORTED and b"keys span" in L.wam_last_error()
+    # FP8 projections need K % 16 == 0; FFN2's K is ffn = 13832 (a multiple of 8 only)
+    odd = w.make_dims(d=5120, H=40, Dh=128, ffn=13832, n_layers=1)
+    st = L.wam_dit_block_fwd(C.byref(odd), C.byref(weights(fp8=True)), C.byref(io(0, 64)), ws, 1 << 40, None)
+    assert st == b.WAM_EINVAL and b"K%16==0" in L.wam_last_error()
+    # the same block with bf16 projections passes validation and reaches the first launch,
+    # which fails here for want of a GPU
+    st = L.wam_dit_block_fwd(C.byref(odd), C.byref(weights()), C.byref(io(0, 64)), ws, 1 << 40, None)
+    assert st == b.WAM_EHIP
+
+
+def test_block_event_kinds_match_the_header():
+    w = lib()
+    src = open(os.path.join(ROOT, "include", "wamdit.h")).read()
+    kinds = {int(v): n.lower() for n, v in re.findall(r"\bWAM_EV_([A-Z0-9_]+)\s*=\s*(\d+)", src)}
+    assert [kinds[i] for i in range(len(kinds))] == list(w.binding.BLOCK_EVENT_NAMES)
+    assert int(re.search(r"WAM_BLOCK_EVENTS\s*=\s*(\d+)", src).group(1)) == w.binding.WAM_BLOCK_EVENTS

@@ -6,7 +6,7 @@ import pytest
 
 import oracle
 import synth
-from dit_cases import BlockCase, dims_of, f64, gpu_rope_tables, upload_cache
+from dit_cases import BlockCase, dims_of, f64, gpu_rope_tables, oracle_positions, prev_chunk_ids, upload_cache
 from gpu_helpers import dev, host, log, rel_l2, workspace
 
 pytestmark = pytest.mark.gpu
@@ -173,3 +173,70 @@ def test_block_precomputed_cross_kv_matches():
                         ws=workspace(w.wam_block_workspace_bytes(dims, wl.B, wl.L, wl.Lc)))
     torch.cuda.synchronize()
     assert torch.equal(x, x1)
+
+
+@pytest.mark.timeout(900)
+def test_block_b2_3view_sampled_rows():
+    """One 14B-class block at the two-sample, three-view shape: batch 2 of 9392 rows
+    (2 frames x 30 x 156 patches + 32 actions) after six cached chunks (56352 rows, 65744
+    keys), e0 from the time MLP of two different t and ctx from the text projection, all
+    on the GPU.  The oracle takes every row's K and V (they are appended, and every query
+    sees them) and the rest of the block on sampled rows of both samples.  The residual,
+    the cache and the cached rows are drawn on the device from seeded streams (the host
+    generator would take minutes at this size); the oracle reads host copies."""
+    import torch
+    w = lib()
+    wl = synth.WORKLOADS["step_14b_b2_3view"]
+    B, L, d, H, Dh = wl.B, wl.L, wl.d, wl.H, wl.Dh
+    log(f"block b2 3-view B={B} L={L} Lk={wl.Lk}: inputs")
+    P = synth.model_params(wl)
+    t = synth.uniform(wl.seed, "t", (B,))
+    assert abs(float(t.f64[0] - t.f64[1])) > 1e-3
+    text = synth.normal(wl.seed, "text", (B, wl.Lc, wl.text_dim), 1.0)
+    W = synth.block_params(wl, 0)
+    top = {k: dev(v) for k, v in P.items()}
+    m = w.make_model(dims_of(wl, 0), top, [])
+    e = torch.empty((B, d), dtype=torch.float32, device="cuda")
+    e0 = torch.empty((B, 6, d), dtype=torch.float32, device="cuda")
+    ctx = torch.empty((B, wl.Lc, d), dtype=torch.bfloat16, device="cuda")
+    w.wam_time_embed_fwd(m, dev(t), e, e0, workspace(w.wam_time_embed_workspace_bytes(m.dims, B)))
+    w.wam_text_proj_fwd(m, dev(text), ctx, workspace(w.wam_text_proj_workspace_bytes(m.dims, B, wl.Lc)))
+    x = synth.device_normal(wl.seed, "x", (B, L, d), 1.0, dtype="f32")
+    kc = torch.zeros((B, wl.Lcap, H, Dh), dtype=torch.bfloat16, device="cuda")
+    vc = torch.zeros_like(kc)
+    kc[:, :wl.cache_rows] = synth.device_normal(wl.seed, "k_cache", (B, wl.cache_rows, H, Dh))
+    vc[:, :wl.cache_rows] = synth.device_normal(wl.seed, "v_cache", (B, wl.cache_rows, H, Dh))
+    x_in = host(x)
+    Wd = {k: dev(v) for k, v in W.items()}
+    cos, sin = gpu_rope_tables(wl)
+    dims = dims_of(wl, 1)
+    log("block b2 3-view: GPU")
+    w.wam_dit_block_fwd(dims, w.make_block_weights(Wd), x, e0, cos, sin, kc, vc, wl.cache_rows,
+                        w.cached_chunks(wl.cache_rows, L), ctx=ctx,
+                        ws=workspace(w.wam_block_workspace_bytes(dims, B, L, wl.Lc)))
+    torch.cuda.synchronize()
+    del Wd
+    rng = np.random.default_rng(7)
+    rows = sorted({0, 1, 127, 128, 4679, 4680, 9215, 9216, wl.Lv - 1, wl.Lv, L - 1}
+                  | set(rng.integers(0, L, 53).tolist()))
+    rows = np.array(rows)
+    xg = host(x[:, rows])
+    app = slice(wl.cache_rows, wl.cache_rows + L)
+    kg, vg = host(kc[:, app]), host(vc[:, app])
+    log("block b2 3-view: oracle")
+    f = f64(P)
+    _, re0 = oracle.time_embedding(t.f64, f["w_t1"], f["b_t1"], f["w_t2"], f["b_t2"], f["w_t6"], f["b_t6"])
+    rctx = oracle.text_projection(text.f64, f["w_x1"], f["b_x1"], f["w_x2"], f["b_x2"])
+    kp, vp = host(kc[:, :wl.cache_rows]), host(vc[:, :wl.cache_rows])
+    del kc, vc
+    rx, rk, rv = oracle.dit_block(x_in, re0, f64(W), H, wl.eps, oracle_positions(wl), np.full(L, wl.n_cached),
+                                  kp, vp, prev_chunk_ids(wl), ctx=rctx, rows=rows)
+    x0 = x_in[:, rows]
+    err, derr = rel_l2(xg, rx), rel_l2(xg - x0, rx - x0)
+    ek, ev = rel_l2(kg, rk), rel_l2(vg, rv)
+    print(f"  {len(rows)} rows per sample: block rel L2 {err:.2e}, of the update {derr:.2e}; "
+          f"appended K {ek:.2e} V {ev:.2e}", flush=True)
+    for b in range(B):
+        print(f"  sample {b}: update rel L2 {rel_l2(xg[b] - x0[b], rx[b] - x0[b]):.2e}", flush=True)
+    assert err <= TOL and derr <= TOL
+    assert ek <= 5e-3 and ev <= 5e-3

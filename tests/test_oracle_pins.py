@@ -401,6 +401,28 @@ def test_block_precomputed_cross_kv():
     assert np.array_equal(a, b)
 
 
+def test_block_row_subset_equals_rows_of_the_full_block():
+    """The row-sampled block (queries and token-wise work for listed rows only, every
+    row's K and V) equals those rows of the full block: with a cache, batch 2, a
+    per-sample and a per-token modulation, rows in any order."""
+    d, H, Fh, B = 16, 2, 32, 2
+    W = small_block_weights(d, Fh, 550)
+    Fg, Hg, Wg, A = 2, 2, 2, 2
+    L = Fg * Hg * Wg + A
+    pos = chunk_positions(1, Fg, Hg, Wg, A)
+    ch = np.full(L, 1)
+    kp, vp = rnd(B, 5, H, d // H, seed=551), rnd(B, 5, H, d // H, seed=552)
+    pc = np.zeros(5, int)
+    x, ctx = rnd(B, L, d, seed=553), rnd(B, 3, d, seed=554)
+    rows = np.array([7, 0, 9, 3])
+    for e0 in (rnd(B, 6, d, seed=555) * 0.5, rnd(B, L, 6, d, seed=556) * 0.5):
+        full, kf, vf = oracle.dit_block(x, e0, W, H, 1e-6, pos, ch, kp, vp, pc, ctx=ctx)
+        sub, ks, vs = oracle.dit_block(x, e0, W, H, 1e-6, pos, ch, kp, vp, pc, ctx=ctx, rows=rows)
+        assert sub.shape == (B, len(rows), d)
+        assert np.max(np.abs(sub - full[:, rows])) <= 1e-12
+        assert np.array_equal(ks, kf) and np.array_equal(vs, vf)
+
+
 # ----------------------------------------------------------------------------- every branch live, by hand
 def _ln_by_hand(v, eps):
     n = len(v)
@@ -646,6 +668,22 @@ def test_step_identity_blocks_reduce_to_embed_and_head():
                             assert abs(vv[b, c, f, 2 * r + ph, 2 * s_ + pw] - out[c * 4 + ph * 2 + pw]) < 1e-10
             else:
                 assert np.allclose(va[b, tok - Lv], P["w_ha"] @ ht + P["b_ha"], atol=1e-10)
+
+
+
+def test_step_depth_taps_equal_shallower_steps():
+    """dit_step(depths=[1, 3]) gives the velocities of the 1-block and the 3-block steps."""
+    g = np.random.default_rng(560)
+    B, C, F, Hl, Wl, A, ad, d, H, tdim, Lc = 1, 4, 2, 4, 4, 2, 5, 16, 2, 6, 3
+    P = small_model_params(g, d, C, ad, tdim)
+    Ws = [small_block_weights(d, 24, 561 + l) for l in range(3)]
+    z, a = g.standard_normal((B, C, F, Hl, Wl)), g.standard_normal((B, A, ad))
+    t, text = np.array([0.3]), g.standard_normal((B, Lc, tdim))
+    pos = chunk_positions(0, F, Hl // 2, Wl // 2, A)
+    taps = oracle.dit_step(z, a, t, text, P, lambda l: (Ws[l], None, None), 3, H, 1e-6, 0, pos, depths=[1, 3])
+    for (tv, ta), n in zip(taps, (1, 3)):
+        rv, ra = oracle.dit_step(z, a, t, text, P, lambda l: (Ws[l], None, None), n, H, 1e-6, 0, pos)
+        assert np.array_equal(tv, rv) and np.array_equal(ta, ra)
 
 
 # ----------------------------------------------------------------------------- update pass

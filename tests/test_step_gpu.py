@@ -46,6 +46,53 @@ def test_step_14b_shapes_one_block():
     check_step(case, vv, va)
 
 
+@pytest.mark.timeout(900)
+def test_step_14b_shapes_four_blocks():
+    """The 40-block step's shapes (3152 rows, 4 cached chunks, 15760 keys, 512x4096 text)
+    with 4 seeded blocks of random weights: the velocities after 1, 2 and 4 blocks
+    against the oracle (each layer drawn once and shared by both sides)."""
+    wl = synth.WORKLOADS["step_14b"].replace(n_layers=4)
+    depths = [1, 2, 4]
+    log("step 14b 4 blocks: inputs")
+    case = StepCase(wl, 4, keep_layers=True)
+    case.upload()
+    got = []
+    for n in depths:
+        log(f"step 14b 4 blocks: GPU at depth {n}")
+        got.append([host(a) for a in case.run_gpu(depth=n)])
+    log("step 14b 4 blocks: oracle")
+    refs = case.run_oracle(depths=depths)
+    errs = []
+    for n, (gv, ga), (rv, ra) in zip(depths, got, refs):
+        ev, ea = rel_l2(gv, rv), rel_l2(ga, ra)
+        errs.append((ev, ea))
+        print(f"  depth {n}: rel L2 video {ev:.2e} action {ea:.2e}", flush=True)
+    assert all(ev <= TOL and ea <= TOL for ev, ea in errs)
+
+
+def test_step_d512_forty_blocks_error_growth():
+    """A 40-block d=512 step (batch 1, two cached chunks, block modulation tables of
+    std 0.02 as at 14B): how the velocities' error against the oracle grows with depth
+    up to the model's 40 blocks."""
+    wl = synth.WORKLOADS["block_d512"].replace(n_cached=2, n_layers=40, mod_std=0.02)
+    depths = [1, 2, 5, 10, 20, 40]
+    log("step d512 40 blocks: inputs")
+    case = StepCase(wl, 40, bias_std=0.05, keep_layers=True)
+    case.upload()
+    got = []
+    for n in depths:
+        log(f"step d512 40 blocks: GPU at depth {n}")
+        got.append([host(a) for a in case.run_gpu(depth=n)])
+    log("step d512 40 blocks: oracle")
+    refs = case.run_oracle(depths=depths)
+    errs = []
+    for n, (gv, ga), (rv, ra) in zip(depths, got, refs):
+        ev, ea = rel_l2(gv, rv), rel_l2(ga, ra)
+        errs.append((ev, ea))
+        print(f"  depth {n}: rel L2 video {ev:.2e} action {ea:.2e}", flush=True)
+    assert all(ev <= TOL and ea <= TOL for ev, ea in errs)
+
+
 def identity_model(wl, n_layers, identity=True):
     """Seeded model-level weights with the gate rows of the time projection zeroed, and
     device-random blocks whose gates and cross-attention output projection are zero: every
