@@ -423,6 +423,21 @@ size_t wam_cosine_workspace_bytes(void);
 wam_status wam_cosine_similarity(const float* a, const float* b, int64_t n, void* ws,
                                  size_t ws_bytes, float* out, hipStream_t stream);
 
+/* wam_cosine_similarity without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops, harnesses that forbid
+ * hipMalloc): the same kernels and the same result, bit for bit, with the partial sums
+ * in a static device array of the library (12 KiB per GPU, the fixed 512 x 3 fp64
+ * partials of the reduction whatever n is; each GPU the library runs on holds its copy
+ * until the process ends).  Nothing in it needs clearing: every call writes all
+ * partials before reading them.  The call allocates nothing and uses the current
+ * device's copy (its address looked up on the first call on that device), so `stream`
+ * must belong to the current device.  Every call on one GPU shares that copy: calls that
+ * overlap in time on one GPU (on different streams, or from different threads without
+ * ordering) race and may return wrong values; calls ordered on one stream do not.
+ * WAM_EWORKSPACE if the library's partials outgrow the array (a build mismatch). */
+wam_status wam_cosine_similarity_noalloc(const float* a, const float* b, int64_t n,
+                                         float* out, hipStream_t stream);
+
 typedef struct {
   int32_t n_steps;        /* N >= 1 solver steps */
   const float* t_sched;   /* HOST [N + 1] scheduler times t_0 .. t_N */

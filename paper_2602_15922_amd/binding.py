@@ -33,6 +33,7 @@ EXPORTED = (
     "wam_embed_workspace_bytes", "wam_embed_fwd", "wam_head_workspace_bytes", "wam_head_fwd",
     "wam_chunk_positions", "wam_rope_tables", "wam_attn_blockcausal_fp8", "wam_quantize_mx_fp8",
     "wam_quantize_scaled_fp8", "wam_rope_qkv_fp8", "wam_unipc_plan", "wam_unipc_step",
+    "wam_cosine_similarity_noalloc",
 )
 
 _vp, _fp, _i32, _i64, _sz = C.c_void_p, C.POINTER(C.c_float), C.c_int32, C.c_int64, C.c_size_t
@@ -159,6 +160,7 @@ def lib():
                                     _vp, _vp]
         L.wam_cosine_workspace_bytes.argtypes = []
         L.wam_cosine_similarity.argtypes = [_vp, _vp, _i64, _vp, _sz, _vp, _vp]
+        L.wam_cosine_similarity_noalloc.argtypes = [_vp, _vp, _i64, _vp, _vp]
         L.wam_denoise_workspace_bytes.argtypes = [C.POINTER(wam_model), C.POINTER(wam_step_io),
                                                   C.POINTER(wam_denoise_params)]
         L.wam_denoise_chunk.argtypes = [C.POINTER(wam_model), C.POINTER(wam_step_io), C.POINTER(wam_denoise_params),
@@ -545,6 +547,11 @@ def wam_cosine_workspace_bytes() -> int:
 def wam_cosine_similarity(a, b, out, ws, stream=None):
     """out[0] = cos(a, b) over all elements (device fp32 tensors)."""
     _check(lib().wam_cosine_similarity(_p(a), _p(b), a.numel(), _p(ws), ws.numel(), _p(out), _stream(stream)))
+
+
+def wam_cosine_similarity_noalloc(a, b, out, stream=None):
+    """out[0] = cos(a, b), partial sums in the library's static scratch (no workspace)."""
+    _check(lib().wam_cosine_similarity_noalloc(_p(a), _p(b), a.numel(), _p(out), _stream(stream)))
 
 
 def wam_unipc_plan(t_sched, order=2):

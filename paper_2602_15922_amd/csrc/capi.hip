@@ -1328,6 +1328,20 @@ wam_status wam_cosine_similarity(const float* a, const float* b, int64_t n, void
   return WAM_OK;
 }
 
+wam_status wam_cosine_similarity_noalloc(const float* a, const float* b, int64_t n, float* out,
+                                         hipStream_t stream) {
+  CHECK(n >= 0, WAM_EINVAL, "n < 0");
+  TRY(need_ptr(out, "out"));
+  if (n > 0) { TRY(need_ptr(a, "a")); TRY(need_ptr(b, "b")); }
+  CHECK(cosine_workspace_bytes() <= cosine_static_scratch_bytes(), WAM_EWORKSPACE,
+        "the partial sums need %zu bytes, the static scratch holds %zu", cosine_workspace_bytes(),
+        cosine_static_scratch_bytes());
+  void* part = nullptr;
+  HIPCHECK(cosine_static_scratch(&part));
+  HIPCHECK(launch_cosine(a, b, n, part, out, stream));
+  return WAM_OK;
+}
+
 size_t wam_denoise_workspace_bytes(const wam_model* m, const wam_step_io* io, const wam_denoise_params* p) {
   if (!m || !io || !p || io->B < 0 || io->F < 0 || io->Hl < 0 || io->Wl < 0 || io->A < 0 || io->Lc < 0) return 0;
   return denoise_ws(*m, *io, *p).total;

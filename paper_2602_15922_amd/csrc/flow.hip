@@ -1,6 +1,8 @@
 // The denoising loop's own kernels for gfx950: the flow-matching solver steps (Euler and
 // UniPC) with classifier-free guidance, the cosine similarity behind DiT caching, and the
 // timestep fill.  All HBM-bound elementwise work over one chunk's latents and actions.
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -186,6 +188,36 @@ hipError_t launch_unipc_step(const UnipcArgs& a, hipStream_t s) {
 }
 
 size_t cosine_workspace_bytes() { return (size_t)COS_BLOCKS * 3 * sizeof(double); }
+
+// The allocation-free cosine similarity keeps its partial sums in this file-scope device
+// array: one copy per GPU, at its own address, held until the process ends.  Host code
+// never passes the array's name to a kernel (on the host it is only a stand-in); it
+// passes the device address hipGetSymbolAddress returns, looked up once per device.
+static __device__ __align__(256) double scratch[COS_BLOCKS * 3];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+}  // namespace
+
+size_t cosine_static_scratch_bytes() { return sizeof(scratch); }
+
+hipError_t cosine_static_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_cosine(const float* x, const float* y, int64_t n, void* ws, float* out, hipStream_t s,
                          const int32_t* skip) {

@@ -167,6 +167,10 @@ struct UnipcArgs {
 hipError_t launch_unipc_step(const UnipcArgs& a, hipStream_t s);
 // cosine similarity of x and y (n floats) into out[0]; ws of cosine_workspace_bytes()
 size_t cosine_workspace_bytes();
+// the current device's copy of the allocation-free cosine's static scratch
+// (cosine_static_scratch_bytes() bytes), its address looked up on first use
+size_t cosine_static_scratch_bytes();
+hipError_t cosine_static_scratch(void** ptr);
 hipError_t launch_cosine(const float* x, const float* y, int64_t n, void* ws, float* out, hipStream_t s,
                          const int32_t* skip = nullptr);
 // p[0..n) = v for n <= 64
