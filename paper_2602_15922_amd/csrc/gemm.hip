@@ -8,16 +8,20 @@
 // with buffer loads straight into LDS (a scalar resource, a loop-invariant 32-bit lane
 // offset and a scalar slice offset: no vector ALU work per load) into a ring of STAGES
 // LDS buffers; the steady-state loop handles STAGES slices per iteration so each
-// stage's LDS offsets are immediates.  The loads of slice t+STAGES-1 are issued while
-// slice t is consumed, so each load has STAGES-1 slices of MFMA work to land (no
-// staging registers, one barrier per slice, waits on the vector-memory counter only
-// for the slice about to be used).  Within a slice the fragment reads of the next 16-wide
-// k-step are issued before the current step's MFMAs.  LDS rows are BK bf16 with
+// stage's LDS offsets are immediates.  One barrier per slice, placed before the
+// slice's last k-step: after it, that k-step's MFMAs run while the slice STAGES ahead
+// is fetched into the stage just freed and the next slice's first fragments are read,
+// so no wave starts a slice waiting on LDS (no staging registers; waits on the
+// vector-memory counter only for the slice about to be used).  Within a slice the
+// fragment reads of the next 16-wide k-step are issued between the current step's
+// MFMAs.  LDS rows are BK bf16 with
 // 16-byte chunks XOR-swizzled by row so the fragment reads (32 consecutive rows, same
 // chunk) are bank-conflict free; since lane l of a direct load lands at LDS unit
 // base+l, the swizzle is applied by choosing each lane's source chunk.  Tail
 // rows/columns are clamped on load and skipped on store; a K tail is zeroed in LDS
 // after it lands.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -172,34 +176,149 @@ WAM_DEV void zero_tail(char* smem, int buf, const GemmLane<C>& L, int kt, int K,
     if (kt * C::BK + L.klb[c] >= K) *reinterpret_cast<u32x4*>(Bs + ((L.w * C::NIB + c) * 64 + lane) * 16) = u32x4{};
 }
 
-// The MFMAs of one landed slice in ring stage `cur`.  Fragments are double-buffered in
-// registers: the reads of k-step ks+1 are in flight while the MFMAs of k-step ks run.
-// With `cur` a compile-time constant every LDS read is a lane offset plus an immediate.
+// Fragments: bf16 operands are one 16-byte read per 32x32x16 MFMA operand; FP8
+// operands are two (32 consecutive k of the lane's row for the 32x32x64 MFMA).
 template <typename C>
-WAM_DEV void mma_slice(const char* smem, int cur, const GemmLane<C>& L, f32x16 (*acc)[C::TN]) {
-  const char* As = smem + cur * C::STAGE;
+using Frag = typename std::conditional<C::EB == 2, bf16x8, i32x8>::type;
+
+// The lane's fragments of k-step ks from ring stage `stage` (a compile-time constant in
+// the steady state, so every LDS address is a lane offset plus an immediate).
+template <typename C>
+WAM_DEV void read_frags(const char* smem, int stage, const GemmLane<C>& L, int ks, Frag<C> (&fa)[C::TM],
+                        Frag<C> (&fb)[C::TN]) {
+  const char* As = smem + stage * C::STAGE;
   const char* Bs = As + C::BM * C::ROWB;
   constexpr int RB = 32 * C::ROWB;  // bytes of 32 LDS rows
   if constexpr (C::EB == 2) {
-    bf16x8 fa[2][C::TM], fb[2][C::TN];
-    auto read_frags = [&](int ks, int slot) {
 #pragma unroll
-      for (int a = 0; a < C::TM; ++a) fa[slot][a] = *reinterpret_cast<const bf16x8*>(As + L.fa_off[ks][0] + a * RB);
+    for (int a = 0; a < C::TM; ++a) fa[a] = *reinterpret_cast<const bf16x8*>(As + L.fa_off[ks][0] + a * RB);
 #pragma unroll
-      for (int b = 0; b < C::TN; ++b) fb[slot][b] = *reinterpret_cast<const bf16x8*>(Bs + L.fb_off[ks][0] + b * RB);
-    };
-    read_frags(0, 0);
-#pragma unroll
-    for (int ks = 0; ks < C::KS; ++ks) {
-      if (ks + 1 < C::KS) read_frags(ks + 1, (ks + 1) & 1);
-#pragma unroll
-      for (int a = 0; a < C::TM; ++a)
-#pragma unroll
-        for (int b = 0; b < C::TN; ++b) acc[a][b] = mfma32(fa[ks & 1][a], fb[ks & 1][b], acc[a][b]);
-      // fence the k-step: the next step's LDS reads stay in this step's region
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    for (int b = 0; b < C::TN; ++b) fb[b] = *reinterpret_cast<const bf16x8*>(Bs + L.fb_off[ks][0] + b * RB);
   } else {
+    auto two = [](const char* lo, const char* hi) {
+      const u32x4 x = *reinterpret_cast<const u32x4*>(lo), y = *reinterpret_cast<const u32x4*>(hi);
+      return i32x8{(int)x[0], (int)x[1], (int)x[2], (int)x[3], (int)y[0], (int)y[1], (int)y[2], (int)y[3]};
+    };
+#pragma unroll
+    for (int a = 0; a < C::TM; ++a) fa[a] = two(As + L.fa_off[ks][0] + a * RB, As + L.fa_off[ks][1] + a * RB);
+#pragma unroll
+    for (int b = 0; b < C::TN; ++b) fb[b] = two(Bs + L.fb_off[ks][0] + b * RB, Bs + L.fb_off[ks][1] + b * RB);
+  }
+}
+
+// The TM x TN MFMAs of one k-step.
+template <typename C>
+WAM_DEV void mfma_step(const Frag<C> (&fa)[C::TM], const Frag<C> (&fb)[C::TN], f32x16 (*acc)[C::TN]) {
+#pragma unroll
+  for (int a = 0; a < C::TM; ++a)
+#pragma unroll
+    for (int b = 0; b < C::TN; ++b) {
+      if constexpr (C::EB == 2) acc[a][b] = mfma32(fa[a], fb[b], acc[a][b]);
+      else acc[a][b] = mfma32_fp8(fa[a], fb[b], acc[a][b]);
+    }
+}
+
+// Instruction order of one k-step: one LDS read (while any of the NDS are left) and one
+// direct global load (while any of the NVM are left) ahead of each of its NMF MFMAs, so
+// the reads for the next k-step and the next slice's prefetch issue between the MFMAs.
+template <int NMF, int NDS, int NVM>
+WAM_DEV void interleave_step() {
+#pragma unroll
+  for (int i = 0; i < NMF; ++i) {
+    if (i < NDS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+    if (i < NVM) __builtin_amdgcn_sched_group_barrier(0x20, 1, 0);   // vector memory read
+    __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);                 // MFMA
+  }
+}
+
+WAM_DEV void block_barrier() {
+  // a plain s_barrier: __syncthreads would also wait for the prefetched slices in flight
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Slice t of the steady state, in ring stage CUR; on entry fa/fb[0] hold its k-step 0
+// fragments.  Every k-step but the last reads the next k-step's fragments while its
+// MFMAs run.  Before the last k-step the wave waits for its reads of this slice and for
+// its loads of slice t+1, and the workgroup meets at the slice's only barrier: slice t+1
+// is then visible to all, and stage CUR (slice t) is free, so the last k-step's MFMAs
+// run while slice t+S is fetched into stage CUR and k-step 0 of slice t+1 is read.  No
+// wave waits on an LDS read right after the barrier.
+template <typename C, int CUR>
+WAM_DEV void slice_steady(char* smem, const GemmLane<C>& L, int t, int K, f32x16 (*acc)[C::TN],
+                          Frag<C> (&fa)[2][C::TM], Frag<C> (&fb)[2][C::TN]) {
+  constexpr int S = C::STAGES, KS = C::KS, NI = C::NIA + C::NIB;
+  constexpr int NMF = C::TM * C::TN, NR = (C::TM + C::TN) * C::FCH;
+#pragma unroll
+  for (int ks = 0; ks < KS - 1; ++ks) {
+    read_frags<C>(smem, CUR, L, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
+    mfma_step<C>(fa[ks & 1], fb[ks & 1], acc);
+    interleave_step<NMF, NR, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  WAM_WAIT_LGKMCNT0();
+  WAM_WAIT_VMCNT((S - 2) * NI);
+  block_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  fetch_slice<C>(smem, CUR, L, t + S, K);
+  read_frags<C>(smem, (CUR + 1) % S, L, 0, fa[KS & 1], fb[KS & 1]);
+  mfma_step<C>(fa[(KS - 1) & 1], fb[(KS - 1) & 1], acc);
+  interleave_step<NMF, NR, NI>();
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+template <typename C, int CUR>
+WAM_DEV void steady_group(char* smem, const GemmLane<C>& L, int t, int K, f32x16 (*acc)[C::TN],
+                          Frag<C> (&fa)[2][C::TM], Frag<C> (&fb)[2][C::TN]) {
+  slice_steady<C, CUR>(smem, L, t + CUR, K, acc, fa, fb);
+  if constexpr (CUR + 1 < C::STAGES) steady_group<C, CUR + 1>(smem, L, t, K, acc, fa, fb);
+}
+
+// A slice after the steady state (the last few: fewer younger slices in flight, the next
+// one may run past K and need its tail zeroed, nothing to prefetch past the end), with
+// the same order as slice_steady and a runtime stage.
+template <typename C>
+WAM_DEV void slice_tail(char* smem, const GemmLane<C>& L, int t, int nk, int K, int lane, f32x16 (*acc)[C::TN],
+                        Frag<C> (&fa)[2][C::TM], Frag<C> (&fb)[2][C::TN]) {
+  constexpr int S = C::STAGES, KS = C::KS, NI = C::NIA + C::NIB;
+  const int cur = t % S;
+#pragma unroll
+  for (int ks = 0; ks < KS - 1; ++ks) {
+    read_frags<C>(smem, cur, L, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
+    mfma_step<C>(fa[ks & 1], fb[ks & 1], acc);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (t + 1 < nk) {
+    const int younger = (nk - 2 - t) < (S - 2) ? (nk - 2 - t) : (S - 2);  // slices past t+1 in flight
+    WAM_WAIT_LGKMCNT0();
+    if (younger >= 2) WAM_WAIT_VMCNT(2 * NI);
+    else if (younger == 1) WAM_WAIT_VMCNT(NI);
+    else WAM_WAIT_VMCNT(0);
+    if ((t + 2) * C::BK > K) {
+      zero_tail<C>(smem, (t + 1) % S, L, t + 1, K, lane);
+      WAM_WAIT_LGKMCNT0();
+    }
+    block_barrier();
+    if (t + S < nk) fetch_slice<C>(smem, cur, L, t + S, K);
+    read_frags<C>(smem, (t + 1) % S, L, 0, fa[KS & 1], fb[KS & 1]);
+  }
+  mfma_step<C>(fa[(KS - 1) & 1], fb[(KS - 1) & 1], acc);
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// FP8 operands keep the earlier main loop: one barrier at the start of each slice, then
+// its MFMAs with the next k-step's fragments in flight.  Their 32-byte fragments
+// double-buffered across the slice boundary (as the bf16 loop does) exceed the register
+// budget of the 8-wavefront tiles.  With `cur` a compile-time constant every LDS read is
+// a lane offset plus an immediate.
+template <typename C>
+WAM_DEV void mma_slice_fp8(const char* smem, int cur, const GemmLane<C>& L, f32x16 (*acc)[C::TN]) {
+  static_assert(C::EB == 1, "FP8 operands");
+  const char* As = smem + cur * C::STAGE;
+  const char* Bs = As + C::BM * C::ROWB;
+  constexpr int RB = 32 * C::ROWB;  // bytes of 32 LDS rows
+  {
     // FP8: a lane's fragment is 32 consecutive k (two 16-byte chunks) of its row
     i32x8 fa[2][C::TM], fb[2][C::TN];
     auto frag = [&](const char* base) {
@@ -235,20 +354,20 @@ WAM_DEV void mma_slice(const char* smem, int cur, const GemmLane<C>& L, f32x16 (
 // flight when S = 3, S-2 in general): wait for slice kt, barrier, prefetch slice
 // kt+S-1 into the stage freed by slice kt-1, then the slice's MFMAs.
 template <typename C, int CUR>
-WAM_DEV void steady_step(char* smem, const GemmLane<C>& L, int kt, int K, f32x16 (*acc)[C::TN]) {
+WAM_DEV void steady_step_fp8(char* smem, const GemmLane<C>& L, int kt, int K, f32x16 (*acc)[C::TN]) {
   constexpr int S = C::STAGES, NI = C::NIA + C::NIB;
   WAM_WAIT_VMCNT((S - 2) * NI);
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
   fetch_slice<C>(smem, (CUR + S - 1) % S, L, kt + S - 1, K);
-  mma_slice<C>(smem, CUR, L, acc);
+  mma_slice_fp8<C>(smem, CUR, L, acc);
 }
 
 template <typename C, int CUR>
-WAM_DEV void steady_group(char* smem, const GemmLane<C>& L, int kt, int K, f32x16 (*acc)[C::TN]) {
-  steady_step<C, CUR>(smem, L, kt + CUR, K, acc);
-  if constexpr (CUR + 1 < C::STAGES) steady_group<C, CUR + 1>(smem, L, kt, K, acc);
+WAM_DEV void steady_group_fp8(char* smem, const GemmLane<C>& L, int kt, int K, f32x16 (*acc)[C::TN]) {
+  steady_step_fp8<C, CUR>(smem, L, kt + CUR, K, acc);
+  if constexpr (CUR + 1 < C::STAGES) steady_group_fp8<C, CUR + 1>(smem, L, kt, K, acc);
 }
 
 // XCD-aware remap: the hardware deals workgroups round-robin over 8 XCDs; give each
@@ -314,32 +433,58 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn) {
 
   const int nk = (g.K + BK - 1) / BK;
   constexpr int NI = C::NIA + C::NIB;  // loads per slice per wave
+  if constexpr (C::EB == 2) {
+    static_assert(C::KS % 2 == 0, "fragment slots alternate per k-step and slice");
+    // prologue: the first S slices in flight, slice 0 landed and visible, its k-step 0 read
 #pragma unroll
-  for (int p = 0; p < S - 1; ++p)
-    if (p < nk) fetch_slice<C>(smem, p, L, p, g.K);
-  int kt = 0;
-  // steady state, S slices per iteration so each stage index is a constant; every
-  // slice here has S-2 younger slices in flight at its wait and prefetches a slice < nk
-  for (; kt + 2 * S - 2 < nk; kt += S) steady_group<C, 0>(smem, L, kt, g.K, acc);
-  // the remaining slices (fewer younger slices in flight; the last may run past K)
-  for (; kt < nk; ++kt) {
-    const int younger = (nk - 1 - kt) < (S - 2) ? (nk - 1 - kt) : (S - 2);
-    if (younger >= 2) WAM_WAIT_VMCNT(2 * NI);
-    else if (younger == 1) WAM_WAIT_VMCNT(NI);
-    else WAM_WAIT_VMCNT(0);
-    if ((kt + 1) * BK > g.K) {
-      zero_tail<C>(smem, kt % S, L, kt, g.K, lane);
-      WAM_WAIT_LGKMCNT0();
+    for (int p = 0; p < S; ++p)
+      if (p < nk) fetch_slice<C>(smem, p, L, p, g.K);
+    {
+      const int younger = nk - 1 < S - 1 ? nk - 1 : S - 1;
+      if (younger >= 2) WAM_WAIT_VMCNT(2 * NI);
+      else if (younger == 1) WAM_WAIT_VMCNT(NI);
+      else WAM_WAIT_VMCNT(0);
+      if (BK > g.K) {
+        zero_tail<C>(smem, 0, L, 0, g.K, lane);
+        WAM_WAIT_LGKMCNT0();
+      }
+      block_barrier();
     }
-    // Slice kt is visible to all waves and slice kt-1's stage is free once every wave
-    // is here: each wave has waited for its own loads of slice kt above, and its reads
-    // of slice kt-1 were consumed by its MFMAs.  A plain s_barrier (the __syncthreads
-    // fence would also wait for the prefetched slices still in flight).
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    if (kt + S - 1 < nk) fetch_slice<C>(smem, (kt + S - 1) % S, L, kt + S - 1, g.K);
-    mma_slice<C>(smem, kt % S, L, acc);
+    Frag<C> fa[2][C::TM], fb[2][C::TN];
+    read_frags<C>(smem, 0, L, 0, fa[0], fb[0]);
+    int kt = 0;
+    // steady state, S slices per iteration so each stage index is a constant: every slice
+    // here has a successor, prefetches a slice < nk, and waits for a full slice
+    for (; kt + 2 * S + 1 <= nk && (kt + 2 * S + 1) * BK <= g.K; kt += S) steady_group<C, 0>(smem, L, kt, g.K, acc, fa, fb);
+    for (; kt < nk; ++kt) slice_tail<C>(smem, L, kt, nk, g.K, lane, acc, fa, fb);
+  } else {
+#pragma unroll
+    for (int p = 0; p < S - 1; ++p)
+      if (p < nk) fetch_slice<C>(smem, p, L, p, g.K);
+    int kt = 0;
+    // steady state, S slices per iteration so each stage index is a constant; every
+    // slice here has S-2 younger slices in flight at its wait and prefetches a slice < nk
+    for (; kt + 2 * S - 2 < nk; kt += S) steady_group_fp8<C, 0>(smem, L, kt, g.K, acc);
+    // the remaining slices (fewer younger slices in flight; the last may run past K)
+    for (; kt < nk; ++kt) {
+      const int younger = (nk - 1 - kt) < (S - 2) ? (nk - 1 - kt) : (S - 2);
+      if (younger >= 2) WAM_WAIT_VMCNT(2 * NI);
+      else if (younger == 1) WAM_WAIT_VMCNT(NI);
+      else WAM_WAIT_VMCNT(0);
+      if ((kt + 1) * BK > g.K) {
+        zero_tail<C>(smem, kt % S, L, kt, g.K, lane);
+        WAM_WAIT_LGKMCNT0();
+      }
+      // Slice kt is visible to all waves and slice kt-1's stage is free once every wave
+      // is here: each wave has waited for its own loads of slice kt above, and its reads
+      // of slice kt-1 were consumed by its MFMAs.  A plain s_barrier (the __syncthreads
+      // fence would also wait for the prefetched slices still in flight).
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      if (kt + S - 1 < nk) fetch_slice<C>(smem, (kt + S - 1) % S, L, kt + S - 1, g.K);
+      mma_slice_fp8<C>(smem, kt % S, L, acc);
+    }
   }
   __syncthreads();  // all waves done with the operand ring before it is reused
 
@@ -448,11 +593,20 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn) {
   }
 }
 
+// Tile order within an XCD's contiguous range: ids walk 8 row tiles of one column tile,
+// then the same 8 row tiles of the next column tile, so the ~32 tiles an XCD runs at
+// once form an 8 x 4 block that shares 8 A panels and 4 W panels in its L2 (instead of
+// ~25 A panels and 2 W panels when all row tiles of a column come first; measured
+// 0-2.5% faster on the step's projections, interleaved launches).
 template <typename C, int EPI>
 __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int tiles_m, int tiles_n) {
   if (skip_step(g.skip)) return;
   const int lid = xcd_tile(tiles_m * tiles_n);
-  gemm_tile<C, EPI>(g, lid % tiles_m, lid / tiles_m);  // consecutive tiles share a W panel
+  constexpr int GM = 8;
+  const int per = GM * tiles_n, grp = lid / per, first = grp * GM;
+  const int gm = tiles_m - first < GM ? tiles_m - first : GM;
+  const int r = lid - grp * per;
+  gemm_tile<C, EPI>(g, first + r % gm, r / gm);
 }
 
 // gg.n products of the same shape and A, each with its own W, bias and output: one
