@@ -53,6 +53,10 @@ def parse():
                         "block (per-role kernel times: the GEMM fractions of the JSON line)")
     p.add_argument("--pmc-summary", default=None, metavar="DIR",
                    help="no GPU: print per-kernel averages of a rocprofv3 counter CSV under DIR")
+    p.add_argument("--trace-summary", default=None, metavar="DIR",
+                   help="no GPU: print per-kernel and per-launch-shape times of a rocprofv3 kernel trace "
+                        "under DIR (with --trace-steps: the dispatches of that many steps per step)")
+    p.add_argument("--trace-steps", type=int, default=0)
     return p.parse_args()
 
 
@@ -524,10 +528,60 @@ def pmc_summary(path):
               + f" | {util} | {clk} |")
 
 
+def trace_summary(path, steps):
+    """Kernel time by (kernel, grid size) from a rocprofv3 kernel-trace CSV: calls, average,
+    min and max duration, total, share of all kernel time, and (steps > 0) milliseconds per
+    step over the dispatches of the run's last `steps` steps, a step being delimited by
+    the time-embedding kernel that opens it."""
+    import csv
+    import glob
+    files = sorted(glob.glob(os.path.join(path, "**", "*kernel_trace.csv"), recursive=True))
+    if not files:
+        sys.exit(f"no kernel_trace.csv under {path}")
+    rows = []
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            name = r["Kernel_Name"].replace("(anonymous namespace)::", "").replace("wam::", "")
+            rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), name.split("(")[0][:80], r.get("Grid_Size") or r.get("Grid_Size_X")))
+    rows.sort()
+    total = sum(e - b for b, e, _, _ in rows)
+    if steps > 0:
+        starts = [i for i, r in enumerate(rows) if r[2].startswith("sinusoid_kernel")]
+        if len(starts) >= steps:
+            rows_s = rows[starts[-steps]:]
+        else:
+            rows_s = rows
+    agg = {}
+    for b, e, n, g in rows:
+        a = agg.setdefault((n, g), [0, 0, 1e18, 0])
+        a[0] += 1
+        a[1] += e - b
+        a[2] = min(a[2], e - b)
+        a[3] = max(a[3], e - b)
+    per_step = {}
+    if steps > 0:
+        for b, e, n, g in rows_s:
+            per_step[(n, g)] = per_step.get((n, g), 0) + e - b
+    print("| kernel | grid | calls | avg us | min us | max us | total ms | % |" + (" ms/step |" if steps else ""))
+    print("|---|---:|---:|---:|---:|---:|---:|---:|" + ("---:|" if steps else ""))
+    for (n, g), a in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+        if a[1] < 0.001 * total:
+            continue
+        line = (f"| `{n}` | {g} | {a[0]} | {a[1] / a[0] / 1e3:.1f} | {a[2] / 1e3:.1f} | {a[3] / 1e3:.1f} | "
+                f"{a[1] / 1e6:.1f} | {100.0 * a[1] / total:.1f} |")
+        if steps:
+            line += f" {per_step.get((n, g), 0) / 1e6 / steps:.3f} |"
+        print(line)
+    if steps:
+        print(f"\nkernel time per step over the last {steps} steps: {sum(per_step.values()) / 1e6 / steps:.2f} ms")
+
+
 def main():
     args = parse()
     if args.pmc_summary:
         return pmc_summary(args.pmc_summary)
+    if args.trace_summary:
+        return trace_summary(args.trace_summary, args.trace_steps)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: this build runs on one GPU only (no sharding or collectives); "
