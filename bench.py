@@ -43,7 +43,7 @@ def parse():
                         "launches at the workload's shape; prints what ran and exits")
     p.add_argument("--probe-attn-fp8", type=int, default=0, metavar="N",
                    help="the same with the FP8 self-attention (operands quantized by the library)")
-    p.add_argument("--probe", choices=("gemm", "ln", "rope"), default=None,
+    p.add_argument("--probe", choices=("gemm", "ln", "rope", "torch_linear"), default=None,
                    help="counter-collection mode: the calibration copy, then --probe-n launches of each "
                         "of the block's six projections (gemm), of the AdaLN LayerNorm (ln) or of the "
                         "RoPE/KV-append kernel (rope) at the workload's shapes")
@@ -445,7 +445,18 @@ def probe_kernels(wl, kind, n):
 
     copy_bytes = _calibration_copy(torch, g)
     ran = []
-    if kind == "gemm":
+    if kind == "torch_linear":
+        # reference point, not part of the library: PyTorch's linear (hipBLASLt) on the same
+        # projection shapes, plain bf16 output, no fused epilogue
+        for name, K, N in (("qkv", d, 3 * d), ("o", d, d), ("ffn1", d, F), ("ffn2", F, d)):
+            A, Wt = rn(M, K), rn(N, K, std=0.02)
+            torch.cuda.synchronize()
+            for _ in range(n):
+                out = torch.nn.functional.linear(A, Wt)
+            torch.cuda.synchronize()
+            ran.append({"role": name, "M": M, "N": N, "K": K, "launches": n, "out": list(out.shape)})
+            del A, Wt, out
+    elif kind == "gemm":
         x = torch.randn(M, d, generator=g, device="cuda")
         gate = torch.randn(6, d, generator=g, device="cuda") * 0.02
         roles = (("qkv", d, 3 * d, w.WAM_EPI_BF16), ("o", d, d, w.WAM_EPI_RESID_F32),
