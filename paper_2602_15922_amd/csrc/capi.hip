@@ -393,8 +393,11 @@ wam_status mark(const BlockEvents& e, int kind, int end, hipStream_t s) {
   return WAM_OK;
 }
 
+// pq: this block's folded AdaLN shift/scale rows (AdalnFoldArgs layout, nseg segments), or
+// NULL to sum the block's and the sample's rows in each LayerNorm
 wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_block_io& io, char* ws,
-                     hipStream_t s, const BlockEvents& ev = BlockEvents{}, int32_t seg = 0, int64_t alt = 0) {
+                     hipStream_t s, const BlockEvents& ev = BlockEvents{}, int32_t seg = 0, int64_t alt = 0,
+                     const float* pq = nullptr, int32_t nseg = 1) {
   const int d = D.d, B = io.B, L = io.L, M = B * L;
   const BlockWs lay = block_ws(D, B, L, io.Lc);
   void* h = ws + lay.h;
@@ -411,6 +414,8 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
 
   // 1. AdaLN: h = LN(x)(1 + scale1) + shift1
   LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h, seg, alt};
+  const int64_t pq_ms = (int64_t)nseg * 2 * d, pq_alt = 2 * (int64_t)d, pq_norm = (int64_t)B * pq_ms;
+  if (pq) ln = LnArgs{M, L, d, D.eps, io.x, nullptr, nullptr, nullptr, pq, nullptr, pq + d, pq_ms, h, seg, pq_alt};
   TRY(mark(ev, WAM_EV_LN1, 0, s));
   LAUNCH(launch_ln_mod(pred(ln), s));
   TRY(mark(ev, WAM_EV_LN1, 1, s));
@@ -484,6 +489,9 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   TRY(mark(ev, WAM_EV_CO, 1, s));
   // 11. AdaLN #2
   LnArgs l2{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 3 * d, e0 + 3 * d, m6 + 4 * d, e0 + 4 * d, ms, h, seg, alt};
+  if (pq)
+    l2 = LnArgs{M, L, d, D.eps, io.x, nullptr, nullptr, nullptr, pq + pq_norm, nullptr, pq + pq_norm + d, pq_ms, h,
+                seg, pq_alt};
   TRY(mark(ev, WAM_EV_LN2, 0, s));
   LAUNCH(launch_ln_mod(pred(l2), s));
   TRY(mark(ev, WAM_EV_LN2, 1, s));
@@ -506,7 +514,8 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
 // The part of a block that an update pass needs from its last layer: AdaLN #1, the K|V
 // columns of the QKV projection, and RoPE on k with the cache append.
 wam_status block_kv_run(const wam_dims& D, const wam_block_weights& W, const wam_block_io& io, char* ws,
-                        hipStream_t s, int32_t seg = 0, int64_t alt = 0) {
+                        hipStream_t s, int32_t seg = 0, int64_t alt = 0, const float* pq = nullptr,
+                        int32_t nseg = 1) {
   const int d = D.d, B = io.B, L = io.L, M = B * L;
   const BlockWs lay = block_ws(D, B, L, io.Lc);
   void* h = ws + lay.h;
@@ -515,6 +524,9 @@ wam_status block_kv_run(const wam_dims& D, const wam_block_weights& W, const wam
   const float* e0 = io.e0;
   const int64_t ms = 6 * (int64_t)d;
   LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h, seg, alt};
+  if (pq)
+    ln = LnArgs{M, L, d, D.eps, io.x, nullptr, nullptr, nullptr, pq, nullptr, pq + d, (int64_t)nseg * 2 * d, h, seg,
+                2 * (int64_t)d};
   LAUNCH(launch_ln_mod(pred(ln), s));
   // rows d..3d of W_qkv (the k and v outputs) into columns d..3d of the [M][3d] buffer
   const wam_block_fp8* F8 = W.fp8;
@@ -678,7 +690,8 @@ wam_status cross_kv_run(const wam_model& m, int32_t B, int32_t Lc, const void* c
 }
 
 struct StepWs {
-  size_t x, e, e0, ctx, piece, block, kv, kv_layer, total;
+  size_t x, e, e0, ctx, piece, block, pq, pq_layer, kv, kv_layer, total;
+  int32_t nseg;
 };
 StepWs step_ws(const wam_model& m, const wam_step_io& io) {
   const wam_dims& D = m.dims;
@@ -697,6 +710,10 @@ StepWs step_ws(const wam_model& m, const wam_step_io& io) {
   piece = std::max(piece, head_ws(D, io.B, io.F, io.Hl, io.Wl, io.A).total);
   w.piece = off; off += align256(piece);
   w.block = off; off += block_ws(D, io.B, (int32_t)L, io.Lc).total;
+  // every block's folded AdaLN rows (two norms x B samples x segments x shift/scale)
+  w.nseg = io.t_action != nullptr && io.A > 0 ? 2 : 1;
+  w.pq_layer = (size_t)2 * io.B * w.nseg * 2 * D.d;  // floats
+  w.pq = off; off += align256((size_t)std::max(D.n_layers, 0) * w.pq_layer * 4);
   // without ctx_kv: every block's cross K|V, projected before the first block.  Last, so
   // every other offset is the same with and without it.
   w.kv_layer = io.ctx_kv ? 0 : align256((size_t)io.B * io.Lc * 2 * D.d * 2);
@@ -773,6 +790,25 @@ BlockEvents block_events(const wam_step_io& io, int l) {
   return e;
 }
 
+// Every block's combined AdaLN rows for this step's time embeddings (e0, and at alt_e0 the
+// action rows' own), in chunks of at most ADALN_FOLD_MAX_LAYERS layers per launch.
+wam_status fold_run(const wam_model& m, int32_t B, const float* e0, int64_t alt_e0, const StepWs& lay, char* w,
+                    hipStream_t s) {
+  const wam_dims& D = m.dims;
+  for (int l0 = 0; l0 < D.n_layers; l0 += ADALN_FOLD_MAX_LAYERS) {
+    AdalnFoldArgs a{};
+    a.n_layers = std::min(D.n_layers - l0, ADALN_FOLD_MAX_LAYERS);
+    a.d = D.d; a.B = B; a.nseg = lay.nseg;
+    a.e0 = e0; a.e0_stride = 6 * (int64_t)D.d; a.alt = alt_e0;
+    for (int i = 0; i < a.n_layers; ++i) a.mod6[i] = m.blocks[l0 + i].mod6;
+    a.out = reinterpret_cast<float*>(w + lay.pq) + (size_t)l0 * lay.pq_layer;
+    a.layer_stride = (int64_t)lay.pq_layer;
+    a.skip = t_skip;
+    LAUNCH(launch_adaln_fold(a, s));
+  }
+  return WAM_OK;
+}
+
 // The launch sequence of one step; arguments already validated.
 wam_status step_run(const wam_model& m, const wam_step_io& io, char* w, hipStream_t stream) {
   const StepWs lay = step_ws(m, io);
@@ -789,6 +825,7 @@ wam_status step_run(const wam_model& m, const wam_step_io& io, char* w, hipStrea
   const bool flash = io.t_action != nullptr && io.A > 0;
   const int64_t alt_e = flash ? (int64_t)io.B * D.d : 0, alt_e0 = flash ? (int64_t)io.B * 6 * D.d : 0;
   if (flash) TRY(time_run(m, io.B, io.t_action, e + alt_e, e0 + alt_e0, piece, stream));
+  TRY(fold_run(m, io.B, e0, alt_e0, lay, w, stream));
   if (!io.ctx_kv) {
     TRY(text_run(m, io.B, io.Lc, io.text, ctx, piece, stream));
     const BlockWs bl = block_ws(D, io.B, L, io.Lc);
@@ -803,7 +840,8 @@ wam_status step_run(const wam_model& m, const wam_step_io& io, char* w, hipStrea
     b.ch = io.ch; b.ctx = ctx; b.ctx_kv = io.ctx_kv ? io.ctx_kv[l] : w + lay.kv + (size_t)l * lay.kv_layer;
     b.B = io.B; b.L = L; b.Lc = io.Lc;
     b.k_exp = io.k_exp ? io.k_exp[l] : nullptr; b.v_scale = io.v_scale ? io.v_scale[l] : 1.0f;
-    TRY(block_run(D, m.blocks[l], b, w + lay.block, stream, block_events(io, l), flash ? Lv : 0, alt_e0));
+    TRY(block_run(D, m.blocks[l], b, w + lay.block, stream, block_events(io, l), flash ? Lv : 0, alt_e0,
+                  reinterpret_cast<const float*>(w + lay.pq) + (size_t)l * lay.pq_layer, lay.nseg));
   }
   TRY(head_run(m, io.B, io.F, io.Hl, io.Wl, io.A, x, e, io.v_video, io.v_action, piece, stream, alt_e));
   return WAM_OK;
@@ -1002,6 +1040,7 @@ wam_status update_run(const wam_model* m, const wam_step_io* io, void* ws, hipSt
   const bool flash = io->t_action != nullptr && io->A > 0;
   const int64_t alt_e0 = flash ? (int64_t)io->B * 6 * D.d : 0;
   if (flash) TRY(time_run(*m, io->B, io->t_action, e + (int64_t)io->B * D.d, e0 + alt_e0, piece, stream));
+  TRY(fold_run(*m, io->B, e0, alt_e0, lay, w, stream));
   // the last block only projects its K/V, so the cross K|V of the others
   if (!io->ctx_kv && D.n_layers > 1) {
     TRY(text_run(*m, io->B, io->Lc, io->text, ctx, piece, stream));
@@ -1018,10 +1057,12 @@ wam_status update_run(const wam_model* m, const wam_step_io* io, void* ws, hipSt
     b.ctx_kv = io->ctx_kv ? io->ctx_kv[l] : w + lay.kv + (size_t)l * lay.kv_layer;
     b.B = io->B; b.L = L; b.Lc = io->Lc;
     b.k_exp = io->k_exp ? io->k_exp[l] : nullptr; b.v_scale = io->v_scale ? io->v_scale[l] : 1.0f;
+    const float* pq = reinterpret_cast<const float*>(w + lay.pq) + (size_t)l * lay.pq_layer;
     if (l + 1 == D.n_layers) {
-      TRY(block_kv_run(D, m->blocks[l], b, w + lay.block, stream, flash ? Lv : 0, alt_e0));
+      TRY(block_kv_run(D, m->blocks[l], b, w + lay.block, stream, flash ? Lv : 0, alt_e0, pq, lay.nseg));
     } else {
-      TRY(block_run(D, m->blocks[l], b, w + lay.block, stream, block_events(*io, l), flash ? Lv : 0, alt_e0));
+      TRY(block_run(D, m->blocks[l], b, w + lay.block, stream, block_events(*io, l), flash ? Lv : 0, alt_e0, pq,
+                    lay.nseg));
     }
   }
   return WAM_OK;

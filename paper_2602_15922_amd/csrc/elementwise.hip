@@ -94,6 +94,30 @@ __global__ __launch_bounds__(LN_ROWS * 64, NV <= 20 ? 4 : 2) void ln_mod_kernel(
     }
 }
 
+// One thread per 4 columns of one (layer, norm, sample, segment): the shift and scale
+// sums of the AdaLN modulation (the same fp32 additions the LayerNorm performs).
+__global__ __launch_bounds__(256) void adaln_fold_kernel(const AdalnFoldArgs a) {
+  if (skip_step(a.skip)) return;
+  const int d4 = a.d >> 2;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t n = (int64_t)a.n_layers * 2 * a.B * a.nseg * d4;
+  if (i >= n) return;
+  int64_t t = i;
+  const int c = (int)(t % d4) * 4; t /= d4;
+  const int g = (int)(t % a.nseg); t /= a.nseg;
+  const int b = (int)(t % a.B); t /= a.B;
+  const int k = (int)(t % 2);
+  const int l = (int)(t / 2);
+  const float* m6 = a.mod6[l];
+  const float* e0 = a.e0 + (int64_t)b * a.e0_stride + (g ? a.alt : 0);
+  float* o = a.out + (int64_t)l * a.layer_stride + ((((int64_t)k * a.B + b) * a.nseg + g) * 2) * a.d;
+  const int sh = 3 * k, sc = 3 * k + 1;
+  *reinterpret_cast<f32x4*>(o + c) =
+      *reinterpret_cast<const f32x4*>(m6 + sh * a.d + c) + *reinterpret_cast<const f32x4*>(e0 + sh * a.d + c);
+  *reinterpret_cast<f32x4*>(o + a.d + c) =
+      *reinterpret_cast<const f32x4*>(m6 + sc * a.d + c) + *reinterpret_cast<const f32x4*>(e0 + sc * a.d + c);
+}
+
 // ---------------------------------------------------------------------------------
 // Per-row E4M3 quantization for the FP8 GEMMs: one wavefront per row of K bf16 values,
 // amax over the row, inv = 448 / amax (fp32), q = E4M3(x * inv) rounded to nearest even
@@ -284,42 +308,68 @@ __global__ __launch_bounds__(256) void rope_qkv_fp8_kernel(const RopeFp8Args f) 
 }
 
 // ---------------------------------------------------------------------------------
-// Small-batch GEMV for the time MLP: one wavefront per output feature n computes it
-// for every sample b (B <= 8); W row read once with 16-byte loads.
+// Small-batch GEMV for the time MLP (B <= 8): a workgroup of 4 wavefronts owns
+// GEMV_ROWS output features, GEMV_WROWS per wavefront, for every sample b.  The input
+// (after its activation, evaluated once per workgroup instead of once per feature) is
+// staged in LDS in passes of up to GEMV_LDS floats; each lane then reads 8 consecutive
+// k of each of its wavefront's W rows per 16-byte load, so W streams from HBM once with
+// GEMV_WROWS loads in flight per lane.  Lane l sums k = 8 l + 512 i (+0..7), the same
+// order for any pass length (passes are multiples of 512 columns).
 // ---------------------------------------------------------------------------------
 constexpr int GEMV_MAXB = 8;
+constexpr int GEMV_WROWS = 4;
+constexpr int GEMV_ROWS = 4 * GEMV_WROWS;
+constexpr int GEMV_LDS = 16384;
 
 __global__ __launch_bounds__(256) void gemv_kernel(int B, int N, int K, const float* __restrict__ x,
                                                    int act, const bf16* __restrict__ W,
                                                    const float* __restrict__ bias, float* __restrict__ out,
                                                    const int32_t* skip) {
+  __shared__ __attribute__((aligned(16))) float xs[GEMV_LDS];
+  if (skip_step(skip)) return;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int n = blockIdx.x * 4 + w;
-  if (n >= N || skip_step(skip)) return;
-  float acc[GEMV_MAXB];
+  const int n0 = blockIdx.x * GEMV_ROWS + w * GEMV_WROWS;
+  float acc[GEMV_MAXB][GEMV_WROWS];
 #pragma unroll
-  for (int b = 0; b < GEMV_MAXB; ++b) acc[b] = 0.f;
-  const bf16* wr = W + (int64_t)n * K;
-  for (int k0 = lane * 8; k0 < K; k0 += 512) {
-    const bf16x8 wv = load_bf16x8(wr + k0);
+  for (int b = 0; b < GEMV_MAXB; ++b)
 #pragma unroll
-    for (int b = 0; b < GEMV_MAXB; ++b)
-      if (b < B) {
-        const float* xb = x + (int64_t)b * K + k0;
+    for (int r = 0; r < GEMV_WROWS; ++r) acc[b][r] = 0.f;
+  const int kc = (GEMV_LDS / B) & ~511;  // columns per pass (B <= 8: at least 2048)
+  for (int k0 = 0; k0 < K; k0 += kc) {
+    const int kn = K - k0 < kc ? K - k0 : kc;
+    __syncthreads();
+    for (int i = threadIdx.x; i < B * kn; i += 256) {
+      const int b = i / kn, k = i - b * kn;
+      const float v = x[(int64_t)b * K + k0 + k];
+      xs[b * kn + k] = act == GEMV_ACT_SILU ? silu_f(v) : v;
+    }
+    __syncthreads();
+    for (int kk = lane * 8; kk < kn; kk += 512) {
+      bf16x8 wv[GEMV_WROWS];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          float xv = xb[j];
-          if (act == GEMV_ACT_SILU) xv = silu_f(xv);
-          acc[b] += xv * (float)wv[j];
+      for (int r = 0; r < GEMV_WROWS; ++r)
+        wv[r] = n0 + r < N ? load_bf16x8(W + (int64_t)(n0 + r) * K + k0 + kk) : bf16x8{};
+#pragma unroll
+      for (int b = 0; b < GEMV_MAXB; ++b)
+        if (b < B) {
+          const f32x4 x0 = *reinterpret_cast<const f32x4*>(xs + b * kn + kk);
+          const f32x4 x1 = *reinterpret_cast<const f32x4*>(xs + b * kn + kk + 4);
+          const float xv[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+#pragma unroll
+          for (int r = 0; r < GEMV_WROWS; ++r)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc[b][r] += xv[j] * (float)wv[r][j];
         }
-      }
+    }
   }
 #pragma unroll
   for (int b = 0; b < GEMV_MAXB; ++b)
-    if (b < B) {
-      const float s = wave_sum(acc[b]);
-      if (lane == 0) out[(int64_t)b * N + n] = s + (bias ? bias[n] : 0.f);
-    }
+    if (b < B)
+#pragma unroll
+      for (int r = 0; r < GEMV_WROWS; ++r) {
+        const float s = wave_sum(acc[b][r]);
+        if (lane == 0 && n0 + r < N) out[(int64_t)b * N + n0 + r] = s + (bias ? bias[n0 + r] : 0.f);
+      }
 }
 
 // [cos(1000 t w_k), sin(1000 t w_k)], w_k = 10000^(-k/half); evaluated in double so the
@@ -385,6 +435,14 @@ hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t launch_adaln_fold(const AdalnFoldArgs& a, hipStream_t s) {
+  const int64_t n = (int64_t)a.n_layers * 2 * a.B * a.nseg * (a.d / 4);
+  if (n == 0) return hipSuccess;
+  if (a.n_layers > ADALN_FOLD_MAX_LAYERS || a.d % 4 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(adaln_fold_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_quant_rows(int32_t M, int32_t K, const void* x, int64_t ldx, void* q, int64_t ldq, float* scale,
                              hipStream_t s, const int32_t* skip) {
   if (M == 0) return hipSuccess;
@@ -402,7 +460,9 @@ hipError_t launch_rope_qkv(const RopeArgs& a, hipStream_t s) {
 
 hipError_t launch_gemv(int32_t B, int32_t N, int32_t K, const float* x, int32_t act, const void* W,
                        const float* bias, float* out, hipStream_t s, const int32_t* skip) {
-  hipLaunchKernelGGL(gemv_kernel, dim3((N + 3) / 4), dim3(256), 0, s, B, N, K, x, act,
+  if (B <= 0 || N <= 0) return hipSuccess;
+  if (B > GEMV_MAXB || K % 8 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gemv_kernel, dim3((N + GEMV_ROWS - 1) / GEMV_ROWS), dim3(256), 0, s, B, N, K, x, act,
                      static_cast<const bf16*>(W), bias, out, skip);
   return hipGetLastError();
 }

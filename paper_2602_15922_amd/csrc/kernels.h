@@ -90,6 +90,24 @@ struct LnArgs {
 };
 hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s);
 
+// The combined AdaLN modulation of every block's two modulated LayerNorms, formed once per
+// step: for layer l, norm k (0: shift/scale rows 0/1 of the six, 1: rows 3/4), sample b and
+// segment g, out[l][k][b][g][0] = mod6_l[3k] + e0_b[3k] (shift) and [1] = mod6_l[3k+1] +
+// e0_b[3k+1] (scale), d floats each; segment 1 reads e0 at +alt.  A LayerNorm given the
+// shift and scale rows as its per-sample vectors (stride nseg*2*d, segment offset 2*d) then
+// forms exactly the sums it forms from the four vectors.
+constexpr int ADALN_FOLD_MAX_LAYERS = 64;
+struct AdalnFoldArgs {
+  int32_t n_layers, d, B, nseg;
+  const float* e0;
+  int64_t e0_stride, alt;
+  const float* mod6[ADALN_FOLD_MAX_LAYERS];
+  float* out;
+  int64_t layer_stride;  // floats per layer: 2 * B * nseg * 2 * d
+  const int32_t* skip;
+};
+hipError_t launch_adaln_fold(const AdalnFoldArgs& a, hipStream_t s);
+
 struct RopeArgs {
   int32_t B, L, H, Dh, Lcap, row0;
   const void* qkv;
