@@ -26,6 +26,7 @@
 #include "kernels.h"
 
 namespace wam {
+int cu_count();
 namespace {
 
 // EB: operand bytes per element, 2 (bf16: 32x32x16 MFMA) or 1 (FP8 E4M3: the 32x32x64
@@ -372,8 +373,10 @@ WAM_DEV void steady_group_fp8(char* smem, const GemmLane<C>& L, int kt, int K, f
 
 // XCD-aware remap: the hardware deals workgroups round-robin over 8 XCDs; give each
 // XCD a contiguous range of the nblk tiles so tiles that share a W panel share an L2.
-WAM_DEV int xcd_tile(int nblk) {
-  const int i = blockIdx.x, x = i & 7, j = i >> 3;
+// i is a dispatch slot: the workgroup index, or (persistent workgroups, their count a
+// multiple of 8) blockIdx.x + r * gridDim.x for round r, which stays on the same XCD.
+WAM_DEV int xcd_tile(int i, int nblk) {
+  const int x = i & 7, j = i >> 3;
   const int per = nblk >> 3, rem = nblk & 7;
   return x * per + (x < rem ? x : rem) + j;
 }
@@ -598,15 +601,22 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn) {
 // once form an 8 x 4 block that shares 8 A panels and 4 W panels in its L2 (instead of
 // ~25 A panels and 2 W panels when all row tiles of a column come first; measured
 // 0-2.5% faster on the step's projections, interleaved launches).
+//
+// The workgroups are persistent: one per resident slot, each taking every gridDim.x-th
+// dispatch slot in turn, so a tile's first slices are fetched while the previous tile's
+// output stores drain, without a workgroup launch in between.
 template <typename C, int EPI>
 __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int tiles_m, int tiles_n) {
   if (skip_step(g.skip)) return;
-  const int lid = xcd_tile(tiles_m * tiles_n);
+  const int total = tiles_m * tiles_n;
   constexpr int GM = 8;
-  const int per = GM * tiles_n, grp = lid / per, first = grp * GM;
-  const int gm = tiles_m - first < GM ? tiles_m - first : GM;
-  const int r = lid - grp * per;
-  gemm_tile<C, EPI>(g, first + r % gm, r / gm);
+  for (int slot = blockIdx.x; slot < total; slot += gridDim.x) {
+    const int lid = xcd_tile(slot, total);
+    const int per = GM * tiles_n, grp = lid / per, first = grp * GM;
+    const int gm = tiles_m - first < GM ? tiles_m - first : GM;
+    const int r = lid - grp * per;
+    gemm_tile<C, EPI>(g, first + r % gm, r / gm);
+  }
 }
 
 // gg.n products of the same shape and A, each with its own W, bias and output: one
@@ -615,15 +625,29 @@ template <typename C, int EPI>
 __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt_group(const GemmArgs g, int tiles_m, int tiles_n,
                                                                const GemmGroup gg) {
   if (skip_step(g.skip)) return;
-  const int per_group = tiles_m * tiles_n;
-  const int lid = xcd_tile(per_group * gg.n);
-  const int grp = lid / per_group, r = lid - grp * per_group;
-  GemmArgs gl = g;
-  gl.W = gg.W[grp];
-  gl.bias = gg.bias[grp];
-  gl.out = gg.out[grp];
-  if constexpr (C::EB == 1) gl.w_scale = gg.w_scale[grp];
-  gemm_tile<C, EPI>(gl, r % tiles_m, r / tiles_m);
+  const int per_group = tiles_m * tiles_n, total = per_group * gg.n;
+  for (int slot = blockIdx.x; slot < total; slot += gridDim.x) {
+    const int lid = xcd_tile(slot, total);
+    const int grp = lid / per_group, r = lid - grp * per_group;
+    GemmArgs gl = g;
+    gl.W = gg.W[grp];
+    gl.bias = gg.bias[grp];
+    gl.out = gg.out[grp];
+    if constexpr (C::EB == 1) gl.w_scale = gg.w_scale[grp];
+    gemm_tile<C, EPI>(gl, r % tiles_m, r / tiles_m);
+  }
+}
+
+// Persistent workgroups: as many as are resident at once (by LDS and by wavefronts per
+// SIMD), a multiple of 8 so each keeps its XCD, never more than there are tiles.
+template <typename Cf>
+int persistent_grid(long tiles) {
+  constexpr int LDS = 160 * 1024, by_lds = LDS / (Cf::STAGES * Cf::STAGE);
+  constexpr int by_waves = Cf::OCC * 4 / Cf::NW;
+  constexpr int per_cu = (by_lds < by_waves ? by_lds : by_waves) > 0 ? (by_lds < by_waves ? by_lds : by_waves) : 1;
+  long n = (long)cu_count() * per_cu;
+  if (n >= 8) n &= ~7L;
+  return (int)(tiles < n ? tiles : n);
 }
 
 template <typename Cf>
@@ -632,10 +656,11 @@ hipError_t launch_cfg(const GemmArgs& g, const GemmGroup* gg, hipStream_t s) {
   dim3 block(Cf::NT);
   if (gg) {  // grouped: the bf16 epilogue only
     if (g.epi != WAM_EPI_BF16) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((gemm_nt_group<Cf, WAM_EPI_BF16>), dim3(tm * tn * gg->n), block, 0, s, g, tm, tn, *gg);
+    hipLaunchKernelGGL((gemm_nt_group<Cf, WAM_EPI_BF16>), dim3(persistent_grid<Cf>((long)tm * tn * gg->n)), block, 0,
+                       s, g, tm, tn, *gg);
     return hipGetLastError();
   }
-  dim3 grid(tm * tn);
+  dim3 grid(persistent_grid<Cf>((long)tm * tn));
   switch (g.epi) {
     case WAM_EPI_BF16: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_BF16>), grid, block, 0, s, g, tm, tn); break;
     case WAM_EPI_GELU_BF16: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_GELU_BF16>), grid, block, 0, s, g, tm, tn); break;
