@@ -311,7 +311,7 @@ __global__ __launch_bounds__(256) void rope_qkv_fp8_kernel(const RopeFp8Args f) 
 // Small-batch GEMV for the time MLP (B <= 8): a workgroup of 4 wavefronts owns
 // GEMV_ROWS output features, GEMV_WROWS per wavefront, for every sample b.  The input
 // (after its activation, evaluated once per workgroup instead of once per feature) is
-// staged in LDS in passes of up to GEMV_LDS floats; each lane then reads 8 consecutive
+// staged in LDS (all of it, or passes of up to GEMV_LDS floats); each lane then reads 8 consecutive
 // k of each of its wavefront's W rows per 16-byte load, so W streams from HBM once with
 // GEMV_WROWS loads in flight per lane.  Lane l sums k = 8 l + 512 i (+0..7), the same
 // order for any pass length (passes are multiples of 512 columns).
@@ -321,27 +321,51 @@ constexpr int GEMV_WROWS = 4;
 constexpr int GEMV_ROWS = 4 * GEMV_WROWS;
 constexpr int GEMV_LDS = 16384;
 
-__global__ __launch_bounds__(256) void gemv_kernel(int B, int N, int K, const float* __restrict__ x,
+template <int B>
+__global__ __launch_bounds__(256, 2) void gemv_kernel(int N, int K, int kc, const float* __restrict__ x,
                                                    int act, const bf16* __restrict__ W,
                                                    const float* __restrict__ bias, float* __restrict__ out,
                                                    const int32_t* skip) {
-  __shared__ __attribute__((aligned(16))) float xs[GEMV_LDS];
+  extern __shared__ __attribute__((aligned(16))) float xs[];  // B * kc floats
   if (skip_step(skip)) return;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int n0 = blockIdx.x * GEMV_ROWS + w * GEMV_WROWS;
-  float acc[GEMV_MAXB][GEMV_WROWS];
+  float acc[B][GEMV_WROWS];
 #pragma unroll
-  for (int b = 0; b < GEMV_MAXB; ++b)
+  for (int b = 0; b < B; ++b)
 #pragma unroll
     for (int r = 0; r < GEMV_WROWS; ++r) acc[b][r] = 0.f;
-  const int kc = (GEMV_LDS / B) & ~511;  // columns per pass (B <= 8: at least 2048)
   for (int k0 = 0; k0 < K; k0 += kc) {
     const int kn = K - k0 < kc ? K - k0 : kc;
     __syncthreads();
-    for (int i = threadIdx.x; i < B * kn; i += 256) {
-      const int b = i / kn, k = i - b * kn;
-      const float v = x[(int64_t)b * K + k0 + k];
-      xs[b * kn + k] = act == GEMV_ACT_SILU ? silu_f(v) : v;
+    // 4 floats per load, a thread's loads issued in groups of 8 before any is used (B * kn
+    // <= GEMV_LDS: at most GEMV_LDS / 1024 per thread; kn is a multiple of 8)
+    {
+      const int kn4 = kn >> 2, n4 = B * kn4;
+#pragma unroll
+      for (int j0 = 0; j0 < GEMV_LDS / 1024; j0 += 8) {
+        f32x4 v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int i = threadIdx.x + 256 * (j0 + j);
+          if (i < n4) {
+            const int b = i / kn4, k = (i - b * kn4) * 4;
+            v[j] = *reinterpret_cast<const f32x4*>(x + (int64_t)b * K + k0 + k);
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int i = threadIdx.x + 256 * (j0 + j);
+          if (i < n4) {
+            const int b = i / kn4, k = (i - b * kn4) * 4;
+            f32x4 u = v[j];
+            if (act == GEMV_ACT_SILU)
+#pragma unroll
+              for (int e = 0; e < 4; ++e) u[e] = silu_f(u[e]);
+            *reinterpret_cast<f32x4*>(xs + b * kn + k) = u;
+          }
+        }
+      }
     }
     __syncthreads();
     for (int kk = lane * 8; kk < kn; kk += 512) {
@@ -350,8 +374,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(int B, int N, int K, const fl
       for (int r = 0; r < GEMV_WROWS; ++r)
         wv[r] = n0 + r < N ? load_bf16x8(W + (int64_t)(n0 + r) * K + k0 + kk) : bf16x8{};
 #pragma unroll
-      for (int b = 0; b < GEMV_MAXB; ++b)
-        if (b < B) {
+      for (int b = 0; b < B; ++b) {
           const f32x4 x0 = *reinterpret_cast<const f32x4*>(xs + b * kn + kk);
           const f32x4 x1 = *reinterpret_cast<const f32x4*>(xs + b * kn + kk + 4);
           const float xv[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
@@ -363,8 +386,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(int B, int N, int K, const fl
     }
   }
 #pragma unroll
-  for (int b = 0; b < GEMV_MAXB; ++b)
-    if (b < B)
+  for (int b = 0; b < B; ++b)
 #pragma unroll
       for (int r = 0; r < GEMV_WROWS; ++r) {
         const float s = wave_sum(acc[b][r]);
@@ -462,8 +484,23 @@ hipError_t launch_gemv(int32_t B, int32_t N, int32_t K, const float* x, int32_t 
                        const float* bias, float* out, hipStream_t s, const int32_t* skip) {
   if (B <= 0 || N <= 0) return hipSuccess;
   if (B > GEMV_MAXB || K % 8 != 0) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(gemv_kernel, dim3((N + GEMV_ROWS - 1) / GEMV_ROWS), dim3(256), 0, s, B, N, K, x, act,
-                     static_cast<const bf16*>(W), bias, out, skip);
+  // columns per pass: all of K when B x K floats fit, else a multiple of 512 (B <= 8: at
+  // least 2048); the LDS is sized to the pass, so small inputs leave room for more
+  // workgroups per CU
+  const int kc = (int64_t)B * K <= GEMV_LDS ? K : (GEMV_LDS / B) & ~511;
+  const dim3 grid((N + GEMV_ROWS - 1) / GEMV_ROWS), block(256);
+  const size_t lds = (size_t)B * kc * sizeof(float);
+  const bf16* w = static_cast<const bf16*>(W);
+  switch (B) {
+    case 1: hipLaunchKernelGGL(gemv_kernel<1>, grid, block, lds, s, N, K, kc, x, act, w, bias, out, skip); break;
+    case 2: hipLaunchKernelGGL(gemv_kernel<2>, grid, block, lds, s, N, K, kc, x, act, w, bias, out, skip); break;
+    case 3: hipLaunchKernelGGL(gemv_kernel<3>, grid, block, lds, s, N, K, kc, x, act, w, bias, out, skip); break;
+    case 4: hipLaunchKernelGGL(gemv_kernel<4>, grid, block, lds, s, N, K, kc, x, act, w, bias, out, skip); break;
+    case 5: hipLaunchKernelGGL(gemv_kernel<5>, grid, block, lds, s, N, K, kc, x, act, w, bias, out, skip); break;
+    case 6: hipLaunchKernelGGL(gemv_kernel<6>, grid, block, lds, s, N, K, kc, x, act, w, bias, out, skip); break;
+    case 7: hipLaunchKernelGGL(gemv_kernel<7>, grid, block, lds, s, N, K, kc, x, act, w, bias, out, skip); break;
+    default: hipLaunchKernelGGL(gemv_kernel<8>, grid, block, lds, s, N, K, kc, x, act, w, bias, out, skip); break;
+  }
   return hipGetLastError();
 }
 
