@@ -26,6 +26,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 MI355X_BF16_DENSE_TFLOPS = 2500.0  # published dense bf16 MFMA peak
+MI355X_FP8_DENSE_TFLOPS = 5000.0  # published dense FP8 MFMA peak
 WORKLOAD = "step_14b"
 
 
@@ -125,10 +126,11 @@ def role_work(wl):
 MI355X_HBM_GBPS = 8000.0  # published HBM3E peak
 
 
-def profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, n_steps):
+def profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, n_steps, mfma_peak=None, **io_kw):
     """Per-role average launch time over n_steps untimed steps that record events around
     every launch of every block, with each role's achieved rate and fraction of its peak
-    (bf16 dense MFMA for GEMMs and attention, HBM for LayerNorm and RoPE)."""
+    (dense MFMA at mfma_peak, bf16's by default, for GEMMs and attention; HBM for LayerNorm
+    and RoPE).  io_kw: extra step inputs (the FP8 KV cache's exponents and scales)."""
     import paper_2602_15922_amd as w
     names = w.binding.BLOCK_EVENT_NAMES
     nk = len(names)
@@ -138,7 +140,7 @@ def profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, n_steps):
     for _ in range(n_steps):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * nk * wl.n_layers)]
         io = w.make_step_io(inp["z"], inp["a"], inp["t"], inp["text"], kcs, vcs, inp["cos"], inp["sin"],
-                            wl.cache_rows, chunks, vv, va, block_events=ev)
+                            wl.cache_rows, chunks, vv, va, block_events=ev, **io_kw)
         if ws is None:
             ws = torch.empty(w.wam_step_workspace_bytes(model, io), dtype=torch.uint8, device="cuda")
         w.wam_dit_step_fwd(model, io, ws)
@@ -153,7 +155,7 @@ def profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, n_steps):
         unit, amount = work[name]
         if unit == "TFLOP/s":
             rate = amount / (ms * 1e-3) / 1e12
-            peak = MI355X_BF16_DENSE_TFLOPS
+            peak = mfma_peak or MI355X_BF16_DENSE_TFLOPS
         else:
             rate = amount / (ms * 1e-3) / 1e9
             peak = MI355X_HBM_GBPS
@@ -308,6 +310,13 @@ def extras(wl, model, keep, kcs, vcs, inp, torch, reps=3):
     out["fp8_attn_kernel_ms"] = round(sum(ev[2 * l].elapsed_time(ev[2 * l + 1]) for l in range(wl.n_layers))
                                       / wl.n_layers, 4)
     assert torch.isfinite(vv).all()
+    # the same step with events around every launch of every block: per-role times of the
+    # FP8 path, MFMA roles against the FP8 dense peak (a role's time includes the row
+    # quantization of its FP8 GEMM's input)
+    roles8 = profiled_roles(wl, model8, k8s, v8s, inp, vv, va, torch, 1, mfma_peak=MI355X_FP8_DENSE_TFLOPS,
+                            k_exps=kes, v_scales=vsc)
+    out["fp8_roles"] = {k: {"ms": v["ms"], "achieved": v["achieved"], "unit": v["unit"], "frac": v["frac"]}
+                        for k, v in roles8.items()}
     del blocks8, model8, ws8, k8s, v8s, kes
     return out
 
