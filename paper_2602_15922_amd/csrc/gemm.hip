@@ -381,12 +381,23 @@ WAM_DEV int xcd_tile(int i, int nblk) {
   return x * per + (x < rem ? x : rem) + j;
 }
 
-// One BM x BN output tile (row tile tm, column tile tn) of g.
-template <typename C, int EPI>
-WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn) {
+// The workgroup's LDS: one array per size, so the tiles of two configurations in one
+// kernel share it.
+template <int BYTES>
+WAM_DEV char* lds_ring() {
+  __shared__ __attribute__((aligned(16))) char buf[BYTES];
+  return buf;
+}
+
+// One BM x BN output tile (row tile tm, column tile tn, columns from col0) of g, with
+// the operand ring and the epilogue's staging in the first STAGES * STAGE of LBYTES
+// bytes of LDS.
+template <typename C, int EPI, int LBYTES = C::STAGES * C::STAGE>
+WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn, int col0) {
+  static_assert(LBYTES >= C::STAGES * C::STAGE, "operand ring does not fit");
   constexpr int BM = C::BM, BN = C::BN, BK = C::BK, S = C::STAGES;
-  __shared__ __attribute__((aligned(16))) char smem[S * C::STAGE];
-  const int m0 = tm * BM, n0 = tn * BN;
+  char* smem = lds_ring<LBYTES>();
+  const int m0 = tm * BM, n0 = col0 + tn * BN;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, w < C::NW
@@ -601,7 +612,16 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn) {
 // once form an 8 x 4 block that shares 8 A panels and 4 W panels in its L2 (instead of
 // ~25 A panels and 2 W panels when all row tiles of a column come first; measured
 // 0-2.5% faster on the step's projections, interleaved launches).
-//
+WAM_DEV void grouped_tile(int slot, int tiles_m, int tiles_n, int& tm, int& tn) {
+  constexpr int GM = 8;
+  const int lid = xcd_tile(slot, tiles_m * tiles_n);
+  const int per = GM * tiles_n, grp = lid / per, first = grp * GM;
+  const int gm = tiles_m - first < GM ? tiles_m - first : GM;
+  const int r = lid - grp * per;
+  tm = first + r % gm;
+  tn = r / gm;
+}
+
 // The workgroups are persistent: one per resident slot, each taking every gridDim.x-th
 // dispatch slot in turn, so a tile's first slices are fetched while the previous tile's
 // output stores drain, without a workgroup launch in between.
@@ -615,7 +635,33 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt(const GemmArgs g, int t
     const int per = GM * tiles_n, grp = lid / per, first = grp * GM;
     const int gm = tiles_m - first < GM ? tiles_m - first : GM;
     const int r = lid - grp * per;
-    gemm_tile<C, EPI>(g, first + r % gm, r / gm);
+    gemm_tile<C, EPI>(g, first + r % gm, r / gm, 0);
+  }
+}
+
+// Two column ranges of one product in one persistent launch: columns [0, tn1 * BN) in
+// C1 tiles, the rest in the shorter C2 tiles, dispatch slots of the first range before
+// the second's.  A single tile height can leave the last round of tiles partly filled
+// (at M = 3152, N = 13824: 702 tiles of 256 rows are 2.74 rounds on 256 CUs, so a third
+// of the workgroups idle through the last one); filling it with the cheaper rounds of
+// shorter tiles balances the workgroups with no split of the K sum.
+template <typename C1, typename C2, int EPI>
+__global__ __launch_bounds__(C1::NT, C1::OCC) void gemm_nt2(const GemmArgs g, int tm1, int tn1, int tm2, int tn2) {
+  static_assert(C1::NT == C2::NT && C1::OCC == C2::OCC && C1::BN == C2::BN && C1::EB == C2::EB,
+                "one workgroup shape for both ranges");
+  if (skip_step(g.skip)) return;
+  constexpr int L1 = C1::STAGES * C1::STAGE, L2 = C2::STAGES * C2::STAGE, LB = L1 > L2 ? L1 : L2;
+  const int t1 = tm1 * tn1, total = t1 + tm2 * tn2;
+  for (int slot = blockIdx.x; slot < total; slot += gridDim.x) {
+    int tm, tn;
+    if (slot < t1) {
+      grouped_tile(slot, tm1, tn1, tm, tn);
+      gemm_tile<C1, EPI, LB>(g, tm, tn, 0);
+    } else {
+      // slot - t1 keeps a workgroup's slots on one residue mod 8, i.e. on one XCD range
+      grouped_tile(slot - t1, tm2, tn2, tm, tn);
+      gemm_tile<C2, EPI, LB>(g, tm, tn, tn1 * C1::BN);
+    }
   }
 }
 
@@ -634,7 +680,7 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_nt_group(const GemmArgs g,
     gl.bias = gg.bias[grp];
     gl.out = gg.out[grp];
     if constexpr (C::EB == 1) gl.w_scale = gg.w_scale[grp];
-    gemm_tile<C, EPI>(gl, r % tiles_m, r / tiles_m);
+    gemm_tile<C, EPI>(gl, r % tiles_m, r / tiles_m, 0);
   }
 }
 
@@ -666,6 +712,27 @@ hipError_t launch_cfg(const GemmArgs& g, const GemmGroup* gg, hipStream_t s) {
     case WAM_EPI_GELU_BF16: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_GELU_BF16>), grid, block, 0, s, g, tm, tn); break;
     case WAM_EPI_RESID_F32: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_RESID_F32>), grid, block, 0, s, g, tm, tn); break;
     default: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_F32>), grid, block, 0, s, g, tm, tn); break;
+  }
+  return hipGetLastError();
+}
+
+// Columns [0, c1 * 256) in Ca tiles, the rest in Cb tiles (both 256 wide).
+template <typename Ca, typename Cb>
+hipError_t launch_cfg2(const GemmArgs& g, int c1, hipStream_t s) {
+  const int tm1 = (g.M + Ca::BM - 1) / Ca::BM, tm2 = (g.M + Cb::BM - 1) / Cb::BM;
+  const int tn2 = (g.N - c1 * Ca::BN + Cb::BN - 1) / Cb::BN;
+  const long t = (long)tm1 * c1 + (long)tm2 * tn2;
+  const int ga = persistent_grid<Ca>(t), gb = persistent_grid<Cb>(t);
+  dim3 grid(ga < gb ? ga : gb), block(Ca::NT);
+  switch (g.epi) {
+    case WAM_EPI_BF16: hipLaunchKernelGGL((gemm_nt2<Ca, Cb, WAM_EPI_BF16>), grid, block, 0, s, g, tm1, c1, tm2, tn2); break;
+    case WAM_EPI_GELU_BF16:
+      hipLaunchKernelGGL((gemm_nt2<Ca, Cb, WAM_EPI_GELU_BF16>), grid, block, 0, s, g, tm1, c1, tm2, tn2);
+      break;
+    case WAM_EPI_RESID_F32:
+      hipLaunchKernelGGL((gemm_nt2<Ca, Cb, WAM_EPI_RESID_F32>), grid, block, 0, s, g, tm1, c1, tm2, tn2);
+      break;
+    default: hipLaunchKernelGGL((gemm_nt2<Ca, Cb, WAM_EPI_F32>), grid, block, 0, s, g, tm1, c1, tm2, tn2); break;
   }
   return hipGetLastError();
 }
@@ -703,17 +770,53 @@ hipError_t launch_any(const GemmArgs& gin, const GemmGroup* gg, hipStream_t s) {
   // Taller tiles are more efficient per flop but coarser.  Measured with launches
   // interleaved, a round of 128x256, 192x256 (8 wavefronts of 96x64, 2-stage ring) and
   // 256x256 tiles (8 wavefronts of 128x64, 2 stages) takes time in the ratio 18 : 26 : 33
-  // for 1 : 1.5 : 2 times the work; take the height whose whole rounds cost least.  At
-  // M = 3152: QKV 1020 tiles of 192 rows in 4 rounds (487 -> 469 us), FFN1 702 of 256 rows
-  // in 3 rounds (480 -> 439 us), O and FFN2 keep 128 rows (500 tiles, 2 rounds).
-  // FP8 takes the same tiles with 128-wide slices (the bytes of a 64-wide bf16 slice).
-  auto rounds = [&](int bm) { return (ng * ((g.M + bm - 1) / bm) * ((g.N + 255) / 256) + cus - 1) / cus; };
-  const long c128 = 18 * rounds(128), c192 = 26 * rounds(192), c256 = 33 * rounds(256);
-  if (c256 < c128 && c256 <= c192) {
+  // for 1 : 1.5 : 2 times the work.  One workgroup per CU for all three, so a workgroup
+  // that runs n tiles of one height costs n times its figure, and the launch costs what
+  // its busiest workgroup does: take the least of that over the three heights and over
+  // the splits of the columns into a taller range and a shorter one (gemm_nt2, whose
+  // first workgroup is always among the busiest: slots are dealt in order and the taller
+  // range comes first).  At M = 3152: QKV (60 column tiles) 1020 tiles of 192 rows in 4
+  // rounds; FFN1 (54 column tiles) 39 columns of 256-row tiles and 15 of 192-row ones,
+  // 2 x 33 + 26 = 92 against 3 x 33 = 99 for 256 rows alone; O and FFN2 keep 128 rows
+  // (500 tiles, 2 rounds).  FP8 takes the same tiles with 128-wide slices (the bytes of
+  // a 64-wide bf16 slice).
+  constexpr int NH = 3;
+  const int height[NH] = {128, 192, 256}, cost[NH] = {18, 26, 33};
+  const long ncol = (g.N + 255) / 256;
+  auto tiles_m = [&](int h) { return (g.M + h - 1) / h; };
+  auto ceil_div = [](long a, long b) { return (a + b - 1) / b; };
+  long one[NH];  // one height for all columns
+  for (int a = 0; a < NH; ++a) one[a] = cost[a] * ceil_div(ng * tiles_m(height[a]) * ncol, cus);
+  int best_a = one[2] < one[0] && one[2] <= one[1] ? 2 : one[1] < one[0] ? 1 : 0, best_b = -1, best_c1 = 0;
+  long best = one[best_a];
+  if (!gg) {  // a split must beat one height by 3%; among equal splits, the least total work
+    long best2 = 0, work2 = 0;
+    for (int a = 1; a < NH; ++a)
+      for (int b = 0; b < a; ++b)
+        for (long c1 = 1; c1 < ncol; ++c1) {
+          const long t1 = tiles_m(height[a]) * c1, t2 = tiles_m(height[b]) * (ncol - c1);
+          const long n1 = ceil_div(t1, cus), n2 = ceil_div(t1 + t2, cus) - n1;
+          const long c = cost[a] * n1 + cost[b] * n2, work = cost[a] * t1 + cost[b] * t2;
+          if (100 * c < 97 * best && (best_b < 0 || c < best2 || (c == best2 && work < work2))) {
+            best2 = c; work2 = work; best_a = a; best_b = b; best_c1 = (int)c1;
+          }
+        }
+  }
+  if (best_b >= 0) {
+    if (g.fp8) {
+      if (best_a == 2 && best_b == 1) return launch_cfg2<Cfg<256, 256, 128, 2, 2, 4, 2, 1>, Cfg<192, 256, 128, 2, 2, 4, 2, 1>>(g, best_c1, s);
+      if (best_a == 2) return launch_cfg2<Cfg<256, 256, 128, 2, 2, 4, 2, 1>, Cfg<128, 256, 128, 3, 2, 4, 2, 1>>(g, best_c1, s);
+      return launch_cfg2<Cfg<192, 256, 128, 2, 2, 4, 2, 1>, Cfg<128, 256, 128, 3, 2, 4, 2, 1>>(g, best_c1, s);
+    }
+    if (best_a == 2 && best_b == 1) return launch_cfg2<Cfg<256, 256, 64, 2, 2, 4, 2>, Cfg<192, 256, 64, 2, 2, 4, 2>>(g, best_c1, s);
+    if (best_a == 2) return launch_cfg2<Cfg<256, 256, 64, 2, 2, 4, 2>, Cfg<128, 256, 64, 3, 2, 4, 2>>(g, best_c1, s);
+    return launch_cfg2<Cfg<192, 256, 64, 2, 2, 4, 2>, Cfg<128, 256, 64, 3, 2, 4, 2>>(g, best_c1, s);
+  }
+  if (best_a == 2) {
     if (g.fp8) return launch_cfg<Cfg<256, 256, 128, 2, 2, 4, 2, 1>>(g, gg, s);
     return launch_cfg<Cfg<256, 256, 64, 2, 2, 4, 2>>(g, gg, s);
   }
-  if (c192 < c128) {
+  if (best_a == 1) {
     if (g.fp8) return launch_cfg<Cfg<192, 256, 128, 2, 2, 4, 2, 1>>(g, gg, s);
     return launch_cfg<Cfg<192, 256, 64, 2, 2, 4, 2>>(g, gg, s);
   }

@@ -51,7 +51,7 @@ def test_quantize_rows_fp8(M, K):
     assert np.array_equal(decode(q[:, :K].contiguous()), ref_q)
 
 
-GEMM_SHAPES = [(300, 200, 144), (3152, 5192, 528), (17, 16, 16)]
+GEMM_SHAPES = [(300, 200, 144), (3152, 5192, 528), (17, 16, 16), (3152, 13700, 144)]  # the last: two column ranges
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
