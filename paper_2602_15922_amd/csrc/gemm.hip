@@ -767,21 +767,26 @@ hipError_t launch_any(const GemmArgs& gin, const GemmGroup* gg, hipStream_t s) {
     if (g.fp8) return launch_cfg<Cfg<128, 128, 128, 2, 2, 2, 2, 1>>(g, gg, s);
     return launch_cfg<Cfg<128, 128, 64, 2, 2, 2, 2>>(g, gg, s);
   }
-  // Taller tiles are more efficient per flop but coarser.  Measured with launches
-  // interleaved, a round of 128x256, 192x256 (8 wavefronts of 96x64, 2-stage ring) and
-  // 256x256 tiles (8 wavefronts of 128x64, 2 stages) takes time in the ratio 18 : 26 : 33
-  // for 1 : 1.5 : 2 times the work.  One workgroup per CU for all three, so a workgroup
-  // that runs n tiles of one height costs n times its figure, and the launch costs what
-  // its busiest workgroup does: take the least of that over the three heights and over
-  // the splits of the columns into a taller range and a shorter one (gemm_nt2, whose
-  // first workgroup is always among the busiest: slots are dealt in order and the taller
-  // range comes first).  At M = 3152: QKV (60 column tiles) 1020 tiles of 192 rows in 4
-  // rounds; FFN1 (54 column tiles) 39 columns of 256-row tiles and 15 of 192-row ones,
-  // 2 x 33 + 26 = 92 against 3 x 33 = 99 for 256 rows alone; O and FFN2 keep 128 rows
-  // (500 tiles, 2 rounds).  FP8 takes the same tiles with 128-wide slices (the bytes of
-  // a 64-wide bf16 slice).
+  // Cost of a round of tiles (one per CU), from launches at K = 5120 whose weights are not
+  // in the last-level cache (as in a model step, where every block brings its own):
+  // 128x256 tiles (8 wavefronts of 64x64, 3-stage ring) ~72 us, 192x256 (8 of 96x64, 2
+  // stages) ~110 us, 256x256 (8 of 128x64, 2 stages) ~124 us.  With warm weights the
+  // 192-row tiles cost ~10% less, which once made them look best for QKV; with cold ones
+  // a tile that holds only one slice in flight waits on HBM more often, and the 3-stage
+  // ring and the taller tiles (fewer re-reads per flop) lose less.  One workgroup per CU
+  // for all three, so a workgroup that runs n tiles of one height costs n times its
+  // figure, and the launch costs what its busiest workgroup does: take the least of that
+  // over the three heights and over the splits of the columns into a taller range and a
+  // shorter one (gemm_nt2, whose first workgroup is always among the busiest: slots are
+  // dealt in order and the taller range comes first).  At M = 3152: QKV (60 column
+  // tiles) 19 columns of 256-row tiles and 41 of 128-row ones (124 + 4 x 72 = 412 against
+  // 440 for 192 rows alone: 416 against 441 us measured, cold); FFN1 (54 column tiles) 39
+  // columns of 256-row tiles and 15 of 192-row ones (2 x 124 + 110 = 358 against 372 for
+  // 256 rows alone: 369 against 383 us); O, cross-Q, cross-O and FFN2 (20 column tiles)
+  // 128-row tiles (500 in 2 rounds).  FP8 takes the same tiles with 128-wide slices (the
+  // bytes of a 64-wide bf16 slice).
   constexpr int NH = 3;
-  const int height[NH] = {128, 192, 256}, cost[NH] = {18, 26, 33};
+  const int height[NH] = {128, 192, 256}, cost[NH] = {72, 110, 124};
   const long ncol = (g.N + 255) / 256;
   auto tiles_m = [&](int h) { return (g.M + h - 1) / h; };
   auto ceil_div = [](long a, long b) { return (a + b - 1) / b; };

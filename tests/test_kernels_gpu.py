@@ -79,8 +79,8 @@ GEMM_SHAPES = [
     (3152, 5100, 520),   # 128x256 tiles (500 of them, 2 rounds), ragged M, N and K
     (17, 16, 16),        # the action embedding's K
     (130, 203, 72),      # N % 4 != 0: the last column group is stored element by element
-    (1000, 12700, 520),  # 256x256 tiles (200, one round, beat 300 of 192 rows), ragged M, N and K
-    (570, 15300, 136),   # 192x256 tiles (180 of them beat 300 of 128x256), ragged M, N and K
+    (1000, 12700, 520),  # 256x256 tiles (200, one round), ragged M, N and K
+    (570, 15300, 136),   # 192x256 tiles (180, one round, against 300 of 128 rows), ragged M, N and K
     (3152, 13700, 136),  # two column ranges in one launch: 39 columns of 256-row tiles, 15 of 192
     (1347, 16590, 72),   # two column ranges: 256- and 128-row tiles
     (903, 16590, 136),   # two column ranges: 192- and 128-row tiles
