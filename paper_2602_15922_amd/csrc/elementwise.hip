@@ -156,6 +156,49 @@ __global__ __launch_bounds__(256) void quant_rows_kernel(int M, int K, const bf1
   }
 }
 
+// The same for rows of at most 512 * NC values: the row is held in registers (NC 16-byte
+// loads per lane, all issued before the first is used) and read from memory once.
+template <int NC>
+__global__ __launch_bounds__(256) void quant_rows_reg_kernel(int M, int K, const bf16* __restrict__ x, int64_t ldx,
+                                                             uint8_t* __restrict__ q, int64_t ldq,
+                                                             float* __restrict__ scale, const int32_t* skip) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + w;
+  if (row >= M || skip_step(skip)) return;
+  const bf16* xr = x + (int64_t)row * ldx;
+  bf16x8 v[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int k = c * 512 + lane * 8;
+    v[c] = k < K ? load_bf16x8(xr + k) : bf16x8{};
+  }
+  float amax = 0.f;
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf((float)v[c][j]));
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+  const float inv = amax > 0.f ? 448.0f / amax : 1.0f;
+  if (lane == 0) scale[row] = amax > 0.f ? amax / 448.0f : 1.0f;
+  uint8_t* qr = q + (int64_t)row * ldq;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int k = c * 512 + lane * 8;
+    if (k < K) {
+      float f[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) f[j] = fminf(fmaxf((float)v[c][j] * inv, -448.0f), 448.0f);
+      int lo = 0, hi = 0;
+      lo = __builtin_amdgcn_cvt_pk_fp8_f32(f[0], f[1], lo, false);
+      lo = __builtin_amdgcn_cvt_pk_fp8_f32(f[2], f[3], lo, true);
+      hi = __builtin_amdgcn_cvt_pk_fp8_f32(f[4], f[5], hi, false);
+      hi = __builtin_amdgcn_cvt_pk_fp8_f32(f[6], f[7], hi, true);
+      *reinterpret_cast<u32x2*>(qr + k) = u32x2{(uint32_t)lo, (uint32_t)hi};
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------------
 // FP8 operands of the attention.  MX-style blocks: 32 consecutive elements share the
 // scale 2^e, e the smallest integer with max|x| <= 448 * 2^e (clamped to [-127, 127];
@@ -468,8 +511,16 @@ hipError_t launch_adaln_fold(const AdalnFoldArgs& a, hipStream_t s) {
 hipError_t launch_quant_rows(int32_t M, int32_t K, const void* x, int64_t ldx, void* q, int64_t ldq, float* scale,
                              hipStream_t s, const int32_t* skip) {
   if (M == 0) return hipSuccess;
-  hipLaunchKernelGGL(quant_rows_kernel, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, s, M, K,
-                     static_cast<const bf16*>(x), ldx, static_cast<uint8_t*>(q), ldq, scale, skip);
+  const dim3 grid((unsigned)((M + 3) / 4)), block(256);
+  const bf16* xb = static_cast<const bf16*>(x);
+  uint8_t* qb = static_cast<uint8_t*>(q);
+  // register tiers: up to 2048 / 4096 / 6144 / 14336 values per row (the 14B model's
+  // projection inputs are 5120 and 13824 wide); longer rows take the two-pass kernel
+  if (K <= 2048) hipLaunchKernelGGL(quant_rows_reg_kernel<4>, grid, block, 0, s, M, K, xb, ldx, qb, ldq, scale, skip);
+  else if (K <= 4096) hipLaunchKernelGGL(quant_rows_reg_kernel<8>, grid, block, 0, s, M, K, xb, ldx, qb, ldq, scale, skip);
+  else if (K <= 6144) hipLaunchKernelGGL(quant_rows_reg_kernel<12>, grid, block, 0, s, M, K, xb, ldx, qb, ldq, scale, skip);
+  else if (K <= 14336) hipLaunchKernelGGL(quant_rows_reg_kernel<28>, grid, block, 0, s, M, K, xb, ldx, qb, ldq, scale, skip);
+  else hipLaunchKernelGGL(quant_rows_kernel, grid, block, 0, s, M, K, xb, ldx, qb, ldq, scale, skip);
   return hipGetLastError();
 }
 

@@ -32,7 +32,9 @@ def expected_quant(x_bf16):
     return oracle.fp8.round_e4m3(xs.astype(np.float64)), scale
 
 
-@pytest.mark.parametrize("M,K", [(37, 520), (5, 8), (130, 5120)])
+# one shape per register tier of the quantizer (rows up to 2048 / 4096 / 6144 / 14336 wide)
+# and one row longer than all of them (the two-pass kernel)
+@pytest.mark.parametrize("M,K", [(37, 520), (5, 8), (9, 3000), (130, 5120), (33, 13824), (4, 16392)])
 def test_quantize_rows_fp8(M, K):
     import torch
     w = lib()
