@@ -219,6 +219,19 @@ WAM_DEV void mfma_step(const Frag<C> (&fa)[C::TM], const Frag<C> (&fb)[C::TN], f
     }
 }
 
+// FP8 tiles: an empty asm that reads and writes every accumulator after a k-step's MFMAs,
+// so they stay ahead of what follows in program order.  Without it the compiler sinks
+// them below the next k-step's fragment reads and the slice's barrier, keeps three sets
+// of 32-byte fragments live and spills (the 256x256 tiles' old loop needed 144 bytes of
+// scratch; the 128x256 tiles now take 201 registers instead of 254).
+template <typename C>
+WAM_DEV void pin_acc(f32x16 (*acc)[C::TN]) {
+#pragma unroll
+  for (int a = 0; a < C::TM; ++a)
+#pragma unroll
+    for (int b = 0; b < C::TN; ++b) asm volatile("" : "+v"(acc[a][b]));
+}
+
 // Instruction order of one k-step: one LDS read (while any of the NDS are left) and one
 // direct global load (while any of the NVM are left) ahead of each of its NMF MFMAs, so
 // the reads for the next k-step and the next slice's prefetch issue between the MFMAs.
@@ -256,6 +269,7 @@ WAM_DEV void slice_steady(char* smem, const GemmLane<C>& L, int t, int K, f32x16
     read_frags<C>(smem, CUR, L, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
     mfma_step<C>(fa[ks & 1], fb[ks & 1], acc);
     interleave_step<NMF, NR, 0>();
+    if constexpr (C::EB == 1) pin_acc<C>(acc);
     __builtin_amdgcn_sched_barrier(0);
   }
   WAM_WAIT_LGKMCNT0();
@@ -266,6 +280,7 @@ WAM_DEV void slice_steady(char* smem, const GemmLane<C>& L, int t, int K, f32x16
   read_frags<C>(smem, (CUR + 1) % S, L, 0, fa[KS & 1], fb[KS & 1]);
   mfma_step<C>(fa[(KS - 1) & 1], fb[(KS - 1) & 1], acc);
   interleave_step<NMF, NR, NI>();
+  if constexpr (C::EB == 1) pin_acc<C>(acc);
   __builtin_amdgcn_sched_barrier(0);
 }
 
@@ -288,6 +303,7 @@ WAM_DEV void slice_tail(char* smem, const GemmLane<C>& L, int t, int nk, int K, 
   for (int ks = 0; ks < KS - 1; ++ks) {
     read_frags<C>(smem, cur, L, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
     mfma_step<C>(fa[ks & 1], fb[ks & 1], acc);
+    if constexpr (C::EB == 1) pin_acc<C>(acc);
     __builtin_amdgcn_sched_barrier(0);
   }
   if (t + 1 < nk) {
@@ -305,70 +321,8 @@ WAM_DEV void slice_tail(char* smem, const GemmLane<C>& L, int t, int nk, int K, 
     read_frags<C>(smem, (t + 1) % S, L, 0, fa[KS & 1], fb[KS & 1]);
   }
   mfma_step<C>(fa[(KS - 1) & 1], fb[(KS - 1) & 1], acc);
+  if constexpr (C::EB == 1) pin_acc<C>(acc);
   __builtin_amdgcn_sched_barrier(0);
-}
-
-// FP8 operands keep the earlier main loop: one barrier at the start of each slice, then
-// its MFMAs with the next k-step's fragments in flight.  Their 32-byte fragments
-// double-buffered across the slice boundary (as the bf16 loop does) exceed the register
-// budget of the 8-wavefront tiles.  With `cur` a compile-time constant every LDS read is
-// a lane offset plus an immediate.
-template <typename C>
-WAM_DEV void mma_slice_fp8(const char* smem, int cur, const GemmLane<C>& L, f32x16 (*acc)[C::TN]) {
-  static_assert(C::EB == 1, "FP8 operands");
-  const char* As = smem + cur * C::STAGE;
-  const char* Bs = As + C::BM * C::ROWB;
-  constexpr int RB = 32 * C::ROWB;  // bytes of 32 LDS rows
-  {
-    // FP8: a lane's fragment is 32 consecutive k (two 16-byte chunks) of its row
-    i32x8 fa[2][C::TM], fb[2][C::TN];
-    auto frag = [&](const char* base) {
-      const u32x4 lo = *reinterpret_cast<const u32x4*>(base);
-      return lo;
-    };
-    auto read_frags = [&](int ks, int slot) {
-#pragma unroll
-      for (int a = 0; a < C::TM; ++a) {
-        const u32x4 lo = frag(As + L.fa_off[ks][0] + a * RB), hi = frag(As + L.fa_off[ks][1] + a * RB);
-        fa[slot][a] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
-      }
-#pragma unroll
-      for (int b = 0; b < C::TN; ++b) {
-        const u32x4 lo = frag(Bs + L.fb_off[ks][0] + b * RB), hi = frag(Bs + L.fb_off[ks][1] + b * RB);
-        fb[slot][b] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
-      }
-    };
-    read_frags(0, 0);
-#pragma unroll
-    for (int ks = 0; ks < C::KS; ++ks) {
-      if (ks + 1 < C::KS) read_frags(ks + 1, (ks + 1) & 1);
-#pragma unroll
-      for (int a = 0; a < C::TM; ++a)
-#pragma unroll
-        for (int b = 0; b < C::TN; ++b) acc[a][b] = mfma32_fp8(fa[ks & 1][a], fb[ks & 1][b], acc[a][b]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  }
-}
-
-// One main-loop iteration in steady state (slice kt in stage CUR; one younger slice in
-// flight when S = 3, S-2 in general): wait for slice kt, barrier, prefetch slice
-// kt+S-1 into the stage freed by slice kt-1, then the slice's MFMAs.
-template <typename C, int CUR>
-WAM_DEV void steady_step_fp8(char* smem, const GemmLane<C>& L, int kt, int K, f32x16 (*acc)[C::TN]) {
-  constexpr int S = C::STAGES, NI = C::NIA + C::NIB;
-  WAM_WAIT_VMCNT((S - 2) * NI);
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-  fetch_slice<C>(smem, (CUR + S - 1) % S, L, kt + S - 1, K);
-  mma_slice_fp8<C>(smem, CUR, L, acc);
-}
-
-template <typename C, int CUR>
-WAM_DEV void steady_group_fp8(char* smem, const GemmLane<C>& L, int kt, int K, f32x16 (*acc)[C::TN]) {
-  steady_step_fp8<C, CUR>(smem, L, kt + CUR, K, acc);
-  if constexpr (CUR + 1 < C::STAGES) steady_group_fp8<C, CUR + 1>(smem, L, kt, K, acc);
 }
 
 // XCD-aware remap: the hardware deals workgroups round-robin over 8 XCDs; give each
@@ -447,59 +401,29 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn, int col0) {
 
   const int nk = (g.K + BK - 1) / BK;
   constexpr int NI = C::NIA + C::NIB;  // loads per slice per wave
-  if constexpr (C::EB == 2) {
-    static_assert(C::KS % 2 == 0, "fragment slots alternate per k-step and slice");
-    // prologue: the first S slices in flight, slice 0 landed and visible, its k-step 0 read
+  static_assert(C::KS % 2 == 0, "fragment slots alternate per k-step and slice");
+  // prologue: the first S slices in flight, slice 0 landed and visible, its k-step 0 read
 #pragma unroll
-    for (int p = 0; p < S; ++p)
-      if (p < nk) fetch_slice<C>(smem, p, L, p, g.K);
-    {
-      const int younger = nk - 1 < S - 1 ? nk - 1 : S - 1;
-      if (younger >= 2) WAM_WAIT_VMCNT(2 * NI);
-      else if (younger == 1) WAM_WAIT_VMCNT(NI);
-      else WAM_WAIT_VMCNT(0);
-      if (BK > g.K) {
-        zero_tail<C>(smem, 0, L, 0, g.K, lane);
-        WAM_WAIT_LGKMCNT0();
-      }
-      block_barrier();
+  for (int p = 0; p < S; ++p)
+    if (p < nk) fetch_slice<C>(smem, p, L, p, g.K);
+  {
+    const int younger = nk - 1 < S - 1 ? nk - 1 : S - 1;
+    if (younger >= 2) WAM_WAIT_VMCNT(2 * NI);
+    else if (younger == 1) WAM_WAIT_VMCNT(NI);
+    else WAM_WAIT_VMCNT(0);
+    if (BK > g.K) {
+      zero_tail<C>(smem, 0, L, 0, g.K, lane);
+      WAM_WAIT_LGKMCNT0();
     }
-    Frag<C> fa[2][C::TM], fb[2][C::TN];
-    read_frags<C>(smem, 0, L, 0, fa[0], fb[0]);
-    int kt = 0;
-    // steady state, S slices per iteration so each stage index is a constant: every slice
-    // here has a successor, prefetches a slice < nk, and waits for a full slice
-    for (; kt + 2 * S + 1 <= nk && (kt + 2 * S + 1) * BK <= g.K; kt += S) steady_group<C, 0>(smem, L, kt, g.K, acc, fa, fb);
-    for (; kt < nk; ++kt) slice_tail<C>(smem, L, kt, nk, g.K, lane, acc, fa, fb);
-  } else {
-#pragma unroll
-    for (int p = 0; p < S - 1; ++p)
-      if (p < nk) fetch_slice<C>(smem, p, L, p, g.K);
-    int kt = 0;
-    // steady state, S slices per iteration so each stage index is a constant; every
-    // slice here has S-2 younger slices in flight at its wait and prefetches a slice < nk
-    for (; kt + 2 * S - 2 < nk; kt += S) steady_group_fp8<C, 0>(smem, L, kt, g.K, acc);
-    // the remaining slices (fewer younger slices in flight; the last may run past K)
-    for (; kt < nk; ++kt) {
-      const int younger = (nk - 1 - kt) < (S - 2) ? (nk - 1 - kt) : (S - 2);
-      if (younger >= 2) WAM_WAIT_VMCNT(2 * NI);
-      else if (younger == 1) WAM_WAIT_VMCNT(NI);
-      else WAM_WAIT_VMCNT(0);
-      if ((kt + 1) * BK > g.K) {
-        zero_tail<C>(smem, kt % S, L, kt, g.K, lane);
-        WAM_WAIT_LGKMCNT0();
-      }
-      // Slice kt is visible to all waves and slice kt-1's stage is free once every wave
-      // is here: each wave has waited for its own loads of slice kt above, and its reads
-      // of slice kt-1 were consumed by its MFMAs.  A plain s_barrier (the __syncthreads
-      // fence would also wait for the prefetched slices still in flight).
-      asm volatile("" ::: "memory");
-      __builtin_amdgcn_s_barrier();
-      asm volatile("" ::: "memory");
-      if (kt + S - 1 < nk) fetch_slice<C>(smem, (kt + S - 1) % S, L, kt + S - 1, g.K);
-      mma_slice_fp8<C>(smem, kt % S, L, acc);
-    }
+    block_barrier();
   }
+  Frag<C> fa[2][C::TM], fb[2][C::TN];
+  read_frags<C>(smem, 0, L, 0, fa[0], fb[0]);
+  int kt = 0;
+  // steady state, S slices per iteration so each stage index is a constant: every slice
+  // here has a successor, prefetches a slice < nk, and waits for a full slice
+  for (; kt + 2 * S + 1 <= nk && (kt + 2 * S + 1) * BK <= g.K; kt += S) steady_group<C, 0>(smem, L, kt, g.K, acc, fa, fb);
+  for (; kt < nk; ++kt) slice_tail<C>(smem, L, kt, nk, g.K, lane, acc, fa, fb);
   __syncthreads();  // all waves done with the operand ring before it is reused
 
   // ---- epilogue: each wave stages 32 rows x WCOLS of its tile through LDS (reusing
