@@ -217,7 +217,16 @@ WAM_DEV void attn_tile(const char* Ks, const char* Vs, const bf16x8* qf, f32x16*
                        int row_kend, int hh) {
   constexpr int MT = DH / 32;
   f32x16 s[2] = {f32x16{}, f32x16{}};
+  // The wave raises its issue priority for the score MFMAs only: while it runs them, the
+  // SIMD's other wave, in its softmax or P.V, fills the gaps of this chain instead of
+  // delaying it, and the scores the softmax waits on come out sooner.  Measured with
+  // launches interleaved, outputs bit for bit equal: 980 -> 934 us alone, 0.953 -> 0.918 ms
+  // per launch inside the step.  Held through the softmax as well: 1.7% faster alone; two
+  // levels (scores 2, P.V 1): 1.3% faster; raised for P.V only: 0.4% slower; for the
+  // scores and P.V: 0.9% slower.
+  __builtin_amdgcn_s_setprio(1);
   scores_tile<DH>(Ks, kofs, qf, s);
+  __builtin_amdgcn_s_setprio(0);
   if (MASK) {
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt)

@@ -111,6 +111,10 @@ WAM_DEV void attn_tile(const char* st, const i32x8* qf, const int* qsc, f32x16* 
   const char* Vs = st + KT;
   const char* Es = st + 2 * KT;
   f32x16 s[2] = {f32x16{}, f32x16{}};
+  // The wave raises its issue priority for the score MFMAs only (as the bf16 kernel does):
+  // 0.645 -> 0.635 ms per launch inside the FP8 step, against the priority raised for the
+  // row sum and P.V as well (0.69 -> 0.67 ms against none).
+  __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int nt = 0; nt < 2; ++nt) {
     const unsigned kw = *reinterpret_cast<const unsigned*>(Es + (32 * nt + l32) * 4);
@@ -123,6 +127,7 @@ WAM_DEV void attn_tile(const char* st, const i32x8* qf, const int* qsc, f32x16* 
       s[nt] = mfma_f8(kf, qf[ks], s[nt], ksc, qsc[ks]);
     }
   }
+  __builtin_amdgcn_s_setprio(0);
   if (MASK) {
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt)
