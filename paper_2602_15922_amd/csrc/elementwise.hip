@@ -94,6 +94,88 @@ __global__ __launch_bounds__(LN_ROWS * 64, NV <= 20 ? 4 : 2) void ln_mod_kernel(
     }
 }
 
+// The same with 8 consecutive columns per lane (d a multiple of 512): two adjacent 16-byte
+// loads and one 16-byte store of 8 bf16 per lane and chunk, half the store instructions.
+template <int NC>
+__global__ __launch_bounds__(LN_ROWS * 64, NC <= 10 ? 4 : 2) void ln_mod8_kernel(const LnArgs a, int blocks_per_batch,
+                                                                             int seg, int seg_blocks) {
+  extern __shared__ __attribute__((aligned(16))) float PQ[];  // [2][d]
+  if (skip_step(a.skip)) return;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int b = blockIdx.x / blocks_per_batch, j = blockIdx.x % blocks_per_batch;
+  const bool second = j >= seg_blocks;
+  const int rloc = second ? seg + (j - seg_blocks) * LN_ROWS + w : j * LN_ROWS + w;
+  const int rend = second ? a.rows_per_batch : seg;
+  const int d = a.d, nc = d >> 9;
+  const int64_t mb = (int64_t)b * a.mod_stride + (second ? a.alt_off : 0);
+  const bool active = rloc < rend;
+  const int64_t row = (int64_t)b * a.rows_per_batch + (active ? rloc : rend - 1);
+  const float* xr = a.x + row * d;
+  f32x4 v[NC][2];
+#pragma unroll
+  for (int i = 0; i < NC; ++i)
+    if (i < nc) {
+      const float* p = xr + (i * 64 + lane) * 8;
+      v[i][0] = *reinterpret_cast<const f32x4*>(p);
+      v[i][1] = *reinterpret_cast<const f32x4*>(p + 4);
+    }
+  float* P = PQ;
+  float* Q = PQ + d;
+  for (int c = threadIdx.x * 4; c < d; c += LN_ROWS * 256) {
+    f32x4 g = {1.f, 1.f, 1.f, 1.f}, bt = {0.f, 0.f, 0.f, 0.f}, sc = {0.f, 0.f, 0.f, 0.f}, sh = {0.f, 0.f, 0.f, 0.f};
+    if (a.gamma) g = *reinterpret_cast<const f32x4*>(a.gamma + c);
+    if (a.beta) bt = *reinterpret_cast<const f32x4*>(a.beta + c);
+    if (a.scale_a) sc += *reinterpret_cast<const f32x4*>(a.scale_a + c);
+    if (a.scale_v) sc += *reinterpret_cast<const f32x4*>(a.scale_v + mb + c);
+    if (a.shift_a) sh += *reinterpret_cast<const f32x4*>(a.shift_a + c);
+    if (a.shift_v) sh += *reinterpret_cast<const f32x4*>(a.shift_v + mb + c);
+    const f32x4 one = {1.f, 1.f, 1.f, 1.f};
+    *reinterpret_cast<f32x4*>(P + c) = g * (one + sc);
+    *reinterpret_cast<f32x4*>(Q + c) = bt * (one + sc) + sh;
+  }
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));  // lgkmcnt(0) only
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  if (!active) return;
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < NC; ++i)
+    if (i < nc)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) s += (v[i][h][0] + v[i][h][1]) + (v[i][h][2] + v[i][h][3]);
+  const float mean = wave_sum(s) / (float)d;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < NC; ++i)
+    if (i < nc)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const float t = v[i][h][k] - mean;
+          q += t * t;
+        }
+  const float rstd = rsqrtf(wave_sum(q) / (float)d + a.eps);
+  bf16* hr = static_cast<bf16*>(a.h) + row * d;
+#pragma unroll
+  for (int i = 0; i < NC; ++i)
+    if (i < nc) {
+      const int col = (i * 64 + lane) * 8;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const f32x4 pp = *reinterpret_cast<const f32x4*>(P + col + 4 * h);
+        const f32x4 qq = *reinterpret_cast<const f32x4*>(Q + col + 4 * h);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[i][h][k] = (v[i][h][k] - mean) * rstd * pp[k] + qq[k];
+      }
+      bf16x8 o;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) o[k] = (bf16)v[i][k >> 2][k & 3];
+      *reinterpret_cast<bf16x8*>(hr + col) = o;
+    }
+}
+
 // One thread per 4 columns of one (layer, norm, sample, segment): the shift and scale
 // sums of the AdaLN modulation (the same fp32 additions the LayerNorm performs).
 __global__ __launch_bounds__(256) void adaln_fold_kernel(const AdalnFoldArgs a) {
@@ -493,6 +575,11 @@ hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s) {
   const dim3 grid((unsigned)(B * bpb)), block(LN_ROWS * 64);
   const size_t lds = (size_t)2 * a.d * sizeof(float);  // d <= 8192: at most 64 KB
   const int nv = a.d / 256;
+  if (a.d % 512 == 0 && a.d <= 5120) {  // 8 columns per lane (d up to 5120: 80 values per lane)
+    if (a.d <= 2048) hipLaunchKernelGGL(ln_mod8_kernel<4>, grid, block, lds, s, a, bpb, seg, sb0);
+    else hipLaunchKernelGGL(ln_mod8_kernel<10>, grid, block, lds, s, a, bpb, seg, sb0);
+    return hipGetLastError();
+  }
   if (nv <= 2) hipLaunchKernelGGL(ln_mod_kernel<2>, grid, block, lds, s, a, bpb, seg, sb0);
   else if (nv <= 8) hipLaunchKernelGGL(ln_mod_kernel<8>, grid, block, lds, s, a, bpb, seg, sb0);
   else if (nv <= 20) hipLaunchKernelGGL(ln_mod_kernel<20>, grid, block, lds, s, a, bpb, seg, sb0);
