@@ -570,6 +570,20 @@ wam_status wam_gemm_bf16(const wam_gemm_desc* g, hipStream_t stream);
  * ------------------------------------------------------------------------------ */
 wam_status wam_quantize_rows_fp8(int32_t M, int32_t K, const void* x, int64_t ldx, void* q,
                                  int64_t ldq, float* scale, hipStream_t stream);
+
+/* wam_adaln_ln_mod_fp8: the LayerNorm of wam_adaln_ln_mod (same arguments and arithmetic)
+ * whose bf16 output rows are not stored but quantized as wam_quantize_rows_fp8 would
+ * quantize them: the E4M3 codes into q [B*rows_per_batch][ldq bytes] (ldq >= d, a multiple
+ * of 16) and the row scales into scale [B*rows_per_batch], bit for bit the two calls' result,
+ * in one pass that writes a byte per element.  This is how an FP8 projection's input is
+ * made when the LayerNorm output feeds nothing else (the paper quantizes the DiT's
+ * projections to FP8 for deployment, Section 3.2.4, Appendix D.2).  d must be a multiple of
+ * 512 in [512, 5120] (else WAM_EUNSUPPORTED). */
+wam_status wam_adaln_ln_mod_fp8(int32_t B, int32_t rows_per_batch, int32_t d, float eps,
+                                const float* x, const float* gamma, const float* beta,
+                                const float* shift_a, const float* shift_v,
+                                const float* scale_a, const float* scale_v, int64_t mod_stride,
+                                void* q, int64_t ldq, float* scale, hipStream_t stream);
 wam_status wam_gemm_fp8(const wam_gemm_desc* g, const float* a_scale, const float* w_scale,
                         hipStream_t stream);
 

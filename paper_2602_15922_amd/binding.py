@@ -33,7 +33,7 @@ EXPORTED = (
     "wam_embed_workspace_bytes", "wam_embed_fwd", "wam_head_workspace_bytes", "wam_head_fwd",
     "wam_chunk_positions", "wam_rope_tables", "wam_attn_blockcausal_fp8", "wam_quantize_mx_fp8",
     "wam_quantize_scaled_fp8", "wam_rope_qkv_fp8", "wam_unipc_plan", "wam_unipc_step",
-    "wam_cosine_similarity_noalloc",
+    "wam_cosine_similarity_noalloc", "wam_adaln_ln_mod_fp8",
 )
 
 _vp, _fp, _i32, _i64, _sz = C.c_void_p, C.POINTER(C.c_float), C.c_int32, C.c_int64, C.c_size_t
@@ -173,6 +173,8 @@ def lib():
         L.wam_gemm_bf16.argtypes = [C.POINTER(wam_gemm_desc), _vp]
         L.wam_gemm_fp8.argtypes = [C.POINTER(wam_gemm_desc), _vp, _vp, _vp]
         L.wam_quantize_rows_fp8.argtypes = [_i32, _i32, _vp, _i64, _vp, _i64, _vp, _vp]
+        L.wam_adaln_ln_mod_fp8.argtypes = [_i32, _i32, _i32, C.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64,
+                                           _vp, _i64, _vp, _vp]
         L.wam_embed_fwd.argtypes = [C.POINTER(wam_model), _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp,
                                     _vp, _sz, _vp]
         L.wam_head_fwd.argtypes = [C.POINTER(wam_model), _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp,
@@ -350,6 +352,18 @@ def wam_adaln_ln_mod(x, h, eps, rows_per_batch, gamma=None, beta=None, shift_a=N
     B = rows // rows_per_batch if rows_per_batch else 0
     _check(lib().wam_adaln_ln_mod(B, rows_per_batch, d, eps, _p(x), _p(gamma), _p(beta), _p(shift_a),
                                   _p(shift_v), _p(scale_a), _p(scale_v), mod_stride, _p(h), _stream(stream)))
+
+
+def wam_adaln_ln_mod_fp8(x, q, scale, eps, rows_per_batch, gamma=None, beta=None, shift_a=None, shift_v=None,
+                         scale_a=None, scale_v=None, mod_stride=0, stream=None):
+    """The LayerNorm of wam_adaln_ln_mod written as E4M3 codes q [rows, >=d] uint8 (row stride
+    from the tensor) and row scales scale [rows] fp32."""
+    d = x.shape[-1]
+    rows = x.numel() // d
+    B = rows // rows_per_batch if rows_per_batch else 0
+    _check(lib().wam_adaln_ln_mod_fp8(B, rows_per_batch, d, eps, _p(x), _p(gamma), _p(beta), _p(shift_a),
+                                      _p(shift_v), _p(scale_a), _p(scale_v), mod_stride, _p(q), q.stride(0),
+                                      _p(scale), _stream(stream)))
 
 
 def wam_rope_qkv(qkv, cos_t, sin_t, q_out, k_cache, v_cache, row0, H, Dh, stream=None):

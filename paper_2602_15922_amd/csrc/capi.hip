@@ -328,6 +328,22 @@ wam_status proj(const wam_gemm_desc& g0, const void* w8, const float* s8, char* 
   return gemm_checked(g, s, gate_split, gate_alt, qs, s8);
 }
 
+// An FP8 projection whose activation rows the LayerNorm before it already wrote as E4M3
+// codes (row stride K rounded up to 16) and row scales.
+wam_status proj_q8(const wam_gemm_desc& g0, const void* w8, const float* s8, char* q8, float* qs, hipStream_t s) {
+  wam_gemm_desc g = g0;
+  g.A = q8; g.lda = (g0.K + 15) / 16 * 16; g.a_rows = 0; g.a_batch_stride = 0;
+  g.W = w8; g.ldw = g0.K;
+  return gemm_checked(g, s, 0, 0, qs, s8);
+}
+
+// A LayerNorm that feeds only an FP8 projection writes E4M3 codes and row scales directly.
+void ln_to_fp8(LnArgs& ln, char* q8, float* qs) {
+  ln.q8 = reinterpret_cast<uint8_t*>(q8);
+  ln.ldq = (ln.d + 15) / 16 * 16;
+  ln.q_scale = qs;
+}
+
 wam_status check_block_weights(const wam_block_weights& w) {
   if (!w.fp8) {  // with FP8 copies the bf16 matrices are not read
     TRY(need_ptr(w.w_qkv, "w_qkv")); TRY(need_ptr(w.w_o, "w_o")); TRY(need_ptr(w.w_cq, "w_cq"));
@@ -416,13 +432,17 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   LnArgs ln{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 0 * d, e0 + 0 * d, m6 + 1 * d, e0 + 1 * d, ms, h, seg, alt};
   const int64_t pq_ms = (int64_t)nseg * 2 * d, pq_alt = 2 * (int64_t)d, pq_norm = (int64_t)B * pq_ms;
   if (pq) ln = LnArgs{M, L, d, D.eps, io.x, nullptr, nullptr, nullptr, pq, nullptr, pq + d, pq_ms, h, seg, pq_alt};
+  // FP8 projections after the three LayerNorms: the LayerNorm writes the E4M3 rows itself
+  const bool ln8 = F8 && ln_fp8_supported(d);
+  if (ln8) ln_to_fp8(ln, q8, qs);
   TRY(mark(ev, WAM_EV_LN1, 0, s));
   LAUNCH(launch_ln_mod(pred(ln), s));
   TRY(mark(ev, WAM_EV_LN1, 1, s));
   // 2. fused QKV projection
   TRY(mark(ev, WAM_EV_QKV, 0, s));
-  TRY(proj(gemm(M, 3 * d, d, WAM_EPI_BF16, h, d, W.w_qkv, W.b_qkv, big, 3 * d), F8 ? F8->w_qkv : nullptr,
-           F8 ? F8->s_qkv : nullptr, q8, qs, s));
+  if (ln8) TRY(proj_q8(gemm(M, 3 * d, d, WAM_EPI_BF16, h, d, W.w_qkv, W.b_qkv, big, 3 * d), F8->w_qkv, F8->s_qkv, q8, qs, s));
+  else TRY(proj(gemm(M, 3 * d, d, WAM_EPI_BF16, h, d, W.w_qkv, W.b_qkv, big, 3 * d), F8 ? F8->w_qkv : nullptr,
+                F8 ? F8->s_qkv : nullptr, q8, qs, s));
   TRY(mark(ev, WAM_EV_QKV, 1, s));
   // 3. RoPE on q, k; k, v appended to the cache rows of this chunk (with an FP8 cache:
   // q and k encoded in 32-dim blocks, q into the q buffer with its exponents behind it)
@@ -457,13 +477,15 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   }
   // 6. cross-attention LayerNorm (affine, no modulation)
   LnArgs lc{M, L, d, D.eps, io.x, W.lnc_gamma, W.lnc_beta, nullptr, nullptr, nullptr, nullptr, 0, h};
+  if (ln8) ln_to_fp8(lc, q8, qs);
   TRY(mark(ev, WAM_EV_LNC, 0, s));
   LAUNCH(launch_ln_mod(pred(lc), s));
   TRY(mark(ev, WAM_EV_LNC, 1, s));
   // 7. cross query
   TRY(mark(ev, WAM_EV_CQ, 0, s));
-  TRY(proj(gemm(M, d, d, WAM_EPI_BF16, h, d, W.w_cq, W.b_cq, q, d), F8 ? F8->w_cq : nullptr,
-           F8 ? F8->s_cq : nullptr, q8, qs, s));
+  if (ln8) TRY(proj_q8(gemm(M, d, d, WAM_EPI_BF16, h, d, W.w_cq, W.b_cq, q, d), F8->w_cq, F8->s_cq, q8, qs, s));
+  else TRY(proj(gemm(M, d, d, WAM_EPI_BF16, h, d, W.w_cq, W.b_cq, q, d), F8 ? F8->w_cq : nullptr,
+                F8 ? F8->s_cq : nullptr, q8, qs, s));
   TRY(mark(ev, WAM_EV_CQ, 1, s));
   // 8. cross K|V of the text (unless precomputed for this block)
   const void* kv = io.ctx_kv;
@@ -492,13 +514,15 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   if (pq)
     l2 = LnArgs{M, L, d, D.eps, io.x, nullptr, nullptr, nullptr, pq + pq_norm, nullptr, pq + pq_norm + d, pq_ms, h,
                 seg, pq_alt};
+  if (ln8) ln_to_fp8(l2, q8, qs);
   TRY(mark(ev, WAM_EV_LN2, 0, s));
   LAUNCH(launch_ln_mod(pred(l2), s));
   TRY(mark(ev, WAM_EV_LN2, 1, s));
   // 12. FFN up-projection with tanh-GELU
   TRY(mark(ev, WAM_EV_FFN1, 0, s));
-  TRY(proj(gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, big, D.ffn), F8 ? F8->w_f1 : nullptr,
-           F8 ? F8->s_f1 : nullptr, q8, qs, s));
+  if (ln8) TRY(proj_q8(gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, big, D.ffn), F8->w_f1, F8->s_f1, q8, qs, s));
+  else TRY(proj(gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, big, D.ffn), F8 ? F8->w_f1 : nullptr,
+                F8 ? F8->s_f1 : nullptr, q8, qs, s));
   TRY(mark(ev, WAM_EV_FFN1, 1, s));
   // 13. x += gate2 * (u W_f2^T + b_f2)
   {
@@ -527,14 +551,19 @@ wam_status block_kv_run(const wam_dims& D, const wam_block_weights& W, const wam
   if (pq)
     ln = LnArgs{M, L, d, D.eps, io.x, nullptr, nullptr, nullptr, pq, nullptr, pq + d, (int64_t)nseg * 2 * d, h, seg,
                 2 * (int64_t)d};
+  const wam_block_fp8* F8 = W.fp8;
+  char* q8 = ws + lay.q8;
+  float* qs = reinterpret_cast<float*>(ws + lay.qs);
+  const bool ln8 = F8 && ln_fp8_supported(d);
+  if (ln8) ln_to_fp8(ln, q8, qs);
   LAUNCH(launch_ln_mod(pred(ln), s));
   // rows d..3d of W_qkv (the k and v outputs) into columns d..3d of the [M][3d] buffer
-  const wam_block_fp8* F8 = W.fp8;
   const char* wkv = F8 ? nullptr : static_cast<const char*>(W.w_qkv) + (size_t)d * d * 2;
   const float* bkv = W.b_qkv ? W.b_qkv + d : nullptr;
-  TRY(proj(gemm(M, 2 * d, d, WAM_EPI_BF16, h, d, wkv, bkv, big + (size_t)d * 2, 3 * d),
-           F8 ? static_cast<const char*>(F8->w_qkv) + (size_t)d * d : nullptr, F8 ? F8->s_qkv + d : nullptr,
-           ws + lay.q8, reinterpret_cast<float*>(ws + lay.qs), s));
+  const wam_gemm_desc gkv = gemm(M, 2 * d, d, WAM_EPI_BF16, h, d, wkv, bkv, big + (size_t)d * 2, 3 * d);
+  if (ln8) TRY(proj_q8(gkv, static_cast<const char*>(F8->w_qkv) + (size_t)d * d, F8->s_qkv + d, q8, qs, s));
+  else TRY(proj(gkv, F8 ? static_cast<const char*>(F8->w_qkv) + (size_t)d * d : nullptr, F8 ? F8->s_qkv + d : nullptr,
+                q8, qs, s));
   RopeArgs ra{B, L, D.H, D.Dh, io.Lcap, io.cache_len, big, io.rope_cos, io.rope_sin, nullptr, io.k_cache,
               io.v_cache};
   if (io.k_exp) {
@@ -1122,6 +1151,30 @@ wam_status wam_adaln_ln_mod(int32_t B, int32_t rows_per_batch, int32_t d, float 
   CHECK(mod_stride % 4 == 0, WAM_EINVAL, "mod_stride must be a multiple of 4");
   LnArgs a{B * rows_per_batch, rows_per_batch, d, eps, x, gamma, beta, shift_a, shift_v, scale_a, scale_v,
            mod_stride, h};
+  HIPCHECK(launch_ln_mod(a, stream));
+  return WAM_OK;
+}
+
+wam_status wam_adaln_ln_mod_fp8(int32_t B, int32_t rows_per_batch, int32_t d, float eps, const float* x,
+                                const float* gamma, const float* beta, const float* shift_a, const float* shift_v,
+                                const float* scale_a, const float* scale_v, int64_t mod_stride, void* q,
+                                int64_t ldq, float* scale, hipStream_t stream) {
+  CHECK(B >= 0 && rows_per_batch >= 0, WAM_EINVAL, "negative sizes");
+  CHECK(ln_fp8_supported(d), WAM_EUNSUPPORTED, "d=%d must be a multiple of 512 in [512, 5120]", d);
+  CHECK(eps > 0.f, WAM_EINVAL, "eps must be > 0");
+  CHECK(ldq >= d && ldq % 16 == 0, WAM_EINVAL, "ldq must be >= d and a multiple of 16");
+  if ((int64_t)B * rows_per_batch == 0) return WAM_OK;
+  CHECK((int64_t)B * rows_per_batch < (1ll << 31), WAM_EINVAL, "too many rows");
+  TRY(need_ptr(x, "x")); TRY(need_ptr(q, "q")); TRY(need_ptr(scale, "scale"));
+  TRY(opt_ptr(gamma, "gamma")); TRY(opt_ptr(beta, "beta"));
+  TRY(opt_ptr(shift_a, "shift_a")); TRY(opt_ptr(shift_v, "shift_v"));
+  TRY(opt_ptr(scale_a, "scale_a")); TRY(opt_ptr(scale_v, "scale_v"));
+  CHECK(mod_stride % 4 == 0, WAM_EINVAL, "mod_stride must be a multiple of 4");
+  LnArgs a{B * rows_per_batch, rows_per_batch, d, eps, x, gamma, beta, shift_a, shift_v, scale_a, scale_v,
+           mod_stride, nullptr};
+  a.q8 = static_cast<uint8_t*>(q);
+  a.ldq = ldq;
+  a.q_scale = scale;
   HIPCHECK(launch_ln_mod(a, stream));
   return WAM_OK;
 }

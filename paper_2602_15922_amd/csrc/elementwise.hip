@@ -96,9 +96,14 @@ __global__ __launch_bounds__(LN_ROWS * 64, NV <= 20 ? 4 : 2) void ln_mod_kernel(
 
 // The same with 8 consecutive columns per lane (d a multiple of 512): two adjacent 16-byte
 // loads and one 16-byte store of 8 bf16 per lane and chunk, half the store instructions.
-template <int NC>
+// With Q8 the row is not stored in bf16: its bf16 values are quantized to E4M3 codes with
+// one scale per row (the maximum over the row's bf16 values / 448), the arithmetic of
+// quant_rows_kernel applied to the row this kernel would have stored, and 8 codes per lane
+// and chunk are stored (half the bytes of the bf16 row).
+template <int NC, bool Q8>
 __global__ __launch_bounds__(LN_ROWS * 64, NC <= 10 ? 4 : 2) void ln_mod8_kernel(const LnArgs a, int blocks_per_batch,
                                                                              int seg, int seg_blocks) {
+  // Q8: d is exactly 512 NC (no chunk of the row is conditional)
   extern __shared__ __attribute__((aligned(16))) float PQ[];  // [2][d]
   if (skip_step(a.skip)) return;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -106,7 +111,7 @@ __global__ __launch_bounds__(LN_ROWS * 64, NC <= 10 ? 4 : 2) void ln_mod8_kernel
   const bool second = j >= seg_blocks;
   const int rloc = second ? seg + (j - seg_blocks) * LN_ROWS + w : j * LN_ROWS + w;
   const int rend = second ? a.rows_per_batch : seg;
-  const int d = a.d, nc = d >> 9;
+  const int d = a.d, nc = Q8 ? NC : d >> 9;
   const int64_t mb = (int64_t)b * a.mod_stride + (second ? a.alt_off : 0);
   const bool active = rloc < rend;
   const int64_t row = (int64_t)b * a.rows_per_batch + (active ? rloc : rend - 1);
@@ -157,7 +162,7 @@ __global__ __launch_bounds__(LN_ROWS * 64, NC <= 10 ? 4 : 2) void ln_mod8_kernel
           q += t * t;
         }
   const float rstd = rsqrtf(wave_sum(q) / (float)d + a.eps);
-  bf16* hr = static_cast<bf16*>(a.h) + row * d;
+  float amax = 0.f;  // Q8: the largest |bf16 output| of the row
 #pragma unroll
   for (int i = 0; i < NC; ++i)
     if (i < nc) {
@@ -172,8 +177,36 @@ __global__ __launch_bounds__(LN_ROWS * 64, NC <= 10 ? 4 : 2) void ln_mod8_kernel
       bf16x8 o;
 #pragma unroll
       for (int k = 0; k < 8; ++k) o[k] = (bf16)v[i][k >> 2][k & 3];
-      *reinterpret_cast<bf16x8*>(hr + col) = o;
+      if constexpr (Q8) {  // keep the bf16 values (as fp32) for the second pass
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          v[i][k >> 2][k & 3] = (float)o[k];
+          amax = fmaxf(amax, fabsf((float)o[k]));
+        }
+      } else {
+        *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.h) + row * d + col) = o;
+      }
     }
+  if constexpr (Q8) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+    const float inv = amax > 0.f ? 448.0f / amax : 1.0f;
+    if (lane == 0) a.q_scale[row] = amax > 0.f ? amax / 448.0f : 1.0f;
+    uint8_t* qr = a.q8 + row * a.ldq;
+#pragma unroll
+    for (int i = 0; i < NC; ++i)
+      if (i < nc) {
+        float f[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) f[k] = fminf(fmaxf(v[i][k >> 2][k & 3] * inv, -448.0f), 448.0f);
+        int lo = 0, hi = 0;
+        lo = __builtin_amdgcn_cvt_pk_fp8_f32(f[0], f[1], lo, false);
+        lo = __builtin_amdgcn_cvt_pk_fp8_f32(f[2], f[3], lo, true);
+        hi = __builtin_amdgcn_cvt_pk_fp8_f32(f[4], f[5], hi, false);
+        hi = __builtin_amdgcn_cvt_pk_fp8_f32(f[6], f[7], hi, true);
+        *reinterpret_cast<u32x2*>(qr + (i * 64 + lane) * 8) = u32x2{(uint32_t)lo, (uint32_t)hi};
+      }
+  }
 }
 
 // One thread per 4 columns of one (layer, norm, sample, segment): the shift and scale
@@ -575,9 +608,25 @@ hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s) {
   const dim3 grid((unsigned)(B * bpb)), block(LN_ROWS * 64);
   const size_t lds = (size_t)2 * a.d * sizeof(float);  // d <= 8192: at most 64 KB
   const int nv = a.d / 256;
+  if (a.q8) {  // FP8 output: one kernel per row width
+    if (!ln_fp8_supported(a.d)) return hipErrorInvalidValue;
+    switch (a.d / 512) {
+      case 1: hipLaunchKernelGGL((ln_mod8_kernel<1, true>), grid, block, lds, s, a, bpb, seg, sb0); break;
+      case 2: hipLaunchKernelGGL((ln_mod8_kernel<2, true>), grid, block, lds, s, a, bpb, seg, sb0); break;
+      case 3: hipLaunchKernelGGL((ln_mod8_kernel<3, true>), grid, block, lds, s, a, bpb, seg, sb0); break;
+      case 4: hipLaunchKernelGGL((ln_mod8_kernel<4, true>), grid, block, lds, s, a, bpb, seg, sb0); break;
+      case 5: hipLaunchKernelGGL((ln_mod8_kernel<5, true>), grid, block, lds, s, a, bpb, seg, sb0); break;
+      case 6: hipLaunchKernelGGL((ln_mod8_kernel<6, true>), grid, block, lds, s, a, bpb, seg, sb0); break;
+      case 7: hipLaunchKernelGGL((ln_mod8_kernel<7, true>), grid, block, lds, s, a, bpb, seg, sb0); break;
+      case 8: hipLaunchKernelGGL((ln_mod8_kernel<8, true>), grid, block, lds, s, a, bpb, seg, sb0); break;
+      case 9: hipLaunchKernelGGL((ln_mod8_kernel<9, true>), grid, block, lds, s, a, bpb, seg, sb0); break;
+      default: hipLaunchKernelGGL((ln_mod8_kernel<10, true>), grid, block, lds, s, a, bpb, seg, sb0); break;
+    }
+    return hipGetLastError();
+  }
   if (a.d % 512 == 0 && a.d <= 5120) {  // 8 columns per lane (d up to 5120: 80 values per lane)
-    if (a.d <= 2048) hipLaunchKernelGGL(ln_mod8_kernel<4>, grid, block, lds, s, a, bpb, seg, sb0);
-    else hipLaunchKernelGGL(ln_mod8_kernel<10>, grid, block, lds, s, a, bpb, seg, sb0);
+    if (a.d <= 2048) hipLaunchKernelGGL((ln_mod8_kernel<4, false>), grid, block, lds, s, a, bpb, seg, sb0);
+    else hipLaunchKernelGGL((ln_mod8_kernel<10, false>), grid, block, lds, s, a, bpb, seg, sb0);
     return hipGetLastError();
   }
   if (nv <= 2) hipLaunchKernelGGL(ln_mod_kernel<2>, grid, block, lds, s, a, bpb, seg, sb0);

@@ -87,8 +87,16 @@ struct LnArgs {
   int64_t alt_off;
   // device flag of the denoising loop: while *skip > 0 every workgroup exits at entry (NULL: never)
   const int32_t* skip;
+  // FP8 output (q8 non-null; d a multiple of 512, at most 5120): instead of h, the E4M3
+  // codes of the bf16 output rows (row stride ldq bytes) and their row scales, exactly as
+  // launch_quant_rows would make them from h
+  uint8_t* q8 = nullptr;
+  int64_t ldq = 0;
+  float* q_scale = nullptr;
 };
 hipError_t launch_ln_mod(const LnArgs& a, hipStream_t s);
+// whether launch_ln_mod takes FP8 output for rows of d values
+inline bool ln_fp8_supported(int d) { return d % 512 == 0 && d >= 512 && d <= 5120; }
 
 // The combined AdaLN modulation of every block's two modulated LayerNorms, formed once per
 // step: for layer l, norm k (0: shift/scale rows 0/1 of the six, 1: rows 3/4), sample b and

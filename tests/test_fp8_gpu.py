@@ -53,6 +53,55 @@ def test_quantize_rows_fp8(M, K):
     assert np.array_equal(decode(q[:, :K].contiguous()), ref_q)
 
 
+# ----------------------------------------------------------------------------- LayerNorm to FP8
+@pytest.mark.parametrize("d,B,L", [(512, 1, 144), (5120, 2, 37), (2560, 3, 5)])
+def test_ln_mod_fp8_is_ln_then_quantize(d, B, L):
+    """The LayerNorm that writes E4M3 rows: codes and scales bit for bit those of the bf16
+    LayerNorm followed by the row quantizer (both through the C ABI), modulated and affine,
+    and the decoded rows against the fp64 LayerNorm at E4M3's resolution."""
+    import torch
+    w = lib()
+    log(f"ln_mod_fp8 d={d} B={B} L={L}")
+    x = synth.normal(5, "x", (B, L, d), 3.0, d, dtype="f32")
+    tab = synth.normal(5, "mod6", (6, d), 0.5, d, dtype="f32")
+    e0 = synth.normal(5, "e0", (B, 6, d), 0.5, d, dtype="f32")
+    g = synth.normal(5, "lnc_gamma", (d,), 0.3, d, dtype="f32")
+    bt = synth.normal(5, "lnc_beta", (d,), 0.3, d, dtype="f32")
+    xd, tabd, e0d = dev(x), dev(tab), dev(e0)
+    M, ldq = B * L, (d + 15) // 16 * 16 + 16  # a row stride past d: padding bytes stay untouched
+    m = tab.f64[None] + e0.f64
+    cases = (
+        (dict(shift_a=tabd[0], shift_v=e0d[:, 0], scale_a=tabd[1], scale_v=e0d[:, 1], mod_stride=6 * d),
+         oracle.modulate(x.f64, m[:, 0][:, None], m[:, 1][:, None], 1e-6)),
+        (dict(gamma=dev(g), beta=dev(bt)), oracle.layernorm(x.f64, 1e-6, g.f64, bt.f64)),
+    )
+    for kw, ref in cases:
+        h = torch.empty((M, d), dtype=torch.bfloat16, device="cuda")
+        w.wam_adaln_ln_mod(xd, h, 1e-6, L, **kw)
+        q_ref = torch.zeros((M, ldq), dtype=torch.uint8, device="cuda")
+        s_ref = torch.zeros(M, dtype=torch.float32, device="cuda")
+        w.wam_quantize_rows_fp8(h, q_ref, s_ref)
+        q = torch.full((M, ldq), 7, dtype=torch.uint8, device="cuda")
+        s = torch.zeros(M, dtype=torch.float32, device="cuda")
+        w.wam_adaln_ln_mod_fp8(xd, q, s, 1e-6, L, **kw)
+        torch.cuda.synchronize()
+        assert torch.equal(q[:, :d], q_ref[:, :d])
+        assert torch.equal(s, s_ref)
+        assert bool((q[:, d:] == 7).all())
+        got = decode(q[:, :d].contiguous()) * host(s)[:, None]
+        assert rel_l2(got, ref.reshape(M, d)) <= 4e-2  # E4M3: 3 mantissa bits (relative step 2^-4)
+
+
+def test_ln_mod_fp8_rejects_widths_it_does_not_take():
+    import torch
+    w = lib()
+    x = torch.zeros((2, 1280), dtype=torch.float32, device="cuda")
+    q = torch.zeros((2, 1280), dtype=torch.uint8, device="cuda")
+    s = torch.zeros(2, dtype=torch.float32, device="cuda")
+    with pytest.raises(w.WamError):
+        w.wam_adaln_ln_mod_fp8(x, q, s, 1e-6, 2)
+
+
 GEMM_SHAPES = [(300, 200, 144), (3152, 5192, 528), (17, 16, 16), (3152, 13700, 144)]  # the last: two column ranges
 
 
