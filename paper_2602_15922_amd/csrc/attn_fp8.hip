@@ -104,6 +104,32 @@ WAM_DEV void fetch_tile(char* st, __amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsr
 
 WAM_DEV v4i lds16(const char* p) { return *reinterpret_cast<const v4i*>(p); }
 
+// V^T fragments through inline asm, as in the bf16 kernel: in the compiler's form each
+// tile's first transposing read waits for all outstanding vector memory, i.e. for the next
+// tile's loads (the compiler cannot prove the direct-to-LDS prefetch misses them).  Issued
+// as asm, the reads of P.V MFMA mt+1 go out before MFMA mt, which waits only until its own
+// four reads are done (LDS reads complete in order); the results are tied through the wait.
+template <int OFF>
+WAM_DEV v2i tr8(unsigned addr) {
+  v2i r;
+  asm volatile("ds_read_b64_tr_b8 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+template <int N>
+WAM_DEV void wait_lgkm4(v2i& a, v2i& b, v2i& c, v2i& d) {
+  asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) : "i"(N));
+}
+WAM_DEV unsigned lds_addr(const void* p) {
+  return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char*)(p);
+}
+// the four reads of P.V MFMA mt: keys 16 k + (the lane's 8) for k = 0..3
+WAM_DEV void vreads(unsigned a, v2i* r) {
+  r[0] = tr8<0>(a);
+  r[1] = tr8<16 * ROWB>(a);
+  r[2] = tr8<32 * ROWB>(a);
+  r[3] = tr8<48 * ROWB>(a);
+}
+
 // One 64-key tile for one wavefront's 32 queries.
 template <bool MASK>
 WAM_DEV void attn_tile(const char* st, const i32x8* qf, const int* qsc, f32x16* acc, f32x16& accl, float& m_ref,
@@ -170,14 +196,21 @@ WAM_DEV void attn_tile(const char* st, const i32x8* qf, const int* qsc, f32x16* 
   const i32x8 ones = {0x38383838, 0x38383838, 0x38383838, 0x38383838,
                       0x38383838, 0x38383838, 0x38383838, 0x38383838};  // E4M3 1.0
   accl = mfma_f8(ones, pk, accl, 127, 127);
+  unsigned va[4];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt) va[mt] = lds_addr(Vs + vofs[mt]);
+  v2i r[2][4];
+  vreads(va[0], r[0]);
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt) {
-    const char* vr = Vs + vofs[mt];
-    const v2i r0 = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(vr));
-    const v2i r1 = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(vr + 16 * ROWB));
-    const v2i r2 = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(vr + 32 * ROWB));
-    const v2i r3 = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(vr + 48 * ROWB));
-    const i32x8 vf = {r0[0], r0[1], r1[0], r1[1], r2[0], r2[1], r3[0], r3[1]};
+    v2i* c = r[mt & 1];
+    if (mt + 1 < 4) {
+      vreads(va[mt + 1], r[(mt + 1) & 1]);
+      wait_lgkm4<4>(c[0], c[1], c[2], c[3]);
+    } else {
+      wait_lgkm4<0>(c[0], c[1], c[2], c[3]);
+    }
+    const i32x8 vf = {c[0][0], c[0][1], c[1][0], c[1][1], c[2][0], c[2][1], c[3][0], c[3][1]};
     acc[mt] = mfma_f8(vf, pk, acc[mt], 127, 127);
   }
 }
