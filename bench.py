@@ -112,21 +112,24 @@ def build_model(wl, torch):
 # matrix kernels (2*M*N*K per projection, 4*Dh per visible (q, k) pair per head for
 # attention), bytes for the memory-bound ones (LayerNorm: fp32 row in, bf16 row out;
 # RoPE/append: the bf16 q|k|v row in, q, k and v out).
-def role_work(wl):
+def role_work(wl, ln_out_bytes=2):
+    """Algorithmic work of each role per launch: flops, or bytes (a LayerNorm reads 4 and
+    writes ln_out_bytes per element: 2 for bf16 rows, 1 for the E4M3 rows of the FP8 step)."""
     M, d, F = wl.B * wl.L, wl.d, wl.ffn
+    ln = M * d * (4 + ln_out_bytes)
     return {
-        "ln1": ("GB/s", M * d * 6), "qkv": ("TFLOP/s", 2 * M * d * 3 * d), "rope": ("GB/s", M * 3 * d * 2 * 2),
+        "ln1": ("GB/s", ln), "qkv": ("TFLOP/s", 2 * M * d * 3 * d), "rope": ("GB/s", M * 3 * d * 2 * 2),
         "self_attn": ("TFLOP/s", 4 * wl.H * wl.Dh * M * wl.Lk), "o": ("TFLOP/s", 2 * M * d * d),
-        "lnc": ("GB/s", M * d * 6), "cq": ("TFLOP/s", 2 * M * d * d),
+        "lnc": ("GB/s", ln), "cq": ("TFLOP/s", 2 * M * d * d),
         "cross_attn": ("TFLOP/s", 4 * wl.H * wl.Dh * M * wl.Lc), "co": ("TFLOP/s", 2 * M * d * d),
-        "ln2": ("GB/s", M * d * 6), "ffn1": ("TFLOP/s", 2 * M * d * F), "ffn2": ("TFLOP/s", 2 * M * F * d),
+        "ln2": ("GB/s", ln), "ffn1": ("TFLOP/s", 2 * M * d * F), "ffn2": ("TFLOP/s", 2 * M * F * d),
     }
 
 
 MI355X_HBM_GBPS = 8000.0  # published HBM3E peak
 
 
-def profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, n_steps, mfma_peak=None, **io_kw):
+def profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, n_steps, mfma_peak=None, ln_out_bytes=2, **io_kw):
     """Per-role average launch time over n_steps untimed steps that record events around
     every launch of every block, with each role's achieved rate and fraction of its peak
     (dense MFMA at mfma_peak, bf16's by default, for GEMMs and attention; HBM for LayerNorm
@@ -148,7 +151,7 @@ def profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, n_steps, mfma_peak=N
         for l in range(wl.n_layers):
             for k in range(nk):
                 sums[k] += ev[2 * (l * nk + k)].elapsed_time(ev[2 * (l * nk + k) + 1])
-    work = role_work(wl)
+    work = role_work(wl, ln_out_bytes)
     out = {}
     for k, name in enumerate(names):
         ms = sums[k] / (n_steps * wl.n_layers)
@@ -311,10 +314,12 @@ def extras(wl, model, keep, kcs, vcs, inp, torch, reps=3):
                                       / wl.n_layers, 4)
     assert torch.isfinite(vv).all()
     # the same step with events around every launch of every block: per-role times of the
-    # FP8 path, MFMA roles against the FP8 dense peak (a role's time includes the row
-    # quantization of its FP8 GEMM's input)
+    # FP8 path, MFMA roles against the FP8 dense peak (the O, cross-O and FFN2 roles include
+    # the row quantization of their input; the three LayerNorms write E4M3 rows themselves
+    # where the width allows it, a byte per element)
+    ln8 = wl.d % 512 == 0 and 512 <= wl.d <= 5120
     roles8 = profiled_roles(wl, model8, k8s, v8s, inp, vv, va, torch, 1, mfma_peak=MI355X_FP8_DENSE_TFLOPS,
-                            k_exps=kes, v_scales=vsc)
+                            ln_out_bytes=1 if ln8 else 2, k_exps=kes, v_scales=vsc)
     out["fp8_roles"] = {k: {"ms": v["ms"], "achieved": v["achieved"], "unit": v["unit"], "frac": v["frac"]}
                         for k, v in roles8.items()}
     del blocks8, model8, ws8, k8s, v8s, kes
