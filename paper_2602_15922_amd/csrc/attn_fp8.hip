@@ -13,8 +13,10 @@
 // p = 2^(s c - m c + 6): the reference maximum m is raised whenever a tile exceeds it by
 // 2^2, so p <= 2^8 stays inside E4M3's range and small probabilities keep 6 more binary
 // orders of magnitude above E4M3's smallest subnormal.  The row sum l comes from one more
-// MFMA of the rounded probabilities against a block of ones, so the normaliser adds
-// exactly the values the output product used.
+// MFMA of the rounded probabilities, so the normaliser adds exactly the values the output
+// product used: a 16x16x128 one (half the cycles of the 32x32x64 shape) whose A operand is
+// E4M3 1.0 in two rows only, chosen by lane so that row 0 sums the keys of queries 0-15 and
+// row 4 those of queries 16-31 (below).
 //
 // Layout and schedule follow the bf16 kernel: 4 wavefronts x 32 queries of one (batch,
 // head), S^T = K Q^T and O^T = V^T P^T so a lane owns one query, 64-key tiles of K codes,
@@ -46,6 +48,9 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 WAM_DEV f32x16 mfma_f8(i32x8 a, i32x8 b, f32x16 c, int sa, int sb) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, sa, 0, sb);
+}
+WAM_DEV f32x4 mfma_f8_16(i32x8 a, i32x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
 }
 
 WAM_DEV float other_half(float v) {
@@ -132,7 +137,8 @@ WAM_DEV void vreads(unsigned a, v2i* r) {
 
 // One 64-key tile for one wavefront's 32 queries.
 template <bool MASK>
-WAM_DEV void attn_tile(const char* st, const i32x8* qf, const int* qsc, f32x16* acc, f32x16& accl, float& m_ref,
+WAM_DEV void attn_tile(const char* st, const i32x8* qf, const int* qsc, f32x16* acc, f32x4& accl, const i32x8& sel,
+                       float& m_ref,
                        const int* kofs, const int* vofs, float c, float thr, int kb, int row_kend, int hh, int l32) {
   const char* Vs = st + KT;
   const char* Es = st + 2 * KT;
@@ -193,9 +199,7 @@ WAM_DEV void attn_tile(const char* st, const i32x8* qf, const int* qsc, f32x16* 
       wd = __builtin_amdgcn_cvt_pk_fp8_f32(p2, p3, wd, true);
       pk[4 * nt + q] = wd;
     }
-  const i32x8 ones = {0x38383838, 0x38383838, 0x38383838, 0x38383838,
-                      0x38383838, 0x38383838, 0x38383838, 0x38383838};  // E4M3 1.0
-  accl = mfma_f8(ones, pk, accl, 127, 127);
+  accl = mfma_f8_16(sel, pk, accl);
   unsigned va[4];
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt) va[mt] = lds_addr(Vs + vofs[mt]);
@@ -302,7 +306,15 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_fp8(const AttnFp8Args f, int n
   f32x16 acc[4];
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt) acc[mt] = f32x16{};
-  f32x16 accl = f32x16{};
+  // Row sums.  Read as a 16x16x128 operand, the probabilities of lane l are column l % 16
+  // of k-chunk l / 16: chunks 0 and 2 hold the keys of queries 0-15 (lanes 0-15, 32-47),
+  // chunks 1 and 3 those of queries 16-31.  A is E4M3 1.0 in lanes 0 and 32 (row 0, chunks
+  // 0 and 2) and 20 and 52 (row 4, chunks 1 and 3), zero elsewhere, so row 0 of the result
+  // is the sums of queries 0-15 and row 4 those of 16-31, i.e. register 0 of lane l < 32
+  // holds query l's sum (lanes 32-63 hold zeros).
+  const int sw = ((lane & 15) == 0 && !(lane & 16)) || ((lane & 15) == 4 && (lane & 16)) ? 0x38383838 : 0;
+  const i32x8 sel = {sw, sw, sw, sw, sw, sw, sw, sw};
+  f32x4 accl = f32x4{};
   float m_ref = -INFINITY;
   const float c = a.c, thr = RESCALE_LOG2 / c;
 
@@ -318,7 +330,8 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_fp8(const AttnFp8Args f, int n
       if (tt + 1 < ntiles)
         fetch_tile(smem + (cur ^ 1) * STAGE, kr, vr, er, kv_tsb, e_tsb, a.Lk, (tt + 1) * BN, w, lane, koff, voff,
                    krow);
-      attn_tile<false>(smem + cur * STAGE, qf, qsc, acc, accl, m_ref, kofs, vofs, c, thr, tt * BN, row_kend, hh, l32);
+      attn_tile<false>(smem + cur * STAGE, qf, qsc, acc, accl, sel, m_ref, kofs, vofs, c, thr, tt * BN, row_kend, hh,
+                       l32);
       tile_sync();
     }
   }
@@ -326,12 +339,13 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_fp8(const AttnFp8Args f, int n
     const int cur = t & 1;
     if (t + 1 < ntiles)
       fetch_tile(smem + (cur ^ 1) * STAGE, kr, vr, er, kv_tsb, e_tsb, a.Lk, (t + 1) * BN, w, lane, koff, voff, krow);
-    attn_tile<true>(smem + cur * STAGE, qf, qsc, acc, accl, m_ref, kofs, vofs, c, thr, t * BN, row_kend, hh, l32);
+    attn_tile<true>(smem + cur * STAGE, qf, qsc, acc, accl, sel, m_ref, kofs, vofs, c, thr, t * BN, row_kend, hh, l32);
     tile_sync();
   }
 
+  const float lsum = accl[0] + other_half(accl[0]);  // one of the two is zero
   if (qrow < a.Lq) {
-    const float inv = f.v_scale / accl[0];
+    const float inv = f.v_scale / lsum;
     bf16* ob = static_cast<bf16*>(a.o) + b * a.o_bs + (int64_t)qrow * a.o_ts + h * DH;
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
