@@ -153,6 +153,33 @@ def sampled_rows(bounds, extra, n_random, rng):
     return np.array(sorted(r for r in rows if 0 <= r < bounds[-1][1]))
 
 
+SHORT = [
+    # name, B, H, Lq, Lk: every query sees one key chunk (the cross-attention's layout),
+    # with more (query tile, head) workgroups than the chip holds at once (two per CU)
+    ("one_chunk_ragged", 1, 40, 1700, 77),
+    ("one_chunk_one_tile", 2, 32, 1100, 64),
+    ("one_chunk_16_tiles", 1, 36, 1900, 1024),
+    ("one_chunk_step_shape", 1, 40, 3152, 512),
+    ("one_chunk_ragged_long", 1, 2, 300, 1025),
+]
+
+
+@pytest.mark.parametrize("name,B,H,Lq,Lk", SHORT)
+def test_attention_one_chunk_short_keys(name, B, H, Lq, Lk):
+    """Dh = 128 against the fp64 oracle on the first two and last two rows of every 128-row
+    query tile plus random rows, every head and sample (so every item is checked)."""
+    case = [c[0] for c in SHORT].index(name)
+    w = lib()
+    Dh = 128
+    q, k, v = qkv(300 + case, B, Lq, Lk, H, Dh)
+    log(f"attn one chunk {name} B={B} H={H} Lq={Lq} Lk={Lk}")
+    o = host(run(dev(q), dev(k), dev(v), w.make_chunks([Lk], [Lq], [0])))
+    rows = sampled_rows([(a, min(a + 128, Lq)) for a in range(0, Lq, 128)], [], 20, np.random.default_rng(case))
+    for b in range(B):
+        ref = oracle.attention(q.f64[b, rows], k.f64[b], v.f64[b], np.zeros(len(rows)), np.zeros(Lk))
+        assert rel_l2(o[b, rows], ref) <= TOL, (name, b)
+
+
 def test_attention_full_size_cached_chunk():
     """40 heads x 128, 3152 queries of chunk 2 against 9456 keys (two cached chunks of
     3152 plus the current one), Q/K/V ~ N(0,1); oracle on sampled query rows."""
