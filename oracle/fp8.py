@@ -16,7 +16,10 @@ this is the reading used for the FP8 path here:
   (an 8-bit biased exponent, as the OCP microscaling formats define it), e the
   smallest integer with max|block| <= 448 * 2^e, so no element saturates; v with one
   scale per tensor, code = E4M3(x * (1 / scale)) with the reciprocal and the product
-  rounded to fp32.
+  rounded to fp32;
+* the same block rule over 64 consecutive elements of a row for a projection input
+  that a producer writes already quantized (the FFN's hidden activations): the FP8
+  GEMM then computes sum_k q_a[m][k] 2^e(m, k/64) q_w[n][k] exactly, times scale_w[n].
 """
 import numpy as np
 
@@ -80,19 +83,19 @@ def mx_exponent(amax):
     return np.where(amax == 0, 0, e)
 
 
-def quantize_mx(x):
-    """Block quantization along the last axis (length a multiple of 32): returns
-    (q, e) with e [..., n/32] the block exponents and q the E4M3 values of x / 2^e."""
+def quantize_mx(x, block=MX_BLOCK):
+    """Block quantization along the last axis (length a multiple of block): returns
+    (q, e) with e [..., n/block] the block exponents and q the E4M3 values of x / 2^e."""
     x = np.asarray(x, dtype=np.float64)
-    blocks = x.reshape(x.shape[:-1] + (x.shape[-1] // MX_BLOCK, MX_BLOCK))
+    blocks = x.reshape(x.shape[:-1] + (x.shape[-1] // block, block))
     e = mx_exponent(np.max(np.abs(blocks), axis=-1))
     q = round_e4m3(blocks * 2.0 ** (-e[..., None].astype(np.float64)))
     return q.reshape(x.shape), e
 
 
-def decode_mx(q, e):
-    """x ~ q * 2^e with each exponent applied to its 32-element block."""
-    return np.asarray(q, dtype=np.float64) * np.repeat(2.0 ** np.asarray(e, dtype=np.float64), MX_BLOCK, axis=-1)
+def decode_mx(q, e, block=MX_BLOCK):
+    """x ~ q * 2^e with each exponent applied to its block of consecutive elements."""
+    return np.asarray(q, dtype=np.float64) * np.repeat(2.0 ** np.asarray(e, dtype=np.float64), block, axis=-1)
 
 
 def quantize_scaled(x, scale):

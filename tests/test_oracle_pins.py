@@ -1151,37 +1151,39 @@ def test_mx_exponent_is_smallest_without_saturation():
     assert f(0.0) == 0 and f(2.0 ** -140) == -127 and f(3.0e38) == brute(3.0e38)
 
 
-def test_mx_block_quantization():
-    """32-element blocks along the last axis: codes equal torch's float8_e4m3fn rounding of
-    x / 2^e, each block's largest scaled magnitude lies in (224, 448], every normal-range
+@pytest.mark.parametrize("bl", [32, 64])
+def test_mx_block_quantization(bl):
+    """Blocks of bl elements along the last axis: codes equal torch's float8_e4m3fn rounding
+    of x / 2^e, each block's largest scaled magnitude lies in (224, 448], every normal-range
     element is within half a mantissa unit, a block whose maximum is exactly 448 * 2^e gets
     the per-row quantizer's codes, and blocks do not influence each other."""
     torch = pytest.importorskip("torch")
-    g = np.random.default_rng(173)
-    x = g.standard_normal((6, 256)) * np.repeat(10.0 ** g.uniform(-4, 4, (6, 8)), 32, axis=1)
+    g = np.random.default_rng(173 + bl)
+    nb = 256 // bl
+    x = g.standard_normal((6, 256)) * np.repeat(10.0 ** g.uniform(-4, 4, (6, nb)), bl, axis=1)
     x = x.astype(np.float32).astype(np.float64)
-    x[2, 64:96] = 0.0
-    q, e = oracle.fp8.quantize_mx(x)
-    assert e.shape == (6, 8) and e[2, 2] == 0 and not q[2, 64:96].any()
-    scaled = x * np.repeat(2.0 ** -e.astype(np.float64), 32, axis=1)
+    x[2, 2 * bl:3 * bl] = 0.0
+    q, e = oracle.fp8.quantize_mx(x, bl)
+    assert e.shape == (6, nb) and e[2, 2] == 0 and not q[2, 2 * bl:3 * bl].any()
+    scaled = x * np.repeat(2.0 ** -e.astype(np.float64), bl, axis=1)
     ref = torch.from_numpy(scaled).to(torch.float8_e4m3fn).to(torch.float64).numpy()
     assert np.array_equal(q, ref)
-    bmax = np.max(np.abs(scaled.reshape(6, 8, 32)), axis=-1)
+    bmax = np.max(np.abs(scaled.reshape(6, nb, bl)), axis=-1)
     nz = bmax > 0
     assert np.all(bmax[nz] > 224.0) and np.all(bmax[nz] <= 448.0)
-    deq = oracle.fp8.decode_mx(q, e)
+    deq = oracle.fp8.decode_mx(q, e, bl)
     normal = np.abs(scaled) >= 2.0 ** -6
     assert np.all(np.abs(deq - x)[normal] <= 2.0 ** -4 * np.abs(x)[normal])
-    blk = g.standard_normal(32)
-    blk *= 448.0 * 2.0 ** 5 / np.max(np.abs(blk))
-    qb, eb = oracle.fp8.quantize_mx(blk)
+    blk = g.standard_normal(bl)
+    blk = blk / np.max(np.abs(blk)) * (448.0 * 2.0 ** 5)  # the largest magnitude exactly 448 * 2^5
+    qb, eb = oracle.fp8.quantize_mx(blk, bl)
     qr, sr = oracle.fp8.quantize_rows(blk[None])
     assert eb[0] == 5 and sr[0] == 2.0 ** 5 and np.array_equal(qb, qr[0])
     x2 = x.copy()
-    x2[:, 32:64] *= 1000.0
-    q2, e2 = oracle.fp8.quantize_mx(x2)
+    x2[:, bl:2 * bl] *= 1000.0
+    q2, e2 = oracle.fp8.quantize_mx(x2, bl)
     keep = np.ones(256, bool)
-    keep[32:64] = False
+    keep[bl:2 * bl] = False
     assert np.array_equal(q2[:, keep], q[:, keep]) and np.array_equal(np.delete(e2, 1, 1), np.delete(e, 1, 1))
 
 
