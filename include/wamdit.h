@@ -587,6 +587,27 @@ wam_status wam_adaln_ln_mod_fp8(int32_t B, int32_t rows_per_batch, int32_t d, fl
 wam_status wam_gemm_fp8(const wam_gemm_desc* g, const float* a_scale, const float* w_scale,
                         hipStream_t stream);
 
+/* wam_gemm_fp8_mx: wam_gemm_fp8 with block-scaled activations on one side of it, for a
+ * projection whose input another projection produces (the FFN's hidden activations; the
+ * paper's deployment runs the DiT's projections in FP8, Section 3.2.4, Appendix D.2).  A
+ * block is 64 consecutive columns of a row with one power-of-two scale 2^(e - 127), e an
+ * 8-bit exponent, chosen as for wam_quantize_mx_fp8 (the smallest with max|block| <= 448 *
+ * 2^(e-127)); the exponents of blocks kb of row m sit at exps[(kb / 2) * lde + 4 m + kb % 2]
+ * (per pair of blocks all rows in order, 4 bytes per row of which the first 2 are used;
+ * lde a multiple of 4, >= 4 M; exps 4-byte aligned).
+ *   a_exp (a_scale NULL): A's E4M3 codes are block-scaled, acc[m][n] = sum_k A[m][k]
+ *     2^(e(m, k / 64) - 127) W[n][k] (fp32 accumulation of exact products), v = acc *
+ *     w_scale[n] + bias[n], epilogue WAM_EPI_BF16 or WAM_EPI_RESID_F32; K % 128 == 0,
+ *     a_rows == 0.  (Otherwise a_scale as for wam_gemm_fp8.)
+ *   out_exp (epilogue WAM_EPI_GELU_BF16, with a_scale): the GELU output, rounded to bf16 as
+ *     that epilogue stores it, is written block-scaled instead: E4M3 codes into out (one
+ *     byte per element, row stride ldo bytes, 4-byte aligned) and the exponents into
+ *     out_exp (stride o_lde), bit for bit wam_quantize_mx_fp8's rule over 64-column
+ *     blocks of the bf16 output; N % 128 == 0, out_rows == 0.
+ * Both a_exp and out_exp: WAM_EUNSUPPORTED. */
+wam_status wam_gemm_fp8_mx(const wam_gemm_desc* g, const float* a_scale, const void* a_exp, int64_t a_lde,
+                           const float* w_scale, void* out_exp, int64_t o_lde, hipStream_t stream);
+
 /* Patch and action embedding into the fp32 residual x [B][Lv+A][d]. */
 size_t wam_embed_workspace_bytes(const wam_dims* dims, int32_t B, int32_t F, int32_t Hl, int32_t Wl);
 wam_status wam_embed_fwd(const wam_model* m, int32_t B, int32_t F, int32_t Hl, int32_t Wl,

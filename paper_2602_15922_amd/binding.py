@@ -33,7 +33,7 @@ EXPORTED = (
     "wam_embed_workspace_bytes", "wam_embed_fwd", "wam_head_workspace_bytes", "wam_head_fwd",
     "wam_chunk_positions", "wam_rope_tables", "wam_attn_blockcausal_fp8", "wam_quantize_mx_fp8",
     "wam_quantize_scaled_fp8", "wam_rope_qkv_fp8", "wam_unipc_plan", "wam_unipc_step",
-    "wam_cosine_similarity_noalloc", "wam_adaln_ln_mod_fp8",
+    "wam_cosine_similarity_noalloc", "wam_adaln_ln_mod_fp8", "wam_gemm_fp8_mx",
 )
 
 _vp, _fp, _i32, _i64, _sz = C.c_void_p, C.POINTER(C.c_float), C.c_int32, C.c_int64, C.c_size_t
@@ -172,6 +172,7 @@ def lib():
         L.wam_rope_qkv.argtypes = [_i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp]
         L.wam_gemm_bf16.argtypes = [C.POINTER(wam_gemm_desc), _vp]
         L.wam_gemm_fp8.argtypes = [C.POINTER(wam_gemm_desc), _vp, _vp, _vp]
+        L.wam_gemm_fp8_mx.argtypes = [C.POINTER(wam_gemm_desc), _vp, _vp, _i64, _vp, _vp, _i64, _vp]
         L.wam_quantize_rows_fp8.argtypes = [_i32, _i32, _vp, _i64, _vp, _i64, _vp, _vp]
         L.wam_adaln_ln_mod_fp8.argtypes = [_i32, _i32, _i32, C.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64,
                                            _vp, _i64, _vp, _vp]
@@ -343,6 +344,22 @@ def wam_gemm_fp8(A, W, out, epilogue: int, a_scale, w_scale, bias=None, gate_a=N
                       out_rows=out_rows, gate_a=_p(gate_a), gate_v=_p(gate_v), gate_stride=gate_stride,
                       gate_rows=gate_rows)
     _check(lib().wam_gemm_fp8(C.byref(g), _p(a_scale), _p(w_scale), _stream(stream)))
+
+
+def wam_gemm_fp8_mx(A, W, out, epilogue: int, w_scale, a_scale=None, a_exp=None, a_lde=0, out_exp=None, o_lde=0,
+                    bias=None, gate_a=None, gate_v=None, gate_stride=0, gate_rows=0, M=None, lda=None, ldo=None,
+                    stream=None):
+    """wam_gemm_fp8 with block-scaled activations: a_exp (uint8, 4 bytes per row per pair of
+    64-column blocks, stride a_lde) instead of a_scale, or, with the GELU epilogue, the
+    output as E4M3 codes in out (uint8) with its block exponents in out_exp (stride o_lde)."""
+    N, K = W.shape
+    g = wam_gemm_desc(M=A.shape[0] if M is None else M, N=N, K=K, epilogue=epilogue,
+                      A=_p(A), lda=A.stride(0) if lda is None else lda, a_batch_stride=0, a_rows=0,
+                      W=_p(W), ldw=W.stride(0), bias=_p(bias), out=_p(out),
+                      ldo=out.stride(0) if ldo is None else ldo, out_batch_stride=0, out_rows=0,
+                      gate_a=_p(gate_a), gate_v=_p(gate_v), gate_stride=gate_stride, gate_rows=gate_rows)
+    _check(lib().wam_gemm_fp8_mx(C.byref(g), _p(a_scale), _p(a_exp), a_lde, _p(w_scale), _p(out_exp), o_lde,
+                                 _stream(stream)))
 
 
 def wam_adaln_ln_mod(x, h, eps, rows_per_batch, gamma=None, beta=None, shift_a=None, shift_v=None,

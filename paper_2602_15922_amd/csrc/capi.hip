@@ -229,9 +229,9 @@ wam_chunks single_chunk(int32_t Lq, int32_t Lk) {
 // fp8: A and W are E4M3 bytes with per-row a_scale [M] and per-column w_scale [N].
 // Validate one GEMM descriptor and fill its launch arguments (a.M = 0: nothing to run).
 wam_status gemm_prep(const wam_gemm_desc& g, GemmArgs& a, int32_t gate_split = 0, int64_t gate_alt = 0,
-                     const float* a_scale = nullptr, const float* w_scale = nullptr) {
+                     const float* a_scale = nullptr, const float* w_scale = nullptr, bool a_blocks = false) {
   a = GemmArgs{};
-  const bool fp8 = a_scale != nullptr;
+  const bool fp8 = a_scale != nullptr || a_blocks;
   const int eb = fp8 ? 1 : 2, epc = 16 / eb;  // bytes per element, elements per 16 bytes
   CHECK(g.M >= 0 && g.N >= 1 && g.K >= epc && g.K % epc == 0, WAM_EINVAL,
         "GEMM sizes M=%d N=%d K=%d (need N>=1, K>=%d, K%%%d==0)", g.M, g.N, g.K, epc, epc);
@@ -246,7 +246,7 @@ wam_status gemm_prep(const wam_gemm_desc& g, GemmArgs& a, int32_t gate_split = 0
   CHECK(g.a_rows >= 0 && g.out_rows >= 0 && g.gate_rows >= 0, WAM_EINVAL, "negative row groups");
   CHECK(g.a_batch_stride % epc == 0, WAM_EINVAL, "a_batch_stride must be a multiple of %d", epc);
   if (fp8) {
-    TRY(need_ptr(a_scale, "a_scale"));
+    if (!a_blocks) TRY(need_ptr(a_scale, "a_scale"));
     TRY(need_ptr(w_scale, "w_scale"));
   }
   CHECK(g.ldo % 4 == 0 && g.out_batch_stride % 4 == 0 && g.gate_stride % 4 == 0, WAM_EINVAL,
@@ -279,6 +279,46 @@ wam_status gemm_checked(const wam_gemm_desc& g, hipStream_t s, int32_t gate_spli
   GemmArgs a;
   TRY(gemm_prep(g, a, gate_split, gate_alt, a_scale, w_scale));
   if (a.M == 0) return WAM_OK;
+  LAUNCH(launch_gemm(pred(a), s));
+  return WAM_OK;
+}
+
+// The FP8 GEMM with block-scaled operands on either side (see wam_gemm_fp8_mx): a_exp
+// (instead of a_scale) the exponents of A's 64-column blocks; out_exp (GELU epilogue) the
+// output written as E4M3 codes with the exponents of its 64-column blocks.
+wam_status gemm_fp8_blocks(const wam_gemm_desc& g, const float* a_scale, const void* a_exp, int64_t a_lde,
+                           const float* w_scale, void* out_exp, int64_t o_lde, hipStream_t s,
+                           int32_t gate_split = 0, int64_t gate_alt = 0) {
+  CHECK((a_scale != nullptr) != (a_exp != nullptr), WAM_EINVAL, "exactly one of a_scale and a_exp is required");
+  CHECK(!(a_exp && out_exp), WAM_EUNSUPPORTED, "block-scaled A with a block-scaled output");
+  GemmArgs a;
+  TRY(gemm_prep(g, a, gate_split, gate_alt, a_scale, w_scale, a_exp != nullptr));
+  if (a_exp) {
+    CHECK(g.K % 128 == 0, WAM_EUNSUPPORTED, "block-scaled A needs K %% 128 == 0 (K=%d)", g.K);
+    CHECK(g.epilogue == WAM_EPI_BF16 || g.epilogue == WAM_EPI_RESID_F32, WAM_EUNSUPPORTED,
+          "block-scaled A takes the bf16 or the residual epilogue");
+    CHECK(g.a_rows == 0, WAM_EUNSUPPORTED, "block-scaled A takes plain rows (a_rows = 0)");
+    CHECK(a_lde % 4 == 0 && a_lde >= 4 * (int64_t)g.M, WAM_EINVAL, "a_lde must be a multiple of 4, >= 4*M");
+    CHECK(g.M == 0 || al4(a_exp), WAM_EINVAL, "a_exp must be 4-byte aligned");
+  }
+  if (out_exp) {
+    CHECK(g.epilogue == WAM_EPI_GELU_BF16, WAM_EUNSUPPORTED, "a block-scaled output takes the GELU epilogue");
+    CHECK(g.N % 128 == 0, WAM_EUNSUPPORTED, "a block-scaled output needs N %% 128 == 0 (N=%d)", g.N);
+    CHECK(g.out_rows == 0, WAM_EUNSUPPORTED, "a block-scaled output takes plain rows (out_rows = 0)");
+    CHECK(o_lde % 4 == 0 && o_lde >= 4 * (int64_t)g.M, WAM_EINVAL, "o_lde must be a multiple of 4, >= 4*M");
+    CHECK(g.M == 0 || al4(g.out), WAM_EINVAL, "out must be 4-byte aligned");
+  }
+  if (a.M == 0) return WAM_OK;
+  if (a_exp) {
+    a.epi |= WAM_EPI_MXA;
+    a.a_exp = static_cast<const uint8_t*>(a_exp);
+    a.a_lde = a_lde;
+  }
+  if (out_exp) {
+    a.epi = WAM_EPI_GELU_MX8;
+    a.out_exp = static_cast<uint8_t*>(out_exp);
+    a.o_lde = o_lde;
+  }
   LAUNCH(launch_gemm(pred(a), s));
   return WAM_OK;
 }
@@ -518,18 +558,44 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   TRY(mark(ev, WAM_EV_LN2, 0, s));
   LAUNCH(launch_ln_mod(pred(l2), s));
   TRY(mark(ev, WAM_EV_LN2, 1, s));
-  // 12. FFN up-projection with tanh-GELU
+  // 12. FFN up-projection with tanh-GELU.  With FP8 weights (ffn a multiple of 128) its
+  // output goes to FFN2 block-scaled: E4M3 codes [M][ffn] at big, behind them the
+  // exponents of each row's 64-column blocks (4 bytes per row per pair of blocks), so the
+  // hidden activations are written once, as bytes, and FFN2 needs no quantization pass.
+  const bool ffn_blocks = F8 && D.ffn % 128 == 0;
+  char* u8 = static_cast<char*>(big);
+  char* ue = u8 + align256((size_t)M * D.ffn);
+  const int64_t ue_ld = 4 * (int64_t)M;
   TRY(mark(ev, WAM_EV_FFN1, 0, s));
-  if (ln8) TRY(proj_q8(gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, big, D.ffn), F8->w_f1, F8->s_f1, q8, qs, s));
-  else TRY(proj(gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, big, D.ffn), F8 ? F8->w_f1 : nullptr,
-                F8 ? F8->s_f1 : nullptr, q8, qs, s));
+  if (ffn_blocks) {
+    wam_gemm_desc g = gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, u8, D.ffn);
+    g.W = F8->w_f1; g.ldw = d;
+    if (ln8) {
+      g.A = q8; g.lda = (d + 15) / 16 * 16;
+    } else {
+      const int64_t ldq = (d + 15) / 16 * 16;
+      LAUNCH(launch_quant_rows(M, d, h, d, q8, ldq, qs, s, t_skip));
+      g.A = q8; g.lda = ldq;
+    }
+    TRY(gemm_fp8_blocks(g, qs, nullptr, 0, F8->s_f1, ue, ue_ld, s));
+  } else if (ln8) {
+    TRY(proj_q8(gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, big, D.ffn), F8->w_f1, F8->s_f1, q8, qs, s));
+  } else {
+    TRY(proj(gemm(M, D.ffn, d, WAM_EPI_GELU_BF16, h, d, W.w_f1, W.b_f1, big, D.ffn), F8 ? F8->w_f1 : nullptr,
+             F8 ? F8->s_f1 : nullptr, q8, qs, s));
+  }
   TRY(mark(ev, WAM_EV_FFN1, 1, s));
   // 13. x += gate2 * (u W_f2^T + b_f2)
   {
     wam_gemm_desc g = gemm(M, d, D.ffn, WAM_EPI_RESID_F32, big, D.ffn, W.w_f2, W.b_f2, io.x, d);
     g.gate_a = m6 + 5 * d; g.gate_v = e0 + 5 * d; g.gate_stride = ms; g.gate_rows = L;
     TRY(mark(ev, WAM_EV_FFN2, 0, s));
-    TRY(proj(g, F8 ? F8->w_f2 : nullptr, F8 ? F8->s_f2 : nullptr, q8, qs, s, seg, alt));
+    if (ffn_blocks) {
+      g.A = u8; g.lda = D.ffn; g.W = F8->w_f2; g.ldw = D.ffn;
+      TRY(gemm_fp8_blocks(g, nullptr, ue, ue_ld, F8->s_f2, nullptr, 0, s, seg, alt));
+    } else {
+      TRY(proj(g, F8 ? F8->w_f2 : nullptr, F8 ? F8->s_f2 : nullptr, q8, qs, s, seg, alt));
+    }
     TRY(mark(ev, WAM_EV_FFN2, 1, s));
   }
   return WAM_OK;
@@ -1122,6 +1188,13 @@ wam_status wam_gemm_fp8(const wam_gemm_desc* g, const float* a_scale, const floa
   CHECK(g != nullptr, WAM_EINVAL, "NULL descriptor");
   CHECK(a_scale != nullptr && w_scale != nullptr, WAM_EINVAL, "a_scale and w_scale are required");
   return gemm_checked(*g, stream, 0, 0, a_scale, w_scale);
+}
+
+wam_status wam_gemm_fp8_mx(const wam_gemm_desc* g, const float* a_scale, const void* a_exp, int64_t a_lde,
+                           const float* w_scale, void* out_exp, int64_t o_lde, hipStream_t stream) {
+  CHECK(g != nullptr, WAM_EINVAL, "NULL descriptor");
+  CHECK(w_scale != nullptr, WAM_EINVAL, "w_scale is required");
+  return gemm_fp8_blocks(*g, a_scale, a_exp, a_lde, w_scale, out_exp, o_lde, stream);
 }
 
 wam_status wam_quantize_rows_fp8(int32_t M, int32_t K, const void* x, int64_t ldx, void* q, int64_t ldq,

@@ -33,6 +33,26 @@ WAM_DEV f32x16 mfma32_fp8(i32x8 a, i32x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
 }
 
+// The same with A scaled: byte sel (0 or 1, a constant after inlining) of sa is the biased
+// exponent (scale 2^(byte - 127)) of the lane's row; the two lanes of a row hold the same
+// byte, so both of the instruction's scale blocks take it.  W unscaled.
+WAM_DEV f32x16 mfma32_fp8_sa(i32x8 a, i32x8 b, f32x16 c, int sa, int sel) {
+  if (sel == 0) return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, sa, 0, 127);
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 1, sa, 0, 127);
+}
+
+// Biased (127) exponent of an MX block with largest magnitude amax (finite, >= 0): the
+// smallest e with amax <= 448 * 2^e, clamped to [-127, 127]; 0 (byte 127) for a zero
+// block.  From the bits: amax = m 2^E' with m in [1, 2) takes e = E' - 8 if m <= 1.75
+// (448 = 1.75 * 2^8), else E' - 7; below 2^-126 the clamp gives -127 (byte 0), and a finite
+// amax never reaches the upper clamp.
+WAM_DEV int mx_exp_biased(float amax) {
+  if (!(amax > 0.f)) return 127;
+  const unsigned u = __float_as_uint(amax);
+  const int eb = (int)(u >> 23) - 8 + ((u & 0x7fffffu) > 0x600000u ? 1 : 0);
+  return eb < 0 ? 0 : eb;
+}
+
 // The denoising loop launches a step's kernels with a device flag: while it is > 0 the
 // step reuses an earlier velocity and every workgroup returns at entry.
 WAM_DEV bool skip_step(const int32_t* skip) { return skip != nullptr && *skip > 0; }

@@ -321,15 +321,6 @@ __global__ __launch_bounds__(256) void quant_rows_reg_kernel(int M, int K, const
 // scaling and round to nearest even.  One thread converts 8 elements; the 4 threads of
 // a block (consecutive lanes) share its maximum through two lane exchanges.
 // ---------------------------------------------------------------------------------
-WAM_DEV int mx_exp_biased(float amax) {
-  if (!(amax > 0.f)) return 127;
-  int E;
-  const float f = frexpf(amax, &E);  // amax = f 2^E, f in [0.5, 1): amax / 2^(E-9) = 512 f
-  int e = E - 9 + (f > 0.875f ? 1 : 0);
-  e = e < -127 ? -127 : (e > 127 ? 127 : e);
-  return e + 127;
-}
-
 WAM_DEV u32x2 e4m3x8(const float* f, float mul) {
   float y[8];
 #pragma unroll

@@ -49,6 +49,8 @@ struct Cfg {
   static constexpr int NIA = BM * CPR / (NW * 64);  // direct-load instructions per wave (A)
   static constexpr int NIB = BN * CPR / (NW * 64);  // (W)
   static constexpr int STAGE = (BM + BN) * ROWB;  // bytes per stage
+  static constexpr bool MXA = false;              // block-scaled FP8 A (MxA below)
+  static constexpr int NI = NIA + NIB;            // vector memory instructions per slice per wave
   static_assert(NIA * NW * 64 == BM * CPR && NIB * NW * 64 == BN * CPR, "slice not a whole number of wave loads");
   // XOR pattern.  gfx950 LDS serves 256 bytes (64 banks) per cycle, i.e. 16 lanes of a
   // 16-byte read; the 16 consecutive rows those lanes read at one logical chunk must land
@@ -58,6 +60,33 @@ struct Cfg {
   static WAM_DEV int pch(int row, int ch) { return CPR == 8 ? (ch ^ ((row >> 1) & 7)) : (ch ^ ((row >> 2) & 3)); }
   static WAM_DEV int swz(int row, int ch) { return row * ROWB + (pch(row, ch) << 4); }  // bytes
 };
+
+// Block-scaled FP8 A: every slice also loads, per 32-row tile of the wave, the lane's row's
+// exponents of the slice's two 64-column blocks (one coalesced 4-byte load per tile: the
+// exponent layout keeps a block pair's rows contiguous, 4 bytes per row, of which the
+// MFMA's byte select reads the first two; a 16-bit load would need a zero extension that
+// the compiler places at the loop's head, waiting there for the newest loads).
+template <typename C>
+struct MxA : C {
+  static constexpr bool MXA = true;
+  static constexpr int NI = C::NIA + C::NIB + C::TM;
+};
+
+// The maximum over each row of 16 lanes of a value >= 0, in DPP (no LDS round trips; each
+// step folds into the max instruction): the two quad swaps give each lane its quad's
+// maximum, the half-row mirror (lane i and 7 - i of each 8) pairs the quads, the row
+// mirror (i and 15 - i) the halves.  A source lane that is off reads as 0.  (On the bit
+// patterns, whose unsigned order is the order of non-negative floats.)
+#define WAM_DPP_MAX(u, ctrl) max(u, (unsigned)__builtin_amdgcn_mov_dpp((int)u, ctrl, 0xF, 0xF, true))
+WAM_DEV float row16_max(float v) {
+  unsigned u = __float_as_uint(v);
+  u = WAM_DPP_MAX(u, 0xB1);   // quad_perm [1, 0, 3, 2]
+  u = WAM_DPP_MAX(u, 0x4E);   // quad_perm [2, 3, 0, 1]
+  u = WAM_DPP_MAX(u, 0x141);  // row_half_mirror
+  u = WAM_DPP_MAX(u, 0x140);  // row_mirror
+  return __uint_as_float(u);
+}
+#undef WAM_DPP_MAX
 
 // Exact row -> (group, row-in-group) split for a runtime divisor: a float reciprocal
 // estimate, corrected by one step (rows < 2^23).
@@ -83,6 +112,7 @@ WAM_DEV int64_t gate_off(const GemmArgs& g, int row, float inv) {
 // col + 4): element by element.
 template <int EPI>
 WAM_DEV void epilogue_ragged(const GemmArgs& g, const float inv_o, const float inv_g, int row, int col, f32x4 v) {
+  if constexpr (EPI == WAM_EPI_GELU_MX8) return;  // its N is a multiple of 128: never ragged
   const int64_t orow = group_off(row, g.o_rows, inv_o, g.o_bs, g.ldo);
   if (g.a_scale) v *= g.a_scale[row];  // FP8 operands: per-row and per-column scales
   for (int j = 0; j < 4 && col + j < g.N; ++j) {
@@ -128,14 +158,27 @@ struct GemmLane {
   int kla[C::NIA], klb[C::NIB];      // logical column (elements) of the lane's unit in a slice
   int fa_off[C::KS][C::FCH], fb_off[C::KS][C::FCH];  // LDS byte offsets of the lane's fragment
   int w;
+  const uint8_t* ae;  // block-scaled A: exponents, bytes between block pairs, 4 * the lane's rows
+  int64_t ae_ld;
+  int er[C::TM];
 };
+
+// The exponents of slice kt's two 64-column blocks for the lane's rows (block-scaled A).
+template <typename C>
+WAM_DEV void fetch_exp(const GemmLane<C>& L, int kt, unsigned (&e)[C::TM]) {
+  if constexpr (C::MXA) {
+#pragma unroll
+    for (int a = 0; a < C::TM; ++a) e[a] = *reinterpret_cast<const unsigned*>(L.ae + kt * L.ae_ld + L.er[a]);
+  }
+}
 
 // One BK slice into ring stage `buf` with buffer loads straight into LDS: lane l of
 // wave w's instruction c fills unit (w*NI + c)*64 + l.  Full slices need no per-lane
 // work (scalar slice offset + loop-invariant lane offset); in a slice that runs past K
 // a unit whose chunk lies past K re-reads the row's last in-range chunk instead (it is
 // zeroed in LDS once landed).
-template <typename C>
+// FULL: the caller knows the slice lies inside K (block-scaled A: K a multiple of BK).
+template <typename C, bool FULL = false>
 WAM_DEV void fetch_slice(char* smem, int buf, const GemmLane<C>& L, int kt, int K) {
   // buffer resources over all of A and W (offsets < 2^31 bytes, checked by the host)
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(L.A), (short)0, 0x7fffffff, 0x00020000);
@@ -143,7 +186,7 @@ WAM_DEV void fetch_slice(char* smem, int buf, const GemmLane<C>& L, int kt, int 
   char* As = smem + buf * C::STAGE;
   char* Bs = As + C::BM * C::ROWB;
   const int k0 = kt * C::BK, soff = C::EB * k0;
-  if (k0 + C::BK <= K) {
+  if (FULL || k0 + C::BK <= K) {
 #pragma unroll
     for (int c = 0; c < C::NIA; ++c)
       load_lds16(ra, As + (L.w * C::NIA + c) * 1024, L.a_off[c], soff);
@@ -207,14 +250,17 @@ WAM_DEV void read_frags(const char* smem, int stage, const GemmLane<C>& L, int k
   }
 }
 
-// The TM x TN MFMAs of one k-step.
+// The TM x TN MFMAs of k-step ks of a slice (block-scaled A: ea[a] holds the exponents
+// of the slice's two blocks for tile a's row, k-step ks takes byte ks).
 template <typename C>
-WAM_DEV void mfma_step(const Frag<C> (&fa)[C::TM], const Frag<C> (&fb)[C::TN], f32x16 (*acc)[C::TN]) {
+WAM_DEV void mfma_step(const Frag<C> (&fa)[C::TM], const Frag<C> (&fb)[C::TN], f32x16 (*acc)[C::TN],
+                       const unsigned* ea, int ks) {
 #pragma unroll
   for (int a = 0; a < C::TM; ++a)
 #pragma unroll
     for (int b = 0; b < C::TN; ++b) {
       if constexpr (C::EB == 2) acc[a][b] = mfma32(fa[a], fb[b], acc[a][b]);
+      else if constexpr (C::MXA) acc[a][b] = mfma32_fp8_sa(fa[a], fb[b], acc[a][b], (int)ea[a], ks);
       else acc[a][b] = mfma32_fp8(fa[a], fb[b], acc[a][b]);
     }
 }
@@ -259,15 +305,22 @@ WAM_DEV void block_barrier() {
 // is then visible to all, and stage CUR (slice t) is free, so the last k-step's MFMAs
 // run while slice t+S is fetched into stage CUR and k-step 0 of slice t+1 is read.  No
 // wave waits on an LDS read right after the barrier.
+// (Block-scaled A: ering[stage] holds the exponents of the slice in that stage.  Slice
+// t+S's exponents are loaded after slice t's last MFMAs, so they take the same registers:
+// loaded any earlier, both values are live at once and the compiler moves registers at
+// the loop's back edge, each move waiting for its load and so for every slice in flight.)
+// (Block-scaled A runs every slice here: past the last slice the prefetch re-reads it into
+// the free stage, which is never read; nk is used for that only.)
 template <typename C, int CUR>
 WAM_DEV void slice_steady(char* smem, const GemmLane<C>& L, int t, int K, f32x16 (*acc)[C::TN],
-                          Frag<C> (&fa)[2][C::TM], Frag<C> (&fb)[2][C::TN]) {
-  constexpr int S = C::STAGES, KS = C::KS, NI = C::NIA + C::NIB;
+                          Frag<C> (&fa)[2][C::TM], Frag<C> (&fb)[2][C::TN], unsigned (&ering)[C::STAGES][C::TM],
+                          int nk = 0) {
+  constexpr int S = C::STAGES, KS = C::KS, NI = C::NI;
   constexpr int NMF = C::TM * C::TN, NR = (C::TM + C::TN) * C::FCH;
 #pragma unroll
   for (int ks = 0; ks < KS - 1; ++ks) {
     read_frags<C>(smem, CUR, L, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
-    mfma_step<C>(fa[ks & 1], fb[ks & 1], acc);
+    mfma_step<C>(fa[ks & 1], fb[ks & 1], acc, ering[CUR], ks);
     interleave_step<NMF, NR, 0>();
     if constexpr (C::EB == 1) pin_acc<C>(acc);
     __builtin_amdgcn_sched_barrier(0);
@@ -276,19 +329,25 @@ WAM_DEV void slice_steady(char* smem, const GemmLane<C>& L, int t, int K, f32x16
   WAM_WAIT_VMCNT((S - 2) * NI);
   block_barrier();
   __builtin_amdgcn_sched_barrier(0);
-  fetch_slice<C>(smem, CUR, L, t + S, K);
+  if constexpr (C::MXA) fetch_slice<C, true>(smem, CUR, L, t + S < nk ? t + S : nk - 1, K);
+  else fetch_slice<C>(smem, CUR, L, t + S, K);
   read_frags<C>(smem, (CUR + 1) % S, L, 0, fa[KS & 1], fb[KS & 1]);
-  mfma_step<C>(fa[(KS - 1) & 1], fb[(KS - 1) & 1], acc);
-  interleave_step<NMF, NR, NI>();
+  mfma_step<C>(fa[(KS - 1) & 1], fb[(KS - 1) & 1], acc, ering[CUR], KS - 1);
+  interleave_step<NMF, NR, C::NIA + C::NIB>();
   if constexpr (C::EB == 1) pin_acc<C>(acc);
   __builtin_amdgcn_sched_barrier(0);
+  if constexpr (C::MXA) {
+    fetch_exp<C>(L, t + S < nk ? t + S : nk - 1, ering[CUR]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
 }
 
 template <typename C, int CUR>
 WAM_DEV void steady_group(char* smem, const GemmLane<C>& L, int t, int K, f32x16 (*acc)[C::TN],
-                          Frag<C> (&fa)[2][C::TM], Frag<C> (&fb)[2][C::TN]) {
-  slice_steady<C, CUR>(smem, L, t + CUR, K, acc, fa, fb);
-  if constexpr (CUR + 1 < C::STAGES) steady_group<C, CUR + 1>(smem, L, t, K, acc, fa, fb);
+                          Frag<C> (&fa)[2][C::TM], Frag<C> (&fb)[2][C::TN], unsigned (&ering)[C::STAGES][C::TM],
+                          int nk = 0) {
+  slice_steady<C, CUR>(smem, L, t + CUR, K, acc, fa, fb, ering, nk);
+  if constexpr (CUR + 1 < C::STAGES) steady_group<C, CUR + 1>(smem, L, t, K, acc, fa, fb, ering, nk);
 }
 
 // A slice after the steady state (the last few: fewer younger slices in flight, the next
@@ -296,13 +355,15 @@ WAM_DEV void steady_group(char* smem, const GemmLane<C>& L, int t, int K, f32x16
 // the same order as slice_steady and a runtime stage.
 template <typename C>
 WAM_DEV void slice_tail(char* smem, const GemmLane<C>& L, int t, int nk, int K, int lane, f32x16 (*acc)[C::TN],
-                        Frag<C> (&fa)[2][C::TM], Frag<C> (&fb)[2][C::TN]) {
-  constexpr int S = C::STAGES, KS = C::KS, NI = C::NIA + C::NIB;
+                        Frag<C> (&fa)[2][C::TM], Frag<C> (&fb)[2][C::TN], unsigned (&ering)[C::STAGES][C::TM]) {
+  constexpr int S = C::STAGES, KS = C::KS, NI = C::NI;
+  static_assert(!C::MXA, "block-scaled A runs every slice in the steady state");
   const int cur = t % S;
+  const unsigned* ec = ering[0];
 #pragma unroll
   for (int ks = 0; ks < KS - 1; ++ks) {
     read_frags<C>(smem, cur, L, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
-    mfma_step<C>(fa[ks & 1], fb[ks & 1], acc);
+    mfma_step<C>(fa[ks & 1], fb[ks & 1], acc, ec, ks);
     if constexpr (C::EB == 1) pin_acc<C>(acc);
     __builtin_amdgcn_sched_barrier(0);
   }
@@ -320,7 +381,8 @@ WAM_DEV void slice_tail(char* smem, const GemmLane<C>& L, int t, int nk, int K, 
     if (t + S < nk) fetch_slice<C>(smem, cur, L, t + S, K);
     read_frags<C>(smem, (t + 1) % S, L, 0, fa[KS & 1], fb[KS & 1]);
   }
-  mfma_step<C>(fa[(KS - 1) & 1], fb[(KS - 1) & 1], acc);
+  mfma_step<C>(fa[(KS - 1) & 1], fb[(KS - 1) & 1], acc, ec, KS - 1);
+
   if constexpr (C::EB == 1) pin_acc<C>(acc);
   __builtin_amdgcn_sched_barrier(0);
 }
@@ -346,8 +408,13 @@ WAM_DEV char* lds_ring() {
 // One BM x BN output tile (row tile tm, column tile tn, columns from col0) of g, with
 // the operand ring and the epilogue's staging in the first STAGES * STAGE of LBYTES
 // bytes of LDS.
-template <typename C, int EPI, int LBYTES = C::STAGES * C::STAGE>
+// EPI: the epilogue (low 3 bits), or-ed with WAM_EPI_MXA for block-scaled FP8 A.
+template <typename C0, int EPI, int LBYTES = C0::STAGES * C0::STAGE>
 WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn, int col0) {
+  using C = typename std::conditional<(EPI & WAM_EPI_MXA) != 0, MxA<C0>, C0>::type;
+  constexpr int E = EPI & 7;
+  static_assert(!C::MXA || C::EB == 1, "block-scaled A is FP8");
+  static_assert(E != WAM_EPI_GELU_MX8 || C::EB == 1, "the block-scaled output is an FP8 path's");
   static_assert(LBYTES >= C::STAGES * C::STAGE, "operand ring does not fit");
   constexpr int BM = C::BM, BN = C::BN, BK = C::BK, S = C::STAGES;
   char* smem = lds_ring<LBYTES>();
@@ -382,6 +449,15 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn, int col0) {
     L.klb[c] = C::pch(row, lane % C::CPR) * C::EPC;
     L.b_off[c] = (int)(C::EB * ((int64_t)r * g.ldw + L.klb[c]));
   }
+  if constexpr (C::MXA) {  // the exponents of the lane's A rows (clamped to the last row)
+    L.ae = g.a_exp;
+    L.ae_ld = g.a_lde;
+#pragma unroll
+    for (int a = 0; a < C::TM; ++a) {
+      const int r = m0 + wm * (BM / C::WM) + a * 32 + l32;
+      L.er[a] = 4 * (r < g.M ? r : g.M - 1);
+    }
+  }
   // Fragment reads: rows (wm*BM/WM + a*32 + l32) of A and (wn*BN/WN + b*32 + l32) of W
   // at logical chunks KCH*ks + FCH*hh + f; the XOR only depends on l32 (32-row steps keep it).
 #pragma unroll
@@ -400,13 +476,28 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn, int col0) {
     for (int b = 0; b < C::TN; ++b) acc[a][b] = f32x16{};
 
   const int nk = (g.K + BK - 1) / BK;
-  constexpr int NI = C::NIA + C::NIB;  // loads per slice per wave
+  constexpr int NI = C::NI;  // loads per slice per wave
   static_assert(C::KS % 2 == 0, "fragment slots alternate per k-step and slice");
+  unsigned ering[S][C::TM];  // block-scaled A: exponents of the slice in each stage
   // prologue: the first S slices in flight, slice 0 landed and visible, its k-step 0 read
+  if constexpr (C::MXA) {
+    // Every stage is fetched (past the last slice, the last slice again, into a stage that
+    // is never read; the barrier before the epilogue waits for it), so that no path into
+    // the main loop leaves an exponent load unaccounted for: the compiler's wait analysis
+    // does not correlate the fetch conditions with the wait's, and would wait inside the
+    // loop for the first stage's exponents.
 #pragma unroll
-  for (int p = 0; p < S; ++p)
-    if (p < nk) fetch_slice<C>(smem, p, L, p, g.K);
-  {
+    for (int p = 0; p < S; ++p) {
+      const int kp = p < nk ? p : nk - 1;
+      fetch_slice<C, true>(smem, p, L, kp, g.K);
+      fetch_exp<C>(L, kp, ering[p]);
+    }
+    WAM_WAIT_VMCNT((S - 1) * NI);
+    block_barrier();
+  } else {
+#pragma unroll
+    for (int p = 0; p < S; ++p)
+      if (p < nk) fetch_slice<C>(smem, p, L, p, g.K);
     const int younger = nk - 1 < S - 1 ? nk - 1 : S - 1;
     if (younger >= 2) WAM_WAIT_VMCNT(2 * NI);
     else if (younger == 1) WAM_WAIT_VMCNT(NI);
@@ -422,8 +513,18 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn, int col0) {
   int kt = 0;
   // steady state, S slices per iteration so each stage index is a constant: every slice
   // here has a successor, prefetches a slice < nk, and waits for a full slice
-  for (; kt + 2 * S + 1 <= nk && (kt + 2 * S + 1) * BK <= g.K; kt += S) steady_group<C, 0>(smem, L, kt, g.K, acc, fa, fb);
-  for (; kt < nk; ++kt) slice_tail<C>(smem, L, kt, nk, g.K, lane, acc, fa, fb);
+  if constexpr (C::MXA) {
+    // K is a multiple of the slice: S slices per iteration, then the last nk % S
+    for (; kt + S <= nk; kt += S) steady_group<C, 0>(smem, L, kt, g.K, acc, fa, fb, ering, nk);
+    if (kt < nk) slice_steady<C, 0>(smem, L, kt, g.K, acc, fa, fb, ering, nk);
+    if constexpr (S > 2) {
+      if (kt + 1 < nk) slice_steady<C, 1>(smem, L, kt + 1, g.K, acc, fa, fb, ering, nk);
+    }
+  } else {
+    for (; kt + 2 * S + 1 <= nk && (kt + 2 * S + 1) * BK <= g.K; kt += S)
+      steady_group<C, 0>(smem, L, kt, g.K, acc, fa, fb, ering);
+    for (; kt < nk; ++kt) slice_tail<C>(smem, L, kt, nk, g.K, lane, acc, fa, fb, ering);
+  }
   __syncthreads();  // all waves done with the operand ring before it is reused
 
   // ---- epilogue: each wave stages 32 rows x WCOLS of its tile through LDS (reusing
@@ -439,7 +540,8 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn, int col0) {
   constexpr int CG = WCOLS / 4, RP = 64 / CG, NP = 32 / RP;  // column groups, rows per pass, passes
   static_assert(64 % CG == 0 && 32 % RP == 0, "a lane's columns must not change between passes");
   static_assert(C::WM * C::WN * 32 * SROW * 4 <= S * C::STAGE, "staging does not fit");
-  constexpr bool RESID = EPI == WAM_EPI_RESID_F32;
+  constexpr bool RESID = E == WAM_EPI_RESID_F32;
+  static_assert(E != WAM_EPI_GELU_MX8 || WCOLS == 64, "a wave's columns of a row are one 64-column block");
   float* stage = reinterpret_cast<float*>(smem) + w * 32 * SROW;
   const float inv_o = 1.0f / (float)g.o_rows, inv_g = 1.0f / (float)g.gate_rows;
   const int row_base = m0 + wm * (BM / C::WM), col_base = n0 + wn * WCOLS;
@@ -500,11 +602,31 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn, int col0) {
         f32x4 v = *reinterpret_cast<const f32x4*>(&stage[rloc * SROW + cl]);
         const int64_t orow = group_off(rows[p], g.o_rows, inv_o, g.o_bs, g.ldo);
         v = v * rmul[p] * cmul + cadd;
-        if constexpr (EPI == WAM_EPI_BF16 || EPI == WAM_EPI_GELU_BF16) {
+        if constexpr (E == WAM_EPI_BF16 || E == WAM_EPI_GELU_BF16) {
           bf16x4 o;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) o[j] = (bf16)(EPI == WAM_EPI_GELU_BF16 ? gelu_tanh_f(v[j]) : v[j]);
+          for (int j = 0; j < 4; ++j) o[j] = (bf16)(E == WAM_EPI_GELU_BF16 ? gelu_tanh_f(v[j]) : v[j]);
           *reinterpret_cast<bf16x4*>(static_cast<bf16*>(g.out) + orow + col) = o;
+        } else if constexpr (E == WAM_EPI_GELU_MX8) {
+          // the bf16 GELU values as E4M3 codes of the row's 64-column block, whose 64
+          // values are the 4 of each of the CG = 16 lanes that share this row
+          float y[4], amax = 0.f;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            y[j] = (float)(bf16)gelu_tanh_f(v[j]);
+            amax = fmaxf(amax, fabsf(y[j]));
+          }
+          static_assert(CG == 16, "one row's columns are a DPP row of 16 lanes");
+          amax = row16_max(amax);
+          const int eb = mx_exp_biased(amax);
+          const float mul = ldexpf(1.0f, 127 - eb);  // |y| * mul <= 448 by the exponent's choice
+          int code = __builtin_amdgcn_cvt_pk_fp8_f32(y[0] * mul, y[1] * mul, 0, false);
+          code = __builtin_amdgcn_cvt_pk_fp8_f32(y[2] * mul, y[3] * mul, code, true);
+          *reinterpret_cast<int*>(static_cast<uint8_t*>(g.out) + orow + col) = code;
+          if (cl == 0) {
+            const int blk = col_base >> 6;
+            g.out_exp[(int64_t)(blk >> 1) * g.o_lde + 4 * rows[p] + (blk & 1)] = (uint8_t)eb;
+          }
         } else if constexpr (RESID) {
           *reinterpret_cast<f32x4*>(static_cast<float*>(g.out) + orow + col) = prev[p] + (cgate + gv[p]) * v;
         } else {
@@ -524,7 +646,7 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn, int col0) {
       for (int p = 0; p < NP; ++p) {
         const int rloc = p * RP + rl, row = row_base + a * 32 + rloc;
         const f32x4 v = *reinterpret_cast<const f32x4*>(&stage[rloc * SROW + cl]);
-        if (row < g.M) epilogue_ragged<EPI>(g, inv_o, inv_g, row, col, v);
+        if (row < g.M) epilogue_ragged<E>(g, inv_o, inv_g, row, col, v);
       }
     }
     __syncthreads();
@@ -631,6 +753,16 @@ hipError_t launch_cfg(const GemmArgs& g, const GemmGroup* gg, hipStream_t s) {
     return hipGetLastError();
   }
   dim3 grid(persistent_grid<Cf>((long)tm * tn));
+  if constexpr (Cf::EB == 1) {  // the block-scaled FP8 variants
+    constexpr int MXB = WAM_EPI_MXA | WAM_EPI_BF16, MXR = WAM_EPI_MXA | WAM_EPI_RESID_F32;
+    switch (g.epi) {
+      case WAM_EPI_GELU_MX8: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_GELU_MX8>), grid, block, 0, s, g, tm, tn); break;
+      case MXB: hipLaunchKernelGGL((gemm_nt<Cf, MXB>), grid, block, 0, s, g, tm, tn); break;
+      case MXR: hipLaunchKernelGGL((gemm_nt<Cf, MXR>), grid, block, 0, s, g, tm, tn); break;
+      default: break;
+    }
+    if (g.epi == WAM_EPI_GELU_MX8 || g.epi == MXB || g.epi == MXR) return hipGetLastError();
+  }
   switch (g.epi) {
     case WAM_EPI_BF16: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_BF16>), grid, block, 0, s, g, tm, tn); break;
     case WAM_EPI_GELU_BF16: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_GELU_BF16>), grid, block, 0, s, g, tm, tn); break;
@@ -648,6 +780,18 @@ hipError_t launch_cfg2(const GemmArgs& g, int c1, hipStream_t s) {
   const long t = (long)tm1 * c1 + (long)tm2 * tn2;
   const int ga = persistent_grid<Ca>(t), gb = persistent_grid<Cb>(t);
   dim3 grid(ga < gb ? ga : gb), block(Ca::NT);
+  if constexpr (Ca::EB == 1) {  // the block-scaled FP8 variants
+    constexpr int MXB = WAM_EPI_MXA | WAM_EPI_BF16, MXR = WAM_EPI_MXA | WAM_EPI_RESID_F32;
+    switch (g.epi) {
+      case WAM_EPI_GELU_MX8:
+        hipLaunchKernelGGL((gemm_nt2<Ca, Cb, WAM_EPI_GELU_MX8>), grid, block, 0, s, g, tm1, c1, tm2, tn2);
+        break;
+      case MXB: hipLaunchKernelGGL((gemm_nt2<Ca, Cb, MXB>), grid, block, 0, s, g, tm1, c1, tm2, tn2); break;
+      case MXR: hipLaunchKernelGGL((gemm_nt2<Ca, Cb, MXR>), grid, block, 0, s, g, tm1, c1, tm2, tn2); break;
+      default: break;
+    }
+    if (g.epi == WAM_EPI_GELU_MX8 || g.epi == MXB || g.epi == MXR) return hipGetLastError();
+  }
   switch (g.epi) {
     case WAM_EPI_BF16: hipLaunchKernelGGL((gemm_nt2<Ca, Cb, WAM_EPI_BF16>), grid, block, 0, s, g, tm1, c1, tm2, tn2); break;
     case WAM_EPI_GELU_BF16:

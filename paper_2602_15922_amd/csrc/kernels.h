@@ -58,9 +58,23 @@ struct GemmArgs {
   // FP8 operands (E4M3 A and W, one byte per element): acc * a_scale[m] * w_scale[n]
   int32_t fp8;
   const float *a_scale, *w_scale;
+  // Block-scaled FP8 A (epi | WAM_EPI_MXA, a_scale NULL): one power-of-two scale per 64
+  // columns of a row, an 8-bit exponent biased by 127; block kb of row m at
+  // a_exp[(kb / 2) * a_lde + 4 m + kb % 2] (pairs of blocks, rows contiguous, 4 bytes
+  // per row of which 2 are used; a_lde a multiple of 4)
+  const uint8_t* a_exp;
+  int64_t a_lde;
+  // epi WAM_EPI_GELU_MX8: the bf16-rounded GELU output as E4M3 codes in out (row stride
+  // ldo bytes) with one exponent per 64 columns in out_exp, laid out as a_exp (o_lde)
+  uint8_t* out_exp;
+  int64_t o_lde;
   // device flag of the denoising loop: while *skip > 0 every workgroup exits at entry (NULL: never)
   const int32_t* skip;
 };
+// Internal epilogue codes beyond the public ones: the GELU output written as block-scaled
+// E4M3, and (or-ed in) block-scaled FP8 A.
+constexpr int WAM_EPI_GELU_MX8 = 4;
+constexpr int WAM_EPI_MXA = 8;
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 // n products sharing A (and, for FP8 operands, its row scales) and every size and stride,
 // each with its own W, bias, output and (FP8) column scales, in one launch; bf16 epilogue.

@@ -164,6 +164,28 @@ def test_fp8_entry_points_reject_bad_arguments_without_a_gpu():
     assert r(1, 4, 2, 128, 4096, 8192, 8192, 24576, 0, 12288, 16384, 20480, 1.0, 8, 0, None) == b.WAM_EINVAL
     assert r(1, 4, 2, 128, 4096, 8192, 8192, 0, 0, 12288, 16384, 20480, 1.0, 8, 5, None) == b.WAM_EINVAL  # row0+L>Lcap
 
+    def gm(M=300, N=256, K=256, epi=b.WAM_EPI_BF16, a_scale=None, a_exp=4096, a_lde=None, out_exp=None, o_lde=0,
+           out=8192):
+        g = b.wam_gemm_desc(M=M, N=N, K=K, epilogue=epi, A=12288, lda=K, a_batch_stride=0, a_rows=0, W=16384,
+                            ldw=K, bias=None, out=out, ldo=N, out_batch_stride=0, out_rows=0, gate_a=None,
+                            gate_v=None, gate_stride=0, gate_rows=0)
+        return L.wam_gemm_fp8_mx(C.byref(g), a_scale, a_exp, 4 * M if a_lde is None else a_lde, 20480, out_exp,
+                                 o_lde, None)
+
+    gelu = b.WAM_EPI_GELU_BF16
+    assert gm(a_scale=24576) == b.WAM_EINVAL and b"exactly one" in L.wam_last_error()
+    assert gm(a_exp=None) == b.WAM_EINVAL
+    assert gm(K=192) == b.WAM_EUNSUPPORTED  # block-scaled A: K % 128
+    assert gm(epi=gelu) == b.WAM_EUNSUPPORTED  # block-scaled A: bf16 or residual epilogue
+    assert gm(a_lde=4 * 300 - 4) == b.WAM_EINVAL and b"a_lde" in L.wam_last_error()
+    assert gm(a_exp=4098) == b.WAM_EINVAL and b"aligned" in L.wam_last_error()
+    assert gm(out_exp=28672, o_lde=1200, epi=gelu) == b.WAM_EUNSUPPORTED  # both sides block-scaled
+    blk_out = dict(a_exp=None, a_scale=24576, out_exp=28672, o_lde=1200)
+    assert gm(epi=b.WAM_EPI_BF16, **blk_out) == b.WAM_EUNSUPPORTED  # a block-scaled output is GELU's
+    assert gm(epi=gelu, N=192, **blk_out) == b.WAM_EUNSUPPORTED  # N % 128
+    assert gm(epi=gelu, out=8194, **blk_out) == b.WAM_EINVAL and b"aligned" in L.wam_last_error()
+    assert gm(epi=gelu, **dict(blk_out, o_lde=1198)) == b.WAM_EINVAL  # o_lde % 4, >= 4 M
+
 
 def _apply_unipc_weights(coef, x0, vels):
     """The documented semantics of wam_unipc_step applied in numpy: returns the final

@@ -176,6 +176,129 @@ def test_gemm_fp8_against_the_unquantized_product():
     assert e <= 6e-2
 
 
+# ------------------------------------------------------- block-scaled projection inputs
+def pack_block_exps(e, lde, fill=0xAB):
+    """Unbiased exponents [M][nb] of 64-column blocks -> the library's layout: per pair of
+    blocks all rows in order, 4 bytes per row, block kb of row m at byte
+    (kb // 2) * lde + 4 m + kb % 2; the two unused bytes of each word hold `fill`."""
+    M, nb = e.shape
+    buf = np.full((nb + 1) // 2 * lde, fill, dtype=np.uint8)
+    kb = np.arange(nb)
+    idx = (kb // 2 * lde + kb % 2)[None, :] + 4 * np.arange(M)[:, None]
+    buf[idx] = (np.asarray(e) + 127).astype(np.uint8)
+    return buf
+
+
+def unpack_block_exps(buf, M, nb, lde):
+    kb = np.arange(nb)
+    idx = (kb // 2 * lde + kb % 2)[None, :] + 4 * np.arange(M)[:, None]
+    return buf[idx].astype(np.int64) - 127
+
+
+def codes_dev(vals):
+    """float64 values on the E4M3 grid -> uint8 codes on the device."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(vals)).to(torch.float8_e4m3fn).view(torch.uint8).cuda()
+
+
+MXA_SHAPES = [(300, 200, 512), (1000, 640, 384), (37, 256, 128), (129, 256, 256), (3152, 5120, 13824)]
+
+
+@pytest.mark.parametrize("M,N,K", MXA_SHAPES)
+@pytest.mark.parametrize("epi", ["bf16", "resid"])
+def test_gemm_fp8_block_scaled_a(M, N, K, epi):
+    """A as E4M3 codes with one power-of-two scale per 64 columns of a row (as FFN1 writes
+    the FFN's hidden activations), blocks spread over 10^-3..10^3 so the exponents differ
+    from block to block, against the oracle's fp64 product of the decoded blocks times the
+    per-channel W scales (fp32 accumulation and the bf16 output rounding remain).  The
+    shapes cover one, two and three slices of 128 columns (fewer than the prefetch ring's
+    stages), ragged row and column tiles, and the FFN2 shape (oracle on sampled rows)."""
+    import torch
+    w = lib()
+    log(f"gemm fp8 block-scaled A {epi} M={M} N={N} K={K}")
+    g = np.random.default_rng(M + N + K)
+    nb = K // 64
+    x = g.standard_normal((M, K)) * np.repeat(10.0 ** g.uniform(-3, 3, (M, nb)), 64, axis=1)
+    qa, ea = oracle.fp8.quantize_mx(x, 64)
+    W = synth.normal(11, "w_f2", (N, K), 0.05, K)
+    bias = synth.normal(11, "b_f2", (N,), 0.1, K, dtype="f32")
+    qw = torch.empty((N, K), dtype=torch.uint8, device="cuda")
+    sw = torch.empty(N, dtype=torch.float32, device="cuda")
+    w.wam_quantize_rows_fp8(dev(W), qw, sw)
+    lde = 4 * M + 64
+    exps = torch.from_numpy(pack_block_exps(ea, lde)).cuda()
+    a8 = codes_dev(qa)
+    rows = np.arange(M) if M <= 1000 else sampled_rows(M)
+    acc = oracle.fp8.fp8_linear(oracle.fp8.decode_mx(qa[rows], ea[rows], 64), np.ones(len(rows)), decode(qw),
+                                host(sw), bias.f64)
+    if epi == "bf16":
+        out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+        w.wam_gemm_fp8_mx(a8, qw, out, w.WAM_EPI_BF16, sw, a_exp=exps, a_lde=lde, bias=dev(bias))
+        torch.cuda.synchronize()
+        assert rel_l2(host(out)[rows], acc) <= 3e-3
+    else:
+        x0 = synth.normal(11, "e0", (M, N), 1.0, K, dtype="f32")
+        ga = synth.normal(11, "mod6", (N,), 0.5, K, dtype="f32")
+        out = dev(x0)
+        w.wam_gemm_fp8_mx(a8, qw, out, w.WAM_EPI_RESID_F32, sw, a_exp=exps, a_lde=lde, bias=dev(bias),
+                          gate_a=dev(ga))
+        torch.cuda.synchronize()
+        upd = host(out)[rows] - x0.f64[rows]
+        assert rel_l2(upd, ga.f64[None] * acc) <= 5e-5
+
+
+def sampled_rows(M):
+    """Row-tile boundaries of the 128-, 192- and 256-row tiles and the ragged end, plus random rows."""
+    r = {0, 1, M - 1, M - 2}
+    for t in (128, 192, 256):
+        for b in range(t, M, t):
+            r.update([b - 1, b])
+    r.update(np.random.default_rng(M).integers(0, M, 24).tolist())
+    return np.array(sorted(i for i in r if 0 <= i < M))
+
+
+MX8_SHAPES = [(300, 512, 512), (130, 1280, 256), (3152, 13824, 5120)]
+
+
+@pytest.mark.parametrize("M,N,K", MX8_SHAPES)
+def test_gemm_fp8_gelu_block_output(M, N, K):
+    """The GELU epilogue written block-scaled is, bit for bit, the oracle's 64-element MX
+    quantization of the bf16 GELU output that wam_gemm_fp8 writes for the same inputs:
+    every code and exponent (the same accumulators, the same bf16 rounding, the block
+    exponent rule of wam_quantize_mx_fp8), the unused exponent bytes untouched.  The last
+    shape is FFN1's (two column ranges of 256- and 192-row tiles), checked on sampled rows."""
+    import torch
+    w = lib()
+    log(f"gemm fp8 gelu block output M={M} N={N} K={K}")
+    A = synth.normal(12, "x", (M, K), 1.0, K)
+    W = synth.normal(12, "w_f1", (N, K), 0.05, K)
+    bias = synth.normal(12, "b_f1", (N,), 0.1, K, dtype="f32")
+    qa = torch.empty((M, K), dtype=torch.uint8, device="cuda")
+    qw = torch.empty((N, K), dtype=torch.uint8, device="cuda")
+    sa = torch.empty(M, dtype=torch.float32, device="cuda")
+    sw = torch.empty(N, dtype=torch.float32, device="cuda")
+    w.wam_quantize_rows_fp8(dev(A), qa, sa)
+    w.wam_quantize_rows_fp8(dev(W), qw, sw)
+    bd = dev(bias)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    w.wam_gemm_fp8(qa, qw, y, w.WAM_EPI_GELU_BF16, sa, sw, bias=bd)
+    lde = 4 * M + 32
+    nb = N // 64
+    u8 = torch.full((M, N), 0x7F, dtype=torch.uint8, device="cuda")
+    ue = torch.full(((nb + 1) // 2 * lde,), 0xAB, dtype=torch.uint8, device="cuda")
+    w.wam_gemm_fp8_mx(qa, qw, u8, w.WAM_EPI_GELU_BF16, sw, a_scale=sa, out_exp=ue, o_lde=lde, bias=bd)
+    torch.cuda.synchronize()
+    rows = np.arange(M) if M <= 1000 else sampled_rows(M)
+    q, e = oracle.fp8.quantize_mx(host(y)[rows], 64)
+    assert np.array_equal(decode(u8)[rows], q)
+    ueh = ue.cpu().numpy()
+    assert np.array_equal(unpack_block_exps(ueh, M, nb, lde)[rows], e)
+    used = np.zeros(ueh.size, bool)
+    kb = np.arange(nb)
+    used[((kb // 2 * lde + kb % 2)[None, :] + 4 * np.arange(M)[:, None]).ravel()] = True
+    assert np.all(ueh[~used] == 0xAB)
+
+
 # ------------------------------------------------------------------------------ FP8 blocks
 # Against the fp64 oracle of the unquantized model: each FP8 projection carries ~4%
 # relative error (measured above at the QKV shape) and a branch chains up to three of
