@@ -608,6 +608,22 @@ wam_status wam_gemm_fp8(const wam_gemm_desc* g, const float* a_scale, const floa
 wam_status wam_gemm_fp8_mx(const wam_gemm_desc* g, const float* a_scale, const void* a_exp, int64_t a_lde,
                            const float* w_scale, void* out_exp, int64_t o_lde, hipStream_t stream);
 
+/* wam_attn_blockcausal_mx / wam_attn_blockcausal_fp8_mx: the attentions above (same
+ * arguments and arithmetic, Dh = 128) with the output written block-scaled for the FP8
+ * projection that reads it (the attention output projection, Section 3.2.4, Appendix D.2):
+ * each row's output is rounded to bf16 as the plain entry point stores it, then each head's
+ * dims 0-63 and 64-127 are a block quantized by wam_gemm_fp8_mx's rule.  o8 receives the
+ * E4M3 codes (one byte per element; o_tok_stride and o_batch_stride in bytes, o_batch_stride
+ * = Lq * o_tok_stride when B > 1; 4-byte aligned); for output row m = b * Lq + query the
+ * exponents of head h's two blocks are at o_exp[h * o_lde + 4 m + {0, 1}] (o_lde a multiple
+ * of 4, >= 4 B Lq; o_exp 4-byte aligned), i.e. the a_exp layout of wam_gemm_fp8_mx with K =
+ * H * 128. */
+wam_status wam_attn_blockcausal_mx(const wam_attn_desc* desc, const void* q, const void* k, const void* v,
+                                   void* o8, void* o_exp, int64_t o_lde, hipStream_t stream);
+wam_status wam_attn_blockcausal_fp8_mx(const wam_attn_desc* desc, const void* q8, const void* q_exp,
+                                       const void* k8, const void* k_exp, const void* v8, float v_scale,
+                                       void* o8, void* o_exp, int64_t o_lde, hipStream_t stream);
+
 /* Patch and action embedding into the fp32 residual x [B][Lv+A][d]. */
 size_t wam_embed_workspace_bytes(const wam_dims* dims, int32_t B, int32_t F, int32_t Hl, int32_t Wl);
 wam_status wam_embed_fwd(const wam_model* m, int32_t B, int32_t F, int32_t Hl, int32_t Wl,

@@ -34,6 +34,7 @@ EXPORTED = (
     "wam_chunk_positions", "wam_rope_tables", "wam_attn_blockcausal_fp8", "wam_quantize_mx_fp8",
     "wam_quantize_scaled_fp8", "wam_rope_qkv_fp8", "wam_unipc_plan", "wam_unipc_step",
     "wam_cosine_similarity_noalloc", "wam_adaln_ln_mod_fp8", "wam_gemm_fp8_mx",
+    "wam_attn_blockcausal_mx", "wam_attn_blockcausal_fp8_mx",
 )
 
 _vp, _fp, _i32, _i64, _sz = C.c_void_p, C.POINTER(C.c_float), C.c_int32, C.c_int64, C.c_size_t
@@ -173,6 +174,9 @@ def lib():
         L.wam_gemm_bf16.argtypes = [C.POINTER(wam_gemm_desc), _vp]
         L.wam_gemm_fp8.argtypes = [C.POINTER(wam_gemm_desc), _vp, _vp, _vp]
         L.wam_gemm_fp8_mx.argtypes = [C.POINTER(wam_gemm_desc), _vp, _vp, _i64, _vp, _vp, _i64, _vp]
+        L.wam_attn_blockcausal_mx.argtypes = [C.POINTER(wam_attn_desc), _vp, _vp, _vp, _vp, _vp, _i64, _vp]
+        L.wam_attn_blockcausal_fp8_mx.argtypes = [C.POINTER(wam_attn_desc), _vp, _vp, _vp, _vp, _vp, C.c_float,
+                                                  _vp, _vp, _i64, _vp]
         L.wam_quantize_rows_fp8.argtypes = [_i32, _i32, _vp, _i64, _vp, _i64, _vp, _vp]
         L.wam_adaln_ln_mod_fp8.argtypes = [_i32, _i32, _i32, C.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64,
                                            _vp, _i64, _vp, _vp]
@@ -289,6 +293,35 @@ def wam_attn_blockcausal_fp8(q8, q_exp, k8, k_exp, v8, v_scale, o, chunks: wam_c
             raise ValueError("exponent strides must be the code strides / Dh")
     _check(lib().wam_attn_blockcausal_fp8(C.byref(d), _p(q8), _p(q_exp), _p(k8), _p(k_exp), _p(v8), v_scale,
                                           _p(o), _stream(stream)))
+
+
+def wam_attn_blockcausal_mx(q, k, v, o8, o_exp, o_lde: int, chunks: wam_chunks, scale: float = 0.0, stream=None):
+    """wam_attn_blockcausal with the output block-scaled: o8 [B, Lq, H, 128] uint8 E4M3 codes,
+    o_exp uint8 (4 bytes per output row per head, stride o_lde between heads)."""
+    B, Lq, H, Dh = q.shape
+    d = wam_attn_desc(B=B, H=H, Dh=Dh, Lq=Lq, Lk=k.shape[1],
+                      q_tok_stride=q.stride(1), q_batch_stride=q.stride(0),
+                      kv_tok_stride=k.stride(1), kv_batch_stride=k.stride(0),
+                      o_tok_stride=o8.stride(1), o_batch_stride=o8.stride(0), scale=scale, ch=chunks)
+    if v.stride(1) != k.stride(1) or v.stride(0) != k.stride(0):
+        raise ValueError("k and v must share token and batch strides")
+    _check(lib().wam_attn_blockcausal_mx(C.byref(d), _p(q), _p(k), _p(v), _p(o8), _p(o_exp), o_lde,
+                                         _stream(stream)))
+
+
+def wam_attn_blockcausal_fp8_mx(q8, q_exp, k8, k_exp, v8, v_scale, o8, o_exp, o_lde: int, chunks: wam_chunks,
+                                scale: float = 0.0, stream=None):
+    """wam_attn_blockcausal_fp8 with the output block-scaled (o8 and o_exp as for
+    wam_attn_blockcausal_mx)."""
+    B, Lq, H, Dh = q8.shape
+    d = wam_attn_desc(B=B, H=H, Dh=Dh, Lq=Lq, Lk=k8.shape[1],
+                      q_tok_stride=q8.stride(1), q_batch_stride=q8.stride(0),
+                      kv_tok_stride=k8.stride(1), kv_batch_stride=k8.stride(0),
+                      o_tok_stride=o8.stride(1), o_batch_stride=o8.stride(0), scale=scale, ch=chunks)
+    if v8.stride(1) != k8.stride(1) or v8.stride(0) != k8.stride(0):
+        raise ValueError("k8 and v8 must share token and batch strides")
+    _check(lib().wam_attn_blockcausal_fp8_mx(C.byref(d), _p(q8), _p(q_exp), _p(k8), _p(k_exp), _p(v8), v_scale,
+                                             _p(o8), _p(o_exp), o_lde, _stream(stream)))
 
 
 def wam_quantize_mx_fp8(x, q8, exps, stream=None):

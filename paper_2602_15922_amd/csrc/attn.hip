@@ -296,8 +296,13 @@ WAM_DEV void attn_step(bf16* smem, int cur, __amdgpu_buffer_rsrc_t kr, __amdgpu_
 // query's visible prefix is looked up from its chunk; otherwise (cross-attention to the
 // text, or a single chunk) every query sees all Lk keys and only the ragged last tile
 // is masked.
-template <int DH, bool CHUNKED>
-__global__ __launch_bounds__(NT, 2) void attn_fwd(const AttnArgs a, int nqt) {
+// MX8: the output written block-scaled (store_attn_row_mx8; Dh = 128): E4M3 codes at a.o
+// (strides in bytes), for output row m = b * Lq + query and head h the exponents of dims
+// 0-63 and 64-127 at o_exp[h * o_lde + 4 m + {0, 1}].  (Kernel arguments rather than
+// AttnArgs fields, so that the other instantiations keep their argument layout and code.)
+template <int DH, bool CHUNKED, bool MX8 = false>
+__global__ __launch_bounds__(NT, 2) void attn_fwd(const AttnArgs a, int nqt, uint8_t* o_exp, int64_t o_lde) {
+  static_assert(!MX8 || DH == 128, "the block-scaled output is for Dh = 128");
   constexpr int KS = DH / 16;         // MFMA k-steps over the head dim
   constexpr int MT = DH / 32;         // 32-row tiles of the transposed output
   constexpr int CPR = DH / 8;         // 16-byte chunks per K/V row
@@ -395,7 +400,11 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd(const AttnArgs a, int nqt) {
                         kofs, vofs, c, thr, row_kend, hh);
 
   const float l = l_part + other_half(l_part);
-  if (qrow < a.Lq) {
+  if constexpr (MX8) {
+    uint8_t* o8 = static_cast<uint8_t*>(a.o) + b * a.o_bs + (int64_t)qrow * a.o_ts + h * DH;
+    uint8_t* oe = o_exp + h * o_lde + 4 * ((int64_t)b * a.Lq + qrow);
+    store_attn_row_mx8(o8, oe, acc, 1.0f / l, hh, qrow < a.Lq);
+  } else if (qrow < a.Lq) {
     const float inv = 1.0f / l;
     bf16* ob = static_cast<bf16*>(a.o) + b * a.o_bs + (int64_t)qrow * a.o_ts + h * DH;
 #pragma unroll
@@ -411,16 +420,20 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd(const AttnArgs a, int nqt) {
 
 }  // namespace
 
-hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
+hipError_t launch_attn(const AttnArgs& a, hipStream_t s, uint8_t* o_exp, int64_t o_lde) {
   const int nqt = (a.Lq + BM - 1) / BM;
   const dim3 grid((unsigned)((long)nqt * a.H * a.B)), block(NT);
   const bool chunked = a.n_k_chunks > 1;
-  if (a.Dh == 128) {
-    if (chunked) hipLaunchKernelGGL((attn_fwd<128, true>), grid, block, 0, s, a, nqt);
-    else hipLaunchKernelGGL((attn_fwd<128, false>), grid, block, 0, s, a, nqt);
+  uint8_t* const z = nullptr;
+  if (o_exp) {  // block-scaled output (Dh = 128, checked by the host)
+    if (chunked) hipLaunchKernelGGL((attn_fwd<128, true, true>), grid, block, 0, s, a, nqt, o_exp, o_lde);
+    else hipLaunchKernelGGL((attn_fwd<128, false, true>), grid, block, 0, s, a, nqt, o_exp, o_lde);
+  } else if (a.Dh == 128) {
+    if (chunked) hipLaunchKernelGGL((attn_fwd<128, true>), grid, block, 0, s, a, nqt, z, (int64_t)0);
+    else hipLaunchKernelGGL((attn_fwd<128, false>), grid, block, 0, s, a, nqt, z, (int64_t)0);
   } else {
-    if (chunked) hipLaunchKernelGGL((attn_fwd<64, true>), grid, block, 0, s, a, nqt);
-    else hipLaunchKernelGGL((attn_fwd<64, false>), grid, block, 0, s, a, nqt);
+    if (chunked) hipLaunchKernelGGL((attn_fwd<64, true>), grid, block, 0, s, a, nqt, z, (int64_t)0);
+    else hipLaunchKernelGGL((attn_fwd<64, false>), grid, block, 0, s, a, nqt, z, (int64_t)0);
   }
   return hipGetLastError();
 }

@@ -224,8 +224,9 @@ WAM_DEV void tile_sync() {
   __syncthreads();
 }
 
-template <bool CHUNKED>
-__global__ __launch_bounds__(NT, 2) void attn_fwd_fp8(const AttnFp8Args f, int nqt) {
+// MX8: the output written block-scaled, laid out as attn_fwd's.
+template <bool CHUNKED, bool MX8 = false>
+__global__ __launch_bounds__(NT, 2) void attn_fwd_fp8(const AttnFp8Args f, int nqt, uint8_t* o_exp, int64_t o_lde) {
   constexpr int CPR = ROWB / 16;       // 16-byte chunks per code row
   constexpr int KCH = BN * CPR / NT;   // chunks of K (and of V) per thread
   __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
@@ -344,7 +345,11 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_fp8(const AttnFp8Args f, int n
   }
 
   const float lsum = accl[0] + other_half(accl[0]);  // one of the two is zero
-  if (qrow < a.Lq) {
+  if constexpr (MX8) {
+    uint8_t* o8 = static_cast<uint8_t*>(a.o) + b * a.o_bs + (int64_t)qrow * a.o_ts + h * DH;
+    uint8_t* oe = o_exp + h * o_lde + 4 * ((int64_t)b * a.Lq + qrow);
+    store_attn_row_mx8(o8, oe, acc, f.v_scale / lsum, hh, qrow < a.Lq);
+  } else if (qrow < a.Lq) {
     const float inv = f.v_scale / lsum;
     bf16* ob = static_cast<bf16*>(a.o) + b * a.o_bs + (int64_t)qrow * a.o_ts + h * DH;
 #pragma unroll
@@ -360,12 +365,19 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_fp8(const AttnFp8Args f, int n
 
 }  // namespace
 
-hipError_t launch_attn_fp8(const AttnFp8Args& f, hipStream_t s) {
+hipError_t launch_attn_fp8(const AttnFp8Args& f, hipStream_t s, uint8_t* o_exp, int64_t o_lde) {
   const AttnArgs& a = f.a;
   const int nqt = (a.Lq + BM - 1) / BM;
   const dim3 grid((unsigned)((long)nqt * a.H * a.B)), block(NT);
-  if (a.n_k_chunks > 1) hipLaunchKernelGGL((attn_fwd_fp8<true>), grid, block, 0, s, f, nqt);
-  else hipLaunchKernelGGL((attn_fwd_fp8<false>), grid, block, 0, s, f, nqt);
+  const bool chunked = a.n_k_chunks > 1;
+  if (o_exp) {  // block-scaled output
+    if (chunked) hipLaunchKernelGGL((attn_fwd_fp8<true, true>), grid, block, 0, s, f, nqt, o_exp, o_lde);
+    else hipLaunchKernelGGL((attn_fwd_fp8<false, true>), grid, block, 0, s, f, nqt, o_exp, o_lde);
+  } else {
+    uint8_t* const z = nullptr;
+    if (chunked) hipLaunchKernelGGL((attn_fwd_fp8<true>), grid, block, 0, s, f, nqt, z, (int64_t)0);
+    else hipLaunchKernelGGL((attn_fwd_fp8<false>), grid, block, 0, s, f, nqt, z, (int64_t)0);
+  }
   return hipGetLastError();
 }
 

@@ -74,6 +74,7 @@ struct DryScope {
   } while (0)
 
 bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+bool al4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3) == 0; }
 
 wam_status need_ptr(const void* p, const char* name) {
   if (!p) return fail(WAM_EINVAL, "%s is NULL", name);
@@ -125,8 +126,19 @@ wam_status check_dims(const wam_dims& D) {
 // ---------------------------------------------------------------------------------
 // attention
 // ---------------------------------------------------------------------------------
+// o_exp non-NULL: the output block-scaled (codes at o, one byte per element, strides in
+// bytes; exponents at o_exp, see wam_attn_blockcausal_mx).
+wam_status attn_out_blocks_check(const wam_attn_desc& d, const void* o, const void* o_exp, int64_t o_lde) {
+  CHECK(d.Dh == 128, WAM_EUNSUPPORTED, "a block-scaled attention output needs Dh=128 (got %d)", d.Dh);
+  CHECK(d.B <= 1 || d.o_batch_stride == (int64_t)d.Lq * d.o_tok_stride, WAM_EINVAL,
+        "a block-scaled output takes plain rows (o_batch_stride = Lq * o_tok_stride)");
+  CHECK(o_lde % 4 == 0 && o_lde >= 4 * (int64_t)d.B * d.Lq, WAM_EINVAL, "o_lde must be a multiple of 4, >= 4*B*Lq");
+  CHECK(al4(o) && al4(o_exp), WAM_EINVAL, "o and o_exp must be 4-byte aligned");
+  return WAM_OK;
+}
+
 wam_status attn_checked(const wam_attn_desc& d, const void* q, const void* k, const void* v, void* o,
-                        hipStream_t s) {
+                        hipStream_t s, void* o_exp = nullptr, int64_t o_lde = 0) {
   CHECK(d.Dh == 64 || d.Dh == 128, WAM_EUNSUPPORTED, "Dh=%d (supported: 64, 128)", d.Dh);
   CHECK(d.B >= 0 && d.H >= 1 && d.Lq >= 0 && d.Lk >= 0, WAM_EINVAL, "negative size (B=%d H=%d Lq=%d Lk=%d)",
         d.B, d.H, d.Lq, d.Lk);
@@ -160,17 +172,18 @@ wam_status attn_checked(const wam_attn_desc& d, const void* q, const void* k, co
   a.n_k_chunks = d.ch.n_k_chunks;
   a.n_q_chunks = d.ch.n_q_chunks;
   for (int i = 0; i <= d.ch.n_q_chunks; ++i) a.q_off[i] = d.ch.q_off[i];
-  LAUNCH(launch_attn(pred(a), s));
+  if (o_exp) TRY(attn_out_blocks_check(d, o, o_exp, o_lde));
+  LAUNCH(launch_attn(pred(a), s, static_cast<uint8_t*>(o_exp), o_lde));
   return WAM_OK;
 }
 
-bool al4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3) == 0; }
 
 // FP8 attention (Dh = 128): codes addressed like the bf16 operands with one byte per
 // element; each (token, head) has one uint32 of block exponents, so the exponent arrays'
 // strides are the code strides / Dh.
 wam_status attn_fp8_checked(const wam_attn_desc& d, const void* q, const void* qe, const void* k, const void* ke,
-                            const void* v, float v_scale, void* o, hipStream_t s) {
+                            const void* v, float v_scale, void* o, hipStream_t s, void* o_exp = nullptr,
+                            int64_t o_lde = 0) {
   CHECK(d.Dh == 128, WAM_EUNSUPPORTED, "FP8 attention needs Dh=128 (got %d)", d.Dh);
   CHECK(d.B >= 0 && d.H >= 1 && d.Lq >= 0 && d.Lk >= 0, WAM_EINVAL, "negative size (B=%d H=%d Lq=%d Lk=%d)",
         d.B, d.H, d.Lq, d.Lk);
@@ -212,7 +225,8 @@ wam_status attn_fp8_checked(const wam_attn_desc& d, const void* q, const void* q
   f.qe_ts = d.q_tok_stride / 128; f.qe_bs = d.q_batch_stride / 128;
   f.ke_ts = d.kv_tok_stride / 128; f.ke_bs = d.kv_batch_stride / 128;
   f.v_scale = v_scale;
-  LAUNCH(launch_attn_fp8(f, s));
+  if (o_exp) TRY(attn_out_blocks_check(d, o, o_exp, o_lde));
+  LAUNCH(launch_attn_fp8(f, s, static_cast<uint8_t*>(o_exp), o_lde));
   return WAM_OK;
 }
 
@@ -503,16 +517,28 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   ad.kv_tok_stride = d; ad.kv_batch_stride = (int64_t)io.Lcap * d;
   ad.o_tok_stride = d; ad.o_batch_stride = (int64_t)L * d;
   ad.ch = io.ch;
+  // With FP8 weights both attentions write their output block-scaled: E4M3 codes [M][d] at
+  // o, behind them the exponents of each row's 64-dim blocks (4 bytes per row per head), and
+  // the O and cross-O projections read it as it is, with no quantization pass before them.
+  const bool attn_blocks = F8 && D.Dh == 128;
+  char* oe = static_cast<char*>(o) + align256((size_t)M * d);
+  const int64_t oe_ld = 4 * (int64_t)M;
+  void* const oe_or_null = attn_blocks ? oe : nullptr;
   TRY(mark(ev, WAM_EV_SELF_ATTN, 0, s));
-  if (io.k_exp) TRY(attn_fp8_checked(ad, q, qe, io.k_cache, io.k_exp, io.v_cache, io.v_scale, o, s));
-  else TRY(attn_checked(ad, q, io.k_cache, io.v_cache, o, s));
+  if (io.k_exp) TRY(attn_fp8_checked(ad, q, qe, io.k_cache, io.k_exp, io.v_cache, io.v_scale, o, s, oe_or_null, oe_ld));
+  else TRY(attn_checked(ad, q, io.k_cache, io.v_cache, o, s, oe_or_null, oe_ld));
   TRY(mark(ev, WAM_EV_SELF_ATTN, 1, s));
   // 5. x += gate1 * (o W_o^T + b_o)
   {
     wam_gemm_desc g = gemm(M, d, d, WAM_EPI_RESID_F32, o, d, W.w_o, W.b_o, io.x, d);
     g.gate_a = m6 + 2 * d; g.gate_v = e0 + 2 * d; g.gate_stride = ms; g.gate_rows = L;
     TRY(mark(ev, WAM_EV_O, 0, s));
-    TRY(proj(g, F8 ? F8->w_o : nullptr, F8 ? F8->s_o : nullptr, q8, qs, s, seg, alt));
+    if (attn_blocks) {
+      g.W = F8->w_o; g.ldw = d;
+      TRY(gemm_fp8_blocks(g, nullptr, oe, oe_ld, F8->s_o, nullptr, 0, s, seg, alt));
+    } else {
+      TRY(proj(g, F8 ? F8->w_o : nullptr, F8 ? F8->s_o : nullptr, q8, qs, s, seg, alt));
+    }
     TRY(mark(ev, WAM_EV_O, 1, s));
   }
   // 6. cross-attention LayerNorm (affine, no modulation)
@@ -542,12 +568,17 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   cd.o_tok_stride = d; cd.o_batch_stride = (int64_t)L * d;
   cd.ch = single_chunk(L, io.Lc);
   TRY(mark(ev, WAM_EV_CROSS_ATTN, 0, s));
-  TRY(attn_checked(cd, q, kv, static_cast<const char*>(kv) + (size_t)d * 2, o, s));
+  TRY(attn_checked(cd, q, kv, static_cast<const char*>(kv) + (size_t)d * 2, o, s, oe_or_null, oe_ld));
   TRY(mark(ev, WAM_EV_CROSS_ATTN, 1, s));
   // 10. x += o W_co^T + b_co (no gate)
   TRY(mark(ev, WAM_EV_CO, 0, s));
-  TRY(proj(gemm(M, d, d, WAM_EPI_RESID_F32, o, d, W.w_co, W.b_co, io.x, d), F8 ? F8->w_co : nullptr,
-           F8 ? F8->s_co : nullptr, q8, qs, s));
+  if (attn_blocks) {
+    wam_gemm_desc g = gemm(M, d, d, WAM_EPI_RESID_F32, o, d, F8->w_co, W.b_co, io.x, d);
+    TRY(gemm_fp8_blocks(g, nullptr, oe, oe_ld, F8->s_co, nullptr, 0, s));
+  } else {
+    TRY(proj(gemm(M, d, d, WAM_EPI_RESID_F32, o, d, W.w_co, W.b_co, io.x, d), F8 ? F8->w_co : nullptr,
+             F8 ? F8->s_co : nullptr, q8, qs, s));
+  }
   TRY(mark(ev, WAM_EV_CO, 1, s));
   // 11. AdaLN #2
   LnArgs l2{M, L, d, D.eps, io.x, nullptr, nullptr, m6 + 3 * d, e0 + 3 * d, m6 + 4 * d, e0 + 4 * d, ms, h, seg, alt};
@@ -1179,6 +1210,13 @@ wam_status wam_attn_blockcausal(const wam_attn_desc* desc, const void* q, const 
   return attn_checked(*desc, q, k, v, o, stream);
 }
 
+wam_status wam_attn_blockcausal_mx(const wam_attn_desc* desc, const void* q, const void* k, const void* v, void* o8,
+                                   void* o_exp, int64_t o_lde, hipStream_t stream) {
+  CHECK(desc != nullptr, WAM_EINVAL, "desc is NULL");
+  CHECK(o_exp != nullptr || desc->B == 0 || desc->Lq == 0, WAM_EINVAL, "o_exp is NULL");
+  return attn_checked(*desc, q, k, v, o8, stream, o_exp, o_lde);
+}
+
 wam_status wam_gemm_bf16(const wam_gemm_desc* g, hipStream_t stream) {
   CHECK(g != nullptr, WAM_EINVAL, "desc is NULL");
   return gemm_checked(*g, stream);
@@ -1270,6 +1308,14 @@ wam_status wam_attn_blockcausal_fp8(const wam_attn_desc* desc, const void* q8, c
                                     const void* k_exp, const void* v8, float v_scale, void* o, hipStream_t stream) {
   CHECK(desc != nullptr, WAM_EINVAL, "NULL descriptor");
   return attn_fp8_checked(*desc, q8, q_exp, k8, k_exp, v8, v_scale, o, stream);
+}
+
+wam_status wam_attn_blockcausal_fp8_mx(const wam_attn_desc* desc, const void* q8, const void* q_exp, const void* k8,
+                                       const void* k_exp, const void* v8, float v_scale, void* o8, void* o_exp,
+                                       int64_t o_lde, hipStream_t stream) {
+  CHECK(desc != nullptr, WAM_EINVAL, "NULL descriptor");
+  CHECK(o_exp != nullptr || desc->B == 0 || desc->Lq == 0, WAM_EINVAL, "o_exp is NULL");
+  return attn_fp8_checked(*desc, q8, q_exp, k8, k_exp, v8, v_scale, o8, stream, o_exp, o_lde);
 }
 
 wam_status wam_quantize_mx_fp8(int32_t rows, int32_t cols, const void* x, int64_t ldx, void* q8, int64_t ldq,

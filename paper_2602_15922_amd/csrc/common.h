@@ -41,6 +41,48 @@ WAM_DEV f32x16 mfma32_fp8_sa(i32x8 a, i32x8 b, f32x16 c, int sa, int sel) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 1, sa, 0, 127);
 }
 
+// The value of lane l ^ 32 (the other half of the wavefront).
+WAM_DEV float half_swap(float v) {
+  const unsigned u = __float_as_uint(v);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
+}
+
+WAM_DEV int mx_exp_biased(float amax);
+
+// One query row of an attention output (Dh = 128) as block-scaled E4M3: acc[mt][r] holds
+// dims 32 mt + 8 (r / 4) + 4 hh + r % 4 of the lane's query (lane l ^ 32 the other hh),
+// o = acc * inv.  The output is rounded to bf16 first, as the bf16 store writes it; dims
+// 0-63 (mt 0, 1) and 64-127 (mt 2, 3) are the two 64-element blocks, each with the exponent
+// of mx_exp_biased.  Codes go to o8 (the head's 128 bytes of the row), the two exponents
+// to oe[0] and oe[1].  Every lane calls it (the block maximum takes the other half's);
+// only rows with valid set store.
+WAM_DEV void store_attn_row_mx8(uint8_t* o8, uint8_t* oe, const f32x16* acc, float inv, int hh, bool valid) {
+  float y[4][16], am[2] = {0.f, 0.f};
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      y[mt][r] = (float)(bf16)(acc[mt][r] * inv);
+      am[mt >> 1] = fmaxf(am[mt >> 1], fabsf(y[mt][r]));
+    }
+#pragma unroll
+  for (int k = 0; k < 2; ++k) am[k] = fmaxf(am[k], half_swap(am[k]));
+  const int e0 = mx_exp_biased(am[0]), e1 = mx_exp_biased(am[1]);
+  const float mul[2] = {ldexpf(1.0f, 127 - e0), ldexpf(1.0f, 127 - e1)};  // |y| * mul <= 448
+  if (!valid) return;
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const float k = mul[mt >> 1];
+      int code = __builtin_amdgcn_cvt_pk_fp8_f32(y[mt][4 * rr] * k, y[mt][4 * rr + 1] * k, 0, false);
+      code = __builtin_amdgcn_cvt_pk_fp8_f32(y[mt][4 * rr + 2] * k, y[mt][4 * rr + 3] * k, code, true);
+      *reinterpret_cast<int*>(o8 + 32 * mt + 8 * rr + 4 * hh) = code;
+    }
+  if (hh == 0) *reinterpret_cast<uint16_t*>(oe) = (uint16_t)(e0 | (e1 << 8));
+}
+
 // Biased (127) exponent of an MX block with largest magnitude amax (finite, >= 0): the
 // smallest e with amax <= 448 * 2^e, clamped to [-127, 127]; 0 (byte 127) for a zero
 // block.  From the bits: amax = m 2^E' with m in [1, 2) takes e = E' - 8 if m <= 1.75

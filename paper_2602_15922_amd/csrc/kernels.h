@@ -23,7 +23,10 @@ struct AttnArgs {
   // device flag of the denoising loop: while *skip > 0 every workgroup exits at entry (NULL: never)
   const int32_t* skip;
 };
-hipError_t launch_attn(const AttnArgs& a, hipStream_t s);
+// o_exp non-NULL (Dh = 128): the output as block-scaled E4M3 (codes at a.o, strides in bytes;
+// for output row m = b * Lq + query and head h the exponents of dims 0-63 and 64-127 at
+// o_exp[h * o_lde + 4 m + {0, 1}]), the bf16-rounded values quantized by the MX rule.
+hipError_t launch_attn(const AttnArgs& a, hipStream_t s, uint8_t* o_exp = nullptr, int64_t o_lde = 0);
 
 // FP8 attention (Dh = 128): a.q / a.k / a.v point at E4M3 codes (strides in bytes), a.o
 // at bf16 output; q_exp / k_exp hold one uint32 per (token, head), byte j the biased
@@ -35,7 +38,7 @@ struct AttnFp8Args {
   int64_t qe_ts, qe_bs, ke_ts, ke_bs;
   float v_scale;
 };
-hipError_t launch_attn_fp8(const AttnFp8Args& f, hipStream_t s);
+hipError_t launch_attn_fp8(const AttnFp8Args& f, hipStream_t s, uint8_t* o_exp = nullptr, int64_t o_lde = 0);
 
 struct GemmArgs {
   int32_t M, N, K, epi;

@@ -186,6 +186,25 @@ def test_fp8_entry_points_reject_bad_arguments_without_a_gpu():
     assert gm(epi=gelu, out=8194, **blk_out) == b.WAM_EINVAL and b"aligned" in L.wam_last_error()
     assert gm(epi=gelu, **dict(blk_out, o_lde=1198)) == b.WAM_EINVAL  # o_lde % 4, >= 4 M
 
+    def am(Dh=128, o8=24576, oe=28672, lde=80, fp8=False, **kw):
+        d = b.wam_attn_desc(B=2, H=2, Dh=Dh, Lq=10, Lk=20, q_tok_stride=256, q_batch_stride=2560,
+                            kv_tok_stride=256, kv_batch_stride=5120, o_tok_stride=256, o_batch_stride=2560,
+                            scale=0.0, ch=w.make_chunks([10, 10], [10], [1]))
+        for k_, v_ in kw.items():
+            setattr(d, k_, v_)
+        if fp8:
+            return L.wam_attn_blockcausal_fp8_mx(C.byref(d), 4096, 8192, 12288, 16384, 20480, 1.0, o8, oe, lde, None)
+        return L.wam_attn_blockcausal_mx(C.byref(d), 4096, 12288, 20480, o8, oe, lde, None)
+
+    for f8 in (False, True):
+        assert am(fp8=f8, oe=0) == b.WAM_EINVAL and b"o_exp" in L.wam_last_error()
+        assert am(fp8=f8, lde=76) == b.WAM_EINVAL and b"o_lde" in L.wam_last_error()  # < 4 B Lq
+        assert am(fp8=f8, lde=82) == b.WAM_EINVAL  # not a multiple of 4
+        assert am(fp8=f8, oe=28674) == b.WAM_EINVAL and b"aligned" in L.wam_last_error()
+        assert am(fp8=f8, o_batch_stride=2816) == b.WAM_EINVAL and b"plain rows" in L.wam_last_error()
+    assert am(Dh=64, q_tok_stride=128, kv_tok_stride=128, o_tok_stride=128, q_batch_stride=1280,
+              kv_batch_stride=2560, o_batch_stride=1280) == b.WAM_EUNSUPPORTED
+
 
 def _apply_unipc_weights(coef, x0, vels):
     """The documented semantics of wam_unipc_step applied in numpy: returns the final

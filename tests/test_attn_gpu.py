@@ -180,6 +180,41 @@ def test_attention_one_chunk_short_keys(name, B, H, Lq, Lk):
         assert rel_l2(o[b, rows], ref) <= TOL, (name, b)
 
 
+MX_CASES = [
+    # name, B, H, key chunk sizes, query chunks: Dh = 128
+    ("mx_prefill_masked", 2, 3, [130, 64, 200], [0, 1, 2]),
+    ("mx_cached_ragged", 1, 2, [300, 77], [1]),
+    ("mx_cross_step_shape", 1, 40, [512], [0]),
+]
+
+
+@pytest.mark.parametrize("name,B,H,ks,qc", MX_CASES)
+def test_attention_block_scaled_output(name, B, H, ks, qc):
+    """wam_attn_blockcausal_mx writes, bit for bit, the oracle's 64-element MX quantization
+    (wam_gemm_fp8_mx's rule) of the bf16 output that wam_attn_blockcausal writes for the same
+    inputs, in the a_exp layout of the O projection; the exponent buffer's other bytes are
+    untouched.  The last case is the cross-attention of the step (3152 queries, 512 keys)."""
+    import torch
+    from gpu_helpers import check_block_output
+    case = [c[0] for c in MX_CASES].index(name)
+    w = lib()
+    k_chunk = chunk_ids(ks)
+    off = np.concatenate([[0], np.cumsum(ks)])
+    Lk = int(off[-1])
+    Lq = 3152 if name == "mx_cross_step_shape" else int(sum(ks[c] for c in qc))
+    q, k, v = qkv(400 + case, B, Lq, Lk, H, 128)
+    ch = w.make_chunks(ks, [ks[c] for c in qc] if Lq != 3152 else [Lq], qc)
+    log(f"attn block-scaled output {name} B={B} H={H} Lq={Lq} Lk={Lk}")
+    qd, kd, vd = dev(q), dev(k), dev(v)
+    o = run(qd, kd, vd, ch)
+    o8 = torch.full((B, Lq, H, 128), 0x7F, dtype=torch.uint8, device="cuda")
+    lde = 4 * B * Lq + 16
+    oe = torch.full((H * lde,), 0xAB, dtype=torch.uint8, device="cuda")
+    w.wam_attn_blockcausal_mx(qd, kd, vd, o8, oe, lde, ch)
+    torch.cuda.synchronize()
+    check_block_output(o8.view(B * Lq, H * 128), oe, host(o).reshape(B * Lq, H * 128), lde)
+
+
 def test_attention_full_size_cached_chunk():
     """40 heads x 128, 3152 queries of chunk 2 against 9456 keys (two cached chunks of
     3152 plus the current one), Q/K/V ~ N(0,1); oracle on sampled query rows."""

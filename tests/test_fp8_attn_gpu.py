@@ -230,6 +230,32 @@ def test_attention_fp8_random_operands(name, B, H, ks, qc):
         assert err <= TOL_RANDOM, (name, b, err)
 
 
+@pytest.mark.parametrize("name,B,H,ks,qc", CASES)
+def test_attention_fp8_block_scaled_output(name, B, H, ks, qc):
+    """wam_attn_blockcausal_fp8_mx writes, bit for bit, the oracle's 64-element MX
+    quantization of the bf16 output that wam_attn_blockcausal_fp8 writes for the same
+    operands, in the a_exp layout of the O projection; other exponent bytes untouched."""
+    import torch
+    from gpu_helpers import check_block_output
+    w = lib()
+    case = [c[0] for c in CASES].index(name)
+    k_chunk, q_chunk, Lq, Lk = layout(ks, qc)
+    q = synth.normal(3, "q", (B, Lq, H, 128), 1.0, 700 + case).f64
+    k = synth.normal(3, "k", (B, Lk, H, 128), 1.0, 700 + case).f64
+    v = synth.normal(3, "v", (B, Lk, H, 128), 1.0, 700 + case).f64
+    ops, _ = fp8_operands(q, k, v)
+    ch = w.make_chunks(ks, [ks[c] for c in qc], qc)
+    log(f"attn fp8 block-scaled output {name} B={B} H={H} Lq={Lq} Lk={Lk}")
+    o = host(run_fp8(ops, ch, (B, Lq, H, 128)))
+    o8 = torch.full((B, Lq, H, 128), 0x7F, dtype=torch.uint8, device="cuda")
+    lde = 4 * B * Lq + 8
+    oe = torch.full((H * lde,), 0xAB, dtype=torch.uint8, device="cuda")
+    w.wam_attn_blockcausal_fp8_mx(ops["q8"], ops["q_exp"], ops["k8"], ops["k_exp"], ops["v8"], ops["v_scale"], o8,
+                                  oe, lde, ch)
+    torch.cuda.synchronize()
+    check_block_output(o8.view(B * Lq, H * 128), oe, o.reshape(B * Lq, H * 128), lde)
+
+
 def test_attention_fp8_deterministic_and_future_independent():
     """Bitwise: the same inputs give the same output, and chunk 0's rows do not change
     when chunk 1's keys and values do."""
