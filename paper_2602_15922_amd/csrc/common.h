@@ -113,9 +113,31 @@ WAM_DEV float gelu_tanh_f(float u) {
 
 WAM_DEV float silu_f(float u) { return u / (1.0f + __expf(-u)); }
 
-// 64-lane wavefront reductions
+// 64-lane wavefront reductions (every lane active), with no LDS round trips: within each row
+// of 16 lanes by DPP (the two quad swaps, then the half-row mirror, lane i and 7 - i of each
+// 8, and the row mirror, i and 15 - i), then the four rows' values by readlane.  Every lane
+// gets the same value (each step adds the same two partial values in either lane).
+#define WAM_DPP_F(v, ctrl) __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), ctrl, 0xF, 0xF, true))
 WAM_DEV float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v += WAM_DPP_F(v, 0xB1);   // quad_perm [1, 0, 3, 2]
+  v += WAM_DPP_F(v, 0x4E);   // quad_perm [2, 3, 0, 1]
+  v += WAM_DPP_F(v, 0x141);  // row_half_mirror
+  v += WAM_DPP_F(v, 0x140);  // row_mirror
+  const float a0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float a1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float a2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float a3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return (a0 + a1) + (a2 + a3);
 }
+// the largest of v >= 0 over the wavefront (on the bit patterns: same order as the floats)
+WAM_DEV float wave_max_nonneg(float v) {
+  unsigned u = __float_as_uint(v);
+  u = max(u, (unsigned)__builtin_amdgcn_mov_dpp((int)u, 0xB1, 0xF, 0xF, true));
+  u = max(u, (unsigned)__builtin_amdgcn_mov_dpp((int)u, 0x4E, 0xF, 0xF, true));
+  u = max(u, (unsigned)__builtin_amdgcn_mov_dpp((int)u, 0x141, 0xF, 0xF, true));
+  u = max(u, (unsigned)__builtin_amdgcn_mov_dpp((int)u, 0x140, 0xF, 0xF, true));
+  const unsigned r0 = __builtin_amdgcn_readlane((int)u, 0), r1 = __builtin_amdgcn_readlane((int)u, 16);
+  const unsigned r2 = __builtin_amdgcn_readlane((int)u, 32), r3 = __builtin_amdgcn_readlane((int)u, 48);
+  return __uint_as_float(max(max(r0, r1), max(r2, r3)));
+}
+#undef WAM_DPP_F

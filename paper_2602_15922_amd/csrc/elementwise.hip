@@ -188,8 +188,7 @@ __global__ __launch_bounds__(LN_ROWS * 64, NC <= 10 ? 4 : 2) void ln_mod8_kernel
       }
     }
   if constexpr (Q8) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+    amax = wave_max_nonneg(amax);
     const float inv = amax > 0.f ? 448.0f / amax : 1.0f;
     if (lane == 0) a.q_scale[row] = amax > 0.f ? amax / 448.0f : 1.0f;
     uint8_t* qr = a.q8 + row * a.ldq;
