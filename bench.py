@@ -44,7 +44,7 @@ def parse():
                         "launches at the workload's shape; prints what ran and exits")
     p.add_argument("--probe-attn-fp8", type=int, default=0, metavar="N",
                    help="the same with the FP8 self-attention (operands quantized by the library)")
-    p.add_argument("--probe", choices=("gemm", "ln", "rope", "torch_linear"), default=None,
+    p.add_argument("--probe", choices=("gemm", "gemm_fp8", "ln", "rope", "torch_linear"), default=None,
                    help="counter-collection mode: the calibration copy, then --probe-n launches of each "
                         "of the block's six projections (gemm), of the AdaLN LayerNorm (ln) or of the "
                         "RoPE/KV-append kernel (rope) at the workload's shapes")
@@ -487,6 +487,49 @@ def probe_kernels(wl, kind, n):
                                 gate_v=gate[3] if gated else None, gate_rows=wl.L if gated else 0)
             torch.cuda.synchronize()
             ran.append({"role": name, "M": M, "N": N, "K": K, "epilogue": epi, "launches": n})
+            del A, Wt
+        assert torch.isfinite(x).all()
+    elif kind == "gemm_fp8":
+        # the FP8-attention step's projections: E4M3 operands, per-channel weight scales; QKV,
+        # cross-Q and FFN1 read row-scaled rows (as the LayerNorms write them), O, cross-O and
+        # FFN2 block-scaled ones (as the attentions and FFN1 write them), FFN1 writes its output
+        # block-scaled.  Random codes (no NaN code), unit block exponents: the counters depend
+        # on the shapes and the code path, not on the values.
+        def codes(*shape):
+            c = torch.randint(0, 0x70, shape, generator=g, device="cuda", dtype=torch.int32)
+            return (c | (torch.randint(0, 2, shape, generator=g, device="cuda", dtype=torch.int32) << 7)).to(torch.uint8)
+
+        x = torch.randn(M, d, generator=g, device="cuda")
+        gate = torch.randn(6, d, generator=g, device="cuda") * 0.02
+        roles = (("qkv", d, 3 * d, w.WAM_EPI_BF16, "rows"), ("o", d, d, w.WAM_EPI_RESID_F32, "blocks"),
+                 ("cq", d, d, w.WAM_EPI_BF16, "rows"), ("co", d, d, w.WAM_EPI_RESID_F32, "blocks"),
+                 ("ffn1", d, F, w.WAM_EPI_GELU_BF16, "rows"), ("ffn2", F, d, w.WAM_EPI_RESID_F32, "blocks"))
+        for name, K, N, epi, a_kind in roles:
+            A, Wt = codes(M, K), codes(N, K)
+            sw = torch.rand(N, generator=g, device="cuda") * 1e-3
+            bias = torch.zeros(N, device="cuda")
+            lde = 4 * M
+            if a_kind == "rows":
+                sa, ae = torch.rand(M, generator=g, device="cuda") * 1e-2, None
+            else:
+                sa, ae = None, torch.full(((K // 128) * lde,), 127, dtype=torch.uint8, device="cuda")
+            oe = None
+            if epi == w.WAM_EPI_RESID_F32:
+                out = x
+            elif epi == w.WAM_EPI_GELU_BF16:
+                out = torch.empty(M, N, dtype=torch.uint8, device="cuda")
+                oe = torch.empty(((N // 128) * lde,), dtype=torch.uint8, device="cuda")
+            else:
+                out = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+            gated = name in ("o", "ffn2")
+            torch.cuda.synchronize()
+            for _ in range(n):
+                w.wam_gemm_fp8_mx(A, Wt, out, epi, sw, a_scale=sa, a_exp=ae, a_lde=lde if ae is not None else 0,
+                                  out_exp=oe, o_lde=lde if oe is not None else 0, bias=bias,
+                                  gate_a=gate[2] if gated else None)
+            torch.cuda.synchronize()
+            ran.append({"role": name, "M": M, "N": N, "K": K, "epilogue": epi, "a": a_kind,
+                        "out": "blocks" if oe is not None else "plain", "launches": n})
             del A, Wt
         assert torch.isfinite(x).all()
     elif kind == "ln":
