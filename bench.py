@@ -129,11 +129,14 @@ def role_work(wl, ln_out_bytes=2):
 MI355X_HBM_GBPS = 8000.0  # published HBM3E peak
 
 
-def profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, n_steps, mfma_peak=None, ln_out_bytes=2, **io_kw):
+def profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, n_steps, mfma_peak=None, ln_out_bytes=2, rope_fused=False,
+                   **io_kw):
     """Per-role average launch time over n_steps untimed steps that record events around
     every launch of every block, with each role's achieved rate and fraction of its peak
     (dense MFMA at mfma_peak, bf16's by default, for GEMMs and attention; HBM for LayerNorm
-    and RoPE).  io_kw: extra step inputs (the FP8 KV cache's exponents and scales)."""
+    and RoPE; rope_fused: the step runs RoPE and the K/V append in the QKV projection's
+    epilogue, as the bf16 step does, so its events bracket no launch).  io_kw: extra step
+    inputs (the FP8 KV cache's exponents and scales)."""
     import paper_2602_15922_amd as w
     names = w.binding.BLOCK_EVENT_NAMES
     nk = len(names)
@@ -156,6 +159,10 @@ def profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, n_steps, mfma_peak=N
     for k, name in enumerate(names):
         ms = sums[k] / (n_steps * wl.n_layers)
         unit, amount = work[name]
+        if name == "rope" and rope_fused:
+            out[name] = {"ms": round(ms, 4), "achieved": None, "unit": unit, "frac": None,
+                         "work_per_launch": amount, "fused": "in the QKV projection's epilogue"}
+            continue
         if unit == "TFLOP/s":
             rate = amount / (ms * 1e-3) / 1e12
             peak = mfma_peak or MI355X_BF16_DENSE_TFLOPS
@@ -728,7 +735,7 @@ def main():
         "wall_s_timed": round(wall, 3),
     }
     if args.profile_steps > 0:
-        roles = profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, args.profile_steps)
+        roles = profiled_roles(wl, model, kcs, vcs, inp, vv, va, torch, args.profile_steps, rope_fused=wl.d % 64 == 0)
         rec["gemm_roofline"] = {k: roles[k] for k in ("qkv", "o", "cq", "co", "ffn1", "ffn2")}
         rec["gemm_roofline"]["source"] = (f"events around every launch of every block over {args.profile_steps} "
                                           "untimed steps after the timed ones; peak: bf16 dense MFMA")

@@ -286,8 +286,10 @@ typedef struct {
 /* The launches of a block, in order, that wam_step_io.block_events brackets. */
 typedef enum {
   WAM_EV_LN1 = 0,        /* AdaLN #1                                   */
-  WAM_EV_QKV = 1,        /* fused QKV projection                       */
-  WAM_EV_ROPE = 2,       /* 3D RoPE + KV-cache append                  */
+  WAM_EV_QKV = 1,        /* fused QKV projection (bf16 operands and cache, d % 64 == 0:
+                            with RoPE and the KV-cache append in its epilogue) */
+  WAM_EV_ROPE = 2,       /* 3D RoPE + KV-cache append (brackets no launch when the QKV
+                            projection applies them)                          */
   WAM_EV_SELF_ATTN = 3,  /* block-causal self-attention                */
   WAM_EV_O = 4,          /* output projection + gated residual         */
   WAM_EV_LNC = 5,        /* cross-attention LayerNorm                  */

@@ -391,6 +391,22 @@ wam_status proj_q8(const wam_gemm_desc& g0, const void* w8, const float* s8, cha
   return gemm_checked(g, s, 0, 0, qs, s8);
 }
 
+// The QKV projection with RoPE and the K/V append of rope_qkv_kernel in its epilogue (bf16
+// operands and cache; H * Dh a multiple of 64): the same output bits, without the q|k|v
+// round trip through memory.
+wam_status qkv_rope(const wam_gemm_desc& g, const RopeArgs& r, hipStream_t s) {
+  GemmArgs a;
+  TRY(gemm_prep(g, a));
+  if (a.M == 0) return WAM_OK;
+  a.epi = WAM_EPI_ROPE;
+  a.rope_cos = r.cos_t; a.rope_sin = r.sin_t;
+  a.rope_q = r.q_out; a.rope_k = r.k_cache; a.rope_v = r.v_cache;
+  a.rope_L = r.L; a.rope_Dh = r.Dh; a.rope_d = r.H * r.Dh;
+  a.rope_Lcap = r.Lcap; a.rope_row0 = r.row0;
+  LAUNCH(launch_gemm(pred(a), s));
+  return WAM_OK;
+}
+
 // A LayerNorm that feeds only an FP8 projection writes E4M3 codes and row scales directly.
 void ln_to_fp8(LnArgs& ln, char* q8, float* qs) {
   ln.q8 = reinterpret_cast<uint8_t*>(q8);
@@ -492,21 +508,24 @@ wam_status block_run(const wam_dims& D, const wam_block_weights& W, const wam_bl
   TRY(mark(ev, WAM_EV_LN1, 0, s));
   LAUNCH(launch_ln_mod(pred(ln), s));
   TRY(mark(ev, WAM_EV_LN1, 1, s));
-  // 2. fused QKV projection
+  // 2. fused QKV projection; 3. RoPE on q, k; k, v appended to the cache rows of this chunk
+  // (with an FP8 cache: q and k encoded in 32-dim blocks, q into the q buffer with its
+  // exponents behind it).  With bf16 operands and cache, step 3 runs in step 2's epilogue
+  // and the RoPE events bracket no launch.
+  void* qe = static_cast<char*>(q) + (size_t)M * d;
+  RopeArgs ra{B, L, D.H, D.Dh, io.Lcap, io.cache_len, big, io.rope_cos, io.rope_sin, q, io.k_cache, io.v_cache};
+  const bool rope_epi = !F8 && !io.k_exp && d % 64 == 0;
   TRY(mark(ev, WAM_EV_QKV, 0, s));
   if (ln8) TRY(proj_q8(gemm(M, 3 * d, d, WAM_EPI_BF16, h, d, W.w_qkv, W.b_qkv, big, 3 * d), F8->w_qkv, F8->s_qkv, q8, qs, s));
+  else if (rope_epi) TRY(qkv_rope(gemm(M, 3 * d, d, WAM_EPI_BF16, h, d, W.w_qkv, W.b_qkv, big, 3 * d), ra, s));
   else TRY(proj(gemm(M, 3 * d, d, WAM_EPI_BF16, h, d, W.w_qkv, W.b_qkv, big, 3 * d), F8 ? F8->w_qkv : nullptr,
                 F8 ? F8->s_qkv : nullptr, q8, qs, s));
   TRY(mark(ev, WAM_EV_QKV, 1, s));
-  // 3. RoPE on q, k; k, v appended to the cache rows of this chunk (with an FP8 cache:
-  // q and k encoded in 32-dim blocks, q into the q buffer with its exponents behind it)
-  void* qe = static_cast<char*>(q) + (size_t)M * d;
-  RopeArgs ra{B, L, D.H, D.Dh, io.Lcap, io.cache_len, big, io.rope_cos, io.rope_sin, q, io.k_cache, io.v_cache};
   TRY(mark(ev, WAM_EV_ROPE, 0, s));
   if (io.k_exp) {
     RopeFp8Args rf{pred(ra), qe, io.k_exp, 1.0f / io.v_scale};
     LAUNCH(launch_rope_qkv_fp8(rf, s));
-  } else {
+  } else if (!rope_epi) {
     LAUNCH(launch_rope_qkv(pred(ra), s));
   }
   TRY(mark(ev, WAM_EV_ROPE, 1, s));

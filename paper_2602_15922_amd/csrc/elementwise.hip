@@ -397,10 +397,11 @@ __global__ __launch_bounds__(256) void rope_qkv_kernel(const RopeArgs a) {
   for (int p = 0; p < 4; ++p) {
     const float q0 = (float)qv[2 * p], q1 = (float)qv[2 * p + 1];
     const float k0 = (float)kv[2 * p], k1 = (float)kv[2 * p + 1];
-    qo[2 * p] = (bf16)(q0 * cs[p] - q1 * sn[p]);
-    qo[2 * p + 1] = (bf16)(q0 * sn[p] + q1 * cs[p]);
-    ko[2 * p] = (bf16)(k0 * cs[p] - k1 * sn[p]);
-    ko[2 * p + 1] = (bf16)(k0 * sn[p] + k1 * cs[p]);
+    // the rotation in this fma form wherever it is applied (the QKV epilogue too)
+    qo[2 * p] = (bf16)__builtin_fmaf(q0, cs[p], -(q1 * sn[p]));
+    qo[2 * p + 1] = (bf16)__builtin_fmaf(q0, sn[p], q1 * cs[p]);
+    ko[2 * p] = (bf16)__builtin_fmaf(k0, cs[p], -(k1 * sn[p]));
+    ko[2 * p + 1] = (bf16)__builtin_fmaf(k0, sn[p], k1 * cs[p]);
   }
   if (a.q_out) *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.q_out) + bl * d + col) = qo;
   const int64_t crow = ((int64_t)b * a.Lcap + a.row0 + l) * d + col;

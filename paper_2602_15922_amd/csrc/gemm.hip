@@ -112,6 +112,7 @@ WAM_DEV int64_t gate_off(const GemmArgs& g, int row, float inv) {
 // col + 4): element by element.
 template <int EPI>
 WAM_DEV void epilogue_ragged(const GemmArgs& g, const float inv_o, const float inv_g, int row, int col, f32x4 v) {
+  if constexpr (EPI == WAM_EPI_ROPE) return;  // N = 3 d with d a multiple of 64: no partial column group
   if constexpr (EPI == WAM_EPI_GELU_MX8) return;  // its N is a multiple of 128: never ragged
   const int64_t orow = group_off(row, g.o_rows, inv_o, g.o_bs, g.ldo);
   if (g.a_scale) v *= g.a_scale[row];  // FP8 operands: per-row and per-column scales
@@ -415,6 +416,7 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn, int col0) {
   constexpr int E = EPI & 7;
   static_assert(!C::MXA || C::EB == 1, "block-scaled A is FP8");
   static_assert(E != WAM_EPI_GELU_MX8 || C::EB == 1, "the block-scaled output is an FP8 path's");
+  static_assert(E != WAM_EPI_ROPE || C::EB == 2, "RoPE in the epilogue is a bf16 path's");
   static_assert(LBYTES >= C::STAGES * C::STAGE, "operand ring does not fit");
   constexpr int BM = C::BM, BN = C::BN, BK = C::BK, S = C::STAGES;
   char* smem = lds_ring<LBYTES>();
@@ -562,6 +564,8 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn, int col0) {
     float rmul[NP];
     f32x4 gv[NP], prev[NP];
     int rows[NP];
+    float2 rc[NP], rs[NP];  // RoPE: the lane's two rotation pairs' cos and sin for each row
+    int64_t kvo[NP];        // RoPE: the row's offset in the K/V cache
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
       const int row = row_base + a * 32 + p * RP + rl;
@@ -584,6 +588,17 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn, int col0) {
         for (int p = 0; p < NP; ++p)
           prev[p] = *reinterpret_cast<const f32x4*>(static_cast<const float*>(g.out) +
                                                     group_off(rows[p], g.o_rows, inv_o, g.o_bs, g.ldo) + col);
+      }
+      if constexpr (E == WAM_EPI_ROPE) {
+        const float inv_l = 1.0f / (float)g.rope_L;
+        const int pair0 = ((col % g.rope_d) % g.rope_Dh) >> 1;
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          const int64_t l = group_off(rows[p], g.rope_L, inv_l, 0, 1);
+          rc[p] = *reinterpret_cast<const float2*>(g.rope_cos + l * (g.rope_Dh >> 1) + pair0);
+          rs[p] = *reinterpret_cast<const float2*>(g.rope_sin + l * (g.rope_Dh >> 1) + pair0);
+          kvo[p] = group_off(rows[p], g.rope_L, inv_l, g.rope_Lcap * g.rope_d, g.rope_d) + g.rope_row0 * g.rope_d;
+        }
       }
     }
 #pragma unroll
@@ -627,6 +642,25 @@ WAM_DEV void gemm_tile(const GemmArgs g, int tm, int tn, int col0) {
             const int blk = col_base >> 6;
             g.out_exp[(int64_t)(blk >> 1) * g.o_lde + 4 * rows[p] + (blk & 1)] = (uint8_t)eb;
           }
+        } else if constexpr (E == WAM_EPI_ROPE) {
+          // rounded to bf16 as the projection's output, then rotated in fp32 (q and k)
+          float y[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) y[j] = (float)(bf16)v[j];
+          const int sec = col / g.rope_d, c = col - sec * g.rope_d;  // 0 q, 1 k, 2 v (per lane)
+          bf16x4 o;
+          if (sec < 2) {
+            o[0] = (bf16)__builtin_fmaf(y[0], rc[p].x, -(y[1] * rs[p].x));
+            o[1] = (bf16)__builtin_fmaf(y[0], rs[p].x, y[1] * rc[p].x);
+            o[2] = (bf16)__builtin_fmaf(y[2], rc[p].y, -(y[3] * rs[p].y));
+            o[3] = (bf16)__builtin_fmaf(y[2], rs[p].y, y[3] * rc[p].y);
+          } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) o[j] = (bf16)y[j];
+          }
+          bf16* dst = sec == 0 ? static_cast<bf16*>(g.rope_q) + (int64_t)rows[p] * g.rope_d
+                               : static_cast<bf16*>(sec == 1 ? g.rope_k : g.rope_v) + kvo[p];
+          *reinterpret_cast<bf16x4*>(dst + c) = o;
         } else if constexpr (RESID) {
           *reinterpret_cast<f32x4*>(static_cast<float*>(g.out) + orow + col) = prev[p] + (cgate + gv[p]) * v;
         } else {
@@ -763,6 +797,11 @@ hipError_t launch_cfg(const GemmArgs& g, const GemmGroup* gg, hipStream_t s) {
     }
     if (g.epi == WAM_EPI_GELU_MX8 || g.epi == MXB || g.epi == MXR) return hipGetLastError();
   }
+  if (g.epi == WAM_EPI_ROPE) {  // bf16 operands only
+    if constexpr (Cf::EB == 2) hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_ROPE>), grid, block, 0, s, g, tm, tn);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   switch (g.epi) {
     case WAM_EPI_BF16: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_BF16>), grid, block, 0, s, g, tm, tn); break;
     case WAM_EPI_GELU_BF16: hipLaunchKernelGGL((gemm_nt<Cf, WAM_EPI_GELU_BF16>), grid, block, 0, s, g, tm, tn); break;
@@ -791,6 +830,12 @@ hipError_t launch_cfg2(const GemmArgs& g, int c1, hipStream_t s) {
       default: break;
     }
     if (g.epi == WAM_EPI_GELU_MX8 || g.epi == MXB || g.epi == MXR) return hipGetLastError();
+  }
+  if (g.epi == WAM_EPI_ROPE) {  // bf16 operands only
+    if constexpr (Ca::EB == 2)
+      hipLaunchKernelGGL((gemm_nt2<Ca, Cb, WAM_EPI_ROPE>), grid, block, 0, s, g, tm1, c1, tm2, tn2);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
   }
   switch (g.epi) {
     case WAM_EPI_BF16: hipLaunchKernelGGL((gemm_nt2<Ca, Cb, WAM_EPI_BF16>), grid, block, 0, s, g, tm1, c1, tm2, tn2); break;

@@ -73,10 +73,18 @@ struct GemmArgs {
   int64_t o_lde;
   // device flag of the denoising loop: while *skip > 0 every workgroup exits at entry (NULL: never)
   const int32_t* skip;
+  // epi WAM_EPI_ROPE (N = 3 d, d = H * Dh a multiple of 64; row r = b * rope_L + l): the
+  // bf16-rounded q|k|v row with q and k rotated as rope_qkv_kernel does, q into rope_q
+  // [M][d], k and v into rope_k / rope_v row b * rope_Lcap + rope_row0 + l ([.][d])
+  const float *rope_cos, *rope_sin;
+  void *rope_q, *rope_k, *rope_v;
+  int32_t rope_L, rope_Dh, rope_d;
+  int64_t rope_Lcap, rope_row0;
 };
 // Internal epilogue codes beyond the public ones: the GELU output written as block-scaled
-// E4M3, and (or-ed in) block-scaled FP8 A.
+// E4M3, (or-ed in) block-scaled FP8 A, and RoPE with the K/V append (bf16 operands).
 constexpr int WAM_EPI_GELU_MX8 = 4;
+constexpr int WAM_EPI_ROPE = 5;
 constexpr int WAM_EPI_MXA = 8;
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 // n products sharing A (and, for FP8 operands, its row scales) and every size and stride,
